@@ -1,0 +1,169 @@
+"""CPU oracle for the compliance check -- TEST INFRASTRUCTURE.
+
+Only the tests, the smoke check and the benchmark's CPU-baseline leg may
+import this package.  It wraps `pc_oracle.c` (plain C loops, OpenMP over
+the outermost loop only) through ctypes.  It shares nothing with the GPU
+library: its own record layouts, its own build, its own loops.
+
+Each function states the passage of the paper it follows in the C source.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "pc_oracle.c")
+_LIB = os.path.join(_HERE, "_pc_oracle.so")
+
+TRACE_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port", "<u2"),
+                     ("hops", "u1"), ("state", "u1")])
+assert TRACE_DT.itemsize == 12
+SUMMARY_DT = np.dtype([("counts", "<u8", (4, 8)), ("no_path", "<u8", (4,))])
+
+EGRESS, DROP, MISS, TTL = 0, 1, 2, 3
+F_PRED, F_OFFSETS, F_ACTION, F_SWITCH, F_JUR, F_GRAPH, F_INTENT = 1, 2, 4, 8, 16, 32, 64
+
+_lib = None
+
+
+def build(force=True):
+    """Compile the oracle with gcc (-O2, OpenMP)."""
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Werror",
+           "-o", _LIB + ".tmp", _SRC]
+    if force or not os.path.exists(_LIB):
+        subprocess.check_call(cmd)
+        os.replace(_LIB + ".tmp", _LIB)
+    return _LIB
+
+
+def _load():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=True)
+        _lib = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        I64 = ctypes.c_int64
+        C = ctypes.c_int
+        _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, P, I64, P, P, P, C]
+        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, P, I64, P, P, C]
+        _lib.orc_reach.argtypes = [I64, P, P, I64, P, P, P, P, P, I64, P, P, C]
+        _lib.orc_report.argtypes = [I64, P, I64, P, I64, P, I64, P, I64, P, P, I64, P, P, P, P]
+        _lib.orc_max_threads.restype = C
+    return _lib
+
+
+def _p(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def max_threads():
+    return int(_load().orc_max_threads())
+
+
+def selectors(labels, pred_off, preds, n_preds=None, rows=None, nthreads=0):
+    """Feasible-node bitset and popcount for the given selector rows
+    (all rows by default).  Returns (feasible [nrows, W] u64, popcnt u32, flags)."""
+    lib = _load()
+    labels = np.ascontiguousarray(labels, np.uint8)
+    N, L = labels.shape
+    I = pred_off.shape[0] - 1
+    if rows is None:
+        rows = np.arange(I, dtype=np.int32)
+    rows = np.ascontiguousarray(rows, np.int32)
+    n_preds = preds.shape[0] if n_preds is None else n_preds
+    W = (N + 63) // 64
+    feas = np.zeros((rows.shape[0], W), np.uint64)
+    pc = np.zeros(rows.shape[0], np.uint32)
+    err = np.zeros(1, np.uint32)
+    lib.orc_selectors(_p(labels), N, L, _p(np.ascontiguousarray(pred_off, np.int32)),
+                      _p(np.ascontiguousarray(preds)), n_preds, _p(rows), rows.shape[0],
+                      _p(feas), _p(pc), _p(err), nthreads)
+    return feas, pc, int(err[0])
+
+
+def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=None,
+          n_ports=None, n_rules=None, nthreads=0):
+    """Trace records for the given trace indices (all by default)."""
+    lib = _load()
+    T = ingress.shape[0]
+    if idx is None:
+        idx = np.arange(T, dtype=np.int64)
+    idx = np.ascontiguousarray(idx, np.int64)
+    out = np.zeros(idx.shape[0], TRACE_DT)
+    err = np.zeros(1, np.uint32)
+    n_ports = port_peer.shape[0] if n_ports is None else n_ports
+    n_rules = rules.shape[0] if n_rules is None else n_rules
+    lib.orc_trace(S, _p(np.ascontiguousarray(port_off, np.int32)),
+                  _p(np.ascontiguousarray(port_peer, np.int32)), n_ports,
+                  _p(np.ascontiguousarray(jur, np.uint8)), _p(np.ascontiguousarray(rule_off, np.int32)),
+                  _p(np.ascontiguousarray(rules)), n_rules,
+                  _p(np.ascontiguousarray(hdr, np.uint32)), _p(np.ascontiguousarray(ingress, np.int32)),
+                  ttl, _p(idx), idx.shape[0], _p(out), _p(err), nthreads)
+    return out, int(err[0])
+
+
+def reach(V, adj_off, adj, region, src, allowed, target=None, qidx=None, n_adj=None, nthreads=0):
+    """Masked BFS distances: full rows [nq, V] when target is None, else [nq]."""
+    lib = _load()
+    Q = src.shape[0]
+    if qidx is None:
+        qidx = np.arange(Q, dtype=np.int64)
+    qidx = np.ascontiguousarray(qidx, np.int64)
+    n_adj = adj.shape[0] if n_adj is None else n_adj
+    if target is None:
+        dist = np.zeros((qidx.shape[0], V), np.int32)
+    else:
+        dist = np.zeros(qidx.shape[0], np.int32)
+        target = np.ascontiguousarray(target, np.int32)
+    err = np.zeros(1, np.uint32)
+    lib.orc_reach(V, _p(np.ascontiguousarray(adj_off, np.int32)), _p(np.ascontiguousarray(adj, np.int32)),
+                  n_adj, _p(np.ascontiguousarray(region, np.uint8)), _p(np.ascontiguousarray(src, np.int32)),
+                  _p(np.ascontiguousarray(allowed, np.uint32)), _p(target), _p(qidx), qidx.shape[0],
+                  _p(dist), _p(err), nthreads)
+    return dist, int(err[0])
+
+
+def report(intents, feasible, popcnt, N, traces, expect, reach_d):
+    """Per-intent pass bits, reason codes and the (kind, reason) summary."""
+    lib = _load()
+    I = intents.shape[0]
+    feasible = np.ascontiguousarray(feasible, np.uint64)
+    rows = feasible.shape[0]
+    W = feasible.shape[1] if feasible.ndim == 2 else 0
+    traces = np.ascontiguousarray(traces)
+    reach_d = np.ascontiguousarray(reach_d, np.int32)
+    pass_ = np.zeros((I + 63) // 64, np.uint64)
+    reason = np.zeros(I, np.uint8)
+    summ = np.zeros(1, SUMMARY_DT)
+    err = np.zeros(1, np.uint32)
+    lib.orc_report(I, _p(np.ascontiguousarray(intents)), rows, _p(feasible), W,
+                   _p(np.ascontiguousarray(popcnt, np.uint32)), N, _p(traces), traces.shape[0],
+                   _p(np.ascontiguousarray(expect)), _p(reach_d), reach_d.shape[0],
+                   _p(pass_), _p(reason), _p(summ), _p(err))
+    return pass_, reason, summ[0], int(err[0])
+
+
+def run_workload(wl, nthreads=0):
+    """All four stages of a synth.Workload on the CPU (small workloads)."""
+    out = {}
+    if "labels" in wl.arrays:
+        out["feasible"], out["popcnt"], out["sel_err"] = selectors(
+            wl["labels"], wl["pred_off"], wl["preds"], nthreads=nthreads)
+    if "rules" in wl.arrays:
+        out["traces"], out["trace_err"] = trace(
+            wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+            wl["hdr"], wl["ingress"], wl["ttl"], nthreads=nthreads)
+    if "src" in wl.arrays:
+        out["reach"], out["reach_err"] = reach(
+            wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"],
+            wl.arrays.get("target"), nthreads=nthreads)
+    if "intents" in wl.arrays:
+        out["pass"], out["reason"], out["summary"], out["report_err"] = report(
+            wl["intents"], out["feasible"], out["popcnt"], wl["N"], out["traces"], wl["expect"],
+            out["reach"])
+    return out

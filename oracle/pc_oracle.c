@@ -1,0 +1,373 @@
+/*
+ * Reference oracle for the cross-layer compliance check.  TEST
+ * INFRASTRUCTURE ONLY: tests, the smoke check and the benchmark's CPU
+ * baseline call it; the product path never does.
+ *
+ * Plain, slow, obviously correct scalar loops, parallelised only over the
+ * outermost independent loop (rows, traces, queries).  It shares no code,
+ * header or table with the GPU library; the record layouts below are
+ * restated from the C ABI contract.
+ *
+ * What is computed (paper, Sec. "Formal Model and Satisfaction"): a
+ * configuration satisfies an intent when (i) every placement constraint
+ * holds for the nodes given their labels and (ii) every routing constraint
+ * holds on the paths the installed flow rules realise; a validator check
+ * is one atomic pass/fail assertion and an intent passes only when all of
+ * its checks pass (Sec. "Automated Validation Pipeline", validator check
+ * definition).
+ *
+ * Readings where the paper is silent (operator semantics, priority order,
+ * ties, table miss, TTL, port model) are the ones listed with the C ABI:
+ * Kubernetes node-affinity operators, larger priority wins, lower rule
+ * index breaks ties, a table miss ends the trace, hops count links.
+ */
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+typedef struct { uint16_t label; uint8_t op; uint8_t rsv0; uint32_t rsv1; uint64_t vals[4]; } o_pred;
+typedef struct { uint32_t value[4]; uint32_t mask[4]; uint16_t priority; uint16_t action; uint32_t rsv; } o_rule;
+typedef struct { uint32_t jmask; int32_t last_switch; uint16_t last_port; uint8_t hops; uint8_t state; } o_trace;
+typedef struct {
+    uint8_t kind; uint8_t pad[3]; int32_t sel_row, src_node, dst_node, trace_begin, trace_end;
+    uint32_t allowed; uint32_t pad2;
+} o_intent;
+typedef struct { int32_t dst_switch, dst_port, reach_q; } o_expect;
+typedef struct { uint64_t counts[4][8]; uint64_t no_path[4]; } o_summary;
+
+_Static_assert(sizeof(o_pred) == 40, "pred");
+_Static_assert(sizeof(o_rule) == 40, "rule");
+_Static_assert(sizeof(o_trace) == 12, "trace");
+_Static_assert(sizeof(o_intent) == 32, "intent");
+_Static_assert(sizeof(o_expect) == 12, "expect");
+
+enum { O_IN = 0, O_NOTIN = 1, O_EXISTS = 2 };
+enum { O_EGRESS = 0, O_DROP = 1, O_MISS = 2, O_TTL = 3 };
+/* data-error flags (sticky word) */
+enum { F_PRED = 1, F_OFFSETS = 2, F_ACTION = 4, F_SWITCH = 8, F_JUR = 16, F_GRAPH = 32, F_INTENT = 64 };
+
+static void set_flag(uint32_t *err, uint32_t f)
+{
+#pragma omp atomic
+    *err |= f;
+}
+
+static void set_threads(int nthreads)
+{
+#ifdef _OPENMP
+    if (nthreads > 0) omp_set_num_threads(nthreads);
+#else
+    (void)nthreads;
+#endif
+}
+
+int orc_max_threads(void)
+{
+#ifdef _OPENMP
+    return omp_get_max_threads();
+#else
+    return 1;
+#endif
+}
+
+/* ------------------------------------------------------------------ A1
+ * Selector rows (paper: placement constraint "region=EU is among the
+ * labels of the node the pod is placed on", compiled to a Kubernetes node
+ * selector / affinity).  A row is a conjunction of predicates; a predicate
+ * names one label and an operator:
+ *   In S     : the node has the label and its value is in S
+ *   NotIn S  : the node lacks the label, or its value is not in S
+ *   Exists   : the node has the label
+ * Label value 0xFF means "absent".  Output bit n of row r is set iff node n
+ * satisfies every predicate of row r; words are LSB-first, W = ceil(N/64),
+ * padding bits zero.  An empty row holds for every node.  A malformed
+ * predicate (label >= L, op > 2, reserved field set, or value 255 in an
+ * In/NotIn set) holds for no node and raises F_PRED; a malformed offset
+ * pair makes the whole row empty and raises F_OFFSETS.
+ */
+void orc_selectors(const uint8_t *labels, int64_t N, int64_t L,
+                   const int32_t *pred_off, const o_pred *preds, int64_t n_preds,
+                   const int32_t *rows, int64_t nrows,
+                   uint64_t *feasible, uint32_t *popcnt, uint32_t *err, int nthreads)
+{
+    const int64_t W = (N + 63) / 64;
+    set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows[r];
+        uint64_t *out = feasible + r * W;
+        for (int64_t w = 0; w < W; ++w) out[w] = 0;
+        uint32_t count = 0;
+        const int64_t b = pred_off[i], e = pred_off[i + 1];
+        if (b < 0 || e < b || e > n_preds) {
+            set_flag(err, F_OFFSETS);
+            popcnt[r] = 0;
+            continue;
+        }
+        for (int64_t n = 0; n < N; ++n) {
+            int ok = 1;
+            for (int64_t p = b; p < e; ++p) {
+                const o_pred *q = &preds[p];
+                int valid = q->label < L && q->op <= 2 && q->rsv0 == 0 && q->rsv1 == 0 &&
+                            (q->op == O_EXISTS || ((q->vals[3] >> 63) & 1) == 0);
+                if (!valid) {
+                    set_flag(err, F_PRED);
+                    ok = 0;
+                    continue;
+                }
+                const unsigned x = labels[n * L + q->label];
+                const int present = x != 0xFF;
+                const int in_set = present && ((q->vals[x >> 6] >> (x & 63)) & 1);
+                int sat;
+                if (q->op == O_IN) sat = in_set;
+                else if (q->op == O_NOTIN) sat = !in_set;
+                else sat = present;
+                if (!sat) ok = 0;
+            }
+            if (ok) {
+                out[n >> 6] |= (uint64_t)1 << (n & 63);
+                ++count;
+            }
+        }
+        popcnt[r] = count;
+    }
+}
+
+/* ------------------------------------------------------------------ A3
+ * Trace one header through the flow tables (paper: routing constraints
+ * must hold "for the realized paths induced by" the installed rules; flow
+ * rules are compiled per hop along a path).  At switch s the rule that
+ * applies is the one of highest priority whose value agrees with the
+ * header on every bit its mask cares about; equal priorities go to the
+ * lower index within the switch's table.  No match: MISS.  Action 0xFFFF:
+ * DROP.  Otherwise the action is a local port; a port with no peer switch
+ * faces a host: EGRESS there.  A forward when `ttl` links have already been
+ * crossed ends in TTL at the current switch.  jmask collects the
+ * jurisdiction bit of every switch visited, the ingress included.
+ */
+static int rule_matches(const o_rule *r, const uint32_t *h)
+{
+    for (int w = 0; w < 4; ++w)
+        if (((h[w] ^ r->value[w]) & r->mask[w]) != 0) return 0;
+    return 1;
+}
+
+static uint32_t jur_bit(const uint8_t *jur, int64_t s, uint32_t *err)
+{
+    if (jur[s] >= 32) {
+        set_flag(err, F_JUR);
+        return 0;
+    }
+    return (uint32_t)1 << jur[s];
+}
+
+void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
+               const uint8_t *jur, const int32_t *rule_off, const o_rule *rules, int64_t n_rules,
+               const uint32_t *hdr, const int32_t *ingress, int64_t ttl,
+               const int64_t *idx, int64_t nidx, o_trace *out, uint32_t *err, int nthreads)
+{
+    set_threads(nthreads);
+#pragma omp parallel for schedule(dynamic, 16)
+    for (int64_t k = 0; k < nidx; ++k) {
+        const int64_t t = idx[k];
+        const uint32_t *h = hdr + 4 * t;
+        o_trace res;
+        int64_t s = ingress[t];
+        res.last_port = 0xFFFF;
+        res.hops = 0;
+        if (s < 0 || s >= S) {
+            set_flag(err, F_SWITCH);
+            res.jmask = 0;
+            res.last_switch = (int32_t)s;
+            res.state = O_MISS;
+            out[k] = res;
+            continue;
+        }
+        uint32_t jm = jur_bit(jur, s, err);
+        int64_t hops = 0;
+        int state;
+        for (;;) {
+            const int64_t rb = rule_off[s], re = rule_off[s + 1];
+            int64_t best = -1;
+            if (rb < 0 || re < rb || re > n_rules) {
+                set_flag(err, F_OFFSETS);
+            } else {
+                for (int64_t r = rb; r < re; ++r) {
+                    if (!rule_matches(&rules[r], h)) continue;
+                    if (best < 0 || rules[r].priority > rules[best].priority) best = r;
+                }
+            }
+            if (best < 0) { state = O_MISS; break; }
+            const unsigned a = rules[best].action;
+            if (a == 0xFFFF) { state = O_DROP; break; }
+            const int64_t pb = port_off[s], pe = port_off[s + 1];
+            if (pb < 0 || pe < pb || pe > n_ports) {
+                set_flag(err, F_OFFSETS);
+                state = O_MISS;
+                break;
+            }
+            if ((int64_t)a >= pe - pb) {
+                set_flag(err, F_ACTION);
+                state = O_MISS;
+                break;
+            }
+            const int64_t peer = port_peer[pb + a];
+            if (peer == -1) { state = O_EGRESS; res.last_port = (uint16_t)a; break; }
+            if (peer < -1 || peer >= S) {
+                set_flag(err, F_SWITCH);
+                state = O_MISS;
+                break;
+            }
+            if (hops == ttl) { state = O_TTL; break; }
+            s = peer;
+            ++hops;
+            jm |= jur_bit(jur, s, err);
+        }
+        res.jmask = jm;
+        res.last_switch = (int32_t)s;
+        res.hops = (uint8_t)hops;
+        res.state = (uint8_t)state;
+        out[k] = res;
+    }
+}
+
+/* ------------------------------------------------------------------ A5
+ * Hop distance from src inside the subgraph induced by the allowed
+ * switches: vertex v is allowed when bit region[v] of `allowed` is set
+ * (region >= 32 is never allowed and raises F_JUR).  Textbook FIFO
+ * breadth-first search over the undirected CSR graph.  A disallowed or
+ * out-of-range source leaves every distance at -1.  With target == NULL
+ * the full row [V] is written, else the single distance to target[q].
+ */
+void orc_reach(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+               const uint8_t *region, const int32_t *src, const uint32_t *allowed,
+               const int32_t *target, const int64_t *qidx, int64_t nq,
+               int32_t *dist_out, uint32_t *err, int nthreads)
+{
+    set_threads(nthreads);
+#pragma omp parallel
+    {
+        int32_t *dist = (int32_t *)malloc(sizeof(int32_t) * (size_t)(V > 0 ? V : 1));
+        int64_t *queue = (int64_t *)malloc(sizeof(int64_t) * (size_t)(V > 0 ? V : 1));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t k = 0; k < nq; ++k) {
+            const int64_t q = qidx[k];
+            for (int64_t v = 0; v < V; ++v) dist[v] = -1;
+            const int64_t s = src[q];
+            const uint32_t A = allowed[q];
+            int64_t tgt = -1;
+            int tgt_ok = 1;
+            if (target) {
+                tgt = target[q];
+                if (tgt < 0 || tgt >= V) { set_flag(err, F_SWITCH); tgt_ok = 0; }
+            }
+            int src_ok = 1;
+            if (s < 0 || s >= V) { set_flag(err, F_SWITCH); src_ok = 0; }
+            else if (region[s] >= 32) { set_flag(err, F_JUR); src_ok = 0; }
+            else if (!((A >> region[s]) & 1)) src_ok = 0;
+            if (src_ok) {
+                int64_t head = 0, tail = 0;
+                dist[s] = 0;
+                queue[tail++] = s;
+                while (head < tail) {
+                    const int64_t u = queue[head++];
+                    const int64_t b = adj_off[u], e = adj_off[u + 1];
+                    if (b < 0 || e < b || e > n_adj) { set_flag(err, F_OFFSETS); continue; }
+                    for (int64_t p = b; p < e; ++p) {
+                        const int64_t v = adj[p];
+                        if (v < 0 || v >= V) { set_flag(err, F_GRAPH); continue; }
+                        if (region[v] >= 32) { set_flag(err, F_JUR); continue; }
+                        if (!((A >> region[v]) & 1)) continue;
+                        if (dist[v] != -1) continue;
+                        dist[v] = dist[u] + 1;
+                        queue[tail++] = v;
+                    }
+                }
+            }
+            if (target) {
+                dist_out[k] = tgt_ok ? dist[tgt] : -1;
+            } else {
+                memcpy(dist_out + k * V, dist, sizeof(int32_t) * (size_t)V);
+            }
+        }
+        free(dist);
+        free(queue);
+    }
+}
+
+/* ------------------------------------------------------------------ A6
+ * Per-intent verdict: pass iff every check of the intent passes (paper,
+ * validator check definition); an unenforceable intent fails closed.
+ *   compute (kind bit 0): the selector row admits at least one node
+ *       (NO_FEASIBLE_NODE = 1); a hybrid intent's two placed endpoints must
+ *       both be admitted (ENDPOINT_INFEASIBLE = 2).
+ *   network (kind bit 1): at least one flow (NO_FLOW = 3, the no-op
+ *       policy); every trace stays inside the allowed jurisdictions
+ *       (LEAK = 4), ends in EGRESS (UNDELIVERED = 5) at the expected switch
+ *       and port when given (WRONG_EGRESS = 6).
+ * The reason is the smallest failing code; compute reasons come first.
+ * Bit 7 is added when the intent's reachability query found no compliant
+ * path.  A record that points outside its arrays, or kind not in {1,2,3},
+ * gives MALFORMED = 7 and F_INTENT.
+ */
+void orc_report(int64_t I, const o_intent *intents, int64_t rows, const uint64_t *feasible, int64_t W,
+                const uint32_t *popcnt, int64_t N, const o_trace *traces, int64_t T,
+                const o_expect *expect, const int32_t *reach, int64_t Q,
+                uint64_t *pass, uint8_t *reason, o_summary *summary, uint32_t *err)
+{
+    memset(summary, 0, sizeof(*summary));
+    for (int64_t w = 0; w < (I + 63) / 64; ++w) pass[w] = 0;
+    for (int64_t i = 0; i < I; ++i) {
+        const o_intent *it = &intents[i];
+        const o_expect *ex = &expect[i];
+        const int kind = it->kind;
+        int malformed = (kind < 1 || kind > 3);
+        if (!malformed && (kind & 1)) {
+            if (it->sel_row < 0 || it->sel_row >= rows) malformed = 1;
+            if (kind == 3 && (it->src_node < 0 || it->src_node >= N || it->dst_node < 0 || it->dst_node >= N))
+                malformed = 1;
+        }
+        if (!malformed && (kind & 2)) {
+            if (it->trace_begin < 0 || it->trace_end < it->trace_begin || it->trace_end > T) malformed = 1;
+            if (ex->reach_q < -1 || ex->reach_q >= Q) malformed = 1;
+        }
+        int r = 0, flag = 0;
+        if (malformed) {
+            set_flag(err, F_INTENT);
+            r = 7;
+        } else {
+            if (kind & 1) {
+                const uint64_t *row = feasible + (int64_t)it->sel_row * W;
+                if (popcnt[it->sel_row] == 0) r = 1;
+                else if (kind == 3) {
+                    const int a = (row[it->src_node >> 6] >> (it->src_node & 63)) & 1;
+                    const int b = (row[it->dst_node >> 6] >> (it->dst_node & 63)) & 1;
+                    if (!(a && b)) r = 2;
+                }
+            }
+            if (kind & 2) {
+                if (r == 0) {
+                    if (it->trace_end == it->trace_begin) r = 3;
+                    for (int64_t t = it->trace_begin; t < it->trace_end; ++t) {
+                        const o_trace *tr = &traces[t];
+                        int code = 0;
+                        if (tr->jmask & ~it->allowed) code = 4;
+                        else if (tr->state != O_EGRESS) code = 5;
+                        else if ((ex->dst_switch >= 0 && tr->last_switch != ex->dst_switch) ||
+                                 (ex->dst_port >= 0 && tr->last_port != ex->dst_port)) code = 6;
+                        if (code && (r == 0 || code < r)) r = code;
+                    }
+                }
+                if (ex->reach_q >= 0 && reach[ex->reach_q] < 0) flag = 1;
+            }
+        }
+        reason[i] = (uint8_t)(r | (flag ? 0x80 : 0));
+        if (r == 0) pass[i >> 6] |= (uint64_t)1 << (i & 63);
+        summary->counts[kind & 3][r] += 1;
+        summary->no_path[kind & 3] += flag;
+    }
+}
