@@ -1,0 +1,226 @@
+"""Benchmark: one step = one full validation pass of the combined cross-layer
+workload (selector evaluation, flow tracing, masked reachability, per-intent
+verdict) on one GPU, inputs resident in HBM.
+
+    python bench.py [--gpus 1] [--steps K] [--warmup W] [--workload cfg5|small]
+
+Prints one JSON line.  `value` is selector evaluations ((intent, node)
+pairs) per second of whole-step time; flow lookups ("hops traced") per
+second of whole-step time are reported beside it, with per-kernel times,
+the roofline of the dominant kernel, and the CPU oracle timed on a bounded
+sample of the same workload.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--workload", default="cfg5", choices=["cfg5", "small"])
+    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    return ap.parse_args()
+
+
+def make_workload(name):
+    import synth
+    if name == "cfg5":
+        return synth.cfg5(), ("combined cross-layer validation, seed 4: 50,000 nodes x 64 labels; fat-tree k=48 "
+                              "(2,880 switches), 16,384 rules/switch, 12 jurisdictions; 1,048,576 intents "
+                              "(1/3 compute, 1/3 network, 1/3 hybrid); TTL 32; R-path rule tables")
+    return synth.combined_workload(7, 5000, 64, 16, 8, 2048, 30000), "small combined workload (smoke scale)"
+
+
+def sample_subproblem(wl, stride):
+    """Every `stride`-th intent with the selector rows, traces and reach
+    queries it references, renumbered into a standalone workload."""
+    it = wl["intents"]
+    idx = np.arange(0, it.shape[0], stride)
+    sub = it[idx].copy()
+    ex = wl["expect"][idx].copy()
+    has_sel = (sub["kind"] & 1) == 1
+    rows = sub["sel_row"][has_sel].astype(np.int32)
+    sub["sel_row"][has_sel] = np.arange(rows.shape[0], dtype=np.int32)
+    has_net = (sub["kind"] & 2) == 2
+    tb, te = sub["trace_begin"][has_net], sub["trace_end"][has_net]
+    lens = te - tb
+    tidx = np.concatenate([np.arange(b, e) for b, e in zip(tb, te)]) if lens.sum() else np.zeros(0, np.int64)
+    nb = np.zeros(lens.shape[0] + 1, np.int64)
+    nb[1:] = np.cumsum(lens)
+    sub["trace_begin"][has_net] = nb[:-1]
+    sub["trace_end"][has_net] = nb[1:]
+    q = ex["reach_q"]
+    qsel = q >= 0
+    qidx = q[qsel].astype(np.int64)
+    ex["reach_q"][qsel] = np.arange(qidx.shape[0], dtype=np.int32)
+    return dict(intents=sub, expect=ex, rows=rows, traces=tidx.astype(np.int64), queries=qidx)
+
+
+def cpu_baseline(wl, pairs_total, target_s):
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    env_cap = os.environ.get("OMP_NUM_THREADS")
+    if env_cap and env_cap.isdigit():
+        threads = min(threads, int(env_cap))
+
+    def run(stride):
+        sp = sample_subproblem(wl, stride)
+        t0 = time.perf_counter()
+        feas, pc, _ = oracle.selectors(wl["labels"], wl["pred_off"], wl["preds"], rows=sp["rows"], nthreads=threads)
+        tr, _ = oracle.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+                             wl["hdr"], wl["ingress"], wl["ttl"], idx=sp["traces"], nthreads=threads)
+        rc, _ = oracle.reach(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"],
+                             wl["target"], qidx=sp["queries"], nthreads=threads)
+        oracle.report(sp["intents"], feas, pc, wl["N"], tr, sp["expect"], rc)
+        return time.perf_counter() - t0, sp
+
+    I = wl["intents"].shape[0]
+    stride = 4096
+    t, sp = run(stride)
+    while t < target_s / 8 and stride > 1:
+        stride = max(1, int(stride / max(2.0, min(64.0, target_s / max(t, 1e-3) / 2))))
+        t, sp = run(stride)
+    frac = sp["intents"].shape[0] / I
+    est_full = t / frac
+    return {
+        "value": pairs_total / est_full,
+        "unit": "selector evals/s (whole-job estimate)",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": (f"every {stride}th intent ({sp['intents'].shape[0]} of {I}: {sp['rows'].shape[0]} selector rows "
+                   f"x {wl['N']} nodes, {sp['traces'].shape[0]} traces, {sp['queries'].shape[0]} reach queries, "
+                   f"report) in {t:.2f} s; whole job estimated at {est_full:.1f} s"),
+        "est_step_s": est_full,
+    }
+
+
+def main():
+    args = parse()
+    world = int(os.environ.get("WORLD_SIZE", "1"))
+    if args.gpus != 1 or world != 1:
+        print(f"bench.py measures one GPU only (the check shards by intent with no exchange; see DESIGN.md); "
+              f"--gpus {args.gpus} is not supported", file=sys.stderr)
+        sys.exit(2)
+
+    import torch
+    import paper_2602_16100_amd as pc
+
+    wl, desc = make_workload(args.workload)
+    dev = "cuda:0"
+    torch.cuda.set_device(0)
+    D = {k: pc.to_device(v, dev) for k, v in wl.arrays.items() if isinstance(v, np.ndarray) and k != "pts"}
+    N, L = wl["N"], wl["L"]
+    I_rows = wl["I_rows"]
+    W = (N + 63) // 64
+    I = wl["I"]
+    T = wl["T"]
+    Q = wl["Q"]
+    feasible = torch.empty((I_rows, W), dtype=torch.int64, device=dev)
+    popcnt = torch.empty(I_rows, dtype=torch.int32, device=dev)
+    traces = torch.empty((T, 12), dtype=torch.uint8, device=dev)
+    reach = torch.empty(Q, dtype=torch.int32, device=dev)
+    pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
+    reason = torch.empty(I, dtype=torch.uint8, device=dev)
+    summary = torch.empty(288, dtype=torch.uint8, device=dev)
+    ctx = pc.context(0)
+
+    def step():
+        pc.pc_eval_selectors(D["labels"], D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
+        pc.pc_trace_flows(wl["S"], D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                          D["ingress"], wl["ttl"], out=traces, ctx=ctx)
+        pc.pc_masked_reach(wl["V"], D["adj_off"], D["adj"], D["region"], D["src"], D["allowed"], D["target"],
+                           dist=reach, ctx=ctx)
+        pc.pc_report(D["intents"], feasible, popcnt, N, traces, D["expect"], reach, pass_=pass_, reason=reason,
+                     summary=summary, ctx=ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.data_errors(clear=True)
+    ctx.profile(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = ctx.profile_read()
+    ctx.profile(False)
+    flags = ctx.data_errors(clear=True)
+    elapsed = t1 - t0
+    ms_step = 1e3 * elapsed / args.steps
+
+    tr = pc.records(traces, pc.TRACE_OUT_DT)
+    ing = wl["ingress"]
+    started = (ing >= 0) & (ing < wl["S"])
+    lookups = int((tr["hops"][started].astype(np.int64) + 1).sum())
+    pairs = int(I_rows) * int(N)
+    value = pairs * args.steps / elapsed
+    reasons = reason.cpu().numpy() & 0x7F
+    passed = int((reasons == 0).sum())
+
+    def ktime(prefix):
+        return sum(ms for name, (n, ms) in prof.items() if name.startswith(prefix)) / args.steps
+
+    sel_eval_n, sel_eval_ms = prof.get("k_sel_eval", (0, 0.0))
+    avg_eval_ms = sel_eval_ms / max(sel_eval_n, 1)
+    n_preds = wl["n_preds"]
+    alg_bytes = I_rows * W * 8 + I_rows * 4 + n_preds * 40 + N * L
+    achieved = alg_bytes / (avg_eval_ms * 1e-3) / 1e9 if avg_eval_ms > 0 else 0.0
+    per_kernel = {name: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
+                  for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])}
+    trace_ms = ktime("k_tr_")
+    line = {
+        "metric": "flow hops traced/sec + selector evals/sec on 1 MI355X; % of peak HBM GB/s",
+        "value": value,
+        "unit": "selector evals/s ((intent,node) pairs per second of whole-step time)",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": ms_step,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "u64 bitsets / int32 (integer work, no floating point)",
+        "data": "synthetic (seeded generators; no dataset)",
+        "config": {"workload": desc, "intents": I, "selector_rows": I_rows, "nodes": N, "labels": L,
+                   "switches": wl["S"], "rules": wl["n_rules"], "traces": T, "reach_queries": Q,
+                   "ttl": wl["ttl"], "parallelism": "single GPU"},
+        "flow_hops_per_s": lookups * args.steps / elapsed,
+        "flow_lookups_per_step": lookups,
+        "selector_pairs_per_step": pairs,
+        "kernel_rates": {
+            "selector_evals_per_s_kernel": pairs / (ktime("k_sel_") * 1e-3) if ktime("k_sel_") else None,
+            "flow_hops_per_s_kernel": lookups / (trace_ms * 1e-3) if trace_ms else None,
+        },
+        "entry_ms_per_step": {"pc_eval_selectors": ktime("k_sel_"), "pc_trace_flows": trace_ms,
+                              "pc_masked_reach": ktime("k_rc_"), "pc_report": ktime("k_report")},
+        "per_kernel": per_kernel,
+        "roofline": {"kernel": "k_sel_eval", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": avg_eval_ms},
+        "verdict": {"passed": passed, "intents": I},
+        "data_error_flags": flags,
+    }
+    if not args.no_cpu_baseline:
+        line["cpu_baseline"] = cpu_baseline(wl, pairs, args.cpu_seconds)
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

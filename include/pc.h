@@ -1,0 +1,275 @@
+/*
+ * pc.h -- C ABI of the GPU compliance checker (libpc.so, MI355X / gfx950).
+ *
+ * The library evaluates the validator checks of an LLM-driven, intent-based
+ * privacy orchestration system (arXiv 2602.16100) over a post-deployment
+ * state snapshot:
+ *   - pc_eval_selectors : placement constraints -- node selectors over node
+ *                         labels (Formal Model and Satisfaction, condition
+ *                         (i) and the example intent; Kubernetes node
+ *                         selector / affinity in Intent-driven
+ *                         Orchestration Plane).
+ *   - pc_trace_flows    : routing constraints on the paths realised by the
+ *                         installed flow rules (condition (ii); per-hop flow
+ *                         rules in "Network orchestration").
+ *   - pc_masked_reach   : existence and hop distance of a path that stays
+ *                         inside the allowed jurisdictions (the path
+ *                         scheduler's graph search with BFS fallback).
+ *   - pc_report         : per-intent pass/fail -- an intent passes only if
+ *                         all of its checks pass (Automated Validation
+ *                         Pipeline, validator check definition); an
+ *                         unenforceable intent fails closed.
+ *
+ * Conventions shared by every entry point
+ *   - Every array argument is a DEVICE pointer owned by the caller; it must
+ *     stay valid until the work queued on `stream` has completed.  The
+ *     library keeps no pointer past the call and never frees caller memory.
+ *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
+ *     entry point is asynchronous and stream-ordered, except
+ *     pc_trace_flows, which reads back the size of its rule index once and
+ *     one live-trace count per hop level, and pc_data_errors and
+ *     pc_profile_read, which wait for the stream.
+ *   - Return value: PC_OK, or a negative PC_E* code.  Argument errors are
+ *     detected on the host before any device work is queued; the message
+ *     is available from pc_last_error.  No C++ exception crosses the ABI.
+ *   - Malformed device data (see PC_DERR_*) never causes an out-of-bounds
+ *     access: the item is given the documented neutral meaning and a bit
+ *     is OR-ed into the context's sticky data-error word, read with
+ *     pc_data_errors.  A flag depends only on the input arrays, not on the
+ *     order of the traversal.
+ *   - One context per host thread / stream; calls on one context must not
+ *     overlap.  Scratch memory is owned by the context, grown on demand
+ *     (growing synchronises the device) and freed by pc_destroy.
+ */
+#ifndef PC_H
+#define PC_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define PC_VERSION 1
+
+enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
+
+/* selector operators (Kubernetes node-affinity semantics) */
+enum { PC_OP_IN = 0, PC_OP_NOTIN = 1, PC_OP_EXISTS = 2 };
+#define PC_LABEL_ABSENT 0xFFu   /* label value meaning "node does not carry this label" */
+#define PC_ACTION_DROP 0xFFFFu  /* rule action: drop the packet */
+#define PC_NO_PORT 0xFFFFu      /* pc_trace_out.last_port when not EGRESS */
+
+/* terminal state of a trace */
+enum { PC_EGRESS = 0, PC_DROP = 1, PC_MISS = 2, PC_TTL = 3 };
+
+/* per-intent reason codes (low 7 bits); bit 7 = no compliant path exists */
+enum {
+    PC_R_PASS = 0,
+    PC_R_NO_FEASIBLE_NODE = 1,
+    PC_R_ENDPOINT_INFEASIBLE = 2,
+    PC_R_NO_FLOW = 3,
+    PC_R_LEAK = 4,
+    PC_R_UNDELIVERED = 5,
+    PC_R_WRONG_EGRESS = 6,
+    PC_R_MALFORMED = 7,
+    PC_R_NO_COMPLIANT_PATH = 0x80
+};
+
+/* sticky data-error bits */
+enum {
+    PC_DERR_PRED = 1,     /* a row references a predicate with label >= L, op > 2, a reserved field set,
+                             or value 255 in an In/NotIn set */
+    PC_DERR_OFFSETS = 2,  /* a CSR offset pair is negative, decreasing or past the array end */
+    PC_DERR_ACTION = 4,   /* rule action (not DROP) >= number of ports of its switch */
+    PC_DERR_SWITCH = 8,   /* switch / vertex id out of range (port peer, ingress, src, target) */
+    PC_DERR_JUR = 16,     /* jurisdiction / region >= 32 */
+    PC_DERR_GRAPH = 32,   /* adjacency entry out of [0, V) */
+    PC_DERR_INTENT = 64   /* intent record out of range or kind not in {1,2,3} */
+};
+
+/* One selector predicate, 40 bytes.  vals is a 256-bit value set (bit v of
+ * word v>>6); bit 255 must be clear (0xFF means absent).  Exists ignores vals. */
+typedef struct pc_pred {
+    uint16_t label;
+    uint8_t op;
+    uint8_t rsv0;     /* must be 0 */
+    uint32_t rsv1;    /* must be 0 */
+    uint64_t vals[4];
+} pc_pred;
+
+/* 104-bit 5-tuple, 16 bytes: w[0] src ip, w[1] dst ip, w[2] sport<<16 | dport,
+ * w[3] proto in bits 0..7 (bits 8..31 zero by convention; they take part in
+ * matching like any other bit). */
+typedef struct pc_key {
+    uint32_t w[4];
+} pc_key;
+
+/* One ternary flow rule, 40 bytes.  Matches header h iff ((h ^ value) & mask)
+ * == 0 in all four words (mask bit 1 = care).  Larger priority wins; equal
+ * priorities go to the lower index within the switch's table.  action is a
+ * local out-port of the switch, or PC_ACTION_DROP. */
+typedef struct pc_rule {
+    pc_key value;
+    pc_key mask;
+    uint16_t priority;
+    uint16_t action;
+    uint32_t rsv;
+} pc_rule;
+
+/* Result of one trace, 12 bytes. */
+typedef struct pc_trace_out {
+    uint32_t jmask;       /* OR of 1<<jur[s] over every switch visited, ingress included */
+    int32_t last_switch;  /* switch where the trace ended */
+    uint16_t last_port;   /* egress port when state == PC_EGRESS, else PC_NO_PORT */
+    uint8_t hops;         /* links crossed */
+    uint8_t state;        /* PC_EGRESS / PC_DROP / PC_MISS / PC_TTL */
+} pc_trace_out;
+
+/* Expected egress of an intent's flows, 12 bytes (-1 = not checked). */
+typedef struct pc_flow_expect {
+    int32_t dst_switch;
+    int32_t dst_port;
+    int32_t reach_q;      /* index into the reach array, -1 = none */
+} pc_flow_expect;
+
+/* One intent, 32 bytes.  kind: bit 0 = compute check, bit 1 = network check
+ * (1 compute, 2 network, 3 hybrid). */
+typedef struct pc_intent {
+    uint8_t kind;
+    uint8_t pad[3];
+    int32_t sel_row;      /* selector row (compute / hybrid) */
+    int32_t src_node;     /* hybrid: nodes the endpoints were placed on */
+    int32_t dst_node;
+    int32_t trace_begin;  /* traces [trace_begin, trace_end) carry the intent's flows */
+    int32_t trace_end;
+    uint32_t allowed;     /* allowed jurisdictions, bit j = jurisdiction j */
+    uint32_t pad2;
+} pc_intent;
+
+/* Verdict summary: counts[kind & 3][reason & 0x7F], no_path[kind & 3] counts
+ * intents with PC_R_NO_COMPLIANT_PATH set. */
+typedef struct pc_summary {
+    uint64_t counts[4][8];
+    uint64_t no_path[4];
+} pc_summary;
+
+typedef struct pc_ctx pc_ctx;
+
+/* Create a context on HIP device `device`.  Returns PC_OK and *out, or
+ * PC_EINVAL (bad device / NULL out) or PC_EDEVICE. */
+int pc_create(pc_ctx **out, int device);
+
+/* Free the context and its scratch.  Synchronises the device.  NULL is a no-op. */
+int pc_destroy(pc_ctx *ctx);
+
+/* Text of the last error on this context ("" if none).  Valid until the next call. */
+const char *pc_last_error(const pc_ctx *ctx);
+
+/* PC_VERSION of the library. */
+int pc_version(void);
+
+/* Synchronise `stream`, store the sticky data-error word in *flags (host
+ * pointer) and clear it when `clear` is non-zero. */
+int pc_data_errors(pc_ctx *ctx, void *stream, uint32_t *flags, int clear);
+
+/* Per-kernel GPU timing, for benchmarks.  pc_profile(ctx, 1) resets the
+ * tallies and brackets every library kernel launched on `ctx` afterwards
+ * with HIP events on the launch's stream; pc_profile(ctx, 0) resets and
+ * stops.  pc_profile_read waits for the recorded events and returns, for
+ * the idx-th kernel name seen since the reset, the number of launches and
+ * their summed duration in milliseconds (*name stays valid until the next
+ * pc_profile call); PC_EINVAL when idx is past the last kernel. */
+int pc_profile(pc_ctx *ctx, int enable);
+int pc_profile_read(pc_ctx *ctx, int idx, const char **name, int64_t *launches, double *total_ms);
+
+/*
+ * A1 -- placement constraints.  For every selector row i in [0, I) and node
+ * n in [0, N): bit n of feasible[i] is set iff node n satisfies every
+ * predicate of row i (an empty row admits every node):
+ *   In S    : label present and its value in S
+ *   NotIn S : label absent, or its value not in S
+ *   Exists  : label present
+ * labels   : uint8 [N][L], node-major; PC_LABEL_ABSENT = absent.
+ * pred_off : int32 [I+1]; row i owns preds[pred_off[i] .. pred_off[i+1]).
+ * preds    : pc_pred [n_preds].
+ * feasible : uint64 [I][W], W = ceil(N/64); node n is bit n&63 of word n>>6;
+ *            padding bits of the last word are written as 0.
+ * popcnt   : uint32 [I], number of admitted nodes per row.
+ * Limits: 0 <= N, 1 <= L <= 65535 (L = 0 allowed when no predicate exists),
+ * 0 <= I, n_preds >= 0.  A malformed predicate admits no node
+ * (PC_DERR_PRED); a malformed offset pair empties the row (PC_DERR_OFFSETS).
+ */
+int pc_eval_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L,
+                      const int32_t *pred_off, const pc_pred *preds, int64_t n_preds, int32_t I,
+                      uint64_t *feasible, uint32_t *popcnt, void *stream);
+
+/*
+ * A2+A3+A4 -- routing constraints on realised paths.  Each trace t starts at
+ * switch ingress[t] with header hdr[t] and repeats: find the rule of
+ * highest priority (ties: lower index) matching the header; none -> MISS;
+ * DROP action -> DROP; a port whose peer is -1 faces a host -> EGRESS there;
+ * a forward after `ttl` links -> TTL (the neighbour is not visited);
+ * otherwise move to the peer switch.  jmask ORs 1<<jur[s] of every visited
+ * switch.
+ * port_off : int32 [S+1]; switch s owns ports port_off[s] .. port_off[s+1].
+ * port_peer: int32 [n_ports]; peer switch of each port, -1 = host port.
+ * jur      : uint8 [S], jurisdiction (< 32) of each switch.
+ * rule_off : int32 [S+1]; switch s owns rules[rule_off[s] .. rule_off[s+1]).
+ * rules    : pc_rule [n_rules].
+ * hdr      : pc_key [T]; ingress: int32 [T]; out: pc_trace_out [T].
+ * Limits: 0 <= S, 0 <= T, 0 <= ttl <= 255.  Malformed data: ingress or peer
+ * out of range -> MISS (PC_DERR_SWITCH); invalid action -> MISS
+ * (PC_DERR_ACTION); jur >= 32 adds no bit (PC_DERR_JUR); bad offsets -> the
+ * switch has no rules / ports (PC_DERR_OFFSETS).
+ */
+int pc_trace_flows(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
+                   int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
+                   int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,
+                   pc_trace_out *out, void *stream);
+
+/*
+ * A5 -- compliant-path existence and hop distance.  For query q, vertex v is
+ * allowed iff bit region[v] of allowed[q] is set; dist is the BFS hop
+ * distance from src[q] inside the subgraph induced by the allowed vertices
+ * of the undirected CSR graph, -1 if unreachable or if src[q] itself is not
+ * allowed.
+ * adj_off: int32 [V+1]; adj: int32 [n_adj]; region: uint8 [V].
+ * src, allowed, target: [Q]; target may be NULL.
+ * dist   : int32 [Q][V] (row-major) when target == NULL, else int32 [Q] with
+ *          the distance to target[q].
+ * Limits: 0 <= V, 0 <= Q.  Malformed: adj entry out of range is skipped
+ * (PC_DERR_GRAPH); region >= 32 is never allowed (PC_DERR_JUR); src/target
+ * out of range gives -1 (PC_DERR_SWITCH); bad offsets: no neighbours.
+ */
+int pc_masked_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                    const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,
+                    const int32_t *target, int32_t *dist, void *stream);
+
+/*
+ * A6 -- per-intent verdict.  compute (kind bit 0): popcnt[sel_row] > 0
+ * (else NO_FEASIBLE_NODE); hybrid: both src_node and dst_node admitted by
+ * the row (else ENDPOINT_INFEASIBLE).  network (kind bit 1): the trace range
+ * is non-empty (else NO_FLOW, the no-op policy); every trace satisfies
+ * jmask within allowed (else LEAK), state EGRESS (else UNDELIVERED), at
+ * expect.dst_switch / dst_port when those are >= 0 (else WRONG_EGRESS).  The
+ * reason is the smallest failing code (compute codes first); bit 7 is set
+ * when expect.reach_q >= 0 and reach[reach_q] < 0.  A record pointing out of
+ * range, or kind not in {1,2,3}: MALFORMED (PC_DERR_INTENT).
+ * intents: pc_intent [I]; feasible: uint64 [rows][W]; popcnt: uint32 [rows];
+ * N: number of nodes; traces: pc_trace_out [T]; expect: pc_flow_expect [I];
+ * reach: int32 [Q].
+ * pass   : uint64 [ceil(I/64)], bit i&63 of word i>>6 = intent i passes.
+ * reason : uint8 [I].
+ * summary: pc_summary (device memory), overwritten.
+ */
+int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
+              int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
+              const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass,
+              uint8_t *reason, pc_summary *summary, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PC_H */

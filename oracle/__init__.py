@@ -49,9 +49,9 @@ def _load():
         P = ctypes.c_void_p
         I64 = ctypes.c_int64
         C = ctypes.c_int
-        _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, P, I64, P, P, P, C]
-        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, P, I64, P, P, C]
-        _lib.orc_reach.argtypes = [I64, P, P, I64, P, P, P, P, P, I64, P, P, C]
+        _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
+        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, P, C]
+        _lib.orc_reach.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, P, C]
         _lib.orc_report.argtypes = [I64, P, I64, P, I64, P, I64, P, I64, P, P, I64, P, P, P, P]
         _lib.orc_max_threads.restype = C
     return _lib
@@ -81,7 +81,7 @@ def selectors(labels, pred_off, preds, n_preds=None, rows=None, nthreads=0):
     pc = np.zeros(rows.shape[0], np.uint32)
     err = np.zeros(1, np.uint32)
     lib.orc_selectors(_p(labels), N, L, _p(np.ascontiguousarray(pred_off, np.int32)),
-                      _p(np.ascontiguousarray(preds)), n_preds, _p(rows), rows.shape[0],
+                      _p(np.ascontiguousarray(preds)), n_preds, I, _p(rows), rows.shape[0],
                       _p(feas), _p(pc), _p(err), nthreads)
     return feas, pc, int(err[0])
 
@@ -103,7 +103,7 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
                   _p(np.ascontiguousarray(jur, np.uint8)), _p(np.ascontiguousarray(rule_off, np.int32)),
                   _p(np.ascontiguousarray(rules)), n_rules,
                   _p(np.ascontiguousarray(hdr, np.uint32)), _p(np.ascontiguousarray(ingress, np.int32)),
-                  ttl, _p(idx), idx.shape[0], _p(out), _p(err), nthreads)
+                  T, ttl, _p(idx), idx.shape[0], _p(out), _p(err), nthreads)
     return out, int(err[0])
 
 
@@ -120,9 +120,10 @@ def reach(V, adj_off, adj, region, src, allowed, target=None, qidx=None, n_adj=N
     else:
         dist = np.zeros(qidx.shape[0], np.int32)
         target = np.ascontiguousarray(target, np.int32)
+    assert target is None or target.shape[0] == Q
     err = np.zeros(1, np.uint32)
     lib.orc_reach(V, _p(np.ascontiguousarray(adj_off, np.int32)), _p(np.ascontiguousarray(adj, np.int32)),
-                  n_adj, _p(np.ascontiguousarray(region, np.uint8)), _p(np.ascontiguousarray(src, np.int32)),
+                  n_adj, _p(np.ascontiguousarray(region, np.uint8)), Q, _p(np.ascontiguousarray(src, np.int32)),
                   _p(np.ascontiguousarray(allowed, np.uint32)), _p(target), _p(qidx), qidx.shape[0],
                   _p(dist), _p(err), nthreads)
     return dist, int(err[0])

@@ -47,7 +47,10 @@ _Static_assert(sizeof(o_expect) == 12, "expect");
 
 enum { O_IN = 0, O_NOTIN = 1, O_EXISTS = 2 };
 enum { O_EGRESS = 0, O_DROP = 1, O_MISS = 2, O_TTL = 3 };
-/* data-error flags (sticky word) */
+/* data-error flags (sticky word).  A flag is raised when ANY item of the
+ * corresponding input array is malformed, whichever rows, traces or queries
+ * are evaluated; the evaluation itself gives malformed items a neutral
+ * meaning and never reads out of bounds. */
 enum { F_PRED = 1, F_OFFSETS = 2, F_ACTION = 4, F_SWITCH = 8, F_JUR = 16, F_GRAPH = 32, F_INTENT = 64 };
 
 static void set_flag(uint32_t *err, uint32_t f)
@@ -86,16 +89,34 @@ int orc_max_threads(void)
  * satisfies every predicate of row r; words are LSB-first, W = ceil(N/64),
  * padding bits zero.  An empty row holds for every node.  A malformed
  * predicate (label >= L, op > 2, reserved field set, or value 255 in an
- * In/NotIn set) holds for no node and raises F_PRED; a malformed offset
- * pair makes the whole row empty and raises F_OFFSETS.
+ * In/NotIn set) holds for no node (F_PRED); a malformed offset pair makes
+ * the whole row empty (F_OFFSETS).
  */
+static int pred_valid(const o_pred *q, int64_t L)
+{
+    return q->label < L && q->op <= 2 && q->rsv0 == 0 && q->rsv1 == 0 &&
+           (q->op == O_EXISTS || ((q->vals[3] >> 63) & 1) == 0);
+}
+
+static int range_ok(int64_t b, int64_t e, int64_t n)
+{
+    return b >= 0 && e >= b && e <= n;
+}
+
 void orc_selectors(const uint8_t *labels, int64_t N, int64_t L,
-                   const int32_t *pred_off, const o_pred *preds, int64_t n_preds,
+                   const int32_t *pred_off, const o_pred *preds, int64_t n_preds, int64_t I,
                    const int32_t *rows, int64_t nrows,
                    uint64_t *feasible, uint32_t *popcnt, uint32_t *err, int nthreads)
 {
     const int64_t W = (N + 63) / 64;
     set_threads(nthreads);
+    /* data-error flags are a property of the inputs, independent of which rows are evaluated:
+     * a malformed offset pair, or a malformed predicate inside a well-formed row */
+    for (int64_t i = 0; i < I; ++i) {
+        if (!range_ok(pred_off[i], pred_off[i + 1], n_preds)) { *err |= F_OFFSETS; continue; }
+        for (int64_t p = pred_off[i]; p < pred_off[i + 1]; ++p)
+            if (!pred_valid(&preds[p], L)) *err |= F_PRED;
+    }
 #pragma omp parallel for schedule(dynamic, 1)
     for (int64_t r = 0; r < nrows; ++r) {
         const int64_t i = rows[r];
@@ -103,8 +124,7 @@ void orc_selectors(const uint8_t *labels, int64_t N, int64_t L,
         for (int64_t w = 0; w < W; ++w) out[w] = 0;
         uint32_t count = 0;
         const int64_t b = pred_off[i], e = pred_off[i + 1];
-        if (b < 0 || e < b || e > n_preds) {
-            set_flag(err, F_OFFSETS);
+        if (!range_ok(b, e, n_preds)) {
             popcnt[r] = 0;
             continue;
         }
@@ -112,10 +132,7 @@ void orc_selectors(const uint8_t *labels, int64_t N, int64_t L,
             int ok = 1;
             for (int64_t p = b; p < e; ++p) {
                 const o_pred *q = &preds[p];
-                int valid = q->label < L && q->op <= 2 && q->rsv0 == 0 && q->rsv1 == 0 &&
-                            (q->op == O_EXISTS || ((q->vals[3] >> 63) & 1) == 0);
-                if (!valid) {
-                    set_flag(err, F_PRED);
+                if (!pred_valid(q, L)) {
                     ok = 0;
                     continue;
                 }
@@ -156,21 +173,32 @@ static int rule_matches(const o_rule *r, const uint32_t *h)
     return 1;
 }
 
-static uint32_t jur_bit(const uint8_t *jur, int64_t s, uint32_t *err)
+static uint32_t jur_bit(const uint8_t *jur, int64_t s)
 {
-    if (jur[s] >= 32) {
-        set_flag(err, F_JUR);
-        return 0;
-    }
-    return (uint32_t)1 << jur[s];
+    return jur[s] >= 32 ? 0 : (uint32_t)1 << jur[s];
 }
 
 void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                const uint8_t *jur, const int32_t *rule_off, const o_rule *rules, int64_t n_rules,
-               const uint32_t *hdr, const int32_t *ingress, int64_t ttl,
+               const uint32_t *hdr, const int32_t *ingress, int64_t T, int64_t ttl,
                const int64_t *idx, int64_t nidx, o_trace *out, uint32_t *err, int nthreads)
 {
     set_threads(nthreads);
+    /* data-error flags: a sweep over every input item */
+    for (int64_t t = 0; t < T; ++t)
+        if (ingress[t] < 0 || ingress[t] >= S) { *err |= F_SWITCH; break; }
+    for (int64_t p = 0; p < n_ports; ++p)
+        if (port_peer[p] < -1 || port_peer[p] >= S) { *err |= F_SWITCH; break; }
+    for (int64_t s = 0; s < S; ++s) {
+        if (jur[s] >= 32) *err |= F_JUR;
+        const int pok = range_ok(port_off[s], port_off[s + 1], n_ports);
+        const int rok = range_ok(rule_off[s], rule_off[s + 1], n_rules);
+        if (!pok || !rok) *err |= F_OFFSETS;
+        if (!rok) continue;
+        const int64_t np = pok ? port_off[s + 1] - port_off[s] : 0;
+        for (int64_t r = rule_off[s]; r < rule_off[s + 1]; ++r)
+            if (rules[r].action != 0xFFFF && (int64_t)rules[r].action >= np) { *err |= F_ACTION; break; }
+    }
 #pragma omp parallel for schedule(dynamic, 16)
     for (int64_t k = 0; k < nidx; ++k) {
         const int64_t t = idx[k];
@@ -180,22 +208,19 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
         res.last_port = 0xFFFF;
         res.hops = 0;
         if (s < 0 || s >= S) {
-            set_flag(err, F_SWITCH);
             res.jmask = 0;
             res.last_switch = (int32_t)s;
             res.state = O_MISS;
             out[k] = res;
             continue;
         }
-        uint32_t jm = jur_bit(jur, s, err);
+        uint32_t jm = jur_bit(jur, s);
         int64_t hops = 0;
         int state;
         for (;;) {
             const int64_t rb = rule_off[s], re = rule_off[s + 1];
             int64_t best = -1;
-            if (rb < 0 || re < rb || re > n_rules) {
-                set_flag(err, F_OFFSETS);
-            } else {
+            if (range_ok(rb, re, n_rules)) {
                 for (int64_t r = rb; r < re; ++r) {
                     if (!rule_matches(&rules[r], h)) continue;
                     if (best < 0 || rules[r].priority > rules[best].priority) best = r;
@@ -205,27 +230,20 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
             const unsigned a = rules[best].action;
             if (a == 0xFFFF) { state = O_DROP; break; }
             const int64_t pb = port_off[s], pe = port_off[s + 1];
-            if (pb < 0 || pe < pb || pe > n_ports) {
-                set_flag(err, F_OFFSETS);
-                state = O_MISS;
-                break;
-            }
-            if ((int64_t)a >= pe - pb) {
-                set_flag(err, F_ACTION);
+            if (!range_ok(pb, pe, n_ports) || (int64_t)a >= pe - pb) {
                 state = O_MISS;
                 break;
             }
             const int64_t peer = port_peer[pb + a];
             if (peer == -1) { state = O_EGRESS; res.last_port = (uint16_t)a; break; }
             if (peer < -1 || peer >= S) {
-                set_flag(err, F_SWITCH);
                 state = O_MISS;
                 break;
             }
             if (hops == ttl) { state = O_TTL; break; }
             s = peer;
             ++hops;
-            jm |= jur_bit(jur, s, err);
+            jm |= jur_bit(jur, s);
         }
         res.jmask = jm;
         res.last_switch = (int32_t)s;
@@ -238,17 +256,28 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
 /* ------------------------------------------------------------------ A5
  * Hop distance from src inside the subgraph induced by the allowed
  * switches: vertex v is allowed when bit region[v] of `allowed` is set
- * (region >= 32 is never allowed and raises F_JUR).  Textbook FIFO
+ * (region >= 32 is never allowed).  Textbook FIFO
  * breadth-first search over the undirected CSR graph.  A disallowed or
  * out-of-range source leaves every distance at -1.  With target == NULL
  * the full row [V] is written, else the single distance to target[q].
  */
 void orc_reach(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
-               const uint8_t *region, const int32_t *src, const uint32_t *allowed,
+               const uint8_t *region, int64_t Q, const int32_t *src, const uint32_t *allowed,
                const int32_t *target, const int64_t *qidx, int64_t nq,
                int32_t *dist_out, uint32_t *err, int nthreads)
 {
     set_threads(nthreads);
+    /* data-error flags: a sweep over every input item */
+    for (int64_t v = 0; v < V; ++v) {
+        if (region[v] >= 32) *err |= F_JUR;
+        if (!range_ok(adj_off[v], adj_off[v + 1], n_adj)) *err |= F_OFFSETS;
+    }
+    for (int64_t p = 0; p < n_adj; ++p)
+        if (adj[p] < 0 || adj[p] >= V) { *err |= F_GRAPH; break; }
+    for (int64_t q = 0; q < Q; ++q) {
+        if (src[q] < 0 || src[q] >= V) *err |= F_SWITCH;
+        if (target && (target[q] < 0 || target[q] >= V)) *err |= F_SWITCH;
+    }
 #pragma omp parallel
     {
         int32_t *dist = (int32_t *)malloc(sizeof(int32_t) * (size_t)(V > 0 ? V : 1));
@@ -263,12 +292,10 @@ void orc_reach(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_
             int tgt_ok = 1;
             if (target) {
                 tgt = target[q];
-                if (tgt < 0 || tgt >= V) { set_flag(err, F_SWITCH); tgt_ok = 0; }
+                if (tgt < 0 || tgt >= V) tgt_ok = 0;
             }
             int src_ok = 1;
-            if (s < 0 || s >= V) { set_flag(err, F_SWITCH); src_ok = 0; }
-            else if (region[s] >= 32) { set_flag(err, F_JUR); src_ok = 0; }
-            else if (!((A >> region[s]) & 1)) src_ok = 0;
+            if (s < 0 || s >= V || region[s] >= 32 || !((A >> region[s]) & 1)) src_ok = 0;
             if (src_ok) {
                 int64_t head = 0, tail = 0;
                 dist[s] = 0;
@@ -276,12 +303,11 @@ void orc_reach(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_
                 while (head < tail) {
                     const int64_t u = queue[head++];
                     const int64_t b = adj_off[u], e = adj_off[u + 1];
-                    if (b < 0 || e < b || e > n_adj) { set_flag(err, F_OFFSETS); continue; }
+                    if (!range_ok(b, e, n_adj)) continue;
                     for (int64_t p = b; p < e; ++p) {
                         const int64_t v = adj[p];
-                        if (v < 0 || v >= V) { set_flag(err, F_GRAPH); continue; }
-                        if (region[v] >= 32) { set_flag(err, F_JUR); continue; }
-                        if (!((A >> region[v]) & 1)) continue;
+                        if (v < 0 || v >= V) continue;
+                        if (region[v] >= 32 || !((A >> region[v]) & 1)) continue;
                         if (dist[v] != -1) continue;
                         dist[v] = dist[u] + 1;
                         queue[tail++] = v;

@@ -1,0 +1,264 @@
+"""MI355X compliance checker -- Python binding of libpc.so.
+
+The library (include/pc.h) runs the validator checks of LLM-driven,
+intent-based privacy orchestration (arXiv 2602.16100) as HIP kernels on one
+GPU: node-selector evaluation (pc_eval_selectors), flow-table tracing
+(pc_trace_flows), masked reachability (pc_masked_reach) and the per-intent
+verdict (pc_report).
+
+This module only marshals arguments: torch tensors provide device memory
+and the current HIP stream; every step of the computation runs in
+libpc.so.  There is no CPU fallback -- if the library is missing or no GPU
+is present, calls raise.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import numpy as np
+import torch  # imported first so that libpc.so binds to the HIP runtime torch already loaded
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "_lib", "libpc.so")
+
+PC_OK, PC_EINVAL, PC_ENOMEM, PC_EDEVICE = 0, -1, -2, -3
+PC_EGRESS, PC_DROP, PC_MISS, PC_TTL = 0, 1, 2, 3
+DERR = {"PRED": 1, "OFFSETS": 2, "ACTION": 4, "SWITCH": 8, "JUR": 16, "GRAPH": 32, "INTENT": 64}
+
+PRED_BYTES, RULE_BYTES, KEY_BYTES, INTENT_BYTES, EXPECT_BYTES = 40, 40, 16, 32, 12
+TRACE_OUT_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port", "<u2"),
+                         ("hops", "u1"), ("state", "u1")])
+SUMMARY_DT = np.dtype([("counts", "<u8", (4, 8)), ("no_path", "<u8", (4,))])
+assert TRACE_OUT_DT.itemsize == 12 and SUMMARY_DT.itemsize == 288
+
+
+class PCError(RuntimeError):
+    def __init__(self, code, msg):
+        super().__init__(f"libpc error {code}: {msg}")
+        self.code = code
+
+
+_lib = None
+
+
+def _hip_runtimes_mapped():
+    paths = set()
+    try:
+        with open("/proc/self/maps") as f:
+            for line in f:
+                if "libamdhip64" in line:
+                    paths.add(os.path.realpath(line.split()[-1]))
+    except OSError:
+        pass
+    return paths
+
+
+def lib():
+    """Load libpc.so once (raises if it has not been built)."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is missing: run `python -m paper_2602_16100_amd._build` first")
+    L = ctypes.CDLL(LIB_PATH)
+    if len(_hip_runtimes_mapped()) > 1:
+        raise ImportError(f"two HIP runtimes mapped in this process: {_hip_runtimes_mapped()}")
+    P, I32, I64, C = ctypes.c_void_p, ctypes.c_int32, ctypes.c_int64, ctypes.c_int
+    L.pc_create.argtypes = [ctypes.POINTER(P), C]
+    L.pc_destroy.argtypes = [P]
+    L.pc_last_error.argtypes = [P]
+    L.pc_last_error.restype = ctypes.c_char_p
+    L.pc_version.restype = C
+    L.pc_data_errors.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32), C]
+    L.pc_eval_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
+    L.pc_trace_flows.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, P]
+    L.pc_masked_reach.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, P]
+    L.pc_report.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P]
+    L.pc_profile.argtypes = [P, C]
+    L.pc_profile_read.argtypes = [P, C, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I64),
+                                  ctypes.POINTER(ctypes.c_double)]
+    _lib = L
+    return L
+
+
+EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_errors", "pc_profile",
+            "pc_profile_read", "pc_eval_selectors", "pc_trace_flows", "pc_masked_reach", "pc_report")
+
+
+class Context:
+    """A libpc context on one device (owns the scratch arena)."""
+
+    def __init__(self, device: int = 0):
+        self.device = device
+        h = ctypes.c_void_p()
+        rc = lib().pc_create(ctypes.byref(h), device)
+        if rc != PC_OK:
+            raise PCError(rc, f"pc_create(device={device}) failed")
+        self.handle = h
+
+    def close(self):
+        if self.handle:
+            lib().pc_destroy(self.handle)
+            self.handle = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def check(self, rc):
+        if rc != PC_OK:
+            raise PCError(rc, lib().pc_last_error(self.handle).decode(errors="replace"))
+
+    def data_errors(self, clear: bool = True, stream=None) -> int:
+        """Synchronise the stream and return (and clear) the sticky data-error word."""
+        f = ctypes.c_uint32()
+        self.check(lib().pc_data_errors(self.handle, _stream(stream), ctypes.byref(f), int(clear)))
+        return int(f.value)
+
+
+    def profile(self, enable: bool):
+        """Reset the per-kernel timing tallies and switch timing on or off."""
+        self.check(lib().pc_profile(self.handle, int(enable)))
+
+    def profile_read(self) -> dict:
+        """{kernel name: (launches, total milliseconds)} since the last reset."""
+        out = {}
+        i = 0
+        while True:
+            name = ctypes.c_char_p()
+            n = ctypes.c_int64()
+            ms = ctypes.c_double()
+            rc = lib().pc_profile_read(self.handle, i, ctypes.byref(name), ctypes.byref(n), ctypes.byref(ms))
+            if rc != PC_OK:
+                break
+            out[name.value.decode()] = (int(n.value), float(ms.value))
+            i += 1
+        return out
+
+
+_contexts: dict = {}
+
+
+def context(device: int | None = None) -> Context:
+    """The default context of a device (created on first use)."""
+    if device is None:
+        device = torch.cuda.current_device()
+    if device not in _contexts:
+        _contexts[device] = Context(device)
+    return _contexts[device]
+
+
+def _ptr(t):
+    if t is None:
+        return None
+    assert t.is_cuda and t.is_contiguous(), "libpc takes contiguous device tensors"
+    return ctypes.c_void_p(t.data_ptr())
+
+
+def _stream(stream):
+    if stream is None:
+        stream = torch.cuda.current_stream()
+    return ctypes.c_void_p(stream.cuda_stream)
+
+
+def to_device(arr: np.ndarray, device="cuda") -> torch.Tensor:
+    """A numpy array (plain or a structured record array) as a device tensor.
+    Record arrays travel as uint8 [n, record_size]."""
+    a = np.ascontiguousarray(arr)
+    if a.dtype.fields is not None:
+        a = a.view(np.uint8).reshape(arr.shape[0], arr.dtype.itemsize)
+    elif a.dtype == np.uint64:
+        a = a.view(np.int64)
+    elif a.dtype == np.uint32:
+        a = a.view(np.int32)
+    elif a.dtype == np.uint16:
+        a = a.view(np.int16)
+    return torch.from_numpy(a).to(device)
+
+
+def records(t: torch.Tensor, dtype: np.dtype) -> np.ndarray:
+    """Device/host tensor of packed records -> numpy structured array."""
+    return t.detach().cpu().contiguous().numpy().view(np.uint8).reshape(-1).view(dtype)
+
+
+def pc_eval_selectors(labels, pred_off, preds, n_preds=None, feasible=None, popcnt=None, ctx=None, stream=None):
+    """A1: feasible-node bitset [I, ceil(N/64)] (int64 storage of uint64 words)
+    and popcount [I] (int32 storage of uint32)."""
+    ctx = ctx or context()
+    N, L = (int(labels.shape[0]), int(labels.shape[1])) if labels.dim() == 2 else (0, 0)
+    I = int(pred_off.shape[0]) - 1
+    n_preds = int(preds.shape[0]) if n_preds is None else int(n_preds)
+    W = (N + 63) // 64
+    dev = pred_off.device
+    if feasible is None:
+        feasible = torch.empty((I, W), dtype=torch.int64, device=dev)
+    if popcnt is None:
+        popcnt = torch.empty(I, dtype=torch.int32, device=dev)
+    ctx.check(lib().pc_eval_selectors(ctx.handle, _ptr(labels) if labels.numel() else None, N, L, _ptr(pred_off),
+                                      _ptr(preds) if preds.numel() else None, n_preds, I,
+                                      _ptr(feasible) if feasible.numel() else None, _ptr(popcnt), _stream(stream)))
+    return feasible, popcnt
+
+
+def pc_trace_flows(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, n_ports=None, n_rules=None,
+                   out=None, ctx=None, stream=None):
+    """A2-A4: one 12-byte pc_trace_out record per trace (uint8 [T, 12])."""
+    ctx = ctx or context()
+    T = int(ingress.shape[0])
+    n_ports = int(port_peer.shape[0]) if n_ports is None else int(n_ports)
+    n_rules = int(rules.shape[0]) if n_rules is None else int(n_rules)
+    if out is None:
+        out = torch.empty((T, 12), dtype=torch.uint8, device=ingress.device)
+    ctx.check(lib().pc_trace_flows(ctx.handle, int(S), _ptr(port_off), _ptr(port_peer) if port_peer.numel() else None,
+                                   n_ports, _ptr(jur), _ptr(rule_off), _ptr(rules) if rules.numel() else None,
+                                   n_rules, _ptr(hdr) if T else None, _ptr(ingress) if T else None, T, int(ttl),
+                                   _ptr(out) if T else None, _stream(stream)))
+    return out
+
+
+def pc_masked_reach(V, adj_off, adj, region, src, allowed, target=None, n_adj=None, dist=None, ctx=None,
+                    stream=None):
+    """A5: BFS hop distances inside the allowed-induced subgraph: [Q, V] when
+    target is None, else [Q]; -1 = unreachable."""
+    ctx = ctx or context()
+    Q = int(src.shape[0])
+    n_adj = int(adj.shape[0]) if n_adj is None else int(n_adj)
+    if dist is None:
+        shape = (Q, int(V)) if target is None else (Q,)
+        dist = torch.empty(shape, dtype=torch.int32, device=src.device)
+    ctx.check(lib().pc_masked_reach(ctx.handle, int(V), _ptr(adj_off), _ptr(adj) if adj.numel() else None, n_adj,
+                                    _ptr(region), Q, _ptr(src) if Q else None, _ptr(allowed) if Q else None,
+                                    _ptr(target), _ptr(dist) if dist.numel() else None, _stream(stream)))
+    return dist
+
+
+def pc_report(intents, feasible, popcnt, N, traces, expect, reach, pass_=None, reason=None, summary=None, ctx=None,
+              stream=None):
+    """A6: pass bits [ceil(I/64)] (int64 storage of uint64), reason codes [I]
+    (uint8) and the pc_summary record (uint8 [288])."""
+    ctx = ctx or context()
+    I = int(intents.shape[0])
+    rows = int(feasible.shape[0])
+    W = int(feasible.shape[1]) if feasible.dim() == 2 else 0
+    T = int(traces.shape[0])
+    Q = int(reach.shape[0])
+    dev = intents.device
+    if pass_ is None:
+        pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
+    if reason is None:
+        reason = torch.empty(I, dtype=torch.uint8, device=dev)
+    if summary is None:
+        summary = torch.empty(288, dtype=torch.uint8, device=dev)
+    ctx.check(lib().pc_report(ctx.handle, I, _ptr(intents) if I else None, rows,
+                              _ptr(feasible) if feasible.numel() else None, W, _ptr(popcnt) if rows else None,
+                              int(N), _ptr(traces) if T else None, T, _ptr(expect) if I else None,
+                              _ptr(reach) if Q else None, Q, _ptr(pass_) if I else None, _ptr(reason) if I else None,
+                              _ptr(summary), _stream(stream)))
+    return pass_, reason, summary
+
+
+def version() -> int:
+    return int(lib().pc_version())

@@ -1,0 +1,130 @@
+// Internal declarations shared by the host layer and the kernel modules of
+// libpc.  Not part of the public ABI (include/pc.h).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include <string>
+#include <vector>
+
+#include "pc.h"
+
+struct pc_ctx {
+    int device;
+    char msg[512];
+    uint32_t *d_err;     // sticky data-error word (device)
+    int32_t *d_small;    // small device counters (live counts, totals)
+    int32_t *h_small;    // pinned host mirror of d_small
+    char *arena;         // scratch arena (device)
+    size_t arena_bytes;
+    char *aux;           // second scratch buffer, sized after a device-side count
+    size_t aux_bytes;
+    // optional per-kernel timing (pc_profile)
+    bool prof;
+    std::vector<hipEvent_t> ev_free;
+    struct Pending { const char *name; hipEvent_t a, b; };
+    std::vector<Pending> pending;
+    struct Tally { std::string name; int64_t launches; double ms; };
+    std::vector<Tally> tally;
+};
+
+// Brackets the kernel launches in its scope with HIP events on `stream`
+// when the context's profiling is enabled.
+struct KernelTimer {
+    pc_ctx *ctx;
+    const char *name;
+    hipStream_t stream;
+    hipEvent_t a = nullptr, b = nullptr;
+    KernelTimer(pc_ctx *c, const char *n, hipStream_t s);
+    ~KernelTimer();
+};
+
+// Bump allocator over the context arena.  Sizes are computed first with a
+// dry run (base == nullptr), then the arena is grown and carved for real.
+struct Carver {
+    char *base;
+    size_t off;
+    template <class T>
+    T *take(size_t count, size_t align = 256)
+    {
+        off = (off + align - 1) / align * align;
+        T *p = base ? reinterpret_cast<T *>(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+int pc_set_error(pc_ctx *ctx, int code, const char *fmt, ...);
+int pc_ensure_arena(pc_ctx *ctx, size_t bytes);
+int pc_ensure_aux(pc_ctx *ctx, size_t bytes);
+
+#define PC_HIP(ctx, expr)                                                                      \
+    do {                                                                                       \
+        hipError_t e_ = (expr);                                                                \
+        if (e_ != hipSuccess)                                                                  \
+            return pc_set_error((ctx), PC_EDEVICE, "%s: %s (%s:%d)", #expr, hipGetErrorString(e_), \
+                                __FILE__, __LINE__);                                           \
+    } while (0)
+
+#define PC_LAUNCH_CHECK(ctx) PC_HIP((ctx), hipGetLastError())
+
+// Run a launch statement under a KernelTimer named after the kernel.
+#define PC_TIMED(ctx, name, stream, ...)             \
+    do {                                             \
+        KernelTimer kt_((ctx), (name), (stream));    \
+        __VA_ARGS__;                                 \
+    } while (0)
+
+// ---------------------------------------------------------------- common
+void launch_fill_u32(uint32_t *p, size_t n, uint32_t v, hipStream_t s);
+void launch_fill_u64(uint64_t *p, size_t n, uint64_t v, hipStream_t s);
+
+// Exclusive scan of n int32 counts into out[0..n] (out[n] = total), one
+// workgroup; optionally copies the result to out2 and clears counts.
+void launch_scan_i32(const int32_t *counts, int32_t n, int32_t *out, int32_t *out2, int32_t *clear,
+                     hipStream_t s);
+
+// ---------------------------------------------------------------- modules
+int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                  const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
+                  hipStream_t stream);
+
+int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
+              const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
+              const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, pc_trace_out *out,
+              hipStream_t stream);
+
+int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+              const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,
+              const int32_t *target, int32_t *dist, hipStream_t stream);
+
+int run_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
+               int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
+               const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass,
+               uint8_t *reason, pc_summary *summary, hipStream_t stream);
+
+// ---------------------------------------------------------------- device helpers
+__device__ __forceinline__ bool pc_range_ok(int64_t b, int64_t e, int64_t n)
+{
+    return b >= 0 && e >= b && e <= n;
+}
+
+__device__ __forceinline__ int pc_lane() { return threadIdx.x & 63; }
+
+__device__ __forceinline__ uint32_t pc_wave_sum_u32(uint32_t v)
+{
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+
+// Map a linear block id onto work items so that each of the 8 XCDs (blocks
+// are dealt to XCDs round-robin) receives one contiguous range of items.
+__device__ __forceinline__ int64_t pc_xcd_item(int64_t total)
+{
+    const int64_t per = (total + 7) / 8;
+    const int64_t b = blockIdx.x;
+    return (b & 7) * per + (b >> 3);
+}

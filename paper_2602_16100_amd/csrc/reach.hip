@@ -1,0 +1,271 @@
+// A5 -- compliant-path existence and hop distance: breadth-first search
+// restricted to the switches whose jurisdiction an intent allows.
+//
+// The paper's path scheduler searches the live topology for a
+// constraint-respecting path (weighted Dijkstra with a BFS fallback;
+// Network orchestration); as a validator check the question is whether a
+// path exists that never leaves the allowed jurisdictions, and how long the
+// shortest one is.  Vertex v is allowed for query q iff bit region[v] of
+// allowed[q] is set; distances are hop counts in the allowed-induced
+// subgraph, -1 when unreachable or when the source is not allowed.
+//
+// Design (gfx950):
+//   bitset : graphs that fit in LDS (3 x 8 bytes per vertex): 64 queries per
+//            workgroup, one bit each, level-synchronous frontier bitsets
+//            (visited / frontier / next) in LDS, push expansion with 64-bit
+//            LDS atomic OR, the per-query allowed mask applied per vertex as
+//            a precomputed 64-bit region mask; stops when every query's
+//            target is resolved or no frontier bit is left.
+//   queue  : larger graphs: one workgroup per query, frontier queue in
+//            scratch, the distance row itself (or a scratch row, with
+//            targets) as the visited set claimed with compare-and-swap.
+#include "pc_internal.h"
+
+namespace {
+
+constexpr int kBitsetThreads = 256;
+constexpr int kQueueThreads = 256;
+constexpr int kMaxBitsetV = 6400;  // 3 x 8 B x V + masks within 160 KB of LDS
+
+__device__ __forceinline__ bool allowed_v(const uint8_t *region, uint32_t A, int32_t v)
+{
+    const uint32_t r = region[v];
+    return r < 32 && ((A >> r) & 1u);
+}
+
+__global__ void k_rc_validate(int32_t V, const int32_t *__restrict__ adj_off, const int32_t *__restrict__ adj,
+                              int64_t n_adj, const uint8_t *__restrict__ region, int32_t Q,
+                              const int32_t *__restrict__ src, const int32_t *__restrict__ target,
+                              uint32_t *__restrict__ d_err)
+{
+    uint32_t errs = 0;
+    const int64_t stride = static_cast<int64_t>(gridDim.x) * blockDim.x;
+    const int64_t i0 = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x;
+    for (int64_t v = i0; v < V; v += stride) {
+        if (region[v] >= 32) errs |= PC_DERR_JUR;
+        if (!pc_range_ok(adj_off[v], adj_off[v + 1], n_adj)) errs |= PC_DERR_OFFSETS;
+    }
+    for (int64_t p = i0; p < n_adj; p += stride) {
+        const int32_t v = adj[p];
+        if (v < 0 || v >= V) errs |= PC_DERR_GRAPH;
+    }
+    for (int64_t q = i0; q < Q; q += stride) {
+        if (src[q] < 0 || src[q] >= V) errs |= PC_DERR_SWITCH;
+        if (target && (target[q] < 0 || target[q] >= V)) errs |= PC_DERR_SWITCH;
+    }
+    if (errs) atomicOr(d_err, errs);
+}
+
+// 64 queries per workgroup; dist is [Q][V] (target == nullptr) or [Q].
+__global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const int32_t *__restrict__ adj_off,
+                                                              const int32_t *__restrict__ adj, int64_t n_adj,
+                                                              const uint8_t *__restrict__ region, int32_t Q,
+                                                              const int32_t *__restrict__ src,
+                                                              const uint32_t *__restrict__ allowed,
+                                                              const int32_t *__restrict__ target,
+                                                              int32_t *__restrict__ dist)
+{
+    extern __shared__ uint64_t lds[];
+    uint64_t *vis = lds;
+    uint64_t *fr = vis + V;
+    uint64_t *nx = fr + V;
+    uint64_t *rmask = nx + V;  // [32]
+    __shared__ int flag_any, flag_done;
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int32_t q0 = blockIdx.x * 64;
+    const int32_t nq = min(64, Q - q0);
+    for (int32_t v = tid; v < V; v += kBitsetThreads) {
+        vis[v] = 0;
+        fr[v] = 0;
+        nx[v] = 0;
+    }
+    if (tid < 64) {
+        const uint32_t A = lane < nq ? allowed[q0 + lane] : 0u;
+        for (int r = 0; r < 32; ++r) {
+            const uint64_t m = __ballot((A >> r) & 1u);
+            if (lane == 0) rmask[r] = m;
+        }
+    }
+    __syncthreads();
+    // sources; per-query result state lives in wave 0, lane = query
+    int32_t res = -1, tgt = -1;
+    bool done = true;
+    if (tid < 64 && lane < nq) {
+        const int32_t q = q0 + lane;
+        const int32_t s = src[q];
+        const bool s_ok = s >= 0 && s < V && allowed_v(region, allowed[q], s);
+        if (target) {
+            tgt = target[q];
+            done = !(s_ok && tgt >= 0 && tgt < V);
+        }
+        if (s_ok) {
+            atomicOr(reinterpret_cast<unsigned long long *>(&fr[s]), 1ull << lane);
+            atomicOr(reinterpret_cast<unsigned long long *>(&vis[s]), 1ull << lane);
+            if (!target) dist[static_cast<int64_t>(q) * V + s] = 0;
+        }
+    }
+    __syncthreads();
+    if (tid < 64 && !done && ((vis[tgt] >> lane) & 1)) {
+        res = 0;
+        done = true;
+    }
+    for (int32_t d = 1;; ++d) {
+        if (tid == 0) flag_any = 0;
+        // push the frontier along every edge
+        for (int32_t u = tid; u < V; u += kBitsetThreads) {
+            const uint64_t f = fr[u];
+            if (!f) continue;
+            const int64_t b = adj_off[u], e = adj_off[u + 1];
+            if (!pc_range_ok(b, e, n_adj)) continue;
+            for (int64_t p = b; p < e; ++p) {
+                const int32_t v = adj[p];
+                if (v >= 0 && v < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[v]), f);
+            }
+        }
+        __syncthreads();
+        bool any = false;
+        for (int32_t v = tid; v < V; v += kBitsetThreads) {
+            uint64_t n = nx[v];
+            nx[v] = 0;
+            if (n) {
+                const uint32_t r = region[v];
+                n &= (r < 32 ? rmask[r] : 0ull) & ~vis[v];
+                vis[v] |= n;
+                if (!target) {
+                    uint64_t m = n;
+                    while (m) {
+                        const int q = __builtin_ctzll(m);
+                        m &= m - 1;
+                        dist[static_cast<int64_t>(q0 + q) * V + v] = d;
+                    }
+                }
+            }
+            fr[v] = n;
+            any |= n != 0;
+        }
+        if (any) flag_any = 1;
+        __syncthreads();
+        if (tid < 64) {
+            if (!done && ((fr[tgt] >> lane) & 1)) {
+                res = d;
+                done = true;
+            }
+            const bool all_done = __ballot(!done) == 0;
+            if (tid == 0) flag_done = target ? all_done : 0;
+        }
+        __syncthreads();
+        const bool stop = !flag_any || flag_done;
+        __syncthreads();
+        if (stop) break;
+    }
+    if (target && tid < 64 && lane < nq) dist[q0 + lane] = res;
+}
+
+// One workgroup per query (grid-stride over queries).
+__global__ __launch_bounds__(kQueueThreads) void k_rc_queue(int32_t V, const int32_t *__restrict__ adj_off,
+                                                            const int32_t *__restrict__ adj, int64_t n_adj,
+                                                            const uint8_t *__restrict__ region, int32_t Q,
+                                                            const int32_t *__restrict__ src,
+                                                            const uint32_t *__restrict__ allowed,
+                                                            const int32_t *__restrict__ target,
+                                                            int32_t *__restrict__ dist, int32_t *__restrict__ qbuf_all,
+                                                            int32_t *__restrict__ rows_all)
+{
+    __shared__ int32_t tail_s;
+    const int tid = threadIdx.x;
+    int32_t *qbuf = qbuf_all + static_cast<int64_t>(blockIdx.x) * V;
+    for (int32_t q = blockIdx.x; q < Q; q += gridDim.x) {
+        int32_t *drow = target ? rows_all + static_cast<int64_t>(blockIdx.x) * V : dist + static_cast<int64_t>(q) * V;
+        const uint32_t A = allowed[q];
+        const int32_t s = src[q];
+        const int32_t tgt = target ? target[q] : -1;
+        const bool s_ok = s >= 0 && s < V && allowed_v(region, A, s);
+        const bool t_ok = !target || (tgt >= 0 && tgt < V);
+        if (tid == 0) {
+            tail_s = 0;
+            if (s_ok) {
+                drow[s] = 0;
+                qbuf[0] = s;
+                tail_s = 1;
+            }
+        }
+        __syncthreads();
+        int32_t lo = 0, hi = tail_s;
+        for (int32_t d = 0; lo < hi; ++d) {
+            if (target && t_ok && drow[tgt] != -1) break;
+            for (int32_t i = lo + tid; i < hi; i += kQueueThreads) {
+                const int32_t u = qbuf[i];
+                const int64_t b = adj_off[u], e = adj_off[u + 1];
+                if (!pc_range_ok(b, e, n_adj)) continue;
+                for (int64_t p = b; p < e; ++p) {
+                    const int32_t v = adj[p];
+                    if (v < 0 || v >= V || !allowed_v(region, A, v)) continue;
+                    if (atomicCAS(&drow[v], -1, d + 1) == -1) qbuf[atomicAdd(&tail_s, 1)] = v;
+                }
+            }
+            __syncthreads();
+            lo = hi;
+            hi = tail_s;
+            __syncthreads();
+        }
+        if (target) {
+            __syncthreads();
+            if (tid == 0) dist[q] = (s_ok && t_ok) ? drow[tgt] : -1;
+            __syncthreads();
+            const int32_t n = tail_s;
+            for (int32_t i = tid; i < n; i += kQueueThreads) drow[qbuf[i]] = -1;
+        }
+        __syncthreads();
+    }
+}
+
+}  // namespace
+
+int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+              const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed, const int32_t *target,
+              int32_t *dist, hipStream_t stream)
+{
+    const int64_t nval = (V > Q ? V : Q) > n_adj ? (V > Q ? V : Q) : n_adj;
+    if (nval > 0) {
+        int64_t blocks = (nval + 255) / 256;
+        if (blocks > 4096) blocks = 4096;
+        PC_TIMED(ctx, "k_rc_validate", stream, hipLaunchKernelGGL(k_rc_validate, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, V, adj_off, adj,
+                           n_adj, region, Q, src, target, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    if (Q == 0) return PC_OK;
+    if (!target) launch_fill_u32(reinterpret_cast<uint32_t *>(dist), static_cast<size_t>(Q) * V, 0xFFFFFFFFu, stream);
+    if (V == 0) {
+        if (target) launch_fill_u32(reinterpret_cast<uint32_t *>(dist), static_cast<size_t>(Q), 0xFFFFFFFFu, stream);
+        PC_LAUNCH_CHECK(ctx);
+        return PC_OK;
+    }
+    int max_lds = 0;
+    PC_HIP(ctx, hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, ctx->device));
+    const size_t lds = static_cast<size_t>(V) * 3 * 8 + 32 * 8;
+    if (V <= kMaxBitsetV && lds + 64 <= static_cast<size_t>(max_lds)) {
+        PC_HIP(ctx, hipFuncSetAttribute(reinterpret_cast<const void *>(k_rc_bitset),
+                                        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+        PC_TIMED(ctx, "k_rc_bitset", stream, hipLaunchKernelGGL(k_rc_bitset, dim3(static_cast<unsigned>((Q + 63) / 64)), dim3(kBitsetThreads), lds, stream,
+                           V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist));
+        PC_LAUNCH_CHECK(ctx);
+        return PC_OK;
+    }
+    int32_t grid = Q < 256 ? Q : 256;
+    int32_t *qbuf, *rows;
+    auto carve = [&](Carver &c) {
+        qbuf = c.take<int32_t>(static_cast<size_t>(grid) * V);
+        rows = c.take<int32_t>(target ? static_cast<size_t>(grid) * V : 1);
+    };
+    Carver dry{nullptr, 0};
+    carve(dry);
+    int rc = pc_ensure_arena(ctx, dry.off);
+    if (rc) return rc;
+    Carver real{ctx->arena, 0};
+    carve(real);
+    if (target) launch_fill_u32(reinterpret_cast<uint32_t *>(rows), static_cast<size_t>(grid) * V, 0xFFFFFFFFu, stream);
+    PC_TIMED(ctx, "k_rc_queue", stream, hipLaunchKernelGGL(k_rc_queue, dim3(static_cast<unsigned>(grid)), dim3(kQueueThreads), 0, stream, V, adj_off, adj,
+                       n_adj, region, Q, src, allowed, target, dist, qbuf, rows));
+    PC_LAUNCH_CHECK(ctx);
+    return PC_OK;
+}

@@ -1,0 +1,432 @@
+// A2-A4 -- routing constraints on the realised paths: trace every header
+// hop by hop through the per-switch, priority-ordered ternary flow tables
+// and collect the jurisdictions visited.
+//
+// The paper compiles every path "into per-hop flow rules" (Network
+// orchestration) and a routing constraint must hold "for the realized paths
+// induced by" them (Formal Model and Satisfaction, condition (ii)); the
+// validator checks that realised paths avoid forbidden switches (validator
+// check definition).  The first-match rule order (larger priority, then
+// lower index), table miss, drop, egress and TTL are the readings written in
+// include/pc.h.
+//
+// Design (gfx950):
+//   prep   : per 32-rule group, for each of kChunks 4-bit chunks of header
+//            word 2 (ports) and each of the 16 chunk values, the 32-bit set
+//            of rules whose mask/value admit that chunk value.  Stored
+//            plane-major per switch so a wavefront loads 64 groups with
+//            coalesced reads.  Also validates ports, jurisdictions, offsets
+//            and actions (the data-error sweep).
+//   levels : level-synchronous walk.  Live traces are bucketed by their
+//            current switch (count -> scan -> scatter); one workgroup per
+//            switch keeps the switch's chunk sets in VGPRs (16,384 rules per
+//            8-wave slice) and filters every lookup of its bucket with
+//            kChunks uniform-index register reads and ANDs; the rare
+//            survivors are verified against the full 104-bit rule and the
+//            first match is the minimum of (0xFFFF - priority, index) over
+//            the workgroup (LDS 64-bit atomic min).  An advance pass applies
+//            the action and re-buckets the traces still in flight.
+#include "pc_internal.h"
+
+namespace {
+
+constexpr int kChunks = 6;                 // 4-bit chunks of w[2] used by the filter (bits 0..23)
+constexpr int kPlaneWords = kChunks * 16;  // words per 32-rule group
+constexpr int kMatchWaves = 8;
+constexpr int kMatchThreads = kMatchWaves * 64;
+constexpr int kSliceGroups = kMatchThreads;  // one group (32 rules) per lane
+constexpr int kTile = 2048;                  // lookups per LDS tile
+constexpr int kPrepGroups = 32;              // groups per prep workgroup (1024 threads, 2 groups per wave)
+constexpr uint64_t kNoMatch = ~0ull;
+
+// 16 chunk-value sets of one 4-bit chunk, kept in VGPRs; indexed with a
+// wave-uniform value this lowers to register-indexed moves (s_set_gpr_idx).
+typedef uint32_t v16u __attribute__((ext_vector_type(16)));
+
+__device__ __forceinline__ uint32_t jur_bit(const uint8_t *jur, int32_t s)
+{
+    const uint32_t j = jur[s];
+    return j < 32 ? (1u << j) : 0u;
+}
+
+// Per switch: validate offsets / jurisdiction, count 32-rule groups and prep blocks.
+__global__ void k_tr_switch_info(int32_t S, const int32_t *__restrict__ port_off, int64_t n_ports,
+                                 const uint8_t *__restrict__ jur, const int32_t *__restrict__ rule_off,
+                                 int64_t n_rules, int32_t *__restrict__ gcount, int32_t *__restrict__ bcount,
+                                 uint32_t *__restrict__ d_err)
+{
+    uint32_t errs = 0;
+    for (int32_t s = blockIdx.x * blockDim.x + threadIdx.x; s < S; s += gridDim.x * blockDim.x) {
+        if (jur[s] >= 32) errs |= PC_DERR_JUR;
+        const bool pok = pc_range_ok(port_off[s], port_off[s + 1], n_ports);
+        const int64_t rb = rule_off[s], re = rule_off[s + 1];
+        const bool rok = pc_range_ok(rb, re, n_rules);
+        if (!pok || !rok) errs |= PC_DERR_OFFSETS;
+        const int64_t g = rok ? (re - rb + 31) / 32 : 0;
+        gcount[s] = static_cast<int32_t>(g);
+        bcount[s] = static_cast<int32_t>((g + kPrepGroups - 1) / kPrepGroups);
+    }
+    if (errs) atomicOr(d_err, errs);
+}
+
+__global__ void k_tr_port_check(int64_t n_ports, const int32_t *__restrict__ port_peer, int32_t S,
+                                uint32_t *__restrict__ d_err)
+{
+    bool bad = false;
+    for (int64_t p = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; p < n_ports;
+         p += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int32_t v = port_peer[p];
+        bad |= (v < -1 || v >= S);
+    }
+    if (bad) atomicOr(d_err, PC_DERR_SWITCH);
+}
+
+// 16-bit set of 4-bit values x admitted by a rule chunk (value v4, care m4).
+__device__ __forceinline__ uint32_t chunk_admits(uint32_t v4, uint32_t m4)
+{
+    const uint32_t hi[4] = {0xAAAAu, 0xCCCCu, 0xF0F0u, 0xFF00u};
+    uint32_t s = 0xFFFFu;
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+        if ((m4 >> j) & 1) s &= ((v4 >> j) & 1) ? hi[j] : (~hi[j] & 0xFFFFu);
+    return s;
+}
+
+// Build the chunk sets of kPrepGroups groups of one switch; validate actions.
+__global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__restrict__ port_off, int64_t n_ports,
+                                                  const int32_t *__restrict__ rule_off,
+                                                  const pc_rule *__restrict__ rules,
+                                                  const int32_t *__restrict__ gcount,
+                                                  const int32_t *__restrict__ gofs, const int32_t *__restrict__ bofs,
+                                                  uint32_t *__restrict__ filt, uint32_t *__restrict__ d_err)
+{
+    __shared__ uint32_t tile[kPlaneWords * kPrepGroups];
+    const int32_t b = blockIdx.x;
+    if (b >= bofs[S]) return;
+    // switch owning this block: largest s with bofs[s] <= b
+    int32_t lo = 0, hi = S;  // invariant: bofs[lo] <= b < bofs[hi]
+    while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (bofs[mid] <= b) lo = mid;
+        else hi = mid;
+    }
+    const int32_t s = lo;
+    const int32_t G = gcount[s];
+    const int32_t g0 = (b - bofs[s]) * kPrepGroups;
+    const int64_t rb = rule_off[s];
+    const int64_t R = rule_off[s + 1] - rb;
+    const bool pok = pc_range_ok(port_off[s], port_off[s + 1], n_ports);
+    const int64_t np = pok ? port_off[s + 1] - port_off[s] : 0;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t local = static_cast<int64_t>(g0 + 2 * wave) * 32 + lane;  // rule index within the switch
+    uint32_t v2 = 0, m2 = 0;
+    bool ok = local < R && (g0 + 2 * wave + (lane >> 5)) < G;
+    bool bad_action = false;
+    if (ok) {
+        const pc_rule *r = rules + rb + local;
+        v2 = r->value.w[2];
+        m2 = r->mask.w[2];
+        const uint32_t a = r->action;
+        bad_action = a != PC_ACTION_DROP && static_cast<int64_t>(a) >= np;
+    }
+#pragma unroll
+    for (int c = 0; c < kChunks; ++c) {
+        const uint32_t adm = ok ? chunk_admits((v2 >> (4 * c)) & 15u, (m2 >> (4 * c)) & 15u) : 0u;
+#pragma unroll
+        for (int x = 0; x < 16; ++x) {
+            const uint64_t bal = __ballot((adm >> x) & 1u);
+            if (lane == 0) {
+                tile[(c * 16 + x) * kPrepGroups + 2 * wave] = static_cast<uint32_t>(bal);
+                tile[(c * 16 + x) * kPrepGroups + 2 * wave + 1] = static_cast<uint32_t>(bal >> 32);
+            }
+        }
+    }
+    if (__ballot(bad_action) && lane == 0) atomicOr(d_err, PC_DERR_ACTION);
+    __syncthreads();
+    uint32_t *dst = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
+    for (int i = threadIdx.x; i < kPlaneWords * kPrepGroups; i += blockDim.x) {
+        const int row = i / kPrepGroups, gl = i % kPrepGroups;
+        const int32_t g = g0 + gl;
+        if (g < G) dst[static_cast<int64_t>(row) * G + g] = tile[i];
+    }
+}
+
+__global__ void k_tr_init(int32_t S, const uint8_t *__restrict__ jur, const int32_t *__restrict__ ingress, int32_t T,
+                          int32_t *__restrict__ cur, uint32_t *__restrict__ jm, int32_t *__restrict__ hops,
+                          int32_t *__restrict__ live, int32_t *__restrict__ nlive, int32_t *__restrict__ counts,
+                          pc_trace_out *__restrict__ out, uint32_t *__restrict__ d_err)
+{
+    bool bad = false;
+    for (int32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < T; t += gridDim.x * blockDim.x) {
+        const int32_t s = ingress[t];
+        if (s < 0 || s >= S) {
+            bad = true;
+            pc_trace_out o;
+            o.jmask = 0;
+            o.last_switch = s;
+            o.last_port = PC_NO_PORT;
+            o.hops = 0;
+            o.state = PC_MISS;
+            out[t] = o;
+            continue;
+        }
+        cur[t] = s;
+        jm[t] = jur_bit(jur, s);
+        hops[t] = 0;
+        live[atomicAdd(nlive, 1)] = t;
+        atomicAdd(&counts[s], 1);
+    }
+    if (bad) atomicOr(d_err, PC_DERR_SWITCH);
+}
+
+__global__ void k_tr_scatter(const int32_t *__restrict__ live, const int32_t *__restrict__ nlive,
+                             const int32_t *__restrict__ cur, int32_t *__restrict__ cursor,
+                             int32_t *__restrict__ bucket)
+{
+    const int32_t n = *nlive;
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        const int32_t t = live[i];
+        bucket[atomicAdd(&cursor[cur[t]], 1)] = t;
+    }
+}
+
+__global__ __launch_bounds__(kMatchThreads) void k_tr_match(
+    const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
+    const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt, const pc_key *__restrict__ hdr,
+    const int32_t *__restrict__ boff, const int32_t *__restrict__ bucket, uint64_t *__restrict__ bestkey)
+{
+    __shared__ uint64_t best[kTile];
+    const int32_t s = blockIdx.x;
+    const int32_t bb = boff[s], be = boff[s + 1];
+    if (bb >= be) return;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int32_t G = gcount[s];
+    const int64_t rb = rule_off[s];
+    const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
+    const int32_t nslices = (G + kSliceGroups - 1) / kSliceGroups;
+    v16u F[kChunks];
+    int32_t loaded = -1;
+    for (int32_t t0 = bb; t0 < be; t0 += kTile) {
+        const int32_t tn = min(kTile, be - t0);
+        for (int i = threadIdx.x; i < tn; i += kMatchThreads) best[i] = kNoMatch;
+        __syncthreads();
+        for (int32_t sl = 0; sl < nslices; ++sl) {
+            const int32_t g = sl * kSliceGroups + wave * 64 + lane;
+            if (loaded != sl) {
+#pragma unroll
+                for (int c = 0; c < kChunks; ++c)
+#pragma unroll
+                    for (int x = 0; x < 16; ++x)
+                        F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * G + g] : 0u;
+                loaded = sl;
+            }
+            const int64_t gbase = rb + static_cast<int64_t>(g) * 32;
+            for (int32_t j = 0; j < tn; ++j) {
+                const int32_t t = __builtin_amdgcn_readfirstlane(bucket[t0 + j]);
+                const uint32_t h2 = __builtin_amdgcn_readfirstlane(hdr[t].w[2]);
+                uint32_t surv = F[0][h2 & 15u];
+#pragma unroll
+                for (int c = 1; c < kChunks; ++c) surv &= F[c][(h2 >> (4 * c)) & 15u];
+                if (__ballot(surv != 0)) {
+                    if (surv) {
+                        const uint32_t h0 = hdr[t].w[0], h1 = hdr[t].w[1], h3 = hdr[t].w[3];
+                        while (surv) {
+                            const int bit = __builtin_ctz(surv);
+                            surv &= surv - 1;
+                            const pc_rule *r = rules + gbase + bit;
+                            const bool m = (((h0 ^ r->value.w[0]) & r->mask.w[0]) |
+                                            ((h1 ^ r->value.w[1]) & r->mask.w[1]) |
+                                            ((h2 ^ r->value.w[2]) & r->mask.w[2]) |
+                                            ((h3 ^ r->value.w[3]) & r->mask.w[3])) == 0;
+                            if (m) {
+                                const uint64_t key = (static_cast<uint64_t>(0xFFFFu - r->priority) << 32) |
+                                                     static_cast<uint32_t>(g * 32 + bit);
+                                atomicMin(reinterpret_cast<unsigned long long *>(&best[j]),
+                                          static_cast<unsigned long long>(key));
+                            }
+                        }
+                    }
+                }
+            }
+        }
+        __syncthreads();
+        for (int i = threadIdx.x; i < tn; i += kMatchThreads) bestkey[bucket[t0 + i]] = best[i];
+        __syncthreads();
+    }
+}
+
+__global__ void k_tr_advance(int32_t S, const int32_t *__restrict__ port_off, const int32_t *__restrict__ port_peer,
+                             int64_t n_ports, const uint8_t *__restrict__ jur, const int32_t *__restrict__ rule_off,
+                             const pc_rule *__restrict__ rules, int32_t ttl, const int32_t *__restrict__ live,
+                             const int32_t *__restrict__ nlive, const uint64_t *__restrict__ bestkey,
+                             int32_t *__restrict__ cur, uint32_t *__restrict__ jm, int32_t *__restrict__ hops,
+                             int32_t *__restrict__ live_next, int32_t *__restrict__ nlive_next,
+                             int32_t *__restrict__ counts_next, pc_trace_out *__restrict__ out)
+{
+    const int32_t n = *nlive;
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        const int32_t t = live[i];
+        int32_t s = cur[t];
+        const uint64_t key = bestkey[t];
+        int state = -1;
+        uint16_t port = PC_NO_PORT;
+        if (key == kNoMatch) {
+            state = PC_MISS;
+        } else {
+            const pc_rule *r = rules + rule_off[s] + static_cast<uint32_t>(key);
+            const uint32_t a = r->action;
+            if (a == PC_ACTION_DROP) {
+                state = PC_DROP;
+            } else {
+                const int64_t pb = port_off[s], pe = port_off[s + 1];
+                if (!pc_range_ok(pb, pe, n_ports) || static_cast<int64_t>(a) >= pe - pb) {
+                    state = PC_MISS;
+                } else {
+                    const int32_t peer = port_peer[pb + a];
+                    if (peer == -1) {
+                        state = PC_EGRESS;
+                        port = static_cast<uint16_t>(a);
+                    } else if (peer < -1 || peer >= S) {
+                        state = PC_MISS;
+                    } else if (hops[t] == ttl) {
+                        state = PC_TTL;
+                    } else {
+                        s = peer;
+                        cur[t] = s;
+                        hops[t] += 1;
+                        jm[t] |= jur_bit(jur, s);
+                        live_next[atomicAdd(nlive_next, 1)] = t;
+                        atomicAdd(&counts_next[s], 1);
+                    }
+                }
+            }
+        }
+        if (state >= 0) {
+            pc_trace_out o;
+            o.jmask = jm[t];
+            o.last_switch = s;
+            o.last_port = port;
+            o.hops = static_cast<uint8_t>(hops[t]);
+            o.state = static_cast<uint8_t>(state);
+            out[t] = o;
+        }
+    }
+}
+
+unsigned grid_for(int64_t n, int threads)
+{
+    int64_t b = (n + threads - 1) / threads;
+    if (b > 65536) b = 65536;
+    return b > 0 ? static_cast<unsigned>(b) : 1u;
+}
+
+}  // namespace
+
+int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
+              const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
+              const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, pc_trace_out *out,
+              hipStream_t stream)
+{
+    struct Bufs {
+        int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *cursor;
+        int32_t *cur, *hops, *live0, *live1, *bucket;
+        uint32_t *jm, *filt;
+        uint64_t *bestkey;
+    } B;
+    auto carve = [&](Carver &c) {
+        B.gcount = c.take<int32_t>(S + 1);
+        B.bcount = c.take<int32_t>(S + 1);
+        B.gofs = c.take<int32_t>(S + 1);
+        B.bofs = c.take<int32_t>(S + 1);
+        B.counts0 = c.take<int32_t>(S + 1);
+        B.counts1 = c.take<int32_t>(S + 1);
+        B.boff = c.take<int32_t>(S + 1);
+        B.cursor = c.take<int32_t>(S + 1);
+        B.cur = c.take<int32_t>(T + 1);
+        B.hops = c.take<int32_t>(T + 1);
+        B.live0 = c.take<int32_t>(T + 1);
+        B.live1 = c.take<int32_t>(T + 1);
+        B.bucket = c.take<int32_t>(T + 1);
+        B.jm = c.take<uint32_t>(T + 1);
+        B.bestkey = c.take<uint64_t>(T + 1);
+    };
+    Carver dry{nullptr, 0};
+    carve(dry);
+    int rc = pc_ensure_arena(ctx, dry.off);
+    if (rc) return rc;
+    Carver real{ctx->arena, 0};
+    carve(real);
+
+    // ---- prep: per-switch sizes, offsets, chunk sets, data-error sweep
+    if (S > 0) {
+        PC_TIMED(ctx, "k_tr_switch_info", stream, hipLaunchKernelGGL(k_tr_switch_info, dim3(grid_for(S, 256)), dim3(256), 0, stream, S, port_off, n_ports, jur,
+                           rule_off, n_rules, B.gcount, B.bcount, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+        launch_scan_i32(B.gcount, S, B.gofs, nullptr, nullptr, stream);
+        launch_scan_i32(B.bcount, S, B.bofs, nullptr, nullptr, stream);
+        PC_LAUNCH_CHECK(ctx);
+        // exact sizes of the chunk-set buffer and of the prep grid (switch
+        // ranges may overlap, so no host-side bound from n_rules holds)
+        PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, B.gofs + S, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+        PC_HIP(ctx, hipMemcpyAsync(ctx->h_small + 1, B.bofs + S, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+        PC_HIP(ctx, hipStreamSynchronize(stream));
+        const int64_t total_groups = ctx->h_small[0];
+        const int64_t prep_blocks = ctx->h_small[1];
+        if (total_groups < 0 || prep_blocks < 0)
+            return pc_set_error(ctx, PC_EINVAL, "pc_trace_flows: more than 2^31 rule groups");
+        rc = pc_ensure_aux(ctx, static_cast<size_t>(total_groups + 1) * kPlaneWords * sizeof(uint32_t));
+        if (rc) return rc;
+        B.filt = reinterpret_cast<uint32_t *>(ctx->aux);
+        if (n_ports > 0) {
+            PC_TIMED(ctx, "k_tr_port_check", stream, hipLaunchKernelGGL(k_tr_port_check, dim3(grid_for(n_ports, 256)), dim3(256), 0, stream, n_ports,
+                               port_peer, S, ctx->d_err));
+            PC_LAUNCH_CHECK(ctx);
+        }
+        if (prep_blocks > 0) {
+            PC_TIMED(ctx, "k_tr_prep", stream, hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(prep_blocks)), dim3(1024), 0, stream, S,
+                               port_off, n_ports, rule_off, rules, B.gcount, B.gofs, B.bofs, B.filt, ctx->d_err));
+            PC_LAUNCH_CHECK(ctx);
+        }
+    }
+    if (T == 0) return PC_OK;
+
+    // ---- level-synchronous walk
+    int32_t *d_n = ctx->d_small;  // [0], [1]: live counts of the two live lists
+    launch_fill_u32(reinterpret_cast<uint32_t *>(d_n), 2, 0, stream);
+    if (S > 0) {
+        launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts0), S + 1, 0, stream);
+        launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), S + 1, 0, stream);
+    }
+    PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(grid_for(T, 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
+                       B.hops, B.live0, d_n, B.counts0, out, ctx->d_err));
+    PC_LAUNCH_CHECK(ctx);
+    PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+    PC_HIP(ctx, hipStreamSynchronize(stream));
+    int32_t nlive = ctx->h_small[0];
+    int32_t *live_cur = B.live0, *live_nxt = B.live1;
+    int32_t *cnt_cur = B.counts0, *cnt_nxt = B.counts1;
+    int32_t *n_cur = d_n, *n_nxt = d_n + 1;
+    for (int level = 0; nlive > 0; ++level) {
+        if (level > ttl + 1)
+            return pc_set_error(ctx, PC_EDEVICE, "pc_trace_flows: level loop exceeded ttl+1 levels");
+        launch_scan_i32(cnt_cur, S, B.boff, B.cursor, cnt_cur, stream);
+        PC_TIMED(ctx, "k_tr_scatter", stream, hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, B.cur,
+                           B.cursor, B.bucket));
+        PC_TIMED(ctx, "k_tr_match", stream, hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(S)), dim3(kMatchThreads), 0, stream, rule_off, rules,
+                           B.gcount, B.gofs, B.filt, hdr, B.boff, B.bucket, B.bestkey));
+        launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
+        PC_TIMED(ctx, "k_tr_advance", stream, hipLaunchKernelGGL(k_tr_advance, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, S, port_off, port_peer,
+                           n_ports, jur, rule_off, rules, ttl, live_cur, n_cur, B.bestkey, B.cur, B.jm, B.hops,
+                           live_nxt, n_nxt, cnt_nxt, out));
+        PC_LAUNCH_CHECK(ctx);
+        PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, n_nxt, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+        PC_HIP(ctx, hipStreamSynchronize(stream));
+        nlive = ctx->h_small[0];
+        int32_t *tmp;
+        tmp = live_cur; live_cur = live_nxt; live_nxt = tmp;
+        tmp = cnt_cur; cnt_cur = cnt_nxt; cnt_nxt = tmp;
+        tmp = n_cur; n_cur = n_nxt; n_nxt = tmp;
+    }
+    return PC_OK;
+}

@@ -66,31 +66,41 @@ class Workload:
 
 
 # ------------------------------------------------------------ primitives
-def care_bits(rng, shape, p_care, digits=10):
-    """uint32 words whose bits are independently 1 with probability p_care,
-    rounded to `digits` binary digits.  Built by folding fresh random words
-    with OR (digit 1) or AND (digit 0) from the least significant digit up."""
-    q = int(round(p_care * (1 << digits)))
-    out = np.zeros(shape, np.uint32)
-    if q <= 0:
-        return out
-    if q >= (1 << digits):
-        out[...] = 0xFFFFFFFF
-        return out
-    bits = [(q >> (digits - 1 - i)) & 1 for i in range(digits)]   # MSB first
-    while bits and bits[-1] == 0:
-        bits.pop()
-    first = True
-    for b in reversed(bits):
-        r = rng.integers(0, 1 << 32, size=shape, dtype=np.uint32)
-        if first:
-            out = r
-            first = False
-        elif b:
-            out |= r
-        else:
-            out &= r
-    return out
+def care_bits(rng, shape, p_care):
+    """uint32 words whose bits are 1 with probability ~p_care, independently
+    across bytes: each byte is drawn from the exact 8-bit product
+    distribution quantised to 1/65536 (one 16-bit uniform draw per byte,
+    inverse-CDF lookup).  The per-bit marginal is within 1e-4 of p_care."""
+    if p_care <= 0:
+        return np.zeros(shape, np.uint32)
+    if p_care >= 1:
+        return np.full(shape, 0xFFFFFFFF, np.uint32)
+    lut = _byte_lut(float(p_care))
+    n = int(np.prod(shape)) * 4
+    u = rng.integers(0, 1 << 16, size=n, dtype=np.uint16)
+    return lut[u].view(np.uint32).reshape(shape)
+
+
+_LUTS: dict = {}
+
+
+def _byte_lut(p):
+    """65536-entry table: uniform 16-bit value -> byte with P(bit) = p."""
+    if p not in _LUTS:
+        b = np.arange(256)
+        k = np.array([bin(x).count("1") for x in b])
+        prob = p ** k * (1 - p) ** (8 - k)
+        cdf = np.cumsum(prob)
+        cdf /= cdf[-1]
+        edges = np.round(cdf * 65536).astype(np.int64)
+        lut = np.zeros(65536, np.uint8)
+        lo = 0
+        for x in range(256):
+            hi = int(edges[x])
+            lut[lo:hi] = x
+            lo = hi
+        _LUTS[p] = lut
+    return _LUTS[p]
 
 
 def distinct_values(rng, card, m, mmax=4):
@@ -432,41 +442,42 @@ def build_tables(rng, topo, R, p_care, drop_p=0.05, misroute_p=0.02,
     given, one rule per hop of every flow replaces a random free slot of
     that switch: value = flow key, action = the path's next port, except
     DROP with probability drop_p and a uniform port with probability
-    misroute_p.  Priorities: 'distinct' (a random sample of R distinct
-    uint16 per switch), 'uniform' (i.i.d. uint16, ties possible) or
+    misroute_p.  Priorities: 'distinct' (R distinct uint16 per switch in
+    random order: a random permutation of R strata of width 65536/R, a
+    uniform offset inside each), 'uniform' (i.i.d. uint16, ties possible) or
     'small' (uniform over [0, prio_range), many ties)."""
     S = topo["S"]
     port_off = topo["port_off"]
     nports = np.diff(port_off).astype(np.int64)
     n = S * R
+    assert n < 2**31
     rules = np.zeros(n, RULE_DT)
-    rule_off = (np.arange(S + 1, dtype=np.int64) * R).astype(np.int32) if n < 2**31 else None
-    assert rule_off is not None
-    # i.i.d. rules, switch-chunk by switch-chunk
+    raw = rules.view(np.uint32).reshape(n, 10)   # value[4], mask[4], prio | action << 16, rsv
+    rule_off = (np.arange(S + 1, dtype=np.int64) * R).astype(np.int32)
     for s0 in range(0, S, chunk):
         s1 = min(S, s0 + chunk)
         m = (s1 - s0) * R
-        sl = slice(s0 * R, s1 * R)
         val = random_keys(rng, m)
         msk = care_bits(rng, (m, 4), p_care)
         msk[:, 3] &= np.uint32(0xFF)
-        rules["value"][sl] = val & msk
-        rules["mask"][sl] = msk
+        blk = np.empty((m, 10), np.uint32)
+        blk[:, 0:4] = val & msk
+        blk[:, 4:8] = msk
         np_ = np.repeat(nports[s0:s1], R)
         act = rng.integers(0, np.maximum(np_, 1))
-        act = np.where(rng.random(m) < drop_p, DROP, act)
-        rules["action"][sl] = act
-    # priorities
-    if prio == "distinct":
-        assert R <= 65536
-        pr = np.empty(n, np.uint16)
-        for s in range(S):
-            pr[s * R:(s + 1) * R] = rng.permutation(65536)[:R]
-        rules["priority"] = pr
-    elif prio == "uniform":
-        rules["priority"] = rng.integers(0, 65536, size=n)
-    else:
-        rules["priority"] = rng.integers(0, prio_range, size=n)
+        act = np.where(rng.random(m) < drop_p, DROP, act).astype(np.uint32)
+        if prio == "distinct":
+            assert R <= 65536
+            width = 65536 // R
+            strata = np.argsort(rng.random((s1 - s0, R)), axis=1).reshape(-1).astype(np.int64)
+            pr = strata * width + rng.integers(0, width, size=m)
+        elif prio == "uniform":
+            pr = rng.integers(0, 65536, size=m)
+        else:
+            pr = rng.integers(0, prio_range, size=m)
+        blk[:, 8] = pr.astype(np.uint32) | (act << np.uint32(16))
+        blk[:, 9] = 0
+        raw[s0 * R:s1 * R] = blk
     dropped = 0
     if flows is not None:
         keys, sw, port, nh = flows
@@ -499,12 +510,12 @@ def build_tables(rng, topo, R, p_care, drop_p=0.05, misroute_p=0.02,
         m = pos.shape[0]
         msk = care_bits(rng, (m, 4), p_care)
         msk[:, 3] &= np.uint32(0xFF)
-        rules["mask"][pos] = msk
-        rules["value"][pos] = keys[e_flow] & msk
+        raw[pos, 0:4] = keys[e_flow] & msk
+        raw[pos, 4:8] = msk
         u = rng.random(m)
         mis = rng.integers(0, np.maximum(nports[e_sw], 1))
-        act = np.where(u < drop_p, DROP, np.where(u < drop_p + misroute_p, mis, e_port))
-        rules["action"][pos] = act
+        act = np.where(u < drop_p, DROP, np.where(u < drop_p + misroute_p, mis, e_port)).astype(np.uint32)
+        raw[pos, 8] = (raw[pos, 8] & np.uint32(0xFFFF)) | (act << np.uint32(16))
     return rule_off, rules, dropped
 
 

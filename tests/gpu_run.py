@@ -1,0 +1,79 @@
+"""Run the HIP path (through the C ABI) on a synth.Workload and bring the
+results back as numpy arrays shaped like the oracle's."""
+from __future__ import annotations
+
+import numpy as np
+import torch
+
+import paper_2602_16100_amd as pc
+
+
+def dev(a):
+    return pc.to_device(a, "cuda")
+
+
+def selectors(labels, pred_off, preds, n_preds=None):
+    f, p = pc.pc_eval_selectors(dev(labels), dev(pred_off), dev(preds), n_preds=n_preds)
+    torch.cuda.synchronize()
+    return f.cpu().numpy().view(np.uint64), p.cpu().numpy().view(np.uint32)
+
+
+def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, n_ports=None, n_rules=None):
+    out = pc.pc_trace_flows(S, dev(port_off), dev(port_peer), dev(jur), dev(rule_off), dev(rules),
+                            dev(np.ascontiguousarray(hdr, np.uint32)), dev(ingress), ttl,
+                            n_ports=n_ports, n_rules=n_rules)
+    torch.cuda.synchronize()
+    return pc.records(out, pc.TRACE_OUT_DT)
+
+
+def reach(V, adj_off, adj, region, src, allowed, target=None, n_adj=None):
+    d = pc.pc_masked_reach(V, dev(adj_off), dev(adj), dev(region), dev(src), dev(allowed),
+                           None if target is None else dev(target), n_adj=n_adj)
+    torch.cuda.synchronize()
+    return d.cpu().numpy()
+
+
+def report(intents, feasible, popcnt, N, traces, expect, reach_d):
+    f = torch.from_numpy(np.ascontiguousarray(feasible).view(np.int64)).cuda()
+    p = torch.from_numpy(np.ascontiguousarray(popcnt).view(np.int32)).cuda()
+    t = torch.from_numpy(np.ascontiguousarray(traces).view(np.uint8).reshape(-1, 12)).cuda()
+    r = torch.from_numpy(np.ascontiguousarray(reach_d, np.int32)).cuda()
+    pss, reason, summ = pc.pc_report(dev(intents), f, p, N, t, dev(expect), r)
+    torch.cuda.synchronize()
+    return (pss.cpu().numpy().view(np.uint64), reason.cpu().numpy(),
+            pc.records(summ, pc.SUMMARY_DT)[0])
+
+
+def run_workload(wl):
+    """All stages on the GPU, device-resident between stages (as a caller
+    would chain them); outputs copied back at the end."""
+    out = {}
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    if "labels" in wl.arrays:
+        f, p = pc.pc_eval_selectors(dev(wl["labels"]), dev(wl["pred_off"]), dev(wl["preds"]))
+        out["_f"], out["_p"] = f, p
+    if "rules" in wl.arrays:
+        out["_t"] = pc.pc_trace_flows(wl["S"], dev(wl["port_off"]), dev(wl["port_peer"]), dev(wl["jur"]),
+                                      dev(wl["rule_off"]), dev(wl["rules"]), dev(wl["hdr"]), dev(wl["ingress"]),
+                                      wl["ttl"])
+    if "src" in wl.arrays:
+        tgt = wl.arrays.get("target")
+        out["_r"] = pc.pc_masked_reach(wl["V"], dev(wl["adj_off"]), dev(wl["adj"]), dev(wl["region"]),
+                                       dev(wl["src"]), dev(wl["allowed"]), None if tgt is None else dev(tgt))
+    if "intents" in wl.arrays:
+        pss, reason, summ = pc.pc_report(dev(wl["intents"]), out["_f"], out["_p"], wl["N"], out["_t"],
+                                         dev(wl["expect"]), out["_r"])
+        out["pass"] = pss.cpu().numpy().view(np.uint64)
+        out["reason"] = reason.cpu().numpy()
+        out["summary"] = pc.records(summ, pc.SUMMARY_DT)[0]
+    torch.cuda.synchronize()
+    if "_f" in out:
+        out["feasible"] = out.pop("_f").cpu().numpy().view(np.uint64)
+        out["popcnt"] = out.pop("_p").cpu().numpy().view(np.uint32)
+    if "_t" in out:
+        out["traces"] = pc.records(out.pop("_t"), pc.TRACE_OUT_DT)
+    if "_r" in out:
+        out["reach"] = out.pop("_r").cpu().numpy()
+    out["flags"] = ctx.data_errors(clear=True)
+    return out

@@ -1,0 +1,250 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle, element
+by element, on seeded inputs small enough for the oracle to finish in
+seconds while spanning several tiles and ragged tails.  Everything here is
+integer / bitset work: the bar is bit-exact equality, including the
+data-error flags."""
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def g():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import gpu_run
+    return gpu_run
+
+
+def _same_traces(a, b):
+    assert a.shape == b.shape
+    for f in ("jmask", "last_switch", "last_port", "hops", "state"):
+        bad = np.flatnonzero(a[f] != b[f])
+        assert bad.size == 0, f"field {f}: first mismatch at trace {bad[0]}: gpu {a[bad[0]]} oracle {b[bad[0]]}"
+
+
+def _same(a, b, what):
+    a, b = np.asarray(a), np.asarray(b)
+    assert a.shape == b.shape, (what, a.shape, b.shape)
+    bad = np.argwhere(a != b)
+    assert bad.size == 0, f"{what}: first mismatch at {tuple(bad[0])}: gpu {a[tuple(bad[0])]} oracle {b[tuple(bad[0])]}"
+
+
+def _check_workload(g, orc, wl):
+    gp = g.run_workload(wl)
+    oo = orc.run_workload(wl)
+    flags = 0
+    if "feasible" in oo:
+        _same(gp["feasible"], oo["feasible"], "feasible")
+        _same(gp["popcnt"], oo["popcnt"], "popcnt")
+        flags |= oo["sel_err"]
+    if "traces" in oo:
+        _same_traces(gp["traces"], oo["traces"])
+        flags |= oo["trace_err"]
+    if "reach" in oo:
+        _same(gp["reach"], oo["reach"], "reach")
+        flags |= oo["reach_err"]
+    if "reason" in oo:
+        _same(gp["reason"], oo["reason"], "reason")
+        _same(gp["pass"], oo["pass"], "pass")
+        for f in ("counts", "no_path"):
+            _same(gp["summary"][f], oo["summary"][f], f)
+        flags |= oo["report_err"]
+    assert gp["flags"] == flags
+    return gp, oo
+
+
+@pytest.mark.parametrize("variant", ["rpath", "literal", "dense"])
+def test_cfg1_end_to_end(g, orc, variant):
+    _check_workload(g, orc, synth.cfg1(0, variant))
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_combined_small(g, orc, seed):
+    wl = synth.combined_workload(seed, 3000 + 37, 16, 8, 4, 700, 3001)
+    gp, oo = _check_workload(g, orc, wl)
+    r = oo["reason"] & 0x7F
+    assert (r == 0).sum() > 0 and (r == 1).sum() > 0 and (r == 4).sum() > 0
+
+
+def test_selectors_absent_labels_and_ragged(g, orc):
+    wl = synth.selector_workload(5, 5000 + 37, 12, 700, card_choices=(2, 3, 16, 64, 200), absent_p=0.05)
+    _check_workload(g, orc, wl)
+
+
+def test_selectors_large_value_sets(g, orc):
+    """In/NotIn sets with up to 200 values (beyond the generators' 1..4)."""
+    rng = np.random.default_rng(7)
+    N, L = 3000, 5
+    cards = np.array([250, 255, 7, 130, 2])
+    labels = synth.gen_labels(rng, N, cards, absent_p=0.1)
+    I = 300
+    k = rng.integers(1, 4, size=I)
+    off = np.zeros(I + 1, np.int32)
+    off[1:] = np.cumsum(k)
+    preds = np.zeros(int(off[-1]), synth.PRED_DT)
+    for p in range(preds.shape[0]):
+        l = int(rng.integers(0, L))
+        preds[p]["label"] = l
+        preds[p]["op"] = int(rng.integers(0, 3))
+        m = int(rng.integers(0, min(200, cards[l]) + 1))
+        vals = rng.choice(255, size=m, replace=False)
+        bm = [0, 0, 0, 0]
+        for v in vals:
+            bm[v >> 6] |= 1 << int(v & 63)
+        preds[p]["vals"] = np.array(bm, np.uint64)
+    fg, pg = g.selectors(labels, off, preds)
+    fo, po, _ = orc.selectors(labels, off, preds)
+    _same(fg, fo, "feasible")
+    _same(pg, po, "popcnt")
+
+
+def test_selectors_malformed_flags(g, orc):
+    import paper_2602_16100_amd as pc
+    wl = synth.selector_workload(9, 777, 6, 40)
+    preds = wl["preds"].copy()
+    off = wl["pred_off"].copy()
+    preds[3]["label"] = 99          # label >= L
+    preds[10]["op"] = 7             # bad op
+    preds[20]["rsv1"] = 1
+    off[30] = off[31] + 5           # decreasing pair for row 29 / row 30
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    fg, pg = g.selectors(wl["labels"], off, preds)
+    flags = ctx.data_errors(clear=True)
+    fo, po, err = orc.selectors(wl["labels"], off, preds)
+    _same(fg, fo, "feasible")
+    _same(pg, po, "popcnt")
+    assert flags == err and err & orc.F_PRED and err & orc.F_OFFSETS
+
+
+@pytest.mark.parametrize("variant", ["rpath", "literal", "dense"])
+def test_trace_fat_tree_small(g, orc, variant):
+    wl = synth.trace_workload(3, 8, 4, 512, 20000, 24, 3000, variant=variant)
+    _check_workload(g, orc, wl)
+
+
+def test_trace_multi_slice_and_big_buckets(g, orc):
+    """20,000 rules per switch (two 16,384-rule slices) and buckets larger
+    than one 2,048-lookup tile."""
+    wl = synth.trace_workload(4, 4, 2, 20000, 12000, 16, 2000)
+    _check_workload(g, orc, wl)
+
+
+def test_trace_ties_and_ttl(g, orc):
+    rng = np.random.default_rng(3)
+    topo = synth.random_graph(rng, 9, 14, 2, 4)
+    rule_off, rules, _ = synth.build_tables(rng, topo, 40, 0.03, prio="small", prio_range=3)
+    T = 3000
+    hdr = synth.random_keys(rng, T)
+    ingress = rng.integers(0, 9, size=T).astype(np.int32)
+    for ttl in (0, 1, 7, 255):
+        tg = g.trace(9, topo["port_off"], topo["port_peer"], topo["jur"], rule_off, rules, hdr, ingress, ttl)
+        to, _ = orc.trace(9, topo["port_off"], topo["port_peer"], topo["jur"], rule_off, rules, hdr, ingress, ttl)
+        _same_traces(tg, to)
+
+
+def test_trace_malformed_flags(g, orc):
+    import paper_2602_16100_amd as pc
+    wl = synth.trace_workload(6, 4, 2, 64, 500, 8, 100)
+    jur = wl["jur"].copy()
+    jur[3] = 40
+    peer = wl["port_peer"].copy()
+    peer[5] = 9999
+    rules = wl["rules"].copy()
+    rules["action"][17] = 77
+    ingress = wl["ingress"].copy()
+    ingress[4] = -3
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    tg = g.trace(wl["S"], wl["port_off"], peer, jur, wl["rule_off"], rules, wl["hdr"], ingress, wl["ttl"])
+    flags = ctx.data_errors(clear=True)
+    to, err = orc.trace(wl["S"], wl["port_off"], peer, jur, wl["rule_off"], rules, wl["hdr"], ingress, wl["ttl"])
+    _same_traces(tg, to)
+    assert flags == err == (orc.F_JUR | orc.F_SWITCH | orc.F_ACTION)
+
+
+@pytest.mark.parametrize("full_rows", [True, False])
+def test_reach_small_graph_bitset(g, orc, full_rows):
+    wl = synth.rgg_workload(4, 3000, 8, 200, mean_degree=6.0, full_rows=full_rows)
+    _check_workload(g, orc, wl)
+
+
+@pytest.mark.parametrize("full_rows", [True, False])
+def test_reach_large_graph_queue(g, orc, full_rows):
+    wl = synth.rgg_workload(5, 40000, 16, 40, mean_degree=5.0, full_rows=full_rows)
+    _check_workload(g, orc, wl)
+
+
+def test_reach_fat_tree_targets(g, orc):
+    topo = synth.fat_tree(16, 6)
+    rng = np.random.default_rng(1)
+    Q = 1000
+    src = rng.integers(0, topo["S"], size=Q).astype(np.int32)
+    tgt = rng.integers(0, topo["S"], size=Q).astype(np.int32)
+    allowed = rng.integers(0, 64, size=Q).astype(np.uint32)
+    dg = g.reach(topo["S"], topo["adj_off"], topo["adj"], topo["jur"], src, allowed, tgt)
+    do, _ = orc.reach(topo["S"], topo["adj_off"], topo["adj"], topo["jur"], src, allowed, tgt)
+    _same(dg, do, "dist")
+    assert (do >= 0).sum() > 100 and (do == -1).sum() > 100
+
+
+def test_reach_malformed_flags(g, orc):
+    import paper_2602_16100_amd as pc
+    wl = synth.rgg_workload(2, 800, 4, 70, mean_degree=6.0, full_rows=False)
+    adj = wl["adj"].copy()
+    adj[11] = -5
+    region = wl["region"].copy()
+    region[2] = 33
+    src = wl["src"].copy()
+    src[1] = 10**6
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    dg = g.reach(wl["V"], wl["adj_off"], adj, region, src, wl["allowed"], wl["target"])
+    flags = ctx.data_errors(clear=True)
+    do, err = orc.reach(wl["V"], wl["adj_off"], adj, region, src, wl["allowed"], wl["target"])
+    _same(dg, do, "dist")
+    assert flags == err == (orc.F_GRAPH | orc.F_JUR | orc.F_SWITCH)
+
+
+def test_report_malformed_intents(g, orc):
+    wl = synth.cfg1(0)
+    oo = orc.run_workload(wl)
+    it = wl["intents"].copy()
+    it[2]["kind"] = 9
+    it[4]["trace_end"] = 99999
+    it[5]["sel_row"] = -2
+    pg, rg, sg = g.report(it, oo["feasible"], oo["popcnt"], wl["N"], oo["traces"], wl["expect"], oo["reach"])
+    po, ro, so, err = orc.report(it, oo["feasible"], oo["popcnt"], wl["N"], oo["traces"], wl["expect"], oo["reach"])
+    _same(rg, ro, "reason")
+    _same(pg, po, "pass")
+    _same(sg["counts"], so["counts"], "counts")
+
+
+def test_empty_inputs(g, orc):
+    """N = 0, I = 0, T = 0, Q = 0 and V = 0 all return cleanly."""
+    labels = np.zeros((0, 4), np.uint8)
+    off = np.zeros(4, np.int32)
+    preds = np.zeros(0, synth.PRED_DT)
+    fg, pg = g.selectors(labels, off, preds)
+    assert fg.shape == (3, 0) and list(pg) == [0, 0, 0]
+    topo = synth.fat_tree(4, 2)
+    tg = g.trace(topo["S"], topo["port_off"], topo["port_peer"], topo["jur"], np.zeros(topo["S"] + 1, np.int32),
+                 np.zeros(0, synth.RULE_DT), np.zeros((0, 4), np.uint32), np.zeros(0, np.int32), 5)
+    assert tg.shape == (0,)
+    dg = g.reach(0, np.zeros(1, np.int32), np.zeros(0, np.int32), np.zeros(0, np.uint8), np.array([0], np.int32),
+                 np.array([1], np.uint32), np.array([0], np.int32))
+    assert list(dg) == [-1]
+
+
+def test_determinism(g, orc):
+    wl = synth.combined_workload(3, 2000, 8, 8, 4, 300, 999)
+    a = g.run_workload(wl)
+    b = g.run_workload(wl)
+    for k in ("feasible", "popcnt", "reach", "reason", "pass"):
+        _same(a[k], b[k], k)
+    _same_traces(a["traces"], b["traces"])
