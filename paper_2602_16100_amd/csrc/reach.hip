@@ -10,7 +10,7 @@
 // subgraph, -1 when unreachable or when the source is not allowed.
 //
 // Design (gfx950):
-//   bitset : graphs that fit in LDS (3 x 8 bytes per vertex): 64 queries per
+//   bitset : graphs that fit in LDS (25 bytes per vertex): 64 queries per
 //            workgroup, one bit each, level-synchronous frontier bitsets
 //            (visited / frontier / next) in LDS, push expansion with 64-bit
 //            LDS atomic OR, the per-query allowed mask applied per vertex as
@@ -23,9 +23,10 @@
 
 namespace {
 
-constexpr int kBitsetThreads = 256;
+constexpr int kBitsetThreads = 512;
 constexpr int kQueueThreads = 256;
-constexpr int kMaxBitsetV = 6400;  // 3 x 8 B x V + masks within 160 KB of LDS
+constexpr int kMaxBitsetV = 6144;  // 3 x 8 B + 1 B per vertex, plus masks, within 160 KB of LDS
+constexpr int kAdjBatch = 8;       // adjacency loads in flight per thread
 
 __device__ __forceinline__ bool allowed_v(const uint8_t *region, uint32_t A, int32_t v)
 {
@@ -70,6 +71,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     uint64_t *fr = vis + V;
     uint64_t *nx = fr + V;
     uint64_t *rmask = nx + V;  // [32]
+    uint8_t *reg = reinterpret_cast<uint8_t *>(rmask + 32);  // [V]
     __shared__ int flag_any, flag_done;
     const int tid = threadIdx.x, lane = tid & 63;
     const int32_t q0 = blockIdx.x * 64;
@@ -78,6 +80,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         vis[v] = 0;
         fr[v] = 0;
         nx[v] = 0;
+        reg[v] = region[v];
     }
     if (tid < 64) {
         const uint32_t A = lane < nq ? allowed[q0 + lane] : 0u;
@@ -93,7 +96,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     if (tid < 64 && lane < nq) {
         const int32_t q = q0 + lane;
         const int32_t s = src[q];
-        const bool s_ok = s >= 0 && s < V && allowed_v(region, allowed[q], s);
+        const bool s_ok = s >= 0 && s < V && allowed_v(reg, allowed[q], s);
         if (target) {
             tgt = target[q];
             done = !(s_ok && tgt >= 0 && tgt < V);
@@ -111,15 +114,19 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     }
     for (int32_t d = 1;; ++d) {
         if (tid == 0) flag_any = 0;
-        // push the frontier along every edge
+        // push the frontier along every edge, kAdjBatch neighbour loads at a time
         for (int32_t u = tid; u < V; u += kBitsetThreads) {
             const uint64_t f = fr[u];
             if (!f) continue;
             const int64_t b = adj_off[u], e = adj_off[u + 1];
             if (!pc_range_ok(b, e, n_adj)) continue;
-            for (int64_t p = b; p < e; ++p) {
-                const int32_t v = adj[p];
-                if (v >= 0 && v < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[v]), f);
+            for (int64_t p0 = b; p0 < e; p0 += kAdjBatch) {
+                int32_t nb[kAdjBatch];
+#pragma unroll
+                for (int k = 0; k < kAdjBatch; ++k) nb[k] = p0 + k < e ? adj[p0 + k] : -1;
+#pragma unroll
+                for (int k = 0; k < kAdjBatch; ++k)
+                    if (nb[k] >= 0 && nb[k] < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[nb[k]]), f);
             }
         }
         __syncthreads();
@@ -128,7 +135,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
             uint64_t n = nx[v];
             nx[v] = 0;
             if (n) {
-                const uint32_t r = region[v];
+                const uint32_t r = reg[v];
                 n &= (r < 32 ? rmask[r] : 0ull) & ~vis[v];
                 vis[v] |= n;
                 if (!target) {
@@ -242,7 +249,7 @@ int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
     }
     int max_lds = 0;
     PC_HIP(ctx, hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, ctx->device));
-    const size_t lds = static_cast<size_t>(V) * 3 * 8 + 32 * 8;
+    const size_t lds = static_cast<size_t>(V) * (3 * 8 + 1) + 32 * 8;
     if (V <= kMaxBitsetV && lds + 64 <= static_cast<size_t>(max_lds)) {
         PC_HIP(ctx, hipFuncSetAttribute(reinterpret_cast<const void *>(k_rc_bitset),
                                         hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));

@@ -13,12 +13,15 @@
 //   3. planes    : planes[p][w] = 64-bit set of nodes 64w..64w+63 carrying
 //                  the plane's (label, value); built with one ballot per
 //                  present value per 64-node column.
-//   4. eval      : one row per wavefront (the row's predicates are uniform
-//                  and decoded on the scalar unit), lanes over 64 columns of
-//                  64 nodes.  In S = OR of the planes of S's present values,
-//                  NotIn S = its complement, Exists = complement of the
-//                  absent-value plane.  XCD-aware block -> (column tile, row
-//                  chunk) mapping keeps each XCD's planes in its own L2.
+//   4. compile   : one thread per row turns its predicates into a clause
+//                  program over plane ids (In S = OR of S's planes or NOT OR
+//                  of the rest, whichever is shorter; NotIn the reverse;
+//                  Exists = NOT the absent-value plane) and validates it.
+//   5. eval      : one row per wavefront (its program read with scalar
+//                  loads), lanes over 64 columns of 64 nodes, plane words
+//                  fetched kBatch at a time so the loads overlap.  XCD-aware
+//                  block -> (column tile, row chunk) mapping keeps each XCD's
+//                  planes in its own L2.
 #include "pc_internal.h"
 
 namespace {
@@ -138,11 +141,135 @@ __device__ __forceinline__ bool pred_valid(uint32_t label, uint32_t op, uint32_t
            (op == PC_OP_EXISTS || (v3 >> 63) == 0);
 }
 
+// Program entries: plane id, plus flags on the last entry of a clause.
+constexpr uint32_t kLast = 1u << 30;
+constexpr uint32_t kNeg = 1u << 31;
+constexpr uint32_t kPidMask = kLast - 1;
+constexpr int32_t kRowFalse = -1;  // some clause admits no node (or a malformed predicate)
+constexpr int32_t kRowLong = -2;   // program longer than 4 entries per predicate: decoded on the fly
+constexpr int kBatch = 8;          // plane loads in flight per wavefront
+
+__device__ __forceinline__ uint32_t plane_id(const uint64_t *pres, const uint32_t *wb, uint32_t v)
+{
+    const uint32_t k = v >> 6;
+    return wb[k] + __popcll(pres[k] & ((1ull << (v & 63)) - 1));
+}
+
+// One thread per row: validate the row and compile it into a clause
+// program over plane ids.  A clause is an OR of planes, optionally
+// negated; each label value of a node lies in exactly one present plane,
+// so In S = OR(S) = NOT OR(present \ S) and NotIn S = NOT OR(S) =
+// OR(present \ S): the shorter form is kept.  Entries live at
+// prog[4 * pred_off[i] ...], at most 4 per predicate.
+__global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__ pred_off,
+                                                     const pc_pred *__restrict__ preds, int64_t n_preds, int32_t I,
+                                                     int32_t L, const uint64_t *__restrict__ present,
+                                                     const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog,
+                                                     int32_t *__restrict__ row_len, uint32_t *__restrict__ d_err)
+{
+    uint32_t errs = 0;
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
+        const int64_t b = pred_off[i], e = pred_off[i + 1];
+        if (!pc_range_ok(b, e, n_preds)) {
+            errs |= PC_DERR_OFFSETS;
+            row_len[i] = kRowFalse;
+            continue;
+        }
+        int32_t state = 0;  // 0 ok, kRowFalse, kRowLong
+        int64_t n = 0;
+        const int64_t cap = 4 * (e - b);
+        uint32_t *out = prog + 4 * b;
+        for (int64_t p = b; p < e; ++p) {
+            const pc_pred q = preds[p];
+            if (!pred_valid(q.label, q.op, q.rsv0, q.rsv1, q.vals[3], L)) {
+                errs |= PC_DERR_PRED;
+                state = kRowFalse;
+                continue;
+            }
+            if (state == kRowFalse) continue;
+            const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+            const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+            uint64_t sel[4];
+            bool neg;
+            if (q.op == PC_OP_EXISTS) {
+                // Exists = NOT OR(plane of the absent value), when any node lacks the label
+                sel[0] = sel[1] = sel[2] = 0;
+                sel[3] = pres[3] & (1ull << 63);
+                neg = true;
+            } else {
+                uint64_t in[4], out_[4];
+                uint32_t ms = 0, mc = 0;
+                for (int k = 0; k < 4; ++k) {
+                    in[k] = q.vals[k] & pres[k];
+                    out_[k] = pres[k] & ~q.vals[k];
+                    ms += __popcll(in[k]);
+                    mc += __popcll(out_[k]);
+                }
+                const bool use_in = ms <= mc;
+                for (int k = 0; k < 4; ++k) sel[k] = use_in ? in[k] : out_[k];
+                neg = (q.op == PC_OP_IN) ? !use_in : use_in;
+            }
+            uint32_t cnt = __popcll(sel[0]) + __popcll(sel[1]) + __popcll(sel[2]) + __popcll(sel[3]);
+            if (cnt == 0) {
+                if (!neg) state = kRowFalse;  // empty OR: no node
+                continue;                     // negated empty OR: every node
+            }
+            if (state == kRowLong || n + cnt > cap) {
+                state = kRowLong;
+                continue;
+            }
+            for (int k = 0; k < 4; ++k) {
+                uint64_t m = sel[k];
+                while (m) {
+                    const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                    m &= m - 1;
+                    uint32_t ent = plane_id(pres, wb, v);
+                    if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
+                    out[n++] = ent;
+                }
+            }
+        }
+        row_len[i] = state ? state : static_cast<int32_t>(n);
+    }
+    if (errs) atomicOr(d_err, errs);
+}
+
+// Rows whose program did not fit: decode the predicates on the scalar unit.
+__device__ uint64_t eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, int64_t e,
+                                     const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
+                                     const uint64_t *pcol, int32_t W, bool wok)
+{
+    uint64_t acc = ~0ull;
+    for (int64_t p = b; p < e; ++p) {
+        const pc_pred *q = preds + p;
+        const uint32_t label = q->label, op = q->op;
+        const uint64_t *pres = present + static_cast<int64_t>(label) * 4;
+        const uint32_t *wb = wbase + static_cast<int64_t>(label) * 4;
+        if (op == PC_OP_EXISTS) {
+            const uint64_t p3 = pres[3];
+            if (p3 >> 63) acc &= wok ? ~pcol[static_cast<int64_t>(plane_id(pres, wb, 255)) * W] : 0ull;
+            continue;
+        }
+        uint64_t cur = 0;
+        for (int k = 0; k < 4; ++k) {
+            uint64_t m = q->vals[k] & pres[k];
+            while (m) {
+                const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                m &= m - 1;
+                if (wok) cur |= pcol[static_cast<int64_t>(plane_id(pres, wb, v)) * W];
+            }
+        }
+        acc &= (op == PC_OP_IN) ? cur : ~cur;
+    }
+    return acc;
+}
+
 __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
-    const int32_t *__restrict__ pred_off, const pc_pred *__restrict__ preds, int64_t n_preds, int32_t I, int32_t L,
-    const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase, const uint64_t *__restrict__ planes,
-    int32_t W, int32_t N, uint64_t *__restrict__ feasible, uint32_t *__restrict__ popcnt, int32_t ntiles,
-    int32_t nchunks, int32_t rows_per_chunk, uint32_t *__restrict__ d_err)
+    const int32_t *__restrict__ pred_off, const pc_pred *__restrict__ preds, int32_t I,
+    const uint32_t *__restrict__ prog, const int32_t *__restrict__ row_len, const uint64_t *__restrict__ present,
+    const uint32_t *__restrict__ wbase, const uint64_t *__restrict__ planes, int32_t W, int32_t N,
+    uint64_t *__restrict__ feasible, uint32_t *__restrict__ popcnt, int32_t ntiles, int32_t nchunks,
+    int32_t rows_per_chunk)
 {
     const int64_t total = static_cast<int64_t>(ntiles) * nchunks;
     const int64_t item = pc_xcd_item(total);
@@ -156,55 +283,38 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     uint64_t tail = ~0ull;
     if (!wok) tail = 0;
     else if (w == W - 1 && (N & 63)) tail = (1ull << (N & 63)) - 1;
-    const uint64_t *pcol = planes + w;
+    const uint64_t *pcol = planes + (wok ? w : 0);
     const int32_t r0 = chunk * rows_per_chunk;
     const int32_t r1 = min(I, r0 + rows_per_chunk);
-    uint32_t errs = 0;
     for (int32_t r = r0 + wave; r < r1; r += kEvalThreads / 64) {
-        const int64_t b = pred_off[r], e = pred_off[r + 1];
+        const int32_t len = row_len[r];
         uint64_t acc = ~0ull;
-        bool live = true;  // wave-uniform: some lane still has a candidate node
-        if (!pc_range_ok(b, e, n_preds)) {
+        if (len == kRowFalse) {
             acc = 0;
-            errs |= PC_DERR_OFFSETS;
+        } else if (len == kRowLong) {
+            acc = eval_row_decoded(preds, pred_off[r], pred_off[r + 1], present, wbase, pcol, W, wok);
         } else {
-            for (int64_t p = b; p < e; ++p) {
-                const pc_pred *q = preds + p;
-                const uint32_t label = q->label, op = q->op, rsv0 = q->rsv0, rsv1 = q->rsv1;
-                const uint64_t v0 = q->vals[0], v1 = q->vals[1], v2 = q->vals[2], v3 = q->vals[3];
-                if (!pred_valid(label, op, rsv0, rsv1, v3, L)) {
-                    acc = 0;
-                    live = false;
-                    errs |= PC_DERR_PRED;
-                    continue;  // keep validating the rest of the row
-                }
-                if (!live) continue;
-                const uint64_t *pres = present + static_cast<int64_t>(label) * 4;
-                const uint32_t *wb = wbase + static_cast<int64_t>(label) * 4;
-                if (op == PC_OP_EXISTS) {
-                    const uint64_t p3 = pres[3];
-                    if (p3 >> 63) {
-                        const uint32_t pid = wb[3] + __popcll(p3 & ~(1ull << 63));
-                        acc &= wok ? ~pcol[static_cast<int64_t>(pid) * W] : 0ull;
-                    }
-                } else {
-                    uint64_t cur = 0;
-                    const uint64_t vals[4] = {v0, v1, v2, v3};
+            const uint32_t *pr = prog + 4 * static_cast<int64_t>(pred_off[r]);
+            uint64_t cur = 0;
+            for (int32_t e0 = 0; e0 < len; e0 += kBatch) {
+                uint32_t E[kBatch];
+                uint64_t V[kBatch];
 #pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        const uint64_t pm = pres[k];
-                        uint64_t m = vals[k] & pm;
-                        const uint32_t pb = wb[k];
-                        while (m) {
-                            const int bit = __builtin_ctzll(m);
-                            const uint32_t pid = pb + __popcll(pm & ((1ull << bit) - 1));
-                            if (wok) cur |= pcol[static_cast<int64_t>(pid) * W];
-                            m &= m - 1;
+                for (int k = 0; k < kBatch; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
+#pragma unroll
+                for (int k = 0; k < kBatch; ++k)
+                    V[k] = (e0 + k < len && wok) ? pcol[static_cast<int64_t>(E[k] & kPidMask) * W] : 0ull;
+#pragma unroll
+                for (int k = 0; k < kBatch; ++k) {
+                    if (e0 + k < len) {
+                        cur |= V[k];
+                        if (E[k] & kLast) {
+                            acc &= (E[k] & kNeg) ? ~cur : cur;
+                            cur = 0;
                         }
                     }
-                    acc &= (op == PC_OP_IN) ? cur : ~cur;
                 }
-                live = __ballot((acc & tail) != 0) != 0;
+                if (__ballot((acc & tail) != 0) == 0) break;
             }
         }
         acc &= tail;
@@ -212,7 +322,6 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
         const uint32_t cnt = pc_wave_sum_u32(__popcll(acc));
         if (lane == 0 && cnt) atomicAdd(&popcnt[r], cnt);
     }
-    if (errs && lane == 0) atomicOr(d_err, errs);
 }
 
 }  // namespace
@@ -228,18 +337,21 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
         return pc_set_error(ctx, PC_ENOMEM, "pc_eval_selectors: value planes need %zu bytes (L=%d N=%d)", plane_bytes,
                             L, N);
     Carver c{nullptr, 0};
-    auto carve = [&](Carver &cv, uint64_t *&present, uint32_t *&wbase, uint64_t *&planes) {
+    uint64_t *present, *planes;
+    uint32_t *wbase, *prog;
+    int32_t *row_len;
+    auto carve = [&](Carver &cv) {
         present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
         wbase = cv.take<uint32_t>(static_cast<size_t>(L) * 4 + 1);
         planes = cv.take<uint64_t>(static_cast<size_t>(pmax) * W + 1);
+        prog = cv.take<uint32_t>(static_cast<size_t>(n_preds) * 4 + 1);
+        row_len = cv.take<int32_t>(static_cast<size_t>(I) + 1);
     };
-    uint64_t *present, *planes;
-    uint32_t *wbase;
-    carve(c, present, wbase, planes);
+    carve(c);
     int rc = pc_ensure_arena(ctx, c.off);
     if (rc) return rc;
     Carver real{ctx->arena, 0};
-    carve(real, present, wbase, planes);
+    carve(real);
 
     launch_fill_u32(popcnt, static_cast<size_t>(I), 0, stream);
     launch_fill_u64(present, static_cast<size_t>(L) * 4, 0, stream);
@@ -271,9 +383,18 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     nchunks = (I + rpc - 1) / rpc;
     const int64_t total = ntiles * nchunks;
     const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
-    PC_TIMED(ctx, "k_sel_eval", stream, hipLaunchKernelGGL(k_sel_eval, dim3(blocks), dim3(kEvalThreads), 0, stream, pred_off, preds, n_preds, I, L,
-                       present, wbase, planes, static_cast<int32_t>(W), N, feasible, popcnt, ntiles,
-                       static_cast<int32_t>(nchunks), rpc, ctx->d_err));
+    {
+        int64_t cb = (I + 255) / 256;
+        if (cb > 8192) cb = 8192;
+        PC_TIMED(ctx, "k_sel_compile", stream,
+                 hipLaunchKernelGGL(k_sel_compile, dim3(static_cast<unsigned>(cb)), dim3(256), 0, stream, pred_off,
+                                    preds, n_preds, I, L, present, wbase, prog, row_len, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    PC_TIMED(ctx, "k_sel_eval", stream,
+             hipLaunchKernelGGL(k_sel_eval, dim3(blocks), dim3(kEvalThreads), 0, stream, pred_off, preds, I, prog,
+                                row_len, present, wbase, planes, static_cast<int32_t>(W), N, feasible, popcnt,
+                                ntiles, static_cast<int32_t>(nchunks), rpc));
     PC_LAUNCH_CHECK(ctx);
     return PC_OK;
 }

@@ -26,6 +26,11 @@
 //            first match is the minimum of (0xFFFF - priority, index) over
 //            the workgroup (LDS 64-bit atomic min).  An advance pass applies
 //            the action and re-buckets the traces still in flight.
+//   tail   : once few traces are left in flight, one workgroup per trace
+//            walks it to its end, reading only the chunk-set words its
+//            header selects.
+#include <stdlib.h>
+
 #include "pc_internal.h"
 
 namespace {
@@ -190,12 +195,39 @@ __global__ void k_tr_scatter(const int32_t *__restrict__ live, const int32_t *__
     }
 }
 
+__device__ __forceinline__ bool rule_matches(const pc_rule *r, uint32_t h0, uint32_t h1, uint32_t h2, uint32_t h3)
+{
+    return (((h0 ^ r->value.w[0]) & r->mask.w[0]) | ((h1 ^ r->value.w[1]) & r->mask.w[1]) |
+            ((h2 ^ r->value.w[2]) & r->mask.w[2]) | ((h3 ^ r->value.w[3]) & r->mask.w[3])) == 0;
+}
+
+__device__ __forceinline__ uint64_t rule_key(const pc_rule *r, uint32_t local)
+{
+    return (static_cast<uint64_t>(0xFFFFu - r->priority) << 32) | local;
+}
+
+// Verify the surviving rules of one 32-rule group against the full header
+// and fold their (priority, index) keys into *best.
+__device__ __forceinline__ void verify_group(uint32_t surv, const pc_rule *grp, uint32_t local0, const pc_key &h,
+                                             unsigned long long *best)
+{
+    while (surv) {
+        const int bit = __builtin_ctz(surv);
+        surv &= surv - 1;
+        const pc_rule *r = grp + bit;
+        if (rule_matches(r, h.w[0], h.w[1], h.w[2], h.w[3]))
+            atomicMin(best, static_cast<unsigned long long>(rule_key(r, local0 + bit)));
+    }
+}
+
 __global__ __launch_bounds__(kMatchThreads) void k_tr_match(
     const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
     const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt, const pc_key *__restrict__ hdr,
     const int32_t *__restrict__ boff, const int32_t *__restrict__ bucket, uint64_t *__restrict__ bestkey)
 {
     __shared__ uint64_t best[kTile];
+    __shared__ uint32_t h2s[kTile];
+    __shared__ int32_t tids[kTile];
     const int32_t s = blockIdx.x;
     const int32_t bb = boff[s], be = boff[s + 1];
     if (bb >= be) return;
@@ -209,7 +241,12 @@ __global__ __launch_bounds__(kMatchThreads) void k_tr_match(
     int32_t loaded = -1;
     for (int32_t t0 = bb; t0 < be; t0 += kTile) {
         const int32_t tn = min(kTile, be - t0);
-        for (int i = threadIdx.x; i < tn; i += kMatchThreads) best[i] = kNoMatch;
+        for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
+            const int32_t t = bucket[t0 + i];
+            tids[i] = t;
+            h2s[i] = hdr[t].w[2];
+            best[i] = kNoMatch;
+        }
         __syncthreads();
         for (int32_t sl = 0; sl < nslices; ++sl) {
             const int32_t g = sl * kSliceGroups + wave * 64 + lane;
@@ -221,38 +258,112 @@ __global__ __launch_bounds__(kMatchThreads) void k_tr_match(
                         F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * G + g] : 0u;
                 loaded = sl;
             }
-            const int64_t gbase = rb + static_cast<int64_t>(g) * 32;
+            const pc_rule *grp = rules + rb + static_cast<int64_t>(g) * 32;
             for (int32_t j = 0; j < tn; ++j) {
-                const int32_t t = __builtin_amdgcn_readfirstlane(bucket[t0 + j]);
-                const uint32_t h2 = __builtin_amdgcn_readfirstlane(hdr[t].w[2]);
+                const uint32_t h2 = __builtin_amdgcn_readfirstlane(h2s[j]);
                 uint32_t surv = F[0][h2 & 15u];
 #pragma unroll
                 for (int c = 1; c < kChunks; ++c) surv &= F[c][(h2 >> (4 * c)) & 15u];
-                if (__ballot(surv != 0)) {
-                    if (surv) {
-                        const uint32_t h0 = hdr[t].w[0], h1 = hdr[t].w[1], h3 = hdr[t].w[3];
-                        while (surv) {
-                            const int bit = __builtin_ctz(surv);
-                            surv &= surv - 1;
-                            const pc_rule *r = rules + gbase + bit;
-                            const bool m = (((h0 ^ r->value.w[0]) & r->mask.w[0]) |
-                                            ((h1 ^ r->value.w[1]) & r->mask.w[1]) |
-                                            ((h2 ^ r->value.w[2]) & r->mask.w[2]) |
-                                            ((h3 ^ r->value.w[3]) & r->mask.w[3])) == 0;
-                            if (m) {
-                                const uint64_t key = (static_cast<uint64_t>(0xFFFFu - r->priority) << 32) |
-                                                     static_cast<uint32_t>(g * 32 + bit);
-                                atomicMin(reinterpret_cast<unsigned long long *>(&best[j]),
-                                          static_cast<unsigned long long>(key));
-                            }
-                        }
-                    }
+                if (__ballot(surv != 0) && surv) {
+                    const pc_key h = hdr[tids[j]];
+                    verify_group(surv, grp, static_cast<uint32_t>(g) * 32, h,
+                                 reinterpret_cast<unsigned long long *>(&best[j]));
                 }
             }
         }
         __syncthreads();
-        for (int i = threadIdx.x; i < tn; i += kMatchThreads) bestkey[bucket[t0 + i]] = best[i];
+        for (int i = threadIdx.x; i < tn; i += kMatchThreads) bestkey[tids[i]] = best[i];
         __syncthreads();
+    }
+}
+
+// Apply the chosen rule at switch s: returns the terminal state, or -1 when
+// the trace moves on to *next.
+__device__ __forceinline__ int apply_rule(int32_t S, const int32_t *__restrict__ port_off,
+                                          const int32_t *__restrict__ port_peer, int64_t n_ports,
+                                          const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules,
+                                          int32_t ttl, int32_t s, uint64_t key, int32_t hops, int32_t *next,
+                                          uint16_t *port)
+{
+    if (key == kNoMatch) return PC_MISS;
+    const uint32_t a = rules[rule_off[s] + static_cast<uint32_t>(key)].action;
+    if (a == PC_ACTION_DROP) return PC_DROP;
+    const int64_t pb = port_off[s], pe = port_off[s + 1];
+    if (!pc_range_ok(pb, pe, n_ports) || static_cast<int64_t>(a) >= pe - pb) return PC_MISS;
+    const int32_t peer = port_peer[pb + a];
+    if (peer == -1) {
+        *port = static_cast<uint16_t>(a);
+        return PC_EGRESS;
+    }
+    if (peer < -1 || peer >= S) return PC_MISS;
+    if (hops == ttl) return PC_TTL;
+    *next = peer;
+    return -1;
+}
+
+__device__ __forceinline__ void write_out(pc_trace_out *out, int32_t t, uint32_t jm, int32_t s, uint16_t port,
+                                          int32_t hops, int state)
+{
+    pc_trace_out o;
+    o.jmask = jm;
+    o.last_switch = s;
+    o.last_port = port;
+    o.hops = static_cast<uint8_t>(hops);
+    o.state = static_cast<uint8_t>(state);
+    out[t] = o;
+}
+
+// Sparse tail: one workgroup per trace still in flight walks it to its end,
+// filtering each switch's rule groups with only the kChunks chunk-set words
+// its header selects (coalesced over groups) and reducing the first match in
+// LDS.
+__global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__restrict__ port_off,
+                                                 const int32_t *__restrict__ port_peer, int64_t n_ports,
+                                                 const uint8_t *__restrict__ jur, const int32_t *__restrict__ rule_off,
+                                                 const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
+                                                 const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
+                                                 const pc_key *__restrict__ hdr, int32_t ttl,
+                                                 const int32_t *__restrict__ live, const int32_t *__restrict__ nlive,
+                                                 const int32_t *__restrict__ cur, const uint32_t *__restrict__ jm0,
+                                                 const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out)
+{
+    __shared__ unsigned long long best;
+    const int32_t n = *nlive;
+    for (int32_t i = blockIdx.x; i < n; i += gridDim.x) {
+        const int32_t t = live[i];
+        const pc_key h = hdr[t];
+        int32_t s = cur[t];
+        uint32_t jm = jm0[t];
+        int32_t hops = hops0[t];
+        for (;;) {
+            if (threadIdx.x == 0) best = kNoMatch;
+            __syncthreads();
+            const int32_t G = gcount[s];
+            const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
+            const int64_t rb = rule_off[s];
+            for (int32_t g = threadIdx.x; g < G; g += blockDim.x) {
+                uint32_t surv = ~0u;
+#pragma unroll
+                for (int c = 0; c < kChunks; ++c)
+                    surv &= fs[static_cast<int64_t>(c * 16 + ((h.w[2] >> (4 * c)) & 15u)) * G + g];
+                if (surv) verify_group(surv, rules + rb + static_cast<int64_t>(g) * 32, static_cast<uint32_t>(g) * 32, h,
+                                       &best);
+            }
+            __syncthreads();
+            const uint64_t key = best;
+            int32_t next = -1;
+            uint16_t port = PC_NO_PORT;
+            const int state = apply_rule(S, port_off, port_peer, n_ports, rule_off, rules, ttl, s, key, hops, &next,
+                                         &port);
+            __syncthreads();  // everyone has read `best` before it is reset
+            if (state >= 0) {
+                if (threadIdx.x == 0) write_out(out, t, jm, s, port, hops, state);
+                break;
+            }
+            s = next;
+            hops += 1;
+            jm |= jur_bit(jur, s);
+        }
     }
 }
 
@@ -267,49 +378,19 @@ __global__ void k_tr_advance(int32_t S, const int32_t *__restrict__ port_off, co
     const int32_t n = *nlive;
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
         const int32_t t = live[i];
-        int32_t s = cur[t];
-        const uint64_t key = bestkey[t];
-        int state = -1;
+        const int32_t s = cur[t];
+        int32_t next = -1;
         uint16_t port = PC_NO_PORT;
-        if (key == kNoMatch) {
-            state = PC_MISS;
-        } else {
-            const pc_rule *r = rules + rule_off[s] + static_cast<uint32_t>(key);
-            const uint32_t a = r->action;
-            if (a == PC_ACTION_DROP) {
-                state = PC_DROP;
-            } else {
-                const int64_t pb = port_off[s], pe = port_off[s + 1];
-                if (!pc_range_ok(pb, pe, n_ports) || static_cast<int64_t>(a) >= pe - pb) {
-                    state = PC_MISS;
-                } else {
-                    const int32_t peer = port_peer[pb + a];
-                    if (peer == -1) {
-                        state = PC_EGRESS;
-                        port = static_cast<uint16_t>(a);
-                    } else if (peer < -1 || peer >= S) {
-                        state = PC_MISS;
-                    } else if (hops[t] == ttl) {
-                        state = PC_TTL;
-                    } else {
-                        s = peer;
-                        cur[t] = s;
-                        hops[t] += 1;
-                        jm[t] |= jur_bit(jur, s);
-                        live_next[atomicAdd(nlive_next, 1)] = t;
-                        atomicAdd(&counts_next[s], 1);
-                    }
-                }
-            }
-        }
+        const int state =
+            apply_rule(S, port_off, port_peer, n_ports, rule_off, rules, ttl, s, bestkey[t], hops[t], &next, &port);
         if (state >= 0) {
-            pc_trace_out o;
-            o.jmask = jm[t];
-            o.last_switch = s;
-            o.last_port = port;
-            o.hops = static_cast<uint8_t>(hops[t]);
-            o.state = static_cast<uint8_t>(state);
-            out[t] = o;
+            write_out(out, t, jm[t], s, port, hops[t], state);
+        } else {
+            cur[t] = next;
+            hops[t] += 1;
+            jm[t] |= jur_bit(jur, next);
+            live_next[atomicAdd(nlive_next, 1)] = t;
+            atomicAdd(&counts_next[next], 1);
         }
     }
 }
@@ -407,9 +488,22 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     int32_t *live_cur = B.live0, *live_nxt = B.live1;
     int32_t *cnt_cur = B.counts0, *cnt_nxt = B.counts1;
     int32_t *n_cur = d_n, *n_nxt = d_n + 1;
+    // Levels with few traces in flight are cheaper as independent walks than
+    // as bucketed passes (tunable with PC_TRACE_WALK_MAX, 0 = never walk).
+    int64_t walk_max = 8192;
+    if (const char *env = getenv("PC_TRACE_WALK_MAX")) walk_max = atoll(env);
     for (int level = 0; nlive > 0; ++level) {
         if (level > ttl + 1)
             return pc_set_error(ctx, PC_EDEVICE, "pc_trace_flows: level loop exceeded ttl+1 levels");
+        if (nlive <= walk_max) {
+            const unsigned wb = static_cast<unsigned>(nlive < 8192 ? nlive : 8192);
+            PC_TIMED(ctx, "k_tr_walk", stream,
+                     hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
+                                        rule_off, rules, B.gcount, B.gofs, B.filt, hdr, ttl, live_cur, n_cur, B.cur,
+                                        B.jm, B.hops, out));
+            PC_LAUNCH_CHECK(ctx);
+            break;
+        }
         launch_scan_i32(cnt_cur, S, B.boff, B.cursor, cnt_cur, stream);
         PC_TIMED(ctx, "k_tr_scatter", stream, hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, B.cur,
                            B.cursor, B.bucket));

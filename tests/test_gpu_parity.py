@@ -59,7 +59,7 @@ def _check_workload(g, orc, wl):
 
 
 @pytest.mark.parametrize("variant", ["rpath", "literal", "dense"])
-def test_cfg1_end_to_end(g, orc, variant):
+def test_cfg1_end_to_end(g, orc, variant, trace_path):
     _check_workload(g, orc, synth.cfg1(0, variant))
 
 
@@ -122,20 +122,31 @@ def test_selectors_malformed_flags(g, orc):
     assert flags == err and err & orc.F_PRED and err & orc.F_OFFSETS
 
 
+@pytest.fixture(params=["buckets", "default", "walk"])
+def trace_path(request, monkeypatch):
+    """Force the level-synchronous bucketed path, the default switch-over,
+    or the per-trace walk for every level."""
+    if request.param == "buckets":
+        monkeypatch.setenv("PC_TRACE_WALK_MAX", "0")
+    elif request.param == "walk":
+        monkeypatch.setenv("PC_TRACE_WALK_MAX", str(10**9))
+    return request.param
+
+
 @pytest.mark.parametrize("variant", ["rpath", "literal", "dense"])
-def test_trace_fat_tree_small(g, orc, variant):
+def test_trace_fat_tree_small(g, orc, variant, trace_path):
     wl = synth.trace_workload(3, 8, 4, 512, 20000, 24, 3000, variant=variant)
     _check_workload(g, orc, wl)
 
 
-def test_trace_multi_slice_and_big_buckets(g, orc):
+def test_trace_multi_slice_and_big_buckets(g, orc, trace_path):
     """20,000 rules per switch (two 16,384-rule slices) and buckets larger
     than one 2,048-lookup tile."""
     wl = synth.trace_workload(4, 4, 2, 20000, 12000, 16, 2000)
     _check_workload(g, orc, wl)
 
 
-def test_trace_ties_and_ttl(g, orc):
+def test_trace_ties_and_ttl(g, orc, trace_path):
     rng = np.random.default_rng(3)
     topo = synth.random_graph(rng, 9, 14, 2, 4)
     rule_off, rules, _ = synth.build_tables(rng, topo, 40, 0.03, prio="small", prio_range=3)
