@@ -34,6 +34,8 @@ def parse():
     ap.add_argument("--workload", default="cfg5", choices=["cfg5", "small"])
     ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach"],
+                    help="profiling aid: time one stage only (the JSON line then covers that stage)")
     return ap.parse_args()
 
 
@@ -139,14 +141,20 @@ def main():
     summary = torch.empty(288, dtype=torch.uint8, device=dev)
     ctx = pc.context(0)
 
+    only = args.only
+
     def step():
-        pc.pc_eval_selectors(D["labels"], D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
-        pc.pc_trace_flows(wl["S"], D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
-                          D["ingress"], wl["ttl"], out=traces, ctx=ctx)
-        pc.pc_masked_reach(wl["V"], D["adj_off"], D["adj"], D["region"], D["src"], D["allowed"], D["target"],
-                           dist=reach, ctx=ctx)
-        pc.pc_report(D["intents"], feasible, popcnt, N, traces, D["expect"], reach, pass_=pass_, reason=reason,
-                     summary=summary, ctx=ctx)
+        if only in ("all", "sel"):
+            pc.pc_eval_selectors(D["labels"], D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
+        if only in ("all", "trace"):
+            pc.pc_trace_flows(wl["S"], D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                              D["ingress"], wl["ttl"], out=traces, ctx=ctx)
+        if only in ("all", "reach"):
+            pc.pc_masked_reach(wl["V"], D["adj_off"], D["adj"], D["region"], D["src"], D["allowed"], D["target"],
+                               dist=reach, ctx=ctx)
+        if only == "all":
+            pc.pc_report(D["intents"], feasible, popcnt, N, traces, D["expect"], reach, pass_=pass_, reason=reason,
+                         summary=summary, ctx=ctx)
 
     for _ in range(args.warmup):
         step()
@@ -177,8 +185,16 @@ def main():
     def ktime(prefix):
         return sum(ms for name, (n, ms) in prof.items() if name.startswith(prefix)) / args.steps
 
-    sel_eval_n, sel_eval_ms = prof.get("k_sel_eval", (0, 0.0))
+    roof_kernel = "k_sel_eval"
+    if only in ("all", "sel"):
+        if roof_kernel not in prof:
+            raise SystemExit(f"bench: no timing for {roof_kernel} (timed kernels: {sorted(prof)})")
+        sel_eval_n, sel_eval_ms = prof[roof_kernel]
+    else:
+        sel_eval_n, sel_eval_ms = 0, 0.0
     avg_eval_ms = sel_eval_ms / max(sel_eval_n, 1)
+    # algorithmic bytes of one launch: the feasible bitsets written, one
+    # popcount per row, the node labels and the predicates read once
     n_preds = wl["n_preds"]
     alg_bytes = I_rows * W * 8 + I_rows * 4 + n_preds * 40 + N * L
     achieved = alg_bytes / (avg_eval_ms * 1e-3) / 1e9 if avg_eval_ms > 0 else 0.0
@@ -211,7 +227,7 @@ def main():
         "entry_ms_per_step": {"pc_eval_selectors": ktime("k_sel_"), "pc_trace_flows": trace_ms,
                               "pc_masked_reach": ktime("k_rc_"), "pc_report": ktime("k_report")},
         "per_kernel": per_kernel,
-        "roofline": {"kernel": "k_sel_eval", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+        "roofline": {"kernel": roof_kernel, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
                      "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": avg_eval_ms},
         "verdict": {"passed": passed, "intents": I},

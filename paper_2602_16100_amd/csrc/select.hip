@@ -7,27 +7,36 @@
 // Model and Satisfaction, example; Service Placement Module).
 //
 // Design (gfx950):
-//   1. presence  : which values of each label occur at all (LDS-local OR,
-//                  one global OR per workgroup).
+//   1. presence  : which values of each label occur at all.
 //   2. label scan: plane numbering -- one plane per present (label, value).
-//   3. planes    : planes[p][w] = 64-bit set of nodes 64w..64w+63 carrying
-//                  the plane's (label, value); built with one ballot per
-//                  present value per 64-node column.
+//   3. planes    : one 64-bit node set per (plane, 64-node word), built with
+//                  a ballot per present value; row-major, Wp words a plane.
 //   4. compile   : one thread per row turns its predicates into a clause
 //                  program over plane ids (In S = OR of S's planes or NOT OR
 //                  of the rest, whichever is shorter; NotIn the reverse;
-//                  Exists = NOT the absent-value plane) and validates it.
-//   5. eval      : one row per wavefront (its program read with scalar
-//                  loads), lanes over 64 columns of 64 nodes, plane words
-//                  fetched kBatch at a time so the loads overlap.  XCD-aware
-//                  block -> (column tile, row chunk) mapping keeps each XCD's
-//                  planes in its own L2.
+//                  Exists = NOT the absent-value plane), validates it, and
+//                  writes a 64-byte row record holding programs of up to 15
+//                  entries inline.
+//   5. eval      : one row at a time per wavefront over a tile of 128 words
+//                  (two per lane, 16-byte loads and stores).  A wavefront
+//                  loads the records of 64 rows with one vector load each
+//                  and reads them back one row at a time from registers, so
+//                  a row costs only its plane loads (L2 hits: a tile of
+//                  every plane is P KiB) and its output store.  Popcounts
+//                  are reduced in-wavefront with DPP and stored per (tile,
+//                  row); a last pass sums the tiles.
+#include <algorithm>
+
 #include "pc_internal.h"
 
 namespace {
 
-constexpr int kEvalThreads = 256;     // 4 waves, one row at a time each
-constexpr int kPresenceNodes = 4096;  // nodes per presence workgroup
+constexpr int kEvalThreads = 256;  // 4 wavefronts, one row at a time each
+constexpr int kWpl = 2;            // 64-bit words per lane
+constexpr int kTileW = 64 * kWpl;  // words per tile
+constexpr int kRecWords = 16;      // row record: header + 15 inline entries
+constexpr int kInline = kRecWords - 1;
+constexpr int kGroup = 8;          // plane loads in flight together
 
 __device__ __forceinline__ uint64_t uniform_u64(uint64_t x)
 {
@@ -47,11 +56,17 @@ __global__ __launch_bounds__(256) void k_sel_presence(const uint8_t *__restrict_
     const int32_t l = blockIdx.x * 64 + lt;
     const int64_t n0 = static_cast<int64_t>(blockIdx.y) * chunk;
     const int64_t n1 = min(static_cast<int64_t>(N), n0 + chunk);
+    uint32_t m[8] = {0, 0, 0, 0, 0, 0, 0, 0};  // this thread's 256-bit value set, in registers
     if (l < L) {
         for (int64_t n = n0 + sub; n < n1; n += 4) {
             const uint32_t x = labels[n * L + l];
-            atomicOr(&tab[lt * 8 + (x >> 5)], 1u << (x & 31));
+            const uint32_t word = x >> 5, bit = 1u << (x & 31);
+#pragma unroll
+            for (int k = 0; k < 8; ++k) m[k] |= word == static_cast<uint32_t>(k) ? bit : 0u;
         }
+#pragma unroll
+        for (int k = 0; k < 8; ++k)
+            if (m[k]) atomicOr(&tab[lt * 8 + k], m[k]);
     }
     __syncthreads();
     for (int i = tid; i < 512; i += 256) {
@@ -63,7 +78,7 @@ __global__ __launch_bounds__(256) void k_sel_presence(const uint8_t *__restrict_
 // Exclusive scan of per-label plane counts -> wbase[l][k] = id of the first
 // plane of label l whose value lies in 64-value word k.
 __global__ __launch_bounds__(1024) void k_sel_label_scan(const uint64_t *__restrict__ present, int32_t L,
-                                                         uint32_t *__restrict__ wbase)
+                                                         uint32_t *__restrict__ wbase, int32_t *__restrict__ d_P)
 {
     __shared__ uint32_t wsum[16];
     __shared__ uint32_t carry_s;
@@ -106,19 +121,22 @@ __global__ __launch_bounds__(1024) void k_sel_label_scan(const uint64_t *__restr
         if (tid == 0) carry_s = carry + wsum[15];
         __syncthreads();
     }
+    if (tid == 0) *d_P = static_cast<int32_t>(carry_s);
 }
 
-// One wavefront per (64-node column w, label l): a ballot per present value.
+// One wavefront per (64-node word w, label l): a ballot per present value.
+// Word w of plane p lives at planes[p * Wp + w].
 __global__ __launch_bounds__(256) void k_sel_planes(const uint8_t *__restrict__ labels, int32_t N, int32_t L,
                                                     const uint64_t *__restrict__ present,
                                                     const uint32_t *__restrict__ wbase, uint64_t *__restrict__ planes,
-                                                    int32_t W)
+                                                    int64_t Wp)
 {
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int32_t w = blockIdx.x;
     const int32_t l = blockIdx.y * 4 + wave;
     if (l >= L) return;
+    uint64_t *col = planes + w;
     const int64_t n = static_cast<int64_t>(w) * 64 + lane;
     const uint32_t x = n < N ? labels[n * L + l] : 0x100u;  // 0x100 equals no value
     for (int k = 0; k < 4; ++k) {
@@ -127,7 +145,7 @@ __global__ __launch_bounds__(256) void k_sel_planes(const uint8_t *__restrict__ 
         while (m) {
             const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
             const uint64_t word = __ballot(x == v);
-            if (lane == 0) planes[static_cast<int64_t>(pid) * W + w] = word;
+            if (lane == 0) col[static_cast<int64_t>(pid) * Wp] = word;
             ++pid;
             m &= m - 1;
         }
@@ -145,9 +163,10 @@ __device__ __forceinline__ bool pred_valid(uint32_t label, uint32_t op, uint32_t
 constexpr uint32_t kLast = 1u << 30;
 constexpr uint32_t kNeg = 1u << 31;
 constexpr uint32_t kPidMask = kLast - 1;
-constexpr int32_t kRowFalse = -1;  // some clause admits no node (or a malformed predicate)
-constexpr int32_t kRowLong = -2;   // program longer than 4 entries per predicate: decoded on the fly
-constexpr int kBatch = 8;          // plane loads in flight per wavefront
+// Row record header (word 0); words 1..15 hold an inline program.
+constexpr int32_t kRowFalse = -1;     // some clause admits no node (or a malformed predicate)
+constexpr int32_t kRowIndirect = -2;  // program of more than 15 entries at prog[4 * word1], word2 entries
+constexpr int32_t kRowLong = -3;      // program longer than 4 entries per predicate: decoded on the fly
 
 __device__ __forceinline__ uint32_t plane_id(const uint64_t *pres, const uint32_t *wb, uint32_t v)
 {
@@ -155,69 +174,85 @@ __device__ __forceinline__ uint32_t plane_id(const uint64_t *pres, const uint32_
     return wb[k] + __popcll(pres[k] & ((1ull << (v & 63)) - 1));
 }
 
-// One thread per row: validate the row and compile it into a clause
-// program over plane ids.  A clause is an OR of planes, optionally
-// negated; each label value of a node lies in exactly one present plane,
-// so In S = OR(S) = NOT OR(present \ S) and NotIn S = NOT OR(S) =
-// OR(present \ S): the shorter form is kept.  Entries live at
-// prog[4 * pred_off[i] ...], at most 4 per predicate.
+// The value set a predicate ORs over, and whether the OR is negated.  Each
+// label value of a node lies in exactly one present plane, so In S = OR(S)
+// = NOT OR(present \ S) and NotIn S = NOT OR(S) = OR(present \ S): the
+// shorter form is taken.  Exists = NOT OR(plane of the absent value), an
+// empty OR when every node carries the label.
+__device__ __forceinline__ uint32_t pred_clause(const pc_pred &q, const uint64_t *pres, uint64_t sel[4], bool &neg)
+{
+    if (q.op == PC_OP_EXISTS) {
+        sel[0] = sel[1] = sel[2] = 0;
+        sel[3] = pres[3] & (1ull << 63);
+        neg = true;
+        return static_cast<uint32_t>(sel[3] >> 63);
+    }
+    uint64_t in[4], out[4];
+    uint32_t ms = 0, mc = 0;
+    for (int k = 0; k < 4; ++k) {
+        in[k] = q.vals[k] & pres[k];
+        out[k] = pres[k] & ~q.vals[k];
+        ms += __popcll(in[k]);
+        mc += __popcll(out[k]);
+    }
+    const bool use_in = ms <= mc;
+    for (int k = 0; k < 4; ++k) sel[k] = use_in ? in[k] : out[k];
+    neg = (q.op == PC_OP_IN) ? !use_in : use_in;
+    return use_in ? ms : mc;
+}
+
+// One thread per row, two passes over its predicates: validate and size
+// the program, then emit it -- inline in the row record when it has at most
+// 15 entries, else at prog[4 * pred_off[i] ...] (at most 4 entries per
+// predicate; longer programs are decoded at evaluation time).
 __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__ pred_off,
                                                      const pc_pred *__restrict__ preds, int64_t n_preds, int32_t I,
                                                      int32_t L, const uint64_t *__restrict__ present,
                                                      const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog,
-                                                     int32_t *__restrict__ row_len, uint32_t *__restrict__ d_err)
+                                                     uint32_t *__restrict__ rec, uint32_t *__restrict__ d_err)
 {
     uint32_t errs = 0;
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
+        uint32_t *rr = rec + static_cast<int64_t>(i) * kRecWords;
         const int64_t b = pred_off[i], e = pred_off[i + 1];
         if (!pc_range_ok(b, e, n_preds)) {
             errs |= PC_DERR_OFFSETS;
-            row_len[i] = kRowFalse;
+            rr[0] = static_cast<uint32_t>(kRowFalse);
             continue;
         }
-        int32_t state = 0;  // 0 ok, kRowFalse, kRowLong
+        bool empty = false;
         int64_t n = 0;
-        const int64_t cap = 4 * (e - b);
-        uint32_t *out = prog + 4 * b;
         for (int64_t p = b; p < e; ++p) {
             const pc_pred q = preds[p];
             if (!pred_valid(q.label, q.op, q.rsv0, q.rsv1, q.vals[3], L)) {
                 errs |= PC_DERR_PRED;
-                state = kRowFalse;
+                empty = true;
                 continue;
             }
-            if (state == kRowFalse) continue;
+            uint64_t sel[4];
+            bool neg;
+            const uint32_t cnt = pred_clause(q, present + static_cast<int64_t>(q.label) * 4, sel, neg);
+            if (cnt == 0 && !neg) empty = true;  // empty OR: no node (a negated empty OR is every node)
+            n += cnt;
+        }
+        if (empty) {
+            rr[0] = static_cast<uint32_t>(kRowFalse);
+            continue;
+        }
+        const bool inl = n <= kInline;
+        if (!inl && n > 4 * (e - b)) {
+            rr[0] = static_cast<uint32_t>(kRowLong);
+            continue;
+        }
+        uint32_t *out = inl ? rr + 1 : prog + 4 * b;
+        int64_t k_out = 0;
+        for (int64_t p = b; p < e; ++p) {
+            const pc_pred q = preds[p];
             const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
             const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
             uint64_t sel[4];
             bool neg;
-            if (q.op == PC_OP_EXISTS) {
-                // Exists = NOT OR(plane of the absent value), when any node lacks the label
-                sel[0] = sel[1] = sel[2] = 0;
-                sel[3] = pres[3] & (1ull << 63);
-                neg = true;
-            } else {
-                uint64_t in[4], out_[4];
-                uint32_t ms = 0, mc = 0;
-                for (int k = 0; k < 4; ++k) {
-                    in[k] = q.vals[k] & pres[k];
-                    out_[k] = pres[k] & ~q.vals[k];
-                    ms += __popcll(in[k]);
-                    mc += __popcll(out_[k]);
-                }
-                const bool use_in = ms <= mc;
-                for (int k = 0; k < 4; ++k) sel[k] = use_in ? in[k] : out_[k];
-                neg = (q.op == PC_OP_IN) ? !use_in : use_in;
-            }
-            uint32_t cnt = __popcll(sel[0]) + __popcll(sel[1]) + __popcll(sel[2]) + __popcll(sel[3]);
-            if (cnt == 0) {
-                if (!neg) state = kRowFalse;  // empty OR: no node
-                continue;                     // negated empty OR: every node
-            }
-            if (state == kRowLong || n + cnt > cap) {
-                state = kRowLong;
-                continue;
-            }
+            uint32_t cnt = pred_clause(q, pres, sel, neg);
             for (int k = 0; k < 4; ++k) {
                 uint64_t m = sel[k];
                 while (m) {
@@ -225,51 +260,143 @@ __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__
                     m &= m - 1;
                     uint32_t ent = plane_id(pres, wb, v);
                     if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
-                    out[n++] = ent;
+                    out[k_out++] = ent;
                 }
             }
         }
-        row_len[i] = state ? state : static_cast<int32_t>(n);
+        if (inl) {
+            rr[0] = static_cast<uint32_t>(n);
+        } else {
+            rr[0] = static_cast<uint32_t>(kRowIndirect);
+            rr[1] = static_cast<uint32_t>(b);
+            rr[2] = static_cast<uint32_t>(n);
+        }
     }
     if (errs) atomicOr(d_err, errs);
 }
 
-// Rows whose program did not fit: decode the predicates on the scalar unit.
-__device__ uint64_t eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, int64_t e,
-                                     const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
-                                     const uint64_t *pcol, int32_t W, bool wok)
+// Sum of v over the 64 lanes, returned uniform.  quad_perm [1,0,3,2] and
+// [2,3,0,1], row_half_mirror and row_mirror leave every lane of each row of
+// 16 lanes holding that row's sum; the four row sums are read back.  Every
+// lane must be active.
+__device__ __forceinline__ uint32_t wave_sum_uniform(uint32_t v)
 {
-    uint64_t acc = ~0ull;
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x4E, 0xF, 0xF, false));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x141, 0xF, 0xF, false));
+    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false));
+    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 0)) +
+           static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 16)) +
+           static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 32)) +
+           static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 48));
+}
+
+struct Words {
+    uint64_t a, b;
+};
+typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+
+__device__ __forceinline__ Words load_words(const uint64_t *p)
+{
+    const ulonglong2 v = *reinterpret_cast<const ulonglong2 *>(p);
+    return {v.x, v.y};
+}
+
+__device__ __forceinline__ uint32_t rec_word(const uint4 &h0, const uint4 &h1, const uint4 &h2, const uint4 &h3,
+                                             int k)
+{
+    switch (k) {
+    case 0: return h0.x;
+    case 1: return h0.y;
+    case 2: return h0.z;
+    case 3: return h0.w;
+    case 4: return h1.x;
+    case 5: return h1.y;
+    case 6: return h1.z;
+    case 7: return h1.w;
+    case 8: return h2.x;
+    case 9: return h2.y;
+    case 10: return h2.z;
+    case 11: return h2.w;
+    case 12: return h3.x;
+    case 13: return h3.y;
+    case 14: return h3.z;
+    default: return h3.w;
+    }
+}
+
+// Fold one program entry's plane words into the running clause (c) and,
+// at the end of a clause, into the row's conjunction (a).
+__device__ __forceinline__ void fold(uint32_t ent, const Words &v, Words &c, Words &a)
+{
+    c.a |= v.a;
+    c.b |= v.b;
+    if (ent & kLast) {
+        if (ent & kNeg) {
+            a.a &= ~c.a;
+            a.b &= ~c.b;
+        } else {
+            a.a &= c.a;
+            a.b &= c.b;
+        }
+        c.a = c.b = 0;
+    }
+}
+
+// Rows whose program did not fit its slot: decode the predicates on the
+// scalar unit.  `pcol` points at this lane's two words of plane 0.
+__device__ Words eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, int64_t e,
+                                  const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
+                                  const uint64_t *pcol, int64_t Wp, bool lok)
+{
+    Words a{~0ull, ~0ull};
     for (int64_t p = b; p < e; ++p) {
         const pc_pred *q = preds + p;
         const uint32_t label = q->label, op = q->op;
         const uint64_t *pres = present + static_cast<int64_t>(label) * 4;
         const uint32_t *wb = wbase + static_cast<int64_t>(label) * 4;
         if (op == PC_OP_EXISTS) {
-            const uint64_t p3 = pres[3];
-            if (p3 >> 63) acc &= wok ? ~pcol[static_cast<int64_t>(plane_id(pres, wb, 255)) * W] : 0ull;
+            if (pres[3] >> 63) {
+                const Words v = lok ? load_words(pcol + static_cast<int64_t>(plane_id(pres, wb, 255)) * Wp)
+                                    : Words{0, 0};
+                a.a &= ~v.a;
+                a.b &= ~v.b;
+            }
             continue;
         }
-        uint64_t cur = 0;
+        Words c{0, 0};
         for (int k = 0; k < 4; ++k) {
             uint64_t m = q->vals[k] & pres[k];
             while (m) {
                 const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
                 m &= m - 1;
-                if (wok) cur |= pcol[static_cast<int64_t>(plane_id(pres, wb, v)) * W];
+                if (lok) {
+                    const Words x = load_words(pcol + static_cast<int64_t>(plane_id(pres, wb, v)) * Wp);
+                    c.a |= x.a;
+                    c.b |= x.b;
+                }
             }
         }
-        acc &= (op == PC_OP_IN) ? cur : ~cur;
+        if (op == PC_OP_IN) {
+            a.a &= c.a;
+            a.b &= c.b;
+        } else {
+            a.a &= ~c.a;
+            a.b &= ~c.b;
+        }
     }
-    return acc;
+    return a;
 }
 
+// Work item (tile, chunk): the wavefronts of a workgroup take turns on
+// batches of 64 consecutive rows of the chunk; lane l covers words
+// tile * 128 + 2l and + 1.  part[tile * I + r] receives row r's popcount
+// over the tile.
 __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
-    const int32_t *__restrict__ pred_off, const pc_pred *__restrict__ preds, int32_t I,
-    const uint32_t *__restrict__ prog, const int32_t *__restrict__ row_len, const uint64_t *__restrict__ present,
-    const uint32_t *__restrict__ wbase, const uint64_t *__restrict__ planes, int32_t W, int32_t N,
-    uint64_t *__restrict__ feasible, uint32_t *__restrict__ popcnt, int32_t ntiles, int32_t nchunks,
-    int32_t rows_per_chunk)
+    const uint32_t *__restrict__ rec, const uint32_t *__restrict__ prog, const int32_t *__restrict__ pred_off,
+    const pc_pred *__restrict__ preds, const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
+    const uint64_t *__restrict__ planes, int64_t Wp, int32_t I, int32_t W, int32_t N,
+    uint64_t *__restrict__ feasible, uint32_t *__restrict__ part, int32_t ntiles, int32_t nchunks, int32_t rpc)
 {
     const int64_t total = static_cast<int64_t>(ntiles) * nchunks;
     const int64_t item = pc_xcd_item(total);
@@ -278,50 +405,105 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     const int32_t chunk = static_cast<int32_t>(item % nchunks);
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int32_t w = tile * 64 + lane;
-    const bool wok = w < W;
-    uint64_t tail = ~0ull;
-    if (!wok) tail = 0;
-    else if (w == W - 1 && (N & 63)) tail = (1ull << (N & 63)) - 1;
-    const uint64_t *pcol = planes + (wok ? w : 0);
-    const int32_t r0 = chunk * rows_per_chunk;
-    const int32_t r1 = min(I, r0 + rows_per_chunk);
-    for (int32_t r = r0 + wave; r < r1; r += kEvalThreads / 64) {
-        const int32_t len = row_len[r];
-        uint64_t acc = ~0ull;
-        if (len == kRowFalse) {
-            acc = 0;
-        } else if (len == kRowLong) {
-            acc = eval_row_decoded(preds, pred_off[r], pred_off[r + 1], present, wbase, pcol, W, wok);
-        } else {
-            const uint32_t *pr = prog + 4 * static_cast<int64_t>(pred_off[r]);
-            uint64_t cur = 0;
-            for (int32_t e0 = 0; e0 < len; e0 += kBatch) {
-                uint32_t E[kBatch];
-                uint64_t V[kBatch];
-#pragma unroll
-                for (int k = 0; k < kBatch; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
-#pragma unroll
-                for (int k = 0; k < kBatch; ++k)
-                    V[k] = (e0 + k < len && wok) ? pcol[static_cast<int64_t>(E[k] & kPidMask) * W] : 0ull;
-#pragma unroll
-                for (int k = 0; k < kBatch; ++k) {
-                    if (e0 + k < len) {
-                        cur |= V[k];
-                        if (E[k] & kLast) {
-                            acc &= (E[k] & kNeg) ? ~cur : cur;
-                            cur = 0;
-                        }
-                    }
-                }
-                if (__ballot((acc & tail) != 0) == 0) break;
+    const int32_t w0 = tile * kTileW + lane * kWpl;
+    const bool ok0 = w0 < W, ok1 = w0 + 1 < W;
+    const uint64_t last = (N & 63) ? (1ull << (N & 63)) - 1 : ~0ull;
+    const uint64_t m0 = ok0 ? (w0 == W - 1 ? last : ~0ull) : 0ull;
+    const uint64_t m1 = ok1 ? (w0 + 1 == W - 1 ? last : ~0ull) : 0ull;
+    const uint64_t *pcol = planes + (ok0 ? w0 : 0);
+    const bool even = (W & 1) == 0;
+    uint32_t *prt = part + static_cast<int64_t>(tile) * I;
+    const int32_t r0 = chunk * rpc;
+    const int32_t r1 = min(I, r0 + rpc);
+    for (int32_t bat = r0 + wave * 64; bat < r1; bat += kEvalThreads) {
+        const int32_t rr = bat + lane;
+        const bool rv = rr < r1;
+        uint4 h0 = make_uint4(static_cast<uint32_t>(kRowFalse), 0, 0, 0);
+        uint4 h1 = make_uint4(0, 0, 0, 0), h2 = h1, h3 = h1;
+        if (rv) {
+            const uint4 *rp = reinterpret_cast<const uint4 *>(rec + static_cast<int64_t>(rr) * kRecWords);
+            h0 = rp[0];
+            h1 = rp[1];
+            if (static_cast<int32_t>(h0.x) > 7) {
+                h2 = rp[2];
+                h3 = rp[3];
             }
         }
-        acc &= tail;
-        if (wok) feasible[static_cast<int64_t>(r) * W + w] = acc;
-        const uint32_t cnt = pc_wave_sum_u32(__popcll(acc));
-        if (lane == 0 && cnt) atomicAdd(&popcnt[r], cnt);
+        const int32_t nb = min(64, r1 - bat);
+        uint32_t cvec = 0;
+        for (int32_t i = 0; i < nb; ++i) {
+            const int32_t hdr = __builtin_amdgcn_readlane(static_cast<int>(h0.x), i);
+            const int32_t r = bat + i;
+            Words a{~0ull, ~0ull};
+            if (hdr == kRowFalse) {
+                a = Words{0, 0};
+            } else if (hdr >= 0) {
+                Words c{0, 0};
+#pragma unroll
+                for (int g = 0; g < kInline; g += kGroup) {
+                    if (g < hdr) {
+                        uint32_t E[kGroup];
+                        Words V[kGroup];
+#pragma unroll
+                        for (int k = 0; k < kGroup; ++k) {
+                            if (g + k < kInline && g + k < hdr) {
+                                E[k] = static_cast<uint32_t>(__builtin_amdgcn_readlane(
+                                    static_cast<int>(rec_word(h0, h1, h2, h3, 1 + g + k)), i));
+                                V[k] = ok0 ? load_words(pcol + static_cast<int64_t>(E[k] & kPidMask) * Wp)
+                                           : Words{0, 0};
+                            }
+                        }
+#pragma unroll
+                        for (int k = 0; k < kGroup; ++k)
+                            if (g + k < kInline && g + k < hdr) fold(E[k], V[k], c, a);
+                    }
+                }
+            } else if (hdr == kRowIndirect) {
+                const int64_t pb = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(h0.y), i));
+                const int32_t len = __builtin_amdgcn_readlane(static_cast<int>(h0.z), i);
+                const uint32_t *pr = prog + 4 * pb;
+                Words c{0, 0};
+                for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
+                    uint32_t E[kGroup];
+                    Words V[kGroup];
+#pragma unroll
+                    for (int k = 0; k < kGroup; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
+#pragma unroll
+                    for (int k = 0; k < kGroup; ++k)
+                        V[k] = (e0 + k < len && ok0) ? load_words(pcol + static_cast<int64_t>(E[k] & kPidMask) * Wp)
+                                                     : Words{0, 0};
+#pragma unroll
+                    for (int k = 0; k < kGroup; ++k)
+                        if (e0 + k < len) fold(E[k], V[k], c, a);
+                }
+            } else {
+                a = eval_row_decoded(preds, pred_off[r], pred_off[r + 1], present, wbase, pcol, Wp, ok0);
+            }
+            a.a &= m0;
+            a.b &= m1;
+            uint64_t *dst = feasible + static_cast<int64_t>(r) * W + w0;
+            if (even) {
+                if (ok0) __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(dst));
+            } else {
+                if (ok0) __builtin_nontemporal_store(a.a, dst);
+                if (ok1) __builtin_nontemporal_store(a.b, dst + 1);
+            }
+            const uint32_t cnt = wave_sum_uniform(__popcll(a.a) + __popcll(a.b));
+            cvec = lane == i ? cnt : cvec;
+        }
+        if (rv) prt[rr] = cvec;
     }
+}
+
+// popcnt[r] = sum over tiles of part[t * I + r].
+__global__ __launch_bounds__(256) void k_sel_popsum(const uint32_t *__restrict__ part, int32_t I, int32_t ntiles,
+                                                    uint32_t *__restrict__ popcnt)
+{
+    const int32_t r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= I) return;
+    uint32_t s = 0;
+    for (int32_t t = 0; t < ntiles; ++t) s += part[static_cast<int64_t>(t) * I + r];
+    popcnt[r] = s;
 }
 
 }  // namespace
@@ -331,70 +513,84 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
                   hipStream_t stream)
 {
     const int64_t W = (static_cast<int64_t>(N) + 63) / 64;
+    const int64_t Wp = (W + 1) / 2 * 2;  // even: 16-byte aligned plane rows
+    const int64_t ntiles = (W + kTileW - 1) / kTileW;
     const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
-    const size_t plane_bytes = static_cast<size_t>(pmax) * static_cast<size_t>(W) * 8;
+    const size_t plane_bytes = static_cast<size_t>(pmax) * static_cast<size_t>(Wp) * 8;
     if (plane_bytes > (size_t(64) << 30))
         return pc_set_error(ctx, PC_ENOMEM, "pc_eval_selectors: value planes need %zu bytes (L=%d N=%d)", plane_bytes,
                             L, N);
-    Carver c{nullptr, 0};
     uint64_t *present, *planes;
-    uint32_t *wbase, *prog;
-    int32_t *row_len;
+    uint32_t *wbase, *prog, *rec, *part;
+    int32_t *d_P;
     auto carve = [&](Carver &cv) {
         present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
         wbase = cv.take<uint32_t>(static_cast<size_t>(L) * 4 + 1);
-        planes = cv.take<uint64_t>(static_cast<size_t>(pmax) * W + 1);
-        prog = cv.take<uint32_t>(static_cast<size_t>(n_preds) * 4 + 1);
-        row_len = cv.take<int32_t>(static_cast<size_t>(I) + 1);
+        planes = cv.take<uint64_t>(static_cast<size_t>(pmax) * Wp + 2);
+        prog = cv.take<uint32_t>(static_cast<size_t>(n_preds) * 4 + 4);
+        rec = cv.take<uint32_t>(static_cast<size_t>(I) * kRecWords + kRecWords);
+        part = ntiles > 1 ? cv.take<uint32_t>(static_cast<size_t>(ntiles) * I + 1) : nullptr;
+        d_P = cv.take<int32_t>(1);
     };
-    carve(c);
-    int rc = pc_ensure_arena(ctx, c.off);
+    Carver dry{nullptr, 0};
+    carve(dry);
+    int rc = pc_ensure_arena(ctx, dry.off);
     if (rc) return rc;
     Carver real{ctx->arena, 0};
     carve(real);
 
-    launch_fill_u32(popcnt, static_cast<size_t>(I), 0, stream);
     launch_fill_u64(present, static_cast<size_t>(L) * 4, 0, stream);
+    if (W == 0) launch_fill_u32(popcnt, static_cast<size_t>(I), 0, stream);
     PC_LAUNCH_CHECK(ctx);
     if (N > 0 && L > 0) {
-        int64_t chunk = kPresenceNodes;
+        // about 2048 workgroups: a few hundred nodes each
+        const int64_t ltiles = (L + 63) / 64;
+        int64_t chunk = (static_cast<int64_t>(N) * ltiles + 2047) / 2048;
+        chunk = chunk < 64 ? 64 : (chunk + 3) / 4 * 4;
         while ((N + chunk - 1) / chunk > 65535) chunk *= 2;
         dim3 gp((L + 63) / 64, static_cast<unsigned>((N + chunk - 1) / chunk));
-        PC_TIMED(ctx, "k_sel_presence", stream, hipLaunchKernelGGL(k_sel_presence, gp, dim3(256), 0, stream, labels, N, L, chunk,
-                           reinterpret_cast<uint32_t *>(present)));
+        PC_TIMED(ctx, "k_sel_presence", stream,
+                 hipLaunchKernelGGL(k_sel_presence, gp, dim3(256), 0, stream, labels, N, L, chunk,
+                                    reinterpret_cast<uint32_t *>(present)));
         PC_LAUNCH_CHECK(ctx);
     }
     if (L > 0) {
-        PC_TIMED(ctx, "k_sel_label_scan", stream, hipLaunchKernelGGL(k_sel_label_scan, dim3(1), dim3(1024), 0, stream, present, L, wbase));
+        PC_TIMED(ctx, "k_sel_label_scan", stream,
+                 hipLaunchKernelGGL(k_sel_label_scan, dim3(1), dim3(1024), 0, stream, present, L, wbase, d_P));
         PC_LAUNCH_CHECK(ctx);
     }
     if (N > 0 && L > 0) {
         dim3 gb(static_cast<unsigned>(W), static_cast<unsigned>((L + 3) / 4));
-        PC_TIMED(ctx, "k_sel_planes", stream, hipLaunchKernelGGL(k_sel_planes, gb, dim3(256), 0, stream, labels, N, L, present, wbase, planes,
-                           static_cast<int32_t>(W)));
+        PC_TIMED(ctx, "k_sel_planes", stream,
+                 hipLaunchKernelGGL(k_sel_planes, gb, dim3(256), 0, stream, labels, N, L, present, wbase, planes, Wp));
         PC_LAUNCH_CHECK(ctx);
     }
-    const int32_t ntiles = static_cast<int32_t>(W > 0 ? (W + 63) / 64 : 1);
-    int64_t nchunks = (4096 + ntiles - 1) / ntiles;
-    const int64_t max_chunks = (static_cast<int64_t>(I) + 3) / 4;
-    if (nchunks > max_chunks) nchunks = max_chunks;
-    if (nchunks < 1) nchunks = 1;
-    const int32_t rpc = static_cast<int32_t>((I + nchunks - 1) / nchunks);
+    const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
+    PC_TIMED(ctx, "k_sel_compile", stream,
+             hipLaunchKernelGGL(k_sel_compile, dim3(rgrid), dim3(256), 0, stream, pred_off, preds, n_preds, I, L,
+                                present, wbase, prog, rec, ctx->d_err));
+    PC_LAUNCH_CHECK(ctx);
+    if (W == 0) return PC_OK;
+
+    // about 4096 workgroups; a chunk is a whole number of 256-row passes
+    int64_t nchunks = std::max<int64_t>((4096 + ntiles - 1) / ntiles, 1);
+    int64_t rpc = (I + nchunks - 1) / nchunks;
+    rpc = (rpc + kEvalThreads - 1) / kEvalThreads * kEvalThreads;
     nchunks = (I + rpc - 1) / rpc;
     const int64_t total = ntiles * nchunks;
     const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
-    {
-        int64_t cb = (I + 255) / 256;
-        if (cb > 8192) cb = 8192;
-        PC_TIMED(ctx, "k_sel_compile", stream,
-                 hipLaunchKernelGGL(k_sel_compile, dim3(static_cast<unsigned>(cb)), dim3(256), 0, stream, pred_off,
-                                    preds, n_preds, I, L, present, wbase, prog, row_len, ctx->d_err));
+    uint32_t *cnt_out = ntiles > 1 ? part : popcnt;
+    PC_TIMED(ctx, "k_sel_eval", stream,
+             hipLaunchKernelGGL(k_sel_eval, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, pred_off, preds,
+                                present, wbase, planes, Wp, I, static_cast<int32_t>(W), N, feasible, cnt_out,
+                                static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
+                                static_cast<int32_t>(rpc)));
+    PC_LAUNCH_CHECK(ctx);
+    if (ntiles > 1) {
+        PC_TIMED(ctx, "k_sel_popsum", stream,
+                 hipLaunchKernelGGL(k_sel_popsum, dim3(static_cast<unsigned>((I + 255) / 256)), dim3(256), 0, stream,
+                                    part, I, static_cast<int32_t>(ntiles), popcnt));
         PC_LAUNCH_CHECK(ctx);
     }
-    PC_TIMED(ctx, "k_sel_eval", stream,
-             hipLaunchKernelGGL(k_sel_eval, dim3(blocks), dim3(kEvalThreads), 0, stream, pred_off, preds, I, prog,
-                                row_len, present, wbase, planes, static_cast<int32_t>(W), N, feasible, popcnt,
-                                ntiles, static_cast<int32_t>(nchunks), rpc));
-    PC_LAUNCH_CHECK(ctx);
     return PC_OK;
 }

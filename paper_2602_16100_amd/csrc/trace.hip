@@ -220,13 +220,13 @@ __device__ __forceinline__ void verify_group(uint32_t surv, const pc_rule *grp, 
     }
 }
 
-__global__ __launch_bounds__(kMatchThreads) void k_tr_match(
+__global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
     const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt, const pc_key *__restrict__ hdr,
     const int32_t *__restrict__ boff, const int32_t *__restrict__ bucket, uint64_t *__restrict__ bestkey)
 {
     __shared__ uint64_t best[kTile];
-    __shared__ uint32_t h2s[kTile];
+    __shared__ __align__(16) uint32_t h2s[kTile];
     __shared__ int32_t tids[kTile];
     const int32_t s = blockIdx.x;
     const int32_t bb = boff[s], be = boff[s + 1];
@@ -236,44 +236,53 @@ __global__ __launch_bounds__(kMatchThreads) void k_tr_match(
     const int32_t G = gcount[s];
     const int64_t rb = rule_off[s];
     const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
-    const int32_t nslices = (G + kSliceGroups - 1) / kSliceGroups;
-    v16u F[kChunks];
-    int32_t loaded = -1;
-    for (int32_t t0 = bb; t0 < be; t0 += kTile) {
-        const int32_t tn = min(kTile, be - t0);
-        for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
-            const int32_t t = bucket[t0 + i];
-            tids[i] = t;
-            h2s[i] = hdr[t].w[2];
-            best[i] = kNoMatch;
-        }
-        __syncthreads();
-        for (int32_t sl = 0; sl < nslices; ++sl) {
-            const int32_t g = sl * kSliceGroups + wave * 64 + lane;
-            if (loaded != sl) {
+    const int32_t nslices = max(1, (G + kSliceGroups - 1) / kSliceGroups);
+    // slice-major: each lane's chunk sets are loaded once per slice; the
+    // running best of every lookup is carried in bestkey between slices
+    for (int32_t sl = 0; sl < nslices; ++sl) {
+        const int32_t g = sl * kSliceGroups + wave * 64 + lane;
+        v16u F[kChunks];
 #pragma unroll
-                for (int c = 0; c < kChunks; ++c)
+        for (int c = 0; c < kChunks; ++c)
 #pragma unroll
-                    for (int x = 0; x < 16; ++x)
-                        F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * G + g] : 0u;
-                loaded = sl;
+            for (int x = 0; x < 16; ++x) F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * G + g] : 0u;
+        const pc_rule *grp = rules + rb + static_cast<int64_t>(g) * 32;
+        for (int32_t t0 = bb; t0 < be; t0 += kTile) {
+            const int32_t tn = min(kTile, be - t0);
+            for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
+                const int32_t t = bucket[t0 + i];
+                tids[i] = t;
+                h2s[i] = hdr[t].w[2];
+                best[i] = sl == 0 ? kNoMatch : bestkey[t];
             }
-            const pc_rule *grp = rules + rb + static_cast<int64_t>(g) * 32;
-            for (int32_t j = 0; j < tn; ++j) {
-                const uint32_t h2 = __builtin_amdgcn_readfirstlane(h2s[j]);
-                uint32_t surv = F[0][h2 & 15u];
+            __syncthreads();
+            for (int32_t j0 = 0; j0 < tn; j0 += 4) {
+                const uint4 h4 = *reinterpret_cast<const uint4 *>(&h2s[j0]);
+                const uint32_t hv[4] = {h4.x, h4.y, h4.z, h4.w};
+                uint32_t sv[4];
 #pragma unroll
-                for (int c = 1; c < kChunks; ++c) surv &= F[c][(h2 >> (4 * c)) & 15u];
-                if (__ballot(surv != 0) && surv) {
-                    const pc_key h = hdr[tids[j]];
-                    verify_group(surv, grp, static_cast<uint32_t>(g) * 32, h,
-                                 reinterpret_cast<unsigned long long *>(&best[j]));
+                for (int k = 0; k < 4; ++k) {
+                    const uint32_t h2 = __builtin_amdgcn_readfirstlane(hv[k]);
+                    uint32_t surv = F[0][h2 & 15u];
+#pragma unroll
+                    for (int c = 1; c < kChunks; ++c) surv &= F[c][(h2 >> (4 * c)) & 15u];
+                    sv[k] = j0 + k < tn ? surv : 0u;
+                }
+                if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        if (sv[k]) {
+                            const pc_key h = hdr[tids[j0 + k]];
+                            verify_group(sv[k], grp, static_cast<uint32_t>(g) * 32, h,
+                                         reinterpret_cast<unsigned long long *>(&best[j0 + k]));
+                        }
+                    }
                 }
             }
+            __syncthreads();
+            for (int i = threadIdx.x; i < tn; i += kMatchThreads) bestkey[tids[i]] = best[i];
+            __syncthreads();
         }
-        __syncthreads();
-        for (int i = threadIdx.x; i < tn; i += kMatchThreads) bestkey[tids[i]] = best[i];
-        __syncthreads();
     }
 }
 

@@ -76,6 +76,13 @@ def test_selectors_absent_labels_and_ragged(g, orc):
     _check_workload(g, orc, wl)
 
 
+def test_selectors_many_planes(g, orc):
+    """About 3,000 value planes with a few absent labels: long In/NotIn
+    programs and a ragged last word."""
+    wl = synth.selector_workload(21, 2000 + 11, 12, 300, card_choices=(250,), absent_p=0.01)
+    _check_workload(g, orc, wl)
+
+
 def test_selectors_large_value_sets(g, orc):
     """In/NotIn sets with up to 200 values (beyond the generators' 1..4)."""
     rng = np.random.default_rng(7)
@@ -183,6 +190,15 @@ def test_trace_malformed_flags(g, orc):
 def test_reach_small_graph_bitset(g, orc, full_rows):
     wl = synth.rgg_workload(4, 3000, 8, 200, mean_degree=6.0, full_rows=full_rows)
     _check_workload(g, orc, wl)
+
+
+@pytest.mark.parametrize("V", [700, 1500, 2900, 4000, 5500, 6144])
+def test_reach_bitset_vertex_ownership(g, orc, V):
+    """Every per-thread vertex-ownership width of the bitset BFS (1..6
+    vertices per thread), target mode and full rows."""
+    for full_rows in (False, True):
+        wl = synth.rgg_workload(V, V, 8, 130, mean_degree=7.0, full_rows=full_rows)
+        _check_workload(g, orc, wl)
 
 
 @pytest.mark.parametrize("full_rows", [True, False])
