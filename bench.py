@@ -25,6 +25,26 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 
+# HBM bytes per launch of k_sel_eval on the combined workload, from one
+# rocprofv3 FETCH_SIZE pass and one WRITE_SIZE pass, each scaled by what
+# the same counter reads for a plain copy of known size (the command lines
+# and counter values are in profiles/k_sel_eval_cfg5_hbm_counters.md).
+# Valid only for the kernel source it was measured on.
+SEL_TRAFFIC = {"source": "paper_2602_16100_amd/csrc/select.hip",
+               "sha256": "a262fd3d663422e6c9c3bfa4eef8319b0b96e94aab6426d0355cda00f83e338b",
+               "workload": "cfg5", "bytes_per_launch": 444_465_152 + 4_473_939_968}
+
+
+def measured_traffic(workload):
+    import hashlib
+    path = os.path.join(ROOT, SEL_TRAFFIC["source"])
+    if workload != SEL_TRAFFIC["workload"] or not os.path.exists(path):
+        return None
+    with open(path, "rb") as f:
+        if hashlib.sha256(f.read()).hexdigest() != SEL_TRAFFIC["sha256"]:
+            return None
+    return SEL_TRAFFIC["bytes_per_launch"]
+
 
 def parse():
     ap = argparse.ArgumentParser()
@@ -32,11 +52,28 @@ def parse():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--workload", default="cfg5", choices=["cfg5", "small"])
-    ap.add_argument("--cpu-seconds", type=float, default=15.0, help="target oracle time for the CPU baseline")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0,
+                    help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach"],
                     help="profiling aid: time one stage only (the JSON line then covers that stage)")
+    ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
+                    help="profiling aid: run a plain device copy of MIB MiB three times (HBM counter calibration)")
     return ap.parse_args()
+
+
+def calibrate_copy(mib):
+    """A plain elementwise copy (read n bytes, write n bytes) of known size,
+    the yardstick the FETCH_SIZE / WRITE_SIZE counters are scaled by."""
+    import torch
+    n = mib << 20
+    src = torch.ones(n // 4, dtype=torch.int32, device="cuda:0")
+    dst = torch.empty_like(src)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        torch.add(src, 0, out=dst)
+    torch.cuda.synchronize()
+    print(json.dumps({"calibrate_copy_bytes_read": n, "calibrate_copy_bytes_written": n, "launches": 3}), flush=True)
 
 
 def make_workload(name):
@@ -94,8 +131,9 @@ def cpu_baseline(wl, pairs_total, target_s):
     I = wl["intents"].shape[0]
     stride = 4096
     t, sp = run(stride)
-    while t < target_s / 8 and stride > 1:
-        stride = max(1, int(stride / max(2.0, min(64.0, target_s / max(t, 1e-3) / 2))))
+    # shrink the stride (at most 64x per probe) until the sample takes about target_s
+    while t < target_s / 2 and stride > 1:
+        stride = max(1, stride // 64, int(stride * max(t, 1e-3) / target_s))
         t, sp = run(stride)
     frac = sp["intents"].shape[0] / I
     est_full = t / frac
@@ -118,6 +156,10 @@ def main():
         print(f"bench.py measures one GPU only (the check shards by intent with no exchange; see DESIGN.md); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
+
+    if args.calibrate_copy:
+        calibrate_copy(args.calibrate_copy)
+        return
 
     import torch
     import paper_2602_16100_amd as pc
@@ -228,7 +270,7 @@ def main():
                               "pc_masked_reach": ktime("k_rc_"), "pc_report": ktime("k_report")},
         "per_kernel": per_kernel,
         "roofline": {"kernel": roof_kernel, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": None,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.workload),
                      "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": avg_eval_ms},
         "verdict": {"passed": passed, "intents": I},
         "data_error_flags": flags,
