@@ -40,7 +40,8 @@ constexpr int kPlaneWords = kChunks * 16;  // words per 32-rule group
 constexpr int kMatchWaves = 8;
 constexpr int kMatchThreads = kMatchWaves * 64;
 constexpr int kSliceGroups = kMatchThreads;  // one group (32 rules) per lane
-constexpr int kTile = 2048;                  // lookups per LDS tile
+constexpr int kTile = 1024;                  // lookups per LDS tile
+constexpr int kQueue = 512;                  // queued filter survivors per wavefront (>= 4 x 64)
 constexpr int kPrepGroups = 32;              // groups per prep workgroup (1024 threads, 2 groups per wave)
 constexpr uint64_t kNoMatch = ~0ull;
 
@@ -158,8 +159,8 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
 
 __global__ void k_tr_init(int32_t S, const uint8_t *__restrict__ jur, const int32_t *__restrict__ ingress, int32_t T,
                           int32_t *__restrict__ cur, uint32_t *__restrict__ jm, int32_t *__restrict__ hops,
-                          int32_t *__restrict__ live, int32_t *__restrict__ nlive, int32_t *__restrict__ counts,
-                          pc_trace_out *__restrict__ out, uint32_t *__restrict__ d_err)
+                          int32_t *__restrict__ rank, int32_t *__restrict__ live, int32_t *__restrict__ nlive,
+                          int32_t *__restrict__ counts, pc_trace_out *__restrict__ out, uint32_t *__restrict__ d_err)
 {
     bool bad = false;
     for (int32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < T; t += gridDim.x * blockDim.x) {
@@ -178,20 +179,22 @@ __global__ void k_tr_init(int32_t S, const uint8_t *__restrict__ jur, const int3
         cur[t] = s;
         jm[t] = jur_bit(jur, s);
         hops[t] = 0;
+        rank[t] = atomicAdd(&counts[s], 1);
         live[atomicAdd(nlive, 1)] = t;
-        atomicAdd(&counts[s], 1);
     }
     if (bad) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
+// Bucket the live traces by current switch: trace t goes to slot
+// boff[cur[t]] + rank[t], its rank having been taken when it was counted.
 __global__ void k_tr_scatter(const int32_t *__restrict__ live, const int32_t *__restrict__ nlive,
-                             const int32_t *__restrict__ cur, int32_t *__restrict__ cursor,
-                             int32_t *__restrict__ bucket)
+                             const int32_t *__restrict__ cur, const int32_t *__restrict__ rank,
+                             const int32_t *__restrict__ boff, int32_t *__restrict__ bucket)
 {
     const int32_t n = *nlive;
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
         const int32_t t = live[i];
-        bucket[atomicAdd(&cursor[cur[t]], 1)] = t;
+        bucket[boff[cur[t]] + rank[t]] = t;
     }
 }
 
@@ -217,72 +220,6 @@ __device__ __forceinline__ void verify_group(uint32_t surv, const pc_rule *grp, 
         const pc_rule *r = grp + bit;
         if (rule_matches(r, h.w[0], h.w[1], h.w[2], h.w[3]))
             atomicMin(best, static_cast<unsigned long long>(rule_key(r, local0 + bit)));
-    }
-}
-
-__global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
-    const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
-    const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt, const pc_key *__restrict__ hdr,
-    const int32_t *__restrict__ boff, const int32_t *__restrict__ bucket, uint64_t *__restrict__ bestkey)
-{
-    __shared__ uint64_t best[kTile];
-    __shared__ __align__(16) uint32_t h2s[kTile];
-    __shared__ int32_t tids[kTile];
-    const int32_t s = blockIdx.x;
-    const int32_t bb = boff[s], be = boff[s + 1];
-    if (bb >= be) return;
-    const int lane = threadIdx.x & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int32_t G = gcount[s];
-    const int64_t rb = rule_off[s];
-    const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
-    const int32_t nslices = max(1, (G + kSliceGroups - 1) / kSliceGroups);
-    // slice-major: each lane's chunk sets are loaded once per slice; the
-    // running best of every lookup is carried in bestkey between slices
-    for (int32_t sl = 0; sl < nslices; ++sl) {
-        const int32_t g = sl * kSliceGroups + wave * 64 + lane;
-        v16u F[kChunks];
-#pragma unroll
-        for (int c = 0; c < kChunks; ++c)
-#pragma unroll
-            for (int x = 0; x < 16; ++x) F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * G + g] : 0u;
-        const pc_rule *grp = rules + rb + static_cast<int64_t>(g) * 32;
-        for (int32_t t0 = bb; t0 < be; t0 += kTile) {
-            const int32_t tn = min(kTile, be - t0);
-            for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
-                const int32_t t = bucket[t0 + i];
-                tids[i] = t;
-                h2s[i] = hdr[t].w[2];
-                best[i] = sl == 0 ? kNoMatch : bestkey[t];
-            }
-            __syncthreads();
-            for (int32_t j0 = 0; j0 < tn; j0 += 4) {
-                const uint4 h4 = *reinterpret_cast<const uint4 *>(&h2s[j0]);
-                const uint32_t hv[4] = {h4.x, h4.y, h4.z, h4.w};
-                uint32_t sv[4];
-#pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const uint32_t h2 = __builtin_amdgcn_readfirstlane(hv[k]);
-                    uint32_t surv = F[0][h2 & 15u];
-#pragma unroll
-                    for (int c = 1; c < kChunks; ++c) surv &= F[c][(h2 >> (4 * c)) & 15u];
-                    sv[k] = j0 + k < tn ? surv : 0u;
-                }
-                if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        if (sv[k]) {
-                            const pc_key h = hdr[tids[j0 + k]];
-                            verify_group(sv[k], grp, static_cast<uint32_t>(g) * 32, h,
-                                         reinterpret_cast<unsigned long long *>(&best[j0 + k]));
-                        }
-                    }
-                }
-            }
-            __syncthreads();
-            for (int i = threadIdx.x; i < tn; i += kMatchThreads) bestkey[tids[i]] = best[i];
-            __syncthreads();
-        }
     }
 }
 
@@ -320,6 +257,148 @@ __device__ __forceinline__ void write_out(pc_trace_out *out, int32_t t, uint32_t
     o.hops = static_cast<uint8_t>(hops);
     o.state = static_cast<uint8_t>(state);
     out[t] = o;
+}
+
+// Per-trace state of the level loop and where a level's results go.
+struct Level {
+    int32_t S;
+    const int32_t *port_off;
+    const int32_t *port_peer;
+    int64_t n_ports;
+    const uint8_t *jur;
+    int32_t ttl;
+    int32_t *cur;
+    uint32_t *jm;
+    int32_t *hops;
+    int32_t *rank;          // slot of the trace within its next switch's bucket
+    int32_t *live_next;     // traces still in flight after this level
+    int32_t *nlive_next;
+    int32_t *counts_next;   // live traces per switch after this level
+    pc_trace_out *out;
+};
+
+__global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
+    const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
+    const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt, const pc_key *__restrict__ hdr,
+    const int32_t *__restrict__ boff, const int32_t *__restrict__ bucket, Level lv)
+{
+    __shared__ uint64_t best[kTile];
+    __shared__ __align__(16) uint32_t h2s[kTile];
+    __shared__ __align__(16) pc_key keys[kTile];
+    __shared__ int32_t tids[kTile];
+    __shared__ uint2 queue[kMatchWaves][kQueue];  // per wavefront: (survivor set, lookup << 6 | lane)
+    const int32_t s = blockIdx.x;
+    const int32_t bb = boff[s], be = boff[s + 1];
+    if (bb >= be) return;
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int32_t G = gcount[s];
+    const int64_t rb = rule_off[s];
+    const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
+    const int32_t nslices = max(1, (G + kSliceGroups - 1) / kSliceGroups);
+    uint2 *q = queue[wave];
+    for (int32_t t0 = bb; t0 < be; t0 += kTile) {
+        const int32_t tn = min(kTile, be - t0);
+        for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
+            const int32_t t = bucket[t0 + i];
+            const pc_key h = hdr[t];
+            tids[i] = t;
+            keys[i] = h;
+            h2s[i] = h.w[2];
+            best[i] = kNoMatch;
+        }
+        __syncthreads();
+        // one slice of kSliceGroups groups at a time, one group per lane,
+        // its chunk sets held in VGPRs while the tile's lookups stream past
+        for (int32_t sl = 0; sl < nslices; ++sl) {
+            const int32_t g = sl * kSliceGroups + wave * 64 + lane;
+            const int32_t gw = sl * kSliceGroups + wave * 64;  // group of lane 0
+            // Filter phase: survivors of the chunk filter are queued (per
+            // wavefront) until the queue could overflow.  Verify phase: the
+            // queued survivors are checked against their full rules, 64 at a
+            // time, with the chunk sets dead.  Then filtering resumes.  A quad
+            // of lookups queues at most 256 entries, so every round advances.
+            for (int32_t jr = 0; jr < tn;) {
+                // an opaque copy of G keeps the 96 load addresses from being
+                // hoisted out of the loops (and spilled) as invariants
+                int32_t Gr = G;
+                asm volatile("" : "+s"(Gr));
+                v16u F[kChunks];
+#pragma unroll
+                for (int c = 0; c < kChunks; ++c)
+#pragma unroll
+                    for (int x = 0; x < 16; ++x) F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * Gr + g] : 0u;
+                int32_t qn = 0;
+                int32_t j0 = jr;
+                for (; j0 < tn; j0 += 4) {
+                    const uint4 h4 = *reinterpret_cast<const uint4 *>(&h2s[j0]);
+                    const uint32_t hv[4] = {h4.x, h4.y, h4.z, h4.w};
+                    uint32_t sv[4];
+#pragma unroll
+                    for (int k = 0; k < 4; ++k) {
+                        const uint32_t h2 = __builtin_amdgcn_readfirstlane(hv[k]);
+                        uint32_t surv = F[0][h2 & 15u];
+#pragma unroll
+                        for (int c = 1; c < kChunks; ++c) surv &= F[c][(h2 >> (4 * c)) & 15u];
+                        sv[k] = (j0 + k < tn && g < G) ? surv : 0u;
+                    }
+                    if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
+                        uint64_t m[4];
+                        int32_t n = 0;
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            m[k] = __ballot(sv[k] != 0);
+                            n += __popcll(m[k]);
+                        }
+                        if (qn + n > kQueue) break;  // resume at this quad after verifying
+#pragma unroll
+                        for (int k = 0; k < 4; ++k) {
+                            if (sv[k]) {
+                                const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+                                    static_cast<uint32_t>(m[k] >> 32),
+                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m[k]), 0u));
+                                q[qn + below] = make_uint2(sv[k], static_cast<uint32_t>(j0 + k) << 6 | lane);
+                            }
+                            qn += __popcll(m[k]);
+                        }
+                    }
+                }
+                jr = j0;
+                // the queue entries were written by other lanes of this wavefront
+                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+                __builtin_amdgcn_wave_barrier();
+                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+                for (int32_t e = lane; e < qn; e += 64) {
+                    const uint2 en = q[e];
+                    const int32_t j = static_cast<int32_t>(en.y >> 6);
+                    const int32_t gg = gw + static_cast<int32_t>(en.y & 63u);
+                    verify_group(en.x, rules + rb + static_cast<int64_t>(gg) * 32, static_cast<uint32_t>(gg) * 32,
+                                 keys[j], reinterpret_cast<unsigned long long *>(&best[j]));
+                }
+                __builtin_amdgcn_wave_barrier();
+            }
+        }
+        __syncthreads();
+        // apply the first match, then count and list the traces that move on
+        for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
+            const int32_t t = tids[i];
+            const int32_t h = lv.hops[t];
+            int32_t next = -1;
+            uint16_t port = PC_NO_PORT;
+            const int state = apply_rule(lv.S, lv.port_off, lv.port_peer, lv.n_ports, rule_off, rules, lv.ttl, s,
+                                         best[i], h, &next, &port);
+            if (state >= 0) {
+                write_out(lv.out, t, lv.jm[t], s, port, h, state);
+            } else {
+                lv.cur[t] = next;
+                lv.hops[t] = h + 1;
+                lv.jm[t] |= jur_bit(lv.jur, next);
+                lv.rank[t] = atomicAdd(&lv.counts_next[next], 1);
+                lv.live_next[atomicAdd(lv.nlive_next, 1)] = t;
+            }
+        }
+        __syncthreads();
+    }
 }
 
 // Sparse tail: one workgroup per trace still in flight walks it to its end,
@@ -376,34 +455,6 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
     }
 }
 
-__global__ void k_tr_advance(int32_t S, const int32_t *__restrict__ port_off, const int32_t *__restrict__ port_peer,
-                             int64_t n_ports, const uint8_t *__restrict__ jur, const int32_t *__restrict__ rule_off,
-                             const pc_rule *__restrict__ rules, int32_t ttl, const int32_t *__restrict__ live,
-                             const int32_t *__restrict__ nlive, const uint64_t *__restrict__ bestkey,
-                             int32_t *__restrict__ cur, uint32_t *__restrict__ jm, int32_t *__restrict__ hops,
-                             int32_t *__restrict__ live_next, int32_t *__restrict__ nlive_next,
-                             int32_t *__restrict__ counts_next, pc_trace_out *__restrict__ out)
-{
-    const int32_t n = *nlive;
-    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-        const int32_t t = live[i];
-        const int32_t s = cur[t];
-        int32_t next = -1;
-        uint16_t port = PC_NO_PORT;
-        const int state =
-            apply_rule(S, port_off, port_peer, n_ports, rule_off, rules, ttl, s, bestkey[t], hops[t], &next, &port);
-        if (state >= 0) {
-            write_out(out, t, jm[t], s, port, hops[t], state);
-        } else {
-            cur[t] = next;
-            hops[t] += 1;
-            jm[t] |= jur_bit(jur, next);
-            live_next[atomicAdd(nlive_next, 1)] = t;
-            atomicAdd(&counts_next[next], 1);
-        }
-    }
-}
-
 unsigned grid_for(int64_t n, int threads)
 {
     int64_t b = (n + threads - 1) / threads;
@@ -419,10 +470,9 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
               hipStream_t stream)
 {
     struct Bufs {
-        int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *cursor;
-        int32_t *cur, *hops, *live0, *live1, *bucket;
+        int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff;
+        int32_t *cur, *hops, *rank, *live0, *live1, *bucket;
         uint32_t *jm, *filt;
-        uint64_t *bestkey;
     } B;
     auto carve = [&](Carver &c) {
         B.gcount = c.take<int32_t>(S + 1);
@@ -432,14 +482,13 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         B.counts0 = c.take<int32_t>(S + 1);
         B.counts1 = c.take<int32_t>(S + 1);
         B.boff = c.take<int32_t>(S + 1);
-        B.cursor = c.take<int32_t>(S + 1);
         B.cur = c.take<int32_t>(T + 1);
         B.hops = c.take<int32_t>(T + 1);
+        B.rank = c.take<int32_t>(T + 1);
         B.live0 = c.take<int32_t>(T + 1);
         B.live1 = c.take<int32_t>(T + 1);
         B.bucket = c.take<int32_t>(T + 1);
         B.jm = c.take<uint32_t>(T + 1);
-        B.bestkey = c.take<uint64_t>(T + 1);
     };
     Carver dry{nullptr, 0};
     carve(dry);
@@ -489,7 +538,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), S + 1, 0, stream);
     }
     PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(grid_for(T, 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
-                       B.hops, B.live0, d_n, B.counts0, out, ctx->d_err));
+                       B.hops, B.rank, B.live0, d_n, B.counts0, out, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
@@ -513,15 +562,16 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_LAUNCH_CHECK(ctx);
             break;
         }
-        launch_scan_i32(cnt_cur, S, B.boff, B.cursor, cnt_cur, stream);
-        PC_TIMED(ctx, "k_tr_scatter", stream, hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, B.cur,
-                           B.cursor, B.bucket));
-        PC_TIMED(ctx, "k_tr_match", stream, hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(S)), dim3(kMatchThreads), 0, stream, rule_off, rules,
-                           B.gcount, B.gofs, B.filt, hdr, B.boff, B.bucket, B.bestkey));
+        launch_scan_i32(cnt_cur, S, B.boff, nullptr, cnt_cur, stream);
+        PC_TIMED(ctx, "k_tr_scatter", stream,
+                 hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur,
+                                    B.cur, B.rank, B.boff, B.bucket));
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
-        PC_TIMED(ctx, "k_tr_advance", stream, hipLaunchKernelGGL(k_tr_advance, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, S, port_off, port_peer,
-                           n_ports, jur, rule_off, rules, ttl, live_cur, n_cur, B.bestkey, B.cur, B.jm, B.hops,
-                           live_nxt, n_nxt, cnt_nxt, out));
+        const Level lv{S, port_off, port_peer, n_ports, jur, ttl, B.cur, B.jm, B.hops, B.rank, live_nxt, n_nxt, cnt_nxt,
+                       out};
+        PC_TIMED(ctx, "k_tr_match", stream,
+                 hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(S)), dim3(kMatchThreads), 0, stream, rule_off,
+                                    rules, B.gcount, B.gofs, B.filt, hdr, B.boff, B.bucket, lv));
         PC_LAUNCH_CHECK(ctx);
         PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, n_nxt, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
         PC_HIP(ctx, hipStreamSynchronize(stream));
