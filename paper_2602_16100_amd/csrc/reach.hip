@@ -10,12 +10,14 @@
 // subgraph, -1 when unreachable or when the source is not allowed.
 //
 // Design (gfx950):
-//   bitset : graphs that fit in LDS (25 bytes per vertex): 64 queries per
+//   bitset : graphs that fit in LDS (27 bytes per vertex): 64 queries per
 //            workgroup, one bit each, level-synchronous frontier bitsets
-//            (visited / frontier / next) in LDS, push expansion with 64-bit
-//            LDS atomic OR, the per-query allowed mask applied per vertex as
-//            a precomputed 64-bit region mask; stops when every query's
-//            target is resolved or no frontier bit is left.
+//            (visited / frontier / next) in LDS, push expansion of a
+//            compacted frontier list (a few lanes per vertex, coalesced
+//            adjacency reads) with 64-bit LDS atomic OR, the per-query
+//            allowed mask applied per vertex as a precomputed 64-bit region
+//            mask; stops when every query's target is resolved or no
+//            frontier bit is left.
 //   queue  : larger graphs: one workgroup per query, frontier queue in
 //            scratch, the distance row itself (or a scratch row, with
 //            targets) as the visited set claimed with compare-and-swap.
@@ -25,8 +27,7 @@ namespace {
 
 constexpr int kBitsetThreads = 512;
 constexpr int kQueueThreads = 256;
-constexpr int kMaxBitsetV = 6144;  // 3 x 8 B + 1 B per vertex, plus masks, within 160 KB of LDS
-constexpr int kAdjBatch = 8;       // adjacency loads in flight per thread
+constexpr int kMaxBitsetV = 6016;  // 3 x 8 B + 1 B + 2 B per vertex, plus masks, within 160 KB of LDS
 
 __device__ __forceinline__ bool allowed_v(const uint8_t *region, uint32_t A, int32_t v)
 {
@@ -58,6 +59,12 @@ __global__ void k_rc_validate(int32_t V, const int32_t *__restrict__ adj_off, co
 }
 
 // 64 queries per workgroup; dist is [Q][V] (target == nullptr) or [Q].
+// Each level pushes the frontier along its edges: the frontier vertices are
+// kept as a list in LDS and GS lanes share one vertex's adjacency, so the
+// adjacency loads are coalesced and the vertex's frontier word is a
+// broadcast; the next frontier is built (and the list rewritten) in one
+// pass over the vertices.
+template <int GS>
 __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const int32_t *__restrict__ adj_off,
                                                               const int32_t *__restrict__ adj, int64_t n_adj,
                                                               const uint8_t *__restrict__ region, int32_t Q,
@@ -70,9 +77,11 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     uint64_t *vis = lds;
     uint64_t *fr = vis + V;
     uint64_t *nx = fr + V;
-    uint64_t *rmask = nx + V;  // [32]
-    uint8_t *reg = reinterpret_cast<uint8_t *>(rmask + 32);  // [V]
-    __shared__ int flag_any, flag_done;
+    uint64_t *rmask = nx + V;                                               // [32]
+    uint8_t *reg = reinterpret_cast<uint8_t *>(rmask + 32);                 // [V]
+    uint16_t *flist = reinterpret_cast<uint16_t *>(reg + ((V + 3) & ~3));  // [V] frontier vertices
+    __shared__ int32_t nfr[2];                                              // list lengths, by level parity
+    __shared__ int flag_done;
     const int tid = threadIdx.x, lane = tid & 63;
     const int32_t q0 = blockIdx.x * 64;
     const int32_t nq = min(64, Q - q0);
@@ -89,6 +98,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
             if (lane == 0) rmask[r] = m;
         }
     }
+    if (tid == 0) nfr[0] = nfr[1] = 0;
     __syncthreads();
     // sources; per-query result state lives in wave 0, lane = query
     int32_t res = -1, tgt = -1;
@@ -108,33 +118,33 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         }
     }
     __syncthreads();
+    for (int32_t v = tid; v < V; v += kBitsetThreads)
+        if (fr[v]) flist[atomicAdd(&nfr[0], 1)] = static_cast<uint16_t>(v);
     if (tid < 64 && !done && ((vis[tgt] >> lane) & 1)) {
         res = 0;
         done = true;
     }
+    __syncthreads();
+    const int grp = tid / GS, gl = tid % GS;
     for (int32_t d = 1;; ++d) {
-        if (tid == 0) flag_any = 0;
-        // push the frontier along every edge, kAdjBatch neighbour loads at a time
-        for (int32_t u = tid; u < V; u += kBitsetThreads) {
+        const int cur = (d - 1) & 1;
+        const int32_t nf = nfr[cur];
+        if (tid == 0) nfr[cur ^ 1] = 0;  // last read at the start of the previous level
+        for (int32_t i = grp; i < nf; i += kBitsetThreads / GS) {
+            const int32_t u = flist[i];
             const uint64_t f = fr[u];
-            if (!f) continue;
             const int64_t b = adj_off[u], e = adj_off[u + 1];
             if (!pc_range_ok(b, e, n_adj)) continue;
-            for (int64_t p0 = b; p0 < e; p0 += kAdjBatch) {
-                int32_t nb[kAdjBatch];
-#pragma unroll
-                for (int k = 0; k < kAdjBatch; ++k) nb[k] = p0 + k < e ? adj[p0 + k] : -1;
-#pragma unroll
-                for (int k = 0; k < kAdjBatch; ++k)
-                    if (nb[k] >= 0 && nb[k] < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[nb[k]]), f);
+            for (int64_t p = b + gl; p < e; p += GS) {
+                const int32_t v = adj[p];
+                if (v >= 0 && v < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[v]), f);
             }
         }
         __syncthreads();
-        bool any = false;
         for (int32_t v = tid; v < V; v += kBitsetThreads) {
             uint64_t n = nx[v];
-            nx[v] = 0;
             if (n) {
+                nx[v] = 0;
                 const uint32_t r = reg[v];
                 n &= (r < 32 ? rmask[r] : 0ull) & ~vis[v];
                 vis[v] |= n;
@@ -148,9 +158,8 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                 }
             }
             fr[v] = n;
-            any |= n != 0;
+            if (n) flist[atomicAdd(&nfr[cur ^ 1], 1)] = static_cast<uint16_t>(v);
         }
-        if (any) flag_any = 1;
         __syncthreads();
         if (tid < 64) {
             if (!done && ((fr[tgt] >> lane) & 1)) {
@@ -161,9 +170,9 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
             if (tid == 0) flag_done = target ? all_done : 0;
         }
         __syncthreads();
-        const bool stop = !flag_any || flag_done;
-        __syncthreads();
-        if (stop) break;
+        // nfr[cur ^ 1] is reset only two levels on; flag_done is rewritten
+        // only after the next level's second barrier
+        if (nfr[cur ^ 1] == 0 || flag_done) break;
     }
     if (target && tid < 64 && lane < nq) dist[q0 + lane] = res;
 }
@@ -249,14 +258,27 @@ int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
     }
     int max_lds = 0;
     PC_HIP(ctx, hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, ctx->device));
-    const size_t lds = static_cast<size_t>(V) * (3 * 8 + 1) + 32 * 8;
+    // visited / frontier / next (8 B each), region (1 B) and list (2 B) per vertex
+    const size_t lds = static_cast<size_t>(V) * 3 * 8 + 32 * 8 + ((static_cast<size_t>(V) + 3) & ~size_t(3)) +
+                       static_cast<size_t>(V) * 2;
     if (V <= kMaxBitsetV && lds + 64 <= static_cast<size_t>(max_lds)) {
-        PC_HIP(ctx, hipFuncSetAttribute(reinterpret_cast<const void *>(k_rc_bitset),
-                                        hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
-        PC_TIMED(ctx, "k_rc_bitset", stream, hipLaunchKernelGGL(k_rc_bitset, dim3(static_cast<unsigned>((Q + 63) / 64)), dim3(kBitsetThreads), lds, stream,
-                           V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist));
-        PC_LAUNCH_CHECK(ctx);
-        return PC_OK;
+        // lanes per frontier vertex: a power of two near a third of the mean degree
+        const int64_t avg = n_adj / V;
+        const int gs = avg <= 12 ? 4 : avg <= 24 ? 8 : avg <= 48 ? 16 : 32;
+        const dim3 grid_b(static_cast<unsigned>((Q + 63) / 64));
+        auto launch = [&](auto kern) -> int {
+            PC_HIP(ctx, hipFuncSetAttribute(reinterpret_cast<const void *>(kern),
+                                            hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+            PC_TIMED(ctx, "k_rc_bitset", stream,
+                     hipLaunchKernelGGL(kern, grid_b, dim3(kBitsetThreads), lds, stream, V, adj_off, adj, n_adj,
+                                        region, Q, src, allowed, target, dist));
+            PC_LAUNCH_CHECK(ctx);
+            return PC_OK;
+        };
+        if (gs == 4) return launch(k_rc_bitset<4>);
+        if (gs == 8) return launch(k_rc_bitset<8>);
+        if (gs == 16) return launch(k_rc_bitset<16>);
+        return launch(k_rc_bitset<32>);
     }
     int32_t grid = Q < 256 ? Q : 256;
     int32_t *qbuf, *rows;

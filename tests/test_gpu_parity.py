@@ -192,12 +192,20 @@ def test_reach_small_graph_bitset(g, orc, full_rows):
     _check_workload(g, orc, wl)
 
 
-@pytest.mark.parametrize("V", [700, 1500, 2900, 4000, 5500, 6144])
-def test_reach_bitset_vertex_ownership(g, orc, V):
-    """Every per-thread vertex-ownership width of the bitset BFS (1..6
-    vertices per thread), target mode and full rows."""
+@pytest.mark.parametrize("V", [700, 1500, 2900, 4000, 5500, 6016, 6200])
+def test_reach_bitset_sizes(g, orc, V):
+    """The bitset BFS up to its largest LDS-resident graph (6,016 vertices)
+    and just past it (the queue path), target mode and full rows."""
     for full_rows in (False, True):
         wl = synth.rgg_workload(V, V, 8, 130, mean_degree=7.0, full_rows=full_rows)
+        _check_workload(g, orc, wl)
+
+
+@pytest.mark.parametrize("deg", [7.0, 20.0, 40.0, 80.0])
+def test_reach_bitset_lane_groups(g, orc, deg):
+    """Mean degrees that select 4, 8, 16 and 32 lanes per frontier vertex."""
+    for full_rows in (False, True):
+        wl = synth.rgg_workload(int(deg), 1500, 8, 150, mean_degree=deg, full_rows=full_rows)
         _check_workload(g, orc, wl)
 
 
