@@ -31,6 +31,8 @@
 //            header selects.
 #include <stdlib.h>
 
+#include <algorithm>
+
 #include "pc_internal.h"
 
 namespace {
@@ -40,10 +42,12 @@ constexpr int kPlaneWords = kChunks * 16;  // words per 32-rule group
 constexpr int kMatchWaves = 8;
 constexpr int kMatchThreads = kMatchWaves * 64;
 constexpr int kSliceGroups = kMatchThreads;  // one group (32 rules) per lane
-constexpr int kTile = 1024;                  // lookups per LDS tile
+constexpr int kChunk = 256;                  // lookups per match work item (a multiple of 4, <= kMatchThreads)
 constexpr int kQueue = 512;                  // queued filter survivors per wavefront (>= 4 x 64)
 constexpr int kPrepGroups = 32;              // groups per prep workgroup (1024 threads, 2 groups per wave)
 constexpr uint64_t kNoMatch = ~0ull;
+static_assert(kChunk % 4 == 0 && kChunk <= kMatchThreads, "one epilogue thread per lookup");
+constexpr int kCountPad = 32;  // live-trace counters are 128 bytes apart: contended atomics on one line serialise
 
 // 16 chunk-value sets of one 4-bit chunk, kept in VGPRs; indexed with a
 // wave-uniform value this lowers to register-indexed moves (s_set_gpr_idx).
@@ -157,13 +161,21 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
     }
 }
 
-__global__ void k_tr_init(int32_t S, const uint8_t *__restrict__ jur, const int32_t *__restrict__ ingress, int32_t T,
-                          int32_t *__restrict__ cur, uint32_t *__restrict__ jm, int32_t *__restrict__ hops,
-                          int32_t *__restrict__ rank, int32_t *__restrict__ live, int32_t *__restrict__ nlive,
-                          int32_t *__restrict__ counts, pc_trace_out *__restrict__ out, uint32_t *__restrict__ d_err)
+__global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__restrict__ jur,
+                                                 const int32_t *__restrict__ ingress, int32_t T,
+                                                 int32_t *__restrict__ cur, uint32_t *__restrict__ jm,
+                                                 int32_t *__restrict__ hops, int32_t *__restrict__ rank,
+                                                 int32_t *__restrict__ live, int32_t *__restrict__ nlive,
+                                                 int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
+                                                 uint32_t *__restrict__ d_err)
 {
+    __shared__ int32_t nloc, base;
+    if (threadIdx.x == 0) nloc = 0;
+    __syncthreads();
+    const int32_t t = blockIdx.x * 256 + threadIdx.x;
+    int32_t slot = -1;
     bool bad = false;
-    for (int32_t t = blockIdx.x * blockDim.x + threadIdx.x; t < T; t += gridDim.x * blockDim.x) {
+    if (t < T) {
         const int32_t s = ingress[t];
         if (s < 0 || s >= S) {
             bad = true;
@@ -174,27 +186,32 @@ __global__ void k_tr_init(int32_t S, const uint8_t *__restrict__ jur, const int3
             o.hops = 0;
             o.state = PC_MISS;
             out[t] = o;
-            continue;
+        } else {
+            cur[t] = s;
+            jm[t] = jur_bit(jur, s);
+            hops[t] = 0;
+            rank[t] = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
+            slot = atomicAdd(&nloc, 1);
         }
-        cur[t] = s;
-        jm[t] = jur_bit(jur, s);
-        hops[t] = 0;
-        rank[t] = atomicAdd(&counts[s], 1);
-        live[atomicAdd(nlive, 1)] = t;
     }
-    if (bad) atomicOr(d_err, PC_DERR_SWITCH);
+    __syncthreads();
+    if (threadIdx.x == 0) base = nloc ? atomicAdd(nlive, nloc) : 0;
+    __syncthreads();
+    if (slot >= 0) live[base + slot] = t;
+    if (__ballot(bad) && (threadIdx.x & 63) == 0) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
 // Bucket the live traces by current switch: trace t goes to slot
 // boff[cur[t]] + rank[t], its rank having been taken when it was counted.
-__global__ void k_tr_scatter(const int32_t *__restrict__ live, const int32_t *__restrict__ nlive,
+__global__ void k_tr_scatter(const int32_t *__restrict__ live, const int32_t *__restrict__ nlive, int32_t T,
                              const int32_t *__restrict__ cur, const int32_t *__restrict__ rank,
                              const int32_t *__restrict__ boff, int32_t *__restrict__ bucket)
 {
-    const int32_t n = *nlive;
+    const int32_t n = min(*nlive, T);
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
         const int32_t t = live[i];
-        bucket[boff[cur[t]] + rank[t]] = t;
+        const int32_t pos = boff[cur[t]] + rank[t];
+        if (pos >= 0 && pos < T) bucket[pos] = t;
     }
 }
 
@@ -262,6 +279,7 @@ __device__ __forceinline__ void write_out(pc_trace_out *out, int32_t t, uint32_t
 // Per-trace state of the level loop and where a level's results go.
 struct Level {
     int32_t S;
+    int32_t T;              // capacity of the live list
     const int32_t *port_off;
     const int32_t *port_peer;
     int64_t n_ports;
@@ -277,19 +295,98 @@ struct Level {
     pc_trace_out *out;
 };
 
-__global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
-    const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
-    const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt, const pc_key *__restrict__ hdr,
-    const int32_t *__restrict__ boff, const int32_t *__restrict__ bucket, Level lv)
+// Per level: bucket offsets boff = exclusive scan of counts (which are
+// cleared for reuse) and work-item offsets ioff = exclusive scan of
+// ceil(counts / kChunk); one workgroup of 1024 threads.
+__global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, int32_t S, int32_t *__restrict__ boff,
+                                                  int32_t *__restrict__ ioff)
 {
-    __shared__ uint64_t best[kTile];
-    __shared__ __align__(16) uint32_t h2s[kTile];
-    __shared__ __align__(16) pc_key keys[kTile];
-    __shared__ int32_t tids[kTile];
+    __shared__ int32_t wsum[2][16];
+    __shared__ int32_t carry_s[2];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    if (tid < 2) carry_s[tid] = 0;
+    __syncthreads();
+    for (int32_t base = 0; base < S; base += 1024) {
+        const int32_t i = base + tid;
+        const int32_t v0 = i < S ? counts[static_cast<int64_t>(i) * kCountPad] : 0;
+        const int32_t v1 = (v0 + kChunk - 1) / kChunk;
+        int32_t x0 = v0, x1 = v1;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t y0 = __shfl_up(x0, off, 64), y1 = __shfl_up(x1, off, 64);
+            if (lane >= off) {
+                x0 += y0;
+                x1 += y1;
+            }
+        }
+        if (lane == 63) {
+            wsum[0][wid] = x0;
+            wsum[1][wid] = x1;
+        }
+        __syncthreads();
+        if (wid < 2) {
+            int32_t w = lane < 16 ? wsum[wid][lane] : 0;
+#pragma unroll
+            for (int off = 1; off < 16; off <<= 1) {
+                const int32_t y = __shfl_up(w, off, 64);
+                if (lane >= off) w += y;
+            }
+            if (lane < 16) wsum[wid][lane] = w;
+        }
+        __syncthreads();
+        const int32_t c0 = carry_s[0], c1 = carry_s[1];
+        if (i < S) {
+            boff[i] = c0 + (wid ? wsum[0][wid - 1] : 0) + x0 - v0;
+            ioff[i] = c1 + (wid ? wsum[1][wid - 1] : 0) + x1 - v1;
+            counts[static_cast<int64_t>(i) * kCountPad] = 0;
+        }
+        __syncthreads();
+        if (tid == 0) {
+            carry_s[0] = c0 + wsum[0][15];
+            carry_s[1] = c1 + wsum[1][15];
+        }
+        __syncthreads();
+    }
+    if (tid == 0) {
+        boff[S] = carry_s[0];
+        ioff[S] = carry_s[1];
+    }
+}
+
+// One workgroup per work item = (switch, chunk of at most kChunk lookups of
+// its bucket).  Items are dealt to XCDs in contiguous ranges, so the chunks
+// of one switch share an L2.
+__global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
+    int32_t S, const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules,
+    const int32_t *__restrict__ gcount, const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
+    const pc_key *__restrict__ hdr, const int32_t *__restrict__ boff, const int32_t *__restrict__ ioff,
+    const int32_t *__restrict__ bucket, Level lv)
+{
+    __shared__ uint64_t best[kChunk];
+    __shared__ __align__(16) uint32_t cidx[kChunks][kChunk];  // chunk values of each lookup's header word 2
+    __shared__ __align__(16) pc_key keys[kChunk];
+    __shared__ int32_t tids[kChunk];
     __shared__ uint2 queue[kMatchWaves][kQueue];  // per wavefront: (survivor set, lookup << 6 | lane)
-    const int32_t s = blockIdx.x;
-    const int32_t bb = boff[s], be = boff[s + 1];
-    if (bb >= be) return;
+    // the grid was sized from an upper bound on the item count: blocks past
+    // the real count's per-XCD share return at once
+    const int32_t n_items = ioff[S];
+    const int32_t per = (n_items + 7) / 8;
+    const int32_t kx = static_cast<int32_t>(blockIdx.x >> 3);
+    if (kx >= per) return;
+    const int32_t item = static_cast<int32_t>(blockIdx.x & 7) * per + kx;
+    if (item >= n_items) return;
+    // switch owning the item: largest s with ioff[s] <= item
+    int32_t lo = 0, hi = S;
+    while (hi - lo > 1) {
+        const int32_t mid = (lo + hi) >> 1;
+        if (ioff[mid] <= item) lo = mid;
+        else hi = mid;
+    }
+    const int32_t s = lo;
+    const int32_t bb = boff[s] + (item - ioff[s]) * kChunk;
+    const int32_t tn = min(kChunk, min(boff[s + 1], lv.T) - bb);  // bucket holds at most T entries
+    if (tn <= 0) return;
+    const int32_t tn4 = (tn + 3) & ~3;
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
     const int32_t G = gcount[s];
@@ -297,108 +394,121 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
     const int32_t nslices = max(1, (G + kSliceGroups - 1) / kSliceGroups);
     uint2 *q = queue[wave];
-    for (int32_t t0 = bb; t0 < be; t0 += kTile) {
-        const int32_t tn = min(kTile, be - t0);
-        for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
-            const int32_t t = bucket[t0 + i];
-            const pc_key h = hdr[t];
-            tids[i] = t;
-            keys[i] = h;
-            h2s[i] = h.w[2];
-            best[i] = kNoMatch;
-        }
-        __syncthreads();
-        // one slice of kSliceGroups groups at a time, one group per lane,
-        // its chunk sets held in VGPRs while the tile's lookups stream past
-        for (int32_t sl = 0; sl < nslices; ++sl) {
-            const int32_t g = sl * kSliceGroups + wave * 64 + lane;
-            const int32_t gw = sl * kSliceGroups + wave * 64;  // group of lane 0
-            // Filter phase: survivors of the chunk filter are queued (per
-            // wavefront) until the queue could overflow.  Verify phase: the
-            // queued survivors are checked against their full rules, 64 at a
-            // time, with the chunk sets dead.  Then filtering resumes.  A quad
-            // of lookups queues at most 256 entries, so every round advances.
-            for (int32_t jr = 0; jr < tn;) {
-                // an opaque copy of G keeps the 96 load addresses from being
-                // hoisted out of the loops (and spilled) as invariants
-                int32_t Gr = G;
-                asm volatile("" : "+s"(Gr));
-                v16u F[kChunks];
+    // stage the chunk; pad to a multiple of 4 lookups with copies of the last
+    for (int i = threadIdx.x; i < tn4; i += kMatchThreads) {
+        int32_t t = bucket[bb + min(i, tn - 1)];
+        if (static_cast<uint32_t>(t) >= static_cast<uint32_t>(lv.T)) t = -1;  // not a trace id: skipped
+        pc_key h = {};
+        if (t >= 0) h = hdr[t];
+        tids[i] = t;
+        keys[i] = h;
+        best[i] = kNoMatch;
 #pragma unroll
-                for (int c = 0; c < kChunks; ++c)
+        for (int c = 0; c < kChunks; ++c) cidx[c][i] = (h.w[2] >> (4 * c)) & 15u;
+    }
+    __syncthreads();
+    // one slice of kSliceGroups groups at a time, one group per lane,
+    // its chunk sets held in VGPRs while the chunk's lookups stream past
+    for (int32_t sl = 0; sl < nslices; ++sl) {
+        const int32_t g = sl * kSliceGroups + wave * 64 + lane;
+        const int32_t gw = sl * kSliceGroups + wave * 64;  // group of lane 0
+        // Filter phase: survivors of the chunk filter are queued (per
+        // wavefront) until the queue could overflow.  Verify phase: the
+        // queued survivors are checked against their full rules, 64 at a
+        // time, with the chunk sets dead.  Then filtering resumes.  A quad
+        // of lookups queues at most 256 entries, so every round advances.
+        for (int32_t jr = 0; jr < tn4;) {
+            // an opaque copy of G keeps the 96 load addresses from being
+            // hoisted out of the loops (and spilled) as invariants
+            int32_t Gr = G;
+            asm volatile("" : "+s"(Gr));
+            v16u F[kChunks];
 #pragma unroll
-                    for (int x = 0; x < 16; ++x) F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * Gr + g] : 0u;
-                int32_t qn = 0;
-                int32_t j0 = jr;
-                for (; j0 < tn; j0 += 4) {
-                    const uint4 h4 = *reinterpret_cast<const uint4 *>(&h2s[j0]);
-                    const uint32_t hv[4] = {h4.x, h4.y, h4.z, h4.w};
-                    uint32_t sv[4];
+            for (int c = 0; c < kChunks; ++c)
+#pragma unroll
+                for (int x = 0; x < 16; ++x) F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * Gr + g] : 0u;
+            int32_t qn = 0;
+            int32_t j0 = jr;
+            for (; j0 < tn4; j0 += 4) {
+                uint4 X[kChunks];
+#pragma unroll
+                for (int c = 0; c < kChunks; ++c) X[c] = reinterpret_cast<const uint4 *>(cidx[c])[j0 >> 2];
+                uint32_t sv[4];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    uint32_t surv = ~0u;
+#pragma unroll
+                    for (int c = 0; c < kChunks; ++c) {
+                        const uint32_t xv = k == 0 ? X[c].x : k == 1 ? X[c].y : k == 2 ? X[c].z : X[c].w;
+                        surv &= F[c][__builtin_amdgcn_readfirstlane(xv)];
+                    }
+                    sv[k] = surv;
+                }
+                if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
+                    uint64_t m[4];
+                    int32_t n = 0;
 #pragma unroll
                     for (int k = 0; k < 4; ++k) {
-                        const uint32_t h2 = __builtin_amdgcn_readfirstlane(hv[k]);
-                        uint32_t surv = F[0][h2 & 15u];
-#pragma unroll
-                        for (int c = 1; c < kChunks; ++c) surv &= F[c][(h2 >> (4 * c)) & 15u];
-                        sv[k] = (j0 + k < tn && g < G) ? surv : 0u;
+                        m[k] = __ballot(sv[k] != 0);
+                        n += __popcll(m[k]);
                     }
-                    if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
-                        uint64_t m[4];
-                        int32_t n = 0;
+                    if (qn + n > kQueue) break;  // resume at this quad after verifying
 #pragma unroll
-                        for (int k = 0; k < 4; ++k) {
-                            m[k] = __ballot(sv[k] != 0);
-                            n += __popcll(m[k]);
+                    for (int k = 0; k < 4; ++k) {
+                        if (sv[k]) {
+                            const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+                                static_cast<uint32_t>(m[k] >> 32),
+                                __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m[k]), 0u));
+                            q[qn + below] = make_uint2(sv[k], static_cast<uint32_t>(j0 + k) << 6 | lane);
                         }
-                        if (qn + n > kQueue) break;  // resume at this quad after verifying
-#pragma unroll
-                        for (int k = 0; k < 4; ++k) {
-                            if (sv[k]) {
-                                const uint32_t below = __builtin_amdgcn_mbcnt_hi(
-                                    static_cast<uint32_t>(m[k] >> 32),
-                                    __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m[k]), 0u));
-                                q[qn + below] = make_uint2(sv[k], static_cast<uint32_t>(j0 + k) << 6 | lane);
-                            }
-                            qn += __popcll(m[k]);
-                        }
+                        qn += __popcll(m[k]);
                     }
                 }
-                jr = j0;
-                // the queue entries were written by other lanes of this wavefront
-                __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-                __builtin_amdgcn_wave_barrier();
-                __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-                for (int32_t e = lane; e < qn; e += 64) {
-                    const uint2 en = q[e];
-                    const int32_t j = static_cast<int32_t>(en.y >> 6);
-                    const int32_t gg = gw + static_cast<int32_t>(en.y & 63u);
-                    verify_group(en.x, rules + rb + static_cast<int64_t>(gg) * 32, static_cast<uint32_t>(gg) * 32,
-                                 keys[j], reinterpret_cast<unsigned long long *>(&best[j]));
-                }
-                __builtin_amdgcn_wave_barrier();
             }
+            jr = j0;
+            // the queue entries were written by other lanes of this wavefront
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+            for (int32_t e = lane; e < qn; e += 64) {
+                const uint2 en = q[e];
+                const int32_t j = static_cast<int32_t>(en.y >> 6);
+                const int32_t gg = gw + static_cast<int32_t>(en.y & 63u);
+                verify_group(en.x, rules + rb + static_cast<int64_t>(gg) * 32, static_cast<uint32_t>(gg) * 32,
+                             keys[j], reinterpret_cast<unsigned long long *>(&best[j]));
+            }
+            __builtin_amdgcn_wave_barrier();
         }
-        __syncthreads();
-        // apply the first match, then count and list the traces that move on
-        for (int i = threadIdx.x; i < tn; i += kMatchThreads) {
-            const int32_t t = tids[i];
+    }
+    __shared__ int32_t nmove, mbase;
+    if (threadIdx.x == 0) nmove = 0;
+    __syncthreads();
+    // apply the first match, then count and list the traces that move on
+    // (one global reservation of live-list slots per workgroup)
+    int32_t slot = -1, t = -1;
+    if (threadIdx.x < tn) {  // tn <= kChunk <= kMatchThreads
+        t = tids[threadIdx.x];
+        if (t >= 0) {
             const int32_t h = lv.hops[t];
             int32_t next = -1;
             uint16_t port = PC_NO_PORT;
             const int state = apply_rule(lv.S, lv.port_off, lv.port_peer, lv.n_ports, rule_off, rules, lv.ttl, s,
-                                         best[i], h, &next, &port);
+                                         best[threadIdx.x], h, &next, &port);
             if (state >= 0) {
                 write_out(lv.out, t, lv.jm[t], s, port, h, state);
             } else {
                 lv.cur[t] = next;
                 lv.hops[t] = h + 1;
                 lv.jm[t] |= jur_bit(lv.jur, next);
-                lv.rank[t] = atomicAdd(&lv.counts_next[next], 1);
-                lv.live_next[atomicAdd(lv.nlive_next, 1)] = t;
+                lv.rank[t] = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
+                slot = atomicAdd(&nmove, 1);
             }
         }
-        __syncthreads();
     }
+    __syncthreads();
+    if (threadIdx.x == 0) mbase = nmove ? atomicAdd(lv.nlive_next, nmove) : 0;
+    __syncthreads();
+    if (slot >= 0 && mbase + slot < lv.T) lv.live_next[mbase + slot] = t;
 }
 
 // Sparse tail: one workgroup per trace still in flight walks it to its end,
@@ -470,7 +580,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
               hipStream_t stream)
 {
     struct Bufs {
-        int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff;
+        int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
         int32_t *cur, *hops, *rank, *live0, *live1, *bucket;
         uint32_t *jm, *filt;
     } B;
@@ -479,9 +589,10 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         B.bcount = c.take<int32_t>(S + 1);
         B.gofs = c.take<int32_t>(S + 1);
         B.bofs = c.take<int32_t>(S + 1);
-        B.counts0 = c.take<int32_t>(S + 1);
-        B.counts1 = c.take<int32_t>(S + 1);
+        B.counts0 = c.take<int32_t>(static_cast<size_t>(S + 1) * kCountPad);
+        B.counts1 = c.take<int32_t>(static_cast<size_t>(S + 1) * kCountPad);
         B.boff = c.take<int32_t>(S + 1);
+        B.ioff = c.take<int32_t>(S + 1);
         B.cur = c.take<int32_t>(T + 1);
         B.hops = c.take<int32_t>(T + 1);
         B.rank = c.take<int32_t>(T + 1);
@@ -534,10 +645,10 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     int32_t *d_n = ctx->d_small;  // [0], [1]: live counts of the two live lists
     launch_fill_u32(reinterpret_cast<uint32_t *>(d_n), 2, 0, stream);
     if (S > 0) {
-        launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts0), S + 1, 0, stream);
-        launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), S + 1, 0, stream);
+        launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts0), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
+        launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
     }
-    PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(grid_for(T, 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
+    PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
                        B.hops, B.rank, B.live0, d_n, B.counts0, out, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
@@ -562,16 +673,20 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_LAUNCH_CHECK(ctx);
             break;
         }
-        launch_scan_i32(cnt_cur, S, B.boff, nullptr, cnt_cur, stream);
+        PC_TIMED(ctx, "k_tr_plan", stream,
+                 hipLaunchKernelGGL(k_tr_plan, dim3(1), dim3(1024), 0, stream, cnt_cur, S, B.boff, B.ioff));
         PC_TIMED(ctx, "k_tr_scatter", stream,
-                 hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur,
+                 hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, T,
                                     B.cur, B.rank, B.boff, B.bucket));
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
-        const Level lv{S, port_off, port_peer, n_ports, jur, ttl, B.cur, B.jm, B.hops, B.rank, live_nxt, n_nxt, cnt_nxt,
-                       out};
+        const Level lv{S, T, port_off, port_peer, n_ports, jur, ttl, B.cur, B.jm, B.hops, B.rank, live_nxt, n_nxt,
+                       cnt_nxt, out};
+        // at most nlive / kChunk + (switches with a partial chunk) items
+        const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);
         PC_TIMED(ctx, "k_tr_match", stream,
-                 hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(S)), dim3(kMatchThreads), 0, stream, rule_off,
-                                    rules, B.gcount, B.gofs, B.filt, hdr, B.boff, B.bucket, lv));
+                 hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(8 * ((max_items + 7) / 8))),
+                                    dim3(kMatchThreads), 0, stream, S, rule_off, rules, B.gcount, B.gofs, B.filt, hdr,
+                                    B.boff, B.ioff, B.bucket, lv));
         PC_LAUNCH_CHECK(ctx);
         PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, n_nxt, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
         PC_HIP(ctx, hipStreamSynchronize(stream));
