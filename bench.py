@@ -31,8 +31,8 @@ HBM_PEAK_GBS = 8000.0
 # and counter values are in profiles/k_sel_eval_cfg5_hbm_counters.md).
 # Valid only for the kernel source it was measured on.
 SEL_TRAFFIC = {"source": "paper_2602_16100_amd/csrc/select.hip",
-               "sha256": "a262fd3d663422e6c9c3bfa4eef8319b0b96e94aab6426d0355cda00f83e338b",
-               "workload": "cfg5", "bytes_per_launch": 444_465_152 + 4_473_939_968}
+               "sha256": "7a6761f972af716cbf6e589176a0ff057677988f419f97acbe6ffd2abc62088c",
+               "workload": "cfg5", "bytes_per_launch": 797_608_752 + 4_473_972_928}
 
 
 def measured_traffic(workload):

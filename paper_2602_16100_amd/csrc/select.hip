@@ -18,13 +18,12 @@
 //                  writes a 64-byte row record holding programs of up to 15
 //                  entries inline.
 //   5. eval      : one row at a time per wavefront over a tile of 128 words
-//                  (two per lane, 16-byte loads and stores).  A wavefront
-//                  loads the records of 64 rows with one vector load each
-//                  and reads them back one row at a time from registers, so
-//                  a row costs only its plane loads (L2 hits: a tile of
-//                  every plane is P KiB) and its output store.  Popcounts
-//                  are reduced in-wavefront with DPP and stored per (tile,
-//                  row); a last pass sums the tiles.
+//                  (two per lane, 16-byte loads and stores).  The row's
+//                  record arrives through scalar loads, so its plane loads
+//                  (L2 hits: a tile of every plane is P KiB) all go out
+//                  together with scalar offsets, followed by one output
+//                  store.  Per-lane popcounts are collected as bytes in LDS
+//                  and summed once per 64 rows; a last pass sums the tiles.
 #include <algorithm>
 
 #include "pc_internal.h"
@@ -208,8 +207,9 @@ __device__ __forceinline__ uint32_t pred_clause(const pc_pred &q, const uint64_t
 __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__ pred_off,
                                                      const pc_pred *__restrict__ preds, int64_t n_preds, int32_t I,
                                                      int32_t L, const uint64_t *__restrict__ present,
-                                                     const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog,
-                                                     uint32_t *__restrict__ rec, uint32_t *__restrict__ d_err)
+                                                     const uint32_t *__restrict__ wbase, uint32_t zero_pid,
+                                                     uint32_t *__restrict__ prog, uint32_t *__restrict__ rec,
+                                                     uint32_t *__restrict__ d_err)
 {
     uint32_t errs = 0;
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
@@ -265,6 +265,11 @@ __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__
             }
         }
         if (inl) {
+            // pad to a whole group (8, or all 15 slots) with the all-zero
+            // plane, which changes no clause: evaluation then needs no
+            // per-entry bound checks
+            const int64_t padded = n == 0 ? 0 : (n <= kGroup ? kGroup : kInline);
+            for (int64_t k = n; k < padded; ++k) rr[1 + k] = zero_pid;
             rr[0] = static_cast<uint32_t>(n);
         } else {
             rr[0] = static_cast<uint32_t>(kRowIndirect);
@@ -275,54 +280,16 @@ __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__
     if (errs) atomicOr(d_err, errs);
 }
 
-// Sum of v over the 64 lanes, returned uniform.  quad_perm [1,0,3,2] and
-// [2,3,0,1], row_half_mirror and row_mirror leave every lane of each row of
-// 16 lanes holding that row's sum; the four row sums are read back.  Every
-// lane must be active.
-__device__ __forceinline__ uint32_t wave_sum_uniform(uint32_t v)
-{
-    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0xB1, 0xF, 0xF, false));
-    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x4E, 0xF, 0xF, false));
-    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x141, 0xF, 0xF, false));
-    v += static_cast<uint32_t>(__builtin_amdgcn_update_dpp(0, static_cast<int>(v), 0x140, 0xF, 0xF, false));
-    return static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 0)) +
-           static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 16)) +
-           static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 32)) +
-           static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(v), 48));
-}
-
 struct Words {
     uint64_t a, b;
 };
 typedef uint64_t u64x2 __attribute__((ext_vector_type(2)));
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ Words load_words(const uint64_t *p)
 {
     const ulonglong2 v = *reinterpret_cast<const ulonglong2 *>(p);
     return {v.x, v.y};
-}
-
-__device__ __forceinline__ uint32_t rec_word(const uint4 &h0, const uint4 &h1, const uint4 &h2, const uint4 &h3,
-                                             int k)
-{
-    switch (k) {
-    case 0: return h0.x;
-    case 1: return h0.y;
-    case 2: return h0.z;
-    case 3: return h0.w;
-    case 4: return h1.x;
-    case 5: return h1.y;
-    case 6: return h1.z;
-    case 7: return h1.w;
-    case 8: return h2.x;
-    case 9: return h2.y;
-    case 10: return h2.z;
-    case 11: return h2.w;
-    case 12: return h3.x;
-    case 13: return h3.y;
-    case 14: return h3.z;
-    default: return h3.w;
-    }
 }
 
 // Fold one program entry's plane words into the running clause (c) and,
@@ -343,11 +310,36 @@ __device__ __forceinline__ void fold(uint32_t ent, const Words &v, Words &c, Wor
     }
 }
 
+// This lane's two words of plane `pid`.  The buffer form (planes within
+// 4 GiB) takes the plane offset as a scalar operand: one scalar multiply
+// per load and no vector address arithmetic.
+template <bool kBuf>
+struct Planes {
+    __amdgpu_buffer_rsrc_t rsrc;
+    uint32_t lane_off;  // bytes: this lane's first word within a plane row
+    uint32_t rowbytes;  // bytes per plane row
+    const uint64_t *pcol;
+    int64_t Wp;
+
+    __device__ __forceinline__ Words operator()(uint32_t pid) const
+    {
+        if constexpr (kBuf) {
+            const u32x4 v = __builtin_bit_cast(
+                u32x4, __builtin_amdgcn_raw_buffer_load_b128(rsrc, lane_off, pid * rowbytes, 0));
+            return {static_cast<uint64_t>(v.x) | static_cast<uint64_t>(v.y) << 32,
+                    static_cast<uint64_t>(v.z) | static_cast<uint64_t>(v.w) << 32};
+        } else {
+            return load_words(pcol + static_cast<int64_t>(pid) * Wp);
+        }
+    }
+};
+
 // Rows whose program did not fit its slot: decode the predicates on the
-// scalar unit.  `pcol` points at this lane's two words of plane 0.
+// scalar unit.
+template <bool kBuf>
 __device__ Words eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, int64_t e,
                                   const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
-                                  const uint64_t *pcol, int64_t Wp, bool lok)
+                                  const Planes<kBuf> &pl)
 {
     Words a{~0ull, ~0ull};
     for (int64_t p = b; p < e; ++p) {
@@ -357,8 +349,7 @@ __device__ Words eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, 
         const uint32_t *wb = wbase + static_cast<int64_t>(label) * 4;
         if (op == PC_OP_EXISTS) {
             if (pres[3] >> 63) {
-                const Words v = lok ? load_words(pcol + static_cast<int64_t>(plane_id(pres, wb, 255)) * Wp)
-                                    : Words{0, 0};
+                const Words v = pl(plane_id(pres, wb, 255));
                 a.a &= ~v.a;
                 a.b &= ~v.b;
             }
@@ -370,11 +361,9 @@ __device__ Words eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, 
             while (m) {
                 const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
                 m &= m - 1;
-                if (lok) {
-                    const Words x = load_words(pcol + static_cast<int64_t>(plane_id(pres, wb, v)) * Wp);
-                    c.a |= x.a;
-                    c.b |= x.b;
-                }
+                const Words x = pl(plane_id(pres, wb, v));
+                c.a |= x.a;
+                c.b |= x.b;
             }
         }
         if (op == PC_OP_IN) {
@@ -390,14 +379,22 @@ __device__ Words eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, 
 
 // Work item (tile, chunk): the wavefronts of a workgroup take turns on
 // batches of 64 consecutive rows of the chunk; lane l covers words
-// tile * 128 + 2l and + 1.  part[tile * I + r] receives row r's popcount
-// over the tile.
+// tile * 128 + 2l and + 1.  A row's record is read with scalar loads (the
+// next row's is requested while the current row's planes load), so the
+// plane loads of a row are all in flight together.  Each lane leaves its
+// popcount of row i as byte (i, lane) of an LDS table; at the end of a
+// batch lane i sums row i's 64 bytes with dot4 and stores
+// part[tile * I + r].  Lanes past the last word load in-bounds words and
+// mask them.
+template <bool kBuf>
 __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     const uint32_t *__restrict__ rec, const uint32_t *__restrict__ prog, const int32_t *__restrict__ pred_off,
     const pc_pred *__restrict__ preds, const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
-    const uint64_t *__restrict__ planes, int64_t Wp, int32_t I, int32_t W, int32_t N,
+    const uint64_t *__restrict__ planes, int64_t plane_bytes, int64_t Wp, int32_t I, int32_t W, int32_t N,
     uint64_t *__restrict__ feasible, uint32_t *__restrict__ part, int32_t ntiles, int32_t nchunks, int32_t rpc)
 {
+    constexpr int kCntStride = 68;  // bytes per row of the count table (17 dwords: conflict-free column reads)
+    __shared__ uint32_t cnt_lds[kEvalThreads / 64][64 * kCntStride / 4];
     const int64_t total = static_cast<int64_t>(ntiles) * nchunks;
     const int64_t item = pc_xcd_item(total);
     if (item >= total) return;
@@ -410,88 +407,106 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     const uint64_t last = (N & 63) ? (1ull << (N & 63)) - 1 : ~0ull;
     const uint64_t m0 = ok0 ? (w0 == W - 1 ? last : ~0ull) : 0ull;
     const uint64_t m1 = ok1 ? (w0 + 1 == W - 1 ? last : ~0ull) : 0ull;
-    const uint64_t *pcol = planes + (ok0 ? w0 : 0);
+    const int32_t wl = ok0 ? w0 : 0;  // in-bounds column for lanes past the last word
+    Planes<kBuf> pl;
+    if constexpr (kBuf)
+        pl.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint64_t *>(planes), static_cast<short>(0),
+                                                    static_cast<int>(plane_bytes), 0x00020000);
+    pl.lane_off = static_cast<uint32_t>(wl) * 8u;
+    pl.rowbytes = static_cast<uint32_t>(Wp * 8);
+    pl.pcol = planes + wl;
+    pl.Wp = Wp;
     const bool even = (W & 1) == 0;
+    uint8_t *cb = reinterpret_cast<uint8_t *>(cnt_lds[wave]);
     uint32_t *prt = part + static_cast<int64_t>(tile) * I;
     const int32_t r0 = chunk * rpc;
     const int32_t r1 = min(I, r0 + rpc);
+    // one row: its record R (uniform, in SGPRs) -> bitset store and count byte
+    auto row = [&](int32_t r, int32_t i, const uint32_t (&R)[kRecWords]) {
+        const int32_t hdr = static_cast<int32_t>(R[0]);
+        Words a{~0ull, ~0ull};
+        if (hdr == kRowFalse) {
+            a = Words{0, 0};
+        } else if (hdr > 0) {
+            // inline program, padded with the zero plane to 8 or 15 entries
+            Words c{0, 0};
+            {
+                Words V[kGroup];
+#pragma unroll
+                for (int k = 0; k < kGroup; ++k) V[k] = pl(R[1 + k] & kPidMask);
+#pragma unroll
+                for (int k = 0; k < kGroup; ++k) fold(R[1 + k], V[k], c, a);
+            }
+            if (hdr > kGroup) {
+                Words V[kInline - kGroup];
+#pragma unroll
+                for (int k = 0; k < kInline - kGroup; ++k) V[k] = pl(R[1 + kGroup + k] & kPidMask);
+#pragma unroll
+                for (int k = 0; k < kInline - kGroup; ++k) fold(R[1 + kGroup + k], V[k], c, a);
+            }
+        } else if (hdr == kRowIndirect) {
+            const uint32_t *pr = prog + 4 * static_cast<int64_t>(R[1]);
+            const int32_t len = static_cast<int32_t>(R[2]);
+            Words c{0, 0};
+            for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
+                uint32_t E[kGroup];
+                Words V[kGroup];
+#pragma unroll
+                for (int k = 0; k < kGroup; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
+#pragma unroll
+                for (int k = 0; k < kGroup; ++k)
+                    if (e0 + k < len) V[k] = pl(E[k] & kPidMask);
+#pragma unroll
+                for (int k = 0; k < kGroup; ++k)
+                    if (e0 + k < len) fold(E[k], V[k], c, a);
+            }
+        } else if (hdr == kRowLong) {
+            a = eval_row_decoded<kBuf>(preds, pred_off[r], pred_off[r + 1], present, wbase, pl);
+        }
+        a.a &= m0;
+        a.b &= m1;
+        uint64_t *dst = feasible + static_cast<int64_t>(r) * W + w0;
+        if (even) {
+            if (ok0) __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(dst));
+        } else {
+            if (ok0) __builtin_nontemporal_store(a.a, dst);
+            if (ok1) __builtin_nontemporal_store(a.b, dst + 1);
+        }
+        cb[i * kCntStride + lane] = static_cast<uint8_t>(__popcll(a.a) + __popcll(a.b));
+    };
+    auto load_rec = [&](int32_t r, uint32_t (&R)[kRecWords]) {
+        const uint32_t *rp = rec + static_cast<int64_t>(r) * kRecWords;
+#pragma unroll
+        for (int k = 0; k < kRecWords; ++k) R[k] = rp[k];
+    };
     for (int32_t bat = r0 + wave * 64; bat < r1; bat += kEvalThreads) {
-        const int32_t rr = bat + lane;
-        const bool rv = rr < r1;
-        uint4 h0 = make_uint4(static_cast<uint32_t>(kRowFalse), 0, 0, 0);
-        uint4 h1 = make_uint4(0, 0, 0, 0), h2 = h1, h3 = h1;
-        if (rv) {
-            const uint4 *rp = reinterpret_cast<const uint4 *>(rec + static_cast<int64_t>(rr) * kRecWords);
-            h0 = rp[0];
-            h1 = rp[1];
-            if (static_cast<int32_t>(h0.x) > 7) {
-                h2 = rp[2];
-                h3 = rp[3];
-            }
-        }
         const int32_t nb = min(64, r1 - bat);
-        uint32_t cvec = 0;
-        for (int32_t i = 0; i < nb; ++i) {
-            const int32_t hdr = __builtin_amdgcn_readlane(static_cast<int>(h0.x), i);
-            const int32_t r = bat + i;
-            Words a{~0ull, ~0ull};
-            if (hdr == kRowFalse) {
-                a = Words{0, 0};
-            } else if (hdr >= 0) {
-                Words c{0, 0};
-#pragma unroll
-                for (int g = 0; g < kInline; g += kGroup) {
-                    if (g < hdr) {
-                        uint32_t E[kGroup];
-                        Words V[kGroup];
-#pragma unroll
-                        for (int k = 0; k < kGroup; ++k) {
-                            if (g + k < kInline && g + k < hdr) {
-                                E[k] = static_cast<uint32_t>(__builtin_amdgcn_readlane(
-                                    static_cast<int>(rec_word(h0, h1, h2, h3, 1 + g + k)), i));
-                                V[k] = ok0 ? load_words(pcol + static_cast<int64_t>(E[k] & kPidMask) * Wp)
-                                           : Words{0, 0};
-                            }
-                        }
-#pragma unroll
-                        for (int k = 0; k < kGroup; ++k)
-                            if (g + k < kInline && g + k < hdr) fold(E[k], V[k], c, a);
-                    }
-                }
-            } else if (hdr == kRowIndirect) {
-                const int64_t pb = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(h0.y), i));
-                const int32_t len = __builtin_amdgcn_readlane(static_cast<int>(h0.z), i);
-                const uint32_t *pr = prog + 4 * pb;
-                Words c{0, 0};
-                for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
-                    uint32_t E[kGroup];
-                    Words V[kGroup];
-#pragma unroll
-                    for (int k = 0; k < kGroup; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
-#pragma unroll
-                    for (int k = 0; k < kGroup; ++k)
-                        V[k] = (e0 + k < len && ok0) ? load_words(pcol + static_cast<int64_t>(E[k] & kPidMask) * Wp)
-                                                     : Words{0, 0};
-#pragma unroll
-                    for (int k = 0; k < kGroup; ++k)
-                        if (e0 + k < len) fold(E[k], V[k], c, a);
-                }
-            } else {
-                a = eval_row_decoded(preds, pred_off[r], pred_off[r + 1], present, wbase, pcol, Wp, ok0);
+        // two record buffers: the next row's record loads while this row's
+        // planes load (the last row reloads its own record)
+        uint32_t RA[kRecWords], RB[kRecWords];
+        load_rec(bat, RA);
+        for (int32_t i = 0; i < nb; i += 2) {
+            load_rec(bat + min(i + 1, nb - 1), RB);
+            row(bat + i, i, RA);
+            if (i + 1 < nb) {
+                load_rec(bat + min(i + 2, nb - 1), RA);
+                row(bat + i + 1, i + 1, RB);
             }
-            a.a &= m0;
-            a.b &= m1;
-            uint64_t *dst = feasible + static_cast<int64_t>(r) * W + w0;
-            if (even) {
-                if (ok0) __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(dst));
-            } else {
-                if (ok0) __builtin_nontemporal_store(a.a, dst);
-                if (ok1) __builtin_nontemporal_store(a.b, dst + 1);
-            }
-            const uint32_t cnt = wave_sum_uniform(__popcll(a.a) + __popcll(a.b));
-            cvec = lane == i ? cnt : cvec;
         }
-        if (rv) prt[rr] = cvec;
+        // the count table was written by every lane of this wavefront
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        if (lane < nb) {
+            const uint32_t *row = cnt_lds[wave] + lane * (kCntStride / 4);
+            uint32_t sum = 0;
+#pragma unroll
+            for (int k = 0; k < 16; ++k) sum = __builtin_amdgcn_udot4(row[k], 0x01010101u, sum, false);
+            prt[bat + lane] = sum;
+        }
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
     }
 }
 
@@ -516,7 +531,7 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     const int64_t Wp = (W + 1) / 2 * 2;  // even: 16-byte aligned plane rows
     const int64_t ntiles = (W + kTileW - 1) / kTileW;
     const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
-    const size_t plane_bytes = static_cast<size_t>(pmax) * static_cast<size_t>(Wp) * 8;
+    const size_t plane_bytes = static_cast<size_t>(pmax + 1) * static_cast<size_t>(Wp) * 8;
     if (plane_bytes > (size_t(64) << 30))
         return pc_set_error(ctx, PC_ENOMEM, "pc_eval_selectors: value planes need %zu bytes (L=%d N=%d)", plane_bytes,
                             L, N);
@@ -526,7 +541,7 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     auto carve = [&](Carver &cv) {
         present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
         wbase = cv.take<uint32_t>(static_cast<size_t>(L) * 4 + 1);
-        planes = cv.take<uint64_t>(static_cast<size_t>(pmax) * Wp + 2);
+        planes = cv.take<uint64_t>(static_cast<size_t>(pmax + 1) * Wp + 2);  // + the all-zero plane pmax
         prog = cv.take<uint32_t>(static_cast<size_t>(n_preds) * 4 + 4);
         rec = cv.take<uint32_t>(static_cast<size_t>(I) * kRecWords + kRecWords);
         part = ntiles > 1 ? cv.take<uint32_t>(static_cast<size_t>(ntiles) * I + 1) : nullptr;
@@ -540,6 +555,7 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     carve(real);
 
     launch_fill_u64(present, static_cast<size_t>(L) * 4, 0, stream);
+    if (Wp > 0) launch_fill_u64(planes + static_cast<size_t>(pmax) * Wp, static_cast<size_t>(Wp), 0, stream);
     if (W == 0) launch_fill_u32(popcnt, static_cast<size_t>(I), 0, stream);
     PC_LAUNCH_CHECK(ctx);
     if (N > 0 && L > 0) {
@@ -568,7 +584,7 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
     PC_TIMED(ctx, "k_sel_compile", stream,
              hipLaunchKernelGGL(k_sel_compile, dim3(rgrid), dim3(256), 0, stream, pred_off, preds, n_preds, I, L,
-                                present, wbase, prog, rec, ctx->d_err));
+                                present, wbase, static_cast<uint32_t>(pmax), prog, rec, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     if (W == 0) return PC_OK;
 
@@ -580,11 +596,16 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     const int64_t total = ntiles * nchunks;
     const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
     uint32_t *cnt_out = ntiles > 1 ? part : popcnt;
-    PC_TIMED(ctx, "k_sel_eval", stream,
-             hipLaunchKernelGGL(k_sel_eval, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, pred_off, preds,
-                                present, wbase, planes, Wp, I, static_cast<int32_t>(W), N, feasible, cnt_out,
-                                static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
-                                static_cast<int32_t>(rpc)));
+    const int64_t pbytes = static_cast<int64_t>(pmax + 1) * Wp * 8;
+    auto eval = [&](auto kern) {
+        PC_TIMED(ctx, "k_sel_eval", stream,
+                 hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, pred_off, preds,
+                                    present, wbase, planes, pbytes, Wp, I, static_cast<int32_t>(W), N, feasible,
+                                    cnt_out, static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
+                                    static_cast<int32_t>(rpc)));
+    };
+    if (pbytes < (int64_t(1) << 31)) eval(k_sel_eval<true>);  // buffer offsets are 32-bit
+    else eval(k_sel_eval<false>);
     PC_LAUNCH_CHECK(ctx);
     if (ntiles > 1) {
         PC_TIMED(ctx, "k_sel_popsum", stream,

@@ -110,6 +110,49 @@ def test_selectors_large_value_sets(g, orc):
     _same(pg, po, "popcnt")
 
 
+def test_selectors_program_lengths(g, orc):
+    """Rows whose compiled programs have every length from 0 to 40 entries:
+    the empty program, the 8-entry group boundary, the 15-entry inline
+    limit and the indirect programs beyond it.  Each row is one In/NotIn
+    predicate of m values on a 128-value label (a program of min(m, 128 - m)
+    entries), possibly followed by an Exists and a second small predicate;
+    absent values make Exists cost one entry."""
+    rng = np.random.default_rng(12)
+    N, L = 2500 + 17, 3
+    cards = np.array([128, 128, 5])
+    labels = synth.gen_labels(rng, N, cards, absent_p=0.05)
+    rows = []
+    for m in range(0, 41):
+        for extra in range(3):
+            preds = []
+            for op in (0, 1):
+                row = [(0, op, rng.choice(128, size=m, replace=False))]
+                if extra >= 1:
+                    row.append((1, 2, []))
+                if extra >= 2:
+                    row.append((2, int(rng.integers(0, 2)), rng.choice(5, size=2, replace=False)))
+                preds.append(row)
+            rows.extend(preds)
+    off = np.zeros(len(rows) + 1, np.int32)
+    off[1:] = np.cumsum([len(r) for r in rows])
+    preds = np.zeros(int(off[-1]), synth.PRED_DT)
+    p = 0
+    for row in rows:
+        for lab, op, vals in row:
+            bm = [0, 0, 0, 0]
+            for v in vals:
+                bm[int(v) >> 6] |= 1 << int(v & 63)
+            preds[p]["label"] = lab
+            preds[p]["op"] = op
+            preds[p]["vals"] = np.array(bm, np.uint64)
+            p += 1
+    fg, pg = g.selectors(labels, off, preds)
+    fo, po, err = orc.selectors(labels, off, preds)
+    assert err == 0
+    _same(fg, fo, "feasible")
+    _same(pg, po, "popcnt")
+
+
 def test_selectors_malformed_flags(g, orc):
     import paper_2602_16100_amd as pc
     wl = synth.selector_workload(9, 777, 6, 40)
