@@ -91,17 +91,6 @@ __global__ void k_tr_port_check(int64_t n_ports, const int32_t *__restrict__ por
     if (bad) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
-// 16-bit set of 4-bit values x admitted by a rule chunk (value v4, care m4).
-__device__ __forceinline__ uint32_t chunk_admits(uint32_t v4, uint32_t m4)
-{
-    const uint32_t hi[4] = {0xAAAAu, 0xCCCCu, 0xF0F0u, 0xFF00u};
-    uint32_t s = 0xFFFFu;
-#pragma unroll
-    for (int j = 0; j < 4; ++j)
-        if ((m4 >> j) & 1) s &= ((v4 >> j) & 1) ? hi[j] : (~hi[j] & 0xFFFFu);
-    return s;
-}
-
 // Build the chunk sets of kPrepGroups groups of one switch; validate actions.
 __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__restrict__ port_off, int64_t n_ports,
                                                   const int32_t *__restrict__ rule_off,
@@ -139,17 +128,25 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
         const uint32_t a = r->action;
         bad_action = a != PC_ACTION_DROP && static_cast<int64_t>(a) >= np;
     }
+    // Lane L < 32 assembles output word (chunk c, value x = L / 2) of group
+    // 2 * wave + L % 2: a rule admits value x iff, for each of the chunk's 4
+    // bits j, it admits x's bit j, so the word is the AND over j of the
+    // ballot of rules admitting 0 (or 1, following x's bit j) at bit j.
+    const bool hi_half = lane & 1;
 #pragma unroll
     for (int c = 0; c < kChunks; ++c) {
-        const uint32_t adm = ok ? chunk_admits((v2 >> (4 * c)) & 15u, (m2 >> (4 * c)) & 15u) : 0u;
+        const uint32_t v4 = (v2 >> (4 * c)) & 15u, m4 = (m2 >> (4 * c)) & 15u;
+        uint32_t word = ~0u;
 #pragma unroll
-        for (int x = 0; x < 16; ++x) {
-            const uint64_t bal = __ballot((adm >> x) & 1u);
-            if (lane == 0) {
-                tile[(c * 16 + x) * kPrepGroups + 2 * wave] = static_cast<uint32_t>(bal);
-                tile[(c * 16 + x) * kPrepGroups + 2 * wave + 1] = static_cast<uint32_t>(bal >> 32);
-            }
+        for (int j = 0; j < 4; ++j) {
+            const bool vj = (v4 >> j) & 1u, mj = (m4 >> j) & 1u;
+            const uint64_t b0 = __ballot(ok && !(mj && vj));  // admits bit j = 0
+            const uint64_t b1 = __ballot(ok && (!mj || vj));  // admits bit j = 1
+            const uint32_t s0 = hi_half ? static_cast<uint32_t>(b0 >> 32) : static_cast<uint32_t>(b0);
+            const uint32_t s1 = hi_half ? static_cast<uint32_t>(b1 >> 32) : static_cast<uint32_t>(b1);
+            word &= ((lane >> (1 + j)) & 1) ? s1 : s0;
         }
+        if (lane < 32) tile[(c * 16 + (lane >> 1)) * kPrepGroups + 2 * wave + (lane & 1)] = word;
     }
     if (__ballot(bad_action) && lane == 0) atomicOr(d_err, PC_DERR_ACTION);
     __syncthreads();
