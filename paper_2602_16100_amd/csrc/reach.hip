@@ -25,7 +25,7 @@
 
 namespace {
 
-constexpr int kBitsetThreads = 512;
+constexpr int kBitsetThreads = 1024;  // two workgroups per CU fill all 32 wave slots
 constexpr int kQueueThreads = 256;
 constexpr int kMaxBitsetV = 6016;  // 3 x 8 B + 1 B + 2 B per vertex, plus masks, within 160 KB of LDS
 
@@ -130,14 +130,35 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         const int cur = (d - 1) & 1;
         const int32_t nf = nfr[cur];
         if (tid == 0) nfr[cur ^ 1] = 0;  // last read at the start of the previous level
-        for (int32_t i = grp; i < nf; i += kBitsetThreads / GS) {
-            const int32_t u = flist[i];
-            const uint64_t f = fr[u];
-            const int64_t b = adj_off[u], e = adj_off[u + 1];
-            if (!pc_range_ok(b, e, n_adj)) continue;
-            for (int64_t p = b + gl; p < e; p += GS) {
-                const int32_t v = adj[p];
-                if (v >= 0 && v < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[v]), f);
+        // A group takes GS frontier entries at a time: lane k loads entry k's
+        // adjacency range and frontier word in one round (no dependent load
+        // chain per vertex), then the group walks the GS entries, taking
+        // each range and word from lane k by shuffle.
+        constexpr int kNG = kBitsetThreads / GS;  // groups
+        for (int32_t i0 = grp; i0 < nf; i0 += kNG * GS) {
+            const int32_t my = i0 + kNG * gl;
+            int32_t b = 0, e = 0;
+            uint32_t flo = 0, fhi = 0;
+            if (my < nf) {
+                const int32_t u = flist[my];
+                const int64_t b64 = adj_off[u], e64 = adj_off[u + 1];
+                if (pc_range_ok(b64, e64, n_adj)) {
+                    b = static_cast<int32_t>(b64);
+                    e = static_cast<int32_t>(e64);
+                    const uint64_t f = fr[u];
+                    flo = static_cast<uint32_t>(f);
+                    fhi = static_cast<uint32_t>(f >> 32);
+                }
+            }
+            const int32_t nk = min(GS, (nf - i0 + kNG - 1) / kNG);
+            for (int k = 0; k < nk; ++k) {
+                const int32_t bk = __shfl(b, k, GS), ek = __shfl(e, k, GS);
+                const uint64_t fk = static_cast<uint64_t>(static_cast<uint32_t>(__shfl(fhi, k, GS))) << 32 |
+                                    static_cast<uint32_t>(__shfl(flo, k, GS));
+                for (int32_t p = bk + gl; p < ek; p += GS) {
+                    const int32_t v = adj[p];
+                    if (v >= 0 && v < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[v]), fk);
+                }
             }
         }
         __syncthreads();
