@@ -145,7 +145,9 @@ int pc_create(pc_ctx **out, int device)
         hipMalloc(reinterpret_cast<void **>(&ctx->d_err), 256) != hipSuccess ||
         hipMemset(ctx->d_err, 0, 256) != hipSuccess ||
         hipMalloc(reinterpret_cast<void **>(&ctx->d_small), 256) != hipSuccess ||
-        hipHostMalloc(reinterpret_cast<void **>(&ctx->h_small), 256, hipHostMallocDefault) != hipSuccess) {
+        hipHostMalloc(reinterpret_cast<void **>(&ctx->h_small), 256, hipHostMallocDefault) != hipSuccess ||
+        hipEventCreateWithFlags(&ctx->lvl_ev[0], hipEventDisableTiming) != hipSuccess ||
+        hipEventCreateWithFlags(&ctx->lvl_ev[1], hipEventDisableTiming) != hipSuccess) {
         (void)hipGetLastError();
         pc_destroy(ctx);
         return PC_EDEVICE;
@@ -164,6 +166,8 @@ int pc_destroy(pc_ctx *ctx)
     if (ctx->d_err) (void)hipFree(ctx->d_err);
     if (ctx->d_small) (void)hipFree(ctx->d_small);
     if (ctx->h_small) (void)hipHostFree(ctx->h_small);
+    for (auto e : ctx->lvl_ev)
+        if (e) (void)hipEventDestroy(e);
     for (auto &p : ctx->pending) {
         (void)hipEventDestroy(p.a);
         (void)hipEventDestroy(p.b);

@@ -21,6 +21,7 @@ struct pc_ctx {
     size_t arena_bytes;
     char *aux;           // second scratch buffer, sized after a device-side count
     size_t aux_bytes;
+    hipEvent_t lvl_ev[2];  // trace level loop: completion of a level's live count copy
     // optional per-kernel timing (pc_profile)
     bool prof;
     std::vector<hipEvent_t> ev_free;

@@ -82,6 +82,9 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     uint16_t *flist = reinterpret_cast<uint16_t *>(reg + ((V + 3) & ~3));  // [V] frontier vertices
     __shared__ int32_t nfr[2];                                              // list lengths, by level parity
     __shared__ int flag_done;
+    // target look-ahead: the targets' adjacency as (query, entry) pairs
+    __shared__ int32_t toff[65], tbeg[64];
+    __shared__ unsigned long long found, act;
     const int tid = threadIdx.x, lane = tid & 63;
     const int32_t q0 = blockIdx.x * 64;
     const int32_t nq = min(64, Q - q0);
@@ -120,9 +123,35 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     __syncthreads();
     for (int32_t v = tid; v < V; v += kBitsetThreads)
         if (fr[v]) flist[atomicAdd(&nfr[0], 1)] = static_cast<uint16_t>(v);
-    if (tid < 64 && !done && ((vis[tgt] >> lane) & 1)) {
-        res = 0;
-        done = true;
+    if (tid < 64) {
+        if (!done && ((vis[tgt] >> lane) & 1)) {
+            res = 0;
+            done = true;
+        }
+        // A query whose target is allowed and has a neighbour in its
+        // frontier at distance d is resolved at d + 1 without expanding
+        // that frontier: list each such target's adjacency once.
+        int32_t deg = 0, b = 0;
+        bool t_allowed = false;
+        if (target && !done) {
+            const int64_t b64 = adj_off[tgt], e64 = adj_off[tgt + 1];
+            t_allowed = allowed_v(reg, allowed[q0 + lane], tgt);
+            if (t_allowed && pc_range_ok(b64, e64, n_adj)) {
+                b = static_cast<int32_t>(b64);
+                deg = static_cast<int32_t>(e64 - b64);
+            }
+        }
+        int32_t x = deg;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        toff[lane] = x - deg;
+        tbeg[lane] = b;
+        if (lane == 63) toff[64] = x;
+        const uint64_t a = __ballot(deg > 0);
+        if (lane == 0) act = a;
     }
     __syncthreads();
     const int grp = tid / GS, gl = tid % GS;
@@ -181,14 +210,39 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
             fr[v] = n;
             if (n) flist[atomicAdd(&nfr[cur ^ 1], 1)] = static_cast<uint16_t>(v);
         }
+        if (tid == 0) found = 0;
         __syncthreads();
+        if (target) {
+            const uint64_t a = act;
+            if (a) {
+                const int32_t total = toff[64];
+                for (int32_t i = tid; i < total; i += kBitsetThreads) {
+                    int32_t lo = 0, hi = 64;  // query q: toff[q] <= i < toff[q + 1]
+                    while (hi - lo > 1) {
+                        const int32_t mid = (lo + hi) >> 1;
+                        if (toff[mid] <= i) lo = mid;
+                        else hi = mid;
+                    }
+                    if (!((a >> lo) & 1)) continue;
+                    const int32_t u = adj[tbeg[lo] + (i - toff[lo])];
+                    if (u >= 0 && u < V && ((fr[u] >> lo) & 1)) atomicOr(&found, 1ull << lo);
+                }
+            }
+            __syncthreads();
+        }
         if (tid < 64) {
             if (!done && ((fr[tgt] >> lane) & 1)) {
                 res = d;
                 done = true;
+            } else if (!done && target && ((found >> lane) & 1)) {
+                res = d + 1;
+                done = true;
             }
-            const bool all_done = __ballot(!done) == 0;
-            if (tid == 0) flag_done = target ? all_done : 0;
+            const uint64_t still = __ballot(!done);
+            if (tid == 0) {
+                flag_done = target ? still == 0 : 0;
+                act &= still;
+            }
         }
         __syncthreads();
         // nfr[cur ^ 1] is reset only two levels on; flag_done is rewritten
@@ -282,7 +336,9 @@ int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
     // visited / frontier / next (8 B each), region (1 B) and list (2 B) per vertex
     const size_t lds = static_cast<size_t>(V) * 3 * 8 + 32 * 8 + ((static_cast<size_t>(V) + 3) & ~size_t(3)) +
                        static_cast<size_t>(V) * 2;
-    if (V <= kMaxBitsetV && lds + 64 <= static_cast<size_t>(max_lds)) {
+    hipFuncAttributes fa{};
+    PC_HIP(ctx, hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(k_rc_bitset<16>)));  // static LDS
+    if (V <= kMaxBitsetV && lds + fa.sharedSizeBytes <= static_cast<size_t>(max_lds)) {
         // lanes per frontier vertex: a power of two near a third of the mean degree
         const int64_t avg = n_adj / V;
         const int gs = avg <= 12 ? 4 : avg <= 24 ? 8 : avg <= 48 ? 16 : 32;

@@ -650,7 +650,6 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
-    int32_t nlive = ctx->h_small[0];
     int32_t *live_cur = B.live0, *live_nxt = B.live1;
     int32_t *cnt_cur = B.counts0, *cnt_nxt = B.counts1;
     int32_t *n_cur = d_n, *n_nxt = d_n + 1;
@@ -658,11 +657,20 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     // as bucketed passes (tunable with PC_TRACE_WALK_MAX, 0 = never walk).
     int64_t walk_max = 8192;
     if (const char *env = getenv("PC_TRACE_WALK_MAX")) walk_max = atoll(env);
-    for (int level = 0; nlive > 0; ++level) {
-        if (level > ttl + 1)
-            return pc_set_error(ctx, PC_EDEVICE, "pc_trace_flows: level loop exceeded ttl+1 levels");
-        if (nlive <= walk_max) {
-            const unsigned wb = static_cast<unsigned>(nlive < 8192 ? nlive : 8192);
+    // The host does not wait for a level before queueing the next one: live
+    // counts only shrink, so level L is launched with the latest count the
+    // host has (exact for level 0, else the count entering level L - 1) as
+    // the bound for its grids, and the kernels read the exact count on the
+    // device.  The count entering level L is copied back after level L - 1
+    // and waited for (an event one level behind) while level L runs.
+    int32_t *h_cnt = ctx->h_small + 8;  // two pinned slots, by level parity
+    int64_t known = ctx->h_small[0];    // an upper bound on the count entering the next level
+    for (int level = 0;; ++level) {
+        if (level > ttl + 2)
+            return pc_set_error(ctx, PC_EDEVICE, "pc_trace_flows: level loop exceeded ttl+2 levels");
+        if (known == 0) break;
+        if (known <= walk_max) {
+            const unsigned wb = static_cast<unsigned>(known < 8192 ? known : 8192);
             PC_TIMED(ctx, "k_tr_walk", stream,
                      hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
                                         rule_off, rules, B.gcount, B.gofs, B.filt, hdr, ttl, live_cur, n_cur, B.cur,
@@ -670,6 +678,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_LAUNCH_CHECK(ctx);
             break;
         }
+        const int32_t nlive = static_cast<int32_t>(known);
         PC_TIMED(ctx, "k_tr_plan", stream,
                  hipLaunchKernelGGL(k_tr_plan, dim3(1), dim3(1024), 0, stream, cnt_cur, S, B.boff, B.ioff));
         PC_TIMED(ctx, "k_tr_scatter", stream,
@@ -685,9 +694,18 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                                     dim3(kMatchThreads), 0, stream, S, rule_off, rules, B.gcount, B.gofs, B.filt, hdr,
                                     B.boff, B.ioff, B.bucket, lv));
         PC_LAUNCH_CHECK(ctx);
-        PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, n_nxt, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
-        PC_HIP(ctx, hipStreamSynchronize(stream));
-        nlive = ctx->h_small[0];
+        // the count leaving this level
+        const int slot = (level + 1) & 1;
+        PC_HIP(ctx, hipMemcpyAsync(h_cnt + slot, n_nxt, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+        PC_HIP(ctx, hipEventRecord(ctx->lvl_ev[slot], stream));
+        if (level == 0) {
+            known = nlive;  // the bound for level 1; its exact count is learned after level 0 completes
+        } else {
+            // the count entering this level (left by the previous level): its
+            // copy completed before this level started
+            PC_HIP(ctx, hipEventSynchronize(ctx->lvl_ev[level & 1]));
+            known = h_cnt[level & 1];
+        }
         int32_t *tmp;
         tmp = live_cur; live_cur = live_nxt; live_nxt = tmp;
         tmp = cnt_cur; cnt_cur = cnt_nxt; cnt_nxt = tmp;
