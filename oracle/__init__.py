@@ -22,7 +22,8 @@ _LIB = os.path.join(_HERE, "_pc_oracle.so")
 TRACE_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port", "<u2"),
                      ("hops", "u1"), ("state", "u1")])
 assert TRACE_DT.itemsize == 12
-SUMMARY_DT = np.dtype([("counts", "<u8", (4, 8)), ("no_path", "<u8", (4,))])
+SUMMARY_DT = np.dtype([("counts", "<u8", (4, 16)), ("no_path", "<u8", (4,))])
+PATH_EXPECT_DT = np.dtype([("must", "<u4"), ("forbid", "<u4")])
 
 EGRESS, DROP, MISS, TTL = 0, 1, 2, 3
 F_PRED, F_OFFSETS, F_ACTION, F_SWITCH, F_JUR, F_GRAPH, F_INTENT = 1, 2, 4, 8, 16, 32, 64
@@ -50,9 +51,10 @@ def _load():
         I64 = ctypes.c_int64
         C = ctypes.c_int
         _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
-        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, P, C]
+        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, C]
         _lib.orc_reach.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, P, C]
-        _lib.orc_report.argtypes = [I64, P, I64, P, I64, P, I64, P, I64, P, P, I64, P, P, P, P]
+        _lib.orc_reach_via.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, I64, P, I64, P, P, C]
+        _lib.orc_report.argtypes = [I64, P, I64, P, I64, P, I64, P, I64, P, P, I64, P, P, P, P, P, P]
         _lib.orc_max_threads.restype = C
     return _lib
 
@@ -87,8 +89,10 @@ def selectors(labels, pred_off, preds, n_preds=None, rows=None, nthreads=0):
 
 
 def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=None,
-          n_ports=None, n_rules=None, nthreads=0):
-    """Trace records for the given trace indices (all by default)."""
+          n_ports=None, n_rules=None, nthreads=0, watch=None):
+    """Trace records for the given trace indices (all by default).  With a
+    watch list [T, K] (switch ids, -1 = unused) also returns the visit words:
+    (out, visit, flags)."""
     lib = _load()
     T = ingress.shape[0]
     if idx is None:
@@ -96,6 +100,13 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
     idx = np.ascontiguousarray(idx, np.int64)
     out = np.zeros(idx.shape[0], TRACE_DT)
     err = np.zeros(1, np.uint32)
+    K = 0
+    visit = None
+    if watch is not None:
+        watch = np.ascontiguousarray(watch, np.int32)
+        assert watch.ndim == 2 and watch.shape[0] == T
+        K = watch.shape[1]
+        visit = np.zeros(idx.shape[0], np.uint32)
     n_ports = port_peer.shape[0] if n_ports is None else n_ports
     n_rules = rules.shape[0] if n_rules is None else n_rules
     lib.orc_trace(S, _p(np.ascontiguousarray(port_off, np.int32)),
@@ -103,7 +114,9 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
                   _p(np.ascontiguousarray(jur, np.uint8)), _p(np.ascontiguousarray(rule_off, np.int32)),
                   _p(np.ascontiguousarray(rules)), n_rules,
                   _p(np.ascontiguousarray(hdr, np.uint32)), _p(np.ascontiguousarray(ingress, np.int32)),
-                  T, ttl, _p(idx), idx.shape[0], _p(out), _p(err), nthreads)
+                  T, ttl, _p(watch), K, _p(idx), idx.shape[0], _p(out), _p(visit), _p(err), nthreads)
+    if watch is not None:
+        return out, visit, int(err[0])
     return out, int(err[0])
 
 
@@ -129,8 +142,33 @@ def reach(V, adj_off, adj, region, src, allowed, target=None, qidx=None, n_adj=N
     return dist, int(err[0])
 
 
-def report(intents, feasible, popcnt, N, traces, expect, reach_d):
-    """Per-intent pass bits, reason codes and the (kind, reason) summary."""
+def reach_via(V, adj_off, adj, region, src, allowed, target, via, forbid, qidx=None, n_adj=None, nthreads=0):
+    """Shortest walk src -> via... -> target over allowed, non-forbidden
+    vertices: int32 [nq], -1 = none.  via [Q, Kv] and forbid [Q, Kf] hold
+    vertex ids, -1 = unused (via ends at its first -1)."""
+    lib = _load()
+    Q = src.shape[0]
+    if qidx is None:
+        qidx = np.arange(Q, dtype=np.int64)
+    qidx = np.ascontiguousarray(qidx, np.int64)
+    n_adj = adj.shape[0] if n_adj is None else n_adj
+    via = np.ascontiguousarray(via, np.int32)
+    forbid = np.ascontiguousarray(forbid, np.int32)
+    assert via.ndim == 2 and forbid.ndim == 2 and via.shape[0] == Q and forbid.shape[0] == Q
+    dist = np.zeros(qidx.shape[0], np.int32)
+    err = np.zeros(1, np.uint32)
+    lib.orc_reach_via(V, _p(np.ascontiguousarray(adj_off, np.int32)), _p(np.ascontiguousarray(adj, np.int32)),
+                      n_adj, _p(np.ascontiguousarray(region, np.uint8)), Q, _p(np.ascontiguousarray(src, np.int32)),
+                      _p(np.ascontiguousarray(allowed, np.uint32)), _p(np.ascontiguousarray(target, np.int32)),
+                      _p(via), via.shape[1], _p(forbid), forbid.shape[1], _p(qidx), qidx.shape[0], _p(dist),
+                      _p(err), nthreads)
+    return dist, int(err[0])
+
+
+def report(intents, feasible, popcnt, N, traces, expect, reach_d, visit=None, pexp=None):
+    """Per-intent pass bits, reason codes and the (kind, reason) summary.
+    With visit words [T] and path expectations [I] (PATH_EXPECT_DT) the
+    forbidden-switch and waypoint checks are added."""
     lib = _load()
     I = intents.shape[0]
     feasible = np.ascontiguousarray(feasible, np.uint64)
@@ -145,6 +183,8 @@ def report(intents, feasible, popcnt, N, traces, expect, reach_d):
     lib.orc_report(I, _p(np.ascontiguousarray(intents)), rows, _p(feasible), W,
                    _p(np.ascontiguousarray(popcnt, np.uint32)), N, _p(traces), traces.shape[0],
                    _p(np.ascontiguousarray(expect)), _p(reach_d), reach_d.shape[0],
+                   _p(None if visit is None else np.ascontiguousarray(visit, np.uint32)),
+                   _p(None if pexp is None else np.ascontiguousarray(pexp)),
                    _p(pass_), _p(reason), _p(summ), _p(err))
     return pass_, reason, summ[0], int(err[0])
 

@@ -37,13 +37,15 @@ typedef struct {
     uint32_t allowed; uint32_t pad2;
 } o_intent;
 typedef struct { int32_t dst_switch, dst_port, reach_q; } o_expect;
-typedef struct { uint64_t counts[4][8]; uint64_t no_path[4]; } o_summary;
+typedef struct { uint32_t must, forbid; } o_path_expect;
+typedef struct { uint64_t counts[4][16]; uint64_t no_path[4]; } o_summary;
 
 _Static_assert(sizeof(o_pred) == 40, "pred");
 _Static_assert(sizeof(o_rule) == 40, "rule");
 _Static_assert(sizeof(o_trace) == 12, "trace");
 _Static_assert(sizeof(o_intent) == 32, "intent");
 _Static_assert(sizeof(o_expect) == 12, "expect");
+_Static_assert(sizeof(o_path_expect) == 8, "path expect");
 
 enum { O_IN = 0, O_NOTIN = 1, O_EXISTS = 2 };
 enum { O_EGRESS = 0, O_DROP = 1, O_MISS = 2, O_TTL = 3 };
@@ -181,12 +183,15 @@ static uint32_t jur_bit(const uint8_t *jur, int64_t s)
 void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                const uint8_t *jur, const int32_t *rule_off, const o_rule *rules, int64_t n_rules,
                const uint32_t *hdr, const int32_t *ingress, int64_t T, int64_t ttl,
-               const int64_t *idx, int64_t nidx, o_trace *out, uint32_t *err, int nthreads)
+               const int32_t *watch, int64_t K, const int64_t *idx, int64_t nidx, o_trace *out, uint32_t *visit,
+               uint32_t *err, int nthreads)
 {
     set_threads(nthreads);
     /* data-error flags: a sweep over every input item */
     for (int64_t t = 0; t < T; ++t)
         if (ingress[t] < 0 || ingress[t] >= S) { *err |= F_SWITCH; break; }
+    for (int64_t i = 0; i < T * K; ++i)
+        if (watch[i] < -1 || watch[i] >= S) { *err |= F_SWITCH; break; }
     for (int64_t p = 0; p < n_ports; ++p)
         if (port_peer[p] < -1 || port_peer[p] >= S) { *err |= F_SWITCH; break; }
     for (int64_t s = 0; s < S; ++s) {
@@ -199,7 +204,11 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
         for (int64_t r = rule_off[s]; r < rule_off[s + 1]; ++r)
             if (rules[r].action != 0xFFFF && (int64_t)rules[r].action >= np) { *err |= F_ACTION; break; }
     }
-#pragma omp parallel for schedule(dynamic, 16)
+#pragma omp parallel
+    {
+    /* the switches the walk visits, in order (ingress first) */
+    int64_t *path = (int64_t *)malloc(sizeof(int64_t) * (size_t)(ttl + 1));
+#pragma omp for schedule(dynamic, 16)
     for (int64_t k = 0; k < nidx; ++k) {
         const int64_t t = idx[k];
         const uint32_t *h = hdr + 4 * t;
@@ -207,6 +216,7 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
         int64_t s = ingress[t];
         res.last_port = 0xFFFF;
         res.hops = 0;
+        if (visit) visit[k] = 0;
         if (s < 0 || s >= S) {
             res.jmask = 0;
             res.last_switch = (int32_t)s;
@@ -216,6 +226,8 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
         }
         uint32_t jm = jur_bit(jur, s);
         int64_t hops = 0;
+        int64_t npath = 0;
+        path[npath++] = s;
         int state;
         for (;;) {
             const int64_t rb = rule_off[s], re = rule_off[s + 1];
@@ -244,12 +256,24 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
             s = peer;
             ++hops;
             jm |= jur_bit(jur, s);
+            path[npath++] = s;
         }
         res.jmask = jm;
         res.last_switch = (int32_t)s;
         res.hops = (uint8_t)hops;
         res.state = (uint8_t)state;
         out[k] = res;
+        /* watch slot j is set iff its switch is on the visited path (the
+         * paper's must-go / forbidden checks over realised paths) */
+        if (visit) {
+            uint32_t m = 0;
+            for (int64_t j = 0; j < K; ++j)
+                for (int64_t p = 0; p < npath; ++p)
+                    if (watch[t * K + j] == path[p]) { m |= (uint32_t)1 << j; break; }
+            visit[k] = m;
+        }
+    }
+    free(path);
     }
 }
 
@@ -325,6 +349,93 @@ void orc_reach(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_
     }
 }
 
+/* ------------------------------------------------------------------ A5, waypoints
+ * Required waypoints and forbidden switches (paper: the routing constraints
+ * of a Configuration name required waypoints and forbidden vertices; the
+ * JSON constraints carry must_go and forbidden lists).  The walk must go
+ * src -> via[0] -> ... -> via[m-1] -> target (m = entries before the first
+ * -1) on switches that are allowed and not forbidden.  The shortest such
+ * walk is the sum over its legs of the leg's shortest path, each found by a
+ * textbook FIFO breadth-first search; a leg without a path makes the whole
+ * distance -1.  Sums saturate at INT32_MAX.
+ */
+static int usable(const uint8_t *region, uint32_t A, const int32_t *fb, int64_t Kf, int64_t v)
+{
+    if (region[v] >= 32 || !((A >> region[v]) & 1)) return 0;
+    for (int64_t k = 0; k < Kf; ++k)
+        if (fb[k] == v) return 0;
+    return 1;
+}
+
+static int64_t leg_bfs(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                       const uint8_t *region, uint32_t A, const int32_t *fb, int64_t Kf, int64_t s, int64_t t,
+                       int32_t *dist, int64_t *queue)
+{
+    if (s < 0 || s >= V || t < 0 || t >= V) return -1;
+    if (!usable(region, A, fb, Kf, s)) return -1;
+    for (int64_t v = 0; v < V; ++v) dist[v] = -1;
+    int64_t head = 0, tail = 0;
+    dist[s] = 0;
+    queue[tail++] = s;
+    while (head < tail) {
+        const int64_t u = queue[head++];
+        const int64_t b = adj_off[u], e = adj_off[u + 1];
+        if (!range_ok(b, e, n_adj)) continue;
+        for (int64_t p = b; p < e; ++p) {
+            const int64_t v = adj[p];
+            if (v < 0 || v >= V || dist[v] != -1) continue;
+            if (!usable(region, A, fb, Kf, v)) continue;
+            dist[v] = dist[u] + 1;
+            queue[tail++] = v;
+        }
+    }
+    return dist[t];
+}
+
+void orc_reach_via(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                   const uint8_t *region, int64_t Q, const int32_t *src, const uint32_t *allowed,
+                   const int32_t *target, const int32_t *via, int64_t Kv, const int32_t *forbid, int64_t Kf,
+                   const int64_t *qidx, int64_t nq, int32_t *dist_out, uint32_t *err, int nthreads)
+{
+    set_threads(nthreads);
+    for (int64_t v = 0; v < V; ++v) {
+        if (region[v] >= 32) *err |= F_JUR;
+        if (!range_ok(adj_off[v], adj_off[v + 1], n_adj)) *err |= F_OFFSETS;
+    }
+    for (int64_t p = 0; p < n_adj; ++p)
+        if (adj[p] < 0 || adj[p] >= V) { *err |= F_GRAPH; break; }
+    for (int64_t q = 0; q < Q; ++q)
+        if (src[q] < 0 || src[q] >= V || target[q] < 0 || target[q] >= V) *err |= F_SWITCH;
+    for (int64_t i = 0; i < Q * Kv; ++i)
+        if (via[i] < -1 || via[i] >= V) { *err |= F_SWITCH; break; }
+    for (int64_t i = 0; i < Q * Kf; ++i)
+        if (forbid[i] < -1 || forbid[i] >= V) { *err |= F_SWITCH; break; }
+#pragma omp parallel
+    {
+        int32_t *dist = (int32_t *)malloc(sizeof(int32_t) * (size_t)(V > 0 ? V : 1));
+        int64_t *queue = (int64_t *)malloc(sizeof(int64_t) * (size_t)(V > 0 ? V : 1));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t k = 0; k < nq; ++k) {
+            const int64_t q = qidx[k];
+            const int32_t *w = via + q * Kv;
+            const int32_t *fb = forbid + q * Kf;
+            int64_t total = 0, from = src[q];
+            int64_t m = 0;
+            while (m < Kv && w[m] != -1) ++m;
+            for (int64_t leg = 0; leg <= m; ++leg) {
+                const int64_t to = leg < m ? w[leg] : target[q];
+                const int64_t d = leg_bfs(V, adj_off, adj, n_adj, region, allowed[q], fb, Kf, from, to, dist, queue);
+                if (d < 0) { total = -1; break; }
+                total += d;
+                from = to;
+            }
+            dist_out[k] = (int32_t)(total > 0x7FFFFFFF ? 0x7FFFFFFF : total);
+        }
+        free(dist);
+        free(queue);
+    }
+}
+
 /* ------------------------------------------------------------------ A6
  * Per-intent verdict: pass iff every check of the intent passes (paper,
  * validator check definition); an unenforceable intent fails closed.
@@ -334,7 +445,10 @@ void orc_reach(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_
  *   network (kind bit 1): at least one flow (NO_FLOW = 3, the no-op
  *       policy); every trace stays inside the allowed jurisdictions
  *       (LEAK = 4), ends in EGRESS (UNDELIVERED = 5) at the expected switch
- *       and port when given (WRONG_EGRESS = 6).
+ *       and port when given (WRONG_EGRESS = 6); with path constraints, it
+ *       visits none of the intent's forbidden switches (FORBIDDEN_SWITCH =
+ *       8) and every required waypoint (WAYPOINT_MISSED = 9) -- the checks
+ *       over realised paths in the validator check definition.
  * The reason is the smallest failing code; compute reasons come first.
  * Bit 7 is added when the intent's reachability query found no compliant
  * path.  A record that points outside its arrays, or kind not in {1,2,3},
@@ -342,8 +456,8 @@ void orc_reach(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_
  */
 void orc_report(int64_t I, const o_intent *intents, int64_t rows, const uint64_t *feasible, int64_t W,
                 const uint32_t *popcnt, int64_t N, const o_trace *traces, int64_t T,
-                const o_expect *expect, const int32_t *reach, int64_t Q,
-                uint64_t *pass, uint8_t *reason, o_summary *summary, uint32_t *err)
+                const o_expect *expect, const int32_t *reach, int64_t Q, const uint32_t *visit,
+                const o_path_expect *pexp, uint64_t *pass, uint8_t *reason, o_summary *summary, uint32_t *err)
 {
     memset(summary, 0, sizeof(*summary));
     for (int64_t w = 0; w < (I + 63) / 64; ++w) pass[w] = 0;
@@ -385,6 +499,8 @@ void orc_report(int64_t I, const o_intent *intents, int64_t rows, const uint64_t
                         else if (tr->state != O_EGRESS) code = 5;
                         else if ((ex->dst_switch >= 0 && tr->last_switch != ex->dst_switch) ||
                                  (ex->dst_port >= 0 && tr->last_port != ex->dst_port)) code = 6;
+                        else if (visit && (visit[t] & pexp[i].forbid)) code = 8;
+                        else if (visit && (visit[t] & pexp[i].must) != pexp[i].must) code = 9;
                         if (code && (r == 0 || code < r)) r = code;
                     }
                 }

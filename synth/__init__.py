@@ -15,6 +15,7 @@ Record layouts (little-endian, packed as listed) are the C ABI's:
   intent  32 B  {u8 kind, u8 pad[3], i32 sel_row, i32 src_node, i32 dst_node,
                  i32 trace_begin, i32 trace_end, u32 allowed, u32 pad2}
   expect  12 B  {i32 dst_switch, i32 dst_port, i32 reach_q}
+  pexp     8 B  {u32 must, u32 forbid}   (masks over a trace's watch slots)
 
 The workload recipes follow the paper's system model (labelled nodes,
 a labelled switch graph, flow rules compiled per hop along a chosen
@@ -45,6 +46,7 @@ OP_IN, OP_NOTIN, OP_EXISTS = 0, 1, 2
 ABSENT = 0xFF
 DROP = 0xFFFF
 KIND_COMPUTE, KIND_NETWORK, KIND_HYBRID = 1, 2, 3
+PATH_EXPECT_DT = np.dtype([("must", "<u4"), ("forbid", "<u4")])
 
 
 @dataclass
@@ -654,8 +656,53 @@ def cfg4(seed=3):
     return rgg_workload(seed, 1_000_000, 16, 256, name="cfg4")
 
 
+def path_constraints(seed, S, sw, nh, n_forbid=2, p_on_path=0.5, p_forbid_on_path=0.125):
+    """Required waypoint and forbidden switches per flow (the routing
+    constraints of a Configuration: must-go waypoints and forbidden
+    vertices).  Flow f's compiled path is sw[f, :nh[f]].  The waypoint is,
+    with probability p_on_path, a uniform interior switch of the path (its
+    only switch when it has no interior), else a uniform switch.  Each of
+    the n_forbid forbidden switches is, with probability p_forbid_on_path, an
+    interior switch of the path, else a uniform switch; none equals the
+    waypoint.  Uses its own generator (seed, 7), so the other arrays of a
+    workload do not change.  Returns (via [F, 1], forbid [F, n_forbid])."""
+    rng = np.random.default_rng([seed, 7])
+    F = sw.shape[0]
+    nh = np.asarray(nh, np.int64)
+    n_in = np.maximum(nh - 2, 0)
+
+    def pick_interior():
+        j = np.where(n_in > 0, 1 + (rng.random(F) * np.maximum(n_in, 1)).astype(np.int64), 0)
+        return sw[np.arange(F), j].astype(np.int64)
+
+    way = np.where(rng.random(F) < p_on_path, pick_interior(), rng.integers(0, S, size=F))
+    forbid = np.empty((F, n_forbid), np.int64)
+    for c in range(n_forbid):
+        f = np.where(rng.random(F) < p_forbid_on_path, pick_interior(), rng.integers(0, S, size=F))
+        for _ in range(64):
+            bad = f == way
+            if not bad.any():
+                break
+            f[bad] = rng.integers(0, S, size=int(bad.sum()))
+        f[f == way] = -1
+        forbid[:, c] = f
+    return way[:, None].astype(np.int32), forbid.astype(np.int32)
+
+
+def _add_paths(wl, via_q, forb_q, trace_q, pexp_rows):
+    """Attach path constraints: query q's via / forbid lists; trace t
+    watches [waypoint, forbidden...] of its query trace_q[t]; network
+    intents expect the waypoint in slot 0 and the rest forbidden."""
+    watch = np.concatenate([via_q, forb_q], axis=1)[trace_q]
+    K = watch.shape[1]
+    pexp = np.zeros(wl["intents"].shape[0], PATH_EXPECT_DT)
+    pexp["must"][pexp_rows] = 1
+    pexp["forbid"][pexp_rows] = ((1 << K) - 1) & ~1
+    wl.arrays.update(via=via_q, forbid=forb_q, watch=np.ascontiguousarray(watch, np.int32), pexp=pexp)
+
+
 def combined_workload(seed, N, L, k, J, R, I, ttl=32, p_care=0.7, kmin=1, kmax=8,
-                      card_choices=(2, 4, 16, 64), name="combined"):
+                      card_choices=(2, 4, 16, 64), name="combined", paths=False):
     """Cross-layer validation: kind = [compute, network, hybrid][i mod 3].
     Compute and hybrid intents own a selector row (1..kmax predicates).
     Network intents join two distinct uniform hosts; hybrid intents join
@@ -665,7 +712,8 @@ def combined_workload(seed, N, L, k, J, R, I, ttl=32, p_care=0.7, kmin=1, kmax=8
     trace of the flow's header from its ingress edge switch, and one
     reachability query from the ingress to the egress edge switch.  The
     allowed jurisdictions are those of both edge switches plus each other
-    jurisdiction with probability 1/2."""
+    jurisdiction with probability 1/2.  paths=True adds a waypoint and two
+    forbidden switches per flow (path_constraints)."""
     rng = np.random.default_rng(seed)
     cards = rng.choice(np.asarray(card_choices), size=L)
     labels = gen_labels(rng, N, cards)
@@ -752,17 +800,21 @@ def combined_workload(seed, N, L, k, J, R, I, ttl=32, p_care=0.7, kmin=1, kmax=8
                      intents=intents, expect=expect)
     wl.sizes.update(T=F, ttl=ttl, n_rules=int(rules.shape[0]), Q=F, I=I)
     wl.meta.update(k=k, J=J, R=R, cards=cards, path_rules_dropped=dropped)
+    if paths:
+        via, forb = path_constraints(seed, topo["S"], sw, nh)
+        _add_paths(wl, via, forb, np.arange(F), fl_int)
     return wl
 
 
-def cfg5(seed=4):
+def cfg5(seed=4, paths=False):
     """50,000 nodes x 64 labels; fat-tree k=48 (2,880 switches), 16,384 rules
     per switch, 12 jurisdictions; 1,048,576 intents split evenly between
-    compute-only, network-only and hybrid."""
-    return combined_workload(seed, 50_000, 64, 48, 12, 16_384, 1_048_576, name="cfg5")
+    compute-only, network-only and hybrid.  paths=True adds waypoint and
+    forbidden-switch constraints."""
+    return combined_workload(seed, 50_000, 64, 48, 12, 16_384, 1_048_576, name="cfg5", paths=paths)
 
 
-def cfg1(seed=0, variant="rpath"):
+def cfg1(seed=0, variant="rpath", paths=False):
     """Tiny end-to-end case: 16 nodes x 8 labels (region over 4, trust tier
     0..3, six categorical labels of cardinality 8); 12 switches on a random
     connected graph with 18 links (mean degree 3), 2 host ports each,
@@ -771,7 +823,8 @@ def cfg1(seed=0, variant="rpath"):
     allowed subset; 1,024 traces with TTL 16.  variant 'rpath' compiles one
     flow per network/hybrid intent along the spanning-tree path; 'literal'
     uses i.i.d. rules and uniform headers at random switches; 'dense' uses
-    95% wildcard bits and priorities in [0, 8)."""
+    95% wildcard bits and priorities in [0, 8).  paths=True adds a waypoint
+    and two forbidden switches per network intent (path_constraints)."""
     rng = np.random.default_rng(seed)
     N, L, S, I, T, R, J, TTL = 16, 8, 12, 64, 1024, 32, 4, 16
     cards = np.array([4, 4, 8, 8, 8, 8, 8, 8], np.int64)
@@ -852,6 +905,9 @@ def cfg1(seed=0, variant="rpath"):
                      intents=intents, expect=expect)
     wl.sizes.update(T=T, ttl=TTL, n_rules=int(rules.shape[0]), Q=int(net.shape[0]), I=I)
     wl.meta.update(variant=variant, cards=cards, path_rules_dropped=dropped, topo=topo)
+    if paths:
+        via, forb = path_constraints(seed, S, sw, nh)
+        _add_paths(wl, via, forb, owner, net)
     return wl
 
 

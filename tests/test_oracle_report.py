@@ -101,7 +101,7 @@ def _check_invariants(orc, wl, out):
     bits = np.array([(int(pss[i >> 6]) >> (i & 63)) & 1 for i in range(I)])
     assert np.array_equal(bits == 1, (reason & 0x7F) == 0)
     # summary = histogram of reasons per kind
-    hist = np.zeros((4, 8), np.uint64)
+    hist = np.zeros((4, 16), np.uint64)
     np.add.at(hist, (it["kind"] & 3, reason & 0x7F), 1)
     assert np.array_equal(summ["counts"], hist)
     nop = np.zeros(4, np.uint64)
