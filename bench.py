@@ -180,7 +180,7 @@ def main():
     reach = torch.empty(Q, dtype=torch.int32, device=dev)
     pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
     reason = torch.empty(I, dtype=torch.uint8, device=dev)
-    summary = torch.empty(288, dtype=torch.uint8, device=dev)
+    summary = torch.empty(libpc.SUMMARY_BYTES, dtype=torch.uint8, device=dev)
     ctx = pc.context(0)
 
     only = args.only

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 1
+#define PC_VERSION 2
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -73,6 +73,8 @@ enum {
     PC_R_UNDELIVERED = 5,
     PC_R_WRONG_EGRESS = 6,
     PC_R_MALFORMED = 7,
+    PC_R_FORBIDDEN_SWITCH = 8,   /* pc_report_paths only */
+    PC_R_WAYPOINT_MISSED = 9,    /* pc_report_paths only */
     PC_R_NO_COMPLIANT_PATH = 0x80
 };
 
@@ -147,10 +149,19 @@ typedef struct pc_intent {
     uint32_t pad2;
 } pc_intent;
 
+/* Path constraints of an intent's flows for pc_report_paths, 8 bytes: masks
+ * over the watch slots of each of the intent's traces (pc_trace_flows_watch).
+ * must: slots holding required waypoints; forbid: slots holding forbidden
+ * switches. */
+typedef struct pc_path_expect {
+    uint32_t must;
+    uint32_t forbid;
+} pc_path_expect;
+
 /* Verdict summary: counts[kind & 3][reason & 0x7F], no_path[kind & 3] counts
  * intents with PC_R_NO_COMPLIANT_PATH set. */
 typedef struct pc_summary {
-    uint64_t counts[4][8];
+    uint64_t counts[4][16];
     uint64_t no_path[4];
 } pc_summary;
 
@@ -267,6 +278,67 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
               int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
               const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass,
               uint8_t *reason, pc_summary *summary, void *stream);
+
+/*
+ * Waypoint and forbidden-switch constraints on realised paths.  The paper's
+ * routing constraints name required waypoints and forbidden vertices (Formal
+ * Model and Satisfaction, "Configuration"; the must_go / forbidden lists of
+ * the JSON constraints in "Network orchestration"), and a network check
+ * asserts that every realised path of a flow avoids the forbidden switches
+ * and includes the required waypoints (Automated Validation Pipeline,
+ * validator check definition).
+ *
+ * pc_trace_flows_watch: pc_trace_flows, and in addition, for every trace t,
+ * bit k of visit[t] is set iff the trace visited switch watch[t][k] at any
+ * point of its walk (ingress and last switch included).  Neighbours that a
+ * TTL-terminated trace would have moved to are not visited.
+ * watch : int32 [T][K], row-major; -1 = an unused slot (never matches).
+ * K     : slots per trace, 0 <= K <= 32 (K = 0: watch may be NULL and every
+ *         visit word is 0).
+ * visit : uint32 [T], written for every trace.
+ * Malformed: a watch entry < -1 or >= S matches nothing (PC_DERR_SWITCH).
+ */
+int pc_trace_flows_watch(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
+                         int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
+                         int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,
+                         const int32_t *watch, int32_t K, pc_trace_out *out, uint32_t *visit, void *stream);
+
+/*
+ * pc_masked_reach_via: length of the shortest walk src[q] -> via[q][0] ->
+ * ... -> via[q][m-1] -> target[q] that stays on allowed switches (bit
+ * region[v] of allowed[q], as in pc_masked_reach) none of which is in
+ * forbid[q]; m is the number of via entries before the first -1.  Each leg
+ * is a shortest path of the induced subgraph, so the walk may repeat
+ * switches.  dist[q] = the sum of the leg distances, or -1 when any leg has
+ * no path (including an endpoint or waypoint that is not allowed or is
+ * forbidden).
+ * via   : int32 [Q][Kv] row-major (Kv >= 0; NULL when Kv == 0).
+ * forbid: int32 [Q][Kf] row-major, -1 = unused slot (Kf >= 0; NULL when
+ *         Kf == 0).
+ * target: int32 [Q] (required).  dist: int32 [Q].
+ * Limits: 0 <= Kv, Kf <= 32.  Malformed: a via or forbid entry < -1 or >= V
+ * raises PC_DERR_SWITCH; such a waypoint has no path, such a forbidden entry
+ * is ignored.  Scratch: int32 [Q][Kv + 1] leg records.
+ */
+int pc_masked_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                        const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,
+                        const int32_t *target, const int32_t *via, int32_t Kv, const int32_t *forbid,
+                        int32_t Kf, int32_t *dist, void *stream);
+
+/*
+ * pc_report_paths: pc_report with the path checks of network intents added.
+ * A trace whose visit word meets pexp[i].forbid fails with
+ * PC_R_FORBIDDEN_SWITCH; one whose visit word lacks a bit of pexp[i].must
+ * fails with PC_R_WAYPOINT_MISSED.  Per trace the smallest failing code
+ * counts, as for the other trace codes (so LEAK, UNDELIVERED and
+ * WRONG_EGRESS come first).
+ * visit: uint32 [T] (pc_trace_flows_watch); pexp: pc_path_expect [I].
+ */
+int pc_report_paths(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
+                    int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
+                    const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
+                    const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary,
+                    void *stream);
 
 #ifdef __cplusplus
 }

@@ -4,7 +4,8 @@ The library (include/pc.h) runs the validator checks of LLM-driven,
 intent-based privacy orchestration (arXiv 2602.16100) as HIP kernels on one
 GPU: node-selector evaluation (pc_eval_selectors), flow-table tracing
 (pc_trace_flows), masked reachability (pc_masked_reach) and the per-intent
-verdict (pc_report).
+verdict (pc_report), with waypoint and forbidden-switch constraints
+(pc_trace_flows_watch, pc_masked_reach_via, pc_report_paths).
 
 This module only marshals arguments: torch tensors provide device memory
 and the current HIP stream; every step of the computation runs in
@@ -29,8 +30,10 @@ DERR = {"PRED": 1, "OFFSETS": 2, "ACTION": 4, "SWITCH": 8, "JUR": 16, "GRAPH": 3
 PRED_BYTES, RULE_BYTES, KEY_BYTES, INTENT_BYTES, EXPECT_BYTES = 40, 40, 16, 32, 12
 TRACE_OUT_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port", "<u2"),
                          ("hops", "u1"), ("state", "u1")])
-SUMMARY_DT = np.dtype([("counts", "<u8", (4, 8)), ("no_path", "<u8", (4,))])
-assert TRACE_OUT_DT.itemsize == 12 and SUMMARY_DT.itemsize == 288
+SUMMARY_DT = np.dtype([("counts", "<u8", (4, 16)), ("no_path", "<u8", (4,))])
+PATH_EXPECT_DT = np.dtype([("must", "<u4"), ("forbid", "<u4")])
+SUMMARY_BYTES = 544
+assert TRACE_OUT_DT.itemsize == 12 and SUMMARY_DT.itemsize == SUMMARY_BYTES and PATH_EXPECT_DT.itemsize == 8
 
 
 class PCError(RuntimeError):
@@ -75,6 +78,9 @@ def lib():
     L.pc_trace_flows.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, P]
     L.pc_masked_reach.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, P]
     L.pc_report.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P]
+    L.pc_trace_flows_watch.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, I32, P, P, P]
+    L.pc_masked_reach_via.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, I32, P, I32, P, P]
+    L.pc_report_paths.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P, P, P]
     L.pc_profile.argtypes = [P, C]
     L.pc_profile_read.argtypes = [P, C, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I64),
                                   ctypes.POINTER(ctypes.c_double)]
@@ -83,7 +89,8 @@ def lib():
 
 
 EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_errors", "pc_profile",
-            "pc_profile_read", "pc_eval_selectors", "pc_trace_flows", "pc_masked_reach", "pc_report")
+            "pc_profile_read", "pc_eval_selectors", "pc_trace_flows", "pc_masked_reach", "pc_report",
+            "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths")
 
 
 class Context:
@@ -238,7 +245,7 @@ def pc_masked_reach(V, adj_off, adj, region, src, allowed, target=None, n_adj=No
 def pc_report(intents, feasible, popcnt, N, traces, expect, reach, pass_=None, reason=None, summary=None, ctx=None,
               stream=None):
     """A6: pass bits [ceil(I/64)] (int64 storage of uint64), reason codes [I]
-    (uint8) and the pc_summary record (uint8 [288])."""
+    (uint8) and the pc_summary record (uint8 [544])."""
     ctx = ctx or context()
     I = int(intents.shape[0])
     rows = int(feasible.shape[0])
@@ -251,12 +258,80 @@ def pc_report(intents, feasible, popcnt, N, traces, expect, reach, pass_=None, r
     if reason is None:
         reason = torch.empty(I, dtype=torch.uint8, device=dev)
     if summary is None:
-        summary = torch.empty(288, dtype=torch.uint8, device=dev)
+        summary = torch.empty(SUMMARY_BYTES, dtype=torch.uint8, device=dev)
     ctx.check(lib().pc_report(ctx.handle, I, _ptr(intents) if I else None, rows,
                               _ptr(feasible) if feasible.numel() else None, W, _ptr(popcnt) if rows else None,
                               int(N), _ptr(traces) if T else None, T, _ptr(expect) if I else None,
                               _ptr(reach) if Q else None, Q, _ptr(pass_) if I else None, _ptr(reason) if I else None,
                               _ptr(summary), _stream(stream)))
+    return pass_, reason, summary
+
+
+def pc_trace_flows_watch(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, watch, n_ports=None,
+                         n_rules=None, out=None, visit=None, ctx=None, stream=None):
+    """pc_trace_flows plus, per trace, the visit word over its watch slots:
+    watch is int32 [T, K] (K <= 32, -1 = unused); returns (out uint8 [T, 12],
+    visit int32 [T] storage of uint32)."""
+    ctx = ctx or context()
+    T = int(ingress.shape[0])
+    K = int(watch.shape[1]) if watch is not None and watch.dim() == 2 else 0
+    n_ports = int(port_peer.shape[0]) if n_ports is None else int(n_ports)
+    n_rules = int(rules.shape[0]) if n_rules is None else int(n_rules)
+    dev = ingress.device
+    if out is None:
+        out = torch.empty((T, 12), dtype=torch.uint8, device=dev)
+    if visit is None:
+        visit = torch.empty(T, dtype=torch.int32, device=dev)
+    ctx.check(lib().pc_trace_flows_watch(
+        ctx.handle, int(S), _ptr(port_off), _ptr(port_peer) if port_peer.numel() else None, n_ports, _ptr(jur),
+        _ptr(rule_off), _ptr(rules) if rules.numel() else None, n_rules, _ptr(hdr) if T else None,
+        _ptr(ingress) if T else None, T, int(ttl), _ptr(watch) if T and K else None, K, _ptr(out) if T else None,
+        _ptr(visit) if T else None, _stream(stream)))
+    return out, visit
+
+
+def pc_masked_reach_via(V, adj_off, adj, region, src, allowed, target, via, forbid, n_adj=None, dist=None, ctx=None,
+                        stream=None):
+    """Shortest walk through the waypoints via [Q, Kv] avoiding forbid [Q, Kf]
+    inside the allowed-induced subgraph: int32 [Q], -1 = none."""
+    ctx = ctx or context()
+    Q = int(src.shape[0])
+    Kv = int(via.shape[1]) if via is not None and via.dim() == 2 else 0
+    Kf = int(forbid.shape[1]) if forbid is not None and forbid.dim() == 2 else 0
+    n_adj = int(adj.shape[0]) if n_adj is None else int(n_adj)
+    if dist is None:
+        dist = torch.empty(Q, dtype=torch.int32, device=src.device)
+    ctx.check(lib().pc_masked_reach_via(
+        ctx.handle, int(V), _ptr(adj_off), _ptr(adj) if adj.numel() else None, n_adj, _ptr(region), Q,
+        _ptr(src) if Q else None, _ptr(allowed) if Q else None, _ptr(target) if Q else None,
+        _ptr(via) if Q and Kv else None, Kv, _ptr(forbid) if Q and Kf else None, Kf, _ptr(dist) if Q else None,
+        _stream(stream)))
+    return dist
+
+
+def pc_report_paths(intents, feasible, popcnt, N, traces, expect, reach, visit, pexp, pass_=None, reason=None,
+                    summary=None, ctx=None, stream=None):
+    """pc_report with the forbidden-switch and waypoint checks: visit [T]
+    (from pc_trace_flows_watch) and pexp, pc_path_expect records (uint8
+    [I, 8])."""
+    ctx = ctx or context()
+    I = int(intents.shape[0])
+    rows = int(feasible.shape[0])
+    W = int(feasible.shape[1]) if feasible.dim() == 2 else 0
+    T = int(traces.shape[0])
+    Q = int(reach.shape[0])
+    dev = intents.device
+    if pass_ is None:
+        pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
+    if reason is None:
+        reason = torch.empty(I, dtype=torch.uint8, device=dev)
+    if summary is None:
+        summary = torch.empty(SUMMARY_BYTES, dtype=torch.uint8, device=dev)
+    ctx.check(lib().pc_report_paths(
+        ctx.handle, I, _ptr(intents) if I else None, rows, _ptr(feasible) if feasible.numel() else None, W,
+        _ptr(popcnt) if rows else None, int(N), _ptr(traces) if T else None, T, _ptr(expect) if I else None,
+        _ptr(reach) if Q else None, Q, _ptr(visit) if T else None, _ptr(pexp) if I else None,
+        _ptr(pass_) if I else None, _ptr(reason) if I else None, _ptr(summary), _stream(stream)))
     return pass_, reason, summary
 
 

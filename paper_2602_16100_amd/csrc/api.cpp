@@ -234,7 +234,29 @@ int pc_trace_flows(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_
     if (T == 0 && S == 0) return PC_OK;
     PC_HIP(ctx, hipSetDevice(ctx->device));
     return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                     out, static_cast<hipStream_t>(stream));
+                     nullptr, 0, out, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int pc_trace_flows_watch(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
+                         int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
+                         int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,
+                         const int32_t *watch, int32_t K, pc_trace_out *out, uint32_t *visit, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(S >= 0 && T >= 0 && n_ports >= 0 && n_rules >= 0, "pc_trace_flows_watch: negative size");
+    PC_REQUIRE(ttl >= 0 && ttl <= 255, "pc_trace_flows_watch: ttl=%d out of [0, 255]", ttl);
+    PC_REQUIRE(K >= 0 && K <= 32, "pc_trace_flows_watch: K=%d out of [0, 32]", K);
+    PC_REQUIRE(n_rules < (int64_t(1) << 40), "pc_trace_flows_watch: n_rules too large");
+    PC_REQUIRE(T == 0 || (hdr && ingress && out && visit), "pc_trace_flows_watch: null hdr/ingress/out/visit");
+    PC_REQUIRE(T == 0 || K == 0 || watch, "pc_trace_flows_watch: null watch");
+    PC_REQUIRE(S == 0 || (port_off && rule_off && jur), "pc_trace_flows_watch: null topology array");
+    PC_REQUIRE(n_ports == 0 || port_peer, "pc_trace_flows_watch: null port_peer");
+    PC_REQUIRE(n_rules == 0 || rules, "pc_trace_flows_watch: null rules");
+    if (T == 0 && S == 0) return PC_OK;
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
+                     watch, K, out, T ? visit : nullptr, static_cast<hipStream_t>(stream));
 }
 
 int pc_masked_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
@@ -253,6 +275,27 @@ int pc_masked_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_
                      static_cast<hipStream_t>(stream));
 }
 
+int pc_masked_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                        const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,
+                        const int32_t *target, const int32_t *via, int32_t Kv, const int32_t *forbid,
+                        int32_t Kf, int32_t *dist, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(V >= 0 && Q >= 0 && n_adj >= 0, "pc_masked_reach_via: negative size");
+    PC_REQUIRE(Kv >= 0 && Kv <= 32 && Kf >= 0 && Kf <= 32, "pc_masked_reach_via: Kv=%d Kf=%d out of [0, 32]", Kv,
+               Kf);
+    PC_REQUIRE(Q == 0 || (src && allowed && target && dist), "pc_masked_reach_via: null src/allowed/target/dist");
+    PC_REQUIRE(Q == 0 || Kv == 0 || via, "pc_masked_reach_via: null via");
+    PC_REQUIRE(Q == 0 || Kf == 0 || forbid, "pc_masked_reach_via: null forbid");
+    PC_REQUIRE(V == 0 || (adj_off && region), "pc_masked_reach_via: null adj_off/region");
+    PC_REQUIRE(n_adj == 0 || adj, "pc_masked_reach_via: null adj");
+    if (Q == 0 && V == 0) return PC_OK;
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_reach_via(ctx, V, adj_off, adj, n_adj, region, Q, src, allowed, target, via, Kv, forbid, Kf, dist,
+                         static_cast<hipStream_t>(stream));
+}
+
 int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
               int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
               const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass, uint8_t *reason,
@@ -268,8 +311,28 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
     PC_REQUIRE(T == 0 || traces, "pc_report: null traces");
     PC_REQUIRE(Q == 0 || reach, "pc_report: null reach");
     PC_HIP(ctx, hipSetDevice(ctx->device));
-    return run_report(ctx, I, intents, rows, feasible, W, popcnt, N, traces, T, expect, reach, Q, pass, reason,
-                      summary, static_cast<hipStream_t>(stream));
+    return run_report(ctx, I, intents, rows, feasible, W, popcnt, N, traces, T, expect, reach, Q, nullptr, nullptr,
+                      pass, reason, summary, static_cast<hipStream_t>(stream));
+}
+
+int pc_report_paths(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
+                    int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
+                    const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
+                    const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary,
+                    void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(I >= 0 && rows >= 0 && W >= 0 && N >= 0 && T >= 0 && Q >= 0, "pc_report_paths: negative size");
+    PC_REQUIRE(int64_t(W) * 64 >= N, "pc_report_paths: W=%d too small for N=%d", W, N);
+    PC_REQUIRE(summary, "pc_report_paths: null summary");
+    PC_REQUIRE(I == 0 || (intents && expect && pass && reason && pexp), "pc_report_paths: null intent arrays");
+    PC_REQUIRE(rows == 0 || (popcnt && (W == 0 || feasible)), "pc_report_paths: null feasible/popcnt");
+    PC_REQUIRE(T == 0 || (traces && visit), "pc_report_paths: null traces/visit");
+    PC_REQUIRE(Q == 0 || reach, "pc_report_paths: null reach");
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_report(ctx, I, intents, rows, feasible, W, popcnt, N, traces, T, expect, reach, Q, visit, pexp, pass,
+                      reason, summary, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

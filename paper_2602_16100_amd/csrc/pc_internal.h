@@ -94,17 +94,22 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
 
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
-              const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, pc_trace_out *out,
-              hipStream_t stream);
+              const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *watch, int32_t K,
+              pc_trace_out *out, uint32_t *visit, hipStream_t stream);
 
 int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
               const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,
               const int32_t *target, int32_t *dist, hipStream_t stream);
 
+int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                  const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,
+                  const int32_t *target, const int32_t *via, int32_t Kv, const int32_t *forbid, int32_t Kf,
+                  int32_t *dist, hipStream_t stream);
+
 int run_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
                int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
-               const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass,
-               uint8_t *reason, pc_summary *summary, hipStream_t stream);
+               const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
+               const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary, hipStream_t stream);
 
 // ---------------------------------------------------------------- device helpers
 __device__ __forceinline__ bool pc_range_ok(int64_t b, int64_t e, int64_t n)

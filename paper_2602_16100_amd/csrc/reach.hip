@@ -21,6 +21,8 @@
 //   queue  : larger graphs: one workgroup per query, frontier queue in
 //            scratch, the distance row itself (or a scratch row, with
 //            targets) as the visited set claimed with compare-and-swap.
+#include <algorithm>
+
 #include "pc_internal.h"
 
 namespace {
@@ -33,6 +35,26 @@ __device__ __forceinline__ bool allowed_v(const uint8_t *region, uint32_t A, int
 {
     const uint32_t r = region[v];
     return r < 32 && ((A >> r) & 1u);
+}
+
+// Is v in the forbidden list of one query (Kf entries, -1 = unused)?
+__device__ __forceinline__ bool forbidden_v(const int32_t *__restrict__ fl, int32_t Kf, int32_t v)
+{
+    for (int32_t k = 0; k < Kf; ++k)
+        if (fl[k] == v) return true;
+    return false;
+}
+
+// Waypoint / forbidden lists: every entry must be -1 or a vertex.
+__global__ void k_rc_id_check(int64_t n, const int32_t *__restrict__ ids, int32_t V, uint32_t *__restrict__ d_err)
+{
+    bool bad = false;
+    for (int64_t i = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; i < n;
+         i += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int32_t v = ids[i];
+        bad |= (v < -1 || v >= V);
+    }
+    if (bad) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
 __global__ void k_rc_validate(int32_t V, const int32_t *__restrict__ adj_off, const int32_t *__restrict__ adj,
@@ -71,7 +93,9 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                                                               const int32_t *__restrict__ src,
                                                               const uint32_t *__restrict__ allowed,
                                                               const int32_t *__restrict__ target,
-                                                              int32_t *__restrict__ dist)
+                                                              int32_t *__restrict__ dist,
+                                                              const int32_t *__restrict__ forbid, int32_t Kf,
+                                                              int32_t qdiv)
 {
     extern __shared__ uint64_t lds[];
     uint64_t *vis = lds;
@@ -95,7 +119,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         reg[v] = region[v];
     }
     if (tid < 64) {
-        const uint32_t A = lane < nq ? allowed[q0 + lane] : 0u;
+        const uint32_t A = lane < nq ? allowed[(q0 + lane) / qdiv] : 0u;
         for (int r = 0; r < 32; ++r) {
             const uint64_t m = __ballot((A >> r) & 1u);
             if (lane == 0) rmask[r] = m;
@@ -103,16 +127,27 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     }
     if (tid == 0) nfr[0] = nfr[1] = 0;
     __syncthreads();
+    // forbidden vertices start out visited, so they are never entered
+    if (Kf > 0) {
+        if (tid < 64 && lane < nq) {
+            const int32_t *fl = forbid + static_cast<int64_t>((q0 + lane) / qdiv) * Kf;
+            for (int32_t k = 0; k < Kf; ++k) {
+                const int32_t f = fl[k];
+                if (f >= 0 && f < V) atomicOr(reinterpret_cast<unsigned long long *>(&vis[f]), 1ull << lane);
+            }
+        }
+        __syncthreads();
+    }
     // sources; per-query result state lives in wave 0, lane = query
     int32_t res = -1, tgt = -1;
     bool done = true;
     if (tid < 64 && lane < nq) {
         const int32_t q = q0 + lane;
         const int32_t s = src[q];
-        const bool s_ok = s >= 0 && s < V && allowed_v(reg, allowed[q], s);
+        const bool s_ok = s >= 0 && s < V && allowed_v(reg, allowed[q / qdiv], s) && !((vis[s] >> lane) & 1);
         if (target) {
             tgt = target[q];
-            done = !(s_ok && tgt >= 0 && tgt < V);
+            done = !(s_ok && tgt >= 0 && tgt < V && !((vis[tgt] >> lane) & 1));
         }
         if (s_ok) {
             atomicOr(reinterpret_cast<unsigned long long *>(&fr[s]), 1ull << lane);
@@ -135,7 +170,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         bool t_allowed = false;
         if (target && !done) {
             const int64_t b64 = adj_off[tgt], e64 = adj_off[tgt + 1];
-            t_allowed = allowed_v(reg, allowed[q0 + lane], tgt);
+            t_allowed = allowed_v(reg, allowed[(q0 + lane) / qdiv], tgt);
             if (t_allowed && pc_range_ok(b64, e64, n_adj)) {
                 b = static_cast<int32_t>(b64);
                 deg = static_cast<int32_t>(e64 - b64);
@@ -260,17 +295,20 @@ __global__ __launch_bounds__(kQueueThreads) void k_rc_queue(int32_t V, const int
                                                             const uint32_t *__restrict__ allowed,
                                                             const int32_t *__restrict__ target,
                                                             int32_t *__restrict__ dist, int32_t *__restrict__ qbuf_all,
-                                                            int32_t *__restrict__ rows_all)
+                                                            int32_t *__restrict__ rows_all,
+                                                            const int32_t *__restrict__ forbid, int32_t Kf,
+                                                            int32_t qdiv)
 {
     __shared__ int32_t tail_s;
     const int tid = threadIdx.x;
     int32_t *qbuf = qbuf_all + static_cast<int64_t>(blockIdx.x) * V;
     for (int32_t q = blockIdx.x; q < Q; q += gridDim.x) {
         int32_t *drow = target ? rows_all + static_cast<int64_t>(blockIdx.x) * V : dist + static_cast<int64_t>(q) * V;
-        const uint32_t A = allowed[q];
+        const uint32_t A = allowed[q / qdiv];
         const int32_t s = src[q];
         const int32_t tgt = target ? target[q] : -1;
-        const bool s_ok = s >= 0 && s < V && allowed_v(region, A, s);
+        const int32_t *fl = Kf > 0 ? forbid + static_cast<int64_t>(q / qdiv) * Kf : nullptr;
+        const bool s_ok = s >= 0 && s < V && allowed_v(region, A, s) && !forbidden_v(fl, Kf, s);
         const bool t_ok = !target || (tgt >= 0 && tgt < V);
         if (tid == 0) {
             tail_s = 0;
@@ -290,7 +328,7 @@ __global__ __launch_bounds__(kQueueThreads) void k_rc_queue(int32_t V, const int
                 if (!pc_range_ok(b, e, n_adj)) continue;
                 for (int64_t p = b; p < e; ++p) {
                     const int32_t v = adj[p];
-                    if (v < 0 || v >= V || !allowed_v(region, A, v)) continue;
+                    if (v < 0 || v >= V || !allowed_v(region, A, v) || forbidden_v(fl, Kf, v)) continue;
                     if (atomicCAS(&drow[v], -1, d + 1) == -1) qbuf[atomicAdd(&tail_s, 1)] = v;
                 }
             }
@@ -312,9 +350,10 @@ __global__ __launch_bounds__(kQueueThreads) void k_rc_queue(int32_t V, const int
 
 }  // namespace
 
-int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
-              const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed, const int32_t *target,
-              int32_t *dist, hipStream_t stream)
+namespace {
+
+void validate(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+              const uint8_t *region, int32_t Q, const int32_t *src, const int32_t *target, hipStream_t stream)
 {
     const int64_t nval = (V > Q ? V : Q) > n_adj ? (V > Q ? V : Q) : n_adj;
     if (nval > 0) {
@@ -322,9 +361,16 @@ int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
         if (blocks > 4096) blocks = 4096;
         PC_TIMED(ctx, "k_rc_validate", stream, hipLaunchKernelGGL(k_rc_validate, dim3(static_cast<unsigned>(blocks)), dim3(256), 0, stream, V, adj_off, adj,
                            n_adj, region, Q, src, target, ctx->d_err));
-        PC_LAUNCH_CHECK(ctx);
     }
-    if (Q == 0) return PC_OK;
+}
+
+// BFS of Q queries; query j's allowed mask is allowed[j / qdiv] and its
+// forbidden list forbid[(j / qdiv) * Kf ...] (Kf = 0: none).  Takes the
+// context's arena when it needs scratch.
+int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj, const uint8_t *region,
+        int32_t Q, const int32_t *src, const uint32_t *allowed, const int32_t *target, int32_t *dist,
+        const int32_t *forbid, int32_t Kf, int32_t qdiv, hipStream_t stream)
+{
     if (!target) launch_fill_u32(reinterpret_cast<uint32_t *>(dist), static_cast<size_t>(Q) * V, 0xFFFFFFFFu, stream);
     if (V == 0) {
         if (target) launch_fill_u32(reinterpret_cast<uint32_t *>(dist), static_cast<size_t>(Q), 0xFFFFFFFFu, stream);
@@ -348,7 +394,7 @@ int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
             PC_TIMED(ctx, "k_rc_bitset", stream,
                      hipLaunchKernelGGL(kern, grid_b, dim3(kBitsetThreads), lds, stream, V, adj_off, adj, n_adj,
-                                        region, Q, src, allowed, target, dist));
+                                        region, Q, src, allowed, target, dist, forbid, Kf, qdiv));
             PC_LAUNCH_CHECK(ctx);
             return PC_OK;
         };
@@ -371,7 +417,120 @@ int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
     carve(real);
     if (target) launch_fill_u32(reinterpret_cast<uint32_t *>(rows), static_cast<size_t>(grid) * V, 0xFFFFFFFFu, stream);
     PC_TIMED(ctx, "k_rc_queue", stream, hipLaunchKernelGGL(k_rc_queue, dim3(static_cast<unsigned>(grid)), dim3(kQueueThreads), 0, stream, V, adj_off, adj,
-                       n_adj, region, Q, src, allowed, target, dist, qbuf, rows));
+                       n_adj, region, Q, src, allowed, target, dist, qbuf, rows, forbid, Kf, qdiv));
+    PC_LAUNCH_CHECK(ctx);
+    return PC_OK;
+}
+
+// Leg k of query q (k <= m, m = waypoints before the first -1) runs from the
+// previous waypoint (or src) to the next one (or target); legs past m are
+// inactive (src -1).
+__global__ void k_rc_legs(int32_t Q, const int32_t *__restrict__ src, const int32_t *__restrict__ target,
+                          const int32_t *__restrict__ via, int32_t Kv, int32_t *__restrict__ leg_src,
+                          int32_t *__restrict__ leg_tgt)
+{
+    const int32_t q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= Q) return;
+    const int32_t *w = via + static_cast<int64_t>(q) * Kv;
+    int32_t *ls = leg_src + static_cast<int64_t>(q) * (Kv + 1);
+    int32_t *lt = leg_tgt + static_cast<int64_t>(q) * (Kv + 1);
+    int32_t from = src[q];
+    bool active = true;
+    for (int32_t k = 0; k <= Kv; ++k) {
+        const int32_t nxt = k < Kv ? w[k] : -1;
+        if (!active) {
+            ls[k] = -1;
+            lt[k] = -1;
+        } else if (nxt == -1) {  // last leg: to the target
+            ls[k] = from;
+            lt[k] = target[q];
+            active = false;
+        } else {
+            ls[k] = from;
+            lt[k] = nxt;
+            from = nxt;
+        }
+    }
+}
+
+// dist[q] = sum of the distances of q's active legs, -1 if any is -1
+// (saturating at INT32_MAX).
+__global__ void k_rc_via_sum(int32_t Q, const int32_t *__restrict__ via, int32_t Kv,
+                             const int32_t *__restrict__ leg_dist, int32_t *__restrict__ dist)
+{
+    const int32_t q = blockIdx.x * blockDim.x + threadIdx.x;
+    if (q >= Q) return;
+    const int32_t *w = via + static_cast<int64_t>(q) * Kv;
+    const int32_t *ld = leg_dist + static_cast<int64_t>(q) * (Kv + 1);
+    int64_t total = 0;
+    for (int32_t k = 0; k <= Kv; ++k) {
+        const int32_t d = ld[k];
+        if (d < 0) {
+            total = -1;
+            break;
+        }
+        total += d;
+        if (k == Kv || w[k] == -1) break;
+    }
+    dist[q] = static_cast<int32_t>(total > 0x7FFFFFFF ? 0x7FFFFFFF : total);
+}
+
+}  // namespace
+
+int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+              const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed, const int32_t *target,
+              int32_t *dist, hipStream_t stream)
+{
+    validate(ctx, V, adj_off, adj, n_adj, region, Q, src, target, stream);
+    PC_LAUNCH_CHECK(ctx);
+    return bfs(ctx, V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist, nullptr, 0, 1, stream);
+}
+
+int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                  const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,
+                  const int32_t *target, const int32_t *via, int32_t Kv, const int32_t *forbid, int32_t Kf,
+                  int32_t *dist, hipStream_t stream)
+{
+    validate(ctx, V, adj_off, adj, n_adj, region, Q, src, target, stream);
+    const int64_t nv = static_cast<int64_t>(Q) * Kv, nf = static_cast<int64_t>(Q) * Kf;
+    if (nv > 0)
+        PC_TIMED(ctx, "k_rc_id_check", stream,
+                 hipLaunchKernelGGL(k_rc_id_check, dim3(static_cast<unsigned>(std::min<int64_t>((nv + 255) / 256, 4096))),
+                                    dim3(256), 0, stream, nv, via, V, ctx->d_err));
+    if (nf > 0)
+        PC_TIMED(ctx, "k_rc_id_check", stream,
+                 hipLaunchKernelGGL(k_rc_id_check, dim3(static_cast<unsigned>(std::min<int64_t>((nf + 255) / 256, 4096))),
+                                    dim3(256), 0, stream, nf, forbid, V, ctx->d_err));
+    PC_LAUNCH_CHECK(ctx);
+    if (Q == 0) return PC_OK;
+    if (Kv == 0)
+        return bfs(ctx, V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist, forbid, Kf, 1, stream);
+    // legs [Q][Kv + 1] (sources, targets, distances) in the auxiliary
+    // buffer; leg j belongs to query j / (Kv + 1)
+    const int64_t nl = static_cast<int64_t>(Q) * (Kv + 1);
+    if (nl > 0x7FFFFFFF) return pc_set_error(ctx, PC_EINVAL, "pc_masked_reach_via: Q*(Kv+1) over 2^31 legs");
+    int32_t *leg_src, *leg_tgt, *leg_dist;
+    auto carve = [&](Carver &c) {
+        leg_src = c.take<int32_t>(static_cast<size_t>(nl));
+        leg_tgt = c.take<int32_t>(static_cast<size_t>(nl));
+        leg_dist = c.take<int32_t>(static_cast<size_t>(nl));
+    };
+    Carver dry{nullptr, 0};
+    carve(dry);
+    int rc = pc_ensure_aux(ctx, dry.off);
+    if (rc) return rc;
+    Carver real{ctx->aux, 0};
+    carve(real);
+    const unsigned qb = static_cast<unsigned>((Q + 255) / 256);
+    PC_TIMED(ctx, "k_rc_legs", stream,
+             hipLaunchKernelGGL(k_rc_legs, dim3(qb), dim3(256), 0, stream, Q, src, target, via, Kv, leg_src,
+                                leg_tgt));
+    PC_LAUNCH_CHECK(ctx);
+    rc = bfs(ctx, V, adj_off, adj, n_adj, region, static_cast<int32_t>(nl), leg_src, allowed, leg_tgt, leg_dist,
+             forbid, Kf, Kv + 1, stream);
+    if (rc) return rc;
+    PC_TIMED(ctx, "k_rc_via_sum", stream,
+             hipLaunchKernelGGL(k_rc_via_sum, dim3(qb), dim3(256), 0, stream, Q, via, Kv, leg_dist, dist));
     PC_LAUNCH_CHECK(ctx);
     return PC_OK;
 }

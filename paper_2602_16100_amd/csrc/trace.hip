@@ -53,6 +53,16 @@ constexpr int kCountPad = 32;  // live-trace counters are 128 bytes apart: conte
 // wave-uniform value this lowers to register-indexed moves (s_set_gpr_idx).
 typedef uint32_t v16u __attribute__((ext_vector_type(16)));
 
+// Bit k set iff slot k of trace t's watch list names switch s (K = 0: none).
+__device__ __forceinline__ uint32_t watch_bits(const int32_t *__restrict__ watch, int32_t K, int32_t t, int32_t s)
+{
+    uint32_t m = 0;
+    const int32_t *w = watch + static_cast<int64_t>(t) * K;
+    for (int32_t k = 0; k < K; ++k)
+        if (w[k] == s) m |= 1u << k;
+    return m;
+}
+
 __device__ __forceinline__ uint32_t jur_bit(const uint8_t *jur, int32_t s)
 {
     const uint32_t j = jur[s];
@@ -164,7 +174,8 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
                                                  int32_t *__restrict__ hops, int32_t *__restrict__ rank,
                                                  int32_t *__restrict__ live, int32_t *__restrict__ nlive,
                                                  int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
-                                                 uint32_t *__restrict__ d_err)
+                                                 const int32_t *__restrict__ watch, int32_t K,
+                                                 uint32_t *__restrict__ visit, uint32_t *__restrict__ d_err)
 {
     __shared__ int32_t nloc, base;
     if (threadIdx.x == 0) nloc = 0;
@@ -183,9 +194,11 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
             o.hops = 0;
             o.state = PC_MISS;
             out[t] = o;
+            if (visit) visit[t] = 0;
         } else {
             cur[t] = s;
             jm[t] = jur_bit(jur, s);
+            if (visit) visit[t] = watch_bits(watch, K, t, s);
             hops[t] = 0;
             rank[t] = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
             slot = atomicAdd(&nloc, 1);
@@ -290,6 +303,9 @@ struct Level {
     int32_t *nlive_next;
     int32_t *counts_next;   // live traces per switch after this level
     pc_trace_out *out;
+    const int32_t *watch;   // [T][K] switches whose visit is recorded
+    int32_t K;
+    uint32_t *visit;        // [T] or nullptr
 };
 
 // Per level: bucket offsets boff = exclusive scan of counts (which are
@@ -497,6 +513,7 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
                 lv.cur[t] = next;
                 lv.hops[t] = h + 1;
                 lv.jm[t] |= jur_bit(lv.jur, next);
+                if (lv.visit) lv.visit[t] |= watch_bits(lv.watch, lv.K, t, next);
                 lv.rank[t] = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
                 slot = atomicAdd(&nmove, 1);
             }
@@ -520,7 +537,9 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                                                  const pc_key *__restrict__ hdr, int32_t ttl,
                                                  const int32_t *__restrict__ live, const int32_t *__restrict__ nlive,
                                                  const int32_t *__restrict__ cur, const uint32_t *__restrict__ jm0,
-                                                 const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out)
+                                                 const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out,
+                                                 const int32_t *__restrict__ watch, int32_t K,
+                                                 uint32_t *__restrict__ visit)
 {
     __shared__ unsigned long long best;
     const int32_t n = *nlive;
@@ -529,6 +548,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
         const pc_key h = hdr[t];
         int32_t s = cur[t];
         uint32_t jm = jm0[t];
+        uint32_t vis = visit ? visit[t] : 0u;
         int32_t hops = hops0[t];
         for (;;) {
             if (threadIdx.x == 0) best = kNoMatch;
@@ -552,12 +572,16 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                                          &port);
             __syncthreads();  // everyone has read `best` before it is reset
             if (state >= 0) {
-                if (threadIdx.x == 0) write_out(out, t, jm, s, port, hops, state);
+                if (threadIdx.x == 0) {
+                    write_out(out, t, jm, s, port, hops, state);
+                    if (visit) visit[t] = vis;
+                }
                 break;
             }
             s = next;
             hops += 1;
             jm |= jur_bit(jur, s);
+            if (visit) vis |= watch_bits(watch, K, t, s);
         }
     }
 }
@@ -573,8 +597,8 @@ unsigned grid_for(int64_t n, int threads)
 
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
-              const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, pc_trace_out *out,
-              hipStream_t stream)
+              const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *watch, int32_t K,
+              pc_trace_out *out, uint32_t *visit, hipStream_t stream)
 {
     struct Bufs {
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
@@ -637,6 +661,13 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         }
     }
     if (T == 0) return PC_OK;
+    if (visit && K > 0) {
+        PC_TIMED(ctx, "k_tr_watch_check", stream,
+                 hipLaunchKernelGGL(k_tr_port_check, dim3(grid_for(static_cast<int64_t>(T) * K, 256)), dim3(256), 0,
+                                    stream, static_cast<int64_t>(T) * K, watch, S, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    if (!visit) K = 0;
 
     // ---- level-synchronous walk
     int32_t *d_n = ctx->d_small;  // [0], [1]: live counts of the two live lists
@@ -646,7 +677,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
     }
     PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
-                       B.hops, B.rank, B.live0, d_n, B.counts0, out, ctx->d_err));
+                       B.hops, B.rank, B.live0, d_n, B.counts0, out, watch, K, visit, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
@@ -674,7 +705,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_TIMED(ctx, "k_tr_walk", stream,
                      hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
                                         rule_off, rules, B.gcount, B.gofs, B.filt, hdr, ttl, live_cur, n_cur, B.cur,
-                                        B.jm, B.hops, out));
+                                        B.jm, B.hops, out, watch, K, visit));
             PC_LAUNCH_CHECK(ctx);
             break;
         }
@@ -685,8 +716,8 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                  hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, T,
                                     B.cur, B.rank, B.boff, B.bucket));
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
-        const Level lv{S, T, port_off, port_peer, n_ports, jur, ttl, B.cur, B.jm, B.hops, B.rank, live_nxt, n_nxt,
-                       cnt_nxt, out};
+        const Level lv{S,     T,     port_off, port_peer, n_ports, jur,   ttl, B.cur, B.jm,
+                       B.hops, B.rank, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit};
         // at most nlive / kChunk + (switches with a partial chunk) items
         const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);
         PC_TIMED(ctx, "k_tr_match", stream,

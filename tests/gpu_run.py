@@ -77,3 +77,57 @@ def run_workload(wl):
         out["reach"] = out.pop("_r").cpu().numpy()
     out["flags"] = ctx.data_errors(clear=True)
     return out
+
+
+def trace_watch(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, watch):
+    out, visit = pc.pc_trace_flows_watch(S, dev(port_off), dev(port_peer), dev(jur), dev(rule_off), dev(rules),
+                                         dev(np.ascontiguousarray(hdr, np.uint32)), dev(ingress), ttl,
+                                         dev(np.ascontiguousarray(watch, np.int32)))
+    torch.cuda.synchronize()
+    return pc.records(out, pc.TRACE_OUT_DT), visit.cpu().numpy().view(np.uint32)
+
+
+def reach_via(V, adj_off, adj, region, src, allowed, target, via, forbid):
+    d = pc.pc_masked_reach_via(V, dev(adj_off), dev(adj), dev(region), dev(src), dev(allowed), dev(target),
+                               dev(np.ascontiguousarray(via, np.int32)), dev(np.ascontiguousarray(forbid, np.int32)))
+    torch.cuda.synchronize()
+    return d.cpu().numpy()
+
+
+def report_paths(intents, feasible, popcnt, N, traces, expect, reach_d, visit, pexp):
+    f = torch.from_numpy(np.ascontiguousarray(feasible).view(np.int64)).cuda()
+    p = torch.from_numpy(np.ascontiguousarray(popcnt).view(np.int32)).cuda()
+    t = torch.from_numpy(np.ascontiguousarray(traces).view(np.uint8).reshape(-1, 12)).cuda()
+    r = torch.from_numpy(np.ascontiguousarray(reach_d, np.int32)).cuda()
+    v = torch.from_numpy(np.ascontiguousarray(visit, np.uint32).view(np.int32)).cuda()
+    pss, reason, summ = pc.pc_report_paths(dev(intents), f, p, N, t, dev(expect), r, v, dev(pexp))
+    torch.cuda.synchronize()
+    return (pss.cpu().numpy().view(np.uint64), reason.cpu().numpy(),
+            pc.records(summ, pc.SUMMARY_DT)[0])
+
+
+def run_paths_workload(wl):
+    """All stages with the path constraints (watch lists, waypoints,
+    forbidden switches), device-resident between stages."""
+    out = {}
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    f, p = pc.pc_eval_selectors(dev(wl["labels"]), dev(wl["pred_off"]), dev(wl["preds"]))
+    t, v = pc.pc_trace_flows_watch(wl["S"], dev(wl["port_off"]), dev(wl["port_peer"]), dev(wl["jur"]),
+                                   dev(wl["rule_off"]), dev(wl["rules"]), dev(wl["hdr"]), dev(wl["ingress"]),
+                                   wl["ttl"], dev(wl["watch"]))
+    r = pc.pc_masked_reach_via(wl["V"], dev(wl["adj_off"]), dev(wl["adj"]), dev(wl["region"]), dev(wl["src"]),
+                               dev(wl["allowed"]), dev(wl["target"]), dev(wl["via"]), dev(wl["forbid"]))
+    pss, reason, summ = pc.pc_report_paths(dev(wl["intents"]), f, p, wl["N"], t, dev(wl["expect"]), r, v,
+                                           dev(wl["pexp"]))
+    torch.cuda.synchronize()
+    out["feasible"] = f.cpu().numpy().view(np.uint64)
+    out["popcnt"] = p.cpu().numpy().view(np.uint32)
+    out["traces"] = pc.records(t, pc.TRACE_OUT_DT)
+    out["visit"] = v.cpu().numpy().view(np.uint32)
+    out["reach"] = r.cpu().numpy()
+    out["pass"] = pss.cpu().numpy().view(np.uint64)
+    out["reason"] = reason.cpu().numpy()
+    out["summary"] = pc.records(summ, pc.SUMMARY_DT)[0]
+    out["flags"] = ctx.data_errors(clear=True)
+    return out

@@ -84,7 +84,7 @@ def test_cfg5_end_to_end_sampled(g, orc):
     reason = gp["reason"]
     bits = np.unpackbits(gp["pass"].view(np.uint8), bitorder="little")[:I]
     assert np.array_equal(bits == 1, (reason & 0x7F) == 0)
-    hist = np.zeros((4, 8), np.uint64)
+    hist = np.zeros((4, 16), np.uint64)
     np.add.at(hist, (wl["intents"]["kind"] & 3, reason & 0x7F), 1)
     assert np.array_equal(gp["summary"]["counts"], hist)
     # a passing network intent has a compliant path no longer than its trace

@@ -1,0 +1,237 @@
+"""Parity of the waypoint and forbidden-switch checks (pc_trace_flows_watch,
+pc_masked_reach_via, pc_report_paths) with the CPU oracle, bit-exact, on
+seeded inputs: the tiny end-to-end case, small combined workloads, fat-trees
+with long and full watch lists, both BFS paths (LDS bitset and queue), and
+malformed lists."""
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+
+
+@pytest.fixture(scope="module")
+def g():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import gpu_run
+    return gpu_run
+
+
+@pytest.fixture(params=["buckets", "default", "walk"])
+def trace_path(request, monkeypatch):
+    if request.param == "buckets":
+        monkeypatch.setenv("PC_TRACE_WALK_MAX", "0")
+    elif request.param == "walk":
+        monkeypatch.setenv("PC_TRACE_WALK_MAX", str(10**9))
+    return request.param
+
+
+def _same(a, b, what):
+    a, b = np.asarray(a), np.asarray(b)
+    assert a.shape == b.shape, (what, a.shape, b.shape)
+    bad = np.argwhere(a != b)
+    assert bad.size == 0, f"{what}: first mismatch at {tuple(bad[0])}: gpu {a[tuple(bad[0])]} oracle {b[tuple(bad[0])]}"
+
+
+def _same_traces(a, b):
+    for f in ("jmask", "last_switch", "last_port", "hops", "state"):
+        _same(a[f], b[f], f)
+
+
+def _oracle_paths(orc, wl):
+    oo = orc.run_workload(wl)
+    tr, visit, terr = orc.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+                                wl["hdr"], wl["ingress"], wl["ttl"], watch=wl["watch"])
+    d, rerr = orc.reach_via(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"],
+                            wl["target"], wl["via"], wl["forbid"])
+    pss, reason, summ, perr = orc.report(wl["intents"], oo["feasible"], oo["popcnt"], wl["N"], tr, wl["expect"], d,
+                                         visit, wl["pexp"])
+    return dict(feasible=oo["feasible"], popcnt=oo["popcnt"], traces=tr, visit=visit, reach=d, pass_=pss,
+                reason=reason, summary=summ, flags=oo["sel_err"] | terr | rerr | perr)
+
+
+def _check_paths(g, orc, wl):
+    gp = g.run_paths_workload(wl)
+    oo = _oracle_paths(orc, wl)
+    _same(gp["feasible"], oo["feasible"], "feasible")
+    _same(gp["popcnt"], oo["popcnt"], "popcnt")
+    _same_traces(gp["traces"], oo["traces"])
+    _same(gp["visit"], oo["visit"], "visit")
+    _same(gp["reach"], oo["reach"], "reach_via")
+    _same(gp["reason"], oo["reason"], "reason")
+    _same(gp["pass"], oo["pass_"], "pass")
+    for f in ("counts", "no_path"):
+        _same(gp["summary"][f], oo["summary"][f], f)
+    assert gp["flags"] == oo["flags"]
+    return gp, oo
+
+
+@pytest.mark.parametrize("variant", ["rpath", "literal", "dense"])
+def test_paths_cfg1(g, orc, variant, trace_path):
+    _check_paths(g, orc, synth.cfg1(0, variant, paths=True))
+
+
+@pytest.mark.parametrize("seed", [1, 2])
+def test_paths_combined_small(g, orc, seed):
+    wl = synth.combined_workload(seed, 3000 + 37, 16, 8, 4, 700, 3001, paths=True)
+    gp, oo = _check_paths(g, orc, wl)
+    r = oo["reason"] & 0x7F
+    assert (r == 0).sum() > 0 and (r == 8).sum() > 0 and (r == 9).sum() > 0
+
+
+def _watch_lists(rng, T, K, S, ingress):
+    w = rng.integers(-1, S, size=(T, K)).astype(np.int32)
+    w[::5, 0] = ingress[::5]
+    return w
+
+
+@pytest.mark.parametrize("K", [1, 7, 32])
+def test_trace_watch_fat_tree(g, orc, K, trace_path):
+    wl = synth.trace_workload(3, 8, 4, 512, 20000, 24, 3000, variant="rpath")
+    rng = np.random.default_rng(K)
+    watch = _watch_lists(rng, wl["hdr"].shape[0], K, wl["S"], wl["ingress"])
+    tg, vg = g.trace_watch(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+                           wl["hdr"], wl["ingress"], wl["ttl"], watch)
+    to, vo, err = orc.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+                            wl["hdr"], wl["ingress"], wl["ttl"], watch=watch)
+    _same_traces(tg, to)
+    _same(vg, vo, "visit")
+    assert (vo != 0).sum() > 1000
+
+
+def test_trace_watch_dense_loops(g, orc, trace_path):
+    """Random walks with loops and TTL ends; slot k watches switch k, so the
+    visit word is the whole visited set."""
+    rng = np.random.default_rng(3)
+    topo = synth.random_graph(rng, 9, 14, 2, 4)
+    rule_off, rules, _ = synth.build_tables(rng, topo, 40, 0.03, prio="small", prio_range=3)
+    T = 3000
+    hdr = synth.random_keys(rng, T)
+    ingress = rng.integers(0, 9, size=T).astype(np.int32)
+    watch = np.tile(np.arange(9, dtype=np.int32), (T, 1))
+    for ttl in (0, 1, 7, 255):
+        tg, vg = g.trace_watch(9, topo["port_off"], topo["port_peer"], topo["jur"], rule_off, rules, hdr, ingress,
+                               ttl, watch)
+        to, vo, _ = orc.trace(9, topo["port_off"], topo["port_peer"], topo["jur"], rule_off, rules, hdr, ingress,
+                              ttl, watch=watch)
+        _same_traces(tg, to)
+        _same(vg, vo, "visit")
+
+
+def test_trace_watch_malformed(g, orc):
+    import paper_2602_16100_amd as pc
+    wl = synth.trace_workload(6, 4, 2, 64, 500, 8, 100)
+    rng = np.random.default_rng(6)
+    watch = _watch_lists(rng, wl["hdr"].shape[0], 3, wl["S"], wl["ingress"])
+    watch[7, 1] = wl["S"] + 5
+    watch[9, 2] = -4
+    ingress = wl["ingress"].copy()
+    ingress[4] = -3
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    tg, vg = g.trace_watch(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+                           wl["hdr"], ingress, wl["ttl"], watch)
+    flags = ctx.data_errors(clear=True)
+    to, vo, err = orc.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+                            wl["hdr"], ingress, wl["ttl"], watch=watch)
+    _same_traces(tg, to)
+    _same(vg, vo, "visit")
+    assert flags == err == orc.F_SWITCH
+
+
+def _via_lists(rng, Q, V, Kv, Kf, src, target):
+    via = rng.integers(0, V, size=(Q, Kv)).astype(np.int32)
+    m = rng.integers(0, Kv + 1, size=Q)
+    for q in range(Q):
+        via[q, m[q]:] = -1
+    if Kv >= 2:
+        via[::9, 1] = via[::9, 0]
+    forbid = rng.integers(-1, V, size=(Q, Kf)).astype(np.int32)
+    if Kf:
+        forbid[::11, 0] = src[::11]       # forbidden source
+        forbid[5::11, 0] = target[5::11]  # forbidden target
+        if Kv:
+            forbid[7::13, -1] = via[7::13, 0]  # forbidden waypoint (or -1)
+    return via, forbid
+
+
+@pytest.mark.parametrize("Kv,Kf", [(0, 0), (0, 3), (1, 2), (3, 5)])
+@pytest.mark.parametrize("V", [1500, 40000])
+def test_reach_via_rgg(g, orc, V, Kv, Kf):
+    """Bitset (1,500 vertices) and queue (40,000) BFS paths."""
+    Q = 300 if V <= 6016 else 40
+    wl = synth.rgg_workload(V + Kv + Kf, V, 8, Q, mean_degree=7.0, full_rows=False)
+    rng = np.random.default_rng(V + 10 * Kv + Kf)
+    via, forbid = _via_lists(rng, Q, V, Kv, Kf, wl["src"], wl["target"])
+    if V <= 6016 and Kv:
+        # waypoints near the source, so that many walks exist
+        near = wl["adj"][wl["adj_off"][wl["src"]]]
+        via[::2, 0] = near[::2]
+    dg = g.reach_via(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"], wl["target"], via,
+                     forbid)
+    do, _ = orc.reach_via(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"], wl["target"],
+                          via, forbid)
+    _same(dg, do, "reach_via")
+    if V <= 6016:
+        assert (do >= 0).sum() > 10 and (do == -1).sum() > 10
+
+
+def test_reach_via_fat_tree(g, orc):
+    k = 16
+    topo = synth.fat_tree(k, 6)
+    S = topo["S"]
+    rng = np.random.default_rng(4)
+    Q = 2000
+    src = rng.integers(0, k * k, size=Q).astype(np.int32)
+    tgt = rng.integers(0, k * k, size=Q).astype(np.int32)
+    allowed = rng.integers(0, 64, size=Q).astype(np.uint32)
+    allowed[::3] = 63
+    via = rng.integers(k * k, S, size=(Q, 2)).astype(np.int32)  # cores
+    via[::2, 1] = -1
+    forbid = rng.integers(0, S, size=(Q, 2)).astype(np.int32)
+    dg = g.reach_via(S, topo["adj_off"], topo["adj"], topo["jur"], src, allowed, tgt, via, forbid)
+    do, _ = orc.reach_via(S, topo["adj_off"], topo["adj"], topo["jur"], src, allowed, tgt, via, forbid)
+    _same(dg, do, "reach_via")
+    assert (do >= 0).sum() > 100 and (do == -1).sum() > 100
+
+
+def test_reach_via_malformed(g, orc):
+    import paper_2602_16100_amd as pc
+    wl = synth.rgg_workload(2, 800, 4, 70, mean_degree=6.0, full_rows=False)
+    rng = np.random.default_rng(2)
+    via, forbid = _via_lists(rng, 70, 800, 2, 2, wl["src"], wl["target"])
+    via[3, 0] = 5000
+    forbid[4, 1] = -9
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    dg = g.reach_via(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"], wl["target"], via,
+                     forbid)
+    flags = ctx.data_errors(clear=True)
+    do, err = orc.reach_via(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"],
+                            wl["target"], via, forbid)
+    _same(dg, do, "reach_via")
+    assert flags == err == orc.F_SWITCH
+
+
+def test_report_paths_cfg1_visit_patterns(g, orc):
+    """Every combination of must / forbid masks and visit words on the tiny
+    case's traces."""
+    wl = synth.cfg1(0, paths=True)
+    oo = orc.run_workload(wl)
+    rng = np.random.default_rng(8)
+    T = wl["hdr"].shape[0]
+    visit = rng.integers(0, 8, size=T).astype(np.uint32)
+    pexp = np.zeros(wl["intents"].shape[0], synth.PATH_EXPECT_DT)
+    pexp["must"] = rng.integers(0, 8, size=pexp.shape[0])
+    pexp["forbid"] = rng.integers(0, 8, size=pexp.shape[0]) & ~pexp["must"]
+    pg, rg, sg = g.report_paths(wl["intents"], oo["feasible"], oo["popcnt"], wl["N"], oo["traces"], wl["expect"],
+                                oo["reach"], visit, pexp)
+    po, ro, so, _ = orc.report(wl["intents"], oo["feasible"], oo["popcnt"], wl["N"], oo["traces"], wl["expect"],
+                               oo["reach"], visit, pexp)
+    _same(rg, ro, "reason")
+    _same(pg, po, "pass")
+    _same(sg["counts"], so["counts"], "counts")
+    _same(sg["no_path"], so["no_path"], "no_path")
