@@ -57,6 +57,8 @@ def parse():
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach"],
                     help="profiling aid: time one stage only (the JSON line then covers that stage)")
+    ap.add_argument("--no-paths", action="store_true",
+                    help="skip the second timed pass with waypoint / forbidden-switch constraints")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="profiling aid: run a plain device copy of MIB MiB three times (HBM counter calibration)")
     return ap.parse_args()
@@ -79,10 +81,11 @@ def calibrate_copy(mib):
 def make_workload(name):
     import synth
     if name == "cfg5":
-        return synth.cfg5(), ("combined cross-layer validation, seed 4: 50,000 nodes x 64 labels; fat-tree k=48 "
+        return synth.cfg5(paths=True), ("combined cross-layer validation, seed 4: 50,000 nodes x 64 labels; fat-tree k=48 "
                               "(2,880 switches), 16,384 rules/switch, 12 jurisdictions; 1,048,576 intents "
                               "(1/3 compute, 1/3 network, 1/3 hybrid); TTL 32; R-path rule tables")
-    return synth.combined_workload(7, 5000, 64, 16, 8, 2048, 30000), "small combined workload (smoke scale)"
+    return (synth.combined_workload(7, 5000, 64, 16, 8, 2048, 30000, paths=True),
+            "small combined workload (smoke scale)")
 
 
 def sample_subproblem(wl, stride):
@@ -149,6 +152,68 @@ def cpu_baseline(wl, pairs_total, target_s):
     }
 
 
+def time_paths(args, wl, D, pc, ctx, feasible, popcnt):
+    """Second timed pass: the same traces and queries with a required
+    waypoint and two forbidden switches per flow (trace with watch lists,
+    reachability through the waypoint avoiding the forbidden switches,
+    verdict with the path checks).  The selector bitsets of the main pass
+    are reused: the constraints do not touch them."""
+    import torch
+    dev = feasible.device
+    T, Q, I = wl["T"], wl["Q"], wl["I"]
+    traces = torch.empty((T, 12), dtype=torch.uint8, device=dev)
+    visit = torch.empty(T, dtype=torch.int32, device=dev)
+    reach = torch.empty(Q, dtype=torch.int32, device=dev)
+    pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
+    reason = torch.empty(I, dtype=torch.uint8, device=dev)
+    summary = torch.empty(pc.SUMMARY_BYTES, dtype=torch.uint8, device=dev)
+
+    def step():
+        pc.pc_trace_flows_watch(wl["S"], D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                                D["ingress"], wl["ttl"], D["watch"], out=traces, visit=visit, ctx=ctx)
+        pc.pc_masked_reach_via(wl["V"], D["adj_off"], D["adj"], D["region"], D["src"], D["allowed"], D["target"],
+                               D["via"], D["forbid"], dist=reach, ctx=ctx)
+        pc.pc_report_paths(D["intents"], feasible, popcnt, wl["N"], traces, D["expect"], reach, visit, D["pexp"],
+                           pass_=pass_, reason=reason, summary=summary, ctx=ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.profile(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = ctx.profile_read()
+    ctx.profile(False)
+
+    def ktime(prefix):
+        return sum(ms for name, (n, ms) in prof.items() if name.startswith(prefix)) / args.steps
+
+    tr = pc.records(traces, pc.TRACE_OUT_DT)
+    ing = wl["ingress"]
+    started = (ing >= 0) & (ing < wl["S"])
+    lookups = int((tr["hops"][started].astype(np.int64) + 1).sum())
+    via = wl["via"]
+    legs = int(Q + (via >= 0).sum())
+    r = reason.cpu().numpy() & 0x7F
+    return {
+        "constraints": "per flow: 1 required waypoint (on the compiled path with p=1/2), 2 forbidden switches "
+                       "(each on the path with p=1/8); watch lists of 3 switches per trace",
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "entry_ms_per_step": {"pc_trace_flows_watch": ktime("k_tr_"), "pc_masked_reach_via": ktime("k_rc_"),
+                              "pc_report_paths": ktime("k_report")},
+        "flow_hops_per_s_kernel": lookups / (ktime("k_tr_") * 1e-3) if ktime("k_tr_") else None,
+        "reach_legs_per_step": legs,
+        "reach_legs_per_s_kernel": legs / (ktime("k_rc_") * 1e-3) if ktime("k_rc_") else None,
+        "per_kernel": {name: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
+                       for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])},
+        "verdict": {"passed": int((r == 0).sum()), "forbidden_switch": int((r == 8).sum()),
+                    "waypoint_missed": int((r == 9).sum()), "intents": I},
+    }
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -180,7 +245,7 @@ def main():
     reach = torch.empty(Q, dtype=torch.int32, device=dev)
     pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
     reason = torch.empty(I, dtype=torch.uint8, device=dev)
-    summary = torch.empty(libpc.SUMMARY_BYTES, dtype=torch.uint8, device=dev)
+    summary = torch.empty(pc.SUMMARY_BYTES, dtype=torch.uint8, device=dev)
     ctx = pc.context(0)
 
     only = args.only
@@ -275,6 +340,8 @@ def main():
         "verdict": {"passed": passed, "intents": I},
         "data_error_flags": flags,
     }
+    if only == "all" and not args.no_paths:
+        line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, pairs, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -57,6 +57,42 @@ __global__ void k_rc_id_check(int64_t n, const int32_t *__restrict__ ids, int32_
     if (bad) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
+// *flag stays 1 only if every adjacency list is sorted and every valid
+// entry u -> v has its reverse v -> u (a vertex whose offsets are invalid has
+// no entries, so no valid list may name it): then the search from v reaches
+// u exactly when the search from u reaches v, at the same distance.  One
+// wavefront per vertex, its lanes over the vertex's entries.
+__global__ __launch_bounds__(256) void k_rc_symcheck(int32_t V, const int32_t *__restrict__ adj_off,
+                                                     const int32_t *__restrict__ adj, int64_t n_adj,
+                                                     int32_t *__restrict__ flag)
+{
+    const int lane = threadIdx.x & 63;
+    const int32_t waves = gridDim.x * 4;
+    bool bad = false;
+    for (int32_t u = blockIdx.x * 4 + (threadIdx.x >> 6); u < V; u += waves) {
+        const int64_t b = adj_off[u], e = adj_off[u + 1];
+        if (!pc_range_ok(b, e, n_adj)) continue;
+        for (int64_t p = b + lane; p < e; p += 64) {
+            const int32_t v = adj[p];
+            if (p > b && adj[p - 1] > v) bad = true;
+            if (v < 0 || v >= V) continue;
+            int64_t lo = adj_off[v], hi = adj_off[v + 1];
+            if (!pc_range_ok(lo, hi, n_adj)) {
+                bad = true;
+                continue;
+            }
+            const int64_t end = hi;
+            while (lo < hi) {  // first entry >= u
+                const int64_t mid = (lo + hi) >> 1;
+                if (adj[mid] < u) lo = mid + 1;
+                else hi = mid;
+            }
+            if (lo >= end || adj[lo] != u) bad = true;
+        }
+    }
+    if (__ballot(bad) && lane == 0) atomicAnd(flag, 0);
+}
+
 __global__ void k_rc_validate(int32_t V, const int32_t *__restrict__ adj_off, const int32_t *__restrict__ adj,
                               int64_t n_adj, const uint8_t *__restrict__ region, int32_t Q,
                               const int32_t *__restrict__ src, const int32_t *__restrict__ target,
@@ -95,7 +131,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                                                               const int32_t *__restrict__ target,
                                                               int32_t *__restrict__ dist,
                                                               const int32_t *__restrict__ forbid, int32_t Kf,
-                                                              int32_t qdiv)
+                                                              int32_t qdiv, const int32_t *__restrict__ sym)
 {
     extern __shared__ uint64_t lds[];
     uint64_t *vis = lds;
@@ -146,8 +182,11 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         const int32_t s = src[q];
         const bool s_ok = s >= 0 && s < V && allowed_v(reg, allowed[q / qdiv], s) && !((vis[s] >> lane) & 1);
         if (target) {
+            // a target that is not allowed, or forbidden, is never reached:
+            // the query is resolved (-1) without a search
             tgt = target[q];
-            done = !(s_ok && tgt >= 0 && tgt < V && !((vis[tgt] >> lane) & 1));
+            done = !(s_ok && tgt >= 0 && tgt < V && allowed_v(reg, allowed[q / qdiv], tgt) &&
+                     !((vis[tgt] >> lane) & 1));
         }
         if (s_ok) {
             atomicOr(reinterpret_cast<unsigned long long *>(&fr[s]), 1ull << lane);
@@ -165,10 +204,12 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         }
         // A query whose target is allowed and has a neighbour in its
         // frontier at distance d is resolved at d + 1 without expanding
-        // that frontier: list each such target's adjacency once.
+        // that frontier: list each such target's adjacency once.  Only on
+        // a symmetric graph (*sym == 1), where the target's list names
+        // exactly the vertices whose lists name the target.
         int32_t deg = 0, b = 0;
         bool t_allowed = false;
-        if (target && !done) {
+        if (target && !done && *sym == 1) {
             const int64_t b64 = adj_off[tgt], e64 = adj_off[tgt + 1];
             t_allowed = allowed_v(reg, allowed[(q0 + lane) / qdiv], tgt);
             if (t_allowed && pc_range_ok(b64, e64, n_adj)) {
@@ -190,6 +231,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     }
     __syncthreads();
     const int grp = tid / GS, gl = tid % GS;
+    constexpr int kNG = kBitsetThreads / GS;  // groups
     for (int32_t d = 1;; ++d) {
         const int cur = (d - 1) & 1;
         const int32_t nf = nfr[cur];
@@ -198,7 +240,6 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         // adjacency range and frontier word in one round (no dependent load
         // chain per vertex), then the group walks the GS entries, taking
         // each range and word from lane k by shuffle.
-        constexpr int kNG = kBitsetThreads / GS;  // groups
         for (int32_t i0 = grp; i0 < nf; i0 += kNG * GS) {
             const int32_t my = i0 + kNG * gl;
             int32_t b = 0, e = 0;
@@ -309,10 +350,12 @@ __global__ __launch_bounds__(kQueueThreads) void k_rc_queue(int32_t V, const int
         const int32_t tgt = target ? target[q] : -1;
         const int32_t *fl = Kf > 0 ? forbid + static_cast<int64_t>(q / qdiv) * Kf : nullptr;
         const bool s_ok = s >= 0 && s < V && allowed_v(region, A, s) && !forbidden_v(fl, Kf, s);
-        const bool t_ok = !target || (tgt >= 0 && tgt < V);
+        // a target that is not allowed, or forbidden, is never reached
+        const bool t_ok =
+            !target || (tgt >= 0 && tgt < V && allowed_v(region, A, tgt) && !forbidden_v(fl, Kf, tgt));
         if (tid == 0) {
             tail_s = 0;
-            if (s_ok) {
+            if (s_ok && t_ok) {
                 drow[s] = 0;
                 qbuf[0] = s;
                 tail_s = 1;
@@ -364,12 +407,27 @@ void validate(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
     }
 }
 
+// The symmetry flag of the graph, in ctx->d_small[4] (1 = symmetric,
+// sorted lists; see k_rc_symcheck).
+int32_t *symcheck(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
+                  hipStream_t stream)
+{
+    int32_t *sym = ctx->d_small + 4;
+    launch_fill_u32(reinterpret_cast<uint32_t *>(sym), 1, 1u, stream);
+    if (V > 0)
+        PC_TIMED(ctx, "k_rc_symcheck", stream,
+                 hipLaunchKernelGGL(k_rc_symcheck, dim3(static_cast<unsigned>(std::min<int64_t>((V + 3) / 4, 8192))),
+                                    dim3(256), 0, stream, V, adj_off, adj, n_adj, sym));
+    return sym;
+}
+
 // BFS of Q queries; query j's allowed mask is allowed[j / qdiv] and its
-// forbidden list forbid[(j / qdiv) * Kf ...] (Kf = 0: none).  Takes the
+// forbidden list forbid[(j / qdiv) * Kf ...] (Kf = 0: none).  sym: the
+// graph's symmetry flag when the caller has it, else nullptr.  Takes the
 // context's arena when it needs scratch.
 int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj, const uint8_t *region,
         int32_t Q, const int32_t *src, const uint32_t *allowed, const int32_t *target, int32_t *dist,
-        const int32_t *forbid, int32_t Kf, int32_t qdiv, hipStream_t stream)
+        const int32_t *forbid, int32_t Kf, int32_t qdiv, const int32_t *sym, hipStream_t stream)
 {
     if (!target) launch_fill_u32(reinterpret_cast<uint32_t *>(dist), static_cast<size_t>(Q) * V, 0xFFFFFFFFu, stream);
     if (V == 0) {
@@ -385,7 +443,10 @@ int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int6
     hipFuncAttributes fa{};
     PC_HIP(ctx, hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(k_rc_bitset<16>)));  // static LDS
     if (V <= kMaxBitsetV && lds + fa.sharedSizeBytes <= static_cast<size_t>(max_lds)) {
-        // lanes per frontier vertex: a power of two near a third of the mean degree
+        if (!sym && target) sym = symcheck(ctx, V, adj_off, adj, n_adj, stream);
+        if (!sym) sym = ctx->d_small + 5;  // full rows: no look-ahead reads it
+        PC_LAUNCH_CHECK(ctx);
+        // lanes per vertex: a power of two near a third of the mean degree
         const int64_t avg = n_adj / V;
         const int gs = avg <= 12 ? 4 : avg <= 24 ? 8 : avg <= 48 ? 16 : 32;
         const dim3 grid_b(static_cast<unsigned>((Q + 63) / 64));
@@ -394,7 +455,7 @@ int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int6
                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
             PC_TIMED(ctx, "k_rc_bitset", stream,
                      hipLaunchKernelGGL(kern, grid_b, dim3(kBitsetThreads), lds, stream, V, adj_off, adj, n_adj,
-                                        region, Q, src, allowed, target, dist, forbid, Kf, qdiv));
+                                        region, Q, src, allowed, target, dist, forbid, Kf, qdiv, sym));
             PC_LAUNCH_CHECK(ctx);
             return PC_OK;
         };
@@ -424,11 +485,14 @@ int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int6
 
 // Leg k of query q (k <= m, m = waypoints before the first -1) runs from the
 // previous waypoint (or src) to the next one (or target); legs past m are
-// inactive (src -1).
+// inactive (src -1).  On a symmetric graph (*sym == 1) legs 0, 2, 4, ... are
+// searched from their far end, so that legs 2j and 2j + 1 start at the same
+// waypoint and share their frontiers in the workgroup's bitsets.
 __global__ void k_rc_legs(int32_t Q, const int32_t *__restrict__ src, const int32_t *__restrict__ target,
-                          const int32_t *__restrict__ via, int32_t Kv, int32_t *__restrict__ leg_src,
-                          int32_t *__restrict__ leg_tgt)
+                          const int32_t *__restrict__ via, int32_t Kv, const int32_t *__restrict__ sym,
+                          int32_t *__restrict__ leg_src, int32_t *__restrict__ leg_tgt)
 {
+    const bool flip = *sym == 1;
     const int32_t q = blockIdx.x * blockDim.x + threadIdx.x;
     if (q >= Q) return;
     const int32_t *w = via + static_cast<int64_t>(q) * Kv;
@@ -441,14 +505,13 @@ __global__ void k_rc_legs(int32_t Q, const int32_t *__restrict__ src, const int3
         if (!active) {
             ls[k] = -1;
             lt[k] = -1;
-        } else if (nxt == -1) {  // last leg: to the target
-            ls[k] = from;
-            lt[k] = target[q];
-            active = false;
         } else {
-            ls[k] = from;
-            lt[k] = nxt;
-            from = nxt;
+            const int32_t to = nxt == -1 ? target[q] : nxt;  // the last leg ends at the target
+            const bool rev = flip && (k & 1) == 0;
+            ls[k] = rev ? to : from;
+            lt[k] = rev ? from : to;
+            from = to;
+            active = nxt != -1;
         }
     }
 }
@@ -483,7 +546,7 @@ int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj
 {
     validate(ctx, V, adj_off, adj, n_adj, region, Q, src, target, stream);
     PC_LAUNCH_CHECK(ctx);
-    return bfs(ctx, V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist, nullptr, 0, 1, stream);
+    return bfs(ctx, V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist, nullptr, 0, 1, nullptr, stream);
 }
 
 int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
@@ -504,7 +567,8 @@ int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t 
     PC_LAUNCH_CHECK(ctx);
     if (Q == 0) return PC_OK;
     if (Kv == 0)
-        return bfs(ctx, V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist, forbid, Kf, 1, stream);
+        return bfs(ctx, V, adj_off, adj, n_adj, region, Q, src, allowed, target, dist, forbid, Kf, 1, nullptr,
+                   stream);
     // legs [Q][Kv + 1] (sources, targets, distances) in the auxiliary
     // buffer; leg j belongs to query j / (Kv + 1)
     const int64_t nl = static_cast<int64_t>(Q) * (Kv + 1);
@@ -522,12 +586,13 @@ int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t 
     Carver real{ctx->aux, 0};
     carve(real);
     const unsigned qb = static_cast<unsigned>((Q + 255) / 256);
+    const int32_t *sym = symcheck(ctx, V, adj_off, adj, n_adj, stream);
     PC_TIMED(ctx, "k_rc_legs", stream,
-             hipLaunchKernelGGL(k_rc_legs, dim3(qb), dim3(256), 0, stream, Q, src, target, via, Kv, leg_src,
+             hipLaunchKernelGGL(k_rc_legs, dim3(qb), dim3(256), 0, stream, Q, src, target, via, Kv, sym, leg_src,
                                 leg_tgt));
     PC_LAUNCH_CHECK(ctx);
     rc = bfs(ctx, V, adj_off, adj, n_adj, region, static_cast<int32_t>(nl), leg_src, allowed, leg_tgt, leg_dist,
-             forbid, Kf, Kv + 1, stream);
+             forbid, Kf, Kv + 1, sym, stream);
     if (rc) return rc;
     PC_TIMED(ctx, "k_rc_via_sum", stream,
              hipLaunchKernelGGL(k_rc_via_sum, dim3(qb), dim3(256), 0, stream, Q, via, Kv, leg_dist, dist));

@@ -271,6 +271,31 @@ def test_reach_fat_tree_targets(g, orc):
     assert (do >= 0).sum() > 100 and (do == -1).sum() > 100
 
 
+@pytest.mark.parametrize("kind", ["asymmetric", "unsorted", "bad_offsets"])
+def test_reach_targets_on_one_way_graphs(g, orc, kind):
+    """Resolving a target one level early from its own adjacency list is
+    exact only when the lists are symmetric: one-way entries, unsorted lists
+    (which switch the shortcut off) and a vertex with invalid offsets (named
+    by lists it cannot name back) must match the oracle's plain search."""
+    wl = synth.rgg_workload(11, 1200, 4, 130, mean_degree=9.0, full_rows=False)
+    adj_off, adj = wl["adj_off"].copy(), wl["adj"].copy()
+    rng = np.random.default_rng(1)
+    if kind == "asymmetric":
+        for p in rng.choice(adj.shape[0], size=40, replace=False):
+            adj[p] = int(rng.integers(0, wl["V"]))
+        for u in range(wl["V"]):
+            adj[adj_off[u]:adj_off[u + 1]] = np.sort(adj[adj_off[u]:adj_off[u + 1]])
+    elif kind == "unsorted":
+        for u in range(wl["V"]):
+            adj[adj_off[u]:adj_off[u + 1]] = adj[adj_off[u]:adj_off[u + 1]][::-1]
+    else:
+        hub = int(np.argmax(np.diff(adj_off)))
+        adj_off[hub + 1] = adj_off[hub] - 1 if adj_off[hub] > 0 else adj.shape[0] + 5
+    dg = g.reach(wl["V"], adj_off, adj, wl["region"], wl["src"], wl["allowed"], wl["target"])
+    do, _ = orc.reach(wl["V"], adj_off, adj, wl["region"], wl["src"], wl["allowed"], wl["target"])
+    _same(dg, do, "dist")
+
+
 def test_reach_malformed_flags(g, orc):
     import paper_2602_16100_amd as pc
     wl = synth.rgg_workload(2, 800, 4, 70, mean_degree=6.0, full_rows=False)

@@ -235,3 +235,34 @@ def test_report_paths_cfg1_visit_patterns(g, orc):
     _same(pg, po, "pass")
     _same(sg["counts"], so["counts"], "counts")
     _same(sg["no_path"], so["no_path"], "no_path")
+
+
+@pytest.mark.parametrize("kind", ["symmetric", "asymmetric", "unsorted", "bad_offsets"])
+def test_reach_via_leg_direction(g, orc, kind):
+    """Legs are searched from their far end only on symmetric graphs with
+    sorted lists; one-way entries, unsorted lists, or a vertex whose offsets
+    are invalid (push never expands it, yet a neighbour's list names it) must
+    give the forward results."""
+    wl = synth.rgg_workload(11, 1200, 4, 130, mean_degree=9.0, full_rows=False)
+    adj_off, adj = wl["adj_off"].copy(), wl["adj"].copy()
+    rng = np.random.default_rng(1)
+    if kind == "asymmetric":
+        for p in rng.choice(adj.shape[0], size=40, replace=False):
+            adj[p] = int(rng.integers(0, wl["V"]))
+        for u in range(wl["V"]):  # keep each list sorted
+            adj[adj_off[u]:adj_off[u + 1]] = np.sort(adj[adj_off[u]:adj_off[u + 1]])
+    elif kind == "unsorted":
+        for u in range(wl["V"]):
+            adj[adj_off[u]:adj_off[u + 1]] = adj[adj_off[u]:adj_off[u + 1]][::-1]
+    elif kind == "bad_offsets":
+        hub = int(np.argmax(np.diff(adj_off)))
+        adj_off[hub + 1] = adj_off[hub] - 1 if adj_off[hub] > 0 else adj.shape[0] + 5
+    Q = 130
+    near = adj[np.clip(adj_off[wl["src"]], 0, adj.shape[0] - 1)]
+    via = np.stack([near, rng.integers(0, wl["V"], size=Q)], axis=1).astype(np.int32)
+    via[::3, 1] = -1
+    forbid = rng.integers(-1, wl["V"], size=(Q, 2)).astype(np.int32)
+    dg = g.reach_via(wl["V"], adj_off, adj, wl["region"], wl["src"], wl["allowed"], wl["target"], via, forbid)
+    do, _ = orc.reach_via(wl["V"], adj_off, adj, wl["region"], wl["src"], wl["allowed"], wl["target"], via, forbid)
+    _same(dg, do, "reach_via")
+    assert (do >= 0).sum() > 5
