@@ -145,6 +145,9 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     // target look-ahead: the targets' adjacency as (query, entry) pairs
     __shared__ int32_t toff[65], tbeg[64];
     __shared__ unsigned long long found, act;
+    // queries still searching (target mode): resolved queries' frontier
+    // bits are dropped, so their searches stop spreading
+    __shared__ unsigned long long live;
     const int tid = threadIdx.x, lane = tid & 63;
     const int32_t q0 = blockIdx.x * 64;
     const int32_t nq = min(64, Q - q0);
@@ -228,6 +231,8 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         if (lane == 63) toff[64] = x;
         const uint64_t a = __ballot(deg > 0);
         if (lane == 0) act = a;
+        const uint64_t lv = target ? __ballot(!done) : ~0ull;
+        if (lane == 0) live = lv;
     }
     __syncthreads();
     const int grp = tid / GS, gl = tid % GS;
@@ -272,7 +277,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
             if (n) {
                 nx[v] = 0;
                 const uint32_t r = reg[v];
-                n &= (r < 32 ? rmask[r] : 0ull) & ~vis[v];
+                n &= (r < 32 ? rmask[r] : 0ull) & ~vis[v] & live;
                 vis[v] |= n;
                 if (!target) {
                     uint64_t m = n;
@@ -318,6 +323,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
             if (tid == 0) {
                 flag_done = target ? still == 0 : 0;
                 act &= still;
+                if (target) live = still;
             }
         }
         __syncthreads();
