@@ -19,6 +19,10 @@
  *                         all of its checks pass (Automated Validation
  *                         Pipeline, validator check definition); an
  *                         unenforceable intent fails closed.
+ *   - pc_trace_flows_watch, pc_masked_reach_via, pc_report_paths : the same
+ *                         checks with required waypoints and forbidden
+ *                         switches (the routing constraints of a
+ *                         Configuration; must_go / forbidden lists).
  *
  * Conventions shared by every entry point
  *   - Every array argument is a DEVICE pointer owned by the caller; it must
@@ -26,7 +30,7 @@
  *     library keeps no pointer past the call and never frees caller memory.
  *   - `stream` is a hipStream_t (NULL = the legacy default stream).  Every
  *     entry point is asynchronous and stream-ordered, except
- *     pc_trace_flows, which reads back the size of its rule index once and
+ *     pc_trace_flows(_watch), which reads back the size of its rule index once and
  *     one live-trace count per hop level, and pc_data_errors and
  *     pc_profile_read, which wait for the stream.
  *   - Return value: PC_OK, or a negative PC_E* code.  Argument errors are
