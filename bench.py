@@ -55,8 +55,9 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach"],
-                    help="profiling aid: time one stage only (the JSON line then covers that stage)")
+    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths"],
+                    help="profiling aid: time one stage only (the JSON line then covers that stage); 'paths' "
+                         "times only the pass with waypoint / forbidden-switch constraints")
     ap.add_argument("--no-paths", action="store_true",
                     help="skip the second timed pass with waypoint / forbidden-switch constraints")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
@@ -249,6 +250,12 @@ def main():
     ctx = pc.context(0)
 
     only = args.only
+    if only == "paths":
+        # the bitsets the verdict reads, computed once outside the timed pass
+        pc.pc_eval_selectors(D["labels"], D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
+        torch.cuda.synchronize()
+        print(json.dumps({"workload": desc, "paths": time_paths(args, wl, D, pc, ctx, feasible, popcnt)}), flush=True)
+        return
 
     def step():
         if only in ("all", "sel"):
