@@ -199,7 +199,7 @@ def time_paths(args, wl, D, pc, ctx, feasible, popcnt):
     via = wl["via"]
     legs = int(Q + (via >= 0).sum())
     r = reason.cpu().numpy() & 0x7F
-    return {
+    out = {
         "constraints": "per flow: 1 required waypoint (on the compiled path with p=1/2), 2 forbidden switches "
                        "(each on the path with p=1/8); watch lists of 3 switches per trace",
         "ms_per_step": 1e3 * elapsed / args.steps,
@@ -213,6 +213,40 @@ def time_paths(args, wl, D, pc, ctx, feasible, popcnt):
         "verdict": {"passed": int((r == 0).sum()), "forbidden_switch": int((r == 8).sum()),
                     "waypoint_missed": int((r == 9).sum()), "intents": I},
     }
+    if not args.no_cpu_baseline:
+        out["cpu_baseline"] = cpu_baseline_paths(wl, 1e3 * elapsed / args.steps, args.cpu_seconds / 3)
+    return out
+
+
+def cpu_baseline_paths(wl, gpu_ms, target_s):
+    """The oracle on every k-th flow of the constrained pass (traces with
+    watch lists and waypoint reach), scaled to the whole pass."""
+    import oracle
+    threads = len(os.sched_getaffinity(0))
+    env_cap = os.environ.get("OMP_NUM_THREADS")
+    if env_cap and env_cap.isdigit():
+        threads = min(threads, int(env_cap))
+    T = wl["T"]
+
+    def run(stride):
+        idx = np.arange(0, T, stride, dtype=np.int64)
+        t0 = time.perf_counter()
+        oracle.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"], wl["hdr"],
+                     wl["ingress"], wl["ttl"], idx=idx, nthreads=threads, watch=wl["watch"])
+        oracle.reach_via(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"], wl["target"],
+                         wl["via"], wl["forbid"], qidx=idx, nthreads=threads)
+        return time.perf_counter() - t0, idx.shape[0]
+
+    stride = 4096
+    t, n = run(stride)
+    while t < target_s / 2 and stride > 1:
+        stride = max(1, stride // 64, int(stride * max(t, 1e-3) / target_s))
+        t, n = run(stride)
+    est = t * T / n
+    return {"value": T / est, "unit": "constrained flows (trace + waypoint reach) per second, whole-pass estimate",
+            "cores": threads, "kind": "oracle",
+            "sample": f"every {stride}th flow ({n} of {T} traces and reach queries) in {t:.2f} s; whole pass "
+                      f"estimated at {est:.1f} s against {gpu_ms:.2f} ms on the GPU"}
 
 
 def main():
