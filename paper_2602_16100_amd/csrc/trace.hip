@@ -366,6 +366,34 @@ __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, 
     }
 }
 
+// surv = AND over the six chunks c of F[c][x[c]]: GPR index mode stays on
+// for the whole lookup and only its index changes per chunk, and each
+// indexed read feeds the AND directly.  The chunk sets sit in fixed
+// registers v32..v127 (chunk c at v[32 + 16c .. 47 + 16c]); the indices are
+// below 16, so every indexed read stays inside its chunk's sixteen.
+__device__ __forceinline__ uint32_t filter6(const uint32_t (&x)[kChunks], const v16u (&F)[kChunks])
+{
+    uint32_t surv;
+    asm volatile(
+        "s_set_gpr_idx_on %1, gpr_idx(SRC0)\n\t"
+        "v_mov_b32 %0, v32\n\t"
+        "s_set_gpr_idx_idx %2\n\t"
+        "v_and_b32 %0, v48, %0\n\t"
+        "s_set_gpr_idx_idx %3\n\t"
+        "v_and_b32 %0, v64, %0\n\t"
+        "s_set_gpr_idx_idx %4\n\t"
+        "v_and_b32 %0, v80, %0\n\t"
+        "s_set_gpr_idx_idx %5\n\t"
+        "v_and_b32 %0, v96, %0\n\t"
+        "s_set_gpr_idx_idx %6\n\t"
+        "v_and_b32 %0, v112, %0\n\t"
+        "s_set_gpr_idx_off"
+        : "=&v"(surv)
+        : "s"(x[0]), "s"(x[1]), "s"(x[2]), "s"(x[3]), "s"(x[4]), "s"(x[5]), "{v[32:47]}"(F[0]), "{v[48:63]}"(F[1]),
+          "{v[64:79]}"(F[2]), "{v[80:95]}"(F[3]), "{v[96:111]}"(F[4]), "{v[112:127]}"(F[5]));
+    return surv;
+}
+
 // One workgroup per work item = (switch, chunk of at most kChunk lookups of
 // its bucket).  Items are dealt to XCDs in contiguous ranges, so the chunks
 // of one switch share an L2.
@@ -449,13 +477,11 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
                 uint32_t sv[4];
 #pragma unroll
                 for (int k = 0; k < 4; ++k) {
-                    uint32_t surv = ~0u;
+                    uint32_t xi[kChunks];
 #pragma unroll
-                    for (int c = 0; c < kChunks; ++c) {
-                        const uint32_t xv = k == 0 ? X[c].x : k == 1 ? X[c].y : k == 2 ? X[c].z : X[c].w;
-                        surv &= F[c][__builtin_amdgcn_readfirstlane(xv)];
-                    }
-                    sv[k] = surv;
+                    for (int c = 0; c < kChunks; ++c)
+                        xi[c] = __builtin_amdgcn_readfirstlane(k == 0 ? X[c].x : k == 1 ? X[c].y : k == 2 ? X[c].z : X[c].w);
+                    sv[k] = filter6(xi, F);
                 }
                 if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
                     uint64_t m[4];
