@@ -366,33 +366,64 @@ __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, 
     }
 }
 
-// surv = AND over the six chunks c of F[c][x[c]]: GPR index mode stays on
-// for the whole lookup and only its index changes per chunk, and each
-// indexed read feeds the AND directly.  The chunk sets sit in fixed
-// registers v32..v127 (chunk c at v[32 + 16c .. 47 + 16c]); the indices are
-// below 16, so every indexed read stays inside its chunk's sixteen.
-__device__ __forceinline__ uint32_t filter6(const uint32_t (&x)[kChunks], const v16u (&F)[kChunks])
+// Filter four lookups: sv[k] = AND over the six chunks c of F[c][x[c][k]].
+// GPR index mode stays on while only its index changes, and every indexed
+// read feeds its lookup's AND directly; the four lookups' ANDs alternate, so
+// consecutive vector instructions do not depend on each other.  The chunk
+// sets sit in fixed registers v32..v127 (chunk c at v[32 + 16c .. 47 + 16c]);
+// indices are below 16, so every indexed read stays inside its chunk's
+// sixteen registers.  Two blocks of three chunks keep the operand lists short.
+#define PC_IDX(a, b, c, d, base, op)                        \
+    "s_set_gpr_idx_idx %" #a "\n\t"                          \
+    "v_" op "_b32 %0, v" #base ", %0\n\t"                    \
+    "s_set_gpr_idx_idx %" #b "\n\t"                          \
+    "v_" op "_b32 %1, v" #base ", %1\n\t"                    \
+    "s_set_gpr_idx_idx %" #c "\n\t"                          \
+    "v_" op "_b32 %2, v" #base ", %2\n\t"                    \
+    "s_set_gpr_idx_idx %" #d "\n\t"                          \
+    "v_" op "_b32 %3, v" #base ", %3\n\t"
+__device__ __forceinline__ void filter_quad(const uint32_t (&x)[kChunks][4], const v16u (&F)[kChunks],
+                                            uint32_t (&sv)[4])
 {
-    uint32_t surv;
+    uint32_t a0, a1, a2, a3;
     asm volatile(
-        "s_set_gpr_idx_on %1, gpr_idx(SRC0)\n\t"
+        "s_set_gpr_idx_on %4, gpr_idx(SRC0)\n\t"
         "v_mov_b32 %0, v32\n\t"
-        "s_set_gpr_idx_idx %2\n\t"
-        "v_and_b32 %0, v48, %0\n\t"
-        "s_set_gpr_idx_idx %3\n\t"
-        "v_and_b32 %0, v64, %0\n\t"
-        "s_set_gpr_idx_idx %4\n\t"
+        "s_set_gpr_idx_idx %5\n\t"
+        "v_mov_b32 %1, v32\n\t"
+        "s_set_gpr_idx_idx %6\n\t"
+        "v_mov_b32 %2, v32\n\t"
+        "s_set_gpr_idx_idx %7\n\t"
+        "v_mov_b32 %3, v32\n\t"
+        PC_IDX(8, 9, 10, 11, 48, "and")
+        PC_IDX(12, 13, 14, 15, 64, "and")
+        "s_set_gpr_idx_off"
+        : "=&v"(a0), "=&v"(a1), "=&v"(a2), "=&v"(a3)
+        : "s"(x[0][0]), "s"(x[0][1]), "s"(x[0][2]), "s"(x[0][3]), "s"(x[1][0]), "s"(x[1][1]), "s"(x[1][2]),
+          "s"(x[1][3]), "s"(x[2][0]), "s"(x[2][1]), "s"(x[2][2]), "s"(x[2][3]), "{v[32:47]}"(F[0]),
+          "{v[48:63]}"(F[1]), "{v[64:79]}"(F[2]));
+    asm volatile(
+        "s_set_gpr_idx_on %4, gpr_idx(SRC0)\n\t"
         "v_and_b32 %0, v80, %0\n\t"
         "s_set_gpr_idx_idx %5\n\t"
-        "v_and_b32 %0, v96, %0\n\t"
+        "v_and_b32 %1, v80, %1\n\t"
         "s_set_gpr_idx_idx %6\n\t"
-        "v_and_b32 %0, v112, %0\n\t"
+        "v_and_b32 %2, v80, %2\n\t"
+        "s_set_gpr_idx_idx %7\n\t"
+        "v_and_b32 %3, v80, %3\n\t"
+        PC_IDX(8, 9, 10, 11, 96, "and")
+        PC_IDX(12, 13, 14, 15, 112, "and")
         "s_set_gpr_idx_off"
-        : "=&v"(surv)
-        : "s"(x[0]), "s"(x[1]), "s"(x[2]), "s"(x[3]), "s"(x[4]), "s"(x[5]), "{v[32:47]}"(F[0]), "{v[48:63]}"(F[1]),
-          "{v[64:79]}"(F[2]), "{v[80:95]}"(F[3]), "{v[96:111]}"(F[4]), "{v[112:127]}"(F[5]));
-    return surv;
+        : "+v"(a0), "+v"(a1), "+v"(a2), "+v"(a3)
+        : "s"(x[3][0]), "s"(x[3][1]), "s"(x[3][2]), "s"(x[3][3]), "s"(x[4][0]), "s"(x[4][1]), "s"(x[4][2]),
+          "s"(x[4][3]), "s"(x[5][0]), "s"(x[5][1]), "s"(x[5][2]), "s"(x[5][3]), "{v[80:95]}"(F[3]),
+          "{v[96:111]}"(F[4]), "{v[112:127]}"(F[5]));
+    sv[0] = a0;
+    sv[1] = a1;
+    sv[2] = a2;
+    sv[3] = a3;
 }
+#undef PC_IDX
 
 // One workgroup per work item = (switch, chunk of at most kChunk lookups of
 // its bucket).  Items are dealt to XCDs in contiguous ranges, so the chunks
@@ -475,14 +506,15 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
 #pragma unroll
                 for (int c = 0; c < kChunks; ++c) X[c] = reinterpret_cast<const uint4 *>(cidx[c])[j0 >> 2];
                 uint32_t sv[4];
+                uint32_t xi[kChunks][4];
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    uint32_t xi[kChunks];
-#pragma unroll
-                    for (int c = 0; c < kChunks; ++c)
-                        xi[c] = __builtin_amdgcn_readfirstlane(k == 0 ? X[c].x : k == 1 ? X[c].y : k == 2 ? X[c].z : X[c].w);
-                    sv[k] = filter6(xi, F);
+                for (int c = 0; c < kChunks; ++c) {
+                    xi[c][0] = __builtin_amdgcn_readfirstlane(X[c].x);
+                    xi[c][1] = __builtin_amdgcn_readfirstlane(X[c].y);
+                    xi[c][2] = __builtin_amdgcn_readfirstlane(X[c].z);
+                    xi[c][3] = __builtin_amdgcn_readfirstlane(X[c].w);
                 }
+                filter_quad(xi, F, sv);
                 if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
                     uint64_t m[4];
                     int32_t n = 0;
