@@ -51,6 +51,7 @@ def _load():
         I64 = ctypes.c_int64
         C = ctypes.c_int
         _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
+        _lib.orc_affinity.argtypes = [P, I64, I64, P, I64, P, I64, P, I64, P, I64, P, P, P, P, C]
         _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, C]
         _lib.orc_reach.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, P, C]
         _lib.orc_reach_via.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, I64, P, I64, P, P, C]
@@ -86,6 +87,31 @@ def selectors(labels, pred_off, preds, n_preds=None, rows=None, nthreads=0):
                       _p(np.ascontiguousarray(preds)), n_preds, I, _p(rows), rows.shape[0],
                       _p(feas), _p(pc), _p(err), nthreads)
     return feas, pc, int(err[0])
+
+
+def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None, rows=None, nthreads=0):
+    """Required node affinity: rows are ORs of terms, terms ANDs of
+    expressions (six operators).  Returns (feasible [nrows, W] u64,
+    popcnt u32, unknown u8 (bit 0 unknown value, bit 1 unknown label),
+    flags)."""
+    lib = _load()
+    labels = np.ascontiguousarray(labels, np.uint8)
+    N, L = labels.shape
+    I = row_off.shape[0] - 1
+    n_terms = term_off.shape[0] - 1 if n_terms is None else n_terms
+    n_preds = preds.shape[0] if n_preds is None else n_preds
+    if rows is None:
+        rows = np.arange(I, dtype=np.int32)
+    rows = np.ascontiguousarray(rows, np.int32)
+    W = (N + 63) // 64
+    feas = np.zeros((rows.shape[0], W), np.uint64)
+    pc = np.zeros(rows.shape[0], np.uint32)
+    unk = np.zeros(rows.shape[0], np.uint8)
+    err = np.zeros(1, np.uint32)
+    lib.orc_affinity(_p(labels), N, L, _p(np.ascontiguousarray(row_off, np.int32)), I,
+                     _p(np.ascontiguousarray(term_off, np.int32)), n_terms, _p(np.ascontiguousarray(preds)),
+                     n_preds, _p(rows), rows.shape[0], _p(feas), _p(pc), _p(unk), _p(err), nthreads)
+    return feas, pc, unk, int(err[0])
 
 
 def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=None,

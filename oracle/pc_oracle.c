@@ -156,6 +156,121 @@ void orc_selectors(const uint8_t *labels, int64_t N, int64_t L,
     }
 }
 
+/* ------------------------------------------------------------------ A1 (affinity)
+ * Required node affinity (paper: placement directives become Kubernetes
+ * node selection criteria and affinity rules, Sec. "Intent Translation",
+ * "Service Placement Module"; the validator cross-checks every referenced
+ * label against the live node-label inventory and fails a placement that
+ * names a label no node carries, Sec. "Failure modes", hallucinated
+ * identifiers).  Kubernetes semantics:
+ *   a row holds for node n iff at least one of its terms holds; a term
+ *   holds iff every one of its expressions holds.  A row with no terms
+ *   holds for every node (no required affinity); a term with no
+ *   expressions holds for no node.
+ *   Operators: In, NotIn, Exists as for selector rows, and
+ *     DoesNotExist : the node lacks the label
+ *     Gt t / Lt t  : the node has the label and its value, read as the
+ *                    integer it encodes (0..254), is > t / < t, where
+ *                    t = (int64) vals[0].
+ * Malformed: label >= L, op > 5, reserved field set, value 255 in an
+ * In/NotIn set, or vals[1..3] != 0 for Gt/Lt -> the expression holds for
+ * no node (F_PRED, raised for any such expression inside a well-formed
+ * term); a bad term offset pair -> the term holds for no node, a bad row
+ * offset pair -> the row holds for no node (F_OFFSETS, any pair).
+ * Inventory flags per row (unknown[r]): bit 0 when a well-formed In/NotIn
+ * expression of a well-formed term names a value no node carries for that
+ * label; bit 1 when a well-formed expression names a label that every
+ * node lacks.
+ */
+enum { O_DOESNOTEXIST = 3, O_GT = 4, O_LT = 5 };
+
+static int aff_valid(const o_pred *q, int64_t L)
+{
+    if (q->label >= L || q->op > 5 || q->rsv0 != 0 || q->rsv1 != 0) return 0;
+    if ((q->op == O_IN || q->op == O_NOTIN) && ((q->vals[3] >> 63) & 1)) return 0;
+    if ((q->op == O_GT || q->op == O_LT) && (q->vals[1] | q->vals[2] | q->vals[3])) return 0;
+    return 1;
+}
+
+static int aff_holds(const o_pred *q, unsigned x)
+{
+    const int present = x != 0xFF;
+    const int in_set = present && ((q->vals[x >> 6] >> (x & 63)) & 1);
+    const int64_t t = (int64_t)q->vals[0];
+    switch (q->op) {
+    case O_IN: return in_set;
+    case O_NOTIN: return !in_set;
+    case O_EXISTS: return present;
+    case O_DOESNOTEXIST: return !present;
+    case O_GT: return present && (int64_t)x > t;
+    default: return present && (int64_t)x < t;  /* O_LT */
+    }
+}
+
+void orc_affinity(const uint8_t *labels, int64_t N, int64_t L,
+                  const int32_t *row_off, int64_t I, const int32_t *term_off, int64_t n_terms,
+                  const o_pred *preds, int64_t n_preds, const int32_t *rows, int64_t nrows,
+                  uint64_t *feasible, uint32_t *popcnt, uint8_t *unknown, uint32_t *err, int nthreads)
+{
+    const int64_t W = (N + 63) / 64;
+    set_threads(nthreads);
+    for (int64_t t = 0; t < n_terms; ++t) {
+        if (!range_ok(term_off[t], term_off[t + 1], n_preds)) { *err |= F_OFFSETS; continue; }
+        for (int64_t p = term_off[t]; p < term_off[t + 1]; ++p)
+            if (!aff_valid(&preds[p], L)) *err |= F_PRED;
+    }
+    for (int64_t i = 0; i < I; ++i)
+        if (!range_ok(row_off[i], row_off[i + 1], n_terms)) *err |= F_OFFSETS;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows[r];
+        uint64_t *out = feasible + r * W;
+        for (int64_t w = 0; w < W; ++w) out[w] = 0;
+        popcnt[r] = 0;
+        unknown[r] = 0;
+        const int64_t tb = row_off[i], te = row_off[i + 1];
+        if (!range_ok(tb, te, n_terms)) continue;
+        /* inventory cross-check */
+        for (int64_t t = tb; t < te; ++t) {
+            if (!range_ok(term_off[t], term_off[t + 1], n_preds)) continue;
+            for (int64_t p = term_off[t]; p < term_off[t + 1]; ++p) {
+                const o_pred *q = &preds[p];
+                if (!aff_valid(q, L)) continue;
+                int key_seen = 0;
+                for (int64_t n = 0; n < N && !key_seen; ++n) key_seen = labels[n * L + q->label] != 0xFF;
+                if (!key_seen) unknown[r] |= 2;
+                if (q->op == O_IN || q->op == O_NOTIN) {
+                    for (unsigned v = 0; v < 255; ++v) {
+                        if (!((q->vals[v >> 6] >> (v & 63)) & 1)) continue;
+                        int seen = 0;
+                        for (int64_t n = 0; n < N && !seen; ++n) seen = labels[n * L + q->label] == v;
+                        if (!seen) unknown[r] |= 1;
+                    }
+                }
+            }
+        }
+        uint32_t count = 0;
+        for (int64_t n = 0; n < N; ++n) {
+            int ok = te == tb;  /* no terms: no required affinity */
+            for (int64_t t = tb; t < te && !ok; ++t) {
+                const int64_t b = term_off[t], e = term_off[t + 1];
+                if (!range_ok(b, e, n_preds) || b == e) continue;
+                int tok = 1;
+                for (int64_t p = b; p < e; ++p) {
+                    const o_pred *q = &preds[p];
+                    if (!aff_valid(q, L) || !aff_holds(q, labels[n * L + q->label])) tok = 0;
+                }
+                ok = tok;
+            }
+            if (ok) {
+                out[n >> 6] |= (uint64_t)1 << (n & 63);
+                ++count;
+            }
+        }
+        popcnt[r] = count;
+    }
+}
+
 /* ------------------------------------------------------------------ A3
  * Trace one header through the flow tables (paper: routing constraints
  * must hold "for the realized paths induced by" the installed rules; flow

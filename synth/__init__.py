@@ -43,6 +43,7 @@ assert PRED_DT.itemsize == 40 and RULE_DT.itemsize == 40
 assert INTENT_DT.itemsize == 32 and EXPECT_DT.itemsize == 12
 
 OP_IN, OP_NOTIN, OP_EXISTS = 0, 1, 2
+OP_DOESNOTEXIST, OP_GT, OP_LT = 3, 4, 5
 ABSENT = 0xFF
 DROP = 0xFFFF
 KIND_COMPUTE, KIND_NETWORK, KIND_HYBRID = 1, 2, 3
@@ -178,6 +179,58 @@ def gen_preds(rng, I, cards, kmin, kmax, mmax=4, op_p=None):
     bm[op == OP_EXISTS] = 0
     preds["vals"] = bm
     return off, preds
+
+
+def gen_affinity(rng, I, cards, tmin=1, tmax=3, kmin=1, kmax=4, mmax=4):
+    """I required-affinity rows: t ~ U{tmin..tmax} terms per row, each a
+    conjunction of k ~ U{kmin..kmax} expressions.  Label uniform, operator
+    uniform over the six (In, NotIn, Exists, DoesNotExist, Gt, Lt); In and
+    NotIn value sets as gen_preds; Gt and Lt thresholds uniform over
+    [-1, card] (so some admit every value and some none), stored as a
+    signed integer in vals[0].  Returns (row_off [I+1], term_off [T+1],
+    preds)."""
+    cards = np.asarray(cards, np.int64)
+    L = cards.shape[0]
+    t = rng.integers(tmin, tmax + 1, size=I)
+    row_off = np.zeros(I + 1, np.int32)
+    row_off[1:] = np.cumsum(t)
+    T = int(row_off[-1])
+    k = rng.integers(kmin, kmax + 1, size=T)
+    term_off = np.zeros(T + 1, np.int32)
+    term_off[1:] = np.cumsum(k)
+    P = int(term_off[-1])
+    lab = rng.integers(0, L, size=P)
+    op = rng.integers(0, 6, size=P)
+    card = cards[lab]
+    m = np.minimum(rng.integers(1, mmax + 1, size=P), card)
+    vals = distinct_values(rng, card, m, mmax)
+    thr = rng.integers(-1, card + 1)
+    preds = np.zeros(P, PRED_DT)
+    preds["label"] = lab
+    preds["op"] = op
+    bm = values_to_bitmap(vals)
+    setop = (op == OP_IN) | (op == OP_NOTIN)
+    bm[~setop] = 0
+    cmp = (op == OP_GT) | (op == OP_LT)
+    bm[cmp, 0] = thr[cmp].astype(np.int64).view(np.uint64)
+    preds["vals"] = bm
+    return row_off, term_off, preds
+
+
+def affinity_workload(seed, N, L, I, card_choices=(2, 4, 16, 64), absent_p=0.0, tmin=1, tmax=3, kmin=1, kmax=4,
+                      name="affinity"):
+    """N nodes x L uint8 labels (cardinality from card_choices, values
+    uniform, a fraction absent_p absent) and I required-affinity rows
+    (gen_affinity)."""
+    rng = np.random.default_rng([seed, 11])
+    cards = rng.choice(np.asarray(card_choices), size=L)
+    labels = gen_labels(rng, N, cards, absent_p)
+    row_off, term_off, preds = gen_affinity(rng, I, cards, tmin, tmax, kmin, kmax)
+    wl = Workload(name, seed)
+    wl.arrays.update(labels=labels, row_off=row_off, term_off=term_off, preds=preds)
+    wl.sizes.update(N=N, L=L, I=I, n_terms=int(term_off.shape[0] - 1), n_preds=int(preds.shape[0]))
+    wl.meta["cards"] = cards
+    return wl
 
 
 def gen_preds_holding(rng, labels, cards, a, b, kmin, kmax, mmax=4):
