@@ -54,12 +54,16 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 2
+#define PC_VERSION 3
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
 /* selector operators (Kubernetes node-affinity semantics) */
 enum { PC_OP_IN = 0, PC_OP_NOTIN = 1, PC_OP_EXISTS = 2 };
+/* further operators, accepted by pc_eval_affinity only */
+enum { PC_OP_DOESNOTEXIST = 3, PC_OP_GT = 4, PC_OP_LT = 5 };
+/* pc_eval_affinity inventory flags, one byte per row */
+enum { PC_UNKNOWN_VALUE = 1, PC_UNKNOWN_KEY = 2 };
 #define PC_LABEL_ABSENT 0xFFu   /* label value meaning "node does not carry this label" */
 #define PC_ACTION_DROP 0xFFFFu  /* rule action: drop the packet */
 #define PC_NO_PORT 0xFFFFu      /* pc_trace_out.last_port when not EGRESS */
@@ -218,6 +222,41 @@ int pc_profile_read(pc_ctx *ctx, int idx, const char **name, int64_t *launches, 
 int pc_eval_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L,
                       const int32_t *pred_off, const pc_pred *preds, int64_t n_preds, int32_t I,
                       uint64_t *feasible, uint32_t *popcnt, void *stream);
+
+/*
+ * A1, full node affinity -- placement directives compiled into Kubernetes
+ * node selection criteria and affinity rules (paper: Intent Translation,
+ * Service Placement Module), with the validator's cross-check of every
+ * referenced label against the node-label inventory (Failure modes,
+ * hallucinated identifiers).  Row i holds for node n iff at least one of
+ * its terms holds; a term holds iff every one of its expressions holds.  A
+ * row with no terms holds for every node; a term with no expressions holds
+ * for none.  Operators: In, NotIn, Exists as in pc_eval_selectors, and
+ *   DoesNotExist : label absent
+ *   Gt / Lt      : label present and its value (0..254, the integer it
+ *                  encodes) > / < t, t = (int64_t) vals[0]; vals[1..3] = 0.
+ * labels   : uint8 [N][L], node-major; PC_LABEL_ABSENT = absent.
+ * row_off  : int32 [I+1]; row i owns terms row_off[i] .. row_off[i+1].
+ * term_off : int32 [n_terms+1]; term t owns preds[term_off[t] .. term_off[t+1]).
+ * preds    : pc_pred [n_preds].
+ * feasible : uint64 [I][W], W = ceil(N/64), as pc_eval_selectors.
+ * popcnt   : uint32 [I].
+ * unknown  : uint8 [I]; PC_UNKNOWN_VALUE when a well-formed In/NotIn
+ *            expression of the row names a value no node carries for its
+ *            label, PC_UNKNOWN_KEY when a well-formed expression names a
+ *            label every node lacks (whether or not the expression holds).
+ * All arrays are device memory owned by the caller.  Limits: 0 <= N,
+ * 1 <= L <= 65535 (L = 0 allowed when no predicate exists), 0 <= I,
+ * 0 <= n_terms, 0 <= n_preds.  Malformed data: an expression with label
+ * >= L, op > 5, a reserved field set, value 255 in an In/NotIn set or
+ * vals[1..3] != 0 for Gt/Lt holds for no node (PC_DERR_PRED, raised for
+ * any such expression inside a term with a valid offset pair); a bad term
+ * offset pair empties that term, a bad row offset pair the row
+ * (PC_DERR_OFFSETS).
+ */
+int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off,
+                     int32_t I, const int32_t *term_off, int32_t n_terms, const pc_pred *preds, int64_t n_preds,
+                     uint64_t *feasible, uint32_t *popcnt, uint8_t *unknown, void *stream);
 
 /*
  * A2+A3+A4 -- routing constraints on realised paths.  Each trace t starts at

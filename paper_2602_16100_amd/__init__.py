@@ -2,7 +2,8 @@
 
 The library (include/pc.h) runs the validator checks of LLM-driven,
 intent-based privacy orchestration (arXiv 2602.16100) as HIP kernels on one
-GPU: node-selector evaluation (pc_eval_selectors), flow-table tracing
+GPU: node-selector evaluation (pc_eval_selectors; full node affinity with
+OR-ed terms, six operators and label-inventory flags: pc_eval_affinity), flow-table tracing
 (pc_trace_flows), masked reachability (pc_masked_reach) and the per-intent
 verdict (pc_report), with waypoint and forbidden-switch constraints
 (pc_trace_flows_watch, pc_masked_reach_via, pc_report_paths).
@@ -75,6 +76,7 @@ def lib():
     L.pc_version.restype = C
     L.pc_data_errors.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32), C]
     L.pc_eval_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
+    L.pc_eval_affinity.argtypes = [P, P, I32, I32, P, I32, P, I32, P, I64, P, P, P, P]
     L.pc_trace_flows.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, P]
     L.pc_masked_reach.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, P]
     L.pc_report.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P]
@@ -89,8 +91,8 @@ def lib():
 
 
 EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_errors", "pc_profile",
-            "pc_profile_read", "pc_eval_selectors", "pc_trace_flows", "pc_masked_reach", "pc_report",
-            "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths")
+            "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
+            "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths")
 
 
 class Context:
@@ -208,6 +210,33 @@ def pc_eval_selectors(labels, pred_off, preds, n_preds=None, feasible=None, popc
                                       _ptr(preds) if preds.numel() else None, n_preds, I,
                                       _ptr(feasible) if feasible.numel() else None, _ptr(popcnt), _stream(stream)))
     return feasible, popcnt
+
+
+def pc_eval_affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None, feasible=None, popcnt=None,
+                     unknown=None, ctx=None, stream=None):
+    """A1 with full node affinity: rows are ORs of terms (row_off), terms
+    ANDs of expressions (term_off, preds; six operators).  Returns the
+    feasible-node bitset [I, ceil(N/64)], popcount [I] and the inventory
+    flags [I] (uint8: 1 unknown value, 2 unknown label)."""
+    ctx = ctx or context()
+    N, L = (int(labels.shape[0]), int(labels.shape[1])) if labels.dim() == 2 else (0, 0)
+    I = int(row_off.shape[0]) - 1
+    n_terms = int(term_off.shape[0]) - 1 if n_terms is None else int(n_terms)
+    n_preds = int(preds.shape[0]) if n_preds is None else int(n_preds)
+    W = (N + 63) // 64
+    dev = row_off.device
+    if feasible is None:
+        feasible = torch.empty((I, W), dtype=torch.int64, device=dev)
+    if popcnt is None:
+        popcnt = torch.empty(I, dtype=torch.int32, device=dev)
+    if unknown is None:
+        unknown = torch.empty(I, dtype=torch.uint8, device=dev)
+    ctx.check(lib().pc_eval_affinity(ctx.handle, _ptr(labels) if labels.numel() else None, N, L,
+                                     _ptr(row_off), I, _ptr(term_off), n_terms,
+                                     _ptr(preds) if preds.numel() else None, n_preds,
+                                     _ptr(feasible) if feasible.numel() else None,
+                                     _ptr(popcnt) if I else None, _ptr(unknown) if I else None, _stream(stream)))
+    return feasible, popcnt, unknown
 
 
 def pc_trace_flows(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, n_ports=None, n_rules=None,

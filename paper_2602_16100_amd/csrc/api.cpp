@@ -217,6 +217,27 @@ int pc_eval_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, 
                          static_cast<hipStream_t>(stream));
 }
 
+int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off,
+                     int32_t I, const int32_t *term_off, int32_t n_terms, const pc_pred *preds, int64_t n_preds,
+                     uint64_t *feasible, uint32_t *popcnt, uint8_t *unknown, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(N >= 0 && I >= 0 && n_terms >= 0 && n_preds >= 0,
+               "pc_eval_affinity: negative size (N=%d I=%d n_terms=%d n_preds=%lld)", N, I, n_terms,
+               (long long)n_preds);
+    PC_REQUIRE(L >= 0 && L <= 65535, "pc_eval_affinity: L=%d out of [0, 65535]", L);
+    PC_REQUIRE(L > 0 || n_preds == 0, "pc_eval_affinity: L=0 with predicates");
+    PC_REQUIRE(I == 0 || (row_off && popcnt && unknown), "pc_eval_affinity: null row_off/popcnt/unknown");
+    PC_REQUIRE(term_off, "pc_eval_affinity: null term_off");
+    PC_REQUIRE(n_preds == 0 || preds, "pc_eval_affinity: null preds");
+    PC_REQUIRE(N == 0 || L == 0 || labels, "pc_eval_affinity: null labels");
+    PC_REQUIRE(I == 0 || N == 0 || feasible, "pc_eval_affinity: null feasible");
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_affinity(ctx, labels, N, L, row_off, I, term_off, n_terms, preds, n_preds, feasible, popcnt,
+                        unknown, static_cast<hipStream_t>(stream));
+}
+
 int pc_trace_flows(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                    const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
                    const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, pc_trace_out *out,

@@ -158,10 +158,12 @@ __device__ __forceinline__ bool pred_valid(uint32_t label, uint32_t op, uint32_t
            (op == PC_OP_EXISTS || (v3 >> 63) == 0);
 }
 
-// Program entries: plane id, plus flags on the last entry of a clause.
+// Program entries: plane id, plus flags on the last entry of a clause
+// (kLast, kNeg) and, in affinity programs, on the last entry of a term.
+constexpr uint32_t kTermEnd = 1u << 29;
 constexpr uint32_t kLast = 1u << 30;
 constexpr uint32_t kNeg = 1u << 31;
-constexpr uint32_t kPidMask = kLast - 1;
+constexpr uint32_t kPidMask = kTermEnd - 1;
 // Row record header (word 0); words 1..15 hold an inline program.
 constexpr int32_t kRowFalse = -1;     // some clause admits no node (or a malformed predicate)
 constexpr int32_t kRowIndirect = -2;  // program of more than 15 entries at prog[4 * word1], word2 entries
@@ -173,31 +175,77 @@ __device__ __forceinline__ uint32_t plane_id(const uint64_t *pres, const uint32_
     return wb[k] + __popcll(pres[k] & ((1ull << (v & 63)) - 1));
 }
 
-// The value set a predicate ORs over, and whether the OR is negated.  Each
-// label value of a node lies in exactly one present plane, so In S = OR(S)
-// = NOT OR(present \ S) and NotIn S = NOT OR(S) = OR(present \ S): the
-// shorter form is taken.  Exists = NOT OR(plane of the absent value), an
-// empty OR when every node carries the label.
-__device__ __forceinline__ uint32_t pred_clause(const pc_pred &q, const uint64_t *pres, uint64_t sel[4], bool &neg)
+// Values lo..hi (clipped to 0..254) as a 256-bit set.
+__device__ __forceinline__ void value_range(int64_t lo, int64_t hi, uint64_t s[4])
 {
-    if (q.op == PC_OP_EXISTS) {
+    lo = lo < 0 ? 0 : lo;
+    hi = hi > 254 ? 254 : hi;
+    for (int k = 0; k < 4; ++k) {
+        const int64_t a = lo > 64 * k ? lo : 64 * k;
+        const int64_t b = hi < 64 * k + 63 ? hi : 64 * k + 63;
+        if (a > b) {
+            s[k] = 0;
+        } else {
+            const int n = static_cast<int>(b - a + 1);
+            s[k] = (n == 64 ? ~0ull : ((1ull << n) - 1)) << (a - 64 * k);
+        }
+    }
+}
+
+// The value set a clause ORs over, and whether the OR is negated, for an
+// expression with operator op.  Each label value of a node lies in exactly
+// one present plane (the absent value 255 included), so In S = OR(S) =
+// NOT OR(present \ S) and NotIn S = NOT OR(S) = OR(present \ S): the
+// shorter form is taken.  Exists = NOT OR(plane of the absent value), an
+// empty OR when every node carries the label; DoesNotExist = that OR.
+// Gt t / Lt t are In of the values above / below t.
+__device__ __forceinline__ uint32_t expr_clause(uint32_t op, const uint64_t vals[4], const uint64_t *pres,
+                                                uint64_t sel[4], bool &neg)
+{
+    if (op == PC_OP_EXISTS || op == PC_OP_DOESNOTEXIST) {
         sel[0] = sel[1] = sel[2] = 0;
         sel[3] = pres[3] & (1ull << 63);
-        neg = true;
+        neg = op == PC_OP_EXISTS;
         return static_cast<uint32_t>(sel[3] >> 63);
+    }
+    uint64_t set[4];
+    bool is_in = op != PC_OP_NOTIN;
+    if (op == PC_OP_GT || op == PC_OP_LT) {
+        const int64_t t = static_cast<int64_t>(vals[0]);
+        if (op == PC_OP_GT)
+            value_range(t >= 254 ? 255 : t + 1, 254, set);
+        else
+            value_range(0, t <= 0 ? -1 : t - 1, set);
+    } else {
+        for (int k = 0; k < 4; ++k) set[k] = vals[k];
     }
     uint64_t in[4], out[4];
     uint32_t ms = 0, mc = 0;
     for (int k = 0; k < 4; ++k) {
-        in[k] = q.vals[k] & pres[k];
-        out[k] = pres[k] & ~q.vals[k];
+        in[k] = set[k] & pres[k];
+        out[k] = pres[k] & ~set[k];
         ms += __popcll(in[k]);
         mc += __popcll(out[k]);
     }
     const bool use_in = ms <= mc;
     for (int k = 0; k < 4; ++k) sel[k] = use_in ? in[k] : out[k];
-    neg = (q.op == PC_OP_IN) ? !use_in : use_in;
+    neg = is_in ? !use_in : use_in;
     return use_in ? ms : mc;
+}
+
+__device__ __forceinline__ uint32_t pred_clause(const pc_pred &q, const uint64_t *pres, uint64_t sel[4], bool &neg)
+{
+    return expr_clause(q.op, q.vals, pres, sel, neg);
+}
+
+// Well-formed affinity expression: label < L, op <= 5, reserved fields 0,
+// no value 255 in an In / NotIn set, vals[1..3] = 0 for Gt / Lt.
+__device__ __forceinline__ bool aff_valid(const pc_pred &q, int32_t L)
+{
+    if (static_cast<int32_t>(q.label) >= L || q.op > PC_OP_LT || q.rsv0 != 0 || q.rsv1 != 0) return false;
+    if (q.op <= PC_OP_NOTIN && (q.vals[3] >> 63)) return false;
+    if ((q.op == PC_OP_GT || q.op == PC_OP_LT) && (q.vals[1] | q.vals[2] | q.vals[3])) return false;
+    return true;
 }
 
 // One thread per row, two passes over its predicates: validate and size
@@ -280,6 +328,166 @@ __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__
     if (errs) atomicOr(d_err, errs);
 }
 
+// Affinity input sweep: the data-error flags are properties of the whole
+// input.  OFFSETS for any bad term or row offset pair, PRED for any
+// malformed expression inside a term with a valid offset pair.
+__global__ __launch_bounds__(256) void k_aff_validate(const int32_t *__restrict__ row_off, int32_t I,
+                                                      const int32_t *__restrict__ term_off, int32_t n_terms,
+                                                      const pc_pred *__restrict__ preds, int64_t n_preds, int32_t L,
+                                                      uint32_t *__restrict__ d_err)
+{
+    uint32_t errs = 0;
+    const int64_t tot = I > n_terms ? I : n_terms;
+    for (int64_t x = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; x < tot;
+         x += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        if (x < n_terms) {
+            const int64_t b = term_off[x], e = term_off[x + 1];
+            if (!pc_range_ok(b, e, n_preds)) {
+                errs |= PC_DERR_OFFSETS;
+            } else {
+                for (int64_t p = b; p < e; ++p)
+                    if (!aff_valid(preds[p], L)) {
+                        errs |= PC_DERR_PRED;
+                        break;
+                    }
+            }
+        }
+        if (x < I && !pc_range_ok(row_off[x], row_off[x + 1], n_terms)) errs |= PC_DERR_OFFSETS;
+    }
+    if (errs) atomicOr(d_err, errs);
+}
+
+// Inventory flags of one well-formed expression: its label carries no
+// value on any node, or an In / NotIn value no node carries.
+__device__ __forceinline__ uint32_t aff_unknown(const pc_pred &q, const uint64_t *pres)
+{
+    uint32_t u = 0;
+    if ((pres[0] | pres[1] | pres[2] | (pres[3] & ~(1ull << 63))) == 0) u |= PC_UNKNOWN_KEY;
+    if (q.op <= PC_OP_NOTIN &&
+        ((q.vals[0] & ~pres[0]) | (q.vals[1] & ~pres[1]) | (q.vals[2] & ~pres[2]) | (q.vals[3] & ~pres[3])))
+        u |= PC_UNKNOWN_VALUE;
+    return u;
+}
+
+// Whether term [b, e) can hold for some node at all (valid offsets, at
+// least one expression, every expression well-formed, no clause that is an
+// empty OR), and its program length.
+__device__ __forceinline__ bool aff_term(const pc_pred *__restrict__ preds, int64_t b, int64_t e, int64_t n_preds,
+                                         int32_t L, const uint64_t *__restrict__ present, int64_t &len)
+{
+    len = 0;
+    if (!pc_range_ok(b, e, n_preds) || b == e) return false;
+    bool ok = true;
+    for (int64_t p = b; p < e; ++p) {
+        const pc_pred q = preds[p];
+        if (!aff_valid(q, L)) return false;
+        uint64_t sel[4];
+        bool neg;
+        const uint32_t cnt = expr_clause(q.op, q.vals, present + static_cast<int64_t>(q.label) * 4, sel, neg);
+        if (cnt == 0 && !neg) ok = false;
+        len += cnt;
+    }
+    return ok;
+}
+
+// One thread per affinity row: inventory flags, then the program.  Terms
+// that hold nowhere are dropped; a term with an empty program holds
+// everywhere, and so does a row without terms (header 0); a row with no
+// term left admits no node.  The last entry of each term carries
+// kTermEnd.  Programs of at most 15 entries sit inline in the row record;
+// longer ones take a slice of prog through a bump counter and, when it is
+// exhausted, are decoded at evaluation time (kRowLong).
+__global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__ row_off, int32_t I,
+                                                     const int32_t *__restrict__ term_off, int32_t n_terms,
+                                                     const pc_pred *__restrict__ preds, int64_t n_preds, int32_t L,
+                                                     const uint64_t *__restrict__ present,
+                                                     const uint32_t *__restrict__ wbase, uint32_t zero_pid,
+                                                     uint32_t *__restrict__ prog, int64_t prog_cap,
+                                                     unsigned long long *__restrict__ prog_used,
+                                                     uint32_t *__restrict__ rec, uint8_t *__restrict__ unknown)
+{
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
+        uint32_t *rr = rec + static_cast<int64_t>(i) * kRecWords;
+        const int64_t tb = row_off[i], te = row_off[i + 1];
+        if (!pc_range_ok(tb, te, n_terms)) {
+            rr[0] = static_cast<uint32_t>(kRowFalse);
+            unknown[i] = 0;
+            continue;
+        }
+        uint32_t unk = 0;
+        for (int64_t t = tb; t < te; ++t) {
+            const int64_t b = term_off[t], e = term_off[t + 1];
+            if (!pc_range_ok(b, e, n_preds)) continue;
+            for (int64_t p = b; p < e; ++p) {
+                const pc_pred q = preds[p];
+                if (aff_valid(q, L)) unk |= aff_unknown(q, present + static_cast<int64_t>(q.label) * 4);
+            }
+        }
+        unknown[i] = static_cast<uint8_t>(unk);
+        bool all = tb == te;
+        int64_t n = 0, live = 0;
+        for (int64_t t = tb; t < te && !all; ++t) {
+            int64_t len;
+            if (!aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len)) continue;
+            if (len == 0) all = true;
+            n += len;
+            ++live;
+        }
+        if (all) {
+            rr[0] = 0;
+            continue;
+        }
+        if (live == 0) {
+            rr[0] = static_cast<uint32_t>(kRowFalse);
+            continue;
+        }
+        const bool inl = n <= kInline;
+        uint32_t *out = rr + 1;
+        if (!inl) {
+            // slices are whole multiples of 4 entries: the record stores off / 4
+            const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>((n + 3) & ~int64_t(3)));
+            if (static_cast<int64_t>(off) + n > prog_cap) {
+                rr[0] = static_cast<uint32_t>(kRowLong);
+                continue;
+            }
+            out = prog + off;
+            rr[0] = static_cast<uint32_t>(kRowIndirect);
+            rr[1] = static_cast<uint32_t>(off / 4);
+            rr[2] = static_cast<uint32_t>(n);
+        }
+        int64_t k_out = 0;
+        for (int64_t t = tb; t < te; ++t) {
+            const int64_t b = term_off[t], e = term_off[t + 1];
+            int64_t len;
+            if (!aff_term(preds, b, e, n_preds, L, present, len)) continue;
+            for (int64_t p = b; p < e; ++p) {
+                const pc_pred q = preds[p];
+                const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+                const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+                uint64_t sel[4];
+                bool neg;
+                uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
+                for (int k = 0; k < 4; ++k) {
+                    uint64_t m = sel[k];
+                    while (m) {
+                        const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                        m &= m - 1;
+                        uint32_t ent = plane_id(pres, wb, v);
+                        if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
+                        out[k_out++] = ent;
+                    }
+                }
+            }
+            out[k_out - 1] |= kTermEnd;
+        }
+        if (inl) {
+            const int64_t padded = n <= kGroup ? kGroup : kInline;
+            for (int64_t k = n; k < padded; ++k) rr[1 + k] = zero_pid;
+            rr[0] = static_cast<uint32_t>(n);
+        }
+    }
+}
+
 struct Words {
     uint64_t a, b;
 };
@@ -294,7 +502,10 @@ __device__ __forceinline__ Words load_words(const uint64_t *p)
 
 // Fold one program entry's plane words into the running clause (c) and,
 // at the end of a clause, into the row's conjunction (a).
-__device__ __forceinline__ void fold(uint32_t ent, const Words &v, Words &c, Words &a)
+// In affinity programs (kTerms) the end of a term ORs the term's
+// conjunction into the row (r) and starts the next term.
+template <bool kTerms>
+__device__ __forceinline__ void fold(uint32_t ent, const Words &v, Words &c, Words &a, Words &r)
 {
     c.a |= v.a;
     c.b |= v.b;
@@ -307,6 +518,13 @@ __device__ __forceinline__ void fold(uint32_t ent, const Words &v, Words &c, Wor
             a.b &= c.b;
         }
         c.a = c.b = 0;
+    }
+    if constexpr (kTerms) {
+        if (ent & kTermEnd) {
+            r.a |= a.a;
+            r.b |= a.b;
+            a.a = a.b = ~0ull;
+        }
     }
 }
 
@@ -377,6 +595,47 @@ __device__ Words eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, 
     return a;
 }
 
+// Affinity rows whose program found no slice: the terms decoded on the
+// scalar unit (the same term rules as k_aff_compile).
+template <bool kBuf>
+__device__ Words eval_row_decoded_aff(const pc_pred *__restrict__ preds, int64_t n_preds,
+                                      const int32_t *__restrict__ term_off, int64_t tb, int64_t te, int32_t L,
+                                      const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
+                                      const Planes<kBuf> &pl)
+{
+    Words r{0, 0};
+    for (int64_t t = tb; t < te; ++t) {
+        int64_t len;
+        const int64_t b = term_off[t], e = term_off[t + 1];
+        if (!aff_term(preds, b, e, n_preds, L, present, len)) continue;
+        Words a{~0ull, ~0ull};
+        for (int64_t p = b; p < e; ++p) {
+            const pc_pred q = preds[p];
+            const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+            const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+            uint64_t sel[4];
+            bool neg;
+            expr_clause(q.op, q.vals, pres, sel, neg);
+            Words c{0, 0};
+            for (int k = 0; k < 4; ++k) {
+                uint64_t m = sel[k];
+                while (m) {
+                    const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                    m &= m - 1;
+                    const Words x = pl(plane_id(pres, wb, v));
+                    c.a |= x.a;
+                    c.b |= x.b;
+                }
+            }
+            a.a &= neg ? ~c.a : c.a;
+            a.b &= neg ? ~c.b : c.b;
+        }
+        r.a |= a.a;
+        r.b |= a.b;
+    }
+    return r;
+}
+
 // Work item (tile, chunk): the wavefronts of a workgroup take turns on
 // batches of 64 consecutive rows of the chunk; lane l covers words
 // tile * 128 + 2l and + 1.  A row's record is read with scalar loads (the
@@ -386,12 +645,15 @@ __device__ Words eval_row_decoded(const pc_pred *__restrict__ preds, int64_t b, 
 // batch lane i sums row i's 64 bytes with dot4 and stores
 // part[tile * I + r].  Lanes past the last word load in-bounds words and
 // mask them.
-template <bool kBuf>
+// kTerms: affinity rows (pred_off holds the row -> term offsets, term_off
+// the term -> expression offsets) whose programs OR their terms.
+template <bool kBuf, bool kTerms>
 __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     const uint32_t *__restrict__ rec, const uint32_t *__restrict__ prog, const int32_t *__restrict__ pred_off,
     const pc_pred *__restrict__ preds, const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
     const uint64_t *__restrict__ planes, int64_t plane_bytes, int64_t Wp, int32_t I, int32_t W, int32_t N,
-    uint64_t *__restrict__ feasible, uint32_t *__restrict__ part, int32_t ntiles, int32_t nchunks, int32_t rpc)
+    uint64_t *__restrict__ feasible, uint32_t *__restrict__ part, int32_t ntiles, int32_t nchunks, int32_t rpc,
+    const int32_t *__restrict__ term_off, int64_t n_preds, int32_t L)
 {
     constexpr int kCntStride = 68;  // bytes per row of the count table (17 dwords: conflict-free column reads)
     __shared__ uint32_t cnt_lds[kEvalThreads / 64][64 * kCntStride / 4];
@@ -425,6 +687,7 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     auto row = [&](int32_t r, int32_t i, const uint32_t (&R)[kRecWords]) {
         const int32_t hdr = static_cast<int32_t>(R[0]);
         Words a{~0ull, ~0ull};
+        Words rt{0, 0};  // affinity: OR of the finished terms
         if (hdr == kRowFalse) {
             a = Words{0, 0};
         } else if (hdr > 0) {
@@ -435,14 +698,14 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
 #pragma unroll
                 for (int k = 0; k < kGroup; ++k) V[k] = pl(R[1 + k] & kPidMask);
 #pragma unroll
-                for (int k = 0; k < kGroup; ++k) fold(R[1 + k], V[k], c, a);
+                for (int k = 0; k < kGroup; ++k) fold<kTerms>(R[1 + k], V[k], c, a, rt);
             }
             if (hdr > kGroup) {
                 Words V[kInline - kGroup];
 #pragma unroll
                 for (int k = 0; k < kInline - kGroup; ++k) V[k] = pl(R[1 + kGroup + k] & kPidMask);
 #pragma unroll
-                for (int k = 0; k < kInline - kGroup; ++k) fold(R[1 + kGroup + k], V[k], c, a);
+                for (int k = 0; k < kInline - kGroup; ++k) fold<kTerms>(R[1 + kGroup + k], V[k], c, a, rt);
             }
         } else if (hdr == kRowIndirect) {
             const uint32_t *pr = prog + 4 * static_cast<int64_t>(R[1]);
@@ -458,10 +721,17 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
                     if (e0 + k < len) V[k] = pl(E[k] & kPidMask);
 #pragma unroll
                 for (int k = 0; k < kGroup; ++k)
-                    if (e0 + k < len) fold(E[k], V[k], c, a);
+                    if (e0 + k < len) fold<kTerms>(E[k], V[k], c, a, rt);
             }
         } else if (hdr == kRowLong) {
-            a = eval_row_decoded<kBuf>(preds, pred_off[r], pred_off[r + 1], present, wbase, pl);
+            if constexpr (kTerms)
+                rt = eval_row_decoded_aff<kBuf>(preds, n_preds, term_off, pred_off[r], pred_off[r + 1], L, present,
+                                                wbase, pl);
+            else
+                a = eval_row_decoded<kBuf>(preds, pred_off[r], pred_off[r + 1], present, wbase, pl);
+        }
+        if constexpr (kTerms) {
+            if (hdr > 0 || hdr == kRowIndirect || hdr == kRowLong) a = rt;
         }
         a.a &= m0;
         a.b &= m1;
@@ -523,6 +793,81 @@ __global__ __launch_bounds__(256) void k_sel_popsum(const uint32_t *__restrict__
 
 }  // namespace
 
+namespace {
+
+// Value planes of the node labels: presence, plane numbering (d_P = P),
+// the planes themselves, and the all-zero plane pmax.
+int build_planes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, int64_t W, int64_t Wp, int64_t pmax,
+                 uint64_t *present, uint32_t *wbase, uint64_t *planes, int32_t *d_P, hipStream_t stream)
+{
+    launch_fill_u64(present, static_cast<size_t>(L) * 4, 0, stream);
+    if (Wp > 0) launch_fill_u64(planes + static_cast<size_t>(pmax) * Wp, static_cast<size_t>(Wp), 0, stream);
+    if (L == 0) launch_fill_u32(reinterpret_cast<uint32_t *>(d_P), 1, 0, stream);
+    PC_LAUNCH_CHECK(ctx);
+    if (N > 0 && L > 0) {
+        // about 2048 workgroups: a few hundred nodes each
+        const int64_t ltiles = (L + 63) / 64;
+        int64_t chunk = (static_cast<int64_t>(N) * ltiles + 2047) / 2048;
+        chunk = chunk < 64 ? 64 : (chunk + 3) / 4 * 4;
+        while ((N + chunk - 1) / chunk > 65535) chunk *= 2;
+        dim3 gp((L + 63) / 64, static_cast<unsigned>((N + chunk - 1) / chunk));
+        PC_TIMED(ctx, "k_sel_presence", stream,
+                 hipLaunchKernelGGL(k_sel_presence, gp, dim3(256), 0, stream, labels, N, L, chunk,
+                                    reinterpret_cast<uint32_t *>(present)));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    if (L > 0) {
+        PC_TIMED(ctx, "k_sel_label_scan", stream,
+                 hipLaunchKernelGGL(k_sel_label_scan, dim3(1), dim3(1024), 0, stream, present, L, wbase, d_P));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    if (N > 0 && L > 0) {
+        dim3 gb(static_cast<unsigned>(W), static_cast<unsigned>((L + 3) / 4));
+        PC_TIMED(ctx, "k_sel_planes", stream,
+                 hipLaunchKernelGGL(k_sel_planes, gb, dim3(256), 0, stream, labels, N, L, present, wbase, planes, Wp));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    return PC_OK;
+}
+
+// The evaluator over every row, then the popcount partials' sum.
+template <bool kTerms>
+int launch_eval(pc_ctx *ctx, const uint32_t *rec, const uint32_t *prog, const int32_t *off,
+                const pc_pred *preds, const uint64_t *present, const uint32_t *wbase, const uint64_t *planes,
+                int64_t pmax, int64_t Wp, int32_t I, int64_t W, int32_t N, uint64_t *feasible, uint32_t *popcnt,
+                uint32_t *part, int64_t ntiles, const int32_t *term_off, int64_t n_preds, int32_t L,
+                hipStream_t stream)
+{
+    // about 4096 workgroups; a chunk is a whole number of 256-row passes
+    int64_t nchunks = std::max<int64_t>((4096 + ntiles - 1) / ntiles, 1);
+    int64_t rpc = (I + nchunks - 1) / nchunks;
+    rpc = (rpc + kEvalThreads - 1) / kEvalThreads * kEvalThreads;
+    nchunks = (I + rpc - 1) / rpc;
+    const int64_t total = ntiles * nchunks;
+    const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
+    uint32_t *cnt_out = ntiles > 1 ? part : popcnt;
+    const int64_t pbytes = static_cast<int64_t>(pmax + 1) * Wp * 8;
+    auto eval = [&](auto kern) {
+        PC_TIMED(ctx, kTerms ? "k_aff_eval" : "k_sel_eval", stream,
+                 hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, off, preds,
+                                    present, wbase, planes, pbytes, Wp, I, static_cast<int32_t>(W), N, feasible,
+                                    cnt_out, static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
+                                    static_cast<int32_t>(rpc), term_off, n_preds, L));
+    };
+    if (pbytes < (int64_t(1) << 31)) eval(k_sel_eval<true, kTerms>);  // buffer offsets are 32-bit
+    else eval(k_sel_eval<false, kTerms>);
+    PC_LAUNCH_CHECK(ctx);
+    if (ntiles > 1) {
+        PC_TIMED(ctx, kTerms ? "k_aff_popsum" : "k_sel_popsum", stream,
+                 hipLaunchKernelGGL(k_sel_popsum, dim3(static_cast<unsigned>((I + 255) / 256)), dim3(256), 0, stream,
+                                    part, I, static_cast<int32_t>(ntiles), popcnt));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    return PC_OK;
+}
+
+}  // namespace
+
 int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                   const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
                   hipStream_t stream)
@@ -554,64 +899,75 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     Carver real{ctx->arena, 0};
     carve(real);
 
-    launch_fill_u64(present, static_cast<size_t>(L) * 4, 0, stream);
-    if (Wp > 0) launch_fill_u64(planes + static_cast<size_t>(pmax) * Wp, static_cast<size_t>(Wp), 0, stream);
     if (W == 0) launch_fill_u32(popcnt, static_cast<size_t>(I), 0, stream);
-    PC_LAUNCH_CHECK(ctx);
-    if (N > 0 && L > 0) {
-        // about 2048 workgroups: a few hundred nodes each
-        const int64_t ltiles = (L + 63) / 64;
-        int64_t chunk = (static_cast<int64_t>(N) * ltiles + 2047) / 2048;
-        chunk = chunk < 64 ? 64 : (chunk + 3) / 4 * 4;
-        while ((N + chunk - 1) / chunk > 65535) chunk *= 2;
-        dim3 gp((L + 63) / 64, static_cast<unsigned>((N + chunk - 1) / chunk));
-        PC_TIMED(ctx, "k_sel_presence", stream,
-                 hipLaunchKernelGGL(k_sel_presence, gp, dim3(256), 0, stream, labels, N, L, chunk,
-                                    reinterpret_cast<uint32_t *>(present)));
-        PC_LAUNCH_CHECK(ctx);
-    }
-    if (L > 0) {
-        PC_TIMED(ctx, "k_sel_label_scan", stream,
-                 hipLaunchKernelGGL(k_sel_label_scan, dim3(1), dim3(1024), 0, stream, present, L, wbase, d_P));
-        PC_LAUNCH_CHECK(ctx);
-    }
-    if (N > 0 && L > 0) {
-        dim3 gb(static_cast<unsigned>(W), static_cast<unsigned>((L + 3) / 4));
-        PC_TIMED(ctx, "k_sel_planes", stream,
-                 hipLaunchKernelGGL(k_sel_planes, gb, dim3(256), 0, stream, labels, N, L, present, wbase, planes, Wp));
-        PC_LAUNCH_CHECK(ctx);
-    }
+    rc = build_planes(ctx, labels, N, L, W, Wp, pmax, present, wbase, planes, d_P, stream);
+    if (rc) return rc;
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
     PC_TIMED(ctx, "k_sel_compile", stream,
              hipLaunchKernelGGL(k_sel_compile, dim3(rgrid), dim3(256), 0, stream, pred_off, preds, n_preds, I, L,
                                 present, wbase, static_cast<uint32_t>(pmax), prog, rec, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     if (W == 0) return PC_OK;
+    return launch_eval<false>(ctx, rec, prog, pred_off, preds, present, wbase, planes, pmax, Wp, I, W, N, feasible,
+                              popcnt, part, ntiles, nullptr, n_preds, L, stream);
+}
 
-    // about 4096 workgroups; a chunk is a whole number of 256-row passes
-    int64_t nchunks = std::max<int64_t>((4096 + ntiles - 1) / ntiles, 1);
-    int64_t rpc = (I + nchunks - 1) / nchunks;
-    rpc = (rpc + kEvalThreads - 1) / kEvalThreads * kEvalThreads;
-    nchunks = (I + rpc - 1) / rpc;
-    const int64_t total = ntiles * nchunks;
-    const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
-    uint32_t *cnt_out = ntiles > 1 ? part : popcnt;
-    const int64_t pbytes = static_cast<int64_t>(pmax + 1) * Wp * 8;
-    auto eval = [&](auto kern) {
-        PC_TIMED(ctx, "k_sel_eval", stream,
-                 hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, pred_off, preds,
-                                    present, wbase, planes, pbytes, Wp, I, static_cast<int32_t>(W), N, feasible,
-                                    cnt_out, static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
-                                    static_cast<int32_t>(rpc)));
+int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off, int32_t I,
+                 const int32_t *term_off, int32_t n_terms, const pc_pred *preds, int64_t n_preds, uint64_t *feasible,
+                 uint32_t *popcnt, uint8_t *unknown, hipStream_t stream)
+{
+    const int64_t W = (static_cast<int64_t>(N) + 63) / 64;
+    const int64_t Wp = (W + 1) / 2 * 2;
+    const int64_t ntiles = (W + kTileW - 1) / kTileW;
+    const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
+    const size_t plane_bytes = static_cast<size_t>(pmax + 1) * static_cast<size_t>(Wp) * 8;
+    if (plane_bytes > (size_t(64) << 30))
+        return pc_set_error(ctx, PC_ENOMEM, "pc_eval_affinity: value planes need %zu bytes (L=%d N=%d)", plane_bytes,
+                            L, N);
+    // indirect programs take slices of prog: room for 4 entries per
+    // expression on average, rounded per row; the rest decode on the fly
+    const int64_t prog_cap = 4 * n_preds + 4 * static_cast<int64_t>(I) + 64;
+    uint64_t *present, *planes;
+    uint32_t *wbase, *prog, *rec, *part;
+    int32_t *d_P;
+    unsigned long long *prog_used;
+    auto carve = [&](Carver &cv) {
+        present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
+        wbase = cv.take<uint32_t>(static_cast<size_t>(L) * 4 + 1);
+        planes = cv.take<uint64_t>(static_cast<size_t>(pmax + 1) * Wp + 2);
+        prog = cv.take<uint32_t>(static_cast<size_t>(prog_cap));
+        rec = cv.take<uint32_t>(static_cast<size_t>(I) * kRecWords + kRecWords);
+        part = ntiles > 1 ? cv.take<uint32_t>(static_cast<size_t>(ntiles) * I + 1) : nullptr;
+        d_P = cv.take<int32_t>(1);
+        prog_used = cv.take<unsigned long long>(1);
     };
-    if (pbytes < (int64_t(1) << 31)) eval(k_sel_eval<true>);  // buffer offsets are 32-bit
-    else eval(k_sel_eval<false>);
-    PC_LAUNCH_CHECK(ctx);
-    if (ntiles > 1) {
-        PC_TIMED(ctx, "k_sel_popsum", stream,
-                 hipLaunchKernelGGL(k_sel_popsum, dim3(static_cast<unsigned>((I + 255) / 256)), dim3(256), 0, stream,
-                                    part, I, static_cast<int32_t>(ntiles), popcnt));
+    Carver dry{nullptr, 0};
+    carve(dry);
+    int rc = pc_ensure_arena(ctx, dry.off);
+    if (rc) return rc;
+    Carver real{ctx->arena, 0};
+    carve(real);
+
+    const int64_t nval = std::max<int64_t>(I, n_terms);
+    if (nval > 0) {
+        const unsigned vgrid = static_cast<unsigned>(std::min<int64_t>((nval + 255) / 256, 8192));
+        PC_TIMED(ctx, "k_aff_validate", stream,
+                 hipLaunchKernelGGL(k_aff_validate, dim3(vgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
+                                    preds, n_preds, L, ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
     }
-    return PC_OK;
+    if (I == 0) return PC_OK;
+    if (W == 0) launch_fill_u32(popcnt, static_cast<size_t>(I), 0, stream);
+    launch_fill_u64(reinterpret_cast<uint64_t *>(prog_used), 1, 0, stream);
+    rc = build_planes(ctx, labels, N, L, W, Wp, pmax, present, wbase, planes, d_P, stream);
+    if (rc) return rc;
+    const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
+    PC_TIMED(ctx, "k_aff_compile", stream,
+             hipLaunchKernelGGL(k_aff_compile, dim3(rgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
+                                preds, n_preds, L, present, wbase, static_cast<uint32_t>(pmax), prog, prog_cap,
+                                prog_used, rec, unknown));
+    PC_LAUNCH_CHECK(ctx);
+    if (W == 0) return PC_OK;
+    return launch_eval<true>(ctx, rec, prog, row_off, preds, present, wbase, planes, pmax, Wp, I, W, N, feasible,
+                             popcnt, part, ntiles, term_off, n_preds, L, stream);
 }

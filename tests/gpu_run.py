@@ -18,6 +18,17 @@ def selectors(labels, pred_off, preds, n_preds=None):
     return f.cpu().numpy().view(np.uint64), p.cpu().numpy().view(np.uint32)
 
 
+def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None):
+    """Feasible bitset, popcount, inventory flags and the data-error word."""
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    f, p, u = pc.pc_eval_affinity(dev(labels), dev(row_off), dev(term_off), dev(preds), n_terms=n_terms,
+                                  n_preds=n_preds)
+    torch.cuda.synchronize()
+    flags = ctx.data_errors(clear=True)
+    return f.cpu().numpy().view(np.uint64), p.cpu().numpy().view(np.uint32), u.cpu().numpy(), flags
+
+
 def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, n_ports=None, n_rules=None):
     out = pc.pc_trace_flows(S, dev(port_off), dev(port_peer), dev(jur), dev(rule_off), dev(rules),
                             dev(np.ascontiguousarray(hdr, np.uint32)), dev(ingress), ttl,

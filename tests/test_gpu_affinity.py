@@ -1,0 +1,182 @@
+"""Parity of pc_eval_affinity (through the C ABI) with the CPU oracle:
+bitsets, popcounts, inventory flags and the data-error word, bit-exact, on
+seeded inputs spanning several 8,192-node tiles with ragged tails, every
+operator, empty rows and terms, programs past the 15-entry inline limit
+(indirect slices and, once the slice buffer is exhausted, on-the-fly
+decoding), malformed inputs, and sampled rows at the combined workload's
+full size."""
+import json
+import os
+
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+HERE = os.path.dirname(os.path.abspath(__file__))
+
+
+@pytest.fixture(scope="module")
+def g():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import gpu_run
+    return gpu_run
+
+
+def _same(a, b, what):
+    a, b = np.asarray(a), np.asarray(b)
+    assert a.shape == b.shape, (what, a.shape, b.shape)
+    bad = np.argwhere(a != b)
+    assert bad.size == 0, f"{what}: first mismatch at {tuple(bad[0])}: gpu {a[tuple(bad[0])]} oracle {b[tuple(bad[0])]}"
+
+
+def _check(g, orc, labels, row_off, term_off, preds, n_terms=None, n_preds=None):
+    fg, pg, ug, eg = g.affinity(labels, row_off, term_off, preds, n_terms=n_terms, n_preds=n_preds)
+    fo, po, uo, eo = orc.affinity(labels, row_off, term_off, preds, n_terms=n_terms, n_preds=n_preds)
+    _same(fg, fo, "feasible")
+    _same(pg, po, "popcnt")
+    _same(ug, uo, "unknown")
+    assert eg == eo, (eg, eo)
+    return fo, po, uo
+
+
+def _pred(label, op, vals=(), thr=None):
+    p = np.zeros(1, synth.PRED_DT)[0]
+    p["label"] = label
+    p["op"] = op
+    bm = [0, 0, 0, 0]
+    for v in vals:
+        bm[int(v) >> 6] |= 1 << (int(v) & 63)
+    if thr is not None:
+        bm = [int(np.int64(thr).view(np.uint64)), 0, 0, 0]
+    p["vals"] = np.array(bm, np.uint64)
+    return p
+
+
+def _csr(rows):
+    row_off, term_off, preds = [0], [0], []
+    for row in rows:
+        for term in row:
+            preds.extend(term)
+            term_off.append(len(preds))
+        row_off.append(len(term_off) - 1)
+    arr = np.array(preds, synth.PRED_DT) if preds else np.zeros(0, synth.PRED_DT)
+    return np.array(row_off, np.int32), np.array(term_off, np.int32), arr
+
+
+@pytest.mark.parametrize("seed,N,absent", [(0, 5037, 0.1), (1, 20000 + 5, 0.0), (2, 100, 0.3)])
+def test_affinity_random(g, orc, seed, N, absent):
+    wl = synth.affinity_workload(seed, N, 12, 900, card_choices=(2, 3, 16, 64, 200), absent_p=absent,
+                                 tmin=0, tmax=4, kmin=0, kmax=5)
+    fo, po, uo = _check(g, orc, wl["labels"], wl["row_off"], wl["term_off"], wl["preds"])
+    assert (po > 0).any() and (po == 0).any()
+
+
+def test_affinity_paper_fixture(g, orc):
+    fx = json.load(open(os.path.join(HERE, "golden", "paper_affinity.json")))
+    keys, nodes = fx["keys"], fx["nodes"]
+    codes = {k: {v: i for i, v in enumerate(sorted({n[k] for n in nodes if k in n}))} for k in keys}
+    for case in fx["cases"]:
+        for term in case["terms"]:
+            for k, _, vals in term:
+                for v in vals:
+                    codes[k].setdefault(v, len(codes[k]))
+    labels = np.full((len(nodes), len(keys)), synth.ABSENT, np.uint8)
+    for i, n in enumerate(nodes):
+        for j, k in enumerate(keys):
+            if k in n:
+                labels[i, j] = codes[k][n[k]]
+    ops = {"In": 0, "NotIn": 1, "Exists": 2, "DoesNotExist": 3, "Gt": 4, "Lt": 5}
+    rows = [[[_pred(keys.index(k), ops[op], [codes[k][v] for v in vals]) for k, op, vals in term]
+             for term in case["terms"]] for case in fx["cases"]]
+    _, po, uo = _check(g, orc, labels, *_csr(rows))
+    assert po.tolist() == [len(c["expect"]) for c in fx["cases"]]
+    assert uo.tolist() == [c["unknown"] for c in fx["cases"]]
+
+
+def test_affinity_long_programs(g, orc):
+    """Programs of every length up to ~250 entries: inline, indirect slices,
+    and -- once the slice buffer runs out -- rows decoded on the fly."""
+    rng = np.random.default_rng(4)
+    N = 9000 + 3
+    labels = np.stack([rng.integers(0, 254, N), rng.integers(0, 128, N), rng.integers(0, 6, N)],
+                      axis=1).astype(np.uint8)
+    labels[rng.random(labels.shape) < 0.05] = synth.ABSENT
+    rows = []
+    for m in list(range(0, 40, 3)) + [60, 90, 126, 127, 128, 200]:
+        for nterm in (1, 2, 3):
+            row = []
+            for t in range(nterm):
+                term = [_pred(0, int(rng.integers(0, 2)), rng.choice(254, size=m, replace=False))]
+                if t >= 1:
+                    term.append(_pred(1, 4, thr=int(rng.integers(-2, 130))))
+                if t >= 2:
+                    term.append(_pred(2, int(rng.integers(2, 4))))
+                row.append(term)
+            rows.append(row)
+    _check(g, orc, labels, *_csr(rows))
+
+
+def test_affinity_gt_lt_thresholds(g, orc):
+    rng = np.random.default_rng(6)
+    N = 3000
+    labels = np.stack([rng.integers(0, 255, N), rng.integers(0, 7, N)], axis=1).astype(np.uint8)
+    labels[rng.random(labels.shape) < 0.1] = synth.ABSENT
+    rows = [[[_pred(lab, op, thr=t)]] for lab in range(2) for t in list(range(-3, 259)) + [-(1 << 63), (1 << 63) - 1]
+            for op in (4, 5)]
+    rows += [[[_pred(lab, op)]] for lab in range(2) for op in (2, 3)]
+    _check(g, orc, labels, *_csr(rows))
+
+
+def test_affinity_malformed(g, orc):
+    labels = np.array([[0, 1], [1, 1], [2, synth.ABSENT]], np.uint8)
+    good = _pred(0, 0, [1, 2])
+    bad_gt = _pred(0, 4, thr=0)
+    bad_gt["vals"][1] = 1
+    bad_in = _pred(0, 0, [1])
+    bad_in["vals"][3] |= np.uint64(1) << np.uint64(63)
+    bad_rsv = good.copy()
+    bad_rsv["rsv0"] = 1
+    for bad in (_pred(0, 6), _pred(2, 2), bad_gt, bad_in, bad_rsv):
+        _check(g, orc, labels, *_csr([[[bad], [good]], [[good]], [[bad]]]))
+    # a malformed expression in a term no row references still raises the flag
+    row_off, term_off, preds = _csr([[[good]], [[bad_gt]]])
+    _check(g, orc, labels, row_off[:2], term_off, preds)
+    # bad term and row offsets
+    row_off = np.array([0, 2, 1, 3, 7], np.int32)
+    term_off = np.array([0, 1, 9, 2], np.int32)
+    preds = np.array([good, _pred(1, 2)], synth.PRED_DT)
+    _check(g, orc, labels, row_off, term_off, preds)
+
+
+def test_affinity_empty(g, orc):
+    labels = np.array([[0], [1]], np.uint8)
+    good = _pred(0, 0, [1])
+    # rows without terms, empty terms only, and no rows at all (terms still validated)
+    _check(g, orc, labels, *_csr([[], [[]], [[], [good]]]))
+    row_off, term_off, preds = _csr([[[_pred(0, 7)]]])
+    _check(g, orc, labels, row_off[:1], term_off, preds)
+    # no nodes: every referenced label and value is unknown
+    _check(g, orc, np.zeros((0, 1), np.uint8), *_csr([[[good]], [[_pred(0, 3)]]]))
+
+
+def test_affinity_full_size_sampled(g, orc):
+    """The combined workload's cluster (50,000 nodes x 64 labels) with
+    699,051 affinity rows, in the benchmark's launch configuration; every
+    1,024th row re-evaluated by the oracle, popcount = bit count and zero
+    padding on every row."""
+    wl = synth.affinity_workload(4, 50000, 64, 699051)
+    fg, pg, ug, eg = g.affinity(wl["labels"], wl["row_off"], wl["term_off"], wl["preds"])
+    assert eg == 0
+    rows = np.arange(0, 699051, 1024, dtype=np.int32)
+    fo, po, uo, eo = orc.affinity(wl["labels"], wl["row_off"], wl["term_off"], wl["preds"], rows=rows)
+    assert eo == 0
+    _same(fg[rows], fo, "feasible")
+    _same(pg[rows], po, "popcnt")
+    _same(ug[rows], uo, "unknown")
+    bits = np.bitwise_count(fg).sum(axis=1, dtype=np.int64)
+    assert np.array_equal(bits, pg.astype(np.int64))
+    assert ((fg[:, -1] >> np.uint64(50000 % 64)) == 0).all()
