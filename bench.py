@@ -25,25 +25,28 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 
-# HBM bytes per launch of k_sel_eval on the combined workload, from one
-# rocprofv3 FETCH_SIZE pass and one WRITE_SIZE pass, each scaled by what
-# the same counter reads for a plain copy of known size (the command lines
-# and counter values are in profiles/k_sel_eval_cfg5_hbm_counters.md).
-# Valid only for the kernel source it was measured on.
-SEL_TRAFFIC = {"source": "paper_2602_16100_amd/csrc/select.hip",
-               "sha256": "7a6761f972af716cbf6e589176a0ff057677988f419f97acbe6ffd2abc62088c",
-               "workload": "cfg5", "bytes_per_launch": 797_608_752 + 4_473_972_928}
+# HBM bytes per launch of k_sel_eval and k_aff_eval on the combined
+# workload's cluster, from one rocprofv3 FETCH_SIZE pass and one WRITE_SIZE
+# pass each, scaled by what the same counter reads for a plain copy of known
+# size (the command lines and counter values are in
+# profiles/k_sel_eval_cfg5_hbm_counters.md).  Valid only for the kernel
+# source they were measured on.
+TRAFFIC = {"source": "paper_2602_16100_amd/csrc/select.hip",
+           "sha256": "a2f3ab0de4a4625ce0b3aeffca455547a03e1fd788324155eb86fd17fa55ae20",
+           "workload": "cfg5",
+           "bytes_per_launch": {"k_sel_eval": 797_440_007 + 4_473_968_384,
+                                "k_aff_eval": 1_022_633_778 + 4_474_097_162}}
 
 
-def measured_traffic(workload):
+def measured_traffic(workload, kernel):
     import hashlib
-    path = os.path.join(ROOT, SEL_TRAFFIC["source"])
-    if workload != SEL_TRAFFIC["workload"] or not os.path.exists(path):
+    path = os.path.join(ROOT, TRAFFIC["source"])
+    if workload != TRAFFIC["workload"] or not os.path.exists(path):
         return None
     with open(path, "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != SEL_TRAFFIC["sha256"]:
+        if hashlib.sha256(f.read()).hexdigest() != TRAFFIC["sha256"]:
             return None
-    return SEL_TRAFFIC["bytes_per_launch"]
+    return TRAFFIC["bytes_per_launch"].get(kernel)
 
 
 def parse():
@@ -55,11 +58,14 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths"],
+    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity"],
                     help="profiling aid: time one stage only (the JSON line then covers that stage); 'paths' "
-                         "times only the pass with waypoint / forbidden-switch constraints")
+                         "times only the pass with waypoint / forbidden-switch constraints, 'affinity' only the "
+                         "node-affinity pass")
     ap.add_argument("--no-paths", action="store_true",
                     help="skip the second timed pass with waypoint / forbidden-switch constraints")
+    ap.add_argument("--no-affinity", action="store_true",
+                    help="skip the timed pass of full node affinity over the same cluster")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="profiling aid: run a plain device copy of MIB MiB three times (HBM counter calibration)")
     return ap.parse_args()
@@ -218,6 +224,85 @@ def time_paths(args, wl, D, pc, ctx, feasible, popcnt):
     return out
 
 
+def time_affinity(args, wl, pc, ctx, feasible):
+    """Timed pass of full node affinity (pc_eval_affinity) over the same
+    cluster: one required-affinity row per selector row (1-3 OR-ed terms of
+    1-4 expressions, six operators), written into the same bitset shape."""
+    import torch
+    import synth
+    dev = feasible.device
+    I = feasible.shape[0]
+    row_off, term_off, preds = synth.affinity_rows(wl.seed, wl.meta["cards"], I)
+    D = {k: pc.to_device(v, dev) for k, v in (("labels", wl["labels"]), ("row_off", row_off),
+                                               ("term_off", term_off), ("preds", preds))}
+    popcnt = torch.empty(I, dtype=torch.int32, device=dev)
+    unknown = torch.empty(I, dtype=torch.uint8, device=dev)
+
+    def step():
+        pc.pc_eval_affinity(D["labels"], D["row_off"], D["term_off"], D["preds"], feasible=feasible, popcnt=popcnt,
+                            unknown=unknown, ctx=ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.data_errors(clear=True)
+    ctx.profile(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = ctx.profile_read()
+    ctx.profile(False)
+    flags = ctx.data_errors(clear=True)
+    N, L = wl["N"], wl["L"]
+    W = (N + 63) // 64
+    n_eval, eval_ms = prof["k_aff_eval"]
+    avg_ms = eval_ms / max(n_eval, 1)
+    n_terms, n_preds = term_off.shape[0] - 1, preds.shape[0]
+    # the bitset, popcounts and inventory flags written; labels, expressions
+    # and both offset arrays read once
+    alg = I * W * 8 + I * 4 + I + n_preds * 40 + (n_terms + 1) * 4 + (I + 1) * 4 + N * L
+    achieved = alg / (avg_ms * 1e-3) / 1e9
+    pairs = I * N
+    pcnt = popcnt.cpu().numpy()
+    out = {
+        "rows": I, "terms": int(n_terms), "expressions": int(n_preds),
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "evals_per_s": pairs * args.steps / elapsed,
+        "per_kernel": {name: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
+                       for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])},
+        "roofline": {"kernel": "k_aff_eval", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(args.workload, "k_aff_eval"), "alg_bytes_per_launch": alg,
+                     "avg_launch_ms": avg_ms},
+        "feasible_rows": int((pcnt > 0).sum()),
+        "unknown_rows": int((unknown.cpu().numpy() != 0).sum()),
+        "data_error_flags": flags,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = len(os.sched_getaffinity(0))
+        env_cap = os.environ.get("OMP_NUM_THREADS")
+        if env_cap and env_cap.isdigit():
+            threads = min(threads, int(env_cap))
+        stride, t = 4096, 0.0
+        while True:
+            rows = np.arange(0, I, stride, dtype=np.int32)
+            t0 = time.perf_counter()
+            oracle.affinity(wl["labels"], row_off, term_off, preds, rows=rows, nthreads=threads)
+            t = time.perf_counter() - t0
+            if t >= args.cpu_seconds / 6 or stride == 1:
+                break
+            stride = max(1, stride // 64, int(stride * max(t, 1e-3) / (args.cpu_seconds / 3)))
+        est = t * I / rows.shape[0]
+        out["cpu_baseline"] = {"value": pairs / est, "unit": "affinity evals/s (whole-pass estimate)",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"every {stride}th row ({rows.shape[0]} of {I} rows x {N} nodes) in "
+                                         f"{t:.2f} s; whole pass estimated at {est:.1f} s"}
+    return out
+
+
 def cpu_baseline_paths(wl, gpu_ms, target_s):
     """The oracle on every k-th flow of the constrained pass (traces with
     watch lists and waypoint reach), scaled to the whole pass."""
@@ -284,6 +369,9 @@ def main():
     ctx = pc.context(0)
 
     only = args.only
+    if only == "affinity":
+        print(json.dumps({"workload": desc, "affinity": time_affinity(args, wl, pc, ctx, feasible)}), flush=True)
+        return
     if only == "paths":
         # the bitsets the verdict reads, computed once outside the timed pass
         pc.pc_eval_selectors(D["labels"], D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
@@ -376,13 +464,16 @@ def main():
                               "pc_masked_reach": ktime("k_rc_"), "pc_report": ktime("k_report")},
         "per_kernel": per_kernel,
         "roofline": {"kernel": roof_kernel, "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
-                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS, "traffic": measured_traffic(args.workload),
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(args.workload, roof_kernel),
                      "alg_bytes_per_launch": alg_bytes, "avg_launch_ms": avg_eval_ms},
         "verdict": {"passed": passed, "intents": I},
         "data_error_flags": flags,
     }
     if only == "all" and not args.no_paths:
         line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)
+    if only == "all" and not args.no_affinity:
+        line["affinity"] = time_affinity(args, wl, pc, ctx, feasible)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, pairs, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -233,6 +233,12 @@ def affinity_workload(seed, N, L, I, card_choices=(2, 4, 16, 64), absent_p=0.0, 
     return wl
 
 
+def affinity_rows(seed, cards, I, tmin=1, tmax=3, kmin=1, kmax=4):
+    """I required-affinity rows (gen_affinity) over a cluster whose labels
+    have the given cardinalities, from their own generator [seed, 12]."""
+    return gen_affinity(np.random.default_rng([seed, 12]), I, cards, tmin, tmax, kmin, kmax)
+
+
 def gen_preds_holding(rng, labels, cards, a, b, kmin, kmax, mmax=4):
     """Selector rows built so that nodes a[r] and b[r] satisfy row r: In sets
     contain both endpoints' values, NotIn sets avoid them (a NotIn with no
