@@ -24,6 +24,9 @@ TRACE_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port", "<u
 assert TRACE_DT.itemsize == 12
 SUMMARY_DT = np.dtype([("counts", "<u8", (4, 16)), ("no_path", "<u8", (4,))])
 PATH_EXPECT_DT = np.dtype([("must", "<u4"), ("forbid", "<u4")])
+RULE_DT = np.dtype([("value", "<u4", (4,)), ("mask", "<u4", (4,)), ("priority", "<u2"), ("action", "<u2"),
+                    ("rsv", "<u4")])
+assert RULE_DT.itemsize == 40
 
 EGRESS, DROP, MISS, TTL = 0, 1, 2, 3
 F_PRED, F_OFFSETS, F_ACTION, F_SWITCH, F_JUR, F_GRAPH, F_INTENT = 1, 2, 4, 8, 16, 32, 64
@@ -52,6 +55,8 @@ def _load():
         C = ctypes.c_int
         _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
         _lib.orc_affinity.argtypes = [P, I64, I64, P, I64, P, I64, P, I64, P, I64, P, P, P, P, C]
+        _lib.orc_synthesize.argtypes = [I64, P, P, I64, P, P, I64, P, P, P, P, I64, P, I64, P, P, I64, I64, P,
+                                        I64, P, P, P, P, C]
         _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, C]
         _lib.orc_reach.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, P, C]
         _lib.orc_reach_via.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, I64, P, I64, P, P, C]
@@ -112,6 +117,37 @@ def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None, rows=
                      _p(np.ascontiguousarray(term_off, np.int32)), n_terms, _p(np.ascontiguousarray(preds)),
                      n_preds, _p(rows), rows.shape[0], _p(feas), _p(pc), _p(unk), _p(err), nthreads)
     return feas, pc, unk, int(err[0])
+
+
+def synthesize(V, port_off, port_peer, region, src, target, allowed, via, forbid, key, out_port, prio, max_hops,
+               weight=None, qidx=None, n_ports=None, nthreads=0):
+    """Path synthesis: per request the walk's hop count (-1 = none), its
+    switches [nq, max_hops+1] (-1 past the end) and one rule per switch
+    [nq, max_hops+1] (zero past the end).  via [Q, Kv] / forbid [Q, Kf]
+    switch ids, -1 = unused; key uint32 [Q, 4]; weight uint32 per port or
+    None (every link weighs 1).  Returns (hops, path, rules, flags)."""
+    lib = _load()
+    Q = src.shape[0]
+    if qidx is None:
+        qidx = np.arange(Q, dtype=np.int64)
+    qidx = np.ascontiguousarray(qidx, np.int64)
+    via = np.ascontiguousarray(via, np.int32).reshape(Q, -1)
+    forbid = np.ascontiguousarray(forbid, np.int32).reshape(Q, -1)
+    n_ports = port_peer.shape[0] if n_ports is None else n_ports
+    slots = max_hops + 1
+    hops = np.zeros(qidx.shape[0], np.int32)
+    path = np.zeros((qidx.shape[0], slots), np.int32)
+    rules = np.zeros((qidx.shape[0], slots), RULE_DT)
+    err = np.zeros(1, np.uint32)
+    lib.orc_synthesize(V, _p(np.ascontiguousarray(port_off, np.int32)), _p(np.ascontiguousarray(port_peer, np.int32)),
+                       n_ports, None if weight is None else _p(np.ascontiguousarray(weight, np.uint32)),
+                       _p(np.ascontiguousarray(region, np.uint8)), Q, _p(np.ascontiguousarray(src, np.int32)),
+                       _p(np.ascontiguousarray(target, np.int32)), _p(np.ascontiguousarray(allowed, np.uint32)),
+                       _p(via), via.shape[1], _p(forbid), forbid.shape[1],
+                       _p(np.ascontiguousarray(key, np.uint32)), _p(np.ascontiguousarray(out_port, np.int32)),
+                       int(prio), int(max_hops), _p(qidx), qidx.shape[0], _p(hops), _p(path), _p(rules), _p(err),
+                       nthreads)
+    return hops, path, rules, int(err[0])
 
 
 def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=None,

@@ -551,6 +551,226 @@ void orc_reach_via(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_
     }
 }
 
+/* ------------------------------------------------------------------ NEXT-2
+ * Path synthesis (paper, Sec. "Network orchestration": a path scheduler
+ * performs graph search over the current topology -- weighted Dijkstra,
+ * BFS fallback -- to produce a path that respects the constraints, and
+ * each path is turned into per-hop flow rules).
+ * Graph: switch s owns ports port_off[s] .. port_off[s+1]; a port with
+ * peer v in [0, V) and weight >= 1 is a link s -> v of that weight (weight
+ * NULL: every link weighs 1, i.e. BFS).  A switch is usable by a request
+ * when its region is allowed and it is not on the request's forbidden list.
+ * Each leg (src -> via[0] -> ... -> target; the waypoint list ends at its
+ * first -1) is a
+ * minimum-weight path through usable switches; among those, the
+ * predecessor of every switch v is the lowest-numbered u with a link
+ * u -> v and dist(u) + w = dist(v) -- the lexicographically smallest path
+ * read from its end.  The walk is the legs concatenated.  Switch path[k]
+ * of the walk gets one rule: value = key, mask = the key's 104 bits,
+ * priority = prio, action = its port of least (weight, index) to path[k+1],
+ * or out_port at the last switch.
+ * A request fails (hops -1, path -1, rules zero) when an endpoint or
+ * waypoint is out of range, a leg has no path, out_port is not a port of
+ * the target, or the walk has more than max_hops links.
+ * Flags (input properties): OFFSETS bad port_off pair; SWITCH a peer < -1
+ * or >= V, src / target outside [0, V), a via / forbid entry < -1 or >= V;
+ * JUR region >= 32; GRAPH a zero weight (that port is no link); ACTION
+ * out_port not a port of a target whose ports are well-formed.
+ */
+typedef struct { int64_t d; int64_t v; } ps_item;
+
+static void heap_push(ps_item *h, int64_t *n, ps_item x)
+{
+    int64_t i = (*n)++;
+    while (i > 0) {
+        const int64_t par = (i - 1) / 2;
+        if (h[par].d < x.d || (h[par].d == x.d && h[par].v <= x.v)) break;
+        h[i] = h[par];
+        i = par;
+    }
+    h[i] = x;
+}
+
+static ps_item heap_pop(ps_item *h, int64_t *n)
+{
+    const ps_item top = h[0];
+    const ps_item x = h[--(*n)];
+    int64_t i = 0;
+    for (;;) {
+        int64_t c = 2 * i + 1;
+        if (c >= *n) break;
+        if (c + 1 < *n && (h[c + 1].d < h[c].d || (h[c + 1].d == h[c].d && h[c + 1].v < h[c].v))) ++c;
+        if (x.d < h[c].d || (x.d == h[c].d && x.v <= h[c].v)) break;
+        h[i] = h[c];
+        i = c;
+    }
+    if (*n > 0) h[i] = x;
+    return top;
+}
+
+typedef struct {
+    int64_t V, n_ports;
+    const int32_t *port_off, *port_peer;
+    const uint32_t *weight;
+    const uint8_t *region;
+} ps_graph;
+
+/* weight of port p as a link, or 0 when it is none */
+static int64_t ps_link(const ps_graph *g, int64_t p)
+{
+    const int64_t v = g->port_peer[p];
+    if (v < 0 || v >= g->V) return 0;
+    return g->weight ? (int64_t)g->weight[p] : 1;
+}
+
+/* one leg s -> t: number of links (path in buf[0..hops], s first), or -1 */
+static int64_t ps_leg(const ps_graph *g, uint32_t A, const int32_t *fb, int64_t Kf, int64_t s, int64_t t,
+                      int64_t *dist, ps_item *heap, int64_t *buf)
+{
+    const int64_t V = g->V;
+    if (!usable(g->region, A, fb, Kf, s) || !usable(g->region, A, fb, Kf, t)) return -1;
+    for (int64_t v = 0; v < V; ++v) dist[v] = -1;
+    int64_t hn = 0;
+    dist[s] = 0;
+    heap_push(heap, &hn, (ps_item){0, s});
+    while (hn > 0) {
+        const ps_item it = heap_pop(heap, &hn);
+        if (it.d != dist[it.v]) continue; /* stale entry */
+        const int64_t b = g->port_off[it.v], e = g->port_off[it.v + 1];
+        if (!range_ok(b, e, g->n_ports)) continue;
+        for (int64_t p = b; p < e; ++p) {
+            const int64_t w = ps_link(g, p);
+            if (w <= 0) continue;
+            const int64_t u = g->port_peer[p];
+            if (!usable(g->region, A, fb, Kf, u)) continue;
+            if (dist[u] < 0 || it.d + w < dist[u]) {
+                dist[u] = it.d + w;
+                heap_push(heap, &hn, (ps_item){dist[u], u});
+            }
+        }
+    }
+    if (dist[t] < 0) return -1;
+    /* walk back from t: predecessor = lowest-numbered u with a link u -> cur, dist(u) + w = dist(cur) */
+    int64_t n = 0, cur = t;
+    buf[n++] = cur;
+    while (cur != s) {
+        int64_t pred = -1;
+        for (int64_t u = 0; u < V && pred < 0; ++u) {
+            if (dist[u] < 0) continue;
+            const int64_t b = g->port_off[u], e = g->port_off[u + 1];
+            if (!range_ok(b, e, g->n_ports)) continue;
+            for (int64_t p = b; p < e; ++p) {
+                const int64_t w = ps_link(g, p);
+                if (w > 0 && g->port_peer[p] == cur && dist[u] + w == dist[cur]) { pred = u; break; }
+            }
+        }
+        cur = pred;
+        buf[n++] = cur;
+    }
+    for (int64_t i = 0; i < n / 2; ++i) {
+        const int64_t x = buf[i];
+        buf[i] = buf[n - 1 - i];
+        buf[n - 1 - i] = x;
+    }
+    return n - 1;
+}
+
+/* the port of u of least (weight, index) that links u -> v */
+static int64_t ps_port(const ps_graph *g, int64_t u, int64_t v)
+{
+    const int64_t b = g->port_off[u];
+    int64_t best = -1, bw = 0;
+    for (int64_t p = b; p < g->port_off[u + 1]; ++p) {
+        const int64_t w = ps_link(g, p);
+        if (w > 0 && g->port_peer[p] == v && (best < 0 || w < bw)) { best = p - b; bw = w; }
+    }
+    return best;
+}
+
+void orc_synthesize(int64_t V, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
+                    const uint32_t *weight, const uint8_t *region, int64_t Q, const int32_t *src,
+                    const int32_t *target, const uint32_t *allowed, const int32_t *via, int64_t Kv,
+                    const int32_t *forbid, int64_t Kf, const uint32_t *key, const int32_t *out_port,
+                    int64_t prio, int64_t max_hops, const int64_t *qidx, int64_t nq, int32_t *hops,
+                    int32_t *path, o_rule *rules, uint32_t *err, int nthreads)
+{
+    set_threads(nthreads);
+    const ps_graph g = {V, n_ports, port_off, port_peer, weight, region};
+    const int64_t slots = max_hops + 1;
+    for (int64_t v = 0; v < V; ++v) {
+        if (region[v] >= 32) *err |= F_JUR;
+        if (!range_ok(port_off[v], port_off[v + 1], n_ports)) *err |= F_OFFSETS;
+    }
+    for (int64_t p = 0; p < n_ports; ++p) {
+        if (port_peer[p] < -1 || port_peer[p] >= V) *err |= F_SWITCH;
+        if (weight && weight[p] == 0) *err |= F_GRAPH;
+    }
+    for (int64_t q = 0; q < Q; ++q) {
+        const int64_t t = target[q];
+        if (src[q] < 0 || src[q] >= V || t < 0 || t >= V) { *err |= F_SWITCH; continue; }
+        if (range_ok(port_off[t], port_off[t + 1], n_ports) &&
+            (out_port[q] < 0 || out_port[q] >= port_off[t + 1] - port_off[t]))
+            *err |= F_ACTION;
+    }
+    for (int64_t i = 0; i < Q * Kv; ++i)
+        if (via[i] < -1 || via[i] >= V) { *err |= F_SWITCH; break; }
+    for (int64_t i = 0; i < Q * Kf; ++i)
+        if (forbid[i] < -1 || forbid[i] >= V) { *err |= F_SWITCH; break; }
+#pragma omp parallel
+    {
+        const size_t nv = (size_t)(V > 0 ? V : 1);
+        int64_t *dist = (int64_t *)malloc(sizeof(int64_t) * nv);
+        int64_t *buf = (int64_t *)malloc(sizeof(int64_t) * (nv + 1));
+        int64_t *walk = (int64_t *)malloc(sizeof(int64_t) * (size_t)(slots + 1));
+        ps_item *heap = (ps_item *)malloc(sizeof(ps_item) * (size_t)(n_ports + 2));
+#pragma omp for schedule(dynamic, 1)
+        for (int64_t k = 0; k < nq; ++k) {
+            const int64_t q = qidx[k];
+            int32_t *pk = path + k * slots;
+            o_rule *rk = rules + k * slots;
+            for (int64_t i = 0; i < slots; ++i) pk[i] = -1;
+            memset(rk, 0, sizeof(o_rule) * (size_t)slots);
+            hops[k] = -1;
+            const int64_t s = src[q], t = target[q];
+            if (s < 0 || s >= V || t < 0 || t >= V) continue;
+            if (!range_ok(port_off[t], port_off[t + 1], n_ports) || out_port[q] < 0 ||
+                out_port[q] >= port_off[t + 1] - port_off[t])
+                continue;
+            const int32_t *w = via + q * Kv;
+            const int32_t *fb = forbid + q * Kf;
+            int64_t m = 0;
+            while (m < Kv && w[m] != -1) ++m;
+            int64_t total = 0, from = s, ok = 1;
+            walk[0] = s;
+            for (int64_t leg = 0; leg <= m && ok; ++leg) {
+                const int64_t to = leg < m ? w[leg] : t;
+                if (to < 0 || to >= V) { ok = 0; break; }
+                const int64_t d = ps_leg(&g, allowed[q], fb, Kf, from, to, dist, heap, buf);
+                if (d < 0 || total + d > max_hops) { ok = 0; break; }
+                for (int64_t i = 1; i <= d; ++i) walk[total + i] = buf[i];
+                total += d;
+                from = to;
+            }
+            if (!ok) continue;
+            hops[k] = (int32_t)total;
+            for (int64_t i = 0; i <= total; ++i) {
+                pk[i] = (int32_t)walk[i];
+                o_rule *r = &rk[i];
+                for (int j = 0; j < 4; ++j) {
+                    r->value[j] = key[q * 4 + j];
+                    r->mask[j] = j < 3 ? 0xFFFFFFFFu : 0xFFu;
+                }
+                r->priority = (uint16_t)prio;
+                r->action = (uint16_t)(i < total ? ps_port(&g, walk[i], walk[i + 1]) : out_port[q]);
+            }
+        }
+        free(dist);
+        free(buf);
+        free(walk);
+        free(heap);
+    }
+}
+
 /* ------------------------------------------------------------------ A6
  * Per-intent verdict: pass iff every check of the intent passes (paper,
  * validator check definition); an unenforceable intent fails closed.

@@ -748,6 +748,45 @@ def path_constraints(seed, S, sw, nh, n_forbid=2, p_on_path=0.5, p_forbid_on_pat
     return way[:, None].astype(np.int32), forbid.astype(np.int32)
 
 
+def port_weights(seed, n_ports, wmax=10):
+    """Link weights per port, uniform over 1..wmax, from their own
+    generator [seed, 13] (latency-like costs for a weighted path search)."""
+    return np.random.default_rng([seed, 13]).integers(1, wmax + 1, size=n_ports).astype(np.uint32)
+
+
+def synthesis_requests(seed, topo, Q, Kv=1, Kf=2, p_via=0.7, p_other_jur=0.5):
+    """Q path-synthesis requests between uniform distinct hosts of a
+    topology: source and target are the hosts' switches, out_port the
+    destination host's port, key a fresh random 5-tuple per request.  The
+    allowed jurisdictions are both endpoints' plus each other one with
+    probability p_other_jur; up to Kv waypoints (as many as slots drawn
+    with probability p_via, in the first slots; uniform switches; the list
+    ends at its first -1) and Kf uniform forbidden switches
+    (-1 when one would hit an endpoint or a waypoint).  Own generator
+    [seed, 14]."""
+    rng = np.random.default_rng([seed, 14])
+    S, J, H = topo["S"], topo["J"], topo["H"]
+    a = rng.integers(0, H, size=Q)
+    b = (a + rng.integers(1, H, size=Q)) % H
+    src = topo["host_switch"][a].astype(np.int32)
+    dst = topo["host_switch"][b].astype(np.int32)
+    out_port = topo["host_port"][b].astype(np.int32)
+    jur = topo["jur"].astype(np.int64)
+    allowed = (np.left_shift(1, jur[src]) | np.left_shift(1, jur[dst])).astype(np.uint32)
+    for j in range(J):
+        allowed |= np.where(rng.random(Q) < p_other_jur, np.uint32(1 << j), np.uint32(0))
+    # waypoint lists end at their first -1 (used slots first)
+    n_via = (rng.random((Q, Kv)) < p_via).sum(axis=1)
+    via = np.where(np.arange(Kv)[None, :] < n_via[:, None], rng.integers(0, S, size=(Q, Kv)), -1).astype(np.int32)
+    forbid = rng.integers(0, S, size=(Q, Kf)).astype(np.int32)
+    clash = (forbid == src[:, None]) | (forbid == dst[:, None])
+    for c in range(Kv):
+        clash |= forbid == via[:, c:c + 1]
+    forbid[clash] = -1
+    key = random_keys(rng, Q)
+    return dict(src=src, target=dst, out_port=out_port, allowed=allowed, via=via, forbid=forbid, key=key)
+
+
 def _add_paths(wl, via_q, forb_q, trace_q, pexp_rows):
     """Attach path constraints: query q's via / forbid lists; trace t
     watches [waypoint, forbidden...] of its query trace_q[t]; network
