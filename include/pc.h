@@ -23,6 +23,11 @@
  *                         checks with required waypoints and forbidden
  *                         switches (the routing constraints of a
  *                         Configuration; must_go / forbidden lists).
+ *   - pc_eval_affinity  : placement with full node affinity (OR-ed terms,
+ *                         six operators, label-inventory flags).
+ *   - pc_synthesize_paths : the step before validation -- the path
+ *                         scheduler's search for a compliant path and its
+ *                         compilation into per-hop flow rules.
  *
  * Conventions shared by every entry point
  *   - Every array argument is a DEVICE pointer owned by the caller; it must
@@ -54,7 +59,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 3
+#define PC_VERSION 4
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -382,6 +387,51 @@ int pc_report_paths(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t ro
                     const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
                     const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary,
                     void *stream);
+
+/* Largest topology pc_synthesize_paths accepts (its per-request search
+ * state lives in on-chip memory). */
+#define PC_SYNTH_MAX_V 12288
+
+/*
+ * NEXT-2 -- compliant path synthesis (paper: Network orchestration -- a path
+ * scheduler performs graph search over the current topology, weighted
+ * Dijkstra with a BFS fallback, to produce a path that respects the
+ * constraints; each path is transformed into per-hop flow rules).
+ * Graph: switch s owns ports port_off[s] .. port_off[s+1]; a port with peer
+ * v in [0, V) and weight >= 1 is a link s -> v (weight NULL: every link
+ * weighs 1, i.e. BFS).  A switch is usable by request q when its region is
+ * allowed by allowed[q] and it is not in forbid[q][0..Kf) (-1 = unused).
+ * The walk of request q is src[q] -> via[q][0] -> ... -> target[q] (the
+ * waypoint list ends at its first -1), one minimum-weight leg per stop
+ * through usable switches; the predecessor of every switch on a leg is the
+ * lowest-numbered u with a link u -> v and dist(u) + w = dist(v).
+ * Outputs (caller-owned device arrays):
+ *   hops  : int32 [Q], links of the walk, -1 when the request fails.
+ *   path  : int32 [Q][max_hops + 1], the walk's switches (src first), -1 past
+ *           its end (all -1 on failure).
+ *   rules : pc_rule [Q][max_hops + 1], one per switch of the walk: value =
+ *           key[q], mask = the 104 key bits (words 0-2 and bits 0-7 of word
+ *           3), priority = prio, action = the switch's port of least (weight,
+ *           index) to the next switch, out_port[q] at the last switch; zero
+ *           past the walk's end (all zero on failure).  A walk that passes a
+ *           switch twice cannot be realised by rules that match the 5-tuple
+ *           only; it is returned as found.
+ * A request fails when an endpoint or waypoint is out of range or not
+ * usable, a leg has no path, out_port[q] is not a port of the target, or the
+ * walk has more than max_hops links.
+ * Limits: 0 <= V <= PC_SYNTH_MAX_V, 0 <= Q, 0 <= Kv, Kf <= 32,
+ * 0 <= max_hops <= 255, 0 <= prio <= 65535.  Malformed data: bad port_off
+ * pair -> the switch has no ports (PC_DERR_OFFSETS); peer < -1 or >= V, src
+ * or target outside [0, V), via / forbid entry < -1 or >= V
+ * (PC_DERR_SWITCH); region >= 32 never allowed (PC_DERR_JUR); a zero weight
+ * -> that port is no link (PC_DERR_GRAPH); out_port not a port of a target
+ * with valid offsets (PC_DERR_ACTION).
+ */
+int pc_synthesize_paths(pc_ctx *ctx, int32_t V, const int32_t *port_off, const int32_t *port_peer,
+                        int64_t n_ports, const uint32_t *weight, const uint8_t *region, int32_t Q,
+                        const int32_t *src, const int32_t *target, const uint32_t *allowed, const int32_t *via,
+                        int32_t Kv, const int32_t *forbid, int32_t Kf, const pc_key *key, const int32_t *out_port,
+                        int32_t prio, int32_t max_hops, int32_t *hops, int32_t *path, pc_rule *rules, void *stream);
 
 #ifdef __cplusplus
 }

@@ -131,8 +131,10 @@ def synthesize(V, port_off, port_peer, region, src, target, allowed, via, forbid
     if qidx is None:
         qidx = np.arange(Q, dtype=np.int64)
     qidx = np.ascontiguousarray(qidx, np.int64)
-    via = np.ascontiguousarray(via, np.int32).reshape(Q, -1)
-    forbid = np.ascontiguousarray(forbid, np.int32).reshape(Q, -1)
+    via = np.ascontiguousarray(via, np.int32)
+    via = via.reshape(Q, via.shape[1] if via.ndim == 2 else 1)
+    forbid = np.ascontiguousarray(forbid, np.int32)
+    forbid = forbid.reshape(Q, forbid.shape[1] if forbid.ndim == 2 else 1)
     n_ports = port_peer.shape[0] if n_ports is None else n_ports
     slots = max_hops + 1
     hops = np.zeros(qidx.shape[0], np.int32)

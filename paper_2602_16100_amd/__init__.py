@@ -3,7 +3,8 @@
 The library (include/pc.h) runs the validator checks of LLM-driven,
 intent-based privacy orchestration (arXiv 2602.16100) as HIP kernels on one
 GPU: node-selector evaluation (pc_eval_selectors; full node affinity with
-OR-ed terms, six operators and label-inventory flags: pc_eval_affinity), flow-table tracing
+OR-ed terms, six operators and label-inventory flags: pc_eval_affinity), path
+synthesis with per-hop rule compilation (pc_synthesize_paths), flow-table tracing
 (pc_trace_flows), masked reachability (pc_masked_reach) and the per-intent
 verdict (pc_report), with waypoint and forbidden-switch constraints
 (pc_trace_flows_watch, pc_masked_reach_via, pc_report_paths).
@@ -33,7 +34,10 @@ TRACE_OUT_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port",
                          ("hops", "u1"), ("state", "u1")])
 SUMMARY_DT = np.dtype([("counts", "<u8", (4, 16)), ("no_path", "<u8", (4,))])
 PATH_EXPECT_DT = np.dtype([("must", "<u4"), ("forbid", "<u4")])
+RULE_DT = np.dtype([("value", "<u4", (4,)), ("mask", "<u4", (4,)), ("priority", "<u2"), ("action", "<u2"),
+                    ("rsv", "<u4")])
 SUMMARY_BYTES = 544
+assert RULE_DT.itemsize == RULE_BYTES
 assert TRACE_OUT_DT.itemsize == 12 and SUMMARY_DT.itemsize == SUMMARY_BYTES and PATH_EXPECT_DT.itemsize == 8
 
 
@@ -77,6 +81,8 @@ def lib():
     L.pc_data_errors.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32), C]
     L.pc_eval_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
     L.pc_eval_affinity.argtypes = [P, P, I32, I32, P, I32, P, I32, P, I64, P, P, P, P]
+    L.pc_synthesize_paths.argtypes = [P, I32, P, P, I64, P, P, I32, P, P, P, P, I32, P, I32, P, P, I32, I32, P,
+                                      P, P, P]
     L.pc_trace_flows.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, P]
     L.pc_masked_reach.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, P]
     L.pc_report.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P]
@@ -92,7 +98,7 @@ def lib():
 
 EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_errors", "pc_profile",
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
-            "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths")
+            "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths")
 
 
 class Context:
@@ -237,6 +243,36 @@ def pc_eval_affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=Non
                                      _ptr(feasible) if feasible.numel() else None,
                                      _ptr(popcnt) if I else None, _ptr(unknown) if I else None, _stream(stream)))
     return feasible, popcnt, unknown
+
+
+def pc_synthesize_paths(V, port_off, port_peer, region, src, target, allowed, via, forbid, key, out_port, prio,
+                        max_hops, weight=None, n_ports=None, hops=None, path=None, rules=None, ctx=None, stream=None):
+    """NEXT-2: per request the walk's hop count [Q] (-1 = none), its switches
+    [Q, max_hops+1] and one 40-byte rule per switch (uint8 [Q, max_hops+1,
+    40]).  via [Q, Kv] / forbid [Q, Kf] int32 (-1 = unused), key [Q, 4]
+    uint32 storage, weight int32 storage of uint32 per port or None."""
+    ctx = ctx or context()
+    Q = int(src.shape[0])
+    Kv = int(via.shape[1]) if via.dim() == 2 else 0
+    Kf = int(forbid.shape[1]) if forbid.dim() == 2 else 0
+    n_ports = int(port_peer.shape[0]) if n_ports is None else int(n_ports)
+    dev = src.device
+    slots = int(max_hops) + 1
+    if hops is None:
+        hops = torch.empty(Q, dtype=torch.int32, device=dev)
+    if path is None:
+        path = torch.empty((Q, slots), dtype=torch.int32, device=dev)
+    if rules is None:
+        rules = torch.empty((Q, slots, 40), dtype=torch.uint8, device=dev)
+    ctx.check(lib().pc_synthesize_paths(ctx.handle, int(V), _ptr(port_off), _ptr(port_peer) if n_ports else None,
+                                        n_ports, None if weight is None else _ptr(weight), _ptr(region), Q,
+                                        _ptr(src) if Q else None, _ptr(target) if Q else None,
+                                        _ptr(allowed) if Q else None, _ptr(via) if Q and Kv else None, Kv,
+                                        _ptr(forbid) if Q and Kf else None, Kf, _ptr(key) if Q else None,
+                                        _ptr(out_port) if Q else None, int(prio), int(max_hops),
+                                        _ptr(hops) if Q else None, _ptr(path) if Q else None,
+                                        _ptr(rules) if Q else None, _stream(stream)))
+    return hops, path, rules
 
 
 def pc_trace_flows(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, n_ports=None, n_rules=None,

@@ -238,6 +238,34 @@ int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, c
                         unknown, static_cast<hipStream_t>(stream));
 }
 
+int pc_synthesize_paths(pc_ctx *ctx, int32_t V, const int32_t *port_off, const int32_t *port_peer,
+                        int64_t n_ports, const uint32_t *weight, const uint8_t *region, int32_t Q,
+                        const int32_t *src, const int32_t *target, const uint32_t *allowed, const int32_t *via,
+                        int32_t Kv, const int32_t *forbid, int32_t Kf, const pc_key *key, const int32_t *out_port,
+                        int32_t prio, int32_t max_hops, int32_t *hops, int32_t *path, pc_rule *rules, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(V >= 0 && Q >= 0 && n_ports >= 0, "pc_synthesize_paths: negative size");
+    PC_REQUIRE(V <= PC_SYNTH_MAX_V, "pc_synthesize_paths: V=%d above %d", V, PC_SYNTH_MAX_V);
+    PC_REQUIRE(n_ports < (int64_t(1) << 31), "pc_synthesize_paths: n_ports too large");
+    PC_REQUIRE(Kv >= 0 && Kv <= 32 && Kf >= 0 && Kf <= 32, "pc_synthesize_paths: Kv=%d / Kf=%d out of [0, 32]",
+               Kv, Kf);
+    PC_REQUIRE(max_hops >= 0 && max_hops <= 255, "pc_synthesize_paths: max_hops=%d out of [0, 255]", max_hops);
+    PC_REQUIRE(prio >= 0 && prio <= 65535, "pc_synthesize_paths: prio=%d out of [0, 65535]", prio);
+    PC_REQUIRE(V == 0 || (port_off && region), "pc_synthesize_paths: null port_off/region");
+    PC_REQUIRE(n_ports == 0 || port_peer, "pc_synthesize_paths: null port_peer");
+    PC_REQUIRE(Q == 0 || (src && target && allowed && key && out_port && hops && path && rules),
+               "pc_synthesize_paths: null request or output array");
+    PC_REQUIRE(Q == 0 || Kv == 0 || via, "pc_synthesize_paths: null via");
+    PC_REQUIRE(Q == 0 || Kf == 0 || forbid, "pc_synthesize_paths: null forbid");
+    if (Q == 0 && V == 0) return PC_OK;
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_synthesize(ctx, V, port_off, port_peer, n_ports, weight, region, Q, src, target, allowed, via, Kv,
+                          forbid, Kf, key, out_port, prio, max_hops, hops, path, rules,
+                          static_cast<hipStream_t>(stream));
+}
+
 int pc_trace_flows(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                    const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
                    const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, pc_trace_out *out,

@@ -110,6 +110,12 @@ int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t 
                   const int32_t *target, const int32_t *via, int32_t Kv, const int32_t *forbid, int32_t Kf,
                   int32_t *dist, hipStream_t stream);
 
+int run_synthesize(pc_ctx *ctx, int32_t V, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
+                   const uint32_t *weight, const uint8_t *region, int32_t Q, const int32_t *src, const int32_t *target,
+                   const uint32_t *allowed, const int32_t *via, int32_t Kv, const int32_t *forbid, int32_t Kf,
+                   const pc_key *key, const int32_t *out_port, int32_t prio, int32_t max_hops, int32_t *hops,
+                   int32_t *path, pc_rule *rules, hipStream_t stream);
+
 int run_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
                int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
                const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,

@@ -29,6 +29,29 @@ def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None):
     return f.cpu().numpy().view(np.uint64), p.cpu().numpy().view(np.uint32), u.cpu().numpy(), flags
 
 
+def _rows2d(a, Q):
+    a = np.ascontiguousarray(a, np.int32)
+    return a.reshape(Q, a.shape[1] if a.ndim == 2 else 1)
+
+
+def synthesize(V, port_off, port_peer, region, src, target, allowed, via, forbid, key, out_port, prio, max_hops,
+               weight=None, n_ports=None):
+    """Hop counts, walks, rules (numpy records) and the data-error word."""
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    Q = src.shape[0]
+    h, p, r = pc.pc_synthesize_paths(V, dev(port_off), dev(port_peer), dev(region), dev(src), dev(target),
+                                     dev(allowed), dev(_rows2d(via, Q)), dev(_rows2d(forbid, Q)),
+                                     dev(np.ascontiguousarray(key, np.uint32)), dev(out_port), prio, max_hops,
+                                     weight=None if weight is None else dev(np.ascontiguousarray(weight, np.uint32)),
+                                     n_ports=n_ports)
+    torch.cuda.synchronize()
+    flags = ctx.data_errors(clear=True)
+    rules = r.cpu().numpy().reshape(-1).view(pc.RULE_DT).reshape(Q, -1) if Q else np.zeros((0, max_hops + 1),
+                                                                                               pc.RULE_DT)
+    return h.cpu().numpy(), p.cpu().numpy(), rules, flags
+
+
 def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, n_ports=None, n_rules=None):
     out = pc.pc_trace_flows(S, dev(port_off), dev(port_peer), dev(jur), dev(rule_off), dev(rules),
                             dev(np.ascontiguousarray(hdr, np.uint32)), dev(ingress), ttl,
