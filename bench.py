@@ -58,14 +58,18 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity"],
+    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity", "synthesis"],
                     help="profiling aid: time one stage only (the JSON line then covers that stage); 'paths' "
                          "times only the pass with waypoint / forbidden-switch constraints, 'affinity' only the "
-                         "node-affinity pass")
+                         "node-affinity pass, 'synthesis' only the path-synthesis pass")
     ap.add_argument("--no-paths", action="store_true",
                     help="skip the second timed pass with waypoint / forbidden-switch constraints")
     ap.add_argument("--no-affinity", action="store_true",
                     help="skip the timed pass of full node affinity over the same cluster")
+    ap.add_argument("--no-synthesis", action="store_true",
+                    help="skip the timed pass of path synthesis over the same topology")
+    ap.add_argument("--synthesis-requests", type=int, default=65536,
+                    help="requests of the path-synthesis pass (the first flows of the workload)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="profiling aid: run a plain device copy of MIB MiB three times (HBM counter calibration)")
     return ap.parse_args()
@@ -303,6 +307,86 @@ def time_affinity(args, wl, pc, ctx, feasible):
     return out
 
 
+def time_synthesis(args, wl, pc, ctx):
+    """Timed pass of path synthesis (pc_synthesize_paths) over the same
+    topology: the first flows' endpoints, allowed jurisdictions, waypoint,
+    forbidden switches, keys and egress ports, with link weights 1..10
+    (weighted search), at most `ttl` links per walk."""
+    import torch
+    import synth
+    dev = "cuda:0"
+    Q = min(args.synthesis_requests, wl["Q"])
+    ex = wl["expect"]
+    has = ex["reach_q"] >= 0
+    out_port = np.zeros(wl["Q"], np.int32)
+    out_port[ex["reach_q"][has]] = ex["dst_port"][has]
+    weight = synth.port_weights(wl.seed, wl["port_peer"].shape[0])
+    arr = dict(src=wl["src"][:Q], target=wl["target"][:Q], allowed=wl["allowed"][:Q], via=wl["via"][:Q],
+               forbid=wl["forbid"][:Q], key=wl["hdr"][:Q], out_port=out_port[:Q])
+    D = {k: pc.to_device(np.ascontiguousarray(v), dev) for k, v in arr.items()}
+    T = {k: pc.to_device(wl[k], dev) for k in ("port_off", "port_peer", "jur")}
+    Wd = pc.to_device(weight, dev)
+    S, ttl, prio = wl["S"], wl["ttl"], 40000
+    slots = ttl + 1
+    hops = torch.empty(Q, dtype=torch.int32, device=dev)
+    path = torch.empty((Q, slots), dtype=torch.int32, device=dev)
+    rules = torch.empty((Q, slots, 40), dtype=torch.uint8, device=dev)
+
+    def step():
+        pc.pc_synthesize_paths(S, T["port_off"], T["port_peer"], T["jur"], D["src"], D["target"], D["allowed"],
+                               D["via"], D["forbid"], D["key"], D["out_port"], prio, ttl, weight=Wd, hops=hops,
+                               path=path, rules=rules, ctx=ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.data_errors(clear=True)
+    ctx.profile(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = ctx.profile_read()
+    ctx.profile(False)
+    flags = ctx.data_errors(clear=True)
+    h = hops.cpu().numpy()
+    legs = int(Q + (arr["via"] >= 0).sum())
+    out = {
+        "requests": Q, "legs": legs, "weights": "uniform 1..10 per port", "max_hops": ttl,
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "paths_per_s": Q * args.steps / elapsed,
+        "per_kernel": {name: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
+                       for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])},
+        "synthesized": int((h >= 0).sum()),
+        "mean_hops": float(h[h >= 0].mean()) if (h >= 0).any() else None,
+        "data_error_flags": flags,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = len(os.sched_getaffinity(0))
+        env_cap = os.environ.get("OMP_NUM_THREADS")
+        if env_cap and env_cap.isdigit():
+            threads = min(threads, int(env_cap))
+        stride = 1024
+        while True:
+            qidx = np.arange(0, Q, stride, dtype=np.int64)
+            t0 = time.perf_counter()
+            oracle.synthesize(S, wl["port_off"], wl["port_peer"], wl["jur"], arr["src"], arr["target"],
+                              arr["allowed"], arr["via"], arr["forbid"], arr["key"], arr["out_port"], prio, ttl,
+                              weight=weight, qidx=qidx, nthreads=threads)
+            t = time.perf_counter() - t0
+            if t >= args.cpu_seconds / 6 or stride == 1:
+                break
+            stride = max(1, stride // 64, int(stride * max(t, 1e-3) / (args.cpu_seconds / 3)))
+        est = t * Q / qidx.shape[0]
+        out["cpu_baseline"] = {"value": Q / est, "unit": "synthesized paths/s (whole-pass estimate)",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"every {stride}th request ({qidx.shape[0]} of {Q}) in {t:.2f} s; whole "
+                                         f"pass estimated at {est:.1f} s"}
+    return out
+
+
 def cpu_baseline_paths(wl, gpu_ms, target_s):
     """The oracle on every k-th flow of the constrained pass (traces with
     watch lists and waypoint reach), scaled to the whole pass."""
@@ -371,6 +455,9 @@ def main():
     only = args.only
     if only == "affinity":
         print(json.dumps({"workload": desc, "affinity": time_affinity(args, wl, pc, ctx, feasible)}), flush=True)
+        return
+    if only == "synthesis":
+        print(json.dumps({"workload": desc, "synthesis": time_synthesis(args, wl, pc, ctx)}), flush=True)
         return
     if only == "paths":
         # the bitsets the verdict reads, computed once outside the timed pass
@@ -474,6 +561,8 @@ def main():
         line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)
     if only == "all" and not args.no_affinity:
         line["affinity"] = time_affinity(args, wl, pc, ctx, feasible)
+    if only == "all" and not args.no_synthesis:
+        line["synthesis"] = time_synthesis(args, wl, pc, ctx)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, pairs, args.cpu_seconds)
     print(json.dumps(line), flush=True)
