@@ -29,7 +29,7 @@ RULE_DT = np.dtype([("value", "<u4", (4,)), ("mask", "<u4", (4,)), ("priority", 
 assert RULE_DT.itemsize == 40
 
 EGRESS, DROP, MISS, TTL = 0, 1, 2, 3
-F_PRED, F_OFFSETS, F_ACTION, F_SWITCH, F_JUR, F_GRAPH, F_INTENT = 1, 2, 4, 8, 16, 32, 64
+F_PRED, F_OFFSETS, F_ACTION, F_SWITCH, F_JUR, F_GRAPH, F_INTENT, F_NODE = 1, 2, 4, 8, 16, 32, 64, 128
 
 _lib = None
 
@@ -55,6 +55,7 @@ def _load():
         C = ctypes.c_int
         _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
         _lib.orc_affinity.argtypes = [P, I64, I64, P, I64, P, I64, P, I64, P, I64, P, P, P, P, C]
+        _lib.orc_update_nodes.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
         _lib.orc_synthesize.argtypes = [I64, P, P, I64, P, P, I64, P, P, P, P, I64, P, I64, P, P, I64, I64, P,
                                         I64, P, P, P, P, C]
         _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, C]
@@ -92,6 +93,24 @@ def selectors(labels, pred_off, preds, n_preds=None, rows=None, nthreads=0):
                       _p(np.ascontiguousarray(preds)), n_preds, I, _p(rows), rows.shape[0],
                       _p(feas), _p(pc), _p(err), nthreads)
     return feas, pc, int(err[0])
+
+
+def update_nodes(labels, pred_off, preds, nodes, feasible, popcnt, n_preds=None, nthreads=0):
+    """Incremental re-evaluation after the labels of `nodes` changed: returns
+    (feasible', popcnt', flags) from copies of the given feasible [I, W] and
+    popcnt [I] (which must hold the evaluation on the previous labels)."""
+    lib = _load()
+    labels = np.ascontiguousarray(labels, np.uint8)
+    N, L = labels.shape
+    I = pred_off.shape[0] - 1
+    n_preds = preds.shape[0] if n_preds is None else n_preds
+    f = np.array(feasible, np.uint64, copy=True, order="C")
+    pc = np.array(popcnt, np.uint32, copy=True)
+    nodes = np.ascontiguousarray(nodes, np.int32)
+    err = np.zeros(1, np.uint32)
+    lib.orc_update_nodes(_p(labels), N, L, _p(np.ascontiguousarray(pred_off, np.int32)), _p(np.ascontiguousarray(preds)),
+                         n_preds, I, _p(nodes), nodes.shape[0], _p(f), _p(pc), _p(err), nthreads)
+    return f, pc, int(err[0])
 
 
 def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None, rows=None, nthreads=0):

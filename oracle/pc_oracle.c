@@ -53,7 +53,7 @@ enum { O_EGRESS = 0, O_DROP = 1, O_MISS = 2, O_TTL = 3 };
  * corresponding input array is malformed, whichever rows, traces or queries
  * are evaluated; the evaluation itself gives malformed items a neutral
  * meaning and never reads out of bounds. */
-enum { F_PRED = 1, F_OFFSETS = 2, F_ACTION = 4, F_SWITCH = 8, F_JUR = 16, F_GRAPH = 32, F_INTENT = 64 };
+enum { F_PRED = 1, F_OFFSETS = 2, F_ACTION = 4, F_SWITCH = 8, F_JUR = 16, F_GRAPH = 32, F_INTENT = 64, F_NODE = 128 };
 
 static void set_flag(uint32_t *err, uint32_t f)
 {
@@ -153,6 +153,60 @@ void orc_selectors(const uint8_t *labels, int64_t N, int64_t L,
             }
         }
         popcnt[r] = count;
+    }
+}
+
+/* ------------------------------------------------------------------ A1 (incremental)
+ * Continuous re-validation after a label change (paper, Abstract: the
+ * validator is meant for continuous cross-layer compliance checking; the
+ * cluster state the placement checks read changes as nodes are relabelled).  The labels of the listed nodes have changed; every other
+ * node's labels are as when feasible / popcnt were computed.  For every
+ * row r and, in list order, every listed node n: the row's bit of n is set
+ * to the selector definition on n's new labels, and popcnt[r] moves by the
+ * change of that bit.  A listed node outside [0, N) is skipped (F_NODE).
+ * Rows and predicates have the meaning and the flags of orc_selectors.
+ */
+static int row_holds(const uint8_t *lab, int64_t L, const o_pred *preds, int64_t b, int64_t e)
+{
+    for (int64_t p = b; p < e; ++p) {
+        const o_pred *q = &preds[p];
+        if (!pred_valid(q, L)) return 0;
+        const unsigned x = lab[q->label];
+        const int present = x != 0xFF;
+        const int in_set = present && ((q->vals[x >> 6] >> (x & 63)) & 1);
+        const int sat = q->op == O_IN ? in_set : q->op == O_NOTIN ? !in_set : present;
+        if (!sat) return 0;
+    }
+    return 1;
+}
+
+void orc_update_nodes(const uint8_t *labels, int64_t N, int64_t L, const int32_t *pred_off, const o_pred *preds,
+                      int64_t n_preds, int64_t I, const int32_t *nodes, int64_t M, uint64_t *feasible,
+                      uint32_t *popcnt, uint32_t *err, int nthreads)
+{
+    const int64_t W = (N + 63) / 64;
+    set_threads(nthreads);
+    for (int64_t i = 0; i < I; ++i) {
+        if (!range_ok(pred_off[i], pred_off[i + 1], n_preds)) { *err |= F_OFFSETS; continue; }
+        for (int64_t p = pred_off[i]; p < pred_off[i + 1]; ++p)
+            if (!pred_valid(&preds[p], L)) *err |= F_PRED;
+    }
+    for (int64_t m = 0; m < M; ++m)
+        if (nodes[m] < 0 || nodes[m] >= N) *err |= F_NODE;
+#pragma omp parallel for schedule(dynamic, 64)
+    for (int64_t r = 0; r < I; ++r) {
+        const int64_t b = pred_off[r], e = pred_off[r + 1];
+        const int ok_row = range_ok(b, e, n_preds);
+        for (int64_t m = 0; m < M; ++m) {
+            const int64_t n = nodes[m];
+            if (n < 0 || n >= N) continue;
+            const int now = ok_row && row_holds(labels + n * L, L, preds, b, e);
+            uint64_t *w = &feasible[r * W + (n >> 6)];
+            const uint64_t bit = (uint64_t)1 << (n & 63);
+            const int was = (*w & bit) != 0;
+            if (now && !was) { *w |= bit; popcnt[r] += 1; }
+            if (!now && was) { *w &= ~bit; popcnt[r] -= 1; }
+        }
     }
 }
 
