@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 4
+#define PC_VERSION 5
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -100,7 +100,8 @@ enum {
     PC_DERR_SWITCH = 8,   /* switch / vertex id out of range (port peer, ingress, src, target) */
     PC_DERR_JUR = 16,     /* jurisdiction / region >= 32 */
     PC_DERR_GRAPH = 32,   /* adjacency entry out of [0, V) */
-    PC_DERR_INTENT = 64   /* intent record out of range or kind not in {1,2,3} */
+    PC_DERR_INTENT = 64,  /* intent record out of range or kind not in {1,2,3} */
+    PC_DERR_NODE = 128    /* a listed node id outside [0, N) (pc_update_nodes) */
 };
 
 /* One selector predicate, 40 bytes.  vals is a 256-bit value set (bit v of
@@ -387,6 +388,29 @@ int pc_report_paths(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t ro
                     const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
                     const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary,
                     void *stream);
+
+/* Most nodes one pc_update_nodes call accepts. */
+#define PC_UPDATE_MAX_NODES 4096
+
+/*
+ * NEXT-4 -- continuous re-validation: incremental re-evaluation of selector
+ * rows after the labels of some nodes changed (paper, Abstract: continuous
+ * cross-layer compliance checking).  labels already holds the new labels;
+ * feasible / popcnt hold pc_eval_selectors' output for labels that differ
+ * from these only at nodes[0..M).  Afterwards they hold pc_eval_selectors'
+ * output for the new labels: for every row and every listed node the row's
+ * bit of the node is set to the selector definition on its new labels, and
+ * the row's popcount moves by the change.  Repeated nodes are allowed.
+ * Arguments and layouts as pc_eval_selectors; nodes: int32 [M] device
+ * array.  Limits: 0 <= M <= PC_UPDATE_MAX_NODES.  Malformed data: a listed
+ * node outside [0, N) is skipped (PC_DERR_NODE); rows and predicates as in
+ * pc_eval_selectors (PC_DERR_OFFSETS, PC_DERR_PRED).  The cost grows with
+ * the number of distinct bitset words the nodes touch per row; a full
+ * pc_eval_selectors is cheaper once that approaches W.
+ */
+int pc_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                    const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,
+                    uint64_t *feasible, uint32_t *popcnt, void *stream);
 
 /* Largest topology pc_synthesize_paths accepts (its per-request search
  * state lives in on-chip memory). */

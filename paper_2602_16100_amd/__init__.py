@@ -4,7 +4,8 @@ The library (include/pc.h) runs the validator checks of LLM-driven,
 intent-based privacy orchestration (arXiv 2602.16100) as HIP kernels on one
 GPU: node-selector evaluation (pc_eval_selectors; full node affinity with
 OR-ed terms, six operators and label-inventory flags: pc_eval_affinity), path
-synthesis with per-hop rule compilation (pc_synthesize_paths), flow-table tracing
+synthesis with per-hop rule compilation (pc_synthesize_paths), incremental
+re-evaluation after node-label changes (pc_update_nodes), flow-table tracing
 (pc_trace_flows), masked reachability (pc_masked_reach) and the per-intent
 verdict (pc_report), with waypoint and forbidden-switch constraints
 (pc_trace_flows_watch, pc_masked_reach_via, pc_report_paths).
@@ -27,7 +28,7 @@ LIB_PATH = os.path.join(_HERE, "_lib", "libpc.so")
 
 PC_OK, PC_EINVAL, PC_ENOMEM, PC_EDEVICE = 0, -1, -2, -3
 PC_EGRESS, PC_DROP, PC_MISS, PC_TTL = 0, 1, 2, 3
-DERR = {"PRED": 1, "OFFSETS": 2, "ACTION": 4, "SWITCH": 8, "JUR": 16, "GRAPH": 32, "INTENT": 64}
+DERR = {"PRED": 1, "OFFSETS": 2, "ACTION": 4, "SWITCH": 8, "JUR": 16, "GRAPH": 32, "INTENT": 64, "NODE": 128}
 
 PRED_BYTES, RULE_BYTES, KEY_BYTES, INTENT_BYTES, EXPECT_BYTES = 40, 40, 16, 32, 12
 TRACE_OUT_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port", "<u2"),
@@ -81,6 +82,7 @@ def lib():
     L.pc_data_errors.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32), C]
     L.pc_eval_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
     L.pc_eval_affinity.argtypes = [P, P, I32, I32, P, I32, P, I32, P, I64, P, P, P, P]
+    L.pc_update_nodes.argtypes = [P, P, I32, I32, P, P, I64, I32, P, I32, P, P, P]
     L.pc_synthesize_paths.argtypes = [P, I32, P, P, I64, P, P, I32, P, P, P, P, I32, P, I32, P, P, I32, I32, P,
                                       P, P, P]
     L.pc_trace_flows.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, P]
@@ -98,7 +100,8 @@ def lib():
 
 EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_errors", "pc_profile",
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
-            "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths")
+            "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths",
+            "pc_update_nodes")
 
 
 class Context:
@@ -243,6 +246,22 @@ def pc_eval_affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=Non
                                      _ptr(feasible) if feasible.numel() else None,
                                      _ptr(popcnt) if I else None, _ptr(unknown) if I else None, _stream(stream)))
     return feasible, popcnt, unknown
+
+
+def pc_update_nodes(labels, pred_off, preds, nodes, feasible, popcnt, n_preds=None, ctx=None, stream=None):
+    """NEXT-4: re-evaluate every row's bits of the listed nodes (their labels
+    changed) in place in feasible / popcnt, which must hold the evaluation
+    of the previous labels."""
+    ctx = ctx or context()
+    N, L = (int(labels.shape[0]), int(labels.shape[1])) if labels.dim() == 2 else (0, 0)
+    I = int(pred_off.shape[0]) - 1
+    M = int(nodes.shape[0])
+    n_preds = int(preds.shape[0]) if n_preds is None else int(n_preds)
+    ctx.check(lib().pc_update_nodes(ctx.handle, _ptr(labels) if labels.numel() else None, N, L, _ptr(pred_off),
+                                    _ptr(preds) if preds.numel() else None, n_preds, I, _ptr(nodes) if M else None, M,
+                                    _ptr(feasible) if feasible.numel() else None, _ptr(popcnt) if I else None,
+                                    _stream(stream)))
+    return feasible, popcnt
 
 
 def pc_synthesize_paths(V, port_off, port_peer, region, src, target, allowed, via, forbid, key, out_port, prio,

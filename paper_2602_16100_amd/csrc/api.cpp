@@ -238,6 +238,27 @@ int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, c
                         unknown, static_cast<hipStream_t>(stream));
 }
 
+int pc_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                    const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,
+                    uint64_t *feasible, uint32_t *popcnt, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(N >= 0 && I >= 0 && n_preds >= 0 && M >= 0, "pc_update_nodes: negative size");
+    PC_REQUIRE(M <= PC_UPDATE_MAX_NODES, "pc_update_nodes: M=%d above %d", M, PC_UPDATE_MAX_NODES);
+    PC_REQUIRE(L >= 0 && L <= 65535, "pc_update_nodes: L=%d out of [0, 65535]", L);
+    PC_REQUIRE(L > 0 || n_preds == 0, "pc_update_nodes: L=0 with predicates");
+    PC_REQUIRE(I == 0 || (pred_off && popcnt), "pc_update_nodes: null pred_off/popcnt");
+    PC_REQUIRE(n_preds == 0 || preds, "pc_update_nodes: null preds");
+    PC_REQUIRE(M == 0 || nodes, "pc_update_nodes: null nodes");
+    PC_REQUIRE(N == 0 || L == 0 || labels, "pc_update_nodes: null labels");
+    PC_REQUIRE(I == 0 || N == 0 || feasible, "pc_update_nodes: null feasible");
+    if (I == 0 && M == 0) return PC_OK;
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_update_nodes(ctx, labels, N, L, pred_off, preds, n_preds, I, nodes, M, feasible, popcnt,
+                            static_cast<hipStream_t>(stream));
+}
+
 int pc_synthesize_paths(pc_ctx *ctx, int32_t V, const int32_t *port_off, const int32_t *port_peer,
                         int64_t n_ports, const uint32_t *weight, const uint8_t *region, int32_t Q,
                         const int32_t *src, const int32_t *target, const uint32_t *allowed, const int32_t *via,

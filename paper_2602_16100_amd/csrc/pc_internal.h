@@ -110,6 +110,10 @@ int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t 
                   const int32_t *target, const int32_t *via, int32_t Kv, const int32_t *forbid, int32_t Kf,
                   int32_t *dist, hipStream_t stream);
 
+int run_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                     const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,
+                     uint64_t *feasible, uint32_t *popcnt, hipStream_t stream);
+
 int run_synthesize(pc_ctx *ctx, int32_t V, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                    const uint32_t *weight, const uint8_t *region, int32_t Q, const int32_t *src, const int32_t *target,
                    const uint32_t *allowed, const int32_t *via, int32_t Kv, const int32_t *forbid, int32_t Kf,

@@ -1,0 +1,258 @@
+// NEXT-4 -- incremental re-validation of selector rows after node-label
+// changes (paper, Abstract: the validator is meant for continuous
+// cross-layer compliance checking).  Instead of rebuilding every row's
+// bitset, only the listed nodes' bits are re-evaluated.
+//
+// Design (gfx950):
+//   1. validate : PRED / OFFSETS over the rows (as pc_eval_selectors) and
+//                 NODE over the list.
+//   2. prep     : one workgroup sorts the in-range listed nodes (bitonic, in
+//                 LDS), drops repeats, and gathers their label rows into a
+//                 compact block.  A node's new bit depends only on its new
+//                 labels, so a repeated node changes nothing more.
+//   3. rows     : one wavefront per row; the workgroup stages the label rows
+//                 of 64 nodes at a time in LDS.  Lane m evaluates the row's
+//                 predicates (scalar loads, uniform) on node m; the new bits
+//                 are OR-ed per 64-bit bitset word by a segmented shuffle
+//                 reduction over the sorted lanes, and the first lane of each
+//                 word updates it with one atomic clear (which returns the
+//                 old word) and one atomic set, and adds the popcount change.
+#include <climits>
+
+#include "pc_internal.h"
+
+namespace {
+
+constexpr int kUpdMax = PC_UPDATE_MAX_NODES;  // listed nodes per call
+constexpr int kPrepThreads = 1024;
+constexpr int kRowThreads = 256;             // 4 wavefronts, one row each
+
+__device__ __forceinline__ bool upd_pred_valid(const pc_pred &q, int32_t L)
+{
+    return static_cast<int32_t>(q.label) < L && q.op <= PC_OP_EXISTS && q.rsv0 == 0 && q.rsv1 == 0 &&
+           (q.op == PC_OP_EXISTS || (q.vals[3] >> 63) == 0);
+}
+
+__global__ __launch_bounds__(256) void k_upd_validate(const int32_t *__restrict__ pred_off,
+                                                      const pc_pred *__restrict__ preds, int64_t n_preds, int32_t I,
+                                                      int32_t L, const int32_t *__restrict__ nodes, int32_t M, int32_t N,
+                                                      uint32_t *__restrict__ d_err)
+{
+    uint32_t errs = 0;
+    const int64_t tot = I > M ? I : M;
+    for (int64_t x = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; x < tot;
+         x += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        if (x < I) {
+            const int64_t b = pred_off[x], e = pred_off[x + 1];
+            if (!pc_range_ok(b, e, n_preds)) {
+                errs |= PC_DERR_OFFSETS;
+            } else {
+                for (int64_t p = b; p < e; ++p)
+                    if (!upd_pred_valid(preds[p], L)) {
+                        errs |= PC_DERR_PRED;
+                        break;
+                    }
+            }
+        }
+        if (x < M && (nodes[x] < 0 || nodes[x] >= N)) errs |= PC_DERR_NODE;
+    }
+    if (errs) atomicOr(d_err, errs);
+}
+
+// Sorted distinct in-range nodes -> uniq[0..*d_mu), their label rows ->
+// ulab[k * L ...].
+__global__ __launch_bounds__(kPrepThreads) void k_upd_prep(const int32_t *__restrict__ nodes, int32_t M, int32_t N,
+                                                           const uint8_t *__restrict__ labels, int32_t L,
+                                                           int32_t *__restrict__ uniq, uint8_t *__restrict__ ulab,
+                                                           int32_t *__restrict__ d_mu)
+{
+    __shared__ int32_t key[kUpdMax];
+    __shared__ int32_t comp[kUpdMax];
+    __shared__ int32_t wsum[kPrepThreads / 64];
+    const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
+    for (int i = tid; i < kUpdMax; i += kPrepThreads) {
+        const int32_t n = i < M ? nodes[i] : -1;
+        key[i] = (n >= 0 && n < N) ? n : INT32_MAX;
+    }
+    __syncthreads();
+    // bitonic sort, ascending
+    for (int k = 2; k <= kUpdMax; k <<= 1) {
+        for (int j = k >> 1; j > 0; j >>= 1) {
+            for (int i = tid; i < kUpdMax; i += kPrepThreads) {
+                const int l = i ^ j;
+                if (l > i) {
+                    const int32_t a = key[i], b = key[l];
+                    const bool up = (i & k) == 0;
+                    if ((a > b) == up) {
+                        key[i] = b;
+                        key[l] = a;
+                    }
+                }
+            }
+            __syncthreads();
+        }
+    }
+    // keep the first of each run: positions by an exclusive scan, 4 entries per thread
+    constexpr int kPer = kUpdMax / kPrepThreads;
+    int flag[kPer], cnt = 0;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k) {
+        const int i = tid * kPer + k;
+        flag[k] = key[i] != INT32_MAX && (i == 0 || key[i - 1] != key[i]);
+        cnt += flag[k];
+    }
+    int x = cnt;
+#pragma unroll
+    for (int off = 1; off < 64; off <<= 1) {
+        const int y = __shfl_up(x, off, 64);
+        if (lane >= off) x += y;
+    }
+    if (lane == 63) wsum[wid] = x;
+    __syncthreads();
+    int base = 0;
+    for (int w = 0; w < wid; ++w) base += wsum[w];
+    int pos = base + x - cnt;
+#pragma unroll
+    for (int k = 0; k < kPer; ++k)
+        if (flag[k]) {
+            comp[pos] = key[tid * kPer + k];
+            uniq[pos] = key[tid * kPer + k];
+            ++pos;
+        }
+    if (tid == kPrepThreads - 1) *d_mu = pos;
+    __syncthreads();
+    int mu = 0;
+    for (int w = 0; w < kPrepThreads / 64; ++w) mu += wsum[w];
+    for (int64_t i = tid; i < static_cast<int64_t>(mu) * L; i += kPrepThreads) {
+        const int64_t k = i / L, l = i % L;
+        ulab[i] = labels[static_cast<int64_t>(comp[k]) * L + l];
+    }
+}
+
+// One wavefront per row (see the file header).
+__global__ __launch_bounds__(kRowThreads) void k_upd_rows(const int32_t *__restrict__ pred_off,
+                                                          const pc_pred *__restrict__ preds, int64_t n_preds,
+                                                          int32_t I, int32_t L, const int32_t *__restrict__ uniq,
+                                                          const uint8_t *__restrict__ ulab,
+                                                          const int32_t *__restrict__ d_mu, int32_t W,
+                                                          uint64_t *__restrict__ feasible,
+                                                          uint32_t *__restrict__ popcnt)
+{
+    extern __shared__ uint8_t lab_lds[];  // 64 nodes x stride bytes
+    const int32_t stride = (L + 4) & ~3;  // padded row: consecutive lanes start in different banks
+    const int tid = threadIdx.x, lane = tid & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int32_t r = blockIdx.x * (kRowThreads / 64) + wave;
+    const int32_t mu = *d_mu;
+    const bool live = r < I;
+    int64_t b = 0, e = 0;
+    bool row_ok = false;
+    if (live) {
+        b = pred_off[r];
+        e = pred_off[r + 1];
+        row_ok = pc_range_ok(b, e, n_preds);
+    }
+    uint32_t delta = 0;
+    for (int32_t k0 = 0; k0 < mu; k0 += 64) {
+        const int32_t nb = min(64, mu - k0);
+        __syncthreads();  // the previous batch's labels are no longer read
+        for (int32_t i = tid; i < nb * L; i += kRowThreads)
+            lab_lds[(i / L) * stride + (i % L)] = ulab[static_cast<int64_t>(k0) * L + i];
+        __syncthreads();
+        if (!live) continue;
+        const bool act = lane < nb;
+        const int32_t n = act ? uniq[k0 + lane] : INT32_MAX;
+        bool ok = act && row_ok;
+        if (row_ok) {
+            for (int64_t p = b; p < e; ++p) {
+                const pc_pred q = preds[p];
+                if (!upd_pred_valid(q, L)) {
+                    ok = false;
+                    break;  // uniform: every lane sees the same predicate
+                }
+                const uint32_t x = act ? lab_lds[lane * stride + q.label] : 0xFFu;
+                const bool present = x != PC_LABEL_ABSENT;
+                const uint32_t k = x >> 6;  // the value-set word, chosen without a per-lane array index
+                const uint64_t vw = k == 0 ? q.vals[0] : k == 1 ? q.vals[1] : k == 2 ? q.vals[2] : q.vals[3];
+                const bool in_set = present && ((vw >> (x & 63)) & 1);
+                const bool sat = q.op == PC_OP_IN ? in_set : q.op == PC_OP_NOTIN ? !in_set : present;
+                ok = ok && sat;
+            }
+        }
+        // segmented OR of the new bits over lanes of the same word (sorted nodes: words are contiguous)
+        const int32_t w = act ? (n >> 6) : -1 - lane;
+        uint64_t set = ok ? (1ull << (n & 63)) : 0ull;
+        uint64_t mask = act ? (1ull << (n & 63)) : 0ull;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const uint64_t s2 = __shfl_down(set, off, 64);
+            const uint64_t m2 = __shfl_down(mask, off, 64);
+            const int32_t w2 = __shfl_down(w, off, 64);
+            if (lane + off < 64 && w2 == w) {
+                set |= s2;
+                mask |= m2;
+            }
+        }
+        const int32_t wprev = __shfl_up(w, 1, 64);
+        const bool head = act && (lane == 0 || wprev != w);
+        if (head) {
+            // a word can straddle two batches: the update goes through L2
+            // atomics (clear, returning the old word, then set), so the next
+            // batch's read of the same word sees this one's write
+            unsigned long long *dst =
+                reinterpret_cast<unsigned long long *>(feasible + static_cast<int64_t>(r) * W + w);
+            const uint64_t old = atomicAnd(dst, ~(mask & ~set));
+            if (set) atomicOr(dst, set);
+            const uint64_t nw = (old & ~mask) | set;
+            delta += static_cast<uint32_t>(__popcll(nw)) - static_cast<uint32_t>(__popcll(old));
+        }
+    }
+    if (live) {
+        const uint32_t d = pc_wave_sum_u32(delta);
+        if (lane == 0 && d) popcnt[r] += d;
+    }
+}
+
+}  // namespace
+
+int run_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                     const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,
+                     uint64_t *feasible, uint32_t *popcnt, hipStream_t stream)
+{
+    int32_t *uniq, *d_mu;
+    uint8_t *ulab;
+    auto carve = [&](Carver &cv) {
+        uniq = cv.take<int32_t>(kUpdMax);
+        d_mu = cv.take<int32_t>(1);
+        ulab = cv.take<uint8_t>(static_cast<size_t>(kUpdMax) * (L > 0 ? L : 1));
+    };
+    Carver dry{nullptr, 0};
+    carve(dry);
+    int rc = pc_ensure_arena(ctx, dry.off);
+    if (rc) return rc;
+    Carver real{ctx->arena, 0};
+    carve(real);
+    const int64_t tot = std::max<int64_t>(I, M);
+    if (tot > 0) {
+        const unsigned g = static_cast<unsigned>(std::min<int64_t>((tot + 255) / 256, 8192));
+        PC_TIMED(ctx, "k_upd_validate", stream,
+                 hipLaunchKernelGGL(k_upd_validate, dim3(g), dim3(256), 0, stream, pred_off, preds, n_preds, I, L,
+                                    nodes, M, N, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    if (I == 0 || M == 0 || N == 0) return PC_OK;
+    PC_TIMED(ctx, "k_upd_prep", stream,
+             hipLaunchKernelGGL(k_upd_prep, dim3(1), dim3(kPrepThreads), 0, stream, nodes, M, N, labels, L, uniq,
+                                ulab, d_mu));
+    PC_LAUNCH_CHECK(ctx);
+    const int32_t W = (N + 63) / 64;
+    const size_t lds = static_cast<size_t>(64) * ((L + 4) & ~3);
+    PC_HIP(ctx, hipFuncSetAttribute(reinterpret_cast<const void *>(k_upd_rows),
+                                    hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
+    const unsigned g = static_cast<unsigned>((I + 3) / 4);
+    PC_TIMED(ctx, "k_upd_rows", stream,
+             hipLaunchKernelGGL(k_upd_rows, dim3(g), dim3(kRowThreads), lds, stream, pred_off, preds, n_preds, I, L,
+                                uniq, ulab, d_mu, W, feasible, popcnt));
+    PC_LAUNCH_CHECK(ctx);
+    return PC_OK;
+}
