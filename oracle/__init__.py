@@ -56,6 +56,7 @@ def _load():
         _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
         _lib.orc_affinity.argtypes = [P, I64, I64, P, I64, P, I64, P, I64, P, I64, P, P, P, P, C]
         _lib.orc_update_nodes.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
+        _lib.orc_probes.argtypes = [P, I64, I64, P, P, I64, I64, P, P, I64, P, P]
         _lib.orc_synthesize.argtypes = [I64, P, P, I64, P, P, I64, P, P, P, P, I64, P, I64, P, P, I64, I64, P,
                                         I64, P, P, P, P, C]
         _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, C]
@@ -111,6 +112,23 @@ def update_nodes(labels, pred_off, preds, nodes, feasible, popcnt, n_preds=None,
     lib.orc_update_nodes(_p(labels), N, L, _p(np.ascontiguousarray(pred_off, np.int32)), _p(np.ascontiguousarray(preds)),
                          n_preds, I, _p(nodes), nodes.shape[0], _p(f), _p(pc), _p(err), nthreads)
     return f, pc, int(err[0])
+
+
+def probes(labels, pred_off, preds, probe_row, probe_node, n_preds=None):
+    """bit[k] = node probe_node[k] satisfies selector row probe_row[k]
+    (0 when either is out of range).  Returns (bits u8, flags)."""
+    lib = _load()
+    labels = np.ascontiguousarray(labels, np.uint8)
+    N, L = labels.shape
+    I = pred_off.shape[0] - 1
+    n_preds = preds.shape[0] if n_preds is None else n_preds
+    pr = np.ascontiguousarray(probe_row, np.int32)
+    pn = np.ascontiguousarray(probe_node, np.int32)
+    bits = np.zeros(pr.shape[0], np.uint8)
+    err = np.zeros(1, np.uint32)
+    lib.orc_probes(_p(labels), N, L, _p(np.ascontiguousarray(pred_off, np.int32)), _p(np.ascontiguousarray(preds)),
+                   n_preds, I, _p(pr), _p(pn), pr.shape[0], _p(bits), _p(err))
+    return bits, int(err[0])
 
 
 def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None, rows=None, nthreads=0):

@@ -210,6 +210,30 @@ void orc_update_nodes(const uint8_t *labels, int64_t N, int64_t L, const int32_t
     }
 }
 
+/* ------------------------------------------------------------------ A1 (probes)
+ * Membership queries for verdict-only runs: bit[k] = whether node
+ * probe_node[k] satisfies selector row probe_row[k] (the selector
+ * definition above); 0 and F_NODE when the row or the node is out of range.
+ * Rows and predicates have the meaning and the flags of orc_selectors.
+ */
+void orc_probes(const uint8_t *labels, int64_t N, int64_t L, const int32_t *pred_off, const o_pred *preds,
+                int64_t n_preds, int64_t I, const int32_t *probe_row, const int32_t *probe_node, int64_t P,
+                uint8_t *bit, uint32_t *err)
+{
+    for (int64_t i = 0; i < I; ++i) {
+        if (!range_ok(pred_off[i], pred_off[i + 1], n_preds)) { *err |= F_OFFSETS; continue; }
+        for (int64_t p = pred_off[i]; p < pred_off[i + 1]; ++p)
+            if (!pred_valid(&preds[p], L)) *err |= F_PRED;
+    }
+    for (int64_t k = 0; k < P; ++k) {
+        const int64_t r = probe_row[k], n = probe_node[k];
+        bit[k] = 0;
+        if (r < 0 || r >= I || n < 0 || n >= N) { *err |= F_NODE; continue; }
+        const int64_t b = pred_off[r], e = pred_off[r + 1];
+        bit[k] = (uint8_t)(range_ok(b, e, n_preds) && row_holds(labels + n * L, L, preds, b, e));
+    }
+}
+
 /* ------------------------------------------------------------------ A1 (affinity)
  * Required node affinity (paper: placement directives become Kubernetes
  * node selection criteria and affinity rules, Sec. "Intent Translation",

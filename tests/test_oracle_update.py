@@ -66,3 +66,21 @@ def test_update_malformed_rows(orc):
     ff, pf, ef = orc.selectors(new, off, preds)
     assert e1 == ef == e0 == 3
     assert np.array_equal(f1, ff) and np.array_equal(p1, pf)
+
+
+def test_probes_are_bits_of_the_bitset(orc):
+    """Membership probes equal the bits of the (separately pinned) full
+    bitset; out-of-range rows or nodes answer 0 and raise NODE."""
+    wl = synth.selector_workload(11, 2000 + 9, 8, 400, card_choices=(2, 5, 30), absent_p=0.1)
+    labels, off, preds = wl["labels"], wl["pred_off"], wl["preds"]
+    f, _, _ = orc.selectors(labels, off, preds)
+    rng = np.random.default_rng(5)
+    rows = rng.integers(0, 400, size=3000).astype(np.int32)
+    nodes = rng.integers(0, 2009, size=3000).astype(np.int32)
+    bits, err = orc.probes(labels, off, preds, rows, nodes)
+    want = (f[rows, nodes >> 6] >> (nodes & 63).astype(np.uint64)) & np.uint64(1)
+    assert err == 0 and np.array_equal(bits, want.astype(np.uint8))
+    assert 0 < bits.sum() < 3000
+    bits, err = orc.probes(labels, off, preds, np.array([0, -1, 400, 3], np.int32),
+                           np.array([-2, 0, 0, 2009], np.int32))
+    assert err == 128 and bits.tolist() == [0, 0, 0, 0]
