@@ -59,7 +59,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 5
+#define PC_VERSION 6
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -388,6 +388,34 @@ int pc_report_paths(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t ro
                     const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
                     const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary,
                     void *stream);
+
+/*
+ * NEXT-4 -- verdict-only runs.  The verdict (pc_report) reads each selector
+ * row's popcount and, for hybrid intents, two placed endpoints' bits (paper:
+ * an intent passes only if all of its checks pass; hybrid endpoints are the
+ * nodes the pods were placed on).  These three calls give it both without
+ * materialising the I x ceil(N/64) bitset.
+ *
+ * pc_eval_selectors_count: popcnt exactly as pc_eval_selectors, no bitset.
+ * pc_probe_selectors: bit[k] = 1 iff node probe_node[k] satisfies selector
+ *   row probe_row[k]; 0 when the row is outside [0, I) or the node outside
+ *   [0, N) (PC_DERR_NODE).  probe_row, probe_node: int32 [P]; bit: uint8 [P].
+ * pc_report_counts: pc_report with each hybrid intent i's endpoint bits read
+ *   from ends[2i] (src_node) and ends[2i + 1] (dst_node), bit 0 of each,
+ *   instead of bitset words; ends: uint8 [2I] (entries of non-hybrid intents
+ *   are not read).
+ * Arguments, layouts, limits and malformed-data handling otherwise as
+ * pc_eval_selectors / pc_report.
+ */
+int pc_eval_selectors_count(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                            const pc_pred *preds, int64_t n_preds, int32_t I, uint32_t *popcnt, void *stream);
+int pc_probe_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                       const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *probe_row,
+                       const int32_t *probe_node, int32_t P, uint8_t *bit, void *stream);
+int pc_report_counts(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint32_t *popcnt,
+                     int32_t N, const uint8_t *ends, const pc_trace_out *traces, int32_t T,
+                     const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass, uint8_t *reason,
+                     pc_summary *summary, void *stream);
 
 /* Most nodes one pc_update_nodes call accepts. */
 #define PC_UPDATE_MAX_NODES 4096

@@ -5,7 +5,8 @@ intent-based privacy orchestration (arXiv 2602.16100) as HIP kernels on one
 GPU: node-selector evaluation (pc_eval_selectors; full node affinity with
 OR-ed terms, six operators and label-inventory flags: pc_eval_affinity), path
 synthesis with per-hop rule compilation (pc_synthesize_paths), incremental
-re-evaluation after node-label changes (pc_update_nodes), flow-table tracing
+re-evaluation after node-label changes and verdict-only runs (pc_update_nodes,
+pc_eval_selectors_count, pc_probe_selectors, pc_report_counts), flow-table tracing
 (pc_trace_flows), masked reachability (pc_masked_reach) and the per-intent
 verdict (pc_report), with waypoint and forbidden-switch constraints
 (pc_trace_flows_watch, pc_masked_reach_via, pc_report_paths).
@@ -83,6 +84,9 @@ def lib():
     L.pc_eval_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
     L.pc_eval_affinity.argtypes = [P, P, I32, I32, P, I32, P, I32, P, I64, P, P, P, P]
     L.pc_update_nodes.argtypes = [P, P, I32, I32, P, P, I64, I32, P, I32, P, P, P]
+    L.pc_eval_selectors_count.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P]
+    L.pc_probe_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, I32, P, P]
+    L.pc_report_counts.argtypes = [P, I32, P, I32, P, I32, P, P, I32, P, P, I32, P, P, P, P]
     L.pc_synthesize_paths.argtypes = [P, I32, P, P, I64, P, P, I32, P, P, P, P, I32, P, I32, P, P, I32, I32, P,
                                       P, P, P]
     L.pc_trace_flows.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, P]
@@ -101,7 +105,7 @@ def lib():
 EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_errors", "pc_profile",
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
             "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths",
-            "pc_update_nodes")
+            "pc_update_nodes", "pc_eval_selectors_count", "pc_probe_selectors", "pc_report_counts")
 
 
 class Context:
@@ -246,6 +250,61 @@ def pc_eval_affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=Non
                                      _ptr(feasible) if feasible.numel() else None,
                                      _ptr(popcnt) if I else None, _ptr(unknown) if I else None, _stream(stream)))
     return feasible, popcnt, unknown
+
+
+def pc_eval_selectors_count(labels, pred_off, preds, n_preds=None, popcnt=None, ctx=None, stream=None):
+    """NEXT-4: popcount [I] of every selector row, no bitset written."""
+    ctx = ctx or context()
+    N, L = (int(labels.shape[0]), int(labels.shape[1])) if labels.dim() == 2 else (0, 0)
+    I = int(pred_off.shape[0]) - 1
+    n_preds = int(preds.shape[0]) if n_preds is None else int(n_preds)
+    if popcnt is None:
+        popcnt = torch.empty(I, dtype=torch.int32, device=pred_off.device)
+    ctx.check(lib().pc_eval_selectors_count(ctx.handle, _ptr(labels) if labels.numel() else None, N, L,
+                                            _ptr(pred_off), _ptr(preds) if preds.numel() else None, n_preds, I,
+                                            _ptr(popcnt) if I else None, _stream(stream)))
+    return popcnt
+
+
+def pc_probe_selectors(labels, pred_off, preds, probe_row, probe_node, n_preds=None, bits=None, ctx=None,
+                       stream=None):
+    """NEXT-4: uint8 [P], 1 iff node probe_node[k] satisfies row probe_row[k]."""
+    ctx = ctx or context()
+    N, L = (int(labels.shape[0]), int(labels.shape[1])) if labels.dim() == 2 else (0, 0)
+    I = int(pred_off.shape[0]) - 1
+    P = int(probe_row.shape[0])
+    n_preds = int(preds.shape[0]) if n_preds is None else int(n_preds)
+    if bits is None:
+        bits = torch.empty(P, dtype=torch.uint8, device=pred_off.device)
+    ctx.check(lib().pc_probe_selectors(ctx.handle, _ptr(labels) if labels.numel() else None, N, L, _ptr(pred_off),
+                                       _ptr(preds) if preds.numel() else None, n_preds, I,
+                                       _ptr(probe_row) if P else None, _ptr(probe_node) if P else None, P,
+                                       _ptr(bits) if P else None, _stream(stream)))
+    return bits
+
+
+def pc_report_counts(intents, popcnt, N, ends, traces, expect, reach, pass_=None, reason=None, summary=None,
+                     ctx=None, stream=None):
+    """NEXT-4: pc_report from popcounts and per-intent endpoint bits (uint8
+    [2I]) instead of the bitset."""
+    ctx = ctx or context()
+    I = int(intents.shape[0])
+    rows = int(popcnt.shape[0])
+    T = int(traces.shape[0])
+    Q = int(reach.shape[0])
+    dev = intents.device
+    if pass_ is None:
+        pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
+    if reason is None:
+        reason = torch.empty(I, dtype=torch.uint8, device=dev)
+    if summary is None:
+        summary = torch.empty(SUMMARY_BYTES, dtype=torch.uint8, device=dev)
+    ctx.check(lib().pc_report_counts(ctx.handle, I, _ptr(intents) if I else None, rows, _ptr(popcnt) if rows else None,
+                                     int(N), _ptr(ends) if I else None, _ptr(traces) if T else None, T,
+                                     _ptr(expect) if I else None, _ptr(reach) if Q else None, Q,
+                                     _ptr(pass_) if I else None, _ptr(reason) if I else None, _ptr(summary),
+                                     _stream(stream)))
+    return pass_, reason, summary
 
 
 def pc_update_nodes(labels, pred_off, preds, nodes, feasible, popcnt, n_preds=None, ctx=None, stream=None):

@@ -238,6 +238,42 @@ int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, c
                         unknown, static_cast<hipStream_t>(stream));
 }
 
+int pc_eval_selectors_count(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                            const pc_pred *preds, int64_t n_preds, int32_t I, uint32_t *popcnt, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(N >= 0 && I >= 0 && n_preds >= 0, "pc_eval_selectors_count: negative size");
+    PC_REQUIRE(L >= 0 && L <= 65535, "pc_eval_selectors_count: L=%d out of [0, 65535]", L);
+    PC_REQUIRE(L > 0 || n_preds == 0, "pc_eval_selectors_count: L=0 with predicates");
+    PC_REQUIRE(I == 0 || (pred_off && popcnt), "pc_eval_selectors_count: null pred_off/popcnt");
+    PC_REQUIRE(n_preds == 0 || preds, "pc_eval_selectors_count: null preds");
+    PC_REQUIRE(N == 0 || L == 0 || labels, "pc_eval_selectors_count: null labels");
+    if (I == 0) return PC_OK;
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_selectors(ctx, labels, N, L, pred_off, preds, n_preds, I, nullptr, popcnt,
+                         static_cast<hipStream_t>(stream));
+}
+
+int pc_probe_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                       const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *probe_row,
+                       const int32_t *probe_node, int32_t P, uint8_t *bit, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(N >= 0 && I >= 0 && n_preds >= 0 && P >= 0, "pc_probe_selectors: negative size");
+    PC_REQUIRE(L >= 0 && L <= 65535, "pc_probe_selectors: L=%d out of [0, 65535]", L);
+    PC_REQUIRE(L > 0 || n_preds == 0, "pc_probe_selectors: L=0 with predicates");
+    PC_REQUIRE(I == 0 || pred_off, "pc_probe_selectors: null pred_off");
+    PC_REQUIRE(n_preds == 0 || preds, "pc_probe_selectors: null preds");
+    PC_REQUIRE(N == 0 || L == 0 || labels, "pc_probe_selectors: null labels");
+    PC_REQUIRE(P == 0 || (probe_row && probe_node && bit), "pc_probe_selectors: null probe arrays");
+    if (I == 0 && P == 0) return PC_OK;
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_probes(ctx, labels, N, L, pred_off, preds, n_preds, I, probe_row, probe_node, P, bit,
+                      static_cast<hipStream_t>(stream));
+}
+
 int pc_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                     const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,
                     uint64_t *feasible, uint32_t *popcnt, void *stream)
@@ -381,8 +417,26 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
     PC_REQUIRE(T == 0 || traces, "pc_report: null traces");
     PC_REQUIRE(Q == 0 || reach, "pc_report: null reach");
     PC_HIP(ctx, hipSetDevice(ctx->device));
-    return run_report(ctx, I, intents, rows, feasible, W, popcnt, N, traces, T, expect, reach, Q, nullptr, nullptr,
-                      pass, reason, summary, static_cast<hipStream_t>(stream));
+    return run_report(ctx, I, intents, rows, feasible, W, nullptr, popcnt, N, traces, T, expect, reach, Q, nullptr,
+                      nullptr, pass, reason, summary, static_cast<hipStream_t>(stream));
+}
+
+int pc_report_counts(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint32_t *popcnt,
+                     int32_t N, const uint8_t *ends, const pc_trace_out *traces, int32_t T,
+                     const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass, uint8_t *reason,
+                     pc_summary *summary, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(I >= 0 && rows >= 0 && N >= 0 && T >= 0 && Q >= 0, "pc_report_counts: negative size");
+    PC_REQUIRE(summary, "pc_report_counts: null summary");
+    PC_REQUIRE(I == 0 || (intents && expect && pass && reason && ends), "pc_report_counts: null intent arrays");
+    PC_REQUIRE(rows == 0 || popcnt, "pc_report_counts: null popcnt");
+    PC_REQUIRE(T == 0 || traces, "pc_report_counts: null traces");
+    PC_REQUIRE(Q == 0 || reach, "pc_report_counts: null reach");
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_report(ctx, I, intents, rows, nullptr, 0, ends, popcnt, N, traces, T, expect, reach, Q, nullptr,
+                      nullptr, pass, reason, summary, static_cast<hipStream_t>(stream));
 }
 
 int pc_report_paths(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
@@ -401,8 +455,8 @@ int pc_report_paths(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t ro
     PC_REQUIRE(T == 0 || (traces && visit), "pc_report_paths: null traces/visit");
     PC_REQUIRE(Q == 0 || reach, "pc_report_paths: null reach");
     PC_HIP(ctx, hipSetDevice(ctx->device));
-    return run_report(ctx, I, intents, rows, feasible, W, popcnt, N, traces, T, expect, reach, Q, visit, pexp, pass,
-                      reason, summary, static_cast<hipStream_t>(stream));
+    return run_report(ctx, I, intents, rows, feasible, W, nullptr, popcnt, N, traces, T, expect, reach, Q, visit, pexp,
+                      pass, reason, summary, static_cast<hipStream_t>(stream));
 }
 
 }  // extern "C"

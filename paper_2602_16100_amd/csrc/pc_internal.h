@@ -110,6 +110,10 @@ int run_reach_via(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t 
                   const int32_t *target, const int32_t *via, int32_t Kv, const int32_t *forbid, int32_t Kf,
                   int32_t *dist, hipStream_t stream);
 
+int run_probes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+               const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *probe_row,
+               const int32_t *probe_node, int32_t P, uint8_t *bit, hipStream_t stream);
+
 int run_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                      const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,
                      uint64_t *feasible, uint32_t *popcnt, hipStream_t stream);
@@ -121,7 +125,7 @@ int run_synthesize(pc_ctx *ctx, int32_t V, const int32_t *port_off, const int32_
                    int32_t *path, pc_rule *rules, hipStream_t stream);
 
 int run_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible,
-               int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
+               int32_t W, const uint8_t *ends, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
                const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
                const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary, hipStream_t stream);
 

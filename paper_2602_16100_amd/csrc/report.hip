@@ -19,6 +19,7 @@ constexpr int kThreads = 256;
 
 __global__ __launch_bounds__(kThreads) void k_report(int32_t I, const pc_intent *__restrict__ intents, int32_t rows,
                                                      const uint64_t *__restrict__ feasible, int32_t W,
+                                                     const uint8_t *__restrict__ ends,
                                                      const uint32_t *__restrict__ popcnt, int32_t N,
                                                      const pc_trace_out *__restrict__ traces, int32_t T,
                                                      const pc_flow_expect *__restrict__ expect,
@@ -60,9 +61,15 @@ __global__ __launch_bounds__(kThreads) void k_report(int32_t I, const pc_intent 
                 if (popcnt[it.sel_row] == 0) {
                     r = PC_R_NO_FEASIBLE_NODE;
                 } else if (kind == 3) {
-                    const uint64_t *row = feasible + static_cast<int64_t>(it.sel_row) * W;
-                    const bool a = (row[it.src_node >> 6] >> (it.src_node & 63)) & 1;
-                    const bool b = (row[it.dst_node >> 6] >> (it.dst_node & 63)) & 1;
+                    bool a, b;
+                    if (feasible) {
+                        const uint64_t *row = feasible + static_cast<int64_t>(it.sel_row) * W;
+                        a = (row[it.src_node >> 6] >> (it.src_node & 63)) & 1;
+                        b = (row[it.dst_node >> 6] >> (it.dst_node & 63)) & 1;
+                    } else {  // endpoint bits from probes (verdict-only runs)
+                        a = ends[2 * static_cast<int64_t>(i)] & 1;
+                        b = ends[2 * static_cast<int64_t>(i) + 1] & 1;
+                    }
                     if (!(a && b)) r = PC_R_ENDPOINT_INFEASIBLE;
                 }
             }
@@ -103,7 +110,7 @@ __global__ __launch_bounds__(kThreads) void k_report(int32_t I, const pc_intent 
 }  // namespace
 
 int run_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, const uint64_t *feasible, int32_t W,
-               const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
+               const uint8_t *ends, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
                const pc_flow_expect *expect, const int32_t *reach, int32_t Q, const uint32_t *visit,
                const pc_path_expect *pexp, uint64_t *pass, uint8_t *reason, pc_summary *summary, hipStream_t stream)
 {
@@ -112,7 +119,7 @@ int run_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, c
     PC_LAUNCH_CHECK(ctx);
     if (I == 0) return PC_OK;
     PC_TIMED(ctx, "k_report", stream, hipLaunchKernelGGL(k_report, dim3(static_cast<unsigned>((I + kThreads - 1) / kThreads)), dim3(kThreads), 0,
-                       stream, I, intents, rows, feasible, W, popcnt, N, traces, T, expect, reach, Q, visit, pexp, pass, reason,
+                       stream, I, intents, rows, feasible, W, ends, popcnt, N, traces, T, expect, reach, Q, visit, pexp, pass, reason,
                        reinterpret_cast<unsigned long long *>(summary), ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     return PC_OK;

@@ -646,8 +646,9 @@ __device__ Words eval_row_decoded_aff(const pc_pred *__restrict__ preds, int64_t
 // part[tile * I + r].  Lanes past the last word load in-bounds words and
 // mask them.
 // kTerms: affinity rows (pred_off holds the row -> term offsets, term_off
-// the term -> expression offsets) whose programs OR their terms.
-template <bool kBuf, bool kTerms>
+// the term -> expression offsets) whose programs OR their terms.  kStore
+// false: popcounts only, no bitset written (verdict-only runs).
+template <bool kBuf, bool kTerms, bool kStore = true>
 __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     const uint32_t *__restrict__ rec, const uint32_t *__restrict__ prog, const int32_t *__restrict__ pred_off,
     const pc_pred *__restrict__ preds, const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
@@ -735,12 +736,14 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
         }
         a.a &= m0;
         a.b &= m1;
-        uint64_t *dst = feasible + static_cast<int64_t>(r) * W + w0;
-        if (even) {
-            if (ok0) __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(dst));
-        } else {
-            if (ok0) __builtin_nontemporal_store(a.a, dst);
-            if (ok1) __builtin_nontemporal_store(a.b, dst + 1);
+        if constexpr (kStore) {
+            uint64_t *dst = feasible + static_cast<int64_t>(r) * W + w0;
+            if (even) {
+                if (ok0) __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(dst));
+            } else {
+                if (ok0) __builtin_nontemporal_store(a.a, dst);
+                if (ok1) __builtin_nontemporal_store(a.b, dst + 1);
+            }
         }
         cb[i * kCntStride + lane] = static_cast<uint8_t>(__popcll(a.a) + __popcll(a.b));
     };
@@ -830,7 +833,8 @@ int build_planes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, int64
     return PC_OK;
 }
 
-// The evaluator over every row, then the popcount partials' sum.
+// The evaluator over every row (feasible nullptr: popcounts only), then
+// the popcount partials' sum.
 template <bool kTerms>
 int launch_eval(pc_ctx *ctx, const uint32_t *rec, const uint32_t *prog, const int32_t *off,
                 const pc_pred *preds, const uint64_t *present, const uint32_t *wbase, const uint64_t *planes,
@@ -848,14 +852,19 @@ int launch_eval(pc_ctx *ctx, const uint32_t *rec, const uint32_t *prog, const in
     uint32_t *cnt_out = ntiles > 1 ? part : popcnt;
     const int64_t pbytes = static_cast<int64_t>(pmax + 1) * Wp * 8;
     auto eval = [&](auto kern) {
-        PC_TIMED(ctx, kTerms ? "k_aff_eval" : "k_sel_eval", stream,
+        PC_TIMED(ctx, kTerms ? "k_aff_eval" : (feasible ? "k_sel_eval" : "k_sel_count"), stream,
                  hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, off, preds,
                                     present, wbase, planes, pbytes, Wp, I, static_cast<int32_t>(W), N, feasible,
                                     cnt_out, static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
                                     static_cast<int32_t>(rpc), term_off, n_preds, L));
     };
-    if (pbytes < (int64_t(1) << 31)) eval(k_sel_eval<true, kTerms>);  // buffer offsets are 32-bit
-    else eval(k_sel_eval<false, kTerms>);
+    if (!feasible) {
+        if (pbytes < (int64_t(1) << 31)) eval(k_sel_eval<true, kTerms, false>);  // buffer offsets are 32-bit
+        else eval(k_sel_eval<false, kTerms, false>);
+    } else {
+        if (pbytes < (int64_t(1) << 31)) eval(k_sel_eval<true, kTerms>);
+        else eval(k_sel_eval<false, kTerms>);
+    }
     PC_LAUNCH_CHECK(ctx);
     if (ntiles > 1) {
         PC_TIMED(ctx, kTerms ? "k_aff_popsum" : "k_sel_popsum", stream,

@@ -1,7 +1,8 @@
 // NEXT-4 -- incremental re-validation of selector rows after node-label
 // changes (paper, Abstract: the validator is meant for continuous
 // cross-layer compliance checking).  Instead of rebuilding every row's
-// bitset, only the listed nodes' bits are re-evaluated.
+// bitset, only the listed nodes' bits are re-evaluated.  Also the
+// membership probes of verdict-only runs (one (row, node) query a thread).
 //
 // Design (gfx950):
 //   1. validate : PRED / OFFSETS over the rows (as pc_eval_selectors) and
@@ -213,7 +214,62 @@ __global__ __launch_bounds__(kRowThreads) void k_upd_rows(const int32_t *__restr
     }
 }
 
+// Membership probes: one thread per (row, node) query, the row's
+// predicates evaluated on the node's labels.
+__global__ __launch_bounds__(256) void k_probe(const uint8_t *__restrict__ labels, int32_t N, int32_t L,
+                                               const int32_t *__restrict__ pred_off, const pc_pred *__restrict__ preds,
+                                               int64_t n_preds, int32_t I, const int32_t *__restrict__ probe_row,
+                                               const int32_t *__restrict__ probe_node, int32_t P,
+                                               uint8_t *__restrict__ bit, uint32_t *__restrict__ d_err)
+{
+    const int32_t k = blockIdx.x * blockDim.x + threadIdx.x;
+    if (k >= P) return;
+    const int32_t r = probe_row[k], n = probe_node[k];
+    if (r < 0 || r >= I || n < 0 || n >= N) {
+        bit[k] = 0;
+        atomicOr(d_err, PC_DERR_NODE);
+        return;
+    }
+    const int64_t b = pred_off[r], e = pred_off[r + 1];
+    bool ok = pc_range_ok(b, e, n_preds);
+    const uint8_t *lab = labels + static_cast<int64_t>(n) * L;
+    for (int64_t p = b; ok && p < e; ++p) {
+        const pc_pred q = preds[p];
+        if (!upd_pred_valid(q, L)) {
+            ok = false;
+            break;
+        }
+        const uint32_t x = lab[q.label];
+        const bool present = x != PC_LABEL_ABSENT;
+        const uint32_t w = x >> 6;
+        const uint64_t vw = w == 0 ? q.vals[0] : w == 1 ? q.vals[1] : w == 2 ? q.vals[2] : q.vals[3];
+        const bool in_set = present && ((vw >> (x & 63)) & 1);
+        ok = q.op == PC_OP_IN ? in_set : q.op == PC_OP_NOTIN ? !in_set : present;
+    }
+    bit[k] = ok ? 1 : 0;
+}
+
 }  // namespace
+
+int run_probes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+               const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *probe_row,
+               const int32_t *probe_node, int32_t P, uint8_t *bit, hipStream_t stream)
+{
+    if (I > 0) {
+        // the rows' flags, as for pc_eval_selectors (no listed nodes)
+        const unsigned g = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
+        PC_TIMED(ctx, "k_upd_validate", stream,
+                 hipLaunchKernelGGL(k_upd_validate, dim3(g), dim3(256), 0, stream, pred_off, preds, n_preds, I, L,
+                                    nullptr, 0, N, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    if (P == 0) return PC_OK;
+    PC_TIMED(ctx, "k_probe", stream,
+             hipLaunchKernelGGL(k_probe, dim3(static_cast<unsigned>((P + 255) / 256)), dim3(256), 0, stream, labels,
+                                N, L, pred_off, preds, n_preds, I, probe_row, probe_node, P, bit, ctx->d_err));
+    PC_LAUNCH_CHECK(ctx);
+    return PC_OK;
+}
 
 int run_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                      const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,
