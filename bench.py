@@ -58,14 +58,20 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity", "synthesis"],
+    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity", "synthesis", "update",
+                                                     "verdict"],
                     help="profiling aid: time one stage only (the JSON line then covers that stage); 'paths' "
                          "times only the pass with waypoint / forbidden-switch constraints, 'affinity' only the "
-                         "node-affinity pass, 'synthesis' only the path-synthesis pass")
+                         "node-affinity pass, 'synthesis' only the path-synthesis pass, 'update' only the incremental "
+                         "re-evaluation, 'verdict' only the verdict-only pass")
     ap.add_argument("--no-paths", action="store_true",
                     help="skip the second timed pass with waypoint / forbidden-switch constraints")
     ap.add_argument("--no-affinity", action="store_true",
                     help="skip the timed pass of full node affinity over the same cluster")
+    ap.add_argument("--no-verdict-only", action="store_true",
+                    help="skip the timed verdict-only pass (popcounts and endpoint probes instead of the bitset)")
+    ap.add_argument("--no-update", action="store_true",
+                    help="skip the timed incremental re-evaluation after node-label changes")
     ap.add_argument("--no-synthesis", action="store_true",
                     help="skip the timed pass of path synthesis over the same topology")
     ap.add_argument("--synthesis-requests", type=int, default=65536,
@@ -307,6 +313,111 @@ def time_affinity(args, wl, pc, ctx, feasible):
     return out
 
 
+def time_verdict_only(args, wl, pc, ctx, D, traces, reach):
+    """Verdict-only pass: the selector rows' popcounts without the bitset
+    (pc_eval_selectors_count), the hybrid intents' endpoint bits as probes
+    (pc_probe_selectors) and the verdict from both (pc_report_counts), on the
+    traces and reach distances of the main pass.  Its verdict must equal the
+    main pass's."""
+    import torch
+    dev = traces.device
+    it = wl["intents"]
+    I = it.shape[0]
+    hyb = it["kind"] == 3
+    sel = np.repeat(hyb, 2)
+    rows = np.repeat(it["sel_row"], 2)[sel].astype(np.int32)
+    nodes = np.stack([it["src_node"], it["dst_node"]], axis=1).reshape(-1)[sel].astype(np.int32)
+    pos = pc.to_device(np.flatnonzero(sel).astype(np.int64), dev)
+    Dr, Dn = pc.to_device(rows, dev), pc.to_device(nodes, dev)
+    popcnt = torch.empty(wl["I_rows"], dtype=torch.int32, device=dev)
+    bits = torch.empty(rows.shape[0], dtype=torch.uint8, device=dev)
+    ends = torch.zeros(2 * I, dtype=torch.uint8, device=dev)
+    pass_ = torch.empty((I + 63) // 64, dtype=torch.int64, device=dev)
+    reason = torch.empty(I, dtype=torch.uint8, device=dev)
+    summary = torch.empty(pc.SUMMARY_BYTES, dtype=torch.uint8, device=dev)
+
+    def step():
+        pc.pc_eval_selectors_count(D["labels"], D["pred_off"], D["preds"], popcnt=popcnt, ctx=ctx)
+        pc.pc_probe_selectors(D["labels"], D["pred_off"], D["preds"], Dr, Dn, bits=bits, ctx=ctx)
+        ends.index_copy_(0, pos, bits)
+        pc.pc_report_counts(D["intents"], popcnt, wl["N"], ends, traces, D["expect"], reach, pass_=pass_,
+                            reason=reason, summary=summary, ctx=ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.profile(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = ctx.profile_read()
+    ctx.profile(False)
+    return {"ms_per_step": 1e3 * elapsed / args.steps,
+            "per_kernel": {name: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
+                           for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])},
+            "probes": int(rows.shape[0]),
+            "_pass": pass_, "_reason": reason}
+
+
+def time_update(args, wl, pc, ctx, D, feasible, popcnt):
+    """Incremental re-evaluation (pc_update_nodes) after relabelling M random
+    nodes of the cluster, against the full pc_eval_selectors of the new
+    labels.  The bitsets are brought to the old labels' state before each
+    timed call; the timed region is the call alone.  Above W / 16 nodes the
+    library itself takes the full evaluation."""
+    import torch
+    dev = feasible.device
+    rng = np.random.default_rng([wl.seed, 15])
+    N, L, I = wl["N"], wl["L"], feasible.shape[0]
+    W = (N + 63) // 64
+    cards = wl.meta["cards"]
+    labels = wl["labels"]
+    base = pc.to_device(labels, dev)
+    out = {"rows": I, "nodes": N, "full_above": W // 16, "per_m": {}}
+    for M in (1, 16, 64, 1024):
+        nodes = rng.choice(N, size=M, replace=False).astype(np.int32)
+        new = labels.copy()
+        new[nodes] = rng.integers(0, cards[None, :], size=(M, L)).astype(np.uint8)
+        Dn = pc.to_device(new, dev)
+        Dnodes = pc.to_device(nodes, dev)
+        t_upd, t_full = [], []
+        for it in range(args.warmup + args.steps):
+            pc.pc_eval_selectors(base, D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            pc.pc_update_nodes(Dn, D["pred_off"], D["preds"], Dnodes, feasible, popcnt, ctx=ctx)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            pc.pc_eval_selectors(Dn, D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            if it >= args.warmup:
+                t_upd.append(t1 - t0)
+                t_full.append(t2 - t1)
+        u, f = float(np.median(t_upd)), float(np.median(t_full))
+        out["per_m"][str(M)] = {"ms_per_update": 1e3 * u, "ms_full_evaluation": 1e3 * f, "speedup": f / u,
+                                "path": "incremental" if M <= W // 16 else "full re-evaluation"}
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = len(os.sched_getaffinity(0))
+        env_cap = os.environ.get("OMP_NUM_THREADS")
+        if env_cap and env_cap.isdigit():
+            threads = min(threads, int(env_cap))
+        nodes = rng.choice(N, size=1, replace=False).astype(np.int32)
+        f0 = feasible.cpu().numpy().view(np.uint64)
+        p0 = popcnt.cpu().numpy().view(np.uint32)
+        t0 = time.perf_counter()
+        oracle.update_nodes(labels, wl["pred_off"], wl["preds"], nodes, f0, p0, nthreads=threads)
+        t = time.perf_counter() - t0
+        out["cpu_baseline"] = {"value": 1.0 / t, "unit": "updates/s (1 relabelled node, all rows)",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"one update of 1 node over all {I} rows in {t:.3f} s (copies of the "
+                                         f"bitset and popcounts included)"}
+    return out
+
+
 def time_synthesis(args, wl, pc, ctx):
     """Timed pass of path synthesis (pc_synthesize_paths) over the same
     topology: the first flows' endpoints, allowed jurisdictions, waypoint,
@@ -456,6 +567,21 @@ def main():
     if only == "affinity":
         print(json.dumps({"workload": desc, "affinity": time_affinity(args, wl, pc, ctx, feasible)}), flush=True)
         return
+    if only == "update":
+        print(json.dumps({"workload": desc, "update": time_update(args, wl, pc, ctx, D, feasible, popcnt)}),
+              flush=True)
+        return
+    if only == "verdict":
+        # the inputs the verdict reads, computed once outside the timed pass
+        pc.pc_trace_flows(wl["S"], D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                          D["ingress"], wl["ttl"], out=traces, ctx=ctx)
+        pc.pc_masked_reach(wl["V"], D["adj_off"], D["adj"], D["region"], D["src"], D["allowed"], D["target"],
+                           dist=reach, ctx=ctx)
+        vo = time_verdict_only(args, wl, pc, ctx, D, traces, reach)
+        vo.pop("_pass")
+        vo.pop("_reason")
+        print(json.dumps({"workload": desc, "verdict_only": vo}), flush=True)
+        return
     if only == "synthesis":
         print(json.dumps({"workload": desc, "synthesis": time_synthesis(args, wl, pc, ctx)}), flush=True)
         return
@@ -561,6 +687,14 @@ def main():
         line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)
     if only == "all" and not args.no_affinity:
         line["affinity"] = time_affinity(args, wl, pc, ctx, feasible)
+    if only == "all" and not args.no_verdict_only:
+        vo = time_verdict_only(args, wl, pc, ctx, D, traces, reach)
+        vo["verdict_equals_main_pass"] = bool(torch.equal(vo.pop("_pass"), pass_) and
+                                              torch.equal(vo.pop("_reason"), reason))
+        vo["main_pass_selector_plus_report_ms"] = ktime("k_sel_") + ktime("k_report")
+        line["verdict_only"] = vo
+    if only == "all" and not args.no_update:
+        line["update"] = time_update(args, wl, pc, ctx, D, feasible, popcnt)
     if only == "all" and not args.no_synthesis:
         line["synthesis"] = time_synthesis(args, wl, pc, ctx)
     if not args.no_cpu_baseline:

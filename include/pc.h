@@ -432,9 +432,11 @@ int pc_report_counts(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t r
  * Arguments and layouts as pc_eval_selectors; nodes: int32 [M] device
  * array.  Limits: 0 <= M <= PC_UPDATE_MAX_NODES.  Malformed data: a listed
  * node outside [0, N) is skipped (PC_DERR_NODE); rows and predicates as in
- * pc_eval_selectors (PC_DERR_OFFSETS, PC_DERR_PRED).  The cost grows with
- * the number of distinct bitset words the nodes touch per row; a full
- * pc_eval_selectors is cheaper once that approaches W.
+ * pc_eval_selectors (PC_DERR_OFFSETS, PC_DERR_PRED).  The incremental cost
+ * grows with the number of distinct bitset words the nodes touch per row;
+ * above W / 16 listed nodes the call evaluates every row in full instead
+ * (the same result; environment variable PC_UPDATE_FULL_ABOVE overrides the
+ * threshold).
  */
 int pc_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                     const pc_pred *preds, int64_t n_preds, int32_t I, const int32_t *nodes, int32_t M,

@@ -5,20 +5,21 @@
 // membership probes of verdict-only runs (one (row, node) query a thread).
 //
 // Design (gfx950):
-//   1. validate : PRED / OFFSETS over the rows (as pc_eval_selectors) and
-//                 NODE over the list.
+//   1. validate : NODE over the list.
 //   2. prep     : one workgroup sorts the in-range listed nodes (bitonic, in
 //                 LDS), drops repeats, and gathers their label rows into a
 //                 compact block.  A node's new bit depends only on its new
 //                 labels, so a repeated node changes nothing more.
-//   3. rows     : one wavefront per row; the workgroup stages the label rows
-//                 of 64 nodes at a time in LDS.  Lane m evaluates the row's
-//                 predicates (scalar loads, uniform) on node m; the new bits
-//                 are OR-ed per 64-bit bitset word by a segmented shuffle
-//                 reduction over the sorted lanes, and the first lane of each
-//                 word updates it with one atomic clear (which returns the
-//                 old word) and one atomic set, and adds the popcount change.
+//   3. rows     : one thread per row, which also raises the rows' PRED /
+//                 OFFSETS flags (as pc_eval_selectors); the workgroup stages
+//                 the label rows of 64 nodes at a time in LDS.  Each
+//                 predicate of the row is loaded once per batch and tested
+//                 on every node of it into a 64-bit node mask; the masks are
+//                 AND-ed, and each bitset word the batch touches is updated
+//                 with one atomic clear (which returns the old word) and one
+//                 atomic set, the popcount moving by the words' change.
 #include <climits>
+#include <cstdlib>
 
 #include "pc_internal.h"
 
@@ -26,7 +27,7 @@ namespace {
 
 constexpr int kUpdMax = PC_UPDATE_MAX_NODES;  // listed nodes per call
 constexpr int kPrepThreads = 1024;
-constexpr int kRowThreads = 256;             // 4 wavefronts, one row each
+constexpr int kRowThreads = 256;             // one row per thread
 
 __device__ __forceinline__ bool upd_pred_valid(const pc_pred &q, int32_t L)
 {
@@ -62,10 +63,11 @@ __global__ __launch_bounds__(256) void k_upd_validate(const int32_t *__restrict_
 
 // Sorted distinct in-range nodes -> uniq[0..*d_mu), their label rows ->
 // ulab[k * L ...].
+// n2: a power of two >= M (at most kUpdMax); only key[0..n2) is sorted.
 __global__ __launch_bounds__(kPrepThreads) void k_upd_prep(const int32_t *__restrict__ nodes, int32_t M, int32_t N,
                                                            const uint8_t *__restrict__ labels, int32_t L,
                                                            int32_t *__restrict__ uniq, uint8_t *__restrict__ ulab,
-                                                           int32_t *__restrict__ d_mu)
+                                                           int32_t *__restrict__ d_mu, int32_t n2)
 {
     __shared__ int32_t key[kUpdMax];
     __shared__ int32_t comp[kUpdMax];
@@ -76,10 +78,10 @@ __global__ __launch_bounds__(kPrepThreads) void k_upd_prep(const int32_t *__rest
         key[i] = (n >= 0 && n < N) ? n : INT32_MAX;
     }
     __syncthreads();
-    // bitonic sort, ascending
-    for (int k = 2; k <= kUpdMax; k <<= 1) {
+    // bitonic sort of key[0..n2), ascending (the rest holds INT32_MAX)
+    for (int k = 2; k <= n2; k <<= 1) {
         for (int j = k >> 1; j > 0; j >>= 1) {
-            for (int i = tid; i < kUpdMax; i += kPrepThreads) {
+            for (int i = tid; i < n2; i += kPrepThreads) {
                 const int l = i ^ j;
                 if (l > i) {
                     const int32_t a = key[i], b = key[l];
@@ -130,76 +132,88 @@ __global__ __launch_bounds__(kPrepThreads) void k_upd_prep(const int32_t *__rest
     }
 }
 
-// One wavefront per row (see the file header).
+// One thread per row (see the file header).  The row's offset pair and
+// predicates are validated first (PRED / OFFSETS as pc_eval_selectors);
+// then, per batch of up to 64 sorted nodes staged in LDS, each predicate is
+// loaded once and tested on every node of the batch into a 64-bit node
+// mask, the masks are AND-ed, and the row's bitset words are updated word
+// by word (the nodes are sorted, so a word's nodes are consecutive).
 __global__ __launch_bounds__(kRowThreads) void k_upd_rows(const int32_t *__restrict__ pred_off,
                                                           const pc_pred *__restrict__ preds, int64_t n_preds,
                                                           int32_t I, int32_t L, const int32_t *__restrict__ uniq,
                                                           const uint8_t *__restrict__ ulab,
                                                           const int32_t *__restrict__ d_mu, int32_t W,
                                                           uint64_t *__restrict__ feasible,
-                                                          uint32_t *__restrict__ popcnt)
+                                                          uint32_t *__restrict__ popcnt, uint32_t *__restrict__ d_err)
 {
-    extern __shared__ uint8_t lab_lds[];  // 64 nodes x stride bytes
-    const int32_t stride = (L + 4) & ~3;  // padded row: consecutive lanes start in different banks
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int32_t r = blockIdx.x * (kRowThreads / 64) + wave;
+    extern __shared__ uint8_t lab_lds[];  // up to 64 nodes x L bytes, then their ids
+    const int tid = threadIdx.x;
+    const int32_t r = blockIdx.x * kRowThreads + tid;
     const int32_t mu = *d_mu;
+    int32_t *ids = reinterpret_cast<int32_t *>(lab_lds + ((static_cast<int64_t>(64) * L + 3) & ~int64_t(3)));
     const bool live = r < I;
     int64_t b = 0, e = 0;
     bool row_ok = false;
+    uint32_t errs = 0;
     if (live) {
         b = pred_off[r];
         e = pred_off[r + 1];
         row_ok = pc_range_ok(b, e, n_preds);
+        if (!row_ok) errs |= PC_DERR_OFFSETS;
+        if (mu == 0)  // no batch: the predicates are only validated
+            for (int64_t p = b; row_ok && p < e; ++p)
+                if (!upd_pred_valid(preds[p], L)) {
+                    errs |= PC_DERR_PRED;
+                    row_ok = false;
+                }
     }
     uint32_t delta = 0;
     for (int32_t k0 = 0; k0 < mu; k0 += 64) {
         const int32_t nb = min(64, mu - k0);
-        __syncthreads();  // the previous batch's labels are no longer read
-        for (int32_t i = tid; i < nb * L; i += kRowThreads)
-            lab_lds[(i / L) * stride + (i % L)] = ulab[static_cast<int64_t>(k0) * L + i];
+        __syncthreads();  // the previous batch is no longer read
+        for (int32_t i = tid; i < nb * L; i += kRowThreads) lab_lds[i] = ulab[static_cast<int64_t>(k0) * L + i];
+        if (tid < nb) ids[tid] = uniq[k0 + tid];
         __syncthreads();
         if (!live) continue;
-        const bool act = lane < nb;
-        const int32_t n = act ? uniq[k0 + lane] : INT32_MAX;
-        bool ok = act && row_ok;
-        if (row_ok) {
-            for (int64_t p = b; p < e; ++p) {
-                const pc_pred q = preds[p];
-                if (!upd_pred_valid(q, L)) {
-                    ok = false;
-                    break;  // uniform: every lane sees the same predicate
-                }
-                const uint32_t x = act ? lab_lds[lane * stride + q.label] : 0xFFu;
+        // bit m of `hold`: node m of the batch satisfies the row.  The first
+        // batch also validates every predicate (a malformed one admits no
+        // node and raises PRED), so it reads them all.
+        uint64_t hold = nb == 64 ? ~0ull : ((1ull << nb) - 1);
+        if (!row_ok) hold = 0;
+        const bool first = k0 == 0;
+        for (int64_t p = b; row_ok && (hold || first) && p < e; ++p) {
+            const pc_pred q = preds[p];
+            if (first && !upd_pred_valid(q, L)) {
+                errs |= PC_DERR_PRED;
+                row_ok = false;
+                hold = 0;
+                break;
+            }
+            if (!hold) continue;
+            uint64_t m = 0;
+            for (int32_t j = 0; j < nb; ++j) {
+                const uint32_t x = lab_lds[j * L + q.label];
                 const bool present = x != PC_LABEL_ABSENT;
-                const uint32_t k = x >> 6;  // the value-set word, chosen without a per-lane array index
-                const uint64_t vw = k == 0 ? q.vals[0] : k == 1 ? q.vals[1] : k == 2 ? q.vals[2] : q.vals[3];
+                const uint32_t w = x >> 6;
+                const uint64_t vw = w == 0 ? q.vals[0] : w == 1 ? q.vals[1] : w == 2 ? q.vals[2] : q.vals[3];
                 const bool in_set = present && ((vw >> (x & 63)) & 1);
                 const bool sat = q.op == PC_OP_IN ? in_set : q.op == PC_OP_NOTIN ? !in_set : present;
-                ok = ok && sat;
+                m |= static_cast<uint64_t>(sat) << j;
             }
+            hold &= m;
         }
-        // segmented OR of the new bits over lanes of the same word (sorted nodes: words are contiguous)
-        const int32_t w = act ? (n >> 6) : -1 - lane;
-        uint64_t set = ok ? (1ull << (n & 63)) : 0ull;
-        uint64_t mask = act ? (1ull << (n & 63)) : 0ull;
-#pragma unroll
-        for (int off = 1; off < 64; off <<= 1) {
-            const uint64_t s2 = __shfl_down(set, off, 64);
-            const uint64_t m2 = __shfl_down(mask, off, 64);
-            const int32_t w2 = __shfl_down(w, off, 64);
-            if (lane + off < 64 && w2 == w) {
-                set |= s2;
-                mask |= m2;
+        // word by word: the batch's nodes in one word are consecutive
+        int32_t j = 0;
+        while (j < nb) {
+            const int32_t w = ids[j] >> 6;
+            uint64_t set = 0, mask = 0;
+            for (; j < nb && (ids[j] >> 6) == w; ++j) {
+                const uint64_t bit = 1ull << (ids[j] & 63);
+                mask |= bit;
+                if ((hold >> j) & 1) set |= bit;
             }
-        }
-        const int32_t wprev = __shfl_up(w, 1, 64);
-        const bool head = act && (lane == 0 || wprev != w);
-        if (head) {
             // a word can straddle two batches: the update goes through L2
-            // atomics (clear, returning the old word, then set), so the next
-            // batch's read of the same word sees this one's write
+            // atomics (clear, returning the old word, then set)
             unsigned long long *dst =
                 reinterpret_cast<unsigned long long *>(feasible + static_cast<int64_t>(r) * W + w);
             const uint64_t old = atomicAnd(dst, ~(mask & ~set));
@@ -208,10 +222,8 @@ __global__ __launch_bounds__(kRowThreads) void k_upd_rows(const int32_t *__restr
             delta += static_cast<uint32_t>(__popcll(nw)) - static_cast<uint32_t>(__popcll(old));
         }
     }
-    if (live) {
-        const uint32_t d = pc_wave_sum_u32(delta);
-        if (lane == 0 && d) popcnt[r] += d;
-    }
+    if (live && delta) popcnt[r] += delta;
+    if (errs) atomicOr(d_err, errs);
 }
 
 // Membership probes: one thread per (row, node) query, the row's
@@ -288,27 +300,40 @@ int run_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, c
     if (rc) return rc;
     Carver real{ctx->arena, 0};
     carve(real);
-    const int64_t tot = std::max<int64_t>(I, M);
-    if (tot > 0) {
-        const unsigned g = static_cast<unsigned>(std::min<int64_t>((tot + 255) / 256, 8192));
+    if (M > 0) {
+        // NODE over the list (the rows' flags are raised by k_upd_rows)
+        const unsigned g = static_cast<unsigned>(std::min<int64_t>((M + 255) / 256, 8192));
         PC_TIMED(ctx, "k_upd_validate", stream,
-                 hipLaunchKernelGGL(k_upd_validate, dim3(g), dim3(256), 0, stream, pred_off, preds, n_preds, I, L,
+                 hipLaunchKernelGGL(k_upd_validate, dim3(g), dim3(256), 0, stream, pred_off, preds, n_preds, 0, L,
                                     nodes, M, N, ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
     }
-    if (I == 0 || M == 0 || N == 0) return PC_OK;
-    PC_TIMED(ctx, "k_upd_prep", stream,
-             hipLaunchKernelGGL(k_upd_prep, dim3(1), dim3(kPrepThreads), 0, stream, nodes, M, N, labels, L, uniq,
-                                ulab, d_mu));
-    PC_LAUNCH_CHECK(ctx);
+    if (I == 0) return PC_OK;
+    // Above W / 16 listed nodes the scattered word updates cost more than
+    // rewriting every row: evaluate the rows in full instead (same result).
+    // PC_UPDATE_FULL_ABOVE overrides the threshold.
     const int32_t W = (N + 63) / 64;
-    const size_t lds = static_cast<size_t>(64) * ((L + 4) & ~3);
+    int64_t full_above = W / 16;
+    if (const char *env = getenv("PC_UPDATE_FULL_ABOVE")) full_above = atoll(env);
+    if (M > full_above && W > 0)
+        return run_selectors(ctx, labels, N, L, pred_off, preds, n_preds, I, feasible, popcnt, stream);
+    if (M > 0 && N > 0) {
+        int32_t n2 = 2;
+        while (n2 < M) n2 <<= 1;
+        PC_TIMED(ctx, "k_upd_prep", stream,
+                 hipLaunchKernelGGL(k_upd_prep, dim3(1), dim3(kPrepThreads), 0, stream, nodes, M, N, labels, L, uniq,
+                                    ulab, d_mu, n2));
+    } else {
+        launch_fill_u32(reinterpret_cast<uint32_t *>(d_mu), 1, 0, stream);
+    }
+    PC_LAUNCH_CHECK(ctx);
+    const size_t lds = ((static_cast<size_t>(64) * L + 3) & ~size_t(3)) + 64 * sizeof(int32_t);
     PC_HIP(ctx, hipFuncSetAttribute(reinterpret_cast<const void *>(k_upd_rows),
                                     hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
-    const unsigned g = static_cast<unsigned>((I + 3) / 4);
+    const unsigned g = static_cast<unsigned>((I + kRowThreads - 1) / kRowThreads);
     PC_TIMED(ctx, "k_upd_rows", stream,
              hipLaunchKernelGGL(k_upd_rows, dim3(g), dim3(kRowThreads), lds, stream, pred_off, preds, n_preds, I, L,
-                                uniq, ulab, d_mu, W, feasible, popcnt));
+                                uniq, ulab, d_mu, W, feasible, popcnt, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     return PC_OK;
 }

@@ -21,6 +21,17 @@ def g():
     return torch
 
 
+@pytest.fixture(params=["default", "kernel"])
+def path(request, monkeypatch):
+    """default: the library's own switch to full re-evaluation above W/16
+    nodes; kernel: the incremental kernels for every list size."""
+    if request.param == "kernel":
+        monkeypatch.setenv("PC_UPDATE_FULL_ABOVE", str(1 << 30))
+    else:
+        monkeypatch.delenv("PC_UPDATE_FULL_ABOVE", raising=False)
+    return request.param
+
+
 def _relabel(rng, labels, cards, nodes, absent_p=0.1):
     new = labels.copy()
     for n in np.unique(nodes):
@@ -51,7 +62,7 @@ def _gpu_full(labels, off, preds):
 
 @pytest.mark.parametrize("M,clustered", [(1, False), (5, True), (64, False), (65, True), (700, False),
                                          (4096, True)])
-def test_update_matches_full_evaluation(g, orc, M, clustered):
+def test_update_matches_full_evaluation(g, orc, path, M, clustered):
     wl = synth.selector_workload(7, 9000 + 13, 16, 1500, card_choices=(2, 3, 16, 64, 200), absent_p=0.05)
     labels, off, preds = wl["labels"], wl["pred_off"], wl["preds"]
     rng = np.random.default_rng(M)
@@ -71,7 +82,7 @@ def test_update_matches_full_evaluation(g, orc, M, clustered):
     assert np.array_equal(fu, fo) and np.array_equal(pu, po)
 
 
-def test_update_out_of_range_and_malformed(g, orc):
+def test_update_out_of_range_and_malformed(g, orc, path):
     wl = synth.selector_workload(8, 3000, 6, 300, absent_p=0.1)
     labels, off, preds = wl["labels"], wl["pred_off"].copy(), wl["preds"].copy()
     preds[5]["op"] = 7
@@ -89,7 +100,7 @@ def test_update_out_of_range_and_malformed(g, orc):
     assert eu == 3 and np.array_equal(fu, f0) and np.array_equal(pu, p0)
 
 
-def test_update_full_size(g, orc):
+def test_update_full_size(g, orc, path):
     """The combined workload's cluster and selector rows (699,051 rows x
     50,000 nodes): 64 relabelled nodes; the update equals the full
     evaluation of the new labels."""
