@@ -32,10 +32,10 @@ HBM_PEAK_GBS = 8000.0
 # profiles/k_sel_eval_cfg5_hbm_counters.md).  Valid only for the kernel
 # source they were measured on.
 TRAFFIC = {"source": "paper_2602_16100_amd/csrc/select.hip",
-           "sha256": "a2f3ab0de4a4625ce0b3aeffca455547a03e1fd788324155eb86fd17fa55ae20",
+           "sha256": "371dd8d7b186ef479b49591944e2ceeb6c4482da9b2382b26bfd9f1a17c8aefc",
            "workload": "cfg5",
-           "bytes_per_launch": {"k_sel_eval": 797_440_007 + 4_473_968_384,
-                                "k_aff_eval": 1_022_633_778 + 4_474_097_162}}
+           "bytes_per_launch": {"k_sel_eval": 797_446_228 + 4_473_979_605,
+                                "k_aff_eval": 1_022_856_675 + 4_474_095_445}}
 
 
 def measured_traffic(workload, kernel):
@@ -405,16 +405,17 @@ def time_update(args, wl, pc, ctx, D, feasible, popcnt):
         env_cap = os.environ.get("OMP_NUM_THREADS")
         if env_cap and env_cap.isdigit():
             threads = min(threads, int(env_cap))
-        nodes = rng.choice(N, size=1, replace=False).astype(np.int32)
-        f0 = feasible.cpu().numpy().view(np.uint64)
-        p0 = popcnt.cpu().numpy().view(np.uint32)
+        nodes = rng.choice(N, size=64, replace=False).astype(np.int32)
+        R = min(I, 65536)  # the first R rows: the oracle's copies of the bitset stay small
+        f0 = feasible[:R].cpu().numpy().view(np.uint64)
+        p0 = popcnt[:R].cpu().numpy().view(np.uint32)
         t0 = time.perf_counter()
-        oracle.update_nodes(labels, wl["pred_off"], wl["preds"], nodes, f0, p0, nthreads=threads)
-        t = time.perf_counter() - t0
-        out["cpu_baseline"] = {"value": 1.0 / t, "unit": "updates/s (1 relabelled node, all rows)",
+        oracle.update_nodes(labels, wl["pred_off"][:R + 1], wl["preds"], nodes, f0, p0, nthreads=threads)
+        t = (time.perf_counter() - t0) * I / R
+        out["cpu_baseline"] = {"value": 1.0 / t, "unit": "updates/s (64 relabelled nodes, all rows; estimate)",
                                "cores": threads, "kind": "oracle",
-                               "sample": f"one update of 1 node over all {I} rows in {t:.3f} s (copies of the "
-                                         f"bitset and popcounts included)"}
+                               "sample": f"one update of 64 nodes over the first {R} of {I} rows, scaled to all rows: "
+                                         f"{t:.3f} s per update"}
     return out
 
 
