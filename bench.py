@@ -365,7 +365,7 @@ def time_update(args, wl, pc, ctx, D, feasible, popcnt):
     """Incremental re-evaluation (pc_update_nodes) after relabelling M random
     nodes of the cluster, against the full pc_eval_selectors of the new
     labels.  The bitsets are brought to the old labels' state before each
-    timed call; the timed region is the call alone.  Above W / 16 nodes the
+    timed call; the timed region is the call alone.  Above W / 32 nodes the
     library itself takes the full evaluation."""
     import torch
     dev = feasible.device
@@ -375,7 +375,7 @@ def time_update(args, wl, pc, ctx, D, feasible, popcnt):
     cards = wl.meta["cards"]
     labels = wl["labels"]
     base = pc.to_device(labels, dev)
-    out = {"rows": I, "nodes": N, "full_above": W // 16, "per_m": {}}
+    out = {"rows": I, "nodes": N, "full_above": W // 32, "per_m": {}}
     for M in (1, 16, 64, 1024):
         nodes = rng.choice(N, size=M, replace=False).astype(np.int32)
         new = labels.copy()
@@ -398,7 +398,7 @@ def time_update(args, wl, pc, ctx, D, feasible, popcnt):
                 t_full.append(t2 - t1)
         u, f = float(np.median(t_upd)), float(np.median(t_full))
         out["per_m"][str(M)] = {"ms_per_update": 1e3 * u, "ms_full_evaluation": 1e3 * f, "speedup": f / u,
-                                "path": "incremental" if M <= W // 16 else "full re-evaluation"}
+                                "path": "incremental" if M <= W // 32 else "full re-evaluation"}
     if not args.no_cpu_baseline:
         import oracle
         threads = len(os.sched_getaffinity(0))

@@ -434,7 +434,7 @@ int pc_report_counts(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t r
  * node outside [0, N) is skipped (PC_DERR_NODE); rows and predicates as in
  * pc_eval_selectors (PC_DERR_OFFSETS, PC_DERR_PRED).  The incremental cost
  * grows with the number of distinct bitset words the nodes touch per row;
- * above W / 16 listed nodes the call evaluates every row in full instead
+ * above W / 32 listed nodes the call evaluates every row in full instead
  * (the same result; environment variable PC_UPDATE_FULL_ABOVE overrides the
  * threshold).
  */

@@ -16,8 +16,10 @@
 //                 predicate of the row is loaded once per batch and tested
 //                 on every node of it into a 64-bit node mask; the masks are
 //                 AND-ed, and each bitset word the batch touches is updated
-//                 with one atomic clear (which returns the old word) and one
-//                 atomic set, the popcount moving by the words' change.
+//                 (plainly, and only when a listed bit changes, when there is
+//                 one batch; else with one atomic clear that returns the old
+//                 word and one atomic set), the popcount moving by the
+//                 words' change.
 #include <climits>
 #include <cstdlib>
 
@@ -212,12 +214,20 @@ __global__ __launch_bounds__(kRowThreads) void k_upd_rows(const int32_t *__restr
                 mask |= bit;
                 if ((hold >> j) & 1) set |= bit;
             }
-            // a word can straddle two batches: the update goes through L2
-            // atomics (clear, returning the old word, then set)
-            unsigned long long *dst =
-                reinterpret_cast<unsigned long long *>(feasible + static_cast<int64_t>(r) * W + w);
-            const uint64_t old = atomicAnd(dst, ~(mask & ~set));
-            if (set) atomicOr(dst, set);
+            uint64_t *dst = feasible + static_cast<int64_t>(r) * W + w;
+            uint64_t old;
+            if (mu <= 64) {
+                // one batch: every word is touched once, plainly, and written
+                // only when one of its listed bits changes
+                old = *dst;
+                if ((old & mask) != set) *dst = (old & ~mask) | set;
+            } else {
+                // a word can straddle two batches: the update goes through L2
+                // atomics (clear, returning the old word, then set)
+                unsigned long long *adst = reinterpret_cast<unsigned long long *>(dst);
+                old = atomicAnd(adst, ~(mask & ~set));
+                if (set) atomicOr(adst, set);
+            }
             const uint64_t nw = (old & ~mask) | set;
             delta += static_cast<uint32_t>(__popcll(nw)) - static_cast<uint32_t>(__popcll(old));
         }
@@ -309,11 +319,11 @@ int run_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, c
         PC_LAUNCH_CHECK(ctx);
     }
     if (I == 0) return PC_OK;
-    // Above W / 16 listed nodes the scattered word updates cost more than
-    // rewriting every row: evaluate the rows in full instead (same result).
+    // Above W / 32 listed nodes the scattered word updates cost about as much
+    // as rewriting every row: evaluate the rows in full instead (same result).
     // PC_UPDATE_FULL_ABOVE overrides the threshold.
     const int32_t W = (N + 63) / 64;
-    int64_t full_above = W / 16;
+    int64_t full_above = W / 32;
     if (const char *env = getenv("PC_UPDATE_FULL_ABOVE")) full_above = atoll(env);
     if (M > full_above && W > 0)
         return run_selectors(ctx, labels, N, L, pred_off, preds, n_preds, I, feasible, popcnt, stream);
