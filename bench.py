@@ -684,6 +684,18 @@ def main():
         "verdict": {"passed": passed, "intents": I},
         "data_error_flags": flags,
     }
+    if only in ("all", "trace") and "k_tr_prep" in prof:
+        # rule-table preparation: every 40-byte rule read once, 96 chunk-set
+        # words (384 B) written per 32-rule group
+        ro = np.asarray(wl["rule_off"], dtype=np.int64)
+        groups = int(((np.diff(ro) + 31) // 32).sum())
+        prep_bytes = int(wl["n_rules"]) * 40 + groups * 96 * 4
+        prep_n, prep_ms = prof["k_tr_prep"]
+        prep_avg = prep_ms / max(prep_n, 1)
+        prep_gbs = prep_bytes / (prep_avg * 1e-3) / 1e9 if prep_avg > 0 else 0.0
+        line["trace_prep_roofline"] = {"kernel": "k_tr_prep", "bound": "hbm", "achieved": prep_gbs,
+                                       "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": prep_gbs / HBM_PEAK_GBS,
+                                       "alg_bytes_per_launch": prep_bytes, "avg_launch_ms": prep_avg}
     if only == "all" and not args.no_paths:
         line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)
     if only == "all" and not args.no_affinity:

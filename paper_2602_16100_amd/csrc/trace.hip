@@ -13,10 +13,11 @@
 // Design (gfx950):
 //   prep   : per 32-rule group, for each of kChunks 4-bit chunks of header
 //            word 2 (ports) and each of the 16 chunk values, the 32-bit set
-//            of rules whose mask/value admit that chunk value.  Stored
-//            plane-major per switch so a wavefront loads 64 groups with
-//            coalesced reads.  Also validates ports, jurisdictions, offsets
-//            and actions (the data-error sweep).
+//            of rules whose mask/value admit that chunk value (per-rule
+//            admit sets from an LDS table, then a bit transpose across the
+//            half-wavefront).  Stored plane-major per switch so a wavefront
+//            loads 64 groups with coalesced reads.  Also validates ports,
+//            jurisdictions, offsets and actions (the data-error sweep).
 //   levels : level-synchronous walk.  Live traces are bucketed by their
 //            current switch (count -> scan -> scatter); one workgroup per
 //            switch keeps the switch's chunk sets in VGPRs (16,384 rules per
@@ -44,7 +45,7 @@ constexpr int kMatchThreads = kMatchWaves * 64;
 constexpr int kSliceGroups = kMatchThreads;  // one group (32 rules) per lane
 constexpr int kChunk = 256;                  // lookups per match work item (a multiple of 4, <= kMatchThreads)
 constexpr int kQueue = 512;                  // queued filter survivors per wavefront (>= 4 x 64)
-constexpr int kPrepGroups = 32;              // groups per prep workgroup (1024 threads, 2 groups per wave)
+constexpr int kPrepGroups = 128;             // groups per prep workgroup (16 wavefronts x 4 rounds x 2 groups)
 constexpr uint64_t kNoMatch = ~0ull;
 static_assert(kChunk % 4 == 0 && kChunk <= kMatchThreads, "one epilogue thread per lookup");
 constexpr int kCountPad = 32;  // live-trace counters are 128 bytes apart: contended atomics on one line serialise
@@ -101,7 +102,56 @@ __global__ void k_tr_port_check(int64_t n_ports, const int32_t *__restrict__ por
     if (bad) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
+// Rows r of a 32-lane half hold 32-bit words x_r; afterwards lane i holds
+// column i (bit r = bit i of the old x_r).  Five block-swap stages, one per
+// lane-index bit j: the partner's word (lane i ^ j) is rotated so that its
+// blocks land where this lane takes them, then merged under the lane's keep
+// mask.  The stages commute; each costs one cross-lane move and two VALU ops.
+template <int J>
+__device__ __forceinline__ uint32_t lane_xor(uint32_t x)
+{
+    const int v = static_cast<int>(x);
+    if constexpr (J == 1) return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false));  // quad_perm 1,0,3,2
+    if constexpr (J == 2) return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false));  // quad_perm 2,3,0,1
+    if constexpr (J == 4) {
+        // banks 0 and 2 of each row read lane + 4 (row_shl:4), banks 1 and 3 read lane - 4 (row_shr:4)
+        const int lo = __builtin_amdgcn_update_dpp(v, v, 0x104, 0xF, 0x5, false);
+        return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(lo, v, 0x114, 0xF, 0xA, false));
+    }
+    if constexpr (J == 8) return static_cast<uint32_t>(__builtin_amdgcn_update_dpp(v, v, 0x128, 0xF, 0xF, false));  // row_ror:8
+    if constexpr (J == 16) return static_cast<uint32_t>(__builtin_amdgcn_ds_swizzle(v, 0x401F));  // 32-lane groups, xor 16
+    return x;
+}
+
+template <int J>
+__device__ __forceinline__ uint32_t swap_stage(uint32_t x, uint32_t keep, uint32_t rot)
+{
+    const uint32_t y = lane_xor<J>(x);
+    const uint32_t t = __builtin_amdgcn_alignbit(y, y, rot);  // rotate right
+    return (x & keep) | (t & ~keep);
+}
+
+__device__ __forceinline__ uint32_t transpose32(uint32_t x, const uint32_t (&keep)[5], const uint32_t (&rot)[5])
+{
+    x = swap_stage<1>(x, keep[0], rot[0]);
+    x = swap_stage<2>(x, keep[1], rot[1]);
+    x = swap_stage<4>(x, keep[2], rot[2]);
+    x = swap_stage<8>(x, keep[3], rot[3]);
+    return swap_stage<16>(x, keep[4], rot[4]);
+}
+
+constexpr int kPrepWaves = 16;
+constexpr int kPrepRounds = 4;                          // 64-rule rounds per wavefront, loads issued up front
+constexpr int kTileStride = kPrepGroups + 2;            // LDS row pitch (spreads a half-wave's rows over banks)
+static_assert(kPrepGroups == 2 * kPrepWaves * kPrepRounds, "two groups per wavefront round");
+
 // Build the chunk sets of kPrepGroups groups of one switch; validate actions.
+// Lane r of a half-wave holds rule r of a group and looks up, for each chunk,
+// the 16-bit set of chunk values its value/mask admit (a 256-entry LDS table
+// indexed by the chunk's value & mask and mask).  Two chunks share a word;
+// a 32 x 32 bit transpose over the half-wave turns the rules' admit sets
+// into the group's per-value rule sets: word (chunk c, value x) lands in lane
+// (c % 2) * 16 + x of the transpose of word c / 2.
 __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__restrict__ port_off, int64_t n_ports,
                                                   const int32_t *__restrict__ rule_off,
                                                   const pc_rule *__restrict__ rules,
@@ -109,7 +159,8 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
                                                   const int32_t *__restrict__ gofs, const int32_t *__restrict__ bofs,
                                                   uint32_t *__restrict__ filt, uint32_t *__restrict__ d_err)
 {
-    __shared__ uint32_t tile[kPlaneWords * kPrepGroups];
+    __shared__ uint32_t tile[kPlaneWords * kTileStride];
+    __shared__ uint16_t admit[256];
     const int32_t b = blockIdx.x;
     if (b >= bofs[S]) return;
     // switch owning this block: largest s with bofs[s] <= b
@@ -127,36 +178,58 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
     const bool pok = pc_range_ok(port_off[s], port_off[s + 1], n_ports);
     const int64_t np = pok ? port_off[s + 1] - port_off[s] : 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
-    const int64_t local = static_cast<int64_t>(g0 + 2 * wave) * 32 + lane;  // rule index within the switch
-    uint32_t v2 = 0, m2 = 0;
-    bool ok = local < R && (g0 + 2 * wave + (lane >> 5)) < G;
-    bool bad_action = false;
-    if (ok) {
-        const pc_rule *r = rules + rb + local;
-        v2 = r->value.w[2];
-        m2 = r->mask.w[2];
-        const uint32_t a = r->action;
-        bad_action = a != PC_ACTION_DROP && static_cast<int64_t>(a) >= np;
-    }
-    // Lane L < 32 assembles output word (chunk c, value x = L / 2) of group
-    // 2 * wave + L % 2: a rule admits value x iff, for each of the chunk's 4
-    // bits j, it admits x's bit j, so the word is the AND over j of the
-    // ballot of rules admitting 0 (or 1, following x's bit j) at bit j.
-    const bool hi_half = lane & 1;
+    // issue every round's loads before any use
+    uint32_t v2[kPrepRounds], m2[kPrepRounds], act[kPrepRounds];
+    bool ok[kPrepRounds];
 #pragma unroll
-    for (int c = 0; c < kChunks; ++c) {
-        const uint32_t v4 = (v2 >> (4 * c)) & 15u, m4 = (m2 >> (4 * c)) & 15u;
-        uint32_t word = ~0u;
-#pragma unroll
-        for (int j = 0; j < 4; ++j) {
-            const bool vj = (v4 >> j) & 1u, mj = (m4 >> j) & 1u;
-            const uint64_t b0 = __ballot(ok && !(mj && vj));  // admits bit j = 0
-            const uint64_t b1 = __ballot(ok && (!mj || vj));  // admits bit j = 1
-            const uint32_t s0 = hi_half ? static_cast<uint32_t>(b0 >> 32) : static_cast<uint32_t>(b0);
-            const uint32_t s1 = hi_half ? static_cast<uint32_t>(b1 >> 32) : static_cast<uint32_t>(b1);
-            word &= ((lane >> (1 + j)) & 1) ? s1 : s0;
+    for (int k = 0; k < kPrepRounds; ++k) {
+        const int32_t gl = 2 * (wave * kPrepRounds + k) + (lane >> 5);
+        const int64_t local = static_cast<int64_t>(g0 + gl - (lane >> 5)) * 32 + lane;  // rule index within the switch
+        ok[k] = local < R && g0 + gl < G;
+        v2[k] = m2[k] = act[k] = 0;
+        if (ok[k]) {
+            const pc_rule *r = rules + rb + local;
+            v2[k] = r->value.w[2];
+            m2[k] = r->mask.w[2];
+            act[k] = r->action;
         }
-        if (lane < 32) tile[(c * 16 + (lane >> 1)) * kPrepGroups + 2 * wave + (lane & 1)] = word;
+    }
+    // admit[(v & m) | m << 4] = set of 4-bit values y with (y & m) == (v & m)
+    if (threadIdx.x < 256) {
+        const uint32_t m = threadIdx.x >> 4, t = threadIdx.x & 15;
+        uint32_t set = 0;
+        for (uint32_t y = 0; y < 16; ++y) set |= static_cast<uint32_t>((y & m) == t) << y;
+        admit[threadIdx.x] = static_cast<uint16_t>(set);
+    }
+    // per-stage keep masks and rotations of this lane (stage j = 1, 2, 4, 8, 16)
+    uint32_t keep[5], rot[5];
+    {
+        const uint32_t blk[5] = {0x55555555u, 0x33333333u, 0x0F0F0F0Fu, 0x00FF00FFu, 0x0000FFFFu};
+#pragma unroll
+        for (int q = 0; q < 5; ++q) {
+            const bool up = (lane >> q) & 1;
+            keep[q] = up ? ~blk[q] : blk[q];
+            rot[q] = up ? (1u << q) : 32u - (1u << q);
+        }
+    }
+    __syncthreads();
+    bool bad_action = false;
+#pragma unroll
+    for (int k = 0; k < kPrepRounds; ++k) {
+        const uint32_t t2 = v2[k] & m2[k];
+        uint32_t w[kChunks / 2];
+#pragma unroll
+        for (int d = 0; d < kChunks / 2; ++d) {
+            const int c0 = 2 * d, c1 = 2 * d + 1;
+            const uint32_t i0 = ((t2 >> (4 * c0)) & 15u) | (((m2[k] >> (4 * c0)) & 15u) << 4);
+            const uint32_t i1 = ((t2 >> (4 * c1)) & 15u) | (((m2[k] >> (4 * c1)) & 15u) << 4);
+            const uint32_t a0 = ok[k] ? admit[i0] : 0u, a1 = ok[k] ? admit[i1] : 0u;
+            w[d] = transpose32(a0 | (a1 << 16), keep, rot);
+        }
+        bad_action |= ok[k] && act[k] != PC_ACTION_DROP && static_cast<int64_t>(act[k]) >= np;
+        const int gl = 2 * (wave * kPrepRounds + k) + (lane >> 5);
+#pragma unroll
+        for (int d = 0; d < kChunks / 2; ++d) tile[(32 * d + (lane & 31)) * kTileStride + gl] = w[d];
     }
     if (__ballot(bad_action) && lane == 0) atomicOr(d_err, PC_DERR_ACTION);
     __syncthreads();
@@ -164,7 +237,7 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
     for (int i = threadIdx.x; i < kPlaneWords * kPrepGroups; i += blockDim.x) {
         const int row = i / kPrepGroups, gl = i % kPrepGroups;
         const int32_t g = g0 + gl;
-        if (g < G) dst[static_cast<int64_t>(row) * G + g] = tile[i];
+        if (g < G) dst[static_cast<int64_t>(row) * G + g] = tile[row * kTileStride + gl];
     }
 }
 
@@ -713,7 +786,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_LAUNCH_CHECK(ctx);
         }
         if (prep_blocks > 0) {
-            PC_TIMED(ctx, "k_tr_prep", stream, hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(prep_blocks)), dim3(1024), 0, stream, S,
+            PC_TIMED(ctx, "k_tr_prep", stream, hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(prep_blocks)), dim3(kPrepWaves * 64), 0, stream, S,
                                port_off, n_ports, rule_off, rules, B.gcount, B.gofs, B.bofs, B.filt, ctx->d_err));
             PC_LAUNCH_CHECK(ctx);
         }
