@@ -80,9 +80,9 @@ int orc_max_threads(void)
 }
 
 /* ------------------------------------------------------------------ A1
- * Selector rows (paper: placement constraint "region=EU is among the
- * labels of the node the pod is placed on", compiled to a Kubernetes node
- * selector / affinity).  A row is a conjunction of predicates; a predicate
+ * Selector rows (paper: a placement constraint such as a residency region
+ * the chosen node must carry as a label, compiled to a Kubernetes node
+ * selector / affinity; Formal Model and Satisfaction).  A row is a conjunction of predicates; a predicate
  * names one label and an operator:
  *   In S     : the node has the label and its value is in S
  *   NotIn S  : the node lacks the label, or its value is not in S
@@ -350,9 +350,10 @@ void orc_affinity(const uint8_t *labels, int64_t N, int64_t L,
 }
 
 /* ------------------------------------------------------------------ A3
- * Trace one header through the flow tables (paper: routing constraints
- * must hold "for the realized paths induced by" the installed rules; flow
- * rules are compiled per hop along a path).  At switch s the rule that
+ * Trace one header through the flow tables (paper: a routing constraint
+ * is judged on the paths the installed rules actually realise, and flow
+ * rules are compiled per hop along a path; Formal Model and Satisfaction,
+ * Network orchestration).  At switch s the rule that
  * applies is the one of highest priority whose value agrees with the
  * header on every bit its mask cares about; equal priorities go to the
  * lower index within the switch's table.  No match: MISS.  Action 0xFFFF:

@@ -2,9 +2,9 @@
 // row x node, emitting a feasible-node bitset and a popcount per row.
 //
 // The operators are Kubernetes node-affinity's (In / NotIn / Exists over a
-// label), which is how the paper compiles a placement constraint such as
-// "region=EU is among the labels of the node the pod is placed on" (Formal
-// Model and Satisfaction, example; Service Placement Module).
+// label), which is how the paper compiles a placement constraint such as a
+// residency region that the pod's node must carry as a label (Formal Model
+// and Satisfaction, example; Service Placement Module).
 //
 // Design (gfx950):
 //   1. presence  : which values of each label occur at all.
@@ -20,10 +20,13 @@
 //   5. eval      : one row at a time per wavefront over a tile of 128 words
 //                  (two per lane, 16-byte loads and stores).  The row's
 //                  record arrives through scalar loads, so its plane loads
-//                  (L2 hits: a tile of every plane is P KiB) all go out
-//                  together with scalar offsets, followed by one output
-//                  store.  Per-lane popcounts are collected as bytes in LDS
-//                  and summed once per 64 rows; a last pass sums the tiles.
+//                  (L2 hits: a tile of every plane is P KiB), exactly as
+//                  many as its program has entries, all go out together
+//                  with scalar offsets, followed by one output store.  A
+//                  row's tiles are shifted so that stores cover whole
+//                  128-byte lines.  Per-lane popcounts are collected as
+//                  bytes in LDS and summed once per 64 rows; a last pass
+//                  sums the tiles.
 #include <algorithm>
 
 #include "pc_internal.h"
@@ -36,6 +39,7 @@ constexpr int kTileW = 64 * kWpl;  // words per tile
 constexpr int kRecWords = 16;      // row record: header + 15 inline entries
 constexpr int kInline = kRecWords - 1;
 constexpr int kGroup = 8;          // plane loads in flight together
+constexpr int kPad = 16;           // plane rows: words before column 0 (a row's shift is at most 15 words)
 
 __device__ __forceinline__ uint64_t uniform_u64(uint64_t x)
 {
@@ -124,7 +128,7 @@ __global__ __launch_bounds__(1024) void k_sel_label_scan(const uint64_t *__restr
 }
 
 // One wavefront per (64-node word w, label l): a ballot per present value.
-// Word w of plane p lives at planes[p * Wp + w].
+// Word w of plane p lives at planes[p * Wp + kPad + w].
 __global__ __launch_bounds__(256) void k_sel_planes(const uint8_t *__restrict__ labels, int32_t N, int32_t L,
                                                     const uint64_t *__restrict__ present,
                                                     const uint32_t *__restrict__ wbase, uint64_t *__restrict__ planes,
@@ -135,7 +139,7 @@ __global__ __launch_bounds__(256) void k_sel_planes(const uint8_t *__restrict__ 
     const int32_t w = blockIdx.x;
     const int32_t l = blockIdx.y * 4 + wave;
     if (l >= L) return;
-    uint64_t *col = planes + w;
+    uint64_t *col = planes + kPad + w;
     const int64_t n = static_cast<int64_t>(w) * 64 + lane;
     const uint32_t x = n < N ? labels[n * L + l] : 0x100u;  // 0x100 equals no value
     for (int k = 0; k < 4; ++k) {
@@ -255,7 +259,7 @@ __device__ __forceinline__ bool aff_valid(const pc_pred &q, int32_t L)
 __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__ pred_off,
                                                      const pc_pred *__restrict__ preds, int64_t n_preds, int32_t I,
                                                      int32_t L, const uint64_t *__restrict__ present,
-                                                     const uint32_t *__restrict__ wbase, uint32_t zero_pid,
+                                                     const uint32_t *__restrict__ wbase,
                                                      uint32_t *__restrict__ prog, uint32_t *__restrict__ rec,
                                                      uint32_t *__restrict__ d_err)
 {
@@ -313,12 +317,7 @@ __global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__
             }
         }
         if (inl) {
-            // pad to a whole group (8, or all 15 slots) with the all-zero
-            // plane, which changes no clause: evaluation then needs no
-            // per-entry bound checks
-            const int64_t padded = n == 0 ? 0 : (n <= kGroup ? kGroup : kInline);
-            for (int64_t k = n; k < padded; ++k) rr[1 + k] = zero_pid;
-            rr[0] = static_cast<uint32_t>(n);
+            rr[0] = static_cast<uint32_t>(n);  // the evaluator reads entries 1..n only
         } else {
             rr[0] = static_cast<uint32_t>(kRowIndirect);
             rr[1] = static_cast<uint32_t>(b);
@@ -401,7 +400,7 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
                                                      const int32_t *__restrict__ term_off, int32_t n_terms,
                                                      const pc_pred *__restrict__ preds, int64_t n_preds, int32_t L,
                                                      const uint64_t *__restrict__ present,
-                                                     const uint32_t *__restrict__ wbase, uint32_t zero_pid,
+                                                     const uint32_t *__restrict__ wbase,
                                                      uint32_t *__restrict__ prog, int64_t prog_cap,
                                                      unsigned long long *__restrict__ prog_used,
                                                      uint32_t *__restrict__ rec, uint8_t *__restrict__ unknown)
@@ -480,11 +479,7 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
             }
             out[k_out - 1] |= kTermEnd;
         }
-        if (inl) {
-            const int64_t padded = n <= kGroup ? kGroup : kInline;
-            for (int64_t k = n; k < padded; ++k) rr[1 + k] = zero_pid;
-            rr[0] = static_cast<uint32_t>(n);
-        }
+        if (inl) rr[0] = static_cast<uint32_t>(n);
     }
 }
 
@@ -534,7 +529,7 @@ __device__ __forceinline__ void fold(uint32_t ent, const Words &v, Words &c, Wor
 template <bool kBuf>
 struct Planes {
     __amdgpu_buffer_rsrc_t rsrc;
-    uint32_t lane_off;  // bytes: this lane's first word within a plane row
+    uint32_t lane_off;  // bytes: this lane's first word within a plane row (set per row)
     uint32_t rowbytes;  // bytes per plane row
     const uint64_t *pcol;
     int64_t Wp;
@@ -654,7 +649,7 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     const pc_pred *__restrict__ preds, const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
     const uint64_t *__restrict__ planes, int64_t plane_bytes, int64_t Wp, int32_t I, int32_t W, int32_t N,
     uint64_t *__restrict__ feasible, uint32_t *__restrict__ part, int32_t ntiles, int32_t nchunks, int32_t rpc,
-    const int32_t *__restrict__ term_off, int64_t n_preds, int32_t L)
+    const int32_t *__restrict__ term_off, int64_t n_preds, int32_t L, int32_t shift)
 {
     constexpr int kCntStride = 68;  // bytes per row of the count table (17 dwords: conflict-free column reads)
     __shared__ uint32_t cnt_lds[kEvalThreads / 64][64 * kCntStride / 4];
@@ -665,21 +660,37 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     const int32_t chunk = static_cast<int32_t>(item % nchunks);
     const int lane = threadIdx.x & 63;
     const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
-    const int32_t w0 = tile * kTileW + lane * kWpl;
-    const bool ok0 = w0 < W, ok1 = w0 + 1 < W;
+    const int32_t wt = tile * kTileW + lane * kWpl;  // this lane's first word of an unshifted row
     const uint64_t last = (N & 63) ? (1ull << (N & 63)) - 1 : ~0ull;
-    const uint64_t m0 = ok0 ? (w0 == W - 1 ? last : ~0ull) : 0ull;
-    const uint64_t m1 = ok1 ? (w0 + 1 == W - 1 ? last : ~0ull) : 0ull;
-    const int32_t wl = ok0 ? w0 : 0;  // in-bounds column for lanes past the last word
+    // word index of the bitset's start within its 128-byte line
+    const uint32_t base16 = static_cast<uint32_t>(reinterpret_cast<uintptr_t>(feasible) >> 3) & 15u;
     Planes<kBuf> pl;
     if constexpr (kBuf)
         pl.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint64_t *>(planes), static_cast<short>(0),
                                                     static_cast<int>(plane_bytes), 0x00020000);
-    pl.lane_off = static_cast<uint32_t>(wl) * 8u;
     pl.rowbytes = static_cast<uint32_t>(Wp * 8);
-    pl.pcol = planes + wl;
     pl.Wp = Wp;
-    const bool even = (W & 1) == 0;
+    // Per-row geometry.  With shift on, the tiles of row r start s(r) words
+    // early, where s(r) is the row start's word offset within its 128-byte
+    // line: every store then covers whole lines except at the row's two
+    // ends, instead of splitting a line between two tiles at every tile
+    // edge.  Lanes outside [0, W) load pad words of the plane rows and are
+    // masked.
+    int32_t w0 = 0;
+    bool ok0 = false, ok1 = false, pair = false;
+    uint64_t m0 = 0, m1 = 0;
+    auto geom = [&](int32_t r) {
+        const uint32_t rw = (static_cast<uint32_t>(r) & 15u) * (static_cast<uint32_t>(W) & 15u);  // r * W mod 16
+        const int32_t sh = shift ? static_cast<int32_t>((base16 + rw) & 15u) : 0;
+        w0 = wt - sh;
+        ok0 = w0 >= 0 && w0 < W;
+        ok1 = w0 + 1 >= 0 && w0 + 1 < W;
+        m0 = ok0 ? (w0 == W - 1 ? last : ~0ull) : 0ull;
+        m1 = ok1 ? (w0 + 1 == W - 1 ? last : ~0ull) : 0ull;
+        pair = ok0 && ok1 && ((base16 + rw + static_cast<uint32_t>(w0)) & 1u) == 0;  // 16-byte aligned pair
+        pl.lane_off = static_cast<uint32_t>(kPad + w0) * 8u;
+        pl.pcol = planes + kPad + w0;
+    };
     uint8_t *cb = reinterpret_cast<uint8_t *>(cnt_lds[wave]);
     uint32_t *prt = part + static_cast<int64_t>(tile) * I;
     const int32_t r0 = chunk * rpc;
@@ -687,26 +698,32 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     // one row: its record R (uniform, in SGPRs) -> bitset store and count byte
     auto row = [&](int32_t r, int32_t i, const uint32_t (&R)[kRecWords]) {
         const int32_t hdr = static_cast<int32_t>(R[0]);
+        geom(r);
         Words a{~0ull, ~0ull};
         Words rt{0, 0};  // affinity: OR of the finished terms
         if (hdr == kRowFalse) {
             a = Words{0, 0};
         } else if (hdr > 0) {
-            // inline program, padded with the zero plane to 8 or 15 entries
+            // inline program of hdr entries: the length is uniform, so the
+            // guards are scalar branches and only real entries are loaded
             Words c{0, 0};
             {
                 Words V[kGroup];
 #pragma unroll
-                for (int k = 0; k < kGroup; ++k) V[k] = pl(R[1 + k] & kPidMask);
+                for (int k = 0; k < kGroup; ++k)
+                    if (k < hdr) V[k] = pl(R[1 + k] & kPidMask);
 #pragma unroll
-                for (int k = 0; k < kGroup; ++k) fold<kTerms>(R[1 + k], V[k], c, a, rt);
+                for (int k = 0; k < kGroup; ++k)
+                    if (k < hdr) fold<kTerms>(R[1 + k], V[k], c, a, rt);
             }
             if (hdr > kGroup) {
                 Words V[kInline - kGroup];
 #pragma unroll
-                for (int k = 0; k < kInline - kGroup; ++k) V[k] = pl(R[1 + kGroup + k] & kPidMask);
+                for (int k = 0; k < kInline - kGroup; ++k)
+                    if (kGroup + k < hdr) V[k] = pl(R[1 + kGroup + k] & kPidMask);
 #pragma unroll
-                for (int k = 0; k < kInline - kGroup; ++k) fold<kTerms>(R[1 + kGroup + k], V[k], c, a, rt);
+                for (int k = 0; k < kInline - kGroup; ++k)
+                    if (kGroup + k < hdr) fold<kTerms>(R[1 + kGroup + k], V[k], c, a, rt);
             }
         } else if (hdr == kRowIndirect) {
             const uint32_t *pr = prog + 4 * static_cast<int64_t>(R[1]);
@@ -737,12 +754,12 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
         a.a &= m0;
         a.b &= m1;
         if constexpr (kStore) {
-            uint64_t *dst = feasible + static_cast<int64_t>(r) * W + w0;
-            if (even) {
-                if (ok0) __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(dst));
+            const int64_t at = static_cast<int64_t>(r) * W + w0;
+            if (pair) {
+                __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(feasible + at));
             } else {
-                if (ok0) __builtin_nontemporal_store(a.a, dst);
-                if (ok1) __builtin_nontemporal_store(a.b, dst + 1);
+                if (ok0) __builtin_nontemporal_store(a.a, feasible + at);
+                if (ok1) __builtin_nontemporal_store(a.b, feasible + at + 1);
             }
         }
         cb[i * kCntStride + lane] = static_cast<uint8_t>(__popcll(a.a) + __popcll(a.b));
@@ -798,6 +815,25 @@ __global__ __launch_bounds__(256) void k_sel_popsum(const uint32_t *__restrict__
 
 namespace {
 
+// Evaluator geometry for N nodes: W bitset words per row, tiles of kTileW
+// words, plane row pitch Wp.  Rows are shifted onto 128-byte lines when
+// that costs no extra tile (W of at least one tile); every lane's word
+// pair, shifted or not, lies inside [0, Wp - kPad) of a plane row.
+struct EvalGeom {
+    int64_t W, Wp, ntiles;
+    int32_t shift;
+};
+
+EvalGeom eval_geom(int32_t N)
+{
+    EvalGeom g;
+    g.W = (static_cast<int64_t>(N) + 63) / 64;
+    g.ntiles = (g.W + kTileW - 1) / kTileW;
+    g.shift = g.W >= kTileW && (g.W + 15 + kTileW - 1) / kTileW == g.ntiles;
+    g.Wp = kPad + g.ntiles * kTileW;
+    return g;
+}
+
 // Value planes of the node labels: presence, plane numbering (d_P = P),
 // the planes themselves, and the all-zero plane pmax.
 int build_planes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, int64_t W, int64_t Wp, int64_t pmax,
@@ -840,7 +876,7 @@ int launch_eval(pc_ctx *ctx, const uint32_t *rec, const uint32_t *prog, const in
                 const pc_pred *preds, const uint64_t *present, const uint32_t *wbase, const uint64_t *planes,
                 int64_t pmax, int64_t Wp, int32_t I, int64_t W, int32_t N, uint64_t *feasible, uint32_t *popcnt,
                 uint32_t *part, int64_t ntiles, const int32_t *term_off, int64_t n_preds, int32_t L,
-                hipStream_t stream)
+                int32_t shift, hipStream_t stream)
 {
     // about 4096 workgroups; a chunk is a whole number of 256-row passes
     int64_t nchunks = std::max<int64_t>((4096 + ntiles - 1) / ntiles, 1);
@@ -856,7 +892,7 @@ int launch_eval(pc_ctx *ctx, const uint32_t *rec, const uint32_t *prog, const in
                  hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, off, preds,
                                     present, wbase, planes, pbytes, Wp, I, static_cast<int32_t>(W), N, feasible,
                                     cnt_out, static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
-                                    static_cast<int32_t>(rpc), term_off, n_preds, L));
+                                    static_cast<int32_t>(rpc), term_off, n_preds, L, shift));
     };
     if (!feasible) {
         if (pbytes < (int64_t(1) << 31)) eval(k_sel_eval<true, kTerms, false>);  // buffer offsets are 32-bit
@@ -881,9 +917,8 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
                   const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
                   hipStream_t stream)
 {
-    const int64_t W = (static_cast<int64_t>(N) + 63) / 64;
-    const int64_t Wp = (W + 1) / 2 * 2;  // even: 16-byte aligned plane rows
-    const int64_t ntiles = (W + kTileW - 1) / kTileW;
+    const EvalGeom geo = eval_geom(N);
+    const int64_t W = geo.W, Wp = geo.Wp, ntiles = geo.ntiles;
     const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
     const size_t plane_bytes = static_cast<size_t>(pmax + 1) * static_cast<size_t>(Wp) * 8;
     if (plane_bytes > (size_t(64) << 30))
@@ -914,20 +949,19 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
     PC_TIMED(ctx, "k_sel_compile", stream,
              hipLaunchKernelGGL(k_sel_compile, dim3(rgrid), dim3(256), 0, stream, pred_off, preds, n_preds, I, L,
-                                present, wbase, static_cast<uint32_t>(pmax), prog, rec, ctx->d_err));
+                                present, wbase, prog, rec, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     if (W == 0) return PC_OK;
     return launch_eval<false>(ctx, rec, prog, pred_off, preds, present, wbase, planes, pmax, Wp, I, W, N, feasible,
-                              popcnt, part, ntiles, nullptr, n_preds, L, stream);
+                              popcnt, part, ntiles, nullptr, n_preds, L, geo.shift, stream);
 }
 
 int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off, int32_t I,
                  const int32_t *term_off, int32_t n_terms, const pc_pred *preds, int64_t n_preds, uint64_t *feasible,
                  uint32_t *popcnt, uint8_t *unknown, hipStream_t stream)
 {
-    const int64_t W = (static_cast<int64_t>(N) + 63) / 64;
-    const int64_t Wp = (W + 1) / 2 * 2;
-    const int64_t ntiles = (W + kTileW - 1) / kTileW;
+    const EvalGeom geo = eval_geom(N);
+    const int64_t W = geo.W, Wp = geo.Wp, ntiles = geo.ntiles;
     const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
     const size_t plane_bytes = static_cast<size_t>(pmax + 1) * static_cast<size_t>(Wp) * 8;
     if (plane_bytes > (size_t(64) << 30))
@@ -973,10 +1007,10 @@ int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
     PC_TIMED(ctx, "k_aff_compile", stream,
              hipLaunchKernelGGL(k_aff_compile, dim3(rgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
-                                preds, n_preds, L, present, wbase, static_cast<uint32_t>(pmax), prog, prog_cap,
+                                preds, n_preds, L, present, wbase, prog, prog_cap,
                                 prog_used, rec, unknown));
     PC_LAUNCH_CHECK(ctx);
     if (W == 0) return PC_OK;
     return launch_eval<true>(ctx, rec, prog, row_off, preds, present, wbase, planes, pmax, Wp, I, W, N, feasible,
-                             popcnt, part, ntiles, term_off, n_preds, L, stream);
+                             popcnt, part, ntiles, term_off, n_preds, L, geo.shift, stream);
 }

@@ -2,9 +2,9 @@
 // hop by hop through the per-switch, priority-ordered ternary flow tables
 // and collect the jurisdictions visited.
 //
-// The paper compiles every path "into per-hop flow rules" (Network
-// orchestration) and a routing constraint must hold "for the realized paths
-// induced by" them (Formal Model and Satisfaction, condition (ii)); the
+// The paper compiles every path into one flow rule per hop (Network
+// orchestration), and a routing constraint is judged on the paths those
+// rules actually realise (Formal Model and Satisfaction, condition (ii)); the
 // validator checks that realised paths avoid forbidden switches (validator
 // check definition).  The first-match rule order (larger priority, then
 // lower index), table miss, drop, egress and TTL are the readings written in

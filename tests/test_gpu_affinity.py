@@ -67,7 +67,7 @@ def _csr(rows):
     return np.array(row_off, np.int32), np.array(term_off, np.int32), arr
 
 
-@pytest.mark.parametrize("seed,N,absent", [(0, 5037, 0.1), (1, 20000 + 5, 0.0), (2, 100, 0.3)])
+@pytest.mark.parametrize("seed,N,absent", [(0, 5037, 0.1), (1, 20000 + 5, 0.0), (2, 100, 0.3), (3, 64 * 781 - 40, 0.05)])
 def test_affinity_random(g, orc, seed, N, absent):
     wl = synth.affinity_workload(seed, N, 12, 900, card_choices=(2, 3, 16, 64, 200), absent_p=absent,
                                  tmin=0, tmax=4, kmin=0, kmax=5)

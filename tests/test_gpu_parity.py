@@ -153,6 +153,33 @@ def test_selectors_program_lengths(g, orc):
     _same(pg, po, "popcnt")
 
 
+# (W, ragged bits, output offset in words): odd and even widths whose rows
+# are shifted onto 128-byte lines (W = 200, 263, 781, 1000), widths where
+# the shift would cost a tile and is off (W = 128, 255), and outputs that
+# start 8 and 24 bytes into a line
+@pytest.mark.parametrize("W,ragged,offset", [(200, 0, 0), (263, 17, 1), (781, 63, 3), (1000, 5, 0), (128, 1, 1),
+                                             (255, 0, 3)])
+def test_selectors_line_shifted_rows(g, orc, W, ragged, offset):
+    """Every bitset word written exactly once, at its place, with the
+    guard words around the output untouched."""
+    import torch
+
+    import paper_2602_16100_amd as pc
+    N = 64 * W - ragged
+    wl = synth.selector_workload(30 + W, N, 10, 333)
+    fo, po, _ = orc.selectors(wl["labels"], wl["pred_off"], wl["preds"])
+    I = wl["pred_off"].shape[0] - 1
+    guard = np.int64(0x5A5A5A5A5A5A5A5A)
+    buf = torch.full((I * W + offset + 8,), int(guard), dtype=torch.int64, device="cuda")
+    out = buf[offset:offset + I * W].view(I, W)
+    f, p = pc.pc_eval_selectors(g.dev(wl["labels"]), g.dev(wl["pred_off"]), g.dev(wl["preds"]), feasible=out)
+    torch.cuda.synchronize()
+    _same(f.cpu().numpy().view(np.uint64), fo, "feasible")
+    _same(p.cpu().numpy().view(np.uint32), po, "popcnt")
+    b = buf.cpu().numpy()
+    assert (b[:offset] == guard).all() and (b[offset + I * W:] == guard).all()
+
+
 def test_selectors_malformed_flags(g, orc):
     import paper_2602_16100_amd as pc
     wl = synth.selector_workload(9, 777, 6, 40)
