@@ -25,28 +25,41 @@ sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
 
-# HBM bytes per launch of k_sel_eval and k_aff_eval on the combined
-# workload's cluster, from one rocprofv3 FETCH_SIZE pass and one WRITE_SIZE
+# HBM bytes per launch of k_sel_eval, k_aff_eval and k_tr_prep on the
+# combined workload, from one rocprofv3 FETCH_SIZE pass and one WRITE_SIZE
 # pass each, scaled by what the same counter reads for a plain copy of known
 # size (the command lines and counter values are in
-# profiles/k_sel_eval_cfg5_hbm_counters.md).  Valid only for the kernel
-# source they were measured on.
-TRAFFIC = {"source": "paper_2602_16100_amd/csrc/select.hip",
-           "sha256": "371dd8d7b186ef479b49591944e2ceeb6c4482da9b2382b26bfd9f1a17c8aefc",
-           "workload": "cfg5",
-           "bytes_per_launch": {"k_sel_eval": 797_446_228 + 4_473_979_605,
-                                "k_aff_eval": 1_022_856_675 + 4_474_095_445}}
+# profiles/k_sel_eval_k_tr_prep_cfg5_hbm_counters.md).  Valid only for the
+# kernel source they were measured on.
+TRAFFIC = [
+    {"source": "paper_2602_16100_amd/csrc/select.hip",
+     "sha256": "5a444dbfbad2db5b7080ccdafaaa0faf79466936387b1984bed94de82635650f",
+     "workload": "cfg5",
+     "bytes_per_launch": {"k_sel_eval": 680_736_487 + 4_407_304_352,
+                          "k_aff_eval": 848_143_452 + 4_408_032_469}},
+    {"source": "paper_2602_16100_amd/csrc/trace.hip",
+     "sha256": "6cfbabb1a16a04cf28056056d64a124a62c7a8e7a53ee4fe9df74423cbda63d5",
+     "workload": "cfg5",
+     "bytes_per_launch": {"k_tr_prep": 1_888_506_195 + 566_231_040}},
+]
 
 
 def measured_traffic(workload, kernel):
+    """HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE counter runs
+    (scaled by a plain copy's readings), or None when the kernel's source
+    has changed since they were taken."""
     import hashlib
-    path = os.path.join(ROOT, TRAFFIC["source"])
-    if workload != TRAFFIC["workload"] or not os.path.exists(path):
-        return None
-    with open(path, "rb") as f:
-        if hashlib.sha256(f.read()).hexdigest() != TRAFFIC["sha256"]:
+    for t in TRAFFIC:
+        if kernel not in t["bytes_per_launch"]:
+            continue
+        path = os.path.join(ROOT, t["source"])
+        if workload != t["workload"] or not os.path.exists(path):
             return None
-    return TRAFFIC["bytes_per_launch"].get(kernel)
+        with open(path, "rb") as f:
+            if hashlib.sha256(f.read()).hexdigest() != t["sha256"]:
+                return None
+        return t["bytes_per_launch"][kernel]
+    return None
 
 
 def parse():
@@ -695,6 +708,7 @@ def main():
         prep_gbs = prep_bytes / (prep_avg * 1e-3) / 1e9 if prep_avg > 0 else 0.0
         line["trace_prep_roofline"] = {"kernel": "k_tr_prep", "bound": "hbm", "achieved": prep_gbs,
                                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": prep_gbs / HBM_PEAK_GBS,
+                                       "traffic": measured_traffic(args.workload, "k_tr_prep"),
                                        "alg_bytes_per_launch": prep_bytes, "avg_launch_ms": prep_avg}
     if only == "all" and not args.no_paths:
         line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)

@@ -878,10 +878,12 @@ int launch_eval(pc_ctx *ctx, const uint32_t *rec, const uint32_t *prog, const in
                 uint32_t *part, int64_t ntiles, const int32_t *term_off, int64_t n_preds, int32_t L,
                 int32_t shift, hipStream_t stream)
 {
-    // about 4096 workgroups; a chunk is a whole number of 256-row passes
-    int64_t nchunks = std::max<int64_t>((4096 + ntiles - 1) / ntiles, 1);
+    // about 32,768 workgroups (many per workgroup slot of the chip, so the
+    // last wave of workgroups is short); a chunk is a whole number of
+    // 64-row batches
+    int64_t nchunks = std::max<int64_t>((32768 + ntiles - 1) / ntiles, 1);
     int64_t rpc = (I + nchunks - 1) / nchunks;
-    rpc = (rpc + kEvalThreads - 1) / kEvalThreads * kEvalThreads;
+    rpc = (rpc + 63) / 64 * 64;
     nchunks = (I + rpc - 1) / rpc;
     const int64_t total = ntiles * nchunks;
     const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
