@@ -55,6 +55,7 @@ def _load():
         C = ctypes.c_int
         _lib.orc_selectors.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
         _lib.orc_affinity.argtypes = [P, I64, I64, P, I64, P, I64, P, I64, P, I64, P, P, P, P, C]
+        _lib.orc_preferred.argtypes = [P, I64, I64, P, P, I64, P, I64, P, P, I64, P, I64, P, P, P, P, C]
         _lib.orc_update_nodes.argtypes = [P, I64, I64, P, P, I64, I64, P, I64, P, P, P, C]
         _lib.orc_probes.argtypes = [P, I64, I64, P, P, I64, I64, P, P, I64, P, P]
         _lib.orc_synthesize.argtypes = [I64, P, P, I64, P, P, I64, P, P, P, P, I64, P, I64, P, P, I64, I64, P,
@@ -154,6 +155,35 @@ def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None, rows=
                      _p(np.ascontiguousarray(term_off, np.int32)), n_terms, _p(np.ascontiguousarray(preds)),
                      n_preds, _p(rows), rows.shape[0], _p(feas), _p(pc), _p(unk), _p(err), nthreads)
     return feas, pc, unk, int(err[0])
+
+
+def preferred(labels, row_off, term_off, weight, preds, feasible=None, n_terms=None, n_preds=None, rows=None,
+              nthreads=0):
+    """Preferred node affinity: per row the feasible node of largest summed
+    weight of holding terms (lowest index among equals; -1 when no node is
+    feasible), that score and the number of feasible nodes reaching it.
+    feasible: [I, W] u64 bitset or None (every node).  Returns (best int32,
+    score u32, count u32, flags)."""
+    lib = _load()
+    labels = np.ascontiguousarray(labels, np.uint8)
+    N, L = labels.shape
+    I = row_off.shape[0] - 1
+    n_terms = term_off.shape[0] - 1 if n_terms is None else n_terms
+    n_preds = preds.shape[0] if n_preds is None else n_preds
+    if rows is None:
+        rows = np.arange(I, dtype=np.int32)
+    rows = np.ascontiguousarray(rows, np.int32)
+    nr = rows.shape[0]
+    best = np.zeros(nr, np.int32)
+    score = np.zeros(nr, np.uint32)
+    count = np.zeros(nr, np.uint32)
+    err = np.zeros(1, np.uint32)
+    fz = None if feasible is None else np.ascontiguousarray(feasible, np.uint64)
+    lib.orc_preferred(_p(labels), N, L, None if fz is None else _p(fz), _p(np.ascontiguousarray(row_off, np.int32)),
+                      I, _p(np.ascontiguousarray(term_off, np.int32)), n_terms,
+                      _p(np.ascontiguousarray(weight, np.uint32)), _p(np.ascontiguousarray(preds)), n_preds,
+                      _p(rows), nr, _p(best), _p(score), _p(count), _p(err), nthreads)
+    return best, score, count, int(err[0])
 
 
 def synthesize(V, port_off, port_peer, region, src, target, allowed, via, forbid, key, out_port, prio, max_hops,

@@ -349,6 +349,86 @@ void orc_affinity(const uint8_t *labels, int64_t N, int64_t L,
     }
 }
 
+/* ------------------------------------------------------------------ A1
+ * Preferred node affinity: the secondary objective of placement (paper:
+ * among the configurations that satisfy an intent, choose one that is
+ * best for secondary objectives; Problem Definition, item 3), in the
+ * Kubernetes form of weighted preferred terms (affinity rules of the
+ * Placement Directives and the Service Placement Module).
+ *   Row i owns the weighted terms row_off[i] .. row_off[i+1]; term t has
+ *   weight weight[t] (1..100) and the expressions term_off[t] ..
+ *   term_off[t+1], which hold as for required affinity (all of them must
+ *   hold; a term without expressions holds for no node).
+ *   score(i, n) = sum of the weights of row i's terms that hold for node n.
+ *   Among the row's feasible nodes (bit n of feasible row i, or every node
+ *   when feasible is NULL) the best node is the one of largest score, the
+ *   lowest index among equal scores.  Reported per row: that node (-1 when
+ *   no node is feasible), its score and the number of feasible nodes with
+ *   that score (both 0 when no node is feasible).
+ * Malformed: a weight outside 1..100 -> the term holds for no node
+ * (F_PRED, any term); a malformed expression -> its term holds for no node
+ * (F_PRED, as for required affinity); a bad term offset pair -> the term
+ * holds for no node; a bad row offset pair or a row of more than
+ * O_PREF_MAX_TERMS terms -> the row has no terms (F_OFFSETS, any row).
+ */
+enum { O_PREF_MAX_TERMS = 655 };
+
+static int pref_row_ok(const int32_t *row_off, int64_t i, int64_t n_terms)
+{
+    return range_ok(row_off[i], row_off[i + 1], n_terms) && row_off[i + 1] - row_off[i] <= O_PREF_MAX_TERMS;
+}
+
+static int pref_term_holds(const uint8_t *lab, int64_t L, const int32_t *term_off, const uint32_t *weight,
+                           const o_pred *preds, int64_t n_preds, int64_t t)
+{
+    const int64_t b = term_off[t], e = term_off[t + 1];
+    if (weight[t] < 1 || weight[t] > 100 || !range_ok(b, e, n_preds) || b == e) return 0;
+    for (int64_t p = b; p < e; ++p)
+        if (!aff_valid(&preds[p], L) || !aff_holds(&preds[p], lab[preds[p].label])) return 0;
+    return 1;
+}
+
+void orc_preferred(const uint8_t *labels, int64_t N, int64_t L, const uint64_t *feasible,
+                   const int32_t *row_off, int64_t I, const int32_t *term_off, int64_t n_terms,
+                   const uint32_t *weight, const o_pred *preds, int64_t n_preds, const int32_t *rows,
+                   int64_t nrows, int32_t *best, uint32_t *score, uint32_t *count, uint32_t *err, int nthreads)
+{
+    const int64_t W = (N + 63) / 64;
+    set_threads(nthreads);
+    for (int64_t t = 0; t < n_terms; ++t) {
+        if (weight[t] < 1 || weight[t] > 100) *err |= F_PRED;
+        if (!range_ok(term_off[t], term_off[t + 1], n_preds)) { *err |= F_OFFSETS; continue; }
+        for (int64_t p = term_off[t]; p < term_off[t + 1]; ++p)
+            if (!aff_valid(&preds[p], L)) *err |= F_PRED;
+    }
+    for (int64_t i = 0; i < I; ++i)
+        if (!pref_row_ok(row_off, i, n_terms)) *err |= F_OFFSETS;
+#pragma omp parallel for schedule(dynamic, 1)
+    for (int64_t r = 0; r < nrows; ++r) {
+        const int64_t i = rows[r];
+        const int ok = pref_row_ok(row_off, i, n_terms);
+        const int64_t tb = ok ? row_off[i] : 0, te = ok ? row_off[i + 1] : 0;
+        int64_t b_node = -1;
+        uint32_t b_score = 0, b_count = 0;
+        for (int64_t n = 0; n < N; ++n) {
+            if (feasible && !((feasible[i * W + (n >> 6)] >> (n & 63)) & 1)) continue;
+            uint32_t sc = 0;
+            for (int64_t t = tb; t < te; ++t)
+                if (pref_term_holds(labels + n * L, L, term_off, weight, preds, n_preds, t)) sc += weight[t];
+            if (b_node < 0 || sc > b_score) {
+                b_node = n;
+                b_score = sc;
+                b_count = 1;
+            } else if (sc == b_score) {
+                ++b_count;
+            }
+        }
+        best[r] = (int32_t)b_node;
+        score[r] = b_score;
+        count[r] = b_count;
+    }
+}
+
 /* ------------------------------------------------------------------ A3
  * Trace one header through the flow tables (paper: a routing constraint
  * is judged on the paths the installed rules actually realise, and flow

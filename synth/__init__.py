@@ -239,6 +239,17 @@ def affinity_rows(seed, cards, I, tmin=1, tmax=3, kmin=1, kmax=4):
     return gen_affinity(np.random.default_rng([seed, 12]), I, cards, tmin, tmax, kmin, kmax)
 
 
+def preferred_rows(seed, cards, I, tmin=1, tmax=3, kmin=1, kmax=3):
+    """I preferred-affinity rows over a cluster whose labels have the given
+    cardinalities, from their own generator [seed, 15]: terms and
+    expressions as gen_affinity, and one weight per term, uniform over the
+    Kubernetes range 1..100.  Returns (row_off, term_off, preds, weight)."""
+    rng = np.random.default_rng([seed, 15])
+    row_off, term_off, preds = gen_affinity(rng, I, cards, tmin, tmax, kmin, kmax)
+    weight = rng.integers(1, 101, size=term_off.shape[0] - 1).astype(np.uint32)
+    return row_off, term_off, preds, weight
+
+
 def gen_preds_holding(rng, labels, cards, a, b, kmin, kmax, mmax=4):
     """Selector rows built so that nodes a[r] and b[r] satisfy row r: In sets
     contain both endpoints' values, NotIn sets avoid them (a NotIn with no
