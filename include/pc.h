@@ -25,6 +25,8 @@
  *                         Configuration; must_go / forbidden lists).
  *   - pc_eval_affinity  : placement with full node affinity (OR-ed terms,
  *                         six operators, label-inventory flags).
+ *   - pc_score_preferred : the best feasible node under weighted preferred
+ *                         terms (secondary placement objectives).
  *   - pc_synthesize_paths : the step before validation -- the path
  *                         scheduler's search for a compliant path and its
  *                         compilation into per-hop flow rules.
@@ -59,7 +61,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 6
+#define PC_VERSION 7
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -263,6 +265,44 @@ int pc_eval_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L,
 int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off,
                      int32_t I, const int32_t *term_off, int32_t n_terms, const pc_pred *preds, int64_t n_preds,
                      uint64_t *feasible, uint32_t *popcnt, uint8_t *unknown, void *stream);
+
+/*
+ * A1, preferred node affinity -- the secondary objective of placement:
+ * among the configurations that satisfy an intent, one that is best for
+ * secondary objectives (paper: Problem Definition, item 3), in the
+ * Kubernetes form of weighted preferred terms (affinity rules of the
+ * placement directives; Service Placement Module).  Row i owns the terms
+ * row_off[i] .. row_off[i+1]; term t has weight weight[t] (1..100) and the
+ * expressions term_off[t] .. term_off[t+1], which hold as in
+ * pc_eval_affinity (all of them; a term with no expressions holds for no
+ * node).  score(i, n) = sum of the weights of row i's terms that hold for
+ * node n.  Among the row's feasible nodes the best node has the largest
+ * score, the lowest index among equal scores.
+ * labels     : uint8 [N][L], node-major; PC_LABEL_ABSENT = absent.
+ * feasible   : uint64 [I][W], W = ceil(N/64), as written by pc_eval_affinity
+ *              or pc_eval_selectors (bits past N are ignored); NULL = every
+ *              node is feasible.
+ * row_off    : int32 [I+1]; term_off : int32 [n_terms+1];
+ * weight     : uint32 [n_terms]; preds : pc_pred [n_preds].
+ * best_node  : int32 [I], the best feasible node, -1 when none is feasible.
+ * best_score : uint32 [I], its score (0 when none).
+ * n_best     : uint32 [I], the number of feasible nodes with that score (0
+ *              when none).
+ * All arrays are device memory owned by the caller.  Limits: 0 <= N,
+ * 1 <= L <= 65535 (L = 0 allowed when no expression exists), 0 <= I,
+ * 0 <= n_terms, 0 <= n_preds.  Malformed data: a weight outside 1..100 or
+ * a malformed expression (as pc_eval_affinity) makes its term hold for no
+ * node (PC_DERR_PRED, raised for any such term, and for any such
+ * expression inside a term with a valid offset pair); a bad term offset
+ * pair empties the term; a bad row offset pair or a row of more than
+ * PC_PREF_MAX_TERMS terms leaves the row without terms, every score 0
+ * (PC_DERR_OFFSETS).
+ */
+#define PC_PREF_MAX_TERMS 655
+int pc_score_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const uint64_t *feasible,
+                       const int32_t *row_off, int32_t I, const int32_t *term_off, int32_t n_terms,
+                       const uint32_t *weight, const pc_pred *preds, int64_t n_preds, int32_t *best_node,
+                       uint32_t *best_score, uint32_t *n_best, void *stream);
 
 /*
  * A2+A3+A4 -- routing constraints on realised paths.  Each trace t starts at

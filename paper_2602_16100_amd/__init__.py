@@ -83,6 +83,7 @@ def lib():
     L.pc_data_errors.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32), C]
     L.pc_eval_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
     L.pc_eval_affinity.argtypes = [P, P, I32, I32, P, I32, P, I32, P, I64, P, P, P, P]
+    L.pc_score_preferred.argtypes = [P, P, I32, I32, P, P, I32, P, I32, P, P, I64, P, P, P, P]
     L.pc_update_nodes.argtypes = [P, P, I32, I32, P, P, I64, I32, P, I32, P, P, P]
     L.pc_eval_selectors_count.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P]
     L.pc_probe_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, I32, P, P]
@@ -105,7 +106,8 @@ def lib():
 EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_errors", "pc_profile",
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
             "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths",
-            "pc_update_nodes", "pc_eval_selectors_count", "pc_probe_selectors", "pc_report_counts")
+            "pc_update_nodes", "pc_eval_selectors_count", "pc_probe_selectors", "pc_report_counts",
+            "pc_score_preferred")
 
 
 class Context:
@@ -250,6 +252,36 @@ def pc_eval_affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=Non
                                      _ptr(feasible) if feasible.numel() else None,
                                      _ptr(popcnt) if I else None, _ptr(unknown) if I else None, _stream(stream)))
     return feasible, popcnt, unknown
+
+
+def pc_score_preferred(labels, row_off, term_off, weight, preds, feasible=None, n_terms=None, n_preds=None,
+                       best=None, score=None, count=None, ctx=None, stream=None):
+    """A1 preferred node affinity: per row the feasible node of largest summed
+    weight of holding terms (lowest index among equals), its score and the
+    number of feasible nodes with that score.  feasible: [I, ceil(N/64)]
+    int64 storage of the bitset, or None (every node).  Returns (best int32
+    [I] (-1: none feasible), score [I] and count [I], int32 storage of
+    uint32)."""
+    ctx = ctx or context()
+    N, L = (int(labels.shape[0]), int(labels.shape[1])) if labels.dim() == 2 else (0, 0)
+    I = int(row_off.shape[0]) - 1
+    n_terms = int(term_off.shape[0]) - 1 if n_terms is None else int(n_terms)
+    n_preds = int(preds.shape[0]) if n_preds is None else int(n_preds)
+    dev = row_off.device
+    if best is None:
+        best = torch.empty(I, dtype=torch.int32, device=dev)
+    if score is None:
+        score = torch.empty(I, dtype=torch.int32, device=dev)
+    if count is None:
+        count = torch.empty(I, dtype=torch.int32, device=dev)
+    ctx.check(lib().pc_score_preferred(ctx.handle, _ptr(labels) if labels.numel() else None, N, L,
+                                       _ptr(feasible) if feasible is not None and feasible.numel() else None,
+                                       _ptr(row_off), I, _ptr(term_off), n_terms,
+                                       _ptr(weight) if weight.numel() else None,
+                                       _ptr(preds) if preds.numel() else None, n_preds,
+                                       _ptr(best) if I else None, _ptr(score) if I else None,
+                                       _ptr(count) if I else None, _stream(stream)))
+    return best, score, count
 
 
 def pc_eval_selectors_count(labels, pred_off, preds, n_preds=None, popcnt=None, ctx=None, stream=None):

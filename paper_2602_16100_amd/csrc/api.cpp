@@ -238,6 +238,29 @@ int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, c
                         unknown, static_cast<hipStream_t>(stream));
 }
 
+int pc_score_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const uint64_t *feasible,
+                       const int32_t *row_off, int32_t I, const int32_t *term_off, int32_t n_terms,
+                       const uint32_t *weight, const pc_pred *preds, int64_t n_preds, int32_t *best_node,
+                       uint32_t *best_score, uint32_t *n_best, void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(N >= 0 && I >= 0 && n_terms >= 0 && n_preds >= 0,
+               "pc_score_preferred: negative size (N=%d I=%d n_terms=%d n_preds=%lld)", N, I, n_terms,
+               (long long)n_preds);
+    PC_REQUIRE(L >= 0 && L <= 65535, "pc_score_preferred: L=%d out of [0, 65535]", L);
+    PC_REQUIRE(L > 0 || n_preds == 0, "pc_score_preferred: L=0 with expressions");
+    PC_REQUIRE(I == 0 || (row_off && best_node && best_score && n_best),
+               "pc_score_preferred: null row_off/best_node/best_score/n_best");
+    PC_REQUIRE(term_off, "pc_score_preferred: null term_off");
+    PC_REQUIRE(n_terms == 0 || weight, "pc_score_preferred: null weight");
+    PC_REQUIRE(n_preds == 0 || preds, "pc_score_preferred: null preds");
+    PC_REQUIRE(N == 0 || L == 0 || labels, "pc_score_preferred: null labels");
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_preferred(ctx, labels, N, L, feasible, row_off, I, term_off, n_terms, weight, preds, n_preds,
+                         best_node, best_score, n_best, static_cast<hipStream_t>(stream));
+}
+
 int pc_eval_selectors_count(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                             const pc_pred *preds, int64_t n_preds, int32_t I, uint32_t *popcnt, void *stream)
 {

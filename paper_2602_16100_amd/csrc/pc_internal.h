@@ -95,6 +95,10 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
 int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off, int32_t I,
                  const int32_t *term_off, int32_t n_terms, const pc_pred *preds, int64_t n_preds, uint64_t *feasible,
                  uint32_t *popcnt, uint8_t *unknown, hipStream_t stream);
+int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const uint64_t *feasible,
+                  const int32_t *row_off, int32_t I, const int32_t *term_off, int32_t n_terms, const uint32_t *weight,
+                  const pc_pred *preds, int64_t n_preds, int32_t *best, uint32_t *score, uint32_t *count,
+                  hipStream_t stream);
 
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,

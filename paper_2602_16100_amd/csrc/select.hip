@@ -811,6 +811,334 @@ __global__ __launch_bounds__(256) void k_sel_popsum(const uint32_t *__restrict__
     popcnt[r] = s;
 }
 
+// ---------------------------------------------------------------- preferred
+// Preferred node affinity: per row, weighted terms (weight 1..100, terms as
+// in required affinity); a node's score is the sum of the weights of the
+// terms that hold for it; the best feasible node has the largest score, the
+// lowest index among equal scores.  Scores are kept bit-sliced: bit b of
+// every node's score of a 64-node word is one 64-bit word, so adding a
+// term's weight to the nodes where it holds is a ripple add over the score
+// bits, and the maximum over a word's nodes is found from the top bit down.
+constexpr int kScoreBits = 16;         // 655 terms of weight <= 100 stay below 2^16
+constexpr int32_t kPrefMaxTerms = 655;
+constexpr uint32_t kPrefLenBits = 24;  // term header: weight << 24 | program entries
+enum : uint32_t { kPrefProgram = 0, kPrefNone = 1, kPrefDecode = 2 };
+constexpr int kPrefRec = 4;            // row record: program offset, live terms, score bits, kind
+
+__device__ __forceinline__ bool pref_weight_ok(uint32_t w) { return w >= 1 && w <= 100; }
+
+__device__ __forceinline__ bool pref_row_ok(const int32_t *__restrict__ row_off, int64_t i, int32_t n_terms)
+{
+    const int64_t b = row_off[i], e = row_off[i + 1];
+    return pc_range_ok(b, e, n_terms) && e - b <= kPrefMaxTerms;
+}
+
+__device__ __forceinline__ uint32_t bit_length(uint32_t x) { return x ? 32u - __builtin_clz(x) : 0u; }
+
+// Input sweep: the data-error flags are properties of the whole input.
+// PRED for a weight outside 1..100 or a malformed expression inside a term
+// with a valid offset pair; OFFSETS for a bad term or row offset pair or a
+// row of more than kPrefMaxTerms terms.
+__global__ __launch_bounds__(256) void k_pref_validate(const int32_t *__restrict__ row_off, int32_t I,
+                                                       const int32_t *__restrict__ term_off, int32_t n_terms,
+                                                       const uint32_t *__restrict__ weight,
+                                                       const pc_pred *__restrict__ preds, int64_t n_preds, int32_t L,
+                                                       uint32_t *__restrict__ d_err)
+{
+    uint32_t errs = 0;
+    const int64_t tot = I > n_terms ? I : n_terms;
+    for (int64_t x = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; x < tot;
+         x += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        if (x < n_terms) {
+            if (!pref_weight_ok(weight[x])) errs |= PC_DERR_PRED;
+            const int64_t b = term_off[x], e = term_off[x + 1];
+            if (!pc_range_ok(b, e, n_preds)) {
+                errs |= PC_DERR_OFFSETS;
+            } else {
+                for (int64_t p = b; p < e; ++p)
+                    if (!aff_valid(preds[p], L)) {
+                        errs |= PC_DERR_PRED;
+                        break;
+                    }
+            }
+        }
+        if (x < I && !pref_row_ok(row_off, x, n_terms)) errs |= PC_DERR_OFFSETS;
+    }
+    if (errs) atomicOr(d_err, errs);
+}
+
+// One thread per row: the row's live terms (weight in range, and able to
+// hold somewhere) as a program of term headers, each followed by its clause
+// entries (kLast / kNeg as in selector programs), in a slice of prog taken
+// through a bump counter.  When the slice does not fit, or a term has more
+// than 2^24 entries, the row is decoded at evaluation time.
+__global__ __launch_bounds__(256) void k_pref_compile(const int32_t *__restrict__ row_off, int32_t I,
+                                                      const int32_t *__restrict__ term_off, int32_t n_terms,
+                                                      const uint32_t *__restrict__ weight,
+                                                      const pc_pred *__restrict__ preds, int64_t n_preds, int32_t L,
+                                                      const uint64_t *__restrict__ present,
+                                                      const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog,
+                                                      int64_t prog_cap, unsigned long long *__restrict__ prog_used,
+                                                      uint32_t *__restrict__ rec)
+{
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
+        uint32_t *rr = rec + static_cast<int64_t>(i) * kPrefRec;
+        rr[0] = rr[1] = rr[2] = 0;
+        rr[3] = kPrefNone;
+        if (!pref_row_ok(row_off, i, n_terms)) continue;
+        const int64_t tb = row_off[i], te = row_off[i + 1];
+        int64_t n = 0;
+        uint32_t live = 0, sum = 0;
+        bool decode = false;
+        for (int64_t t = tb; t < te; ++t) {
+            int64_t len;
+            if (!pref_weight_ok(weight[t]) || !aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len))
+                continue;
+            if (len >= (int64_t(1) << kPrefLenBits)) decode = true;
+            n += 1 + len;
+            sum += weight[t];
+            ++live;
+        }
+        if (live == 0) continue;
+        rr[1] = live;
+        rr[2] = bit_length(sum);
+        if (!decode) {
+            const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>(n));
+            decode = static_cast<int64_t>(off) + n > prog_cap;
+            if (!decode) {
+                uint32_t *out = prog + off;
+                int64_t k_out = 0;
+                for (int64_t t = tb; t < te; ++t) {
+                    const int64_t b = term_off[t], e = term_off[t + 1];
+                    int64_t len;
+                    if (!pref_weight_ok(weight[t]) || !aff_term(preds, b, e, n_preds, L, present, len)) continue;
+                    out[k_out++] = weight[t] << kPrefLenBits | static_cast<uint32_t>(len);
+                    for (int64_t p = b; p < e; ++p) {
+                        const pc_pred q = preds[p];
+                        const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+                        const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+                        uint64_t sel[4];
+                        bool neg;
+                        uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
+                        for (int k = 0; k < 4; ++k) {
+                            uint64_t m = sel[k];
+                            while (m) {
+                                const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                                m &= m - 1;
+                                uint32_t ent = plane_id(pres, wb, v);
+                                if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
+                                out[k_out++] = ent;
+                            }
+                        }
+                    }
+                }
+                rr[0] = static_cast<uint32_t>(off);
+                rr[3] = kPrefProgram;
+                continue;
+            }
+        }
+        rr[3] = kPrefDecode;
+    }
+}
+
+// acc += w * a, bit-sliced; nb = bit length of the running weight sum, so
+// no carry leaves bit nb - 1.
+__device__ __forceinline__ void score_add(Words (&acc)[kScoreBits], uint32_t w, uint32_t nb, const Words &a)
+{
+    Words carry{0, 0};
+#pragma unroll
+    for (int b = 0; b < kScoreBits; ++b) {
+        if (static_cast<uint32_t>(b) < nb) {
+            const Words x = acc[b];
+            if ((w >> b) & 1u) {
+                acc[b] = Words{x.a ^ a.a ^ carry.a, x.b ^ a.b ^ carry.b};
+                carry = Words{(x.a & a.a) | (carry.a & (x.a ^ a.a)), (x.b & a.b) | (carry.b & (x.b ^ a.b))};
+            } else {
+                acc[b] = Words{x.a ^ carry.a, x.b ^ carry.b};
+                carry = Words{x.a & carry.a, x.b & carry.b};
+            }
+        }
+    }
+}
+
+// One term decoded from its expressions (rows whose program found no slice).
+template <bool kBuf>
+__device__ Words pref_term_decoded(const pc_pred *__restrict__ preds, int64_t b, int64_t e,
+                                   const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
+                                   const Planes<kBuf> &pl)
+{
+    Words a{~0ull, ~0ull};
+    for (int64_t p = b; p < e; ++p) {
+        const pc_pred q = preds[p];
+        const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+        const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+        uint64_t sel[4];
+        bool neg;
+        expr_clause(q.op, q.vals, pres, sel, neg);
+        Words c{0, 0};
+        for (int k = 0; k < 4; ++k) {
+            uint64_t m = sel[k];
+            while (m) {
+                const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                m &= m - 1;
+                const Words x = pl(plane_id(pres, wb, v));
+                c.a |= x.a;
+                c.b |= x.b;
+            }
+        }
+        a.a &= neg ? ~c.a : c.a;
+        a.b &= neg ? ~c.b : c.b;
+    }
+    return a;
+}
+
+// Work item (tile of 128 words, chunk of rows) as in k_sel_eval; one row at
+// a time per wavefront.  Per row: the feasible words (every node when the
+// bitset is absent), the bit-sliced scores of the live terms, the lane's
+// best (score, lowest node) and tie count, reduced over the wavefront into
+// part_key[tile * I + r] = (score + 1) << 32 | ~node (0: no feasible node)
+// and part_cnt[tile * I + r].
+template <bool kBuf>
+__global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
+    const uint32_t *__restrict__ rec, const uint32_t *__restrict__ prog, const int32_t *__restrict__ row_off,
+    const int32_t *__restrict__ term_off, const uint32_t *__restrict__ weight, const pc_pred *__restrict__ preds,
+    int64_t n_preds, int32_t L, const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
+    const uint64_t *__restrict__ planes, int64_t plane_bytes, int64_t Wp, int32_t I, int32_t W, int32_t N,
+    const uint64_t *__restrict__ feasible, uint64_t *__restrict__ part_key, uint32_t *__restrict__ part_cnt,
+    int32_t ntiles, int32_t nchunks, int32_t rpc)
+{
+    const int64_t total = static_cast<int64_t>(ntiles) * nchunks;
+    const int64_t item = pc_xcd_item(total);
+    if (item >= total) return;
+    const int32_t tile = static_cast<int32_t>(item / nchunks);
+    const int32_t chunk = static_cast<int32_t>(item % nchunks);
+    const int lane = threadIdx.x & 63;
+    const int wave = __builtin_amdgcn_readfirstlane(threadIdx.x >> 6);
+    const int32_t w0 = tile * kTileW + lane * kWpl;
+    const bool ok0 = w0 < W, ok1 = w0 + 1 < W;
+    const uint64_t last = (N & 63) ? (1ull << (N & 63)) - 1 : ~0ull;
+    const uint64_t m0 = ok0 ? (w0 == W - 1 ? last : ~0ull) : 0ull;
+    const uint64_t m1 = ok1 ? (w0 + 1 == W - 1 ? last : ~0ull) : 0ull;
+    Planes<kBuf> pl;
+    if constexpr (kBuf)
+        pl.rsrc = __builtin_amdgcn_make_buffer_rsrc(const_cast<uint64_t *>(planes), static_cast<short>(0),
+                                                    static_cast<int>(plane_bytes), 0x00020000);
+    pl.lane_off = static_cast<uint32_t>(kPad + w0) * 8u;  // inside the plane row: kPad + w0 + 1 < Wp
+    pl.rowbytes = static_cast<uint32_t>(Wp * 8);
+    pl.pcol = planes + kPad + w0;
+    pl.Wp = Wp;
+    const int32_t r0 = chunk * rpc;
+    const int32_t r1 = min(I, r0 + rpc);
+    for (int32_t bat = r0 + wave * 64; bat < r1; bat += kEvalThreads) {
+        const int32_t nb_rows = min(64, r1 - bat);
+        for (int32_t i = 0; i < nb_rows; ++i) {
+            const int32_t r = bat + i;
+            Words f{m0, m1};
+            if (feasible != nullptr) {
+                // lanes past the row's end read word 0 of the row, then mask it
+                const uint64_t *fr = feasible + static_cast<int64_t>(r) * W;
+                const uint64_t fa = fr[ok0 ? w0 : 0], fb = fr[ok1 ? w0 + 1 : 0];
+                f.a &= fa;
+                f.b &= fb;
+            }
+            const uint32_t *R = rec + static_cast<int64_t>(r) * kPrefRec;
+            const uint32_t off = R[0], live = R[1], nbits = R[2], kind = R[3];
+            Words acc[kScoreBits];
+#pragma unroll
+            for (int b = 0; b < kScoreBits; ++b) acc[b] = Words{0, 0};
+            uint32_t sum = 0;
+            if (kind == kPrefProgram) {
+                const uint32_t *pr = prog + off;
+                for (uint32_t t = 0; t < live; ++t) {
+                    const uint32_t hdr = *pr++;
+                    const uint32_t w = hdr >> kPrefLenBits;
+                    const int32_t len = static_cast<int32_t>(hdr & ((1u << kPrefLenBits) - 1));
+                    Words a{~0ull, ~0ull}, c{0, 0}, unused{0, 0};
+                    for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
+                        uint32_t E[kGroup];
+                        Words V[kGroup];
+#pragma unroll
+                        for (int k = 0; k < kGroup; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
+#pragma unroll
+                        for (int k = 0; k < kGroup; ++k)
+                            if (e0 + k < len) V[k] = pl(E[k] & kPidMask);
+#pragma unroll
+                        for (int k = 0; k < kGroup; ++k)
+                            if (e0 + k < len) fold<false>(E[k], V[k], c, a, unused);
+                    }
+                    pr += len;
+                    sum += w;
+                    score_add(acc, w, bit_length(sum), a);
+                }
+            } else if (kind == kPrefDecode) {
+                for (int64_t t = row_off[r]; t < row_off[r + 1]; ++t) {
+                    const uint32_t w = weight[t];
+                    int64_t len;
+                    if (!pref_weight_ok(w) || !aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len))
+                        continue;
+                    const Words a = pref_term_decoded<kBuf>(preds, term_off[t], term_off[t + 1], present, wbase, pl);
+                    sum += w;
+                    score_add(acc, w, bit_length(sum), a);
+                }
+            }
+            // best score among this lane's feasible nodes: keep the nodes
+            // that have the highest remaining score bit set, top bit first
+            Words cand = f;
+            uint32_t sc = 0;
+#pragma unroll
+            for (int b = kScoreBits - 1; b >= 0; --b) {
+                if (static_cast<uint32_t>(b) < nbits) {
+                    const Words t{cand.a & acc[b].a, cand.b & acc[b].b};
+                    const bool any = (t.a | t.b) != 0;
+                    cand.a = any ? t.a : cand.a;
+                    cand.b = any ? t.b : cand.b;
+                    sc |= any ? (1u << b) : 0u;
+                }
+            }
+            const bool has = (cand.a | cand.b) != 0;
+            const uint32_t node = static_cast<uint32_t>(w0) * 64u +
+                                  (cand.a ? static_cast<uint32_t>(__builtin_ctzll(cand.a))
+                                          : 64u + static_cast<uint32_t>(__builtin_ctzll(cand.b | (1ull << 63))));
+            const uint64_t mine = has ? (static_cast<uint64_t>(sc + 1) << 32) | (0xFFFFFFFFu - node) : 0ull;
+            uint64_t key = mine;
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) {
+                const uint64_t other = __shfl_xor(key, o);
+                key = other > key ? other : key;
+            }
+            uint32_t cnt = (has && (mine >> 32) == (key >> 32)) ? static_cast<uint32_t>(__popcll(cand.a) + __popcll(cand.b)) : 0u;
+#pragma unroll
+            for (int o = 32; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
+            if (lane == 0) {
+                part_key[static_cast<int64_t>(tile) * I + r] = key;
+                part_cnt[static_cast<int64_t>(tile) * I + r] = cnt;
+            }
+        }
+    }
+}
+
+// Per row: the best key over the tiles and the tie count of that score.
+__global__ __launch_bounds__(256) void k_pref_final(const uint64_t *__restrict__ part_key,
+                                                    const uint32_t *__restrict__ part_cnt, int32_t I, int32_t ntiles,
+                                                    int32_t *__restrict__ best, uint32_t *__restrict__ score,
+                                                    uint32_t *__restrict__ count)
+{
+    const int32_t r = blockIdx.x * 256 + threadIdx.x;
+    if (r >= I) return;
+    uint64_t key = 0;
+    for (int32_t t = 0; t < ntiles; ++t) {
+        const uint64_t k = part_key[static_cast<int64_t>(t) * I + r];
+        key = k > key ? k : key;
+    }
+    uint32_t cnt = 0;
+    if (key != 0)
+        for (int32_t t = 0; t < ntiles; ++t)
+            if ((part_key[static_cast<int64_t>(t) * I + r] >> 32) == (key >> 32)) cnt += part_cnt[static_cast<int64_t>(t) * I + r];
+    best[r] = key ? static_cast<int32_t>(0xFFFFFFFFu - static_cast<uint32_t>(key)) : -1;
+    score[r] = key ? static_cast<uint32_t>(key >> 32) - 1u : 0u;
+    count[r] = cnt;
+}
+
 }  // namespace
 
 namespace {
@@ -1015,4 +1343,85 @@ int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const
     if (W == 0) return PC_OK;
     return launch_eval<true>(ctx, rec, prog, row_off, preds, present, wbase, planes, pmax, Wp, I, W, N, feasible,
                              popcnt, part, ntiles, term_off, n_preds, L, geo.shift, stream);
+}
+
+int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const uint64_t *feasible,
+                  const int32_t *row_off, int32_t I, const int32_t *term_off, int32_t n_terms, const uint32_t *weight,
+                  const pc_pred *preds, int64_t n_preds, int32_t *best, uint32_t *score, uint32_t *count,
+                  hipStream_t stream)
+{
+    const int64_t W = (static_cast<int64_t>(N) + 63) / 64;
+    const int64_t ntiles = (W + kTileW - 1) / kTileW;
+    const int64_t Wp = kPad + ntiles * kTileW;  // unshifted tiles: every lane's pair lies inside a plane row
+    const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
+    const size_t plane_bytes = static_cast<size_t>(pmax + 1) * static_cast<size_t>(Wp) * 8;
+    if (plane_bytes > (size_t(64) << 30))
+        return pc_set_error(ctx, PC_ENOMEM, "pc_score_preferred: value planes need %zu bytes (L=%d N=%d)",
+                            plane_bytes, L, N);
+    // room for a header per term and 4 entries per expression; rows beyond it decode on the fly
+    const int64_t prog_cap = std::min<int64_t>(static_cast<int64_t>(n_terms) + 4 * n_preds + 64, int64_t(1) << 31);
+    uint64_t *present, *planes, *part_key;
+    uint32_t *wbase, *prog, *rec, *part_cnt;
+    int32_t *d_P;
+    unsigned long long *prog_used;
+    auto carve = [&](Carver &cv) {
+        present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
+        wbase = cv.take<uint32_t>(static_cast<size_t>(L) * 4 + 1);
+        planes = cv.take<uint64_t>(static_cast<size_t>(pmax + 1) * Wp + 2);
+        prog = cv.take<uint32_t>(static_cast<size_t>(prog_cap));
+        rec = cv.take<uint32_t>(static_cast<size_t>(I) * kPrefRec + kPrefRec);
+        part_key = cv.take<uint64_t>(static_cast<size_t>(ntiles) * I + 1);
+        part_cnt = cv.take<uint32_t>(static_cast<size_t>(ntiles) * I + 1);
+        d_P = cv.take<int32_t>(1);
+        prog_used = cv.take<unsigned long long>(1);
+    };
+    Carver dry{nullptr, 0};
+    carve(dry);
+    int rc = pc_ensure_arena(ctx, dry.off);
+    if (rc) return rc;
+    Carver real{ctx->arena, 0};
+    carve(real);
+
+    const int64_t nval = std::max<int64_t>(I, n_terms);
+    if (nval > 0) {
+        const unsigned vgrid = static_cast<unsigned>(std::min<int64_t>((nval + 255) / 256, 8192));
+        PC_TIMED(ctx, "k_pref_validate", stream,
+                 hipLaunchKernelGGL(k_pref_validate, dim3(vgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
+                                    weight, preds, n_preds, L, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    if (I == 0) return PC_OK;
+    launch_fill_u64(reinterpret_cast<uint64_t *>(prog_used), 1, 0, stream);
+    rc = build_planes(ctx, labels, N, L, W, Wp, pmax, present, wbase, planes, d_P, stream);
+    if (rc) return rc;
+    const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
+    PC_TIMED(ctx, "k_pref_compile", stream,
+             hipLaunchKernelGGL(k_pref_compile, dim3(rgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
+                                weight, preds, n_preds, L, present, wbase, prog, prog_cap, prog_used, rec));
+    PC_LAUNCH_CHECK(ctx);
+    if (W > 0) {
+        int64_t nchunks = std::max<int64_t>((32768 + ntiles - 1) / ntiles, 1);
+        int64_t rpc = (I + nchunks - 1) / nchunks;
+        rpc = (rpc + 63) / 64 * 64;
+        nchunks = (I + rpc - 1) / rpc;
+        const int64_t total = ntiles * nchunks;
+        const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
+        const int64_t pbytes = static_cast<int64_t>(pmax + 1) * Wp * 8;
+        auto eval = [&](auto kern) {
+            PC_TIMED(ctx, "k_pref_eval", stream,
+                     hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, row_off, term_off,
+                                        weight, preds, n_preds, L, present, wbase, planes, pbytes, Wp, I,
+                                        static_cast<int32_t>(W), N, feasible, part_key, part_cnt,
+                                        static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
+                                        static_cast<int32_t>(rpc)));
+        };
+        if (pbytes < (int64_t(1) << 31)) eval(k_pref_eval<true>);
+        else eval(k_pref_eval<false>);
+        PC_LAUNCH_CHECK(ctx);
+    }
+    PC_TIMED(ctx, "k_pref_final", stream,
+             hipLaunchKernelGGL(k_pref_final, dim3(static_cast<unsigned>((I + 255) / 256)), dim3(256), 0, stream,
+                                part_key, part_cnt, I, static_cast<int32_t>(W > 0 ? ntiles : 0), best, score, count));
+    PC_LAUNCH_CHECK(ctx);
+    return PC_OK;
 }

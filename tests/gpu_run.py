@@ -29,6 +29,19 @@ def affinity(labels, row_off, term_off, preds, n_terms=None, n_preds=None):
     return f.cpu().numpy().view(np.uint64), p.cpu().numpy().view(np.uint32), u.cpu().numpy(), flags
 
 
+def preferred(labels, row_off, term_off, weight, preds, feasible=None, n_terms=None, n_preds=None):
+    """Best node, score, tie count and the data-error word."""
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    f = None if feasible is None else torch.from_numpy(np.ascontiguousarray(feasible).view(np.int64)).cuda()
+    b, s, c = pc.pc_score_preferred(dev(labels), dev(row_off), dev(term_off),
+                                    dev(np.ascontiguousarray(weight, np.uint32)), dev(preds), feasible=f,
+                                    n_terms=n_terms, n_preds=n_preds)
+    torch.cuda.synchronize()
+    flags = ctx.data_errors(clear=True)
+    return (b.cpu().numpy(), s.cpu().numpy().view(np.uint32), c.cpu().numpy().view(np.uint32), flags)
+
+
 def _rows2d(a, Q):
     a = np.ascontiguousarray(a, np.int32)
     return a.reshape(Q, a.shape[1] if a.ndim == 2 else 1)

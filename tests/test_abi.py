@@ -53,6 +53,8 @@ def test_null_context_is_einval(libpc):
     EINVAL = libpc.PC_EINVAL
     assert L.pc_eval_selectors(None, None, 0, 0, None, None, 0, 0, None, None, None) == EINVAL
     assert L.pc_eval_affinity(None, None, 0, 0, None, 0, None, 0, None, 0, None, None, None, None) == EINVAL
+    assert L.pc_score_preferred(None, None, 0, 0, None, None, 0, None, 0, None, None, 0, None, None, None,
+                                None) == EINVAL
     assert L.pc_update_nodes(None, None, 0, 0, None, None, 0, 0, None, 0, None, None, None) == EINVAL
     assert L.pc_eval_selectors_count(None, None, 0, 0, None, None, 0, 0, None, None) == EINVAL
     assert L.pc_probe_selectors(None, None, 0, 0, None, None, 0, 0, None, None, 0, None, None) == EINVAL
