@@ -71,16 +71,19 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
-    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity", "synthesis", "update",
-                                                     "verdict"],
+    ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity", "preferred",
+                                                     "synthesis", "update", "verdict"],
                     help="profiling aid: time one stage only (the JSON line then covers that stage); 'paths' "
                          "times only the pass with waypoint / forbidden-switch constraints, 'affinity' only the "
-                         "node-affinity pass, 'synthesis' only the path-synthesis pass, 'update' only the incremental "
-                         "re-evaluation, 'verdict' only the verdict-only pass")
+                         "node-affinity pass, 'preferred' only the preferred-affinity pass, 'synthesis' only the "
+                         "path-synthesis pass, 'update' only the incremental re-evaluation, 'verdict' only the "
+                         "verdict-only pass")
     ap.add_argument("--no-paths", action="store_true",
                     help="skip the second timed pass with waypoint / forbidden-switch constraints")
     ap.add_argument("--no-affinity", action="store_true",
                     help="skip the timed pass of full node affinity over the same cluster")
+    ap.add_argument("--no-preferred", action="store_true",
+                    help="skip the timed pass of preferred node affinity (best feasible node per row)")
     ap.add_argument("--no-verdict-only", action="store_true",
                     help="skip the timed verdict-only pass (popcounts and endpoint probes instead of the bitset)")
     ap.add_argument("--no-update", action="store_true",
@@ -320,6 +323,88 @@ def time_affinity(args, wl, pc, ctx, feasible):
             stride = max(1, stride // 64, int(stride * max(t, 1e-3) / (args.cpu_seconds / 3)))
         est = t * I / rows.shape[0]
         out["cpu_baseline"] = {"value": pairs / est, "unit": "affinity evals/s (whole-pass estimate)",
+                               "cores": threads, "kind": "oracle",
+                               "sample": f"every {stride}th row ({rows.shape[0]} of {I} rows x {N} nodes) in "
+                                         f"{t:.2f} s; whole pass estimated at {est:.1f} s"}
+    return out
+
+
+def time_preferred(args, wl, pc, ctx, feasible):
+    """Timed pass of preferred node affinity (pc_score_preferred) over the
+    same cluster: per selector row 1-3 weighted terms (weights 1..100) of
+    1-3 expressions, scored over the row's feasible nodes from the main
+    pass's selector bitset."""
+    import torch
+    import synth
+    dev = feasible.device
+    I = feasible.shape[0]
+    row_off, term_off, preds, weight = synth.preferred_rows(wl.seed, wl.meta["cards"], I)
+    D = {k: pc.to_device(v, dev) for k, v in (("labels", wl["labels"]), ("row_off", row_off),
+                                               ("term_off", term_off), ("preds", preds), ("weight", weight))}
+    best = torch.empty(I, dtype=torch.int32, device=dev)
+    score = torch.empty(I, dtype=torch.int32, device=dev)
+    count = torch.empty(I, dtype=torch.int32, device=dev)
+
+    def step():
+        pc.pc_score_preferred(D["labels"], D["row_off"], D["term_off"], D["weight"], D["preds"], feasible=feasible,
+                              best=best, score=score, count=count, ctx=ctx)
+
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.data_errors(clear=True)
+    ctx.profile(True)
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    elapsed = time.perf_counter() - t0
+    prof = ctx.profile_read()
+    ctx.profile(False)
+    flags = ctx.data_errors(clear=True)
+    N, L = wl["N"], wl["L"]
+    W = (N + 63) // 64
+    n_eval, eval_ms = prof["k_pref_eval"]
+    avg_ms = eval_ms / max(n_eval, 1)
+    n_terms, n_preds = term_off.shape[0] - 1, preds.shape[0]
+    # the feasible bitset, expressions, weights, offsets and labels read
+    # once; best node, score and tie count written
+    alg = I * W * 8 + I * 12 + n_preds * 40 + n_terms * 4 + (n_terms + 1) * 4 + (I + 1) * 4 + N * L
+    achieved = alg / (avg_ms * 1e-3) / 1e9
+    pairs = I * N
+    b = best.cpu().numpy()
+    out = {
+        "rows": I, "terms": int(n_terms), "expressions": int(n_preds),
+        "ms_per_step": 1e3 * elapsed / args.steps,
+        "evals_per_s": pairs * args.steps / elapsed,
+        "per_kernel": {name: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
+                       for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])},
+        "roofline": {"kernel": "k_pref_eval", "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
+                     "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
+                     "traffic": measured_traffic(args.workload, "k_pref_eval"), "alg_bytes_per_launch": alg,
+                     "avg_launch_ms": avg_ms},
+        "placed_rows": int((b >= 0).sum()),
+        "mean_best_score": float(score.cpu().numpy()[b >= 0].mean()) if (b >= 0).any() else 0.0,
+        "data_error_flags": flags,
+    }
+    if not args.no_cpu_baseline:
+        import oracle
+        threads = len(os.sched_getaffinity(0))
+        env_cap = os.environ.get("OMP_NUM_THREADS")
+        if env_cap and env_cap.isdigit():
+            threads = min(threads, int(env_cap))
+        fh = feasible.cpu().numpy().view(np.uint64)
+        stride, t = 4096, 0.0
+        while True:
+            rows = np.arange(0, I, stride, dtype=np.int32)
+            t0 = time.perf_counter()
+            oracle.preferred(wl["labels"], row_off, term_off, weight, preds, feasible=fh, rows=rows, nthreads=threads)
+            t = time.perf_counter() - t0
+            if t >= args.cpu_seconds / 6 or stride == 1:
+                break
+            stride = max(1, stride // 64, int(stride * max(t, 1e-3) / (args.cpu_seconds / 3)))
+        est = t * I / rows.shape[0]
+        out["cpu_baseline"] = {"value": pairs / est, "unit": "preferred-affinity evals/s (whole-pass estimate)",
                                "cores": threads, "kind": "oracle",
                                "sample": f"every {stride}th row ({rows.shape[0]} of {I} rows x {N} nodes) in "
                                          f"{t:.2f} s; whole pass estimated at {est:.1f} s"}
@@ -581,6 +666,12 @@ def main():
     if only == "affinity":
         print(json.dumps({"workload": desc, "affinity": time_affinity(args, wl, pc, ctx, feasible)}), flush=True)
         return
+    if only == "preferred":
+        # the feasible sets are the selector rows' bitsets, computed once
+        pc.pc_eval_selectors(D["labels"], D["pred_off"], D["preds"], feasible=feasible, popcnt=popcnt, ctx=ctx)
+        torch.cuda.synchronize()
+        print(json.dumps({"workload": desc, "preferred": time_preferred(args, wl, pc, ctx, feasible)}), flush=True)
+        return
     if only == "update":
         print(json.dumps({"workload": desc, "update": time_update(args, wl, pc, ctx, D, feasible, popcnt)}),
               flush=True)
@@ -714,6 +805,8 @@ def main():
         line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)
     if only == "all" and not args.no_affinity:
         line["affinity"] = time_affinity(args, wl, pc, ctx, feasible)
+    if only == "all" and not args.no_preferred:
+        line["preferred"] = time_preferred(args, wl, pc, ctx, feasible)
     if only == "all" and not args.no_verdict_only:
         vo = time_verdict_only(args, wl, pc, ctx, D, traces, reach)
         vo["verdict_equals_main_pass"] = bool(torch.equal(vo.pop("_pass"), pass_) and

@@ -822,8 +822,13 @@ __global__ __launch_bounds__(256) void k_sel_popsum(const uint32_t *__restrict__
 constexpr int kScoreBits = 16;         // 655 terms of weight <= 100 stay below 2^16
 constexpr int32_t kPrefMaxTerms = 655;
 constexpr uint32_t kPrefLenBits = 24;  // term header: weight << 24 | program entries
-enum : uint32_t { kPrefProgram = 0, kPrefNone = 1, kPrefDecode = 2 };
-constexpr int kPrefRec = 4;            // row record: program offset, live terms, score bits, kind
+// row record, 16 words (one 64-byte line): word 0 = kind << 24 | score bits
+// << 16 | live terms; word 1 = program offset in prog (kPrefIndirect);
+// words 2..15 = the program itself when it has at most 14 words
+enum : uint32_t { kPrefInline = 0, kPrefIndirect = 1, kPrefDecode = 2, kPrefNone = 3 };
+constexpr int kPrefRec = 16;
+constexpr int kPrefInlineWords = kPrefRec - 2;
+constexpr uint32_t kPrefClasses = 3;  // row lists: scores within 8 bits, within 16 bits, decoded on the fly
 
 __device__ __forceinline__ bool pref_weight_ok(uint32_t w) { return w >= 1 && w <= 100; }
 
@@ -867,11 +872,82 @@ __global__ __launch_bounds__(256) void k_pref_validate(const int32_t *__restrict
     if (errs) atomicOr(d_err, errs);
 }
 
+// One row of k_pref_compile: its record, and its class (0: scores fit 8
+// bits, 1: 16 bits, 2: decoded on the fly).
+__device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_t i,
+                                     const int32_t *__restrict__ term_off, int32_t n_terms,
+                                     const uint32_t *__restrict__ weight, const pc_pred *__restrict__ preds,
+                                     int64_t n_preds, int32_t L, const uint64_t *__restrict__ present,
+                                     const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog, int64_t prog_cap,
+                                     unsigned long long *__restrict__ prog_used, uint32_t *__restrict__ rec)
+{
+    uint32_t *rr = rec + static_cast<int64_t>(i) * kPrefRec;
+    rr[0] = kPrefNone << 24;
+    if (!pref_row_ok(row_off, i, n_terms)) return 0;
+    const int64_t tb = row_off[i], te = row_off[i + 1];
+    int64_t n = 0;
+    uint32_t live = 0, sum = 0;
+    bool decode = false;
+    for (int64_t t = tb; t < te; ++t) {
+        int64_t len;
+        if (!pref_weight_ok(weight[t]) || !aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len))
+            continue;
+        if (len >= (int64_t(1) << kPrefLenBits)) decode = true;
+        n += 1 + len;
+        sum += weight[t];
+        ++live;
+    }
+    if (live == 0) return 0;
+    const uint32_t head = live | bit_length(sum) << 16;
+    uint32_t *out = rr + 2;
+    uint32_t kind = kPrefInline;
+    if (!decode && n > kPrefInlineWords) {
+        const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>(n));
+        decode = static_cast<int64_t>(off) + n > prog_cap;
+        out = prog + off;
+        rr[1] = static_cast<uint32_t>(off);
+        kind = kPrefIndirect;
+    }
+    if (decode) {
+        rr[0] = head | kPrefDecode << 24;
+        return 2;
+    }
+    int64_t k_out = 0;
+    for (int64_t t = tb; t < te; ++t) {
+        const int64_t b = term_off[t], e = term_off[t + 1];
+        int64_t len;
+        if (!pref_weight_ok(weight[t]) || !aff_term(preds, b, e, n_preds, L, present, len)) continue;
+        out[k_out++] = weight[t] << kPrefLenBits | static_cast<uint32_t>(len);
+        for (int64_t p = b; p < e; ++p) {
+            const pc_pred q = preds[p];
+            const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+            const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+            uint64_t sel[4];
+            bool neg;
+            uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
+            for (int k = 0; k < 4; ++k) {
+                uint64_t m = sel[k];
+                while (m) {
+                    const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                    m &= m - 1;
+                    uint32_t ent = plane_id(pres, wb, v);
+                    if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
+                    out[k_out++] = ent;
+                }
+            }
+        }
+    }
+    rr[0] = head | kind << 24;
+    return bit_length(sum) <= 8 ? 0u : 1u;
+}
+
 // One thread per row: the row's live terms (weight in range, and able to
 // hold somewhere) as a program of term headers, each followed by its clause
-// entries (kLast / kNeg as in selector programs), in a slice of prog taken
-// through a bump counter.  When the slice does not fit, or a term has more
-// than 2^24 entries, the row is decoded at evaluation time.
+// entries (kLast / kNeg as in selector programs), inline in the row record
+// when it has at most 14 words, else in a slice of prog taken through a
+// bump counter.  When the slice does not fit, or a term has more than 2^24
+// entries, the row is decoded at evaluation time.
+// Each row is appended to the list of its class.
 __global__ __launch_bounds__(256) void k_pref_compile(const int32_t *__restrict__ row_off, int32_t I,
                                                       const int32_t *__restrict__ term_off, int32_t n_terms,
                                                       const uint32_t *__restrict__ weight,
@@ -879,85 +955,86 @@ __global__ __launch_bounds__(256) void k_pref_compile(const int32_t *__restrict_
                                                       const uint64_t *__restrict__ present,
                                                       const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog,
                                                       int64_t prog_cap, unsigned long long *__restrict__ prog_used,
-                                                      uint32_t *__restrict__ rec)
+                                                      uint32_t *__restrict__ rec, int32_t *__restrict__ list,
+                                                      uint32_t *__restrict__ list_len)
 {
-    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
-        uint32_t *rr = rec + static_cast<int64_t>(i) * kPrefRec;
-        rr[0] = rr[1] = rr[2] = 0;
-        rr[3] = kPrefNone;
-        if (!pref_row_ok(row_off, i, n_terms)) continue;
-        const int64_t tb = row_off[i], te = row_off[i + 1];
-        int64_t n = 0;
-        uint32_t live = 0, sum = 0;
-        bool decode = false;
-        for (int64_t t = tb; t < te; ++t) {
-            int64_t len;
-            if (!pref_weight_ok(weight[t]) || !aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len))
-                continue;
-            if (len >= (int64_t(1) << kPrefLenBits)) decode = true;
-            n += 1 + len;
-            sum += weight[t];
-            ++live;
+    const int lane = threadIdx.x & 63;
+    for (int64_t base = static_cast<int64_t>(blockIdx.x) * blockDim.x; base < I;
+         base += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int32_t i = static_cast<int32_t>(base + threadIdx.x);
+        const uint32_t cls = i < I ? pref_compile_row(row_off, i, term_off, n_terms, weight, preds, n_preds, L,
+                                                      present, wbase, prog, prog_cap, prog_used, rec)
+                                   : kPrefClasses;
+        // append i to its class list: one counter update per class and wavefront
+        for (uint32_t c = 0; c < kPrefClasses; ++c) {
+            const uint64_t mask = __ballot(cls == c);
+            if (mask == 0) continue;
+            const int leader = __builtin_ctzll(mask);
+            uint32_t off = 0;
+            if (lane == leader) off = atomicAdd(list_len + c, static_cast<uint32_t>(__popcll(mask)));
+            off = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), leader));
+            const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(mask >> 32),
+                                                             __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(mask), 0u));
+            if (cls == c) list[static_cast<int64_t>(c) * I + off + below] = i;
         }
-        if (live == 0) continue;
-        rr[1] = live;
-        rr[2] = bit_length(sum);
-        if (!decode) {
-            const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>(n));
-            decode = static_cast<int64_t>(off) + n > prog_cap;
-            if (!decode) {
-                uint32_t *out = prog + off;
-                int64_t k_out = 0;
-                for (int64_t t = tb; t < te; ++t) {
-                    const int64_t b = term_off[t], e = term_off[t + 1];
-                    int64_t len;
-                    if (!pref_weight_ok(weight[t]) || !aff_term(preds, b, e, n_preds, L, present, len)) continue;
-                    out[k_out++] = weight[t] << kPrefLenBits | static_cast<uint32_t>(len);
-                    for (int64_t p = b; p < e; ++p) {
-                        const pc_pred q = preds[p];
-                        const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
-                        const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
-                        uint64_t sel[4];
-                        bool neg;
-                        uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
-                        for (int k = 0; k < 4; ++k) {
-                            uint64_t m = sel[k];
-                            while (m) {
-                                const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
-                                m &= m - 1;
-                                uint32_t ent = plane_id(pres, wb, v);
-                                if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
-                                out[k_out++] = ent;
-                            }
-                        }
-                    }
-                }
-                rr[0] = static_cast<uint32_t>(off);
-                rr[3] = kPrefProgram;
-                continue;
-            }
-        }
-        rr[3] = kPrefDecode;
     }
 }
 
-// acc += w * a, bit-sliced; nb = bit length of the running weight sum, so
-// no carry leaves bit nb - 1.
-__device__ __forceinline__ void score_add(Words (&acc)[kScoreBits], uint32_t w, uint32_t nb, const Words &a)
+
+// Wavefront reductions of a 32-bit value with DPP: quad exchanges, then
+// row rotations by 4 and 8 leave every lane with its 16-lane row's result;
+// the four rows' results are combined on the scalar unit.
+template <int kOp>
+__device__ __forceinline__ uint32_t red_op(uint32_t a, uint32_t b)
+{
+    if constexpr (kOp == 0) return a > b ? a : b;
+    else if constexpr (kOp == 1) return a < b ? a : b;
+    else return a + b;
+}
+
+template <int kOp>
+__device__ __forceinline__ uint32_t wave_reduce_u32(uint32_t x)
+{
+    int v = static_cast<int>(x);
+    v = static_cast<int>(red_op<kOp>(static_cast<uint32_t>(v), static_cast<uint32_t>(__builtin_amdgcn_update_dpp(v, v, 0xB1, 0xF, 0xF, false))));
+    v = static_cast<int>(red_op<kOp>(static_cast<uint32_t>(v), static_cast<uint32_t>(__builtin_amdgcn_update_dpp(v, v, 0x4E, 0xF, 0xF, false))));
+    v = static_cast<int>(red_op<kOp>(static_cast<uint32_t>(v), static_cast<uint32_t>(__builtin_amdgcn_update_dpp(v, v, 0x124, 0xF, 0xF, false))));
+    v = static_cast<int>(red_op<kOp>(static_cast<uint32_t>(v), static_cast<uint32_t>(__builtin_amdgcn_update_dpp(v, v, 0x128, 0xF, 0xF, false))));
+    const uint32_t r0 = static_cast<uint32_t>(__builtin_amdgcn_readlane(v, 0));
+    const uint32_t r1 = static_cast<uint32_t>(__builtin_amdgcn_readlane(v, 16));
+    const uint32_t r2 = static_cast<uint32_t>(__builtin_amdgcn_readlane(v, 32));
+    const uint32_t r3 = static_cast<uint32_t>(__builtin_amdgcn_readlane(v, 48));
+    return red_op<kOp>(red_op<kOp>(r0, r1), red_op<kOp>(r2, r3));
+}
+__device__ __forceinline__ uint32_t wave_max_u32(uint32_t x) { return wave_reduce_u32<0>(x); }
+__device__ __forceinline__ uint32_t wave_min_u32(uint32_t x) { return wave_reduce_u32<1>(x); }
+__device__ __forceinline__ uint32_t wave_add_u32(uint32_t x) { return wave_reduce_u32<2>(x); }
+
+// acc += w * a, bit-sliced over kBits score bits (w <= 100 < 2^7): bits
+// 0..6 are full adds of the weight's bit (masked by a) and the carry, above
+// them only the carry moves.  The row's class guarantees that its weight
+// sum fits kBits, so no carry leaves the top bit.  Branch-free, so the
+// score words stay in place.
+template <int kBits>
+__device__ __forceinline__ void score_add(Words (&acc)[kBits], uint32_t w, const Words &a)
 {
     Words carry{0, 0};
 #pragma unroll
-    for (int b = 0; b < kScoreBits; ++b) {
-        if (static_cast<uint32_t>(b) < nb) {
-            const Words x = acc[b];
-            if ((w >> b) & 1u) {
-                acc[b] = Words{x.a ^ a.a ^ carry.a, x.b ^ a.b ^ carry.b};
-                carry = Words{(x.a & a.a) | (carry.a & (x.a ^ a.a)), (x.b & a.b) | (carry.b & (x.b ^ a.b))};
-            } else {
-                acc[b] = Words{x.a ^ carry.a, x.b ^ carry.b};
-                carry = Words{x.a & carry.a, x.b & carry.b};
-            }
-        }
+    for (int b = 0; b < 7; ++b) {
+        const uint64_t wm = ((w >> b) & 1u) ? ~0ull : 0ull;
+        const uint64_t xa = acc[b].a, xb = acc[b].b, ya = a.a & wm, yb = a.b & wm;
+        acc[b].a = xa ^ ya ^ carry.a;
+        acc[b].b = xb ^ yb ^ carry.b;
+        carry.a = (xa & ya) | (carry.a & (xa ^ ya));
+        carry.b = (xb & yb) | (carry.b & (xb ^ yb));
+    }
+#pragma unroll
+    for (int b = 7; b < kBits; ++b) {
+        const uint64_t xa = acc[b].a, xb = acc[b].b;
+        acc[b].a = xa ^ carry.a;
+        acc[b].b = xb ^ carry.b;
+        carry.a &= xa;
+        carry.b &= xb;
     }
 }
 
@@ -998,15 +1075,21 @@ __device__ Words pref_term_decoded(const pc_pred *__restrict__ preds, int64_t b,
 // best (score, lowest node) and tie count, reduced over the wavefront into
 // part_key[tile * I + r] = (score + 1) << 32 | ~node (0: no feasible node)
 // and part_cnt[tile * I + r].
-template <bool kBuf>
+// kCls: the rows of one class list (0: scores within 8 bits, 1: within 16
+// bits, 2: decoded on the fly), so that each launch keeps only the score
+// words it needs and the common one carries no decoding code.
+template <bool kBuf, int kCls>
 __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
     const uint32_t *__restrict__ rec, const uint32_t *__restrict__ prog, const int32_t *__restrict__ row_off,
     const int32_t *__restrict__ term_off, const uint32_t *__restrict__ weight, const pc_pred *__restrict__ preds,
     int64_t n_preds, int32_t L, const uint64_t *__restrict__ present, const uint32_t *__restrict__ wbase,
     const uint64_t *__restrict__ planes, int64_t plane_bytes, int64_t Wp, int32_t I, int32_t W, int32_t N,
     const uint64_t *__restrict__ feasible, uint64_t *__restrict__ part_key, uint32_t *__restrict__ part_cnt,
-    int32_t ntiles, int32_t nchunks, int32_t rpc)
+    int32_t ntiles, int32_t nchunks, int32_t rpc, const int32_t *__restrict__ list,
+    const uint32_t *__restrict__ list_len, int64_t fstride)
 {
+    constexpr int kBits = kCls == 0 ? 8 : kScoreBits;
+    constexpr bool kDecode = kCls == 2;
     const int64_t total = static_cast<int64_t>(ntiles) * nchunks;
     const int64_t item = pc_xcd_item(total);
     if (item >= total) return;
@@ -1027,33 +1110,56 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
     pl.rowbytes = static_cast<uint32_t>(Wp * 8);
     pl.pcol = planes + kPad + w0;
     pl.Wp = Wp;
+    const int32_t *rows = list + static_cast<int64_t>(kCls) * I;
     const int32_t r0 = chunk * rpc;
-    const int32_t r1 = min(I, r0 + rpc);
+    const int32_t r1 = min(static_cast<int32_t>(list_len[kCls]), r0 + rpc);
     for (int32_t bat = r0 + wave * 64; bat < r1; bat += kEvalThreads) {
         const int32_t nb_rows = min(64, r1 - bat);
+        // The batch's row ids, one per lane.  A row's record head and
+        // feasible words (fstride 0: one all-ones row; lanes past the row's
+        // end read its word 0 and mask it) are requested at the end of the
+        // previous row, so their latency hides behind that row's selection.
+        const int32_t my_row = lane < nb_rows ? rows[bat + lane] : 0;
+        auto feas_words = [&](int32_t rr, uint64_t &a, uint64_t &b) {
+            const uint64_t *fr = feasible + static_cast<int64_t>(rr) * fstride;
+            a = fr[ok0 ? w0 : 0];
+            b = fr[ok1 ? w0 + 1 : 0];
+        };
+        int32_t r_next = __builtin_amdgcn_readlane(my_row, 0);
+        uint32_t head_next = rec[static_cast<int64_t>(r_next) * kPrefRec];
+        uint64_t fa_next, fb_next;
+        feas_words(r_next, fa_next, fb_next);
         for (int32_t i = 0; i < nb_rows; ++i) {
-            const int32_t r = bat + i;
-            Words f{m0, m1};
-            if (feasible != nullptr) {
-                // lanes past the row's end read word 0 of the row, then mask it
-                const uint64_t *fr = feasible + static_cast<int64_t>(r) * W;
-                const uint64_t fa = fr[ok0 ? w0 : 0], fb = fr[ok1 ? w0 + 1 : 0];
-                f.a &= fa;
-                f.b &= fb;
-            }
+            const int32_t r = r_next;
             const uint32_t *R = rec + static_cast<int64_t>(r) * kPrefRec;
-            const uint32_t off = R[0], live = R[1], nbits = R[2], kind = R[3];
-            Words acc[kScoreBits];
+            const uint32_t head = head_next;
+            const uint32_t kind = head >> 24, live = head & 0xFFFFu;
+            const uint64_t fa = fa_next, fb = fb_next;
+            Words acc[kBits];
 #pragma unroll
-            for (int b = 0; b < kScoreBits; ++b) acc[b] = Words{0, 0};
-            uint32_t sum = 0;
-            if (kind == kPrefProgram) {
-                const uint32_t *pr = prog + off;
-                for (uint32_t t = 0; t < live; ++t) {
+            for (int b = 0; b < kBits; ++b) acc[b] = Words{0, 0};
+            // one loop over the row's terms, whatever their source, so the
+            // score words have a single update site
+            constexpr bool dec = kDecode;
+            const int64_t tb = dec ? row_off[r] : 0;
+            const uint32_t n_iter = dec ? static_cast<uint32_t>(row_off[r + 1] - tb)
+                                        : (kind == kPrefNone ? 0u : live);
+            const uint32_t *pr = kind == kPrefInline ? R + 2 : prog + R[1];
+            for (uint32_t t = 0; t < n_iter; ++t) {
+                uint32_t w;
+                Words a{~0ull, ~0ull};
+                if constexpr (dec) {
+                    w = weight[tb + t];
+                    int64_t len;
+                    if (!pref_weight_ok(w) ||
+                        !aff_term(preds, term_off[tb + t], term_off[tb + t + 1], n_preds, L, present, len))
+                        continue;
+                    a = pref_term_decoded<kBuf>(preds, term_off[tb + t], term_off[tb + t + 1], present, wbase, pl);
+                } else {
                     const uint32_t hdr = *pr++;
-                    const uint32_t w = hdr >> kPrefLenBits;
+                    w = hdr >> kPrefLenBits;
                     const int32_t len = static_cast<int32_t>(hdr & ((1u << kPrefLenBits) - 1));
-                    Words a{~0ull, ~0ull}, c{0, 0}, unused{0, 0};
+                    Words c{0, 0}, unused{0, 0};
                     for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
                         uint32_t E[kGroup];
                         Words V[kGroup];
@@ -1067,48 +1173,38 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
                             if (e0 + k < len) fold<false>(E[k], V[k], c, a, unused);
                     }
                     pr += len;
-                    sum += w;
-                    score_add(acc, w, bit_length(sum), a);
                 }
-            } else if (kind == kPrefDecode) {
-                for (int64_t t = row_off[r]; t < row_off[r + 1]; ++t) {
-                    const uint32_t w = weight[t];
-                    int64_t len;
-                    if (!pref_weight_ok(w) || !aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len))
-                        continue;
-                    const Words a = pref_term_decoded<kBuf>(preds, term_off[t], term_off[t + 1], present, wbase, pl);
-                    sum += w;
-                    score_add(acc, w, bit_length(sum), a);
-                }
+                score_add<kBits>(acc, w, a);
+            }
+            if (i + 1 < nb_rows) {
+                r_next = __builtin_amdgcn_readlane(my_row, i + 1);
+                head_next = rec[static_cast<int64_t>(r_next) * kPrefRec];
+                feas_words(r_next, fa_next, fb_next);
             }
             // best score among this lane's feasible nodes: keep the nodes
             // that have the highest remaining score bit set, top bit first
-            Words cand = f;
+            Words cand{m0 & fa, m1 & fb};
             uint32_t sc = 0;
+            auto narrow = [&](int b) {
+                const Words t{cand.a & acc[b].a, cand.b & acc[b].b};
+                const bool any = (t.a | t.b) != 0;
+                cand.a = any ? t.a : cand.a;
+                cand.b = any ? t.b : cand.b;
+                sc |= any ? (1u << b) : 0u;
+            };
 #pragma unroll
-            for (int b = kScoreBits - 1; b >= 0; --b) {
-                if (static_cast<uint32_t>(b) < nbits) {
-                    const Words t{cand.a & acc[b].a, cand.b & acc[b].b};
-                    const bool any = (t.a | t.b) != 0;
-                    cand.a = any ? t.a : cand.a;
-                    cand.b = any ? t.b : cand.b;
-                    sc |= any ? (1u << b) : 0u;
-                }
-            }
+            for (int b = kBits - 1; b >= 0; --b) narrow(b);
             const bool has = (cand.a | cand.b) != 0;
             const uint32_t node = static_cast<uint32_t>(w0) * 64u +
                                   (cand.a ? static_cast<uint32_t>(__builtin_ctzll(cand.a))
                                           : 64u + static_cast<uint32_t>(__builtin_ctzll(cand.b | (1ull << 63))));
-            const uint64_t mine = has ? (static_cast<uint64_t>(sc + 1) << 32) | (0xFFFFFFFFu - node) : 0ull;
-            uint64_t key = mine;
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) {
-                const uint64_t other = __shfl_xor(key, o);
-                key = other > key ? other : key;
-            }
-            uint32_t cnt = (has && (mine >> 32) == (key >> 32)) ? static_cast<uint32_t>(__popcll(cand.a) + __popcll(cand.b)) : 0u;
-#pragma unroll
-            for (int o = 32; o >= 1; o >>= 1) cnt += __shfl_xor(cnt, o);
+            // the wavefront's best score (+1; 0 = no feasible node), its
+            // lowest node and the tie count
+            const uint32_t top = wave_max_u32(has ? sc + 1 : 0u);
+            const bool at_top = has && sc + 1 == top;
+            const uint32_t nmin = wave_min_u32(at_top ? node : 0xFFFFFFFFu);
+            const uint32_t cnt = wave_add_u32(at_top ? static_cast<uint32_t>(__popcll(cand.a) + __popcll(cand.b)) : 0u);
+            const uint64_t key = top ? (static_cast<uint64_t>(top) << 32) | (0xFFFFFFFFu - nmin) : 0ull;
             if (lane == 0) {
                 part_key[static_cast<int64_t>(tile) * I + r] = key;
                 part_cnt[static_cast<int64_t>(tile) * I + r] = cnt;
@@ -1360,9 +1456,9 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
                             plane_bytes, L, N);
     // room for a header per term and 4 entries per expression; rows beyond it decode on the fly
     const int64_t prog_cap = std::min<int64_t>(static_cast<int64_t>(n_terms) + 4 * n_preds + 64, int64_t(1) << 31);
-    uint64_t *present, *planes, *part_key;
-    uint32_t *wbase, *prog, *rec, *part_cnt;
-    int32_t *d_P;
+    uint64_t *present, *planes, *part_key, *ones;
+    uint32_t *wbase, *prog, *rec, *part_cnt, *list_len;
+    int32_t *d_P, *list;
     unsigned long long *prog_used;
     auto carve = [&](Carver &cv) {
         present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
@@ -1370,6 +1466,9 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
         planes = cv.take<uint64_t>(static_cast<size_t>(pmax + 1) * Wp + 2);
         prog = cv.take<uint32_t>(static_cast<size_t>(prog_cap));
         rec = cv.take<uint32_t>(static_cast<size_t>(I) * kPrefRec + kPrefRec);
+        list = cv.take<int32_t>(static_cast<size_t>(I) * kPrefClasses + 1);
+        list_len = cv.take<uint32_t>(kPrefClasses);
+        ones = cv.take<uint64_t>(feasible ? 1 : static_cast<size_t>(W) + 1);
         part_key = cv.take<uint64_t>(static_cast<size_t>(ntiles) * I + 1);
         part_cnt = cv.take<uint32_t>(static_cast<size_t>(ntiles) * I + 1);
         d_P = cv.take<int32_t>(1);
@@ -1392,12 +1491,15 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     }
     if (I == 0) return PC_OK;
     launch_fill_u64(reinterpret_cast<uint64_t *>(prog_used), 1, 0, stream);
+    launch_fill_u32(list_len, kPrefClasses, 0, stream);
+    if (!feasible && W > 0) launch_fill_u64(ones, static_cast<size_t>(W), ~0ull, stream);
     rc = build_planes(ctx, labels, N, L, W, Wp, pmax, present, wbase, planes, d_P, stream);
     if (rc) return rc;
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
     PC_TIMED(ctx, "k_pref_compile", stream,
              hipLaunchKernelGGL(k_pref_compile, dim3(rgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
-                                weight, preds, n_preds, L, present, wbase, prog, prog_cap, prog_used, rec));
+                                weight, preds, n_preds, L, present, wbase, prog, prog_cap, prog_used, rec, list,
+                                list_len));
     PC_LAUNCH_CHECK(ctx);
     if (W > 0) {
         int64_t nchunks = std::max<int64_t>((32768 + ntiles - 1) / ntiles, 1);
@@ -1407,16 +1509,26 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
         const int64_t total = ntiles * nchunks;
         const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
         const int64_t pbytes = static_cast<int64_t>(pmax + 1) * Wp * 8;
-        auto eval = [&](auto kern) {
-            PC_TIMED(ctx, "k_pref_eval", stream,
+        auto eval = [&](auto kern, const char *name) {
+            PC_TIMED(ctx, name, stream,
                      hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, row_off, term_off,
                                         weight, preds, n_preds, L, present, wbase, planes, pbytes, Wp, I,
-                                        static_cast<int32_t>(W), N, feasible, part_key, part_cnt,
+                                        static_cast<int32_t>(W), N, feasible ? feasible : ones, part_key, part_cnt,
                                         static_cast<int32_t>(ntiles), static_cast<int32_t>(nchunks),
-                                        static_cast<int32_t>(rpc)));
+                                        static_cast<int32_t>(rpc), list, list_len,
+                                        feasible ? static_cast<int64_t>(W) : int64_t(0)));
         };
-        if (pbytes < (int64_t(1) << 31)) eval(k_pref_eval<true>);
-        else eval(k_pref_eval<false>);
+        // one launch per class list (sized for I rows; items past a list's
+        // length exit at once)
+        if (pbytes < (int64_t(1) << 31)) {
+            eval(k_pref_eval<true, 0>, "k_pref_eval");
+            eval(k_pref_eval<true, 1>, "k_pref_eval16");
+            eval(k_pref_eval<true, 2>, "k_pref_decode");
+        } else {
+            eval(k_pref_eval<false, 0>, "k_pref_eval");
+            eval(k_pref_eval<false, 1>, "k_pref_eval16");
+            eval(k_pref_eval<false, 2>, "k_pref_decode");
+        }
         PC_LAUNCH_CHECK(ctx);
     }
     PC_TIMED(ctx, "k_pref_final", stream,
