@@ -60,7 +60,7 @@ def _load():
         _lib.orc_probes.argtypes = [P, I64, I64, P, P, I64, I64, P, P, I64, P, P]
         _lib.orc_synthesize.argtypes = [I64, P, P, I64, P, P, I64, P, P, P, P, I64, P, I64, P, P, I64, I64, P,
                                         I64, P, P, P, P, C]
-        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, C]
+        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, P, C]
         _lib.orc_reach.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, P, C]
         _lib.orc_reach_via.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, I64, P, I64, P, P, C]
         _lib.orc_report.argtypes = [I64, P, I64, P, I64, P, I64, P, I64, P, P, I64, P, P, P, P, P, P]
@@ -220,10 +220,11 @@ def synthesize(V, port_off, port_peer, region, src, target, allowed, via, forbid
 
 
 def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=None,
-          n_ports=None, n_rules=None, nthreads=0, watch=None):
+          n_ports=None, n_rules=None, nthreads=0, watch=None, summary=False):
     """Trace records for the given trace indices (all by default).  With a
-    watch list [T, K] (switch ids, -1 = unused) also returns the visit words:
-    (out, visit, flags)."""
+    watch list [T, K] (switch ids, -1 = unused) also returns the visit words,
+    with summary=True the visited-switch summaries (u64, bit s mod 64):
+    (out, [visit,] [vsum,] flags)."""
     lib = _load()
     T = ingress.shape[0]
     if idx is None:
@@ -238,6 +239,7 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
         assert watch.ndim == 2 and watch.shape[0] == T
         K = watch.shape[1]
         visit = np.zeros(idx.shape[0], np.uint32)
+    vsum = np.zeros(idx.shape[0], np.uint64) if summary else None
     n_ports = port_peer.shape[0] if n_ports is None else n_ports
     n_rules = rules.shape[0] if n_rules is None else n_rules
     lib.orc_trace(S, _p(np.ascontiguousarray(port_off, np.int32)),
@@ -245,10 +247,14 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
                   _p(np.ascontiguousarray(jur, np.uint8)), _p(np.ascontiguousarray(rule_off, np.int32)),
                   _p(np.ascontiguousarray(rules)), n_rules,
                   _p(np.ascontiguousarray(hdr, np.uint32)), _p(np.ascontiguousarray(ingress, np.int32)),
-                  T, ttl, _p(watch), K, _p(idx), idx.shape[0], _p(out), _p(visit), _p(err), nthreads)
+                  T, ttl, _p(watch), K, _p(idx), idx.shape[0], _p(out), _p(visit), _p(vsum), _p(err), nthreads)
+    res = [out]
     if watch is not None:
-        return out, visit, int(err[0])
-    return out, int(err[0])
+        res.append(visit)
+    if summary:
+        res.append(vsum)
+    res.append(int(err[0]))
+    return tuple(res)
 
 
 def reach(V, adj_off, adj, region, src, allowed, target=None, qidx=None, n_adj=None, nthreads=0):

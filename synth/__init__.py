@@ -626,6 +626,35 @@ def cfg2(seed=1):
     return selector_workload(seed, 100_000, 64, 16_384, name="cfg2")
 
 
+def mutate_tables(seed, port_off, rule_off, rules, switches, resize=False):
+    """New flow tables in which the listed switches' rules are rewritten:
+    every rule of such a switch gets a fresh priority (a permutation of the
+    old ones) and a fresh action (a random local port, DROP with probability
+    0.1).  resize=True also drops the last rule of every other listed switch
+    and repeats the first rule of the rest, so table sizes change too.
+    Other switches keep their rules.  Returns (rule_off, rules)."""
+    rng = np.random.default_rng([seed, 16])
+    rule_off = np.asarray(rule_off, np.int64)
+    S = rule_off.shape[0] - 1
+    chosen = set(int(x) for x in switches if 0 <= int(x) < S)
+    parts = []
+    for s_ in range(S):
+        seg = rules[rule_off[s_]:rule_off[s_ + 1]].copy()
+        if s_ in chosen and seg.shape[0] > 0:
+            seg["priority"] = rng.permutation(seg["priority"])
+            npt = int(port_off[s_ + 1] - port_off[s_])
+            act = rng.integers(0, max(npt, 1), size=seg.shape[0]).astype(np.uint16)
+            act[rng.random(seg.shape[0]) < 0.1] = 0xFFFF
+            seg["action"] = act
+            if resize:
+                seg = seg[:-1] if s_ % 2 == 0 else np.concatenate([seg, seg[:1]])
+        parts.append(seg)
+    new_off = np.zeros(S + 1, np.int32)
+    new_off[1:] = np.cumsum([p.shape[0] for p in parts])
+    new_rules = np.concatenate(parts) if parts else rules[:0].copy()
+    return new_off, new_rules
+
+
 def trace_workload(seed, k, J, R, T, ttl, n_flows, p_care=0.7, variant="rpath",
                    name="trace"):
     """Flow tracing only on a k-ary fat-tree with J jurisdictions by pod and
