@@ -27,6 +27,8 @@
  *                         six operators, label-inventory flags).
  *   - pc_score_preferred : the best feasible node under weighted preferred
  *                         terms (secondary placement objectives).
+ *   - pc_trace_flows_delta : re-traces only the traces whose walk visited a
+ *                         switch whose rules changed.
  *   - pc_synthesize_paths : the step before validation -- the path
  *                         scheduler's search for a compliant path and its
  *                         compilation into per-hop flow rules.
@@ -61,7 +63,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 7
+#define PC_VERSION 8
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -367,6 +369,41 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
               int32_t W, const uint32_t *popcnt, int32_t N, const pc_trace_out *traces, int32_t T,
               const pc_flow_expect *expect, const int32_t *reach, int32_t Q, uint64_t *pass,
               uint8_t *reason, pc_summary *summary, void *stream);
+
+/*
+ * A2+A3, incremental re-validation after rule changes.  The paper's
+ * validator re-checks continuously as the deployed state changes (abstract;
+ * network state that changes with placement, Domain-specific performance).
+ * A walk reads only the flow tables of the switches it visits, so when the
+ * rules of some switches change, only traces whose walk visited one of
+ * them can change.  Every trace carries a visited-switch summary: bit
+ * (s mod 64) of vsum[t] for every switch s on its walk (ingress included;
+ * 0 for an invalid ingress).
+ * C < 0  : trace every trace from scratch, as pc_trace_flows, and write
+ *          vsum; *n_retraced = T.
+ * C >= 0 : out[t] and vsum[t] hold the results of an earlier call on the
+ *          same topology, headers, ingresses and ttl, and the tables
+ *          passed now differ from those only in the rules of the switches
+ *          changed[0 .. C) (table sizes may change).  Every trace whose
+ *          vsum meets the bit of a changed switch is traced again on the
+ *          tables passed now and its out / vsum are overwritten; the others
+ *          are left as they are.  The result equals a call with C < 0 on
+ *          the tables passed now.  *n_retraced = the number of traces
+ *          traced again (shared bits make it a superset of the traces that
+ *          actually visited a changed switch).
+ * changed    : int32 [C]; ids outside [0, S) are ignored (PC_DERR_SWITCH),
+ *              repeats are harmless.
+ * out        : pc_trace_out [T], read and written.
+ * vsum       : uint64 [T], read and written.
+ * n_retraced : int32, device memory.
+ * The tables passed are prepared and swept for data errors on every call,
+ * as in pc_trace_flows; the ingress sweep covers every trace.
+ */
+int pc_trace_flows_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
+                         int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
+                         int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,
+                         const int32_t *changed, int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *n_retraced,
+                         void *stream);
 
 /*
  * Waypoint and forbidden-switch constraints on realised paths.  The paper's

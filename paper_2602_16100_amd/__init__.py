@@ -94,6 +94,7 @@ def lib():
     L.pc_masked_reach.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, P]
     L.pc_report.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P]
     L.pc_trace_flows_watch.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, I32, P, P, P]
+    L.pc_trace_flows_delta.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, I32, P, P, P, P]
     L.pc_masked_reach_via.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, I32, P, I32, P, P]
     L.pc_report_paths.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P, P, P]
     L.pc_profile.argtypes = [P, C]
@@ -107,7 +108,7 @@ EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_e
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
             "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths",
             "pc_update_nodes", "pc_eval_selectors_count", "pc_probe_selectors", "pc_report_counts",
-            "pc_score_preferred")
+            "pc_score_preferred", "pc_trace_flows_delta")
 
 
 class Context:
@@ -440,6 +441,28 @@ def pc_report(intents, feasible, popcnt, N, traces, expect, reach, pass_=None, r
                               _ptr(reach) if Q else None, Q, _ptr(pass_) if I else None, _ptr(reason) if I else None,
                               _ptr(summary), _stream(stream)))
     return pass_, reason, summary
+
+
+def pc_trace_flows_delta(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, out, vsum, changed=None,
+                         n_ports=None, n_rules=None, ctx=None, stream=None):
+    """A2+A3 incremental re-trace.  changed=None: trace everything from
+    scratch into out (uint8 [T, 12]) and vsum (int64 [T], the visited-switch
+    summaries).  changed = int32 tensor of switch ids: out / vsum hold the
+    results on the previous tables; only traces whose summary meets a
+    changed switch are traced again on the tables given.  Returns the number
+    of traces traced again (an int32 device tensor of one element)."""
+    ctx = ctx or context()
+    T = int(ingress.shape[0])
+    n_ports = int(port_peer.shape[0]) if n_ports is None else int(n_ports)
+    n_rules = int(rules.shape[0]) if n_rules is None else int(n_rules)
+    C = -1 if changed is None else int(changed.shape[0])
+    n = torch.empty(1, dtype=torch.int32, device=ingress.device)
+    ctx.check(lib().pc_trace_flows_delta(ctx.handle, int(S), _ptr(port_off), _ptr(port_peer) if n_ports else None,
+                                         n_ports, _ptr(jur), _ptr(rule_off), _ptr(rules) if n_rules else None,
+                                         n_rules, _ptr(hdr) if T else None, _ptr(ingress) if T else None, T,
+                                         int(ttl), _ptr(changed) if C > 0 else None, C, _ptr(out) if T else None,
+                                         _ptr(vsum) if T else None, _ptr(n), _stream(stream)))
+    return n
 
 
 def pc_trace_flows_watch(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, watch, n_ports=None,

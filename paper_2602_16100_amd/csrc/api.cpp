@@ -47,6 +47,8 @@ int pc_ensure_arena(pc_ctx *ctx, size_t bytes) { return ensure_buffer(ctx, &ctx-
 
 int pc_ensure_aux(pc_ctx *ctx, size_t bytes) { return ensure_buffer(ctx, &ctx->aux, &ctx->aux_bytes, bytes); }
 
+int pc_ensure_delta(pc_ctx *ctx, size_t bytes) { return ensure_buffer(ctx, &ctx->delta, &ctx->delta_bytes, bytes); }
+
 static hipEvent_t take_event(pc_ctx *ctx)
 {
     if (!ctx->ev_free.empty()) {
@@ -163,6 +165,7 @@ int pc_destroy(pc_ctx *ctx)
     (void)hipDeviceSynchronize();
     if (ctx->arena) (void)hipFree(ctx->arena);
     if (ctx->aux) (void)hipFree(ctx->aux);
+    if (ctx->delta) (void)hipFree(ctx->delta);
     if (ctx->d_err) (void)hipFree(ctx->d_err);
     if (ctx->d_small) (void)hipFree(ctx->d_small);
     if (ctx->h_small) (void)hipHostFree(ctx->h_small);
@@ -363,7 +366,7 @@ int pc_trace_flows(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_
     if (T == 0 && S == 0) return PC_OK;
     PC_HIP(ctx, hipSetDevice(ctx->device));
     return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                     nullptr, 0, out, nullptr, static_cast<hipStream_t>(stream));
+                     nullptr, 0, out, nullptr, nullptr, static_cast<hipStream_t>(stream));
 }
 
 int pc_trace_flows_watch(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
@@ -385,7 +388,29 @@ int pc_trace_flows_watch(pc_ctx *ctx, int32_t S, const int32_t *port_off, const 
     if (T == 0 && S == 0) return PC_OK;
     PC_HIP(ctx, hipSetDevice(ctx->device));
     return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                     watch, K, out, T ? visit : nullptr, static_cast<hipStream_t>(stream));
+                     watch, K, out, T ? visit : nullptr, nullptr, static_cast<hipStream_t>(stream));
+}
+
+int pc_trace_flows_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
+                         int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
+                         int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,
+                         const int32_t *changed, int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *n_retraced,
+                         void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(S >= 0 && T >= 0 && n_ports >= 0 && n_rules >= 0, "pc_trace_flows_delta: negative size");
+    PC_REQUIRE(ttl >= 0 && ttl <= 255, "pc_trace_flows_delta: ttl=%d out of [0, 255]", ttl);
+    PC_REQUIRE(n_rules < (int64_t(1) << 40), "pc_trace_flows_delta: n_rules too large");
+    PC_REQUIRE(T == 0 || (hdr && ingress && out && vsum), "pc_trace_flows_delta: null hdr/ingress/out/vsum");
+    PC_REQUIRE(n_retraced, "pc_trace_flows_delta: null n_retraced");
+    PC_REQUIRE(C <= 0 || changed, "pc_trace_flows_delta: null changed");
+    PC_REQUIRE(S == 0 || (port_off && rule_off && jur), "pc_trace_flows_delta: null topology array");
+    PC_REQUIRE(n_ports == 0 || port_peer, "pc_trace_flows_delta: null port_peer");
+    PC_REQUIRE(n_rules == 0 || rules, "pc_trace_flows_delta: null rules");
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_trace_delta(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
+                           changed, C, out, vsum, n_retraced, static_cast<hipStream_t>(stream));
 }
 
 int pc_masked_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,

@@ -64,6 +64,9 @@ __device__ __forceinline__ uint32_t watch_bits(const int32_t *__restrict__ watch
     return m;
 }
 
+// Bit of switch s in a visited-switch summary.
+__device__ __forceinline__ uint64_t sum_bit(int32_t s) { return 1ull << (s & 63); }
+
 __device__ __forceinline__ uint32_t jur_bit(const uint8_t *jur, int32_t s)
 {
     const uint32_t j = jur[s];
@@ -248,7 +251,8 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
                                                  int32_t *__restrict__ live, int32_t *__restrict__ nlive,
                                                  int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
-                                                 uint32_t *__restrict__ visit, uint32_t *__restrict__ d_err)
+                                                 uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
+                                                 uint32_t *__restrict__ d_err)
 {
     __shared__ int32_t nloc, base;
     if (threadIdx.x == 0) nloc = 0;
@@ -268,10 +272,12 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
             o.state = PC_MISS;
             out[t] = o;
             if (visit) visit[t] = 0;
+            if (vsum) vsum[t] = 0;
         } else {
             cur[t] = s;
             jm[t] = jur_bit(jur, s);
             if (visit) visit[t] = watch_bits(watch, K, t, s);
+            if (vsum) vsum[t] = sum_bit(s);
             hops[t] = 0;
             rank[t] = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
             slot = atomicAdd(&nloc, 1);
@@ -379,6 +385,7 @@ struct Level {
     const int32_t *watch;   // [T][K] switches whose visit is recorded
     int32_t K;
     uint32_t *visit;        // [T] or nullptr
+    uint64_t *vsum;         // [T] visited-switch summaries or nullptr
 };
 
 // Per level: bucket offsets boff = exclusive scan of counts (which are
@@ -645,6 +652,7 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
                 lv.hops[t] = h + 1;
                 lv.jm[t] |= jur_bit(lv.jur, next);
                 if (lv.visit) lv.visit[t] |= watch_bits(lv.watch, lv.K, t, next);
+                if (lv.vsum) lv.vsum[t] |= sum_bit(next);
                 lv.rank[t] = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
                 slot = atomicAdd(&nmove, 1);
             }
@@ -670,7 +678,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                                                  const int32_t *__restrict__ cur, const uint32_t *__restrict__ jm0,
                                                  const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
-                                                 uint32_t *__restrict__ visit)
+                                                 uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum)
 {
     __shared__ unsigned long long best;
     const int32_t n = *nlive;
@@ -680,6 +688,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
         int32_t s = cur[t];
         uint32_t jm = jm0[t];
         uint32_t vis = visit ? visit[t] : 0u;
+        uint64_t vs = vsum ? vsum[t] : 0ull;
         int32_t hops = hops0[t];
         for (;;) {
             if (threadIdx.x == 0) best = kNoMatch;
@@ -706,6 +715,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                 if (threadIdx.x == 0) {
                     write_out(out, t, jm, s, port, hops, state);
                     if (visit) visit[t] = vis;
+                    if (vsum) vsum[t] = vs;
                 }
                 break;
             }
@@ -713,8 +723,86 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
             hops += 1;
             jm |= jur_bit(jur, s);
             if (visit) vis |= watch_bits(watch, K, t, s);
+            if (vsum) vs |= sum_bit(s);
         }
     }
+}
+
+// ---------------------------------------------------------------- deltas
+// Summary bits of the changed switches (ids outside [0, S) are ignored and
+// raise SWITCH); one workgroup.
+__global__ __launch_bounds__(256) void k_delta_mask(const int32_t *__restrict__ changed, int32_t C, int32_t S,
+                                                    unsigned long long *__restrict__ mask,
+                                                    uint32_t *__restrict__ d_err)
+{
+    __shared__ unsigned long long m;
+    if (threadIdx.x == 0) m = 0;
+    __syncthreads();
+    uint64_t mine = 0;
+    bool bad = false;
+    for (int32_t i = threadIdx.x; i < C; i += blockDim.x) {
+        const int32_t s = changed[i];
+        if (s < 0 || s >= S) bad = true;
+        else mine |= sum_bit(s);
+    }
+    if (mine) atomicOr(&m, static_cast<unsigned long long>(mine));
+    if (__ballot(bad) && (threadIdx.x & 63) == 0) atomicOr(d_err, PC_DERR_SWITCH);
+    __syncthreads();
+    if (threadIdx.x == 0) *mask = m;
+}
+
+// The traces whose summary meets the mask, in a list (one counter update per
+// wavefront); also the ingress sweep of the SWITCH flag over every trace.
+__global__ __launch_bounds__(256) void k_delta_select(const uint64_t *__restrict__ vsum, const int32_t *__restrict__ ingress,
+                                                      int32_t T, int32_t S, const unsigned long long *__restrict__ mask,
+                                                      int32_t *__restrict__ list, uint32_t *__restrict__ count,
+                                                      uint32_t *__restrict__ d_err)
+{
+    const uint64_t m = *mask;
+    const int lane = threadIdx.x & 63;
+    for (int64_t base = static_cast<int64_t>(blockIdx.x) * blockDim.x; base < T;
+         base += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int64_t t = base + threadIdx.x;
+        const bool in = t < T;
+        const bool sel = in && (vsum[t] & m) != 0;
+        const int32_t s = in ? ingress[t] : 0;
+        if (__ballot(in && (s < 0 || s >= S)) && lane == 0) atomicOr(d_err, PC_DERR_SWITCH);
+        const uint64_t b = __ballot(sel);
+        if (b == 0) continue;
+        const int leader = __builtin_ctzll(b);
+        uint32_t off = 0;
+        if (lane == leader) off = atomicAdd(count, static_cast<uint32_t>(__popcll(b)));
+        off = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), leader));
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(b), 0u));
+        if (sel) list[off + below] = static_cast<int32_t>(t);
+    }
+}
+
+__global__ __launch_bounds__(256) void k_delta_gather(const int32_t *__restrict__ list, int32_t n,
+                                                      const pc_key *__restrict__ hdr,
+                                                      const int32_t *__restrict__ ingress, pc_key *__restrict__ hdr_c,
+                                                      int32_t *__restrict__ ing_c)
+{
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        const int32_t t = list[i];
+        hdr_c[i] = hdr[t];
+        ing_c[i] = ingress[t];
+    }
+}
+
+__global__ __launch_bounds__(256) void k_delta_scatter(const int32_t *__restrict__ list, int32_t n,
+                                                       const pc_trace_out *__restrict__ out_c,
+                                                       const uint64_t *__restrict__ vsum_c,
+                                                       pc_trace_out *__restrict__ out, uint64_t *__restrict__ vsum,
+                                                       const uint32_t *__restrict__ count, int32_t *__restrict__ n_out)
+{
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
+        const int32_t t = list[i];
+        out[t] = out_c[i];
+        vsum[t] = vsum_c[i];
+    }
+    if (blockIdx.x == 0 && threadIdx.x == 0) *n_out = static_cast<int32_t>(*count);
 }
 
 unsigned grid_for(int64_t n, int threads)
@@ -729,7 +817,7 @@ unsigned grid_for(int64_t n, int threads)
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
               const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *watch, int32_t K,
-              pc_trace_out *out, uint32_t *visit, hipStream_t stream)
+              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, hipStream_t stream)
 {
     struct Bufs {
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
@@ -808,7 +896,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
     }
     PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
-                       B.hops, B.rank, B.live0, d_n, B.counts0, out, watch, K, visit, ctx->d_err));
+                       B.hops, B.rank, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
@@ -836,7 +924,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_TIMED(ctx, "k_tr_walk", stream,
                      hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
                                         rule_off, rules, B.gcount, B.gofs, B.filt, hdr, ttl, live_cur, n_cur, B.cur,
-                                        B.jm, B.hops, out, watch, K, visit));
+                                        B.jm, B.hops, out, watch, K, visit, vsum));
             PC_LAUNCH_CHECK(ctx);
             break;
         }
@@ -848,7 +936,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                                     B.cur, B.rank, B.boff, B.bucket));
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
         const Level lv{S,     T,     port_off, port_peer, n_ports, jur,   ttl, B.cur, B.jm,
-                       B.hops, B.rank, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit};
+                       B.hops, B.rank, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit, vsum};
         // at most nlive / kChunk + (switches with a partial chunk) items
         const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);
         PC_TIMED(ctx, "k_tr_match", stream,
@@ -873,5 +961,62 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         tmp = cnt_cur; cnt_cur = cnt_nxt; cnt_nxt = tmp;
         tmp = n_cur; n_cur = n_nxt; n_nxt = tmp;
     }
+    return PC_OK;
+}
+
+int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
+                    const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
+                    const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *changed,
+                    int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *n_retraced, hipStream_t stream)
+{
+    if (C < 0) {  // every trace, from scratch
+        launch_fill_u32(reinterpret_cast<uint32_t *>(n_retraced), 1, static_cast<uint32_t>(T), stream);
+        if (T == 0 && S == 0) return PC_OK;
+        return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
+                         nullptr, 0, out, nullptr, T ? vsum : nullptr, stream);
+    }
+    // compacted traces live in their own buffer: run_trace carves the arena
+    const size_t Tn = static_cast<size_t>(T) + 1;
+    const size_t need = 256 * 8 + Tn * (sizeof(int32_t) * 2 + sizeof(pc_key) + sizeof(pc_trace_out) + 8);
+    int rc = pc_ensure_delta(ctx, need);
+    if (rc) return rc;
+    Carver cv{ctx->delta, 0};
+    unsigned long long *mask = cv.take<unsigned long long>(1);
+    uint32_t *count = cv.take<uint32_t>(1);
+    int32_t *list = cv.take<int32_t>(Tn);
+    pc_key *hdr_c = cv.take<pc_key>(Tn);
+    int32_t *ing_c = cv.take<int32_t>(Tn);
+    pc_trace_out *out_c = cv.take<pc_trace_out>(Tn);
+    uint64_t *vsum_c = cv.take<uint64_t>(Tn);
+    launch_fill_u32(count, 1, 0, stream);
+    PC_TIMED(ctx, "k_delta_mask", stream,
+             hipLaunchKernelGGL(k_delta_mask, dim3(1), dim3(256), 0, stream, changed, C, S, mask, ctx->d_err));
+    PC_LAUNCH_CHECK(ctx);
+    if (T > 0) {
+        PC_TIMED(ctx, "k_delta_select", stream,
+                 hipLaunchKernelGGL(k_delta_select, dim3(grid_for(T, 256)), dim3(256), 0, stream, vsum, ingress, T, S,
+                                    mask, list, count, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, count, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
+    PC_HIP(ctx, hipStreamSynchronize(stream));
+    const int32_t n = ctx->h_small[0];
+    if (n > 0) {
+        PC_TIMED(ctx, "k_delta_gather", stream,
+                 hipLaunchKernelGGL(k_delta_gather, dim3(grid_for(n, 256)), dim3(256), 0, stream, list, n, hdr,
+                                    ingress, hdr_c, ing_c));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    // the new tables are prepared (and swept for data errors) even when no
+    // trace needs them
+    if (S > 0 || n > 0) {
+        rc = run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr_c, ing_c, n, ttl,
+                       nullptr, 0, out_c, nullptr, n ? vsum_c : nullptr, stream);
+        if (rc) return rc;
+    }
+    PC_TIMED(ctx, "k_delta_scatter", stream,
+             hipLaunchKernelGGL(k_delta_scatter, dim3(grid_for(n > 0 ? n : 1, 256)), dim3(256), 0, stream, list, n,
+                                out_c, vsum_c, out, vsum, count, n_retraced));
+    PC_LAUNCH_CHECK(ctx);
     return PC_OK;
 }

@@ -1,0 +1,171 @@
+"""Parity of pc_trace_flows_delta (through the C ABI) with the CPU oracle:
+after the rules of some switches change, re-tracing only the traces whose
+visited-switch summary meets a changed switch gives exactly the oracle's
+full trace on the new tables (records and summaries, bit-exact), starting
+from the oracle's old results or from the GPU's own, over chains of
+changes, with resized tables, repeated and out-of-range ids, no change,
+every switch changed and no traces; and at the combined workload's size."""
+import numpy as np
+import pytest
+
+import synth
+
+pytestmark = pytest.mark.gpu
+F_SWITCH = 8
+
+
+@pytest.fixture(scope="module")
+def g():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no GPU")
+    import gpu_run
+    return gpu_run
+
+
+def _run(wl, rule_off, rules, out, vsum, changed):
+    """One delta call; out / vsum as numpy (records, u64) or None for a
+    first call.  Returns (records, vsum, n_retraced, flags)."""
+    import torch
+    import paper_2602_16100_amd as pc
+    ctx = pc.context()
+    ctx.data_errors(clear=True)
+    T = wl["ingress"].shape[0]
+    d = lambda a: pc.to_device(a, "cuda")
+    o = torch.zeros((T, 12), dtype=torch.uint8, device="cuda") if out is None else \
+        torch.from_numpy(np.ascontiguousarray(out).view(np.uint8).reshape(T, 12).copy()).cuda()
+    v = torch.zeros(T, dtype=torch.int64, device="cuda") if vsum is None else \
+        torch.from_numpy(np.ascontiguousarray(vsum, np.uint64).view(np.int64).copy()).cuda()
+    ch = None if changed is None else torch.from_numpy(np.ascontiguousarray(changed, np.int32)).cuda()
+    n = pc.pc_trace_flows_delta(wl["S"], d(wl["port_off"]), d(wl["port_peer"]), d(wl["jur"]), d(rule_off), d(rules),
+                                d(np.ascontiguousarray(wl["hdr"], np.uint32)), d(wl["ingress"]), wl["ttl"], o, v,
+                                changed=ch)
+    torch.cuda.synchronize()
+    flags = ctx.data_errors(clear=True)
+    return (pc.records(o, pc.TRACE_OUT_DT), v.cpu().numpy().view(np.uint64), int(n.cpu().numpy()[0]), flags)
+
+
+def _oracle(orc, wl, rule_off, rules, idx=None):
+    return orc.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], rule_off, rules, wl["hdr"], wl["ingress"],
+                     wl["ttl"], idx=idx, summary=True)
+
+
+def _same_records(a, b):
+    for f in ("jmask", "last_switch", "last_port", "hops", "state"):
+        bad = np.flatnonzero(a[f] != b[f])
+        assert bad.size == 0, f"{f}: first mismatch at trace {bad[0]}: gpu {a[bad[0]]} oracle {b[bad[0]]}"
+
+
+def _mask(changed):
+    m = 0
+    for s in changed:
+        m |= 1 << (int(s) & 63)
+    return np.uint64(m)
+
+
+def _workloads():
+    return {"cfg1-dense": lambda: synth.cfg1(0, "dense"),
+            "fat-tree-80-dense": lambda: synth.trace_workload(5, 8, 4, 24, 3000, 12, 200, variant="dense"),
+            "fat-tree-320-rpath": lambda: synth.trace_workload(6, 16, 8, 300, 20000, 32, 4000)}
+
+
+@pytest.mark.parametrize("name", list(_workloads()))
+def test_first_call_matches_oracle(g, orc, name):
+    wl = _workloads()[name]()
+    rec, vs, n, flags = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
+    ro, vo, err = _oracle(orc, wl, wl["rule_off"], wl["rules"])
+    _same_records(rec, ro)
+    assert np.array_equal(vs, vo) and n == wl["ingress"].shape[0] and flags == err
+
+
+@pytest.mark.parametrize("resize", [False, True])
+@pytest.mark.parametrize("name", list(_workloads()))
+def test_delta_from_oracle_state(g, orc, name, resize):
+    wl = _workloads()[name]()
+    S = wl["S"]
+    ro, vo, _ = _oracle(orc, wl, wl["rule_off"], wl["rules"])
+    changed = np.random.default_rng(3).choice(S, size=min(4, S), replace=False)
+    r_off2, rules2 = synth.mutate_tables(3, wl["port_off"], wl["rule_off"], wl["rules"], changed, resize=resize)
+    rec, vs, n, flags = _run(wl, r_off2, rules2, ro, vo, changed)
+    ro2, vo2, err2 = _oracle(orc, wl, r_off2, rules2)
+    _same_records(rec, ro2)
+    assert np.array_equal(vs, vo2) and flags == err2
+    assert n == int(((vo & _mask(changed)) != 0).sum()) and 0 < n < wl["ingress"].shape[0]
+
+
+@pytest.mark.parametrize("name", ["fat-tree-80-dense", "fat-tree-320-rpath"])
+def test_chained_deltas_on_gpu(g, orc, name):
+    wl = _workloads()[name]()
+    S = wl["S"]
+    rule_off, rules = wl["rule_off"], wl["rules"]
+    rec, vs, _, _ = _run(wl, rule_off, rules, None, None, None)
+    rng = np.random.default_rng(9)
+    for step in range(4):
+        changed = rng.choice(S, size=int(rng.integers(1, 6)), replace=True)  # repeats allowed
+        rule_off, rules = synth.mutate_tables(20 + step, wl["port_off"], rule_off, rules, changed, resize=step % 2 == 1)
+        rec, vs, n, flags = _run(wl, rule_off, rules, rec, vs, changed)
+        ro, vo, err = _oracle(orc, wl, rule_off, rules)
+        _same_records(rec, ro)
+        assert np.array_equal(vs, vo) and flags == err
+
+
+def test_edge_cases(g, orc):
+    wl = synth.trace_workload(5, 8, 4, 24, 3000, 12, 200, variant="dense")
+    S, T = wl["S"], wl["ingress"].shape[0]
+    ingress = wl["ingress"].copy()
+    ingress[:4] = [-1, S, -7, 10 ** 6]  # invalid ingresses: MISS records, empty summaries, SWITCH flag
+    wl.arrays["ingress"] = ingress
+    ro, vo, err = _oracle(orc, wl, wl["rule_off"], wl["rules"])
+    assert err == F_SWITCH and (vo[:4] == 0).all()
+    rec, vs, n, flags = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
+    _same_records(rec, ro)
+    assert np.array_equal(vs, vo) and flags == F_SWITCH
+    # no change: nothing traced again, nothing moves
+    rec2, vs2, n, flags = _run(wl, wl["rule_off"], wl["rules"], ro, vo, np.zeros(0, np.int32))
+    _same_records(rec2, ro)
+    assert np.array_equal(vs2, vo) and n == 0 and flags == F_SWITCH
+    # out-of-range ids are ignored and flagged; a valid one still counts
+    r_off2, rules2 = synth.mutate_tables(4, wl["port_off"], wl["rule_off"], wl["rules"], [17])
+    rec3, vs3, n, flags = _run(wl, r_off2, rules2, ro, vo, np.array([-1, 17, S, 17], np.int32))
+    ro3, vo3, err3 = _oracle(orc, wl, r_off2, rules2)
+    _same_records(rec3, ro3)
+    assert np.array_equal(vs3, vo3) and flags == err3 | F_SWITCH and n == int(((vo & _mask([17])) != 0).sum())
+    # every switch changed: every trace with a valid ingress is traced again
+    r_off4, rules4 = synth.mutate_tables(5, wl["port_off"], wl["rule_off"], wl["rules"], np.arange(S), resize=True)
+    rec4, vs4, n, flags = _run(wl, r_off4, rules4, ro, vo, np.arange(S, dtype=np.int32))
+    ro4, vo4, _ = _oracle(orc, wl, r_off4, rules4)
+    _same_records(rec4, ro4)
+    assert np.array_equal(vs4, vo4) and n == T - 4
+    # no traces
+    wl0 = synth.trace_workload(5, 8, 4, 24, 3000, 12, 200, variant="dense")
+    wl0.arrays["hdr"] = wl0["hdr"][:0]
+    wl0.arrays["ingress"] = wl0["ingress"][:0]
+    rec5, vs5, n, flags = _run(wl0, wl0["rule_off"], wl0["rules"], np.zeros(0, ro.dtype), np.zeros(0, np.uint64),
+                               np.array([3], np.int32))
+    assert n == 0 and rec5.shape[0] == 0
+
+
+def test_delta_combined_workload_size(g, orc):
+    """The combined workload's 699,050 traces over 2,880 switches of 16,384
+    rules: a full first call, then the tables of one core, two aggregation
+    and three edge switches rewritten.  Every record and summary equals a
+    full GPU trace on the new tables; 4,000 sampled traces (half of them
+    re-traced ones) equal the oracle."""
+    wl = synth.cfg5()
+    rec, vs, n, _ = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
+    k, h = 48, 24  # pod p: edge switches p*k + [0, h), aggregation p*k + [h, k); core from k*k
+    changed = np.array([k * k + 5, 3 * k + h + 6, 10 * k + h + 16, 0, 5 * k + 2, 20 * k + 7], np.int32)
+    assert changed.max() < wl["S"]
+    r_off2, rules2 = synth.mutate_tables(8, wl["port_off"], wl["rule_off"], wl["rules"], changed)
+    rec2, vs2, n2, flags = _run(wl, r_off2, rules2, rec, vs, changed)
+    full, vfull, _, _ = _run(wl, r_off2, rules2, None, None, None)
+    _same_records(rec2, full)
+    assert np.array_equal(vs2, vfull) and flags == 0
+    hit = np.flatnonzero((vs & _mask(changed)) != 0)
+    assert n2 == hit.shape[0] and 0 < n2 < wl["ingress"].shape[0]
+    rng = np.random.default_rng(4)
+    idx = np.sort(np.concatenate([rng.choice(hit, 2000, replace=False),
+                                  rng.choice(wl["ingress"].shape[0], 2000, replace=False)]))
+    ro, vo, err = _oracle(orc, wl, r_off2, rules2, idx=idx)
+    _same_records(rec2[idx], ro)
+    assert np.array_equal(vs2[idx], vo) and err == 0
