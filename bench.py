@@ -72,16 +72,18 @@ def parse():
                     help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--only", default="all", choices=["all", "sel", "trace", "reach", "paths", "affinity", "preferred",
-                                                     "synthesis", "update", "verdict"],
+                                                     "synthesis", "update", "verdict", "delta"],
                     help="profiling aid: time one stage only (the JSON line then covers that stage); 'paths' "
                          "times only the pass with waypoint / forbidden-switch constraints, 'affinity' only the "
                          "node-affinity pass, 'preferred' only the preferred-affinity pass, 'synthesis' only the "
                          "path-synthesis pass, 'update' only the incremental re-evaluation, 'verdict' only the "
-                         "verdict-only pass")
+                         "verdict-only pass, 'delta' only the re-trace after rule changes")
     ap.add_argument("--no-paths", action="store_true",
                     help="skip the second timed pass with waypoint / forbidden-switch constraints")
     ap.add_argument("--no-affinity", action="store_true",
                     help="skip the timed pass of full node affinity over the same cluster")
+    ap.add_argument("--no-rule-delta", action="store_true",
+                    help="skip the timed incremental re-trace after rule changes")
     ap.add_argument("--no-preferred", action="store_true",
                     help="skip the timed pass of preferred node affinity (best feasible node per row)")
     ap.add_argument("--no-verdict-only", action="store_true",
@@ -517,6 +519,76 @@ def time_update(args, wl, pc, ctx, D, feasible, popcnt):
     return out
 
 
+def time_rule_delta(args, wl, pc, ctx, D):
+    """Incremental re-trace (pc_trace_flows_delta) after rewriting the rules
+    of 1 core switch, 1 edge switch and 16 random switches of the combined
+    workload's fat-tree, against a full pc_trace_flows on the new tables.
+    The previous records and summaries are restored before each timed call;
+    the timed region is the call alone."""
+    import torch
+    import synth
+    dev = D["ingress"].device
+    S, T, ttl = wl["S"], wl["T"], wl["ttl"]
+    out0 = torch.empty((T, 12), dtype=torch.uint8, device=dev)
+    vs0 = torch.empty(T, dtype=torch.int64, device=dev)
+    pc.pc_trace_flows_delta(S, D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                            D["ingress"], ttl, out0, vs0, ctx=ctx)
+    out, vs = out0.clone(), vs0.clone()
+    k = int(round((4 * S / 5) ** 0.5))  # fat-tree: S = 5 k^2 / 4
+    rng = np.random.default_rng([wl.seed, 17])
+    cases = {"1 core switch": np.array([k * k + 7], np.int32), "1 edge switch": np.array([3 * k + 1], np.int32),
+             "16 switches": rng.choice(S, size=16, replace=False).astype(np.int32)}
+    res = {"traces": T, "switches": S, "per_change": {}}
+    vs_host = vs0.cpu().numpy().view(np.uint64)
+    for name, changed in cases.items():
+        r_off, rules = synth.mutate_tables(wl.seed, wl["port_off"], wl["rule_off"], wl["rules"], changed)
+        Dr = {"rule_off": pc.to_device(r_off, dev), "rules": pc.to_device(rules, dev)}
+        Dc = pc.to_device(changed, dev)
+        t_d, t_f = [], []
+        n = None
+        for it in range(args.warmup + args.steps):
+            out.copy_(out0)
+            vs.copy_(vs0)
+            torch.cuda.synchronize()
+            t0 = time.perf_counter()
+            n = pc.pc_trace_flows_delta(S, D["port_off"], D["port_peer"], D["jur"], Dr["rule_off"], Dr["rules"],
+                                        D["hdr"], D["ingress"], ttl, out, vs, changed=Dc, ctx=ctx)
+            torch.cuda.synchronize()
+            t1 = time.perf_counter()
+            pc.pc_trace_flows(S, D["port_off"], D["port_peer"], D["jur"], Dr["rule_off"], Dr["rules"], D["hdr"],
+                              D["ingress"], ttl, ctx=ctx)
+            torch.cuda.synchronize()
+            t2 = time.perf_counter()
+            if it >= args.warmup:
+                t_d.append(t1 - t0)
+                t_f.append(t2 - t1)
+        d, f = float(np.median(t_d)), float(np.median(t_f))
+        m = 0
+        for sw in changed:
+            m |= 1 << (int(sw) & 63)
+        entry = {"retraced": int(n.cpu().numpy()[0]), "ms_per_delta": 1e3 * d, "ms_full_trace": 1e3 * f,
+                 "speedup": f / d}
+        if not args.no_cpu_baseline:
+            import oracle
+            threads = len(os.sched_getaffinity(0))
+            env_cap = os.environ.get("OMP_NUM_THREADS")
+            if env_cap and env_cap.isdigit():
+                threads = min(threads, int(env_cap))
+            sel = np.flatnonzero((vs_host & np.uint64(m)) != 0)
+            samp = sel[:: max(1, sel.shape[0] // 20000)]
+            t0 = time.perf_counter()
+            oracle.trace(S, wl["port_off"], wl["port_peer"], wl["jur"], r_off, rules, wl["hdr"], wl["ingress"], ttl,
+                         idx=samp, nthreads=threads)
+            t = (time.perf_counter() - t0) * sel.shape[0] / max(samp.shape[0], 1)
+            entry["cpu_baseline"] = {"value": 1.0 / t if t > 0 else None,
+                                     "unit": "deltas/s (the oracle re-tracing the selected traces; estimate)",
+                                     "cores": threads, "kind": "oracle",
+                                     "sample": f"{samp.shape[0]} of the {sel.shape[0]} selected traces, scaled: "
+                                               f"{t:.3f} s per delta"}
+        res["per_change"][name] = entry
+    return res
+
+
 def time_synthesis(args, wl, pc, ctx):
     """Timed pass of path synthesis (pc_synthesize_paths) over the same
     topology: the first flows' endpoints, allowed jurisdictions, waypoint,
@@ -665,6 +737,9 @@ def main():
     only = args.only
     if only == "affinity":
         print(json.dumps({"workload": desc, "affinity": time_affinity(args, wl, pc, ctx, feasible)}), flush=True)
+        return
+    if only == "delta":
+        print(json.dumps({"workload": desc, "rule_delta": time_rule_delta(args, wl, pc, ctx, D)}), flush=True)
         return
     if only == "preferred":
         # the feasible sets are the selector rows' bitsets, computed once
@@ -817,6 +892,8 @@ def main():
         line["update"] = time_update(args, wl, pc, ctx, D, feasible, popcnt)
     if only == "all" and not args.no_synthesis:
         line["synthesis"] = time_synthesis(args, wl, pc, ctx)
+    if only == "all" and not args.no_rule_delta:
+        line["rule_delta"] = time_rule_delta(args, wl, pc, ctx, D)
     if not args.no_cpu_baseline:
         line["cpu_baseline"] = cpu_baseline(wl, pairs, args.cpu_seconds)
     print(json.dumps(line), flush=True)

@@ -751,15 +751,18 @@ __global__ __launch_bounds__(256) void k_delta_mask(const int32_t *__restrict__ 
     if (threadIdx.x == 0) *mask = m;
 }
 
-// The traces whose summary meets the mask, in a list (one counter update per
-// wavefront); also the ingress sweep of the SWITCH flag over every trace.
-__global__ __launch_bounds__(256) void k_delta_select(const uint64_t *__restrict__ vsum, const int32_t *__restrict__ ingress,
-                                                      int32_t T, int32_t S, const unsigned long long *__restrict__ mask,
-                                                      int32_t *__restrict__ list, uint32_t *__restrict__ count,
-                                                      uint32_t *__restrict__ d_err)
+// The traces whose summary meets the mask, in a list (one counter update
+// per workgroup of 1,024 traces); also the ingress sweep of the SWITCH flag
+// over every trace.
+__global__ __launch_bounds__(1024) void k_delta_select(const uint64_t *__restrict__ vsum,
+                                                       const int32_t *__restrict__ ingress, int32_t T, int32_t S,
+                                                       const unsigned long long *__restrict__ mask,
+                                                       int32_t *__restrict__ list, uint32_t *__restrict__ count,
+                                                       uint32_t *__restrict__ d_err)
 {
+    __shared__ uint32_t wcount[16], wbase[16];
     const uint64_t m = *mask;
-    const int lane = threadIdx.x & 63;
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
     for (int64_t base = static_cast<int64_t>(blockIdx.x) * blockDim.x; base < T;
          base += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int64_t t = base + threadIdx.x;
@@ -768,14 +771,22 @@ __global__ __launch_bounds__(256) void k_delta_select(const uint64_t *__restrict
         const int32_t s = in ? ingress[t] : 0;
         if (__ballot(in && (s < 0 || s >= S)) && lane == 0) atomicOr(d_err, PC_DERR_SWITCH);
         const uint64_t b = __ballot(sel);
-        if (b == 0) continue;
-        const int leader = __builtin_ctzll(b);
-        uint32_t off = 0;
-        if (lane == leader) off = atomicAdd(count, static_cast<uint32_t>(__popcll(b)));
-        off = static_cast<uint32_t>(__builtin_amdgcn_readlane(static_cast<int>(off), leader));
+        if (lane == 0) wcount[wave] = static_cast<uint32_t>(__popcll(b));
+        __syncthreads();
+        if (threadIdx.x == 0) {
+            uint32_t tot = 0;
+            for (int w = 0; w < 16; ++w) {
+                wbase[w] = tot;
+                tot += wcount[w];
+            }
+            const uint32_t off = tot ? atomicAdd(count, tot) : 0u;
+            for (int w = 0; w < 16; ++w) wbase[w] += off;
+        }
+        __syncthreads();
         const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b >> 32),
                                                          __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(b), 0u));
-        if (sel) list[off + below] = static_cast<int32_t>(t);
+        if (sel) list[wbase[wave] + below] = static_cast<int32_t>(t);
+        __syncthreads();
     }
 }
 
@@ -994,8 +1005,8 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
     PC_LAUNCH_CHECK(ctx);
     if (T > 0) {
         PC_TIMED(ctx, "k_delta_select", stream,
-                 hipLaunchKernelGGL(k_delta_select, dim3(grid_for(T, 256)), dim3(256), 0, stream, vsum, ingress, T, S,
-                                    mask, list, count, ctx->d_err));
+                 hipLaunchKernelGGL(k_delta_select, dim3(grid_for(T, 1024)), dim3(1024), 0, stream, vsum, ingress, T,
+                                    S, mask, list, count, ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
     }
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, count, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
