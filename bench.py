@@ -33,14 +33,14 @@ HBM_PEAK_GBS = 8000.0
 # kernel source they were measured on.
 TRAFFIC = [
     {"source": "paper_2602_16100_amd/csrc/select.hip",
-     "sha256": "5a444dbfbad2db5b7080ccdafaaa0faf79466936387b1984bed94de82635650f",
+     "sha256": "eee8e1a3a3afb70815ca7a70283f8bd680ce9ca4ec662a115051bff92d3cc79f",
      "workload": "cfg5",
-     "bytes_per_launch": {"k_sel_eval": 680_736_487 + 4_407_304_352,
-                          "k_aff_eval": 848_143_452 + 4_408_032_469}},
+     "bytes_per_launch": {"k_sel_eval": 680_951_677 + 4_407_314_272,
+                          "k_aff_eval": 848_400_357 + 4_408_032_704}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
-     "sha256": "6cfbabb1a16a04cf28056056d64a124a62c7a8e7a53ee4fe9df74423cbda63d5",
+     "sha256": "6dde3af8879a835b0d948b73b0c448bf30909cdf5f9875ee50d7906ee83f08ed",
      "workload": "cfg5",
-     "bytes_per_launch": {"k_tr_prep": 1_888_506_195 + 566_231_040}},
+     "bytes_per_launch": {"k_tr_prep": 1_888_477_228 + 566_231_040}},
 ]
 
 
