@@ -60,7 +60,7 @@ def _load():
         _lib.orc_probes.argtypes = [P, I64, I64, P, P, I64, I64, P, P, I64, P, P]
         _lib.orc_synthesize.argtypes = [I64, P, P, I64, P, P, I64, P, P, P, P, I64, P, I64, P, P, I64, I64, P,
                                         I64, P, P, P, P, C]
-        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, P, C]
+        _lib.orc_trace.argtypes = [I64, P, P, I64, P, P, P, I64, P, P, I64, I64, P, I64, P, I64, P, P, P, P, P, C]
         _lib.orc_reach.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, P, C]
         _lib.orc_reach_via.argtypes = [I64, P, P, I64, P, I64, P, P, P, P, I64, P, I64, P, I64, P, P, C]
         _lib.orc_report.argtypes = [I64, P, I64, P, I64, P, I64, P, I64, P, P, I64, P, P, P, P, P, P]
@@ -223,8 +223,9 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
           n_ports=None, n_rules=None, nthreads=0, watch=None, summary=False):
     """Trace records for the given trace indices (all by default).  With a
     watch list [T, K] (switch ids, -1 = unused) also returns the visit words,
-    with summary=True the visited-switch summaries (u64, bit s mod 64):
-    (out, [visit,] [vsum,] flags)."""
+    with summary=True the visited-switch summaries (u64, bit s mod 64) and
+    the walk records (int32 [n, 8], the first 8 switches, -1 past the end):
+    (out, [visit,] [vsum, walk,] flags)."""
     lib = _load()
     T = ingress.shape[0]
     if idx is None:
@@ -240,6 +241,7 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
         K = watch.shape[1]
         visit = np.zeros(idx.shape[0], np.uint32)
     vsum = np.zeros(idx.shape[0], np.uint64) if summary else None
+    walk = np.zeros((idx.shape[0], 8), np.int32) if summary else None
     n_ports = port_peer.shape[0] if n_ports is None else n_ports
     n_rules = rules.shape[0] if n_rules is None else n_rules
     lib.orc_trace(S, _p(np.ascontiguousarray(port_off, np.int32)),
@@ -247,12 +249,14 @@ def trace(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, idx=N
                   _p(np.ascontiguousarray(jur, np.uint8)), _p(np.ascontiguousarray(rule_off, np.int32)),
                   _p(np.ascontiguousarray(rules)), n_rules,
                   _p(np.ascontiguousarray(hdr, np.uint32)), _p(np.ascontiguousarray(ingress, np.int32)),
-                  T, ttl, _p(watch), K, _p(idx), idx.shape[0], _p(out), _p(visit), _p(vsum), _p(err), nthreads)
+                  T, ttl, _p(watch), K, _p(idx), idx.shape[0], _p(out), _p(visit), _p(vsum), _p(walk), _p(err),
+                  nthreads)
     res = [out]
     if watch is not None:
         res.append(visit)
     if summary:
         res.append(vsum)
+        res.append(walk)
     res.append(int(err[0]))
     return tuple(res)
 

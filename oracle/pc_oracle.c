@@ -443,9 +443,11 @@ void orc_preferred(const uint8_t *labels, int64_t N, int64_t L, const uint64_t *
  * jurisdiction bit of every switch visited, the ingress included.
  * vsum (optional) summarises the visited switches for incremental
  * re-validation: bit (s mod 64) for every switch s on the walk, the
- * ingress included (0 for an invalid ingress).  A walk reads the tables of
- * the switches it visits only, so a walk whose summary has no bit of a
- * changed switch is the same walk after the change.
+ * ingress included (0 for an invalid ingress).  walk (optional, 8 slots
+ * per trace) holds the first 8 switches of the walk in order, -1 past its
+ * end (all -1 for an invalid ingress).  A walk reads the tables of the
+ * switches it visits only, so a walk that visits no changed switch is the
+ * same walk after the change.
  */
 static int rule_matches(const o_rule *r, const uint32_t *h)
 {
@@ -463,7 +465,7 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
                const uint8_t *jur, const int32_t *rule_off, const o_rule *rules, int64_t n_rules,
                const uint32_t *hdr, const int32_t *ingress, int64_t T, int64_t ttl,
                const int32_t *watch, int64_t K, const int64_t *idx, int64_t nidx, o_trace *out, uint32_t *visit,
-               uint64_t *vsum, uint32_t *err, int nthreads)
+               uint64_t *vsum, int32_t *walk, uint32_t *err, int nthreads)
 {
     set_threads(nthreads);
     /* data-error flags: a sweep over every input item */
@@ -497,6 +499,8 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
         res.hops = 0;
         if (visit) visit[k] = 0;
         if (vsum) vsum[k] = 0;
+        if (walk)
+            for (int j = 0; j < 8; ++j) walk[k * 8 + j] = -1;
         if (s < 0 || s >= S) {
             res.jmask = 0;
             res.last_switch = (int32_t)s;
@@ -557,6 +561,8 @@ void orc_trace(int64_t S, const int32_t *port_off, const int32_t *port_peer, int
             for (int64_t p = 0; p < npath; ++p) m |= (uint64_t)1 << (path[p] & 63);
             vsum[k] = m;
         }
+        if (walk)
+            for (int64_t p = 0; p < npath && p < 8; ++p) walk[k * 8 + p] = (int32_t)path[p];
     }
     free(path);
     }
