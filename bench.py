@@ -38,9 +38,9 @@ TRAFFIC = [
      "bytes_per_launch": {"k_sel_eval": 680_951_677 + 4_407_314_272,
                           "k_aff_eval": 848_400_357 + 4_408_032_704}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
-     "sha256": "6dde3af8879a835b0d948b73b0c448bf30909cdf5f9875ee50d7906ee83f08ed",
+     "sha256": "b2bf0d76cc3f24eb1723d1bace832ab21e394073208de62cd0b75000c15df603",
      "workload": "cfg5",
-     "bytes_per_launch": {"k_tr_prep": 1_888_477_228 + 566_231_040}},
+     "bytes_per_launch": {"k_tr_prep": 1_888_492_082 + 566_231_040}},
 ]
 
 
@@ -520,26 +520,30 @@ def time_update(args, wl, pc, ctx, D, feasible, popcnt):
 
 
 def time_rule_delta(args, wl, pc, ctx, D):
-    """Incremental re-trace (pc_trace_flows_delta) after rewriting the rules
-    of 1 core switch, 1 edge switch and 16 random switches of the combined
-    workload's fat-tree, against a full pc_trace_flows on the new tables.
-    The previous records and summaries are restored before each timed call;
-    the timed region is the call alone."""
+    """Incremental re-trace (pc_trace_flows_delta, with walk records) after
+    rewriting the rules of 1 core switch, 1 edge switch and 16 random
+    switches of the combined workload's fat-tree, against a full
+    pc_trace_flows on the new tables.  The previous records, summaries and
+    walk records are restored before each timed call; the timed region is
+    the call alone."""
     import torch
     import synth
     dev = D["ingress"].device
     S, T, ttl = wl["S"], wl["T"], wl["ttl"]
     out0 = torch.empty((T, 12), dtype=torch.uint8, device=dev)
     vs0 = torch.empty(T, dtype=torch.int64, device=dev)
+    wk0 = torch.empty((T, 8), dtype=torch.int32, device=dev)
     pc.pc_trace_flows_delta(S, D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
-                            D["ingress"], ttl, out0, vs0, ctx=ctx)
-    out, vs = out0.clone(), vs0.clone()
+                            D["ingress"], ttl, out0, vs0, walk=wk0, ctx=ctx)
+    out, vs, wk = out0.clone(), vs0.clone(), wk0.clone()
     k = int(round((4 * S / 5) ** 0.5))  # fat-tree: S = 5 k^2 / 4
     rng = np.random.default_rng([wl.seed, 17])
     cases = {"1 core switch": np.array([k * k + 7], np.int32), "1 edge switch": np.array([3 * k + 1], np.int32),
              "16 switches": rng.choice(S, size=16, replace=False).astype(np.int32)}
     res = {"traces": T, "switches": S, "per_change": {}}
     vs_host = vs0.cpu().numpy().view(np.uint64)
+    wk_host = wk0.cpu().numpy()
+    short_host = pc.records(out0, pc.TRACE_OUT_DT)["hops"].astype(np.int64) + 1 <= 8
     for name, changed in cases.items():
         r_off, rules = synth.mutate_tables(wl.seed, wl["port_off"], wl["rule_off"], wl["rules"], changed)
         Dr = {"rule_off": pc.to_device(r_off, dev), "rules": pc.to_device(rules, dev)}
@@ -549,10 +553,11 @@ def time_rule_delta(args, wl, pc, ctx, D):
         for it in range(args.warmup + args.steps):
             out.copy_(out0)
             vs.copy_(vs0)
+            wk.copy_(wk0)
             torch.cuda.synchronize()
             t0 = time.perf_counter()
             n = pc.pc_trace_flows_delta(S, D["port_off"], D["port_peer"], D["jur"], Dr["rule_off"], Dr["rules"],
-                                        D["hdr"], D["ingress"], ttl, out, vs, changed=Dc, ctx=ctx)
+                                        D["hdr"], D["ingress"], ttl, out, vs, changed=Dc, walk=wk, ctx=ctx)
             torch.cuda.synchronize()
             t1 = time.perf_counter()
             pc.pc_trace_flows(S, D["port_off"], D["port_peer"], D["jur"], Dr["rule_off"], Dr["rules"], D["hdr"],
@@ -574,7 +579,8 @@ def time_rule_delta(args, wl, pc, ctx, D):
             env_cap = os.environ.get("OMP_NUM_THREADS")
             if env_cap and env_cap.isdigit():
                 threads = min(threads, int(env_cap))
-            sel = np.flatnonzero((vs_host & np.uint64(m)) != 0)
+            sel = np.flatnonzero(np.where(short_host, np.isin(wk_host, changed).any(axis=1),
+                                          (vs_host & np.uint64(m)) != 0))
             samp = sel[:: max(1, sel.shape[0] // 20000)]
             t0 = time.perf_counter()
             oracle.trace(S, wl["port_off"], wl["port_peer"], wl["jur"], r_off, rules, wl["hdr"], wl["ingress"], ttl,

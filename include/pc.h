@@ -378,23 +378,32 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
  * rules of some switches change, only traces whose walk visited one of
  * them can change.  Every trace carries a visited-switch summary: bit
  * (s mod 64) of vsum[t] for every switch s on its walk (ingress included;
- * 0 for an invalid ingress).
+ * 0 for an invalid ingress), and, when walk is not NULL, a walk record:
+ * walk[t][0 .. 8) = the first 8 switches of its walk in order, -1 past its
+ * end (all -1 for an invalid ingress).
  * C < 0  : trace every trace from scratch, as pc_trace_flows, and write
  *          vsum; *n_retraced = T.
  * C >= 0 : out[t] and vsum[t] hold the results of an earlier call on the
  *          same topology, headers, ingresses and ttl, and the tables
  *          passed now differ from those only in the rules of the switches
- *          changed[0 .. C) (table sizes may change).  Every trace whose
- *          vsum meets the bit of a changed switch is traced again on the
- *          tables passed now and its out / vsum are overwritten; the others
- *          are left as they are.  The result equals a call with C < 0 on
- *          the tables passed now.  *n_retraced = the number of traces
- *          traced again (shared bits make it a superset of the traces that
- *          actually visited a changed switch).
+ *          changed[0 .. C) (table sizes may change).  A trace is traced
+ *          again on the tables passed now, and its out / vsum / walk
+ *          overwritten, when its walk record lists all of its walk
+ *          (out[t].hops + 1 <= 8) and names a changed switch, or, for a
+ *          longer walk or with walk NULL, when its vsum meets the bit of a
+ *          changed switch; the others are left as they are.  The result
+ *          equals a call with C < 0 on the tables passed now.
+ *          *n_retraced = the number of traces traced again (exactly those
+ *          that visited a changed switch when every walk fits its record;
+ *          shared summary bits add others).
  * changed    : int32 [C]; ids outside [0, S) are ignored (PC_DERR_SWITCH),
  *              repeats are harmless.
  * out        : pc_trace_out [T], read and written.
  * vsum       : uint64 [T], read and written.
+ * walk       : int32 [T][8], read and written, or NULL (selection by the
+ *              summaries alone).  With C >= 0 the records must be those
+ *              written with out / vsum: a call with walk NULL leaves them
+ *              stale for later calls.
  * n_retraced : int32, device memory.
  * The tables passed are prepared and swept for data errors on every call,
  * as in pc_trace_flows; the ingress sweep covers every trace.
@@ -402,8 +411,8 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
 int pc_trace_flows_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
                          int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
                          int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,
-                         const int32_t *changed, int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *n_retraced,
-                         void *stream);
+                         const int32_t *changed, int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *walk,
+                         int32_t *n_retraced, void *stream);
 
 /*
  * Waypoint and forbidden-switch constraints on realised paths.  The paper's

@@ -94,7 +94,7 @@ def lib():
     L.pc_masked_reach.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, P]
     L.pc_report.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P]
     L.pc_trace_flows_watch.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, I32, P, P, P]
-    L.pc_trace_flows_delta.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, I32, P, P, P, P]
+    L.pc_trace_flows_delta.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, I32, P, P, P, P, P]
     L.pc_masked_reach_via.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, I32, P, I32, P, P]
     L.pc_report_paths.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P, P, P]
     L.pc_profile.argtypes = [P, C]
@@ -444,13 +444,15 @@ def pc_report(intents, feasible, popcnt, N, traces, expect, reach, pass_=None, r
 
 
 def pc_trace_flows_delta(S, port_off, port_peer, jur, rule_off, rules, hdr, ingress, ttl, out, vsum, changed=None,
-                         n_ports=None, n_rules=None, ctx=None, stream=None):
+                         walk=None, n_ports=None, n_rules=None, ctx=None, stream=None):
     """A2+A3 incremental re-trace.  changed=None: trace everything from
     scratch into out (uint8 [T, 12]) and vsum (int64 [T], the visited-switch
-    summaries).  changed = int32 tensor of switch ids: out / vsum hold the
-    results on the previous tables; only traces whose summary meets a
-    changed switch are traced again on the tables given.  Returns the number
-    of traces traced again (an int32 device tensor of one element)."""
+    summaries) and, when given, walk (int32 [T, 8], the first 8 switches of
+    every walk).  changed = int32 tensor of switch ids: out / vsum / walk
+    hold the results on the previous tables; only traces that visited a
+    changed switch (exactly, for walks that fit their record; by summary
+    bits otherwise) are traced again on the tables given.  Returns the
+    number of traces traced again (an int32 device tensor of one element)."""
     ctx = ctx or context()
     T = int(ingress.shape[0])
     n_ports = int(port_peer.shape[0]) if n_ports is None else int(n_ports)
@@ -461,7 +463,8 @@ def pc_trace_flows_delta(S, port_off, port_peer, jur, rule_off, rules, hdr, ingr
                                          n_ports, _ptr(jur), _ptr(rule_off), _ptr(rules) if n_rules else None,
                                          n_rules, _ptr(hdr) if T else None, _ptr(ingress) if T else None, T,
                                          int(ttl), _ptr(changed) if C > 0 else None, C, _ptr(out) if T else None,
-                                         _ptr(vsum) if T else None, _ptr(n), _stream(stream)))
+                                         _ptr(vsum) if T else None, _ptr(walk) if walk is not None and T else None,
+                                         _ptr(n), _stream(stream)))
     return n
 
 

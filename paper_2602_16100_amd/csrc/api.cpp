@@ -366,7 +366,7 @@ int pc_trace_flows(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_
     if (T == 0 && S == 0) return PC_OK;
     PC_HIP(ctx, hipSetDevice(ctx->device));
     return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                     nullptr, 0, out, nullptr, nullptr, static_cast<hipStream_t>(stream));
+                     nullptr, 0, out, nullptr, nullptr, nullptr, static_cast<hipStream_t>(stream));
 }
 
 int pc_trace_flows_watch(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
@@ -388,14 +388,14 @@ int pc_trace_flows_watch(pc_ctx *ctx, int32_t S, const int32_t *port_off, const 
     if (T == 0 && S == 0) return PC_OK;
     PC_HIP(ctx, hipSetDevice(ctx->device));
     return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                     watch, K, out, T ? visit : nullptr, nullptr, static_cast<hipStream_t>(stream));
+                     watch, K, out, T ? visit : nullptr, nullptr, nullptr, static_cast<hipStream_t>(stream));
 }
 
 int pc_trace_flows_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
                          int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
                          int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,
-                         const int32_t *changed, int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *n_retraced,
-                         void *stream)
+                         const int32_t *changed, int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *walk,
+                         int32_t *n_retraced, void *stream)
 {
     if (!ctx) return PC_EINVAL;
     ctx->msg[0] = 0;
@@ -410,7 +410,7 @@ int pc_trace_flows_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const 
     PC_REQUIRE(n_rules == 0 || rules, "pc_trace_flows_delta: null rules");
     PC_HIP(ctx, hipSetDevice(ctx->device));
     return run_trace_delta(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                           changed, C, out, vsum, n_retraced, static_cast<hipStream_t>(stream));
+                           changed, C, out, vsum, walk, n_retraced, static_cast<hipStream_t>(stream));
 }
 
 int pc_masked_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,

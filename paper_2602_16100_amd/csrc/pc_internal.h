@@ -106,12 +106,13 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
               const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *watch, int32_t K,
-              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, hipStream_t stream);
+              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, int32_t *walk, hipStream_t stream);
 
 int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                     const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
                     const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *changed,
-                    int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *n_retraced, hipStream_t stream);
+                    int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *walk, int32_t *n_retraced,
+                    hipStream_t stream);
 
 int run_reach(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int64_t n_adj,
               const uint8_t *region, int32_t Q, const int32_t *src, const uint32_t *allowed,

@@ -67,6 +67,8 @@ __device__ __forceinline__ uint32_t watch_bits(const int32_t *__restrict__ watch
 // Bit of switch s in a visited-switch summary.
 __device__ __forceinline__ uint64_t sum_bit(int32_t s) { return 1ull << (s & 63); }
 
+constexpr int kWalkSlots = 8;  // walk records: the first 8 switches of a walk
+
 __device__ __forceinline__ uint32_t jur_bit(const uint8_t *jur, int32_t s)
 {
     const uint32_t j = jur[s];
@@ -252,7 +254,7 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
                                                  int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
                                                  uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
-                                                 uint32_t *__restrict__ d_err)
+                                                 int32_t *__restrict__ walk, uint32_t *__restrict__ d_err)
 {
     __shared__ int32_t nloc, base;
     if (threadIdx.x == 0) nloc = 0;
@@ -273,11 +275,15 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
             out[t] = o;
             if (visit) visit[t] = 0;
             if (vsum) vsum[t] = 0;
+            if (walk)
+                for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = -1;
         } else {
             cur[t] = s;
             jm[t] = jur_bit(jur, s);
             if (visit) visit[t] = watch_bits(watch, K, t, s);
             if (vsum) vsum[t] = sum_bit(s);
+            if (walk)
+                for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = j ? -1 : s;
             hops[t] = 0;
             rank[t] = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
             slot = atomicAdd(&nloc, 1);
@@ -386,6 +392,7 @@ struct Level {
     int32_t K;
     uint32_t *visit;        // [T] or nullptr
     uint64_t *vsum;         // [T] visited-switch summaries or nullptr
+    int32_t *walk;          // [T][kWalkSlots] walk records or nullptr
 };
 
 // Per level: bucket offsets boff = exclusive scan of counts (which are
@@ -653,6 +660,7 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
                 lv.jm[t] |= jur_bit(lv.jur, next);
                 if (lv.visit) lv.visit[t] |= watch_bits(lv.watch, lv.K, t, next);
                 if (lv.vsum) lv.vsum[t] |= sum_bit(next);
+                if (lv.walk && h + 1 < kWalkSlots) lv.walk[static_cast<int64_t>(t) * kWalkSlots + h + 1] = next;
                 lv.rank[t] = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
                 slot = atomicAdd(&nmove, 1);
             }
@@ -678,7 +686,8 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                                                  const int32_t *__restrict__ cur, const uint32_t *__restrict__ jm0,
                                                  const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
-                                                 uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum)
+                                                 uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
+                                                 int32_t *__restrict__ walk)
 {
     __shared__ unsigned long long best;
     const int32_t n = *nlive;
@@ -724,16 +733,17 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
             jm |= jur_bit(jur, s);
             if (visit) vis |= watch_bits(watch, K, t, s);
             if (vsum) vs |= sum_bit(s);
+            if (walk && hops < kWalkSlots && threadIdx.x == 0) walk[static_cast<int64_t>(t) * kWalkSlots + hops] = s;
         }
     }
 }
 
 // ---------------------------------------------------------------- deltas
-// Summary bits of the changed switches (ids outside [0, S) are ignored and
-// raise SWITCH); one workgroup.
+// Summary bits and the bitmap of the changed switches (ids outside [0, S)
+// are ignored and raise SWITCH); one workgroup.
 __global__ __launch_bounds__(256) void k_delta_mask(const int32_t *__restrict__ changed, int32_t C, int32_t S,
                                                     unsigned long long *__restrict__ mask,
-                                                    uint32_t *__restrict__ d_err)
+                                                    uint32_t *__restrict__ bitmap, uint32_t *__restrict__ d_err)
 {
     __shared__ unsigned long long m;
     if (threadIdx.x == 0) m = 0;
@@ -742,8 +752,12 @@ __global__ __launch_bounds__(256) void k_delta_mask(const int32_t *__restrict__ 
     bool bad = false;
     for (int32_t i = threadIdx.x; i < C; i += blockDim.x) {
         const int32_t s = changed[i];
-        if (s < 0 || s >= S) bad = true;
-        else mine |= sum_bit(s);
+        if (s < 0 || s >= S) {
+            bad = true;
+        } else {
+            mine |= sum_bit(s);
+            atomicOr(bitmap + (s >> 5), 1u << (s & 31));
+        }
     }
     if (mine) atomicOr(&m, static_cast<unsigned long long>(mine));
     if (__ballot(bad) && (threadIdx.x & 63) == 0) atomicOr(d_err, PC_DERR_SWITCH);
@@ -751,10 +765,15 @@ __global__ __launch_bounds__(256) void k_delta_mask(const int32_t *__restrict__ 
     if (threadIdx.x == 0) *mask = m;
 }
 
-// The traces whose summary meets the mask, in a list (one counter update
-// per workgroup of 1,024 traces); also the ingress sweep of the SWITCH flag
-// over every trace.
+// The traces to trace again, in a list (one counter update per workgroup
+// of 1,024 traces): with walk records, a walk of at most kWalkSlots
+// switches (hops + 1 of its record) is selected iff one of them changed;
+// otherwise, iff its summary meets the mask.  Also the ingress sweep of the
+// SWITCH flag over every trace.
 __global__ __launch_bounds__(1024) void k_delta_select(const uint64_t *__restrict__ vsum,
+                                                       const int32_t *__restrict__ walk,
+                                                       const pc_trace_out *__restrict__ out,
+                                                       const uint32_t *__restrict__ bitmap,
                                                        const int32_t *__restrict__ ingress, int32_t T, int32_t S,
                                                        const unsigned long long *__restrict__ mask,
                                                        int32_t *__restrict__ list, uint32_t *__restrict__ count,
@@ -767,7 +786,19 @@ __global__ __launch_bounds__(1024) void k_delta_select(const uint64_t *__restric
          base += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int64_t t = base + threadIdx.x;
         const bool in = t < T;
-        const bool sel = in && (vsum[t] & m) != 0;
+        bool sel = false;
+        if (in) {
+            const int32_t len = static_cast<int32_t>(out[t].hops) + 1;
+            if (walk != nullptr && len <= kWalkSlots) {
+                const int32_t *w = walk + t * kWalkSlots;
+                for (int j = 0; j < len; ++j) {
+                    const int32_t v = w[j];
+                    if (v >= 0 && v < S && ((bitmap[v >> 5] >> (v & 31)) & 1u)) sel = true;
+                }
+            } else {
+                sel = (vsum[t] & m) != 0;
+            }
+        }
         const int32_t s = in ? ingress[t] : 0;
         if (__ballot(in && (s < 0 || s >= S)) && lane == 0) atomicOr(d_err, PC_DERR_SWITCH);
         const uint64_t b = __ballot(sel);
@@ -805,13 +836,18 @@ __global__ __launch_bounds__(256) void k_delta_gather(const int32_t *__restrict_
 __global__ __launch_bounds__(256) void k_delta_scatter(const int32_t *__restrict__ list, int32_t n,
                                                        const pc_trace_out *__restrict__ out_c,
                                                        const uint64_t *__restrict__ vsum_c,
+                                                       const int32_t *__restrict__ walk_c,
                                                        pc_trace_out *__restrict__ out, uint64_t *__restrict__ vsum,
+                                                       int32_t *__restrict__ walk,
                                                        const uint32_t *__restrict__ count, int32_t *__restrict__ n_out)
 {
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
         const int32_t t = list[i];
         out[t] = out_c[i];
         vsum[t] = vsum_c[i];
+        if (walk)
+            for (int j = 0; j < kWalkSlots; ++j)
+                walk[static_cast<int64_t>(t) * kWalkSlots + j] = walk_c[static_cast<int64_t>(i) * kWalkSlots + j];
     }
     if (blockIdx.x == 0 && threadIdx.x == 0) *n_out = static_cast<int32_t>(*count);
 }
@@ -828,7 +864,7 @@ unsigned grid_for(int64_t n, int threads)
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
               const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *watch, int32_t K,
-              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, hipStream_t stream)
+              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, int32_t *walk, hipStream_t stream)
 {
     struct Bufs {
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
@@ -907,7 +943,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
     }
     PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
-                       B.hops, B.rank, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, ctx->d_err));
+                       B.hops, B.rank, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
@@ -935,7 +971,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_TIMED(ctx, "k_tr_walk", stream,
                      hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
                                         rule_off, rules, B.gcount, B.gofs, B.filt, hdr, ttl, live_cur, n_cur, B.cur,
-                                        B.jm, B.hops, out, watch, K, visit, vsum));
+                                        B.jm, B.hops, out, watch, K, visit, vsum, walk));
             PC_LAUNCH_CHECK(ctx);
             break;
         }
@@ -947,7 +983,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                                     B.cur, B.rank, B.boff, B.bucket));
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
         const Level lv{S,     T,     port_off, port_peer, n_ports, jur,   ttl, B.cur, B.jm,
-                       B.hops, B.rank, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit, vsum};
+                       B.hops, B.rank, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit, vsum, walk};
         // at most nlive / kChunk + (switches with a partial chunk) items
         const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);
         PC_TIMED(ctx, "k_tr_match", stream,
@@ -978,17 +1014,20 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
 int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                     const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
                     const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *changed,
-                    int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *n_retraced, hipStream_t stream)
+                    int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *walk, int32_t *n_retraced,
+                    hipStream_t stream)
 {
     if (C < 0) {  // every trace, from scratch
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_retraced), 1, static_cast<uint32_t>(T), stream);
         if (T == 0 && S == 0) return PC_OK;
         return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                         nullptr, 0, out, nullptr, T ? vsum : nullptr, stream);
+                         nullptr, 0, out, nullptr, T ? vsum : nullptr, T ? walk : nullptr, stream);
     }
     // compacted traces live in their own buffer: run_trace carves the arena
     const size_t Tn = static_cast<size_t>(T) + 1;
-    const size_t need = 256 * 8 + Tn * (sizeof(int32_t) * 2 + sizeof(pc_key) + sizeof(pc_trace_out) + 8);
+    const size_t words = (static_cast<size_t>(S) + 31) / 32 + 1;
+    const size_t need = 256 * 10 + words * 4 +
+                        Tn * (sizeof(int32_t) * 2 + sizeof(pc_key) + sizeof(pc_trace_out) + 8 + 4 * kWalkSlots);
     int rc = pc_ensure_delta(ctx, need);
     if (rc) return rc;
     Carver cv{ctx->delta, 0};
@@ -999,14 +1038,18 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
     int32_t *ing_c = cv.take<int32_t>(Tn);
     pc_trace_out *out_c = cv.take<pc_trace_out>(Tn);
     uint64_t *vsum_c = cv.take<uint64_t>(Tn);
+    int32_t *walk_c = cv.take<int32_t>(Tn * kWalkSlots);
+    uint32_t *bitmap = cv.take<uint32_t>(words);
     launch_fill_u32(count, 1, 0, stream);
+    launch_fill_u32(bitmap, words, 0, stream);
     PC_TIMED(ctx, "k_delta_mask", stream,
-             hipLaunchKernelGGL(k_delta_mask, dim3(1), dim3(256), 0, stream, changed, C, S, mask, ctx->d_err));
+             hipLaunchKernelGGL(k_delta_mask, dim3(1), dim3(256), 0, stream, changed, C, S, mask, bitmap,
+                                ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     if (T > 0) {
         PC_TIMED(ctx, "k_delta_select", stream,
-                 hipLaunchKernelGGL(k_delta_select, dim3(grid_for(T, 1024)), dim3(1024), 0, stream, vsum, ingress, T,
-                                    S, mask, list, count, ctx->d_err));
+                 hipLaunchKernelGGL(k_delta_select, dim3(grid_for(T, 1024)), dim3(1024), 0, stream, vsum, walk, out,
+                                    bitmap, ingress, T, S, mask, list, count, ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
     }
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, count, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
@@ -1022,12 +1065,12 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
     // trace needs them
     if (S > 0 || n > 0) {
         rc = run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr_c, ing_c, n, ttl,
-                       nullptr, 0, out_c, nullptr, n ? vsum_c : nullptr, stream);
+                       nullptr, 0, out_c, nullptr, n ? vsum_c : nullptr, n && walk ? walk_c : nullptr, stream);
         if (rc) return rc;
     }
     PC_TIMED(ctx, "k_delta_scatter", stream,
              hipLaunchKernelGGL(k_delta_scatter, dim3(grid_for(n > 0 ? n : 1, 256)), dim3(256), 0, stream, list, n,
-                                out_c, vsum_c, out, vsum, count, n_retraced));
+                                out_c, vsum_c, walk_c, out, vsum, walk, count, n_retraced));
     PC_LAUNCH_CHECK(ctx);
     return PC_OK;
 }

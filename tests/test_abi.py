@@ -64,7 +64,7 @@ def test_null_context_is_einval(libpc):
                                  None, 0, 0, None, None, None, None) == EINVAL
     assert L.pc_trace_flows(None, 0, None, None, 0, None, None, None, 0, None, None, 0, 0, None, None) == EINVAL
     assert L.pc_trace_flows_delta(None, 0, None, None, 0, None, None, None, 0, None, None, 0, 0, None, 0, None, None,
-                                  None, None) == EINVAL
+                                  None, None, None) == EINVAL
     assert L.pc_masked_reach(None, 0, None, None, 0, None, 0, None, None, None, None, None) == EINVAL
     assert L.pc_report(None, 0, None, 0, None, 0, None, 0, None, 0, None, None, 0, None, None, None, None) == EINVAL
     f = ctypes.c_uint32()

@@ -23,9 +23,10 @@ def g():
     return gpu_run
 
 
-def _run(wl, rule_off, rules, out, vsum, changed):
-    """One delta call; out / vsum as numpy (records, u64) or None for a
-    first call.  Returns (records, vsum, n_retraced, flags)."""
+def _run(wl, rule_off, rules, out, vsum, changed, walk=None, use_walk=True):
+    """One delta call; out / vsum / walk as numpy (records, u64, int32
+    [T, 8]) or None for a first call.  Returns (records, vsum, walk,
+    n_retraced, flags); walk is None with use_walk=False."""
     import torch
     import paper_2602_16100_amd as pc
     ctx = pc.context()
@@ -37,12 +38,17 @@ def _run(wl, rule_off, rules, out, vsum, changed):
     v = torch.zeros(T, dtype=torch.int64, device="cuda") if vsum is None else \
         torch.from_numpy(np.ascontiguousarray(vsum, np.uint64).view(np.int64).copy()).cuda()
     ch = None if changed is None else torch.from_numpy(np.ascontiguousarray(changed, np.int32)).cuda()
+    w = None
+    if use_walk:
+        w = torch.full((T, 8), -5, dtype=torch.int32, device="cuda") if walk is None else \
+            torch.from_numpy(np.ascontiguousarray(walk, np.int32).copy()).cuda()
     n = pc.pc_trace_flows_delta(wl["S"], d(wl["port_off"]), d(wl["port_peer"]), d(wl["jur"]), d(rule_off), d(rules),
                                 d(np.ascontiguousarray(wl["hdr"], np.uint32)), d(wl["ingress"]), wl["ttl"], o, v,
-                                changed=ch)
+                                changed=ch, walk=w)
     torch.cuda.synchronize()
     flags = ctx.data_errors(clear=True)
-    return (pc.records(o, pc.TRACE_OUT_DT), v.cpu().numpy().view(np.uint64), int(n.cpu().numpy()[0]), flags)
+    return (pc.records(o, pc.TRACE_OUT_DT), v.cpu().numpy().view(np.uint64),
+            None if w is None else w.cpu().numpy(), int(n.cpu().numpy()[0]), flags)
 
 
 def _oracle(orc, wl, rule_off, rules, idx=None):
@@ -63,6 +69,18 @@ def _mask(changed):
     return np.uint64(m)
 
 
+def _expected_count(ro, vo, wo, changed, use_walk=True):
+    """Traces to trace again: exact for walks that fit their record, by
+    summary bits otherwise (or always, without records)."""
+    by_sum = (vo & _mask(changed)) != 0
+    if not use_walk:
+        return int(by_sum.sum())
+    ch = np.asarray([c for c in changed if c >= 0], np.int64)
+    short = ro["hops"].astype(np.int64) + 1 <= 8
+    hit = np.isin(wo, ch).any(axis=1)
+    return int(np.where(short, hit, by_sum).sum())
+
+
 def _workloads():
     return {"cfg1-dense": lambda: synth.cfg1(0, "dense"),
             "fat-tree-80-dense": lambda: synth.trace_workload(5, 8, 4, 24, 3000, 12, 200, variant="dense"),
@@ -72,25 +90,28 @@ def _workloads():
 @pytest.mark.parametrize("name", list(_workloads()))
 def test_first_call_matches_oracle(g, orc, name):
     wl = _workloads()[name]()
-    rec, vs, n, flags = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
-    ro, vo, err = _oracle(orc, wl, wl["rule_off"], wl["rules"])
+    rec, vs, wk, n, flags = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
+    ro, vo, wo, err = _oracle(orc, wl, wl["rule_off"], wl["rules"])
     _same_records(rec, ro)
-    assert np.array_equal(vs, vo) and n == wl["ingress"].shape[0] and flags == err
+    assert np.array_equal(vs, vo) and np.array_equal(wk, wo) and n == wl["ingress"].shape[0] and flags == err
 
 
+@pytest.mark.parametrize("use_walk", [True, False])
 @pytest.mark.parametrize("resize", [False, True])
 @pytest.mark.parametrize("name", list(_workloads()))
-def test_delta_from_oracle_state(g, orc, name, resize):
+def test_delta_from_oracle_state(g, orc, name, resize, use_walk):
     wl = _workloads()[name]()
     S = wl["S"]
-    ro, vo, _ = _oracle(orc, wl, wl["rule_off"], wl["rules"])
+    ro, vo, wo, _ = _oracle(orc, wl, wl["rule_off"], wl["rules"])
     changed = np.random.default_rng(3).choice(S, size=min(4, S), replace=False)
     r_off2, rules2 = synth.mutate_tables(3, wl["port_off"], wl["rule_off"], wl["rules"], changed, resize=resize)
-    rec, vs, n, flags = _run(wl, r_off2, rules2, ro, vo, changed)
-    ro2, vo2, err2 = _oracle(orc, wl, r_off2, rules2)
+    rec, vs, wk, n, flags = _run(wl, r_off2, rules2, ro, vo, changed, walk=wo, use_walk=use_walk)
+    ro2, vo2, wo2, err2 = _oracle(orc, wl, r_off2, rules2)
     _same_records(rec, ro2)
     assert np.array_equal(vs, vo2) and flags == err2
-    assert n == int(((vo & _mask(changed)) != 0).sum()) and 0 < n < wl["ingress"].shape[0]
+    if use_walk:
+        assert np.array_equal(wk, wo2)
+    assert n == _expected_count(ro, vo, wo, changed, use_walk) and 0 < n < wl["ingress"].shape[0]
 
 
 @pytest.mark.parametrize("name", ["fat-tree-80-dense", "fat-tree-320-rpath"])
@@ -98,74 +119,80 @@ def test_chained_deltas_on_gpu(g, orc, name):
     wl = _workloads()[name]()
     S = wl["S"]
     rule_off, rules = wl["rule_off"], wl["rules"]
-    rec, vs, _, _ = _run(wl, rule_off, rules, None, None, None)
+    rec, vs, wk, _, _ = _run(wl, rule_off, rules, None, None, None)
     rng = np.random.default_rng(9)
     for step in range(4):
         changed = rng.choice(S, size=int(rng.integers(1, 6)), replace=True)  # repeats allowed
         rule_off, rules = synth.mutate_tables(20 + step, wl["port_off"], rule_off, rules, changed, resize=step % 2 == 1)
-        rec, vs, n, flags = _run(wl, rule_off, rules, rec, vs, changed)
-        ro, vo, err = _oracle(orc, wl, rule_off, rules)
+        rec, vs, wk, n, flags = _run(wl, rule_off, rules, rec, vs, changed, walk=wk)
+        ro, vo, wo, err = _oracle(orc, wl, rule_off, rules)
         _same_records(rec, ro)
-        assert np.array_equal(vs, vo) and flags == err
+        assert np.array_equal(vs, vo) and np.array_equal(wk, wo) and flags == err
 
 
 def test_edge_cases(g, orc):
     wl = synth.trace_workload(5, 8, 4, 24, 3000, 12, 200, variant="dense")
     S, T = wl["S"], wl["ingress"].shape[0]
     ingress = wl["ingress"].copy()
-    ingress[:4] = [-1, S, -7, 10 ** 6]  # invalid ingresses: MISS records, empty summaries, SWITCH flag
+    ingress[:4] = [-1, S, -7, 10 ** 6]  # invalid ingresses: MISS records, empty summaries and walks, SWITCH flag
     wl.arrays["ingress"] = ingress
-    ro, vo, err = _oracle(orc, wl, wl["rule_off"], wl["rules"])
-    assert err == F_SWITCH and (vo[:4] == 0).all()
-    rec, vs, n, flags = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
+    ro, vo, wo, err = _oracle(orc, wl, wl["rule_off"], wl["rules"])
+    assert err == F_SWITCH and (vo[:4] == 0).all() and (wo[:4] == -1).all()
+    rec, vs, wk, n, flags = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
     _same_records(rec, ro)
-    assert np.array_equal(vs, vo) and flags == F_SWITCH
+    assert np.array_equal(vs, vo) and np.array_equal(wk, wo) and flags == F_SWITCH
     # no change: nothing traced again, nothing moves
-    rec2, vs2, n, flags = _run(wl, wl["rule_off"], wl["rules"], ro, vo, np.zeros(0, np.int32))
+    rec2, vs2, wk2, n, flags = _run(wl, wl["rule_off"], wl["rules"], ro, vo, np.zeros(0, np.int32), walk=wo)
     _same_records(rec2, ro)
-    assert np.array_equal(vs2, vo) and n == 0 and flags == F_SWITCH
+    assert np.array_equal(vs2, vo) and np.array_equal(wk2, wo) and n == 0 and flags == F_SWITCH
     # out-of-range ids are ignored and flagged; a valid one still counts
     r_off2, rules2 = synth.mutate_tables(4, wl["port_off"], wl["rule_off"], wl["rules"], [17])
-    rec3, vs3, n, flags = _run(wl, r_off2, rules2, ro, vo, np.array([-1, 17, S, 17], np.int32))
-    ro3, vo3, err3 = _oracle(orc, wl, r_off2, rules2)
+    ids = np.array([-1, 17, S, 17], np.int32)
+    rec3, vs3, wk3, n, flags = _run(wl, r_off2, rules2, ro, vo, ids, walk=wo)
+    ro3, vo3, wo3, err3 = _oracle(orc, wl, r_off2, rules2)
     _same_records(rec3, ro3)
-    assert np.array_equal(vs3, vo3) and flags == err3 | F_SWITCH and n == int(((vo & _mask([17])) != 0).sum())
+    assert np.array_equal(vs3, vo3) and np.array_equal(wk3, wo3) and flags == err3 | F_SWITCH
+    assert n == _expected_count(ro, vo, wo, [17])
     # every switch changed: every trace with a valid ingress is traced again
     r_off4, rules4 = synth.mutate_tables(5, wl["port_off"], wl["rule_off"], wl["rules"], np.arange(S), resize=True)
-    rec4, vs4, n, flags = _run(wl, r_off4, rules4, ro, vo, np.arange(S, dtype=np.int32))
-    ro4, vo4, _ = _oracle(orc, wl, r_off4, rules4)
+    rec4, vs4, wk4, n, flags = _run(wl, r_off4, rules4, ro, vo, np.arange(S, dtype=np.int32), walk=wo)
+    ro4, vo4, wo4, _ = _oracle(orc, wl, r_off4, rules4)
     _same_records(rec4, ro4)
-    assert np.array_equal(vs4, vo4) and n == T - 4
+    assert np.array_equal(vs4, vo4) and np.array_equal(wk4, wo4) and n == T - 4
     # no traces
     wl0 = synth.trace_workload(5, 8, 4, 24, 3000, 12, 200, variant="dense")
     wl0.arrays["hdr"] = wl0["hdr"][:0]
     wl0.arrays["ingress"] = wl0["ingress"][:0]
-    rec5, vs5, n, flags = _run(wl0, wl0["rule_off"], wl0["rules"], np.zeros(0, ro.dtype), np.zeros(0, np.uint64),
-                               np.array([3], np.int32))
+    rec5, vs5, wk5, n, flags = _run(wl0, wl0["rule_off"], wl0["rules"], np.zeros(0, ro.dtype), np.zeros(0, np.uint64),
+                                    np.array([3], np.int32), walk=np.zeros((0, 8), np.int32))
     assert n == 0 and rec5.shape[0] == 0
 
 
 def test_delta_combined_workload_size(g, orc):
     """The combined workload's 699,050 traces over 2,880 switches of 16,384
     rules: a full first call, then the tables of one core, two aggregation
-    and three edge switches rewritten.  Every record and summary equals a
-    full GPU trace on the new tables; 4,000 sampled traces (half of them
-    re-traced ones) equal the oracle."""
+    and three edge switches rewritten.  Every record, summary and walk
+    record equals a full GPU trace on the new tables; the traces traced
+    again are exactly those whose walk visited a changed switch, except walks
+    longer than their record (selected by summary bits); 4,000 sampled traces
+    (half of them re-traced) equal the oracle."""
     wl = synth.cfg5()
-    rec, vs, n, _ = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
+    rec, vs, wk, n, _ = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
     k, h = 48, 24  # pod p: edge switches p*k + [0, h), aggregation p*k + [h, k); core from k*k
     changed = np.array([k * k + 5, 3 * k + h + 6, 10 * k + h + 16, 0, 5 * k + 2, 20 * k + 7], np.int32)
     assert changed.max() < wl["S"]
     r_off2, rules2 = synth.mutate_tables(8, wl["port_off"], wl["rule_off"], wl["rules"], changed)
-    rec2, vs2, n2, flags = _run(wl, r_off2, rules2, rec, vs, changed)
-    full, vfull, _, _ = _run(wl, r_off2, rules2, None, None, None)
+    rec2, vs2, wk2, n2, flags = _run(wl, r_off2, rules2, rec, vs, changed, walk=wk)
+    full, vfull, wfull, _, _ = _run(wl, r_off2, rules2, None, None, None)
     _same_records(rec2, full)
-    assert np.array_equal(vs2, vfull) and flags == 0
-    hit = np.flatnonzero((vs & _mask(changed)) != 0)
-    assert n2 == hit.shape[0] and 0 < n2 < wl["ingress"].shape[0]
+    assert np.array_equal(vs2, vfull) and np.array_equal(wk2, wfull) and flags == 0
+    short = rec["hops"].astype(np.int64) + 1 <= 8
+    assert short.mean() > 0.95  # nearly every walk fits its record
+    assert n2 == _expected_count(rec, vs, wk, changed) and 0 < n2 < wl["ingress"].shape[0] // 10
+    hit = np.flatnonzero(np.isin(wk, changed).any(axis=1) & short)
     rng = np.random.default_rng(4)
-    idx = np.sort(np.concatenate([rng.choice(hit, 2000, replace=False),
+    idx = np.sort(np.concatenate([rng.choice(hit, min(2000, hit.shape[0]), replace=False),
                                   rng.choice(wl["ingress"].shape[0], 2000, replace=False)]))
-    ro, vo, err = _oracle(orc, wl, r_off2, rules2, idx=idx)
+    ro, vo, wo, err = _oracle(orc, wl, r_off2, rules2, idx=idx)
     _same_records(rec2[idx], ro)
-    assert np.array_equal(vs2[idx], vo) and err == 0
+    assert np.array_equal(vs2[idx], vo) and np.array_equal(wk2[idx], wo) and err == 0
