@@ -405,8 +405,16 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
  *              written with out / vsum: a call with walk NULL leaves them
  *              stale for later calls.
  * n_retraced : int32, device memory.
- * The tables passed are prepared and swept for data errors on every call,
- * as in pc_trace_flows; the ingress sweep covers every trace.
+ * Prepared tables: the context keeps the prepared flow tables of its last
+ * pc_trace_flows_delta call.  A call with C >= 0 and the same S reuses
+ * them, re-preparing only the changed switches, when no switch's number of
+ * 32-rule groups changed; otherwise it prepares every switch.  So with
+ * C >= 0 the tables passed must also differ from those of the context's
+ * previous pc_trace_flows_delta call (if it had the same S) only in the
+ * changed switches' rules; a fresh context, or a call with C < 0, starts
+ * from a full preparation.  Every call sweeps the whole input for data
+ * errors, as pc_trace_flows (the action flags of switches not re-prepared
+ * are the ones found when they were prepared).
  */
 int pc_trace_flows_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
                          int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,

@@ -49,6 +49,20 @@ int pc_ensure_aux(pc_ctx *ctx, size_t bytes) { return ensure_buffer(ctx, &ctx->a
 
 int pc_ensure_delta(pc_ctx *ctx, size_t bytes) { return ensure_buffer(ctx, &ctx->delta, &ctx->delta_bytes, bytes); }
 
+int pc_ensure_tc_meta(pc_ctx *ctx, size_t bytes)
+{
+    const int rc = ensure_buffer(ctx, &ctx->tc_meta, &ctx->tc_meta_bytes, bytes);
+    if (rc != PC_OK) ctx->tc_S = -1;
+    return rc;
+}
+
+int pc_ensure_tc_filt(pc_ctx *ctx, size_t bytes)
+{
+    const int rc = ensure_buffer(ctx, &ctx->tc_filt, &ctx->tc_filt_bytes, bytes);
+    if (rc != PC_OK) ctx->tc_S = -1;
+    return rc;
+}
+
 static hipEvent_t take_event(pc_ctx *ctx)
 {
     if (!ctx->ev_free.empty()) {
@@ -166,6 +180,8 @@ int pc_destroy(pc_ctx *ctx)
     if (ctx->arena) (void)hipFree(ctx->arena);
     if (ctx->aux) (void)hipFree(ctx->aux);
     if (ctx->delta) (void)hipFree(ctx->delta);
+    if (ctx->tc_meta) (void)hipFree(ctx->tc_meta);
+    if (ctx->tc_filt) (void)hipFree(ctx->tc_filt);
     if (ctx->d_err) (void)hipFree(ctx->d_err);
     if (ctx->d_small) (void)hipFree(ctx->d_small);
     if (ctx->h_small) (void)hipHostFree(ctx->h_small);

@@ -23,6 +23,16 @@ struct pc_ctx {
     size_t aux_bytes;
     char *delta;         // compacted traces of an incremental re-trace (outside the arena it uses)
     size_t delta_bytes;
+    // prepared tables kept between pc_trace_flows_delta calls: per-switch
+    // group counts / offsets / prep-block offsets / action-error flags, and
+    // the chunk sets; valid for tc_S switches and tc_groups groups
+    char *tc_meta;
+    size_t tc_meta_bytes;
+    char *tc_filt;
+    size_t tc_filt_bytes;
+    int32_t tc_S = -1;
+    int64_t tc_groups = 0;
+    int64_t tc_blocks = 0;
     hipEvent_t lvl_ev[2];  // trace level loop: completion of a level's live count copy
     // optional per-kernel timing (pc_profile)
     bool prof;
@@ -63,6 +73,8 @@ int pc_set_error(pc_ctx *ctx, int code, const char *fmt, ...);
 int pc_ensure_arena(pc_ctx *ctx, size_t bytes);
 int pc_ensure_aux(pc_ctx *ctx, size_t bytes);
 int pc_ensure_delta(pc_ctx *ctx, size_t bytes);
+int pc_ensure_tc_meta(pc_ctx *ctx, size_t bytes);
+int pc_ensure_tc_filt(pc_ctx *ctx, size_t bytes);
 
 #define PC_HIP(ctx, expr)                                                                      \
     do {                                                                                       \
@@ -103,10 +115,19 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
                   const pc_pred *preds, int64_t n_preds, int32_t *best, uint32_t *score, uint32_t *count,
                   hipStream_t stream);
 
+// Flow tables already prepared for the trace engine: chunk sets and their
+// per-switch group counts and offsets.
+struct TracePrep {
+    const uint32_t *filt;
+    const int32_t *gcount;
+    const int32_t *gofs;
+};
+
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
               const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *watch, int32_t K,
-              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, int32_t *walk, hipStream_t stream);
+              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, int32_t *walk, hipStream_t stream,
+              const TracePrep *pre = nullptr);
 
 int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                     const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,

@@ -162,7 +162,8 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
                                                   const pc_rule *__restrict__ rules,
                                                   const int32_t *__restrict__ gcount,
                                                   const int32_t *__restrict__ gofs, const int32_t *__restrict__ bofs,
-                                                  uint32_t *__restrict__ filt, uint32_t *__restrict__ d_err)
+                                                  uint32_t *__restrict__ filt, uint32_t *__restrict__ d_err,
+                                                  const uint32_t *__restrict__ only, uint32_t *__restrict__ sw_bad)
 {
     __shared__ uint32_t tile[kPlaneWords * kTileStride];
     __shared__ uint16_t admit[256];
@@ -176,6 +177,7 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
         else hi = mid;
     }
     const int32_t s = lo;
+    if (only != nullptr && !((only[s >> 5] >> (s & 31)) & 1u)) return;  // only the listed switches (whole block)
     const int32_t G = gcount[s];
     const int32_t g0 = (b - bofs[s]) * kPrepGroups;
     const int64_t rb = rule_off[s];
@@ -236,7 +238,10 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
 #pragma unroll
         for (int d = 0; d < kChunks / 2; ++d) tile[(32 * d + (lane & 31)) * kTileStride + gl] = w[d];
     }
-    if (__ballot(bad_action) && lane == 0) atomicOr(d_err, PC_DERR_ACTION);
+    if (__ballot(bad_action) && lane == 0) {
+        atomicOr(d_err, PC_DERR_ACTION);
+        if (sw_bad != nullptr) atomicOr(sw_bad + s, 1u);
+    }
     __syncthreads();
     uint32_t *dst = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
     for (int i = threadIdx.x; i < kPlaneWords * kPrepGroups; i += blockDim.x) {
@@ -852,6 +857,35 @@ __global__ __launch_bounds__(256) void k_delta_scatter(const int32_t *__restrict
     if (blockIdx.x == 0 && threadIdx.x == 0) *n_out = static_cast<int32_t>(*count);
 }
 
+// Cached prepared tables: 1 in *diff when some switch's group count differs
+// from the cached one.
+__global__ __launch_bounds__(256) void k_tc_compare(const int32_t *__restrict__ gnew, const int32_t *__restrict__ gold,
+                                                    int32_t S, uint32_t *__restrict__ diff)
+{
+    bool d = false;
+    for (int32_t s = blockIdx.x * blockDim.x + threadIdx.x; s < S; s += gridDim.x * blockDim.x) d |= gnew[s] != gold[s];
+    if (__ballot(d) && (threadIdx.x & 63) == 0) atomicOr(diff, 1u);
+}
+
+// Clear the action-error flags of the listed switches (ids outside [0, S) skipped).
+__global__ __launch_bounds__(256) void k_tc_clear(const int32_t *__restrict__ changed, int32_t C, int32_t S,
+                                                  uint32_t *__restrict__ sw_bad)
+{
+    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < C; i += gridDim.x * blockDim.x) {
+        const int32_t s = changed[i];
+        if (s >= 0 && s < S) sw_bad[s] = 0;
+    }
+}
+
+// ACTION when any switch's flag is set.
+__global__ __launch_bounds__(256) void k_tc_badsum(const uint32_t *__restrict__ sw_bad, int32_t S,
+                                                   uint32_t *__restrict__ d_err)
+{
+    bool any = false;
+    for (int32_t s = blockIdx.x * blockDim.x + threadIdx.x; s < S; s += gridDim.x * blockDim.x) any |= sw_bad[s] != 0;
+    if (__ballot(any) && (threadIdx.x & 63) == 0) atomicOr(d_err, PC_DERR_ACTION);
+}
+
 unsigned grid_for(int64_t n, int threads)
 {
     int64_t b = (n + threads - 1) / threads;
@@ -864,7 +898,8 @@ unsigned grid_for(int64_t n, int threads)
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
               const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
               const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *watch, int32_t K,
-              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, int32_t *walk, hipStream_t stream)
+              pc_trace_out *out, uint32_t *visit, uint64_t *vsum, int32_t *walk, hipStream_t stream,
+              const TracePrep *pre)
 {
     struct Bufs {
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
@@ -896,7 +931,12 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     carve(real);
 
     // ---- prep: per-switch sizes, offsets, chunk sets, data-error sweep
-    if (S > 0) {
+    // (done by the caller when it passes prepared tables)
+    if (pre != nullptr) {
+        B.filt = const_cast<uint32_t *>(pre->filt);
+        B.gcount = const_cast<int32_t *>(pre->gcount);
+        B.gofs = const_cast<int32_t *>(pre->gofs);
+    } else if (S > 0) {
         PC_TIMED(ctx, "k_tr_switch_info", stream, hipLaunchKernelGGL(k_tr_switch_info, dim3(grid_for(S, 256)), dim3(256), 0, stream, S, port_off, n_ports, jur,
                            rule_off, n_rules, B.gcount, B.bcount, ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
@@ -922,7 +962,8 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         }
         if (prep_blocks > 0) {
             PC_TIMED(ctx, "k_tr_prep", stream, hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(prep_blocks)), dim3(kPrepWaves * 64), 0, stream, S,
-                               port_off, n_ports, rule_off, rules, B.gcount, B.gofs, B.bofs, B.filt, ctx->d_err));
+                               port_off, n_ports, rule_off, rules, B.gcount, B.gofs, B.bofs, B.filt, ctx->d_err,
+                               nullptr, nullptr));
             PC_LAUNCH_CHECK(ctx);
         }
     }
@@ -1011,28 +1052,107 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     return PC_OK;
 }
 
+namespace {
+
+// Per-switch arrays of the cached prepared tables in ctx->tc_meta.
+struct TcMeta {
+    int32_t *gcount, *bcount, *gofs, *bofs;
+    uint32_t *sw_bad;
+};
+
+TcMeta tc_meta(pc_ctx *ctx, int32_t S)
+{
+    Carver c{ctx->tc_meta, 0};
+    TcMeta m;
+    m.gcount = c.take<int32_t>(static_cast<size_t>(S) + 1);
+    m.bcount = c.take<int32_t>(static_cast<size_t>(S) + 1);
+    m.gofs = c.take<int32_t>(static_cast<size_t>(S) + 1);
+    m.bofs = c.take<int32_t>(static_cast<size_t>(S) + 1);
+    m.sw_bad = c.take<uint32_t>(static_cast<size_t>(S) + 1);
+    return m;
+}
+
+size_t tc_meta_bytes(int32_t S) { return 5 * (256 + (static_cast<size_t>(S) + 1) * 4); }
+
+// Prepare every switch's tables into the context's cache (and sweep them
+// for data errors); the cache then describes these tables.
+int tc_prepare_all(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
+                   const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
+                   hipStream_t stream)
+{
+    ctx->tc_S = -1;
+    int rc = pc_ensure_tc_meta(ctx, tc_meta_bytes(S));
+    if (rc) return rc;
+    const TcMeta m = tc_meta(ctx, S);
+    int64_t groups = 0, blocks = 0;
+    if (S > 0) {
+        PC_TIMED(ctx, "k_tr_switch_info", stream,
+                 hipLaunchKernelGGL(k_tr_switch_info, dim3(grid_for(S, 256)), dim3(256), 0, stream, S, port_off,
+                                    n_ports, jur, rule_off, n_rules, m.gcount, m.bcount, ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+        launch_scan_i32(m.gcount, S, m.gofs, nullptr, nullptr, stream);
+        launch_scan_i32(m.bcount, S, m.bofs, nullptr, nullptr, stream);
+        PC_LAUNCH_CHECK(ctx);
+        PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, m.gofs + S, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+        PC_HIP(ctx, hipMemcpyAsync(ctx->h_small + 1, m.bofs + S, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
+        PC_HIP(ctx, hipStreamSynchronize(stream));
+        groups = ctx->h_small[0];
+        blocks = ctx->h_small[1];
+        if (groups < 0 || blocks < 0)
+            return pc_set_error(ctx, PC_EINVAL, "pc_trace_flows_delta: more than 2^31 rule groups");
+    }
+    rc = pc_ensure_tc_filt(ctx, static_cast<size_t>(groups + 1) * kPlaneWords * sizeof(uint32_t));
+    if (rc) return rc;
+    if (S > 0) {
+        if (n_ports > 0) {
+            PC_TIMED(ctx, "k_tr_port_check", stream,
+                     hipLaunchKernelGGL(k_tr_port_check, dim3(grid_for(n_ports, 256)), dim3(256), 0, stream, n_ports,
+                                        port_peer, S, ctx->d_err));
+            PC_LAUNCH_CHECK(ctx);
+        }
+        launch_fill_u32(m.sw_bad, static_cast<size_t>(S), 0, stream);
+        if (blocks > 0) {
+            PC_TIMED(ctx, "k_tr_prep", stream,
+                     hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(blocks)), dim3(kPrepWaves * 64), 0,
+                                        stream, S, port_off, n_ports, rule_off, rules, m.gcount, m.gofs, m.bofs,
+                                        reinterpret_cast<uint32_t *>(ctx->tc_filt), ctx->d_err, nullptr, m.sw_bad));
+            PC_LAUNCH_CHECK(ctx);
+        }
+    }
+    ctx->tc_S = S;
+    ctx->tc_groups = groups;
+    ctx->tc_blocks = blocks;
+    return PC_OK;
+}
+
+}  // namespace
+
 int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                     const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
                     const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl, const int32_t *changed,
                     int32_t C, pc_trace_out *out, uint64_t *vsum, int32_t *walk, int32_t *n_retraced,
                     hipStream_t stream)
 {
-    if (C < 0) {  // every trace, from scratch
+    if (C < 0) {  // every trace, from scratch; the prepared tables are kept for later deltas
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_retraced), 1, static_cast<uint32_t>(T), stream);
-        if (T == 0 && S == 0) return PC_OK;
+        int rc = tc_prepare_all(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, stream);
+        if (rc) return rc;
+        if (T == 0) return PC_OK;
+        const TcMeta m = tc_meta(ctx, S);
+        const TracePrep pre{reinterpret_cast<const uint32_t *>(ctx->tc_filt), m.gcount, m.gofs};
         return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
-                         nullptr, 0, out, nullptr, T ? vsum : nullptr, T ? walk : nullptr, stream);
+                         nullptr, 0, out, nullptr, vsum, walk, stream, &pre);
     }
     // compacted traces live in their own buffer: run_trace carves the arena
     const size_t Tn = static_cast<size_t>(T) + 1;
     const size_t words = (static_cast<size_t>(S) + 31) / 32 + 1;
-    const size_t need = 256 * 10 + words * 4 +
+    const size_t need = 256 * 14 + words * 4 + 2 * (static_cast<size_t>(S) + 1) * 4 +
                         Tn * (sizeof(int32_t) * 2 + sizeof(pc_key) + sizeof(pc_trace_out) + 8 + 4 * kWalkSlots);
     int rc = pc_ensure_delta(ctx, need);
     if (rc) return rc;
     Carver cv{ctx->delta, 0};
     unsigned long long *mask = cv.take<unsigned long long>(1);
-    uint32_t *count = cv.take<uint32_t>(1);
+    uint32_t *count = cv.take<uint32_t>(2);  // [0] selected traces, [1] a group count differs from the cache
     int32_t *list = cv.take<int32_t>(Tn);
     pc_key *hdr_c = cv.take<pc_key>(Tn);
     int32_t *ing_c = cv.take<int32_t>(Tn);
@@ -1040,7 +1160,9 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
     uint64_t *vsum_c = cv.take<uint64_t>(Tn);
     int32_t *walk_c = cv.take<int32_t>(Tn * kWalkSlots);
     uint32_t *bitmap = cv.take<uint32_t>(words);
-    launch_fill_u32(count, 1, 0, stream);
+    int32_t *gnew = cv.take<int32_t>(static_cast<size_t>(S) + 1);
+    int32_t *bnew = cv.take<int32_t>(static_cast<size_t>(S) + 1);
+    launch_fill_u32(count, 2, 0, stream);
     launch_fill_u32(bitmap, words, 0, stream);
     PC_TIMED(ctx, "k_delta_mask", stream,
              hipLaunchKernelGGL(k_delta_mask, dim3(1), dim3(256), 0, stream, changed, C, S, mask, bitmap,
@@ -1052,20 +1174,58 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
                                     bitmap, ingress, T, S, mask, list, count, ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
     }
-    PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, count, sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
+    // the cache holds the previous tables when its switch count matches; it
+    // serves the new ones when no switch's group count changed
+    const bool cached = ctx->tc_S == S && S > 0;
+    if (cached) {
+        const TcMeta m = tc_meta(ctx, S);
+        PC_TIMED(ctx, "k_tr_switch_info", stream,
+                 hipLaunchKernelGGL(k_tr_switch_info, dim3(grid_for(S, 256)), dim3(256), 0, stream, S, port_off,
+                                    n_ports, jur, rule_off, n_rules, gnew, bnew, ctx->d_err));
+        PC_TIMED(ctx, "k_tc_compare", stream,
+                 hipLaunchKernelGGL(k_tc_compare, dim3(grid_for(S, 256)), dim3(256), 0, stream, gnew, m.gcount, S,
+                                    count + 1));
+        PC_LAUNCH_CHECK(ctx);
+    }
+    PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, count, 2 * sizeof(uint32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
     const int32_t n = ctx->h_small[0];
+    if (cached && ctx->h_small[1] == 0) {
+        // re-prepare only the changed switches, then the ACTION flag over all
+        const TcMeta m = tc_meta(ctx, S);
+        if (n_ports > 0) {
+            PC_TIMED(ctx, "k_tr_port_check", stream,
+                     hipLaunchKernelGGL(k_tr_port_check, dim3(grid_for(n_ports, 256)), dim3(256), 0, stream, n_ports,
+                                        port_peer, S, ctx->d_err));
+        }
+        if (C > 0) {
+            PC_TIMED(ctx, "k_tc_clear", stream,
+                     hipLaunchKernelGGL(k_tc_clear, dim3(grid_for(C, 256)), dim3(256), 0, stream, changed, C, S,
+                                        m.sw_bad));
+        }
+        if (ctx->tc_blocks > 0 && C > 0) {
+            PC_TIMED(ctx, "k_tr_prep", stream,
+                     hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(ctx->tc_blocks)), dim3(kPrepWaves * 64),
+                                        0, stream, S, port_off, n_ports, rule_off, rules, m.gcount, m.gofs, m.bofs,
+                                        reinterpret_cast<uint32_t *>(ctx->tc_filt), ctx->d_err, bitmap, m.sw_bad));
+        }
+        PC_TIMED(ctx, "k_tc_badsum", stream,
+                 hipLaunchKernelGGL(k_tc_badsum, dim3(grid_for(S, 256)), dim3(256), 0, stream, m.sw_bad, S,
+                                    ctx->d_err));
+        PC_LAUNCH_CHECK(ctx);
+    } else {
+        rc = tc_prepare_all(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, stream);
+        if (rc) return rc;
+    }
     if (n > 0) {
         PC_TIMED(ctx, "k_delta_gather", stream,
                  hipLaunchKernelGGL(k_delta_gather, dim3(grid_for(n, 256)), dim3(256), 0, stream, list, n, hdr,
                                     ingress, hdr_c, ing_c));
         PC_LAUNCH_CHECK(ctx);
-    }
-    // the new tables are prepared (and swept for data errors) even when no
-    // trace needs them
-    if (S > 0 || n > 0) {
+        const TcMeta m = tc_meta(ctx, S);
+        const TracePrep pre{reinterpret_cast<const uint32_t *>(ctx->tc_filt), m.gcount, m.gofs};
         rc = run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr_c, ing_c, n, ttl,
-                       nullptr, 0, out_c, nullptr, n ? vsum_c : nullptr, n && walk ? walk_c : nullptr, stream);
+                       nullptr, 0, out_c, nullptr, vsum_c, walk ? walk_c : nullptr, stream, &pre);
         if (rc) return rc;
     }
     PC_TIMED(ctx, "k_delta_scatter", stream,

@@ -23,13 +23,15 @@ def g():
     return gpu_run
 
 
-def _run(wl, rule_off, rules, out, vsum, changed, walk=None, use_walk=True):
+def _run(wl, rule_off, rules, out, vsum, changed, walk=None, use_walk=True, ctx=None):
     """One delta call; out / vsum / walk as numpy (records, u64, int32
     [T, 8]) or None for a first call.  Returns (records, vsum, walk,
-    n_retraced, flags); walk is None with use_walk=False."""
+    n_retraced, flags); walk is None with use_walk=False.  Without ctx a
+    fresh context (no prepared tables kept) serves the call; a chain of calls
+    on the same tables passes its own context."""
     import torch
     import paper_2602_16100_amd as pc
-    ctx = pc.context()
+    ctx = ctx or pc.Context(0)
     ctx.data_errors(clear=True)
     T = wl["ingress"].shape[0]
     d = lambda a: pc.to_device(a, "cuda")
@@ -44,7 +46,7 @@ def _run(wl, rule_off, rules, out, vsum, changed, walk=None, use_walk=True):
             torch.from_numpy(np.ascontiguousarray(walk, np.int32).copy()).cuda()
     n = pc.pc_trace_flows_delta(wl["S"], d(wl["port_off"]), d(wl["port_peer"]), d(wl["jur"]), d(rule_off), d(rules),
                                 d(np.ascontiguousarray(wl["hdr"], np.uint32)), d(wl["ingress"]), wl["ttl"], o, v,
-                                changed=ch, walk=w)
+                                changed=ch, walk=w, ctx=ctx)
     torch.cuda.synchronize()
     flags = ctx.data_errors(clear=True)
     return (pc.records(o, pc.TRACE_OUT_DT), v.cpu().numpy().view(np.uint64),
@@ -119,12 +121,32 @@ def test_chained_deltas_on_gpu(g, orc, name):
     wl = _workloads()[name]()
     S = wl["S"]
     rule_off, rules = wl["rule_off"], wl["rules"]
-    rec, vs, wk, _, _ = _run(wl, rule_off, rules, None, None, None)
+    import paper_2602_16100_amd as pc
+    ctx = pc.Context(0)  # one context: later calls re-prepare only the changed switches
+    rec, vs, wk, _, _ = _run(wl, rule_off, rules, None, None, None, ctx=ctx)
     rng = np.random.default_rng(9)
     for step in range(4):
         changed = rng.choice(S, size=int(rng.integers(1, 6)), replace=True)  # repeats allowed
         rule_off, rules = synth.mutate_tables(20 + step, wl["port_off"], rule_off, rules, changed, resize=step % 2 == 1)
-        rec, vs, wk, n, flags = _run(wl, rule_off, rules, rec, vs, changed, walk=wk)
+        rec, vs, wk, n, flags = _run(wl, rule_off, rules, rec, vs, changed, walk=wk, ctx=ctx)
+        ro, vo, wo, err = _oracle(orc, wl, rule_off, rules)
+        _same_records(rec, ro)
+        assert np.array_equal(vs, vo) and np.array_equal(wk, wo) and flags == err
+
+
+def test_chain_across_group_boundaries(g, orc):
+    """Tables of exactly 32 rules per switch: resizing a switch to 31 or 33
+    rules changes its number of 32-rule groups, so the kept tables cannot
+    serve and every switch is prepared again; the next delta (sizes kept)
+    re-prepares only its changed switch.  Every step equals the oracle."""
+    import paper_2602_16100_amd as pc
+    wl = synth.trace_workload(7, 8, 4, 32, 4000, 12, 300, variant="dense")
+    ctx = pc.Context(0)
+    rule_off, rules = wl["rule_off"], wl["rules"]
+    rec, vs, wk, _, _ = _run(wl, rule_off, rules, None, None, None, ctx=ctx)
+    for step, (sw, resize) in enumerate([([4, 9], True), ([30], False), ([4, 11, 70], True), ([5], False)]):
+        rule_off, rules = synth.mutate_tables(40 + step, wl["port_off"], rule_off, rules, sw, resize=resize)
+        rec, vs, wk, n, flags = _run(wl, rule_off, rules, rec, vs, np.array(sw, np.int32), walk=wk, ctx=ctx)
         ro, vo, wo, err = _oracle(orc, wl, rule_off, rules)
         _same_records(rec, ro)
         assert np.array_equal(vs, vo) and np.array_equal(wk, wo) and flags == err
@@ -176,13 +198,15 @@ def test_delta_combined_workload_size(g, orc):
     again are exactly those whose walk visited a changed switch, except walks
     longer than their record (selected by summary bits); 4,000 sampled traces
     (half of them re-traced) equal the oracle."""
+    import paper_2602_16100_amd as pc
     wl = synth.cfg5()
-    rec, vs, wk, n, _ = _run(wl, wl["rule_off"], wl["rules"], None, None, None)
+    ctx = pc.Context(0)
+    rec, vs, wk, n, _ = _run(wl, wl["rule_off"], wl["rules"], None, None, None, ctx=ctx)
     k, h = 48, 24  # pod p: edge switches p*k + [0, h), aggregation p*k + [h, k); core from k*k
     changed = np.array([k * k + 5, 3 * k + h + 6, 10 * k + h + 16, 0, 5 * k + 2, 20 * k + 7], np.int32)
     assert changed.max() < wl["S"]
     r_off2, rules2 = synth.mutate_tables(8, wl["port_off"], wl["rule_off"], wl["rules"], changed)
-    rec2, vs2, wk2, n2, flags = _run(wl, r_off2, rules2, rec, vs, changed, walk=wk)
+    rec2, vs2, wk2, n2, flags = _run(wl, r_off2, rules2, rec, vs, changed, walk=wk, ctx=ctx)
     full, vfull, wfull, _, _ = _run(wl, r_off2, rules2, None, None, None)
     _same_records(rec2, full)
     assert np.array_equal(vs2, vfull) and np.array_equal(wk2, wfull) and flags == 0
