@@ -828,7 +828,8 @@ constexpr uint32_t kPrefLenBits = 24;  // term header: weight << 24 | program en
 enum : uint32_t { kPrefInline = 0, kPrefIndirect = 1, kPrefDecode = 2, kPrefNone = 3 };
 constexpr int kPrefRec = 16;
 constexpr int kPrefInlineWords = kPrefRec - 2;
-constexpr uint32_t kPrefClasses = 3;  // row lists: scores within 8 bits, within 16 bits, decoded on the fly
+constexpr uint32_t kPrefClasses = 4;  // row lists: scores within 8 bits, within 16 bits, decoded, <= 3 terms
+constexpr uint32_t kPrefFewTerms = 3;  // rows with at most this many live terms: scores from term patterns
 
 __device__ __forceinline__ bool pref_weight_ok(uint32_t w) { return w >= 1 && w <= 100; }
 
@@ -872,8 +873,9 @@ __global__ __launch_bounds__(256) void k_pref_validate(const int32_t *__restrict
     if (errs) atomicOr(d_err, errs);
 }
 
-// One row of k_pref_compile: its record, and its class (0: scores fit 8
-// bits, 1: 16 bits, 2: decoded on the fly).
+// One row of k_pref_compile: its record, and its class (3: at most three
+// live terms, including none; 0: scores fit 8 bits, 1: 16 bits; 2: decoded
+// on the fly).
 __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_t i,
                                      const int32_t *__restrict__ term_off, int32_t n_terms,
                                      const uint32_t *__restrict__ weight, const pc_pred *__restrict__ preds,
@@ -883,7 +885,7 @@ __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_
 {
     uint32_t *rr = rec + static_cast<int64_t>(i) * kPrefRec;
     rr[0] = kPrefNone << 24;
-    if (!pref_row_ok(row_off, i, n_terms)) return 0;
+    if (!pref_row_ok(row_off, i, n_terms)) return 3;
     const int64_t tb = row_off[i], te = row_off[i + 1];
     int64_t n = 0;
     uint32_t live = 0, sum = 0;
@@ -897,7 +899,7 @@ __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_
         sum += weight[t];
         ++live;
     }
-    if (live == 0) return 0;
+    if (live == 0) return 3;
     const uint32_t head = live | bit_length(sum) << 16;
     uint32_t *out = rr + 2;
     uint32_t kind = kPrefInline;
@@ -938,6 +940,7 @@ __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_
         }
     }
     rr[0] = head | kind << 24;
+    if (live <= kPrefFewTerms) return 3;
     return bit_length(sum) <= 8 ? 0u : 1u;
 }
 
@@ -1076,8 +1079,13 @@ __device__ Words pref_term_decoded(const pc_pred *__restrict__ preds, int64_t b,
 // part_key[tile * I + r] = (score + 1) << 32 | ~node (0: no feasible node)
 // and part_cnt[tile * I + r].
 // kCls: the rows of one class list (0: scores within 8 bits, 1: within 16
-// bits, 2: decoded on the fly), so that each launch keeps only the score
-// words it needs and the common one carries no decoding code.
+// bits, 2: decoded on the fly, 3: at most three live terms), so that each
+// launch keeps only the score words it needs and the common one carries no
+// decoding code.  Class 3 keeps the (at most) three term masks instead of
+// score bits: a node's score is fixed by the pattern of terms that hold for
+// it, so the lane's best score is the largest pattern score whose node
+// set meets its candidates, and its best nodes are the union of the
+// candidates in the patterns of that score.
 template <bool kBuf, int kCls>
 __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
     const uint32_t *__restrict__ rec, const uint32_t *__restrict__ prog, const int32_t *__restrict__ row_off,
@@ -1088,7 +1096,7 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
     int32_t ntiles, int32_t nchunks, int32_t rpc, const int32_t *__restrict__ list,
     const uint32_t *__restrict__ list_len, int64_t fstride)
 {
-    constexpr int kBits = kCls == 0 ? 8 : kScoreBits;
+    constexpr int kBits = kCls == 0 ? 8 : (kCls == 3 ? 1 : kScoreBits);
     constexpr bool kDecode = kCls == 2;
     const int64_t total = static_cast<int64_t>(ntiles) * nchunks;
     const int64_t item = pc_xcd_item(total);
@@ -1135,65 +1143,134 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
             const uint32_t head = head_next;
             const uint32_t kind = head >> 24, live = head & 0xFFFFu;
             const uint64_t fa = fa_next, fb = fb_next;
-            Words acc[kBits];
+            Words cand{m0 & fa, m1 & fb};
+            uint32_t sc = 0;
+            if constexpr (kCls == 3) {
+                Words A[kPrefFewTerms];
+                uint32_t wt[kPrefFewTerms];
+                const uint32_t nt = kind == kPrefNone ? 0u : live;
 #pragma unroll
-            for (int b = 0; b < kBits; ++b) acc[b] = Words{0, 0};
-            // one loop over the row's terms, whatever their source, so the
-            // score words have a single update site
-            constexpr bool dec = kDecode;
-            const int64_t tb = dec ? row_off[r] : 0;
-            const uint32_t n_iter = dec ? static_cast<uint32_t>(row_off[r + 1] - tb)
-                                        : (kind == kPrefNone ? 0u : live);
-            const uint32_t *pr = kind == kPrefInline ? R + 2 : prog + R[1];
-            for (uint32_t t = 0; t < n_iter; ++t) {
-                uint32_t w;
-                Words a{~0ull, ~0ull};
-                if constexpr (dec) {
-                    w = weight[tb + t];
-                    int64_t len;
-                    if (!pref_weight_ok(w) ||
-                        !aff_term(preds, term_off[tb + t], term_off[tb + t + 1], n_preds, L, present, len))
-                        continue;
-                    a = pref_term_decoded<kBuf>(preds, term_off[tb + t], term_off[tb + t + 1], present, wbase, pl);
-                } else {
-                    const uint32_t hdr = *pr++;
-                    w = hdr >> kPrefLenBits;
-                    const int32_t len = static_cast<int32_t>(hdr & ((1u << kPrefLenBits) - 1));
-                    Words c{0, 0}, unused{0, 0};
-                    for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
-                        uint32_t E[kGroup];
-                        Words V[kGroup];
-#pragma unroll
-                        for (int k = 0; k < kGroup; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
-#pragma unroll
-                        for (int k = 0; k < kGroup; ++k)
-                            if (e0 + k < len) V[k] = pl(E[k] & kPidMask);
-#pragma unroll
-                        for (int k = 0; k < kGroup; ++k)
-                            if (e0 + k < len) fold<false>(E[k], V[k], c, a, unused);
-                    }
-                    pr += len;
+                for (int t = 0; t < static_cast<int>(kPrefFewTerms); ++t) {
+                    A[t] = Words{0, 0};
+                    wt[t] = 0;
                 }
-                score_add<kBits>(acc, w, a);
+                const uint32_t *pr = kind == kPrefInline ? R + 2 : prog + R[1];
+#pragma unroll
+                for (int t = 0; t < static_cast<int>(kPrefFewTerms); ++t) {
+                    if (static_cast<uint32_t>(t) < nt) {
+                        const uint32_t hdr = *pr++;
+                        wt[t] = hdr >> kPrefLenBits;
+                        const int32_t len = static_cast<int32_t>(hdr & ((1u << kPrefLenBits) - 1));
+                        Words a{~0ull, ~0ull}, c{0, 0}, unused{0, 0};
+                        for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
+                            uint32_t E[kGroup];
+                            Words V[kGroup];
+#pragma unroll
+                            for (int k = 0; k < kGroup; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
+#pragma unroll
+                            for (int k = 0; k < kGroup; ++k)
+                                if (e0 + k < len) V[k] = pl(E[k] & kPidMask);
+#pragma unroll
+                            for (int k = 0; k < kGroup; ++k)
+                                if (e0 + k < len) fold<false>(E[k], V[k], c, a, unused);
+                        }
+                        pr += len;
+                        A[t] = a;
+                    }
+                }
+                // pattern p: term t holds iff bit t of p (terms past nt hold
+                // nowhere, so only p < 2^nt has nodes)
+                auto pattern = [&](int p) {
+                    Words m{~0ull, ~0ull};
+#pragma unroll
+                    for (int t = 0; t < static_cast<int>(kPrefFewTerms); ++t) {
+                        m.a &= ((p >> t) & 1) ? A[t].a : ~A[t].a;
+                        m.b &= ((p >> t) & 1) ? A[t].b : ~A[t].b;
+                    }
+                    return Words{m.a & cand.a, m.b & cand.b};
+                };
+                bool found = false;
+#pragma unroll
+                for (int p = 0; p < (1 << kPrefFewTerms); ++p) {
+                    if (static_cast<uint32_t>(p) < (1u << nt)) {
+                        const uint32_t sp = ((p & 1) ? wt[0] : 0u) + ((p & 2) ? wt[1] : 0u) + ((p & 4) ? wt[2] : 0u);
+                        const Words t = pattern(p);
+                        const bool any = (t.a | t.b) != 0;
+                        sc = any && (!found || sp > sc) ? sp : sc;
+                        found = found || any;
+                    }
+                }
+                Words best{0, 0};
+#pragma unroll
+                for (int p = 0; p < (1 << kPrefFewTerms); ++p) {
+                    if (static_cast<uint32_t>(p) < (1u << nt)) {
+                        const uint32_t sp = ((p & 1) ? wt[0] : 0u) + ((p & 2) ? wt[1] : 0u) + ((p & 4) ? wt[2] : 0u);
+                        const Words t = pattern(p);
+                        const bool take = found && sp == sc;
+                        best.a |= take ? t.a : 0ull;
+                        best.b |= take ? t.b : 0ull;
+                    }
+                }
+                cand = best;
+            } else {
+                Words acc[kBits];
+#pragma unroll
+                for (int b = 0; b < kBits; ++b) acc[b] = Words{0, 0};
+                // one loop over the row's terms, whatever their source, so the
+                // score words have a single update site
+                constexpr bool dec = kDecode;
+                const int64_t tb = dec ? row_off[r] : 0;
+                const uint32_t n_iter = dec ? static_cast<uint32_t>(row_off[r + 1] - tb)
+                                            : (kind == kPrefNone ? 0u : live);
+                const uint32_t *pr = kind == kPrefInline ? R + 2 : prog + R[1];
+                for (uint32_t t = 0; t < n_iter; ++t) {
+                    uint32_t w;
+                    Words a{~0ull, ~0ull};
+                    if constexpr (dec) {
+                        w = weight[tb + t];
+                        int64_t len;
+                        if (!pref_weight_ok(w) ||
+                            !aff_term(preds, term_off[tb + t], term_off[tb + t + 1], n_preds, L, present, len))
+                            continue;
+                        a = pref_term_decoded<kBuf>(preds, term_off[tb + t], term_off[tb + t + 1], present, wbase, pl);
+                    } else {
+                        const uint32_t hdr = *pr++;
+                        w = hdr >> kPrefLenBits;
+                        const int32_t len = static_cast<int32_t>(hdr & ((1u << kPrefLenBits) - 1));
+                        Words c{0, 0}, unused{0, 0};
+                        for (int32_t e0 = 0; e0 < len; e0 += kGroup) {
+                            uint32_t E[kGroup];
+                            Words V[kGroup];
+#pragma unroll
+                            for (int k = 0; k < kGroup; ++k) E[k] = (e0 + k < len) ? pr[e0 + k] : 0u;
+#pragma unroll
+                            for (int k = 0; k < kGroup; ++k)
+                                if (e0 + k < len) V[k] = pl(E[k] & kPidMask);
+#pragma unroll
+                            for (int k = 0; k < kGroup; ++k)
+                                if (e0 + k < len) fold<false>(E[k], V[k], c, a, unused);
+                        }
+                        pr += len;
+                    }
+                    score_add<kBits>(acc, w, a);
+                }
+                // best score among this lane's feasible nodes: keep the nodes
+                // that have the highest remaining score bit set, top bit first
+                auto narrow = [&](int b) {
+                    const Words t{cand.a & acc[b].a, cand.b & acc[b].b};
+                    const bool any = (t.a | t.b) != 0;
+                    cand.a = any ? t.a : cand.a;
+                    cand.b = any ? t.b : cand.b;
+                    sc |= any ? (1u << b) : 0u;
+                };
+#pragma unroll
+                for (int b = kBits - 1; b >= 0; --b) narrow(b);
             }
             if (i + 1 < nb_rows) {
                 r_next = __builtin_amdgcn_readlane(my_row, i + 1);
                 head_next = rec[static_cast<int64_t>(r_next) * kPrefRec];
                 feas_words(r_next, fa_next, fb_next);
             }
-            // best score among this lane's feasible nodes: keep the nodes
-            // that have the highest remaining score bit set, top bit first
-            Words cand{m0 & fa, m1 & fb};
-            uint32_t sc = 0;
-            auto narrow = [&](int b) {
-                const Words t{cand.a & acc[b].a, cand.b & acc[b].b};
-                const bool any = (t.a | t.b) != 0;
-                cand.a = any ? t.a : cand.a;
-                cand.b = any ? t.b : cand.b;
-                sc |= any ? (1u << b) : 0u;
-            };
-#pragma unroll
-            for (int b = kBits - 1; b >= 0; --b) narrow(b);
             const bool has = (cand.a | cand.b) != 0;
             const uint32_t node = static_cast<uint32_t>(w0) * 64u +
                                   (cand.a ? static_cast<uint32_t>(__builtin_ctzll(cand.a))
@@ -1524,10 +1601,12 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
             eval(k_pref_eval<true, 0>, "k_pref_eval");
             eval(k_pref_eval<true, 1>, "k_pref_eval16");
             eval(k_pref_eval<true, 2>, "k_pref_decode");
+            eval(k_pref_eval<true, 3>, "k_pref_eval3");
         } else {
             eval(k_pref_eval<false, 0>, "k_pref_eval");
             eval(k_pref_eval<false, 1>, "k_pref_eval16");
             eval(k_pref_eval<false, 2>, "k_pref_decode");
+            eval(k_pref_eval<false, 3>, "k_pref_eval3");
         }
         PC_LAUNCH_CHECK(ctx);
     }

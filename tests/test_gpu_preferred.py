@@ -67,6 +67,22 @@ def test_preferred_random(g, orc, seed, N, absent, p_feas):
     assert (so > 0).sum() > 100 and (co > 1).sum() > 10
 
 
+@pytest.mark.parametrize("seed,wmax", [(5, 1), (6, 2), (7, 3)])
+def test_preferred_few_terms_ties(g, orc, seed, wmax):
+    """Rows of zero to three terms (the term-pattern class) with weights of
+    at most wmax, so that different patterns of holding terms share a score
+    and the best nodes come from several patterns at once; with and without
+    a feasible bitset, several tiles and a ragged tail."""
+    N = 3 * 8192 + 77
+    wl = synth.affinity_workload(seed, N, 10, 1, card_choices=(2, 3, 5), absent_p=0.1)
+    row_off, term_off, preds, weight = synth.preferred_rows(seed, wl.meta["cards"], 900, tmin=0, tmax=3, kmin=1,
+                                                            kmax=2)
+    weight = (weight % wmax + 1).astype(np.uint32)
+    for feas in (None, _pack(np.random.default_rng(seed).random((900, N)) < 0.4)):
+        bo, so, co = _check(g, orc, wl["labels"], row_off, term_off, weight, preds, feasible=feas)
+        assert (co > 1).sum() > 100
+
+
 def test_preferred_paper_fixture(g, orc):
     fx = json.load(open(os.path.join(HERE, "golden", "paper_preferred.json")))
     keys, nodes = fx["keys"], fx["nodes"]
