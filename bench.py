@@ -33,10 +33,10 @@ HBM_PEAK_GBS = 8000.0
 # kernel source they were measured on.
 TRAFFIC = [
     {"source": "paper_2602_16100_amd/csrc/select.hip",
-     "sha256": "0f6a253f92ff0bf16abc22545aa1b495f094a4543e0191c00f627e2dce3afcbe",
+     "sha256": "32fd272e4456259cbe55b2b205b9511dd1dc619f00d50ec7843a2acc38bb9c0b",
      "workload": "cfg5",
-     "bytes_per_launch": {"k_sel_eval": 680_854_263 + 4_407_299_189,
-                          "k_aff_eval": 848_265_596 + 4_408_032_213}},
+     "bytes_per_launch": {"k_sel_eval": 680_665_526 + 4_407_300_661,
+                          "k_aff_eval": 848_232_795 + 4_408_030_538}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
      "sha256": "a4835d55482cb5524271898947678a16d3070e0962fc1aca6c2a47d57cc47d88",
      "workload": "cfg5",

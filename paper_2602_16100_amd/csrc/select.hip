@@ -1121,6 +1121,11 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
     const int32_t *rows = list + static_cast<int64_t>(kCls) * I;
     const int32_t r0 = chunk * rpc;
     const int32_t r1 = min(static_cast<int32_t>(list_len[kCls]), r0 + rpc);
+    // class 3: each wavefront stages its 64-row batch's records in LDS
+    // (one record per lane), so a row's program words cost an LDS read
+    // instead of a dependent memory load
+    __shared__ uint4 lrec_all[kCls == 3 ? kEvalThreads * (kPrefRec / 4) : 1];
+    const uint32_t *lrec = reinterpret_cast<const uint32_t *>(lrec_all + (kCls == 3 ? wave * 64 * (kPrefRec / 4) : 0));
     for (int32_t bat = r0 + wave * 64; bat < r1; bat += kEvalThreads) {
         const int32_t nb_rows = min(64, r1 - bat);
         // The batch's row ids, one per lane.  A row's record head and
@@ -1128,6 +1133,22 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
         // end read its word 0 and mask it) are requested at the end of the
         // previous row, so their latency hides behind that row's selection.
         const int32_t my_row = lane < nb_rows ? rows[bat + lane] : 0;
+        if constexpr (kCls == 3) {
+            // the previous batch's reads are done (LDS requests of one
+            // wavefront complete in order; the fences keep the compiler's
+            // order)
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            if (lane < nb_rows) {
+                const uint4 *src = reinterpret_cast<const uint4 *>(rec + static_cast<int64_t>(my_row) * kPrefRec);
+                uint4 *dst = lrec_all + (wave * 64 + lane) * (kPrefRec / 4);
+#pragma unroll
+                for (int q = 0; q < kPrefRec / 4; ++q) dst[q] = src[q];
+            }
+            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+            __builtin_amdgcn_wave_barrier();
+            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        }
         auto feas_words = [&](int32_t rr, uint64_t &a, uint64_t &b) {
             const uint64_t *fr = feasible + static_cast<int64_t>(rr) * fstride;
             a = fr[ok0 ? w0 : 0];
@@ -1140,7 +1161,7 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
         for (int32_t i = 0; i < nb_rows; ++i) {
             const int32_t r = r_next;
             const uint32_t *R = rec + static_cast<int64_t>(r) * kPrefRec;
-            const uint32_t head = head_next;
+            const uint32_t head = kCls == 3 ? lrec[i * kPrefRec] : head_next;
             const uint32_t kind = head >> 24, live = head & 0xFFFFu;
             const uint64_t fa = fa_next, fb = fb_next;
             Words cand{m0 & fa, m1 & fb};
@@ -1154,7 +1175,9 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
                     A[t] = Words{0, 0};
                     wt[t] = 0;
                 }
-                const uint32_t *pr = kind == kPrefInline ? R + 2 : prog + R[1];
+                // the program: inline words from the LDS copy, or a slice of
+                // prog; one walk for either source, inlined at each call
+                auto walk = [&](const uint32_t *pr) {
 #pragma unroll
                 for (int t = 0; t < static_cast<int>(kPrefFewTerms); ++t) {
                     if (static_cast<uint32_t>(t) < nt) {
@@ -1178,6 +1201,11 @@ __global__ __launch_bounds__(kEvalThreads) void k_pref_eval(
                         A[t] = a;
                     }
                 }
+                };
+                if (kind == kPrefInline)
+                    walk(lrec + i * kPrefRec + 2);
+                else if (kind == kPrefIndirect)
+                    walk(prog + lrec[i * kPrefRec + 1]);
                 // pattern p: term t holds iff bit t of p (terms past nt hold
                 // nowhere, so only p < 2^nt has nodes)
                 auto pattern = [&](int p) {
