@@ -44,6 +44,21 @@ TRAFFIC = [
 ]
 
 
+# Issue counters of k_tr_match on the combined workload (one rocprofv3 pass;
+# the command and the per-dispatch values are in the profiles folder).
+# Valid only for the kernel source they were measured on.
+MATCH_COUNTERS = {}
+
+
+def source_unchanged(rec):
+    import hashlib
+    path = os.path.join(ROOT, rec["source"])
+    if not os.path.exists(path):
+        return False
+    with open(path, "rb") as f:
+        return hashlib.sha256(f.read()).hexdigest() == rec["sha256"]
+
+
 def measured_traffic(workload, kernel):
     """HBM bytes per launch from the FETCH_SIZE / WRITE_SIZE counter runs
     (scaled by a plain copy's readings), or None when the kernel's source
@@ -148,43 +163,151 @@ def sample_subproblem(wl, stride):
     return dict(intents=sub, expect=ex, rows=rows, traces=tidx.astype(np.int64), queries=qidx)
 
 
-def cpu_baseline(wl, pairs_total, target_s):
+def cpu_baseline(wl, pairs_total, target_s, gpu=None):
+    """The oracle on every k-th intent (with the rows, traces and queries it
+    references) on all the job's cores, k chosen so the sample takes about
+    target_s, scaled to the whole job; the same on one thread for a smaller
+    sample.  With the GPU's outputs, the all-cores sample is compared with
+    them element by element."""
     import oracle
     threads = len(os.sched_getaffinity(0))
     env_cap = os.environ.get("OMP_NUM_THREADS")
     if env_cap and env_cap.isdigit():
         threads = min(threads, int(env_cap))
 
-    def run(stride):
+    def run(stride, nthreads):
         sp = sample_subproblem(wl, stride)
         t0 = time.perf_counter()
-        feas, pc, _ = oracle.selectors(wl["labels"], wl["pred_off"], wl["preds"], rows=sp["rows"], nthreads=threads)
+        feas, pc_, _ = oracle.selectors(wl["labels"], wl["pred_off"], wl["preds"], rows=sp["rows"],
+                                        nthreads=nthreads)
         tr, _ = oracle.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
-                             wl["hdr"], wl["ingress"], wl["ttl"], idx=sp["traces"], nthreads=threads)
+                             wl["hdr"], wl["ingress"], wl["ttl"], idx=sp["traces"], nthreads=nthreads)
         rc, _ = oracle.reach(wl["V"], wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"],
-                             wl["target"], qidx=sp["queries"], nthreads=threads)
-        oracle.report(sp["intents"], feas, pc, wl["N"], tr, sp["expect"], rc)
-        return time.perf_counter() - t0, sp
+                             wl["target"], qidx=sp["queries"], nthreads=nthreads)
+        _, reason, _, _ = oracle.report(sp["intents"], feas, pc_, wl["N"], tr, sp["expect"], rc)
+        return time.perf_counter() - t0, sp, dict(feasible=feas, popcnt=pc_, traces=tr, reach=rc, reason=reason)
+
+    def calibrated(nthreads, target):
+        stride = 4096
+        t, sp, res = run(stride, nthreads)
+        # shrink the stride (at most 64x per probe) until the sample takes about target
+        while t < target / 2 and stride > 1:
+            stride = max(1, stride // 64, int(stride * max(t, 1e-3) / target))
+            t, sp, res = run(stride, nthreads)
+        return stride, t, sp, res
 
     I = wl["intents"].shape[0]
-    stride = 4096
-    t, sp = run(stride)
-    # shrink the stride (at most 64x per probe) until the sample takes about target_s
-    while t < target_s / 2 and stride > 1:
-        stride = max(1, stride // 64, int(stride * max(t, 1e-3) / target_s))
-        t, sp = run(stride)
+    stride, t, sp, res = calibrated(threads, target_s)
     frac = sp["intents"].shape[0] / I
     est_full = t / frac
-    return {
+    s1, t1, sp1, _ = calibrated(1, target_s / 2)
+    est1 = t1 / (sp1["intents"].shape[0] / I)
+    out = {
         "value": pairs_total / est_full,
         "unit": "selector evals/s (whole-job estimate)",
         "cores": threads,
         "kind": "oracle",
+        "cpu_model": cpu_model(),
         "sample": (f"every {stride}th intent ({sp['intents'].shape[0]} of {I}: {sp['rows'].shape[0]} selector rows "
                    f"x {wl['N']} nodes, {sp['traces'].shape[0]} traces, {sp['queries'].shape[0]} reach queries, "
-                   f"report) in {t:.2f} s; whole job estimated at {est_full:.1f} s"),
+                   f"report) in {t:.2f} s on {threads} threads; whole job estimated at {est_full:.1f} s"),
         "est_step_s": est_full,
+        "one_thread": {"value": pairs_total / est1, "cores": 1, "est_step_s": est1,
+                       "sample": f"every {s1}th intent ({sp1['intents'].shape[0]} of {I}) in {t1:.2f} s"},
     }
+    if gpu is not None:
+        idx = np.arange(0, I, stride)
+        checks = [("feasible", res["feasible"], gpu["feasible"][sp["rows"]]),
+                  ("popcnt", res["popcnt"], gpu["popcnt"][sp["rows"]]),
+                  ("reach", res["reach"], gpu["reach"][sp["queries"]]),
+                  ("reason", res["reason"], gpu["reason"][idx])]
+        for f in ("jmask", "last_switch", "last_port", "hops", "state"):
+            checks.append((f"traces.{f}", res["traces"][f], gpu["traces"][f][sp["traces"]]))
+        verdict = "bit-exact"
+        for name, a, b in checks:
+            if a.shape != b.shape or not np.array_equal(a, b):
+                bad = np.argwhere(a != b) if a.shape == b.shape else None
+                verdict = (f"MISMATCH in {name}" + (f" at {tuple(bad[0])}: oracle {a[tuple(bad[0])]} gpu "
+                                                   f"{b[tuple(bad[0])]}" if bad is not None and bad.size else
+                                                   f": shapes {a.shape} vs {b.shape}"))
+                break
+        out["parity"] = verdict
+        out["parity_scope"] = (f"the all-cores sample ({sp['intents'].shape[0]} of {I} intents, "
+                               f"{sp['rows'].shape[0]} selector rows, {sp['traces'].shape[0]} traces, "
+                               f"{sp['queries'].shape[0]} reach queries) against the GPU's outputs of the last step")
+    return out
+
+
+HOP_KERNELS = ("k_tr_init", "k_tr_plan", "k_tr_scatter", "k_tr_match", "k_tr_walk")
+
+
+def trace_levels(wl, pc, ctx, D, full):
+    """Switches touched per hop level, from the library's own traces: run
+    with TTL l, a trace that still looks up at level l stops there (TTL, or
+    its terminal state) with its level-l switch as last_switch.  Returns
+    {"levels": [(lookups, touched switches, rules of the touched switches,
+    32-rule groups of the touched switches)], "lookups": total}."""
+    import torch
+    ing = wl["ingress"]
+    S = wl["S"]
+    started = (ing >= 0) & (ing < S)
+    hops = full["hops"].astype(np.int64)
+    R = np.diff(np.asarray(wl["rule_off"], np.int64))
+    Gs = (R + 31) // 32
+    out = torch.empty((wl["T"], 12), dtype=torch.uint8, device="cuda:0")
+    levels = []
+    for lv in range(int(hops[started].max()) + 1 if started.any() else 0):
+        live = started & (hops >= lv)
+        if lv == 0:
+            sw = ing[live]
+        else:
+            pc.pc_trace_flows(S, D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                              D["ingress"], lv, out=out, ctx=ctx)
+            sw = pc.records(out, pc.TRACE_OUT_DT)["last_switch"][live]
+        u = np.unique(sw)
+        levels.append((int(live.sum()), int(u.shape[0]), int(R[u].sum()), int(Gs[u].sum())))
+    return {"levels": levels, "lookups": int(sum(x[0] for x in levels))}
+
+
+def trace_roofline(wl, pc, ctx, D, full, prof, steps, workload):
+    """The hop loop (every kernel of A3 after the rule-table preparation)
+    against the HBM roofline.  Algorithmic bytes follow the survey's
+    definition: 30 B per rule of every switch a level touches, plus each
+    trace's header, ingress and record (32 B).  `layout_bytes` is what this
+    library's layout needs for the same levels: the 384 B of chunk sets of
+    each 32-rule group of a touched switch, plus the same 32 B per trace."""
+    lv = trace_levels(wl, pc, ctx, D, full)
+    T = wl["T"]
+    alg = sum(r for _, _, r, _ in lv["levels"]) * 30 + T * 32
+    layout = sum(g for _, _, _, g in lv["levels"]) * 384 + T * 32
+    per_k = {k: prof[k][1] / steps for k in HOP_KERNELS if k in prof}
+    ms = sum(per_k.values())
+    gbs = alg / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
+    match_ms = per_k.get("k_tr_match", 0.0)
+    out = {"kernel": "+".join(k for k in HOP_KERNELS if k in per_k), "bound": "hbm", "achieved": gbs,
+           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
+           "traffic": measured_traffic(workload, "hop_loop"),
+           "alg_bytes_per_step": alg, "layout_bytes_per_step": layout,
+           "layout_gbs": layout / (ms * 1e-3) / 1e9 if ms > 0 else 0.0,
+           "ms_per_step": ms, "ms_per_kernel": per_k,
+           "lookups_per_step": lv["lookups"],
+           "switch_levels": [{"lookups": a, "switches": b, "rules": c} for a, b, c, _ in lv["levels"]],
+           "k_tr_match_frac_alg": (alg / (match_ms * 1e-3) / 1e9 / HBM_PEAK_GBS) if match_ms > 0 else None}
+    c = MATCH_COUNTERS.get(workload)
+    if c is not None and source_unchanged(c):
+        out["k_tr_match_counters"] = c["values"]
+    return out
+
+
+def cpu_model():
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def time_paths(args, wl, D, pc, ctx, feasible, popcnt):
@@ -890,6 +1013,13 @@ def main():
                                        "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": prep_gbs / HBM_PEAK_GBS,
                                        "traffic": measured_traffic(args.workload, "k_tr_prep"),
                                        "alg_bytes_per_launch": prep_bytes, "avg_launch_ms": prep_avg}
+    if only in ("all", "trace"):
+        line["trace_roofline"] = trace_roofline(wl, pc, ctx, D, tr, prof, args.steps, args.workload)
+    gpu_out = None
+    if only == "all" and not args.no_cpu_baseline:
+        # the last timed step's outputs, for the oracle's parity check
+        gpu_out = {"feasible": feasible.cpu().numpy().view(np.uint64), "popcnt": popcnt.cpu().numpy().view(np.uint32),
+                   "traces": tr, "reach": reach.cpu().numpy(), "reason": reason.cpu().numpy()}
     if only == "all" and not args.no_paths:
         line["paths"] = time_paths(args, wl, D, pc, ctx, feasible, popcnt)
     if only == "all" and not args.no_affinity:
@@ -909,7 +1039,7 @@ def main():
     if only == "all" and not args.no_rule_delta:
         line["rule_delta"] = time_rule_delta(args, wl, pc, ctx, D)
     if not args.no_cpu_baseline:
-        line["cpu_baseline"] = cpu_baseline(wl, pairs, args.cpu_seconds)
+        line["cpu_baseline"] = cpu_baseline(wl, pairs, args.cpu_seconds, gpu=gpu_out)
     print(json.dumps(line), flush=True)
 
 

@@ -106,3 +106,22 @@ def tables_from_lists(per_switch):
     for i, r in enumerate(allr):
         rules[i] = r
     return rule_off, rules
+
+
+def leak_fixture():
+    """The paper's transit-switch case (golden paper_transit_leak.json): three
+    switches on a line, exact-match rules along the flow's path.
+    Returns (fixture, topology, path, key, rule_off, rules)."""
+    fx = load_golden("paper_transit_leak.json")
+    names = [s["name"] for s in fx["switches"]]
+    nbr = [[names.index(x) for x in s["links"]] for s in fx["switches"]]
+    jur = [fx["regions"].index(s["region"]) for s in fx["switches"]]
+    topo = ports_topology(nbr, jur, hosts_per_switch=1)
+    path = [names.index(x) for x in fx["flow"]["path"]]
+    key = np.array([0x0A000001, 0x0A000003, (4000 << 16) | 443, 6], np.uint32)
+    per = [[] for _ in names]
+    for i, s in enumerate(path):
+        a = topo["nbr"][s].index(path[i + 1]) if i + 1 < len(path) else len(topo["nbr"][s])
+        per[s].append(exact_rule(key, a))
+    rule_off, rules = tables_from_lists(per)
+    return fx, topo, path, key, rule_off, rules

@@ -11,26 +11,10 @@ import numpy as np
 import pytest
 
 import synth
-from helpers import exact_rule, load_golden, ports_topology, tables_from_lists
+from helpers import leak_fixture as _leak_fixture, load_golden
 
 REASONS = {"PASS": 0, "NO_FEASIBLE_NODE": 1, "ENDPOINT_INFEASIBLE": 2, "NO_FLOW": 3, "LEAK": 4,
            "UNDELIVERED": 5, "WRONG_EGRESS": 6, "MALFORMED": 7}
-
-
-def _leak_fixture():
-    fx = load_golden("paper_transit_leak.json")
-    names = [s["name"] for s in fx["switches"]]
-    nbr = [[names.index(x) for x in s["links"]] for s in fx["switches"]]
-    jur = [fx["regions"].index(s["region"]) for s in fx["switches"]]
-    topo = ports_topology(nbr, jur, hosts_per_switch=1)
-    path = [names.index(x) for x in fx["flow"]["path"]]
-    key = np.array([0x0A000001, 0x0A000003, (4000 << 16) | 443, 6], np.uint32)
-    per = [[] for _ in names]
-    for i, s in enumerate(path):
-        a = topo["nbr"][s].index(path[i + 1]) if i + 1 < len(path) else len(topo["nbr"][s])
-        per[s].append(exact_rule(key, a))
-    rule_off, rules = tables_from_lists(per)
-    return fx, topo, path, key, rule_off, rules
 
 
 def test_paper_transit_leak_and_noop(orc):
