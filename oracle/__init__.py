@@ -17,7 +17,9 @@ import numpy as np
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
 _SRC = os.path.join(_HERE, "pc_oracle.c")
-_LIB = os.path.join(_HERE, "_pc_oracle.so")
+# PC_ORACLE_LIB names another build of the same source (the sanitizer test
+# loads an AddressSanitizer / UBSan build through it)
+_LIB = os.environ.get("PC_ORACLE_LIB") or os.path.join(_HERE, "_pc_oracle.so")
 
 TRACE_DT = np.dtype([("jmask", "<u4"), ("last_switch", "<i4"), ("last_port", "<u2"),
                      ("hops", "u1"), ("state", "u1")])
@@ -34,14 +36,18 @@ F_PRED, F_OFFSETS, F_ACTION, F_SWITCH, F_JUR, F_GRAPH, F_INTENT, F_NODE = 1, 2, 
 _lib = None
 
 
-def build(force=True):
-    """Compile the oracle with gcc (-O2, OpenMP)."""
-    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Werror",
-           "-o", _LIB + ".tmp", _SRC]
-    if force or not os.path.exists(_LIB):
+def build(force=True, out=None, sanitize=False):
+    """Compile the oracle with gcc (-O2, OpenMP).  sanitize=True adds
+    AddressSanitizer and UBSan (every finding aborts) for a build at `out`."""
+    out = out or _LIB
+    cmd = ["gcc", "-O2", "-std=c11", "-fopenmp", "-fPIC", "-shared", "-Wall", "-Werror"]
+    if sanitize:
+        cmd += ["-g", "-fno-omit-frame-pointer", "-fsanitize=address,undefined", "-fno-sanitize-recover=all"]
+    cmd += ["-o", out + ".tmp", _SRC]
+    if force or not os.path.exists(out):
         subprocess.check_call(cmd)
-        os.replace(_LIB + ".tmp", _LIB)
-    return _LIB
+        os.replace(out + ".tmp", out)
+    return out
 
 
 def _load():
