@@ -651,10 +651,13 @@ def time_rule_delta(args, wl, pc, ctx, D):
     switches of the combined workload's fat-tree, against a full
     pc_trace_flows on the new tables.  The previous records, summaries and
     walk records are restored before each timed call; the timed region is
-    the call alone.  Each change starts from a context whose kept prepared
-    tables are the original ones."""
+    the call alone.  The context declares the keep-tables promise (tables
+    change only in the listed switches between calls), so each delta
+    re-prepares only its listed switches; each change starts from a context
+    whose kept prepared tables are the original ones."""
     import torch
     import synth
+    ctx.keep_tables(True)
     dev = D["ingress"].device
     S, T, ttl = wl["S"], wl["T"], wl["ttl"]
     out0 = torch.empty((T, 12), dtype=torch.uint8, device=dev)
@@ -723,6 +726,7 @@ def time_rule_delta(args, wl, pc, ctx, D):
                                      "sample": f"{samp.shape[0]} of the {sel.shape[0]} selected traces, scaled: "
                                                f"{t:.3f} s per delta"}
         res["per_change"][name] = entry
+    ctx.keep_tables(False)
     return res
 
 

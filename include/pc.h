@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 8
+#define PC_VERSION 9
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -405,17 +405,28 @@ int pc_report(pc_ctx *ctx, int32_t I, const pc_intent *intents, int32_t rows, co
  *              written with out / vsum: a call with walk NULL leaves them
  *              stale for later calls.
  * n_retraced : int32, device memory.
- * Prepared tables: the context keeps the prepared flow tables of its last
- * pc_trace_flows_delta call.  A call with C >= 0 and the same S reuses
- * them, re-preparing only the changed switches, when no switch's number of
- * 32-rule groups changed; otherwise it prepares every switch.  So with
- * C >= 0 the tables passed must also differ from those of the context's
- * previous pc_trace_flows_delta call (if it had the same S) only in the
- * changed switches' rules; a fresh context, or a call with C < 0, starts
- * from a full preparation.  Every call sweeps the whole input for data
- * errors, as pc_trace_flows (the action flags of switches not re-prepared
+ * Prepared tables: by default every call prepares every switch's tables,
+ * so the result depends only on the arguments.  After
+ * pc_trace_keep_tables(ctx, 1) the context keeps the prepared tables of its
+ * last pc_trace_flows_delta call, and a call with C >= 0 and the same S
+ * reuses them, re-preparing only the changed switches, when no switch's
+ * number of 32-rule groups changed (otherwise it prepares every switch).
+ * That reuse is correct only under the caller's promise that the tables
+ * passed differ from those of the context's previous pc_trace_flows_delta
+ * call only in the changed switches' rules; the library does not check the
+ * contents of unlisted switches.  A call with C < 0 always starts from a
+ * full preparation.  Every call sweeps the whole input for data errors, as
+ * pc_trace_flows (with reuse, the action flags of switches not re-prepared
  * are the ones found when they were prepared).
  */
+/* Declare (enable = 1) or withdraw (enable = 0) the promise that, on this
+ * context, consecutive pc_trace_flows_delta calls with C >= 0 pass tables
+ * that differ from the previous call's only in the listed switches; with
+ * it, those calls re-prepare only the listed switches (see above).
+ * Withdrawing drops the kept tables.  Off on a new context.  PC_EINVAL on
+ * a NULL context. */
+int pc_trace_keep_tables(pc_ctx *ctx, int enable);
+
 int pc_trace_flows_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer,
                          int64_t n_ports, const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules,
                          int64_t n_rules, const pc_key *hdr, const int32_t *ingress, int32_t T, int32_t ttl,

@@ -97,6 +97,7 @@ def lib():
     L.pc_trace_flows_delta.argtypes = [P, I32, P, P, I64, P, P, P, I64, P, P, I32, I32, P, I32, P, P, P, P, P]
     L.pc_masked_reach_via.argtypes = [P, I32, P, P, I64, P, I32, P, P, P, P, I32, P, I32, P, P]
     L.pc_report_paths.argtypes = [P, I32, P, I32, P, I32, P, I32, P, I32, P, P, I32, P, P, P, P, P, P]
+    L.pc_trace_keep_tables.argtypes = [P, C]
     L.pc_profile.argtypes = [P, C]
     L.pc_profile_read.argtypes = [P, C, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I64),
                                   ctypes.POINTER(ctypes.c_double)]
@@ -108,7 +109,7 @@ EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_e
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
             "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths",
             "pc_update_nodes", "pc_eval_selectors_count", "pc_probe_selectors", "pc_report_counts",
-            "pc_score_preferred", "pc_trace_flows_delta")
+            "pc_score_preferred", "pc_trace_flows_delta", "pc_trace_keep_tables")
 
 
 class Context:
@@ -143,6 +144,15 @@ class Context:
         self.check(lib().pc_data_errors(self.handle, _stream(stream), ctypes.byref(f), int(clear)))
         return int(f.value)
 
+
+    def keep_tables(self, enable: bool):
+        """Declare (True) that on this context, consecutive
+        pc_trace_flows_delta calls with a change list pass tables that differ
+        from the previous call's only in the listed switches: those calls
+        then re-prepare only the listed switches.  The library does not check
+        unlisted switches, so breaking the promise gives stale results.
+        Off by default: every delta call prepares every switch."""
+        self.check(lib().pc_trace_keep_tables(self.handle, int(enable)))
 
     def profile(self, enable: bool):
         """Reset the per-kernel timing tallies and switch timing on or off."""
@@ -452,7 +462,10 @@ def pc_trace_flows_delta(S, port_off, port_peer, jur, rule_off, rules, hdr, ingr
     hold the results on the previous tables; only traces that visited a
     changed switch (exactly, for walks that fit their record; by summary
     bits otherwise) are traced again on the tables given.  Returns the
-    number of traces traced again (an int32 device tensor of one element)."""
+    number of traces traced again (an int32 device tensor of one element).
+    Every switch's tables are prepared again on each call unless the
+    context's keep_tables(True) promise is in force (then only the listed
+    switches are; the promise is the caller's to keep)."""
     ctx = ctx or context()
     T = int(ingress.shape[0])
     n_ports = int(port_peer.shape[0]) if n_ports is None else int(n_ports)

@@ -142,6 +142,14 @@ int pc_profile_read(pc_ctx *ctx, int idx, const char **name, int64_t *launches, 
 
 int pc_version(void) { return PC_VERSION; }
 
+int pc_trace_keep_tables(pc_ctx *ctx, int enable)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->tc_keep = enable != 0;
+    if (!ctx->tc_keep) ctx->tc_S = -1;  // nothing kept survives switching reuse off
+    return PC_OK;
+}
+
 const char *pc_last_error(const pc_ctx *ctx) { return ctx ? ctx->msg : "null context"; }
 
 int pc_create(pc_ctx **out, int device)

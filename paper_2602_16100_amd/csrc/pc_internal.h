@@ -33,6 +33,7 @@ struct pc_ctx {
     int32_t tc_S = -1;
     int64_t tc_groups = 0;
     int64_t tc_blocks = 0;
+    bool tc_keep = false;  // pc_trace_keep_tables: delta calls may reuse the kept tables
     hipEvent_t lvl_ev[2];  // trace level loop: completion of a level's live count copy
     // optional per-kernel timing (pc_profile)
     bool prof;

@@ -1174,9 +1174,10 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
                                     bitmap, ingress, T, S, mask, list, count, ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
     }
-    // the cache holds the previous tables when its switch count matches; it
-    // serves the new ones when no switch's group count changed
-    const bool cached = ctx->tc_S == S && S > 0;
+    // with reuse declared (pc_trace_keep_tables) the cache holds the previous
+    // tables when its switch count matches; it serves the new ones when no
+    // switch's group count changed.  Without it every call prepares anew.
+    const bool cached = ctx->tc_keep && ctx->tc_S == S && S > 0;
     if (cached) {
         const TcMeta m = tc_meta(ctx, S);
         PC_TIMED(ctx, "k_tr_switch_info", stream,

@@ -69,6 +69,7 @@ def test_null_context_is_einval(libpc):
     assert L.pc_report(None, 0, None, 0, None, 0, None, 0, None, 0, None, None, 0, None, None, None, None) == EINVAL
     f = ctypes.c_uint32()
     assert L.pc_data_errors(None, None, ctypes.byref(f), 0) == EINVAL
+    assert L.pc_trace_keep_tables(None, 1) == EINVAL
     assert L.pc_create(None, 0) == EINVAL
     assert L.pc_destroy(None) == libpc.PC_OK
 

@@ -123,6 +123,7 @@ def test_chained_deltas_on_gpu(g, orc, name):
     rule_off, rules = wl["rule_off"], wl["rules"]
     import paper_2602_16100_amd as pc
     ctx = pc.Context(0)  # one context: later calls re-prepare only the changed switches
+    ctx.keep_tables(True)
     rec, vs, wk, _, _ = _run(wl, rule_off, rules, None, None, None, ctx=ctx)
     rng = np.random.default_rng(9)
     for step in range(4):
@@ -142,6 +143,7 @@ def test_chain_across_group_boundaries(g, orc):
     import paper_2602_16100_amd as pc
     wl = synth.trace_workload(7, 8, 4, 32, 4000, 12, 300, variant="dense")
     ctx = pc.Context(0)
+    ctx.keep_tables(True)
     rule_off, rules = wl["rule_off"], wl["rules"]
     rec, vs, wk, _, _ = _run(wl, rule_off, rules, None, None, None, ctx=ctx)
     for step, (sw, resize) in enumerate([([4, 9], True), ([30], False), ([4, 11, 70], True), ([5], False)]):
@@ -201,6 +203,7 @@ def test_delta_combined_workload_size(g, orc):
     import paper_2602_16100_amd as pc
     wl = synth.cfg5()
     ctx = pc.Context(0)
+    ctx.keep_tables(True)
     rec, vs, wk, n, _ = _run(wl, wl["rule_off"], wl["rules"], None, None, None, ctx=ctx)
     k, h = 48, 24  # pod p: edge switches p*k + [0, h), aggregation p*k + [h, k); core from k*k
     changed = np.array([k * k + 5, 3 * k + h + 6, 10 * k + h + 16, 0, 5 * k + 2, 20 * k + 7], np.int32)
@@ -220,3 +223,52 @@ def test_delta_combined_workload_size(g, orc):
     ro, vo, wo, err = _oracle(orc, wl, r_off2, rules2, idx=idx)
     _same_records(rec2[idx], ro)
     assert np.array_equal(vs2[idx], vo) and np.array_equal(wk2[idx], wo) and err == 0
+
+
+@pytest.mark.parametrize("keep", [False, True])
+def test_two_workloads_of_equal_size_on_one_context(g, orc, keep):
+    """A delta chain on one workload, then a first call and a delta on a
+    second workload with the same switch count, all on one context.  Without
+    the keep-tables promise every call prepares anew; with it, the second
+    workload's first call (C < 0) replaces the kept tables.  Either way the
+    second workload's delta equals the oracle's full trace."""
+    import paper_2602_16100_amd as pc
+    wa = synth.trace_workload(11, 8, 4, 40, 3000, 12, 250, variant="dense")
+    wb = synth.trace_workload(12, 8, 4, 40, 3000, 12, 250, variant="dense")
+    assert wa["S"] == wb["S"]
+    ctx = pc.Context(0)
+    ctx.keep_tables(keep)
+    rec, vs, wk, _, _ = _run(wa, wa["rule_off"], wa["rules"], None, None, None, ctx=ctx)
+    ra, rules_a = synth.mutate_tables(3, wa["port_off"], wa["rule_off"], wa["rules"], [5, 9])
+    _run(wa, ra, rules_a, rec, vs, np.array([5, 9], np.int32), walk=wk, ctx=ctx)
+    # workload B: its results from the oracle, then a delta on the same context
+    ro, vo, wo, _ = _oracle(orc, wb, wb["rule_off"], wb["rules"])
+    if keep:  # the promise covers calls on the same tables: B starts with a full call
+        rec_b, vs_b, wk_b, _, _ = _run(wb, wb["rule_off"], wb["rules"], None, None, None, ctx=ctx)
+        _same_records(rec_b, ro)
+    rb, rules_b = synth.mutate_tables(4, wb["port_off"], wb["rule_off"], wb["rules"], [7])
+    rec2, vs2, wk2, n, flags = _run(wb, rb, rules_b, ro, vo, np.array([7], np.int32), walk=wo, ctx=ctx)
+    ro2, vo2, wo2, err = _oracle(orc, wb, rb, rules_b)
+    _same_records(rec2, ro2)
+    assert np.array_equal(vs2, vo2) and np.array_equal(wk2, wo2) and flags == err
+
+
+def test_default_context_prepares_every_call(g, orc):
+    """Without the promise, a delta call on tables that differ from the
+    context's previous call in unlisted switches as well still equals the
+    oracle: every call prepares every switch.  (The previous results passed
+    in are those of the tables' last version, as the delta contract asks.)"""
+    import paper_2602_16100_amd as pc
+    wl = synth.trace_workload(13, 8, 4, 40, 3000, 12, 250, variant="dense")
+    ctx = pc.Context(0)
+    _run(wl, wl["rule_off"], wl["rules"], None, None, None, ctx=ctx)          # the context's last tables: A
+    r2, rules2 = synth.mutate_tables(6, wl["port_off"], wl["rule_off"], wl["rules"], [3, 17, 40])   # B
+    rb, vb, wb_, _ = _oracle(orc, wl, r2, rules2)
+    r3, rules3 = synth.mutate_tables(7, wl["port_off"], r2, rules2, [20, 21])                     # C
+    rec3, vs3, wk3, n, flags = _run(wl, r3, rules3, rb, vb, np.array([20, 21], np.int32), walk=wb_, ctx=ctx)
+    ro3, vo3, wo3, err3 = _oracle(orc, wl, r3, rules3)
+    _same_records(rec3, ro3)
+    assert np.array_equal(vs3, vo3) and np.array_equal(wk3, wo3) and flags == err3
+    # the selected walks meet the switches that changed between A and B as well
+    both = np.isin(wb_, [20, 21]).any(axis=1) & np.isin(wb_, [3, 17, 40]).any(axis=1)
+    assert both.sum() > 0
