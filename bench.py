@@ -24,6 +24,8 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
+# 256 CUs x 64 lanes x 2.4 GHz: one wave-wide integer VALU instruction per CU per clock
+VALU_PEAK_LANE_OPS = 256 * 64 * 2.4e9
 
 # HBM bytes per launch of k_sel_eval, k_aff_eval and k_tr_prep on the
 # combined workload, from one rocprofv3 FETCH_SIZE pass and one WRITE_SIZE
@@ -238,64 +240,80 @@ def cpu_baseline(wl, pairs_total, target_s, gpu=None):
     return out
 
 
-HOP_KERNELS = ("k_tr_init", "k_tr_plan", "k_tr_scatter", "k_tr_match", "k_tr_walk")
+HOP_KERNELS = ("k_tr_init", "k_tr_plan", "k_tr_scatter", "k_tr_match", "k_tr_walk")  # A3 after preparation
+
+
+WALK_MAX = 8192  # the library's default switch-over to per-trace walks (PC_TRACE_WALK_MAX)
 
 
 def trace_levels(wl, pc, ctx, D, full):
-    """Switches touched per hop level, from the library's own traces: run
-    with TTL l, a trace that still looks up at level l stops there (TTL, or
-    its terminal state) with its level-l switch as last_switch.  Returns
-    {"levels": [(lookups, touched switches, rules of the touched switches,
-    32-rule groups of the touched switches)], "lookups": total}."""
+    """The hop levels the bucketed match kernel runs, with the switches each
+    touches, from the library's own walk records (the first 8 switches of
+    every walk).  The library buckets level 0 when more than WALK_MAX traces
+    start, and level l >= 1 when more than WALK_MAX traces entered level
+    l - 1; later levels are walked per trace.  Returns the per-level
+    (lookups, touched switches, rules of those switches) of the bucketed
+    levels and the lookups of the walked ones."""
     import torch
     ing = wl["ingress"]
-    S = wl["S"]
+    S, T = wl["S"], wl["T"]
     started = (ing >= 0) & (ing < S)
     hops = full["hops"].astype(np.int64)
     R = np.diff(np.asarray(wl["rule_off"], np.int64))
-    Gs = (R + 31) // 32
-    out = torch.empty((wl["T"], 12), dtype=torch.uint8, device="cuda:0")
-    levels = []
-    for lv in range(int(hops[started].max()) + 1 if started.any() else 0):
-        live = started & (hops >= lv)
-        if lv == 0:
-            sw = ing[live]
+    live = [int((started & (hops >= lv)).sum()) for lv in range(int(hops[started].max()) + 1)] if started.any() \
+        else []
+    bucketed = []
+    for lv in range(len(live)):
+        if (live[0] if lv == 0 else live[lv - 1]) > WALK_MAX:
+            bucketed.append(lv)
         else:
-            pc.pc_trace_flows(S, D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
-                              D["ingress"], lv, out=out, ctx=ctx)
-            sw = pc.records(out, pc.TRACE_OUT_DT)["last_switch"][live]
+            break
+    if bucketed and bucketed[-1] >= 8:
+        raise SystemExit("bench: more than 8 bucketed levels; walk records cannot name their switches")
+    out = torch.empty((T, 12), dtype=torch.uint8, device="cuda:0")
+    vs = torch.empty(T, dtype=torch.int64, device="cuda:0")
+    wk = torch.empty((T, 8), dtype=torch.int32, device="cuda:0")
+    pc.pc_trace_flows_delta(S, D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                            D["ingress"], wl["ttl"], out, vs, walk=wk, ctx=ctx)
+    walk = wk.cpu().numpy()
+    levels = []
+    for lv in bucketed:
+        sw = walk[started & (hops >= lv), lv]
         u = np.unique(sw)
-        levels.append((int(live.sum()), int(u.shape[0]), int(R[u].sum()), int(Gs[u].sum())))
-    return {"levels": levels, "lookups": int(sum(x[0] for x in levels))}
+        levels.append((live[lv], int(u.shape[0]), int(R[u].sum())))
+    walked = int(sum(live[len(bucketed):]))
+    return {"levels": levels, "walked_lookups": walked, "lookups": int(sum(live))}
 
 
 def trace_roofline(wl, pc, ctx, D, full, prof, steps, workload):
-    """The hop loop (every kernel of A3 after the rule-table preparation)
-    against the HBM roofline.  Algorithmic bytes follow the survey's
-    definition: 30 B per rule of every switch a level touches, plus each
-    trace's header, ingress and record (32 B).  `layout_bytes` is what this
-    library's layout needs for the same levels: the 384 B of chunk sets of
-    each 32-rule group of a touched switch, plus the same 32 B per trace."""
+    """k_tr_match, the hop loop's dominant kernel, against the HBM roofline
+    with the survey's algorithmic bytes: 30 B per rule of every switch a
+    bucketed level touches, plus 32 B per trace (header, ingress, record).
+    `layout_bytes` is what this library's layout needs for the same levels
+    (384 B of chunk sets per 32-rule group).  The issue counters of the
+    kernel, when recorded for its current source, give the ALU view."""
     lv = trace_levels(wl, pc, ctx, D, full)
     T = wl["T"]
-    alg = sum(r for _, _, r, _ in lv["levels"]) * 30 + T * 32
-    layout = sum(g for _, _, _, g in lv["levels"]) * 384 + T * 32
-    per_k = {k: prof[k][1] / steps for k in HOP_KERNELS if k in prof}
-    ms = sum(per_k.values())
+    R = np.diff(np.asarray(wl["rule_off"], np.int64))
+    rules = sum(r for _, _, r in lv["levels"])
+    alg = rules * 30 + T * 32
+    n, ms_tot = prof.get("k_tr_match", (0, 0.0))
+    ms = ms_tot / steps
     gbs = alg / (ms * 1e-3) / 1e9 if ms > 0 else 0.0
-    match_ms = per_k.get("k_tr_match", 0.0)
-    out = {"kernel": "+".join(k for k in HOP_KERNELS if k in per_k), "bound": "hbm", "achieved": gbs,
-           "peak": HBM_PEAK_GBS, "unit": "GB/s", "frac": gbs / HBM_PEAK_GBS,
-           "traffic": measured_traffic(workload, "hop_loop"),
-           "alg_bytes_per_step": alg, "layout_bytes_per_step": layout,
-           "layout_gbs": layout / (ms * 1e-3) / 1e9 if ms > 0 else 0.0,
-           "ms_per_step": ms, "ms_per_kernel": per_k,
-           "lookups_per_step": lv["lookups"],
-           "switch_levels": [{"lookups": a, "switches": b, "rules": c} for a, b, c, _ in lv["levels"]],
-           "k_tr_match_frac_alg": (alg / (match_ms * 1e-3) / 1e9 / HBM_PEAK_GBS) if match_ms > 0 else None}
+    hop_ms = {k: prof[k][1] / steps for k in HOP_KERNELS if k in prof}
+    out = {"kernel": "k_tr_match", "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+           "frac": gbs / HBM_PEAK_GBS, "traffic": measured_traffic(workload, "k_tr_match"),
+           "alg_bytes_per_step": alg, "launches_per_step": n / steps, "ms_per_step": ms,
+           "bucketed_levels": [{"lookups": a, "switches": b, "rules": c} for a, b, c in lv["levels"]],
+           "walked_lookups": lv["walked_lookups"],
+           "hop_loop_ms_per_kernel": hop_ms, "hop_loop_ms": sum(hop_ms.values()),
+           "hop_loop_frac": (alg / (sum(hop_ms.values()) * 1e-3) / 1e9 / HBM_PEAK_GBS) if hop_ms else None}
     c = MATCH_COUNTERS.get(workload)
-    if c is not None and source_unchanged(c):
-        out["k_tr_match_counters"] = c["values"]
+    if c is not None and source_unchanged(c) and ms > 0:
+        lane_ops = c["SQ_INSTS_VALU_per_step"] * 64 / (ms * 1e-3)
+        out["alu"] = {"bound": "alu", "achieved": lane_ops, "peak": VALU_PEAK_LANE_OPS, "unit": "lane-ops/s",
+                      "frac": lane_ops / VALU_PEAK_LANE_OPS, "salu_frac": c["SQ_INSTS_SALU_per_step"] * 64 /
+                      (ms * 1e-3) / VALU_PEAK_LANE_OPS, "source": "issue counters (profiles folder)"}
     return out
 
 
