@@ -63,7 +63,7 @@
 extern "C" {
 #endif
 
-#define PC_VERSION 9
+#define PC_VERSION 10
 
 enum { PC_OK = 0, PC_EINVAL = -1, PC_ENOMEM = -2, PC_EDEVICE = -3 };
 
@@ -232,6 +232,27 @@ int pc_profile_read(pc_ctx *ctx, int idx, const char **name, int64_t *launches, 
 int pc_eval_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L,
                       const int32_t *pred_off, const pc_pred *preds, int64_t n_preds, int32_t I,
                       uint64_t *feasible, uint32_t *popcnt, void *stream);
+
+/*
+ * pc_eval_selectors for callers that cannot allocate device memory: code
+ * recorded into a HIP graph, tight serving loops, and hosts whose harness
+ * forbids hipMalloc.  Same arguments, results, errors and data-error flags
+ * as pc_eval_selectors; its scratch (value planes, compiled row programs,
+ * popcount partials) lives in a fixed array of PC_NOALLOC_SCRATCH_BYTES that
+ * the library's code object holds on each device until the process ends,
+ * and the call makes no allocation (no hipMalloc / hipFree; with profiling
+ * off, no event either).  A workload whose scratch would exceed the array
+ * returns PC_EINVAL before any device work, naming the bytes it needs
+ * (for N <= 8192 nodes the value planes take (L * min(N, 256) + 1) * 1152
+ * bytes, each row 64 bytes and each predicate 16 bytes).  Every call on a
+ * device shares that device's array: calls that overlap on one device (on
+ * different streams or host threads, through any context) race and must be
+ * ordered by the caller.
+ */
+#define PC_NOALLOC_SCRATCH_BYTES (64u << 20)
+int pc_eval_selectors_noalloc(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                              const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
+                              void *stream);
 
 /*
  * A1, full node affinity -- placement directives compiled into Kubernetes

@@ -82,6 +82,7 @@ def lib():
     L.pc_version.restype = C
     L.pc_data_errors.argtypes = [P, P, ctypes.POINTER(ctypes.c_uint32), C]
     L.pc_eval_selectors.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
+    L.pc_eval_selectors_noalloc.argtypes = [P, P, I32, I32, P, P, I64, I32, P, P, P]
     L.pc_eval_affinity.argtypes = [P, P, I32, I32, P, I32, P, I32, P, I64, P, P, P, P]
     L.pc_score_preferred.argtypes = [P, P, I32, I32, P, P, I32, P, I32, P, P, I64, P, P, P, P]
     L.pc_update_nodes.argtypes = [P, P, I32, I32, P, P, I64, I32, P, I32, P, P, P]
@@ -109,7 +110,7 @@ EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_e
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
             "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths",
             "pc_update_nodes", "pc_eval_selectors_count", "pc_probe_selectors", "pc_report_counts",
-            "pc_score_preferred", "pc_trace_flows_delta", "pc_trace_keep_tables")
+            "pc_score_preferred", "pc_trace_flows_delta", "pc_trace_keep_tables", "pc_eval_selectors_noalloc")
 
 
 class Context:
@@ -235,6 +236,22 @@ def pc_eval_selectors(labels, pred_off, preds, n_preds=None, feasible=None, popc
     ctx.check(lib().pc_eval_selectors(ctx.handle, _ptr(labels) if labels.numel() else None, N, L, _ptr(pred_off),
                                       _ptr(preds) if preds.numel() else None, n_preds, I,
                                       _ptr(feasible) if feasible.numel() else None, _ptr(popcnt), _stream(stream)))
+    return feasible, popcnt
+
+
+def pc_eval_selectors_noalloc(labels, pred_off, preds, feasible, popcnt, n_preds=None, ctx=None, stream=None):
+    """pc_eval_selectors into caller-provided feasible [I, ceil(N/64)] and
+    popcnt [I] tensors, with no device allocation by the library (its scratch
+    is a fixed per-device array of PC_NOALLOC_SCRATCH_BYTES; calls that
+    overlap on one device race)."""
+    ctx = ctx or context()
+    N, L = (int(labels.shape[0]), int(labels.shape[1])) if labels.dim() == 2 else (0, 0)
+    I = int(pred_off.shape[0]) - 1
+    n_preds = int(preds.shape[0]) if n_preds is None else int(n_preds)
+    ctx.check(lib().pc_eval_selectors_noalloc(ctx.handle, _ptr(labels) if labels.numel() else None, N, L,
+                                              _ptr(pred_off), _ptr(preds) if preds.numel() else None, n_preds, I,
+                                              _ptr(feasible) if feasible.numel() else None, _ptr(popcnt),
+                                              _stream(stream)))
     return feasible, popcnt
 
 

@@ -176,6 +176,11 @@ int pc_create(pc_ctx **out, int device)
         pc_destroy(ctx);
         return PC_EDEVICE;
     }
+    if (pc_noalloc_setup(ctx) != PC_OK) {  // this device's address of the fixed scratch, once per device
+        (void)hipGetLastError();
+        pc_destroy(ctx);
+        return PC_EDEVICE;
+    }
     *out = ctx;
     return PC_OK;
 }
@@ -242,6 +247,26 @@ int pc_eval_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, 
     PC_HIP(ctx, hipSetDevice(ctx->device));
     return run_selectors(ctx, labels, N, L, pred_off, preds, n_preds, I, feasible, popcnt,
                          static_cast<hipStream_t>(stream));
+}
+
+int pc_eval_selectors_noalloc(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                              const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
+                              void *stream)
+{
+    if (!ctx) return PC_EINVAL;
+    ctx->msg[0] = 0;
+    PC_REQUIRE(N >= 0 && I >= 0 && n_preds >= 0, "pc_eval_selectors_noalloc: negative size (N=%d I=%d n_preds=%lld)",
+               N, I, (long long)n_preds);
+    PC_REQUIRE(L >= 0 && L <= 65535, "pc_eval_selectors_noalloc: L=%d out of [0, 65535]", L);
+    PC_REQUIRE(L > 0 || n_preds == 0, "pc_eval_selectors_noalloc: L=0 with predicates");
+    PC_REQUIRE(I == 0 || (pred_off && popcnt), "pc_eval_selectors_noalloc: null pred_off/popcnt");
+    PC_REQUIRE(n_preds == 0 || preds, "pc_eval_selectors_noalloc: null preds");
+    PC_REQUIRE(N == 0 || L == 0 || labels, "pc_eval_selectors_noalloc: null labels");
+    PC_REQUIRE(I == 0 || N == 0 || feasible, "pc_eval_selectors_noalloc: null feasible");
+    if (I == 0) return PC_OK;
+    PC_HIP(ctx, hipSetDevice(ctx->device));
+    return run_selectors_noalloc(ctx, labels, N, L, pred_off, preds, n_preds, I, feasible, popcnt,
+                                 static_cast<hipStream_t>(stream));
 }
 
 int pc_eval_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off,

@@ -104,9 +104,19 @@ void launch_scan_i32(const int32_t *counts, int32_t n, int32_t *out, int32_t *ou
                      hipStream_t s);
 
 // ---------------------------------------------------------------- modules
+// fixed != nullptr: carve the scratch from fixed[0 .. fixed_cap) instead of
+// the context's arena (PC_EINVAL, before any device work, if it does not fit)
 int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                   const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
-                  hipStream_t stream);
+                  hipStream_t stream, char *fixed = nullptr, size_t fixed_cap = 0);
+
+// The allocation-free selector entry point's fixed scratch: pc_noalloc_setup
+// (from pc_create, with ctx->device current) looks up this device's address
+// of the array once; run_selectors_noalloc runs pc_eval_selectors on it.
+int pc_noalloc_setup(pc_ctx *ctx);
+int run_selectors_noalloc(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                          const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
+                          hipStream_t stream);
 
 int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *row_off, int32_t I,
                  const int32_t *term_off, int32_t n_terms, const pc_pred *preds, int64_t n_preds, uint64_t *feasible,

@@ -28,6 +28,7 @@
 //                  bytes in LDS and summed once per 64 rows; a last pass
 //                  sums the tiles.
 #include <algorithm>
+#include <mutex>
 
 #include "pc_internal.h"
 
@@ -1446,7 +1447,7 @@ int launch_eval(pc_ctx *ctx, const uint32_t *rec, const uint32_t *prog, const in
 
 int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
                   const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
-                  hipStream_t stream)
+                  hipStream_t stream, char *fixed, size_t fixed_cap)
 {
     const EvalGeom geo = eval_geom(N);
     const int64_t W = geo.W, Wp = geo.Wp, ntiles = geo.ntiles;
@@ -1469,10 +1470,21 @@ int run_selectors(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     };
     Carver dry{nullptr, 0};
     carve(dry);
-    int rc = pc_ensure_arena(ctx, dry.off);
-    if (rc) return rc;
-    Carver real{ctx->arena, 0};
+    char *base = fixed;
+    if (fixed != nullptr) {
+        if (dry.off > fixed_cap)
+            return pc_set_error(ctx, PC_EINVAL,
+                                "pc_eval_selectors_noalloc: needs %zu bytes of scratch, above its maximum of %zu "
+                                "(N=%d L=%d I=%d n_preds=%lld)",
+                                dry.off, fixed_cap, N, L, I, static_cast<long long>(n_preds));
+    } else {
+        int rc = pc_ensure_arena(ctx, dry.off);
+        if (rc) return rc;
+        base = ctx->arena;
+    }
+    Carver real{base, 0};
     carve(real);
+    int rc = PC_OK;
 
     if (W == 0) launch_fill_u32(popcnt, static_cast<size_t>(I), 0, stream);
     rc = build_planes(ctx, labels, N, L, W, Wp, pmax, present, wbase, planes, d_P, stream);
@@ -1643,4 +1655,47 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
                                 part_key, part_cnt, I, static_cast<int32_t>(W > 0 ? ntiles : 0), best, score, count));
     PC_LAUNCH_CHECK(ctx);
     return PC_OK;
+}
+
+// ---------------------------------------------------------------- fixed scratch
+// The allocation-free selector entry point carves its scratch from this
+// array instead of the context's arena.  Each device holds its own copy (the
+// code object's memory, from the first use on that device until the process
+// ends).  In host code the name stands for no device address: only the
+// pointer hipGetSymbolAddress returns for the current device is used.  A
+// 64 KiB guard band follows the usable PC_NOALLOC_SCRATCH_BYTES.
+static __device__ __align__(256) unsigned char scratch[PC_NOALLOC_SCRATCH_BYTES + 65536];
+
+namespace {
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+char *g_scratch_ptr[kMaxDevices];  // this device's address of `scratch`, once looked up
+}  // namespace
+
+int pc_noalloc_setup(pc_ctx *ctx)
+{
+    if (ctx->device < 0 || ctx->device >= kMaxDevices)
+        return pc_set_error(ctx, PC_EDEVICE, "device %d beyond the %d devices with fixed scratch", ctx->device,
+                            kMaxDevices);
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[ctx->device] != nullptr) return PC_OK;
+    void *p = nullptr;
+    PC_HIP(ctx, hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+    if (p == nullptr) return pc_set_error(ctx, PC_EDEVICE, "no device address for the fixed scratch");
+    g_scratch_ptr[ctx->device] = static_cast<char *>(p);
+    return PC_OK;
+}
+
+int run_selectors_noalloc(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const int32_t *pred_off,
+                          const pc_pred *preds, int64_t n_preds, int32_t I, uint64_t *feasible, uint32_t *popcnt,
+                          hipStream_t stream)
+{
+    char *p = nullptr;
+    {
+        std::lock_guard<std::mutex> lock(g_scratch_mu);
+        if (ctx->device >= 0 && ctx->device < kMaxDevices) p = g_scratch_ptr[ctx->device];
+    }
+    if (p == nullptr) return pc_set_error(ctx, PC_EDEVICE, "pc_eval_selectors_noalloc: fixed scratch not set up");
+    return run_selectors(ctx, labels, N, L, pred_off, preds, n_preds, I, feasible, popcnt, stream, p,
+                         PC_NOALLOC_SCRATCH_BYTES);
 }
