@@ -84,7 +84,12 @@ def parse():
     ap.add_argument("--gpus", type=int, default=1)
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
-    ap.add_argument("--workload", default="cfg5", choices=["cfg5", "small"])
+    ap.add_argument("--workload", default="cfg5", choices=["cfg5", "small", "cfg2", "cfg3", "cfg4"],
+                    help="cfg5 (default): the combined step; cfg2 / cfg3 / cfg4: one stage on its own "
+                         "configuration (selectors / flow tracing / masked reachability), one JSON line each")
+    ap.add_argument("--variant", default="rpath", choices=["rpath", "prefix"],
+                    help="cfg3 rule tables: compiled per-flow rules with i.i.d. care bits (rpath) or "
+                         "destination-prefix routing tables with ports wildcarded (prefix)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0,
                     help="target oracle time of the CPU baseline's sample (10-30 s keeps the run within minutes)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
@@ -249,7 +254,8 @@ WALK_MAX = 8192  # the library's default switch-over to per-trace walks (PC_TRAC
 def trace_levels(wl, pc, ctx, D, full):
     """The hop levels the bucketed match kernel runs, with the switches each
     touches, from the library's own walk records (the first 8 switches of
-    every walk).  The library buckets level 0 when more than WALK_MAX traces
+    every walk; for later levels, a run with TTL l stops every trace that is
+    still going at its level-l switch).  The library buckets level 0 when more than WALK_MAX traces
     start, and level l >= 1 when more than WALK_MAX traces entered level
     l - 1; later levels are walked per trace.  Returns the per-level
     (lookups, touched switches, rules of those switches) of the bucketed
@@ -268,8 +274,6 @@ def trace_levels(wl, pc, ctx, D, full):
             bucketed.append(lv)
         else:
             break
-    if bucketed and bucketed[-1] >= 8:
-        raise SystemExit("bench: more than 8 bucketed levels; walk records cannot name their switches")
     out = torch.empty((T, 12), dtype=torch.uint8, device="cuda:0")
     vs = torch.empty(T, dtype=torch.int64, device="cuda:0")
     wk = torch.empty((T, 8), dtype=torch.int32, device="cuda:0")
@@ -278,7 +282,12 @@ def trace_levels(wl, pc, ctx, D, full):
     walk = wk.cpu().numpy()
     levels = []
     for lv in bucketed:
-        sw = walk[started & (hops >= lv), lv]
+        if lv < 8:
+            sw = walk[started & (hops >= lv), lv]
+        else:  # past the walk records: a run with TTL lv stops every trace still going at its level-lv switch
+            pc.pc_trace_flows(S, D["port_off"], D["port_peer"], D["jur"], D["rule_off"], D["rules"], D["hdr"],
+                              D["ingress"], lv, out=out, ctx=ctx)
+            sw = pc.records(out, pc.TRACE_OUT_DT)["last_switch"][started & (hops >= lv)]
         u = np.unique(sw)
         levels.append((live[lv], int(u.shape[0]), int(R[u].sum())))
     walked = int(sum(live[len(bucketed):]))
@@ -859,6 +868,202 @@ def cpu_baseline_paths(wl, gpu_ms, target_s):
                       f"estimated at {est:.1f} s against {gpu_ms:.2f} ms on the GPU"}
 
 
+def oracle_threads():
+    threads = len(os.sched_getaffinity(0))
+    env_cap = os.environ.get("OMP_NUM_THREADS")
+    if env_cap and env_cap.isdigit():
+        threads = min(threads, int(env_cap))
+    return threads
+
+
+def timed_steps(args, ctx, step):
+    """W warm-up steps, then K steps timed with the per-kernel profiler on;
+    returns (seconds, {kernel: (launches, ms)})."""
+    import torch
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    ctx.data_errors(clear=True)
+    ctx.profile(True)
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
+    t1 = time.perf_counter()
+    prof = ctx.profile_read()
+    ctx.profile(False)
+    return t1 - t0, prof
+
+
+def single_line(args, desc, value, unit, elapsed, config, roofline, extra):
+    line = {"metric": "flow hops traced/sec + selector evals/sec on 1 MI355X; % of peak HBM GB/s",
+            "value": value, "unit": unit, "n_gpus": 1, "steps": args.steps, "warmup": args.warmup,
+            "ms_per_step": 1e3 * elapsed / args.steps, "higher_is_better": True, "scaling": "weak",
+            "vs_baseline": None, "dtype": "u64 bitsets / int32 (integer work, no floating point)",
+            "data": "synthetic (seeded generators; no dataset)",
+            "config": dict({"workload": desc, "parallelism": "single GPU"}, **config), "roofline": roofline}
+    line.update(extra)
+    return line
+
+
+def per_kernel_table(prof, steps):
+    return {name: {"launches_per_step": n / steps, "ms_per_step": ms / steps}
+            for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])}
+
+
+def bench_cfg2(args, pc, ctx):
+    """Selector evaluation on its own: 100,000 nodes x 64 labels, 16,384 rows."""
+    import synth
+    import torch
+    wl = synth.cfg2()
+    desc = ("selector evaluation, seed 1: 100,000 nodes x 64 labels (cardinality from {2,4,16,64}); 16,384 rows "
+            "of 1-8 In / NotIn / Exists predicates")
+    D = {k: pc.to_device(wl[k], "cuda:0") for k in ("labels", "pred_off", "preds")}
+    N, L, I = wl["N"], wl["L"], wl["I_rows"]
+    W = (N + 63) // 64
+    feas = torch.empty((I, W), dtype=torch.int64, device="cuda:0")
+    pop = torch.empty(I, dtype=torch.int32, device="cuda:0")
+    step = lambda: pc.pc_eval_selectors(D["labels"], D["pred_off"], D["preds"], feasible=feas, popcnt=pop,  # noqa
+                                        ctx=ctx)
+    elapsed, prof = timed_steps(args, ctx, step)
+    n, ms = prof["k_sel_eval"]
+    avg = ms / n
+    alg = I * W * 8 + I * 4 + wl["n_preds"] * 40 + N * L
+    gbs = alg / (avg * 1e-3) / 1e9
+    pairs = I * N
+    extra = {"per_kernel": per_kernel_table(prof, args.steps),
+             "kernel_rate_evals_per_s": pairs / (avg * 1e-3),
+             "data_error_flags": ctx.data_errors(clear=True)}
+    roof = {"kernel": "k_sel_eval", "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gbs / HBM_PEAK_GBS, "traffic": None, "alg_bytes_per_launch": alg, "avg_launch_ms": avg,
+            "floor_us_at_peak": alg / (HBM_PEAK_GBS * 1e9) * 1e6}
+    if not args.no_cpu_baseline:
+        import oracle
+        th = oracle_threads()
+        stride = 16
+        rows = np.arange(0, I, stride, dtype=np.int32)
+        t0 = time.perf_counter()
+        fo, po, _ = oracle.selectors(wl["labels"], wl["pred_off"], wl["preds"], rows=rows, nthreads=th)
+        t = (time.perf_counter() - t0) * stride
+        t1s0 = time.perf_counter()
+        oracle.selectors(wl["labels"], wl["pred_off"], wl["preds"], rows=rows[::16], nthreads=1)
+        t1 = (time.perf_counter() - t1s0) * stride * 16
+        fg = feas.cpu().numpy().view(np.uint64)[rows]
+        pg = pop.cpu().numpy().view(np.uint32)[rows]
+        extra["cpu_baseline"] = {"value": pairs / t, "unit": "selector evals/s (whole-job estimate)", "cores": th,
+                                 "kind": "oracle", "cpu_model": cpu_model(),
+                                 "sample": f"every {stride}th row ({rows.shape[0]} of {I}) in {t / stride:.2f} s",
+                                 "one_thread": {"value": pairs / t1, "cores": 1,
+                                                "sample": f"every {stride * 16}th row"},
+                                 "parity": "bit-exact" if np.array_equal(fg, fo) and np.array_equal(pg, po)
+                                 else "MISMATCH", "parity_scope": "the sampled rows"}
+    return single_line(args, desc, pairs * args.steps / elapsed, "selector evals/s ((row,node) pairs per second)",
+                       elapsed, {"rows": I, "nodes": N, "labels": L}, roof, extra)
+
+
+def bench_cfg3(args, pc, ctx):
+    """Flow tracing on its own: fat-tree k=32, 4,096 rules per switch, 4.19 M traces."""
+    import synth
+    import torch
+    wl = synth.cfg3(variant=args.variant)
+    tables = ("per-flow compiled rules with 30% wildcard bits" if args.variant == "rpath" else
+              "destination-prefix routing tables (16-32 bit prefixes; ports, source, protocol wildcarded)")
+    desc = (f"flow tracing, seed 2: fat-tree k=32 (1,280 switches), 4,096 rules per switch ({tables}), "
+            f"4,194,304 headers at edge switches, TTL 32")
+    D = {k: pc.to_device(wl[k], "cuda:0") for k in ("port_off", "port_peer", "jur", "rule_off", "rules", "hdr",
+                                                     "ingress")}
+    T = wl["T"]
+    out = torch.empty((T, 12), dtype=torch.uint8, device="cuda:0")
+    step = lambda: pc.pc_trace_flows(wl["S"], D["port_off"], D["port_peer"], D["jur"], D["rule_off"],  # noqa
+                                     D["rules"], D["hdr"], D["ingress"], wl["ttl"], out=out, ctx=ctx)
+    elapsed, prof = timed_steps(args, ctx, step)
+    tr = pc.records(out, pc.TRACE_OUT_DT)
+    ing = wl["ingress"]
+    started = (ing >= 0) & (ing < wl["S"])
+    lookups = int((tr["hops"][started].astype(np.int64) + 1).sum())
+    roof = trace_roofline(wl, pc, ctx, D, tr, prof, args.steps, f"cfg3-{args.variant}")
+    prep_ms = sum(ms for k, (n, ms) in prof.items() if k in ("k_tr_prep", "k_tr_choose", "k_tr_switch_info",
+                                                             "k_tr_port_check")) / args.steps
+    extra = {"per_kernel": per_kernel_table(prof, args.steps), "flow_lookups_per_step": lookups,
+             "mean_lookups_per_trace": lookups / max(int(started.sum()), 1),
+             "terminal_states": {k: int((tr["state"] == v).sum()) for k, v in
+                                 (("egress", 0), ("drop", 1), ("miss", 2), ("ttl", 3))},
+             "hop_loop_lookups_per_s": lookups / (roof["hop_loop_ms"] * 1e-3) if roof["hop_loop_ms"] else None,
+             "prep_ms_per_step": prep_ms, "data_error_flags": ctx.data_errors(clear=True)}
+    if not args.no_cpu_baseline:
+        import oracle
+        th = oracle_threads()
+        stride = 64
+        idx = np.arange(0, T, stride)
+        t0 = time.perf_counter()
+        to, _ = oracle.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"],
+                             wl["hdr"], wl["ingress"], wl["ttl"], idx=idx, nthreads=th)
+        t = (time.perf_counter() - t0) * stride
+        t1s0 = time.perf_counter()
+        oracle.trace(wl["S"], wl["port_off"], wl["port_peer"], wl["jur"], wl["rule_off"], wl["rules"], wl["hdr"],
+                     wl["ingress"], wl["ttl"], idx=idx[::16], nthreads=1)
+        t1 = (time.perf_counter() - t1s0) * stride * 16
+        same = all(np.array_equal(tr[f][idx], to[f]) for f in ("jmask", "last_switch", "last_port", "hops", "state"))
+        extra["cpu_baseline"] = {"value": lookups / t, "unit": "flow lookups/s (whole-job estimate)", "cores": th,
+                                 "kind": "oracle", "cpu_model": cpu_model(),
+                                 "sample": f"every {stride}th trace ({idx.shape[0]} of {T}) in {t / stride:.2f} s",
+                                 "one_thread": {"value": lookups / t1, "cores": 1,
+                                                "sample": f"every {stride * 16}th trace"},
+                                 "parity": "bit-exact" if same else "MISMATCH", "parity_scope": "the sampled traces"}
+    return single_line(args, desc, lookups * args.steps / elapsed,
+                       "flow lookups/s (hops + 1 per trace, per second of whole-call time incl. table preparation)",
+                       elapsed, {"switches": wl["S"], "rules": wl["n_rules"], "traces": T, "ttl": wl["ttl"],
+                                 "variant": args.variant}, roof, extra)
+
+
+def bench_cfg4(args, pc, ctx):
+    """Masked reachability on its own: 1,000,000-vertex RGG, 256 full-row queries."""
+    import synth
+    import torch
+    wl = synth.cfg4()
+    desc = ("masked reachability, seed 3: random geometric graph of 1,000,000 switches (mean degree 4), "
+            "16-region Voronoi map, 256 queries of 1-8 allowed regions, full distance rows")
+    D = {k: pc.to_device(wl[k], "cuda:0") for k in ("adj_off", "adj", "region", "src", "allowed")}
+    V, Q = wl["V"], wl["Q"]
+    dist = torch.empty((Q, V), dtype=torch.int32, device="cuda:0")
+    step = lambda: pc.pc_masked_reach(V, D["adj_off"], D["adj"], D["region"], D["src"], D["allowed"],  # noqa
+                                      dist=dist, ctx=ctx)
+    elapsed, prof = timed_steps(args, ctx, step)
+    per_k = per_kernel_table(prof, args.steps)
+    fill = per_k.get("k_fill_u32", {}).get("ms_per_step")
+    ms = sum(v["ms_per_step"] for v in per_k.values())
+    store = Q * V * 4
+    alg = store + (V + 1) * 4 + int(wl["adj"].shape[0]) * 4 + V
+    gbs = alg / (ms * 1e-3) / 1e9
+    roof = {"kernel": "+".join(per_k), "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
+            "frac": gbs / HBM_PEAK_GBS, "traffic": None, "alg_bytes_per_launch": alg, "avg_launch_ms": ms,
+            "floor_us_at_peak": alg / (HBM_PEAK_GBS * 1e9) * 1e6}
+    extra = {"per_kernel": per_k, "fill_ms": fill,
+             "fill_gbs": store / (fill * 1e-3) / 1e9 if fill else None,
+             "data_error_flags": ctx.data_errors(clear=True)}
+    d = dist.cpu().numpy()
+    extra["reached_per_query_mean"] = float((d >= 0).sum(1).mean())
+    if not args.no_cpu_baseline:
+        import oracle
+        th = oracle_threads()
+        t0 = time.perf_counter()
+        do, _ = oracle.reach(V, wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"], nthreads=th)
+        t = time.perf_counter() - t0
+        t1s0 = time.perf_counter()
+        qs = np.arange(0, Q, 16)
+        oracle.reach(V, wl["adj_off"], wl["adj"], wl["region"], wl["src"], wl["allowed"], qidx=qs, nthreads=1)
+        t1 = (time.perf_counter() - t1s0) * 16
+        extra["cpu_baseline"] = {"value": Q * V / t, "unit": "(query, vertex) distances/s", "cores": th,
+                                 "kind": "oracle", "cpu_model": cpu_model(),
+                                 "sample": f"all {Q} queries in {t:.2f} s",
+                                 "one_thread": {"value": Q * V / t1, "cores": 1, "sample": "every 16th query"},
+                                 "parity": "bit-exact" if np.array_equal(d, do) else "MISMATCH",
+                                 "parity_scope": "every distance row"}
+    return single_line(args, desc, Q * V * args.steps / elapsed, "(query, vertex) distances/s", elapsed,
+                       {"vertices": V, "queries": Q}, roof, extra)
+
+
 def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -873,6 +1078,13 @@ def main():
 
     import torch
     import paper_2602_16100_amd as pc
+
+    if args.workload in ("cfg2", "cfg3", "cfg4"):
+        torch.cuda.set_device(0)
+        ctx = pc.context(0)
+        fn = {"cfg2": bench_cfg2, "cfg3": bench_cfg3, "cfg4": bench_cfg4}[args.workload]
+        print(json.dumps(fn(args, pc, ctx)), flush=True)
+        return
 
     wl, desc = make_workload(args.workload)
     dev = "cuda:0"

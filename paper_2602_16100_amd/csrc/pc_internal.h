@@ -132,6 +132,7 @@ struct TracePrep {
     const uint32_t *filt;
     const int32_t *gcount;
     const int32_t *gofs;
+    const uint32_t *cpos;  // per switch: the key nibbles its chunk sets filter on (5 bits each)
 };
 
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,

@@ -116,6 +116,69 @@ __global__ void k_rc_validate(int32_t V, const int32_t *__restrict__ adj_off, co
     if (errs) atomicOr(d_err, errs);
 }
 
+// Append v to an LDS list when `add`, one counter update per wavefront
+// (every active lane of the wavefront calls this together).
+__device__ __forceinline__ void wave_append(bool add, uint16_t v, int32_t *count, uint16_t *list)
+{
+    const uint64_t b = __ballot(add);
+    if (b == 0) return;
+    const int leader = __builtin_ctzll(b);
+    const int lane = threadIdx.x & 63;
+    int32_t base = 0;
+    if (lane == leader) base = atomicAdd(count, static_cast<int32_t>(__popcll(b)));
+    base = __shfl(base, leader, 64);
+    if (add) {
+        const uint32_t below = __builtin_amdgcn_mbcnt_hi(static_cast<uint32_t>(b >> 32),
+                                                         __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(b), 0u));
+        list[base + static_cast<int32_t>(below)] = v;
+    }
+}
+
+// Queries ordered by source for the bitset search: a counting sort (the
+// order among queries of one source is arbitrary; every result is per
+// query).  A workgroup's 64 queries then share few sources, so their
+// frontiers overlap and one push along an edge serves many of them.
+// Sources outside [0, V) go to bucket V.  Counting: each workgroup ranks its
+// queries within their buckets in LDS and reserves its share of every
+// bucket it meets with one global atomic (a few thousand instead of one
+// per query on the same few counters); pos[q] = the query's place within
+// its bucket.
+constexpr int kSortThreads = 1024;
+constexpr int kSortPer = 4096;  // queries per counting workgroup
+
+__global__ __launch_bounds__(kSortThreads) void k_rc_src_count(int32_t Q, const int32_t *__restrict__ src, int32_t V,
+                                                               int32_t *__restrict__ cnt, int32_t *__restrict__ pos)
+{
+    extern __shared__ int32_t loc[];  // [V + 1] per-bucket counts, then the workgroup's bases
+    for (int32_t b = threadIdx.x; b <= V; b += kSortThreads) loc[b] = 0;
+    __syncthreads();
+    const int32_t q0 = blockIdx.x * kSortPer;
+    const int32_t q1 = min(Q, q0 + kSortPer);
+    for (int32_t q = q0 + threadIdx.x; q < q1; q += kSortThreads) {
+        const int32_t s = src[q];
+        pos[q] = atomicAdd(loc + ((s >= 0 && s < V) ? s : V), 1);
+    }
+    __syncthreads();
+    for (int32_t b = threadIdx.x; b <= V; b += kSortThreads) {
+        const int32_t n = loc[b];
+        loc[b] = n ? atomicAdd(cnt + b, n) : 0;
+    }
+    __syncthreads();
+    for (int32_t q = q0 + threadIdx.x; q < q1; q += kSortThreads) {
+        const int32_t s = src[q];
+        pos[q] += loc[(s >= 0 && s < V) ? s : V];
+    }
+}
+
+__global__ void k_rc_src_place(int32_t Q, const int32_t *__restrict__ src, int32_t V, const int32_t *__restrict__ off,
+                               const int32_t *__restrict__ pos, int32_t *__restrict__ perm)
+{
+    for (int32_t q = blockIdx.x * blockDim.x + threadIdx.x; q < Q; q += gridDim.x * blockDim.x) {
+        const int32_t s = src[q];
+        perm[off[(s >= 0 && s < V) ? s : V] + pos[q]] = q;
+    }
+}
+
 // 64 queries per workgroup; dist is [Q][V] (target == nullptr) or [Q].
 // Each level pushes the frontier along its edges: the frontier vertices are
 // kept as a list in LDS and GS lanes share one vertex's adjacency, so the
@@ -131,7 +194,8 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                                                               const int32_t *__restrict__ target,
                                                               int32_t *__restrict__ dist,
                                                               const int32_t *__restrict__ forbid, int32_t Kf,
-                                                              int32_t qdiv, const int32_t *__restrict__ sym)
+                                                              int32_t qdiv, const int32_t *__restrict__ sym,
+                                                              const int32_t *__restrict__ perm)
 {
     extern __shared__ uint64_t lds[];
     uint64_t *vis = lds;
@@ -148,9 +212,12 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     // queries still searching (target mode): resolved queries' frontier
     // bits are dropped, so their searches stop spreading
     __shared__ unsigned long long live;
+    // query of bit k: qid[k] (queries taken in perm order when given)
+    __shared__ int32_t qid[64];
     const int tid = threadIdx.x, lane = tid & 63;
     const int32_t q0 = blockIdx.x * 64;
     const int32_t nq = min(64, Q - q0);
+    if (tid < 64) qid[lane] = lane < nq ? (perm ? perm[q0 + lane] : q0 + lane) : 0;
     for (int32_t v = tid; v < V; v += kBitsetThreads) {
         vis[v] = 0;
         fr[v] = 0;
@@ -158,7 +225,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         reg[v] = region[v];
     }
     if (tid < 64) {
-        const uint32_t A = lane < nq ? allowed[(q0 + lane) / qdiv] : 0u;
+        const uint32_t A = lane < nq ? allowed[qid[lane] / qdiv] : 0u;
         for (int r = 0; r < 32; ++r) {
             const uint64_t m = __ballot((A >> r) & 1u);
             if (lane == 0) rmask[r] = m;
@@ -169,7 +236,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     // forbidden vertices start out visited, so they are never entered
     if (Kf > 0) {
         if (tid < 64 && lane < nq) {
-            const int32_t *fl = forbid + static_cast<int64_t>((q0 + lane) / qdiv) * Kf;
+            const int32_t *fl = forbid + static_cast<int64_t>(qid[lane] / qdiv) * Kf;
             for (int32_t k = 0; k < Kf; ++k) {
                 const int32_t f = fl[k];
                 if (f >= 0 && f < V) atomicOr(reinterpret_cast<unsigned long long *>(&vis[f]), 1ull << lane);
@@ -181,7 +248,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     int32_t res = -1, tgt = -1;
     bool done = true;
     if (tid < 64 && lane < nq) {
-        const int32_t q = q0 + lane;
+        const int32_t q = qid[lane];
         const int32_t s = src[q];
         const bool s_ok = s >= 0 && s < V && allowed_v(reg, allowed[q / qdiv], s) && !((vis[s] >> lane) & 1);
         if (target) {
@@ -199,7 +266,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     }
     __syncthreads();
     for (int32_t v = tid; v < V; v += kBitsetThreads)
-        if (fr[v]) flist[atomicAdd(&nfr[0], 1)] = static_cast<uint16_t>(v);
+        wave_append(fr[v] != 0, static_cast<uint16_t>(v), &nfr[0], flist);
     if (tid < 64) {
         if (!done && ((vis[tgt] >> lane) & 1)) {
             res = 0;
@@ -214,7 +281,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         bool t_allowed = false;
         if (target && !done && *sym == 1) {
             const int64_t b64 = adj_off[tgt], e64 = adj_off[tgt + 1];
-            t_allowed = allowed_v(reg, allowed[(q0 + lane) / qdiv], tgt);
+            t_allowed = allowed_v(reg, allowed[qid[lane] / qdiv], tgt);
             if (t_allowed && pc_range_ok(b64, e64, n_adj)) {
                 b = static_cast<int32_t>(b64);
                 deg = static_cast<int32_t>(e64 - b64);
@@ -284,12 +351,12 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                     while (m) {
                         const int q = __builtin_ctzll(m);
                         m &= m - 1;
-                        dist[static_cast<int64_t>(q0 + q) * V + v] = d;
+                        dist[static_cast<int64_t>(qid[q]) * V + v] = d;
                     }
                 }
             }
             fr[v] = n;
-            if (n) flist[atomicAdd(&nfr[cur ^ 1], 1)] = static_cast<uint16_t>(v);
+            wave_append(n != 0, static_cast<uint16_t>(v), &nfr[cur ^ 1], flist);
         }
         if (tid == 0) found = 0;
         __syncthreads();
@@ -331,7 +398,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
         // only after the next level's second barrier
         if (nfr[cur ^ 1] == 0 || flag_done) break;
     }
-    if (target && tid < 64 && lane < nq) dist[q0 + lane] = res;
+    if (target && tid < 64 && lane < nq) dist[qid[lane]] = res;
 }
 
 // One workgroup per query (grid-stride over queries).
@@ -452,6 +519,33 @@ int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int6
         if (!sym && target) sym = symcheck(ctx, V, adj_off, adj, n_adj, stream);
         if (!sym) sym = ctx->d_small + 5;  // full rows: no look-ahead reads it
         PC_LAUNCH_CHECK(ctx);
+        // more than one workgroup: order the queries by source
+        int32_t *perm = nullptr;
+        if (Q > 64) {
+            int32_t *cnt, *off, *pos;
+            auto carve = [&](Carver &c) {
+                cnt = c.take<int32_t>(static_cast<size_t>(V) + 2);
+                off = c.take<int32_t>(static_cast<size_t>(V) + 2);
+                pos = c.take<int32_t>(static_cast<size_t>(Q));
+                perm = c.take<int32_t>(static_cast<size_t>(Q));
+            };
+            Carver dry{nullptr, 0};
+            carve(dry);
+            int rc = pc_ensure_arena(ctx, dry.off);
+            if (rc) return rc;
+            Carver real{ctx->arena, 0};
+            carve(real);
+            launch_fill_u32(reinterpret_cast<uint32_t *>(cnt), static_cast<size_t>(V) + 1, 0, stream);
+            PC_TIMED(ctx, "k_rc_src_count", stream,
+                     hipLaunchKernelGGL(k_rc_src_count, dim3(static_cast<unsigned>((Q + kSortPer - 1) / kSortPer)),
+                                        dim3(kSortThreads), (static_cast<size_t>(V) + 1) * sizeof(int32_t), stream, Q,
+                                        src, V, cnt, pos));
+            launch_scan_i32(cnt, V + 1, off, nullptr, nullptr, stream);
+            PC_TIMED(ctx, "k_rc_src_place", stream,
+                     hipLaunchKernelGGL(k_rc_src_place, dim3(static_cast<unsigned>(std::min<int64_t>((Q + 255) / 256, 4096))),
+                                        dim3(256), 0, stream, Q, src, V, off, pos, perm));
+            PC_LAUNCH_CHECK(ctx);
+        }
         // lanes per vertex: a power of two near a third of the mean degree
         const int64_t avg = n_adj / V;
         const int gs = avg <= 12 ? 4 : avg <= 24 ? 8 : avg <= 48 ? 16 : 32;
@@ -461,7 +555,7 @@ int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int6
                                             hipFuncAttributeMaxDynamicSharedMemorySize, static_cast<int>(lds)));
             PC_TIMED(ctx, "k_rc_bitset", stream,
                      hipLaunchKernelGGL(kern, grid_b, dim3(kBitsetThreads), lds, stream, V, adj_off, adj, n_adj,
-                                        region, Q, src, allowed, target, dist, forbid, Kf, qdiv, sym));
+                                        region, Q, src, allowed, target, dist, forbid, Kf, qdiv, sym, perm));
             PC_LAUNCH_CHECK(ctx);
             return PC_OK;
         };

@@ -38,7 +38,9 @@
 
 namespace {
 
-constexpr int kChunks = 6;                 // 4-bit chunks of w[2] used by the filter (bits 0..23)
+constexpr int kChunks = 6;                 // 4-bit chunks of the key used by the filter (chosen per switch)
+constexpr int kKeyNibbles = 26;            // the 104-bit key: 8 nibbles in each of w0..w2, 2 in w3's low byte
+constexpr int kChooseSample = 512;         // rules per switch sampled to choose its filter chunks
 constexpr int kPlaneWords = kChunks * 16;  // words per 32-rule group
 constexpr int kMatchWaves = 8;
 constexpr int kMatchThreads = kMatchWaves * 64;
@@ -63,6 +65,16 @@ __device__ __forceinline__ uint32_t watch_bits(const int32_t *__restrict__ watch
         if (w[k] == s) m |= 1u << k;
     return m;
 }
+
+// Nibble n (0..25) of a 104-bit key or mask: bits 4(n mod 8) .. +3 of word n / 8.
+__device__ __forceinline__ uint32_t key_nibble(uint32_t w0, uint32_t w1, uint32_t w2, uint32_t w3, uint32_t n)
+{
+    const uint32_t w = n < 8 ? w0 : n < 16 ? w1 : n < 24 ? w2 : w3;
+    return (w >> ((n & 7u) * 4u)) & 15u;
+}
+
+// Filter chunk c of a switch whose chunk positions are packed in cp (5 bits each).
+__device__ __forceinline__ uint32_t chunk_pos(uint32_t cp, int c) { return (cp >> (5 * c)) & 31u; }
 
 // Bit of switch s in a visited-switch summary.
 __device__ __forceinline__ uint64_t sum_bit(int32_t s) { return 1ull << (s & 63); }
@@ -105,6 +117,84 @@ __global__ void k_tr_port_check(int64_t n_ports, const int32_t *__restrict__ por
         bad |= (v < -1 || v >= S);
     }
     if (bad) atomicOr(d_err, PC_DERR_SWITCH);
+}
+
+// Histogram of the headers' nibble values over a strided sample of at most
+// kHeaderSample headers: hh[n][x] = sampled headers whose nibble n is x.
+// hh must be zero on entry.
+constexpr int kHeaderSample = 65536;
+__global__ __launch_bounds__(256) void k_tr_hdr_hist(const pc_key *__restrict__ hdr, int32_t T,
+                                                     uint32_t *__restrict__ hh)
+{
+    __shared__ uint32_t loc[kKeyNibbles * 16];
+    for (int i = threadIdx.x; i < kKeyNibbles * 16; i += 256) loc[i] = 0;
+    __syncthreads();
+    const int64_t stride = T > kHeaderSample ? (static_cast<int64_t>(T) + kHeaderSample - 1) / kHeaderSample : 1;
+    for (int64_t i = blockIdx.x * 256 + threadIdx.x; i * stride < T; i += static_cast<int64_t>(gridDim.x) * 256) {
+        const pc_key h = hdr[i * stride];
+        for (uint32_t n = 0; n < kKeyNibbles; ++n)
+            atomicAdd(&loc[n * 16 + key_nibble(h.w[0], h.w[1], h.w[2], h.w[3], n)], 1u);
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kKeyNibbles * 16; i += 256)
+        if (loc[i]) atomicAdd(hh + i, loc[i]);
+}
+
+// The filter chunks of each switch (one workgroup per switch).  From a
+// sample of at most kChooseSample of its rules (every ceil(R / sample)-th):
+// for each of the key's 26 nibbles and each chunk value x, the number A[x]
+// of sampled rules whose value/mask admit x.  With hh the headers' nibble
+// histogram, score = sum_x (hh[x] + 1) A[x] is proportional to the chance
+// that a header drawn like the traced ones (smoothed towards uniform)
+// passes the nibble's filter against a rule drawn like the switch's.  The
+// kChunks nibbles of smallest score (ties: lower nibble) filter out the
+// most: nibbles the rules wildcard, or where headers and rules agree on a
+// few values, score high.  Any choice gives the same results; it only
+// decides how many rules reach the full 104-bit check.
+__global__ __launch_bounds__(256) void k_tr_choose(int32_t S, const int32_t *__restrict__ rule_off, int64_t n_rules,
+                                                   const pc_rule *__restrict__ rules,
+                                                   const uint32_t *__restrict__ hh, uint32_t *__restrict__ cpos)
+{
+    __shared__ uint32_t hist[kKeyNibbles][256];  // (value & mask, mask) patterns per nibble
+    __shared__ unsigned long long score[kKeyNibbles];
+    const int32_t s = blockIdx.x;
+    if (s >= S) return;
+    for (int i = threadIdx.x; i < kKeyNibbles * 256; i += 256) (&hist[0][0])[i] = 0;
+    if (threadIdx.x < kKeyNibbles) score[threadIdx.x] = 0;
+    __syncthreads();
+    const int64_t rb = rule_off[s], re = rule_off[s + 1];
+    const int64_t R = pc_range_ok(rb, re, n_rules) ? re - rb : 0;
+    const int64_t stride = R > kChooseSample ? (R + kChooseSample - 1) / kChooseSample : 1;
+    for (int64_t i = threadIdx.x; i * stride < R && i < kChooseSample; i += 256) {
+        const pc_rule *r = rules + rb + i * stride;
+        const uint32_t v0 = r->value.w[0], v1 = r->value.w[1], v2 = r->value.w[2], v3 = r->value.w[3];
+        const uint32_t m0 = r->mask.w[0], m1 = r->mask.w[1], m2 = r->mask.w[2], m3 = r->mask.w[3];
+        for (uint32_t n = 0; n < kKeyNibbles; ++n) {
+            const uint32_t m = key_nibble(m0, m1, m2, m3, n);
+            const uint32_t v = key_nibble(v0, v1, v2, v3, n) & m;
+            atomicAdd(&hist[n][m << 4 | v], 1u);
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < kKeyNibbles * 16; i += 256) {
+        const int n = i >> 4;
+        const uint32_t x = i & 15;
+        uint64_t a = 0;  // sampled rules admitting chunk value x: (x & m) == (v & m)
+        for (uint32_t m = 0; m < 16; ++m) a += hist[n][m << 4 | (x & m)];
+        atomicAdd(&score[n], static_cast<unsigned long long>(a * (static_cast<uint64_t>(hh[n * 16 + x]) + 1)));
+    }
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        uint32_t taken = 0, cp = 0;
+        for (int c = 0; c < kChunks; ++c) {
+            int best = -1;
+            for (int n = 0; n < kKeyNibbles; ++n)
+                if (!((taken >> n) & 1u) && (best < 0 || score[n] < score[best])) best = n;
+            taken |= 1u << best;
+            cp |= static_cast<uint32_t>(best) << (5 * c);
+        }
+        cpos[s] = cp;
+    }
 }
 
 // Rows r of a 32-lane half hold 32-bit words x_r; afterwards lane i holds
@@ -163,7 +253,8 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
                                                   const int32_t *__restrict__ gcount,
                                                   const int32_t *__restrict__ gofs, const int32_t *__restrict__ bofs,
                                                   uint32_t *__restrict__ filt, uint32_t *__restrict__ d_err,
-                                                  const uint32_t *__restrict__ only, uint32_t *__restrict__ sw_bad)
+                                                  const uint32_t *__restrict__ only, uint32_t *__restrict__ sw_bad,
+                                                  const uint32_t *__restrict__ cpos)
 {
     __shared__ uint32_t tile[kPlaneWords * kTileStride];
     __shared__ uint16_t admit[256];
@@ -185,19 +276,22 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
     const bool pok = pc_range_ok(port_off[s], port_off[s + 1], n_ports);
     const int64_t np = pok ? port_off[s + 1] - port_off[s] : 0;
     const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const uint32_t cp = cpos[s];
     // issue every round's loads before any use
-    uint32_t v2[kPrepRounds], m2[kPrepRounds], act[kPrepRounds];
+    uint4 vv[kPrepRounds], mm[kPrepRounds];
+    uint32_t act[kPrepRounds];
     bool ok[kPrepRounds];
 #pragma unroll
     for (int k = 0; k < kPrepRounds; ++k) {
         const int32_t gl = 2 * (wave * kPrepRounds + k) + (lane >> 5);
         const int64_t local = static_cast<int64_t>(g0 + gl - (lane >> 5)) * 32 + lane;  // rule index within the switch
         ok[k] = local < R && g0 + gl < G;
-        v2[k] = m2[k] = act[k] = 0;
+        vv[k] = mm[k] = make_uint4(0, 0, 0, 0);
+        act[k] = 0;
         if (ok[k]) {
             const pc_rule *r = rules + rb + local;
-            v2[k] = r->value.w[2];
-            m2[k] = r->mask.w[2];
+            vv[k] = make_uint4(r->value.w[0], r->value.w[1], r->value.w[2], r->value.w[3]);
+            mm[k] = make_uint4(r->mask.w[0], r->mask.w[1], r->mask.w[2], r->mask.w[3]);
             act[k] = r->action;
         }
     }
@@ -223,13 +317,14 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
     bool bad_action = false;
 #pragma unroll
     for (int k = 0; k < kPrepRounds; ++k) {
-        const uint32_t t2 = v2[k] & m2[k];
         uint32_t w[kChunks / 2];
 #pragma unroll
         for (int d = 0; d < kChunks / 2; ++d) {
-            const int c0 = 2 * d, c1 = 2 * d + 1;
-            const uint32_t i0 = ((t2 >> (4 * c0)) & 15u) | (((m2[k] >> (4 * c0)) & 15u) << 4);
-            const uint32_t i1 = ((t2 >> (4 * c1)) & 15u) | (((m2[k] >> (4 * c1)) & 15u) << 4);
+            const uint32_t n0 = chunk_pos(cp, 2 * d), n1 = chunk_pos(cp, 2 * d + 1);
+            const uint32_t ma = key_nibble(mm[k].x, mm[k].y, mm[k].z, mm[k].w, n0);
+            const uint32_t mb = key_nibble(mm[k].x, mm[k].y, mm[k].z, mm[k].w, n1);
+            const uint32_t i0 = (key_nibble(vv[k].x, vv[k].y, vv[k].z, vv[k].w, n0) & ma) | (ma << 4);
+            const uint32_t i1 = (key_nibble(vv[k].x, vv[k].y, vv[k].z, vv[k].w, n1) & mb) | (mb << 4);
             const uint32_t a0 = ok[k] ? admit[i0] : 0u, a1 = ok[k] ? admit[i1] : 0u;
             w[d] = transpose32(a0 | (a1 << 16), keep, rot);
         }
@@ -524,10 +619,10 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     int32_t S, const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules,
     const int32_t *__restrict__ gcount, const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
     const pc_key *__restrict__ hdr, const int32_t *__restrict__ boff, const int32_t *__restrict__ ioff,
-    const int32_t *__restrict__ bucket, Level lv)
+    const int32_t *__restrict__ bucket, const uint32_t *__restrict__ cpos, Level lv)
 {
     __shared__ uint64_t best[kChunk];
-    __shared__ __align__(16) uint32_t cidx[kChunks][kChunk];  // chunk values of each lookup's header word 2
+    __shared__ __align__(16) uint32_t cidx[kChunks][kChunk];  // each lookup's values of the switch's filter chunks
     __shared__ __align__(16) pc_key keys[kChunk];
     __shared__ int32_t tids[kChunk];
     __shared__ uint2 queue[kMatchWaves][kQueue];  // per wavefront: (survivor set, lookup << 6 | lane)
@@ -557,7 +652,19 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     const int64_t rb = rule_off[s];
     const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
     const int32_t nslices = max(1, (G + kSliceGroups - 1) / kSliceGroups);
+    const uint32_t cp = cpos[s];
     uint2 *q = queue[wave];
+    // A table of fewer than kSliceGroups groups fills gws wavefronts; the
+    // workgroup's other wavefronts take further shares of the lookups: wave
+    // = stream * gws + gwi holds groups gwi * 64 .. and filters the lookups
+    // of its stream (contiguous quads).  Waves past the last stream idle.
+    const int32_t gws = G >= kSliceGroups ? kMatchWaves : max(1, (G + 63) / 64);
+    const int32_t streams = kMatchWaves / gws;
+    const int32_t gwi = wave % gws, st = wave / gws;
+    const int32_t nquads = tn4 / 4;
+    const int32_t per_stream = (nquads + streams - 1) / streams;
+    const int32_t jb = st < streams ? min(tn4, 4 * st * per_stream) : tn4;
+    const int32_t je = st < streams ? min(tn4, 4 * (st + 1) * per_stream) : tn4;
     // stage the chunk; pad to a multiple of 4 lookups with copies of the last
     for (int i = threadIdx.x; i < tn4; i += kMatchThreads) {
         int32_t t = bucket[bb + min(i, tn - 1)];
@@ -568,20 +675,20 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         keys[i] = h;
         best[i] = kNoMatch;
 #pragma unroll
-        for (int c = 0; c < kChunks; ++c) cidx[c][i] = (h.w[2] >> (4 * c)) & 15u;
+        for (int c = 0; c < kChunks; ++c) cidx[c][i] = key_nibble(h.w[0], h.w[1], h.w[2], h.w[3], chunk_pos(cp, c));
     }
     __syncthreads();
     // one slice of kSliceGroups groups at a time, one group per lane,
     // its chunk sets held in VGPRs while the chunk's lookups stream past
     for (int32_t sl = 0; sl < nslices; ++sl) {
-        const int32_t g = sl * kSliceGroups + wave * 64 + lane;
-        const int32_t gw = sl * kSliceGroups + wave * 64;  // group of lane 0
+        const int32_t g = sl * kSliceGroups + gwi * 64 + lane;
+        const int32_t gw = sl * kSliceGroups + gwi * 64;  // group of lane 0
         // Filter phase: survivors of the chunk filter are queued (per
         // wavefront) until the queue could overflow.  Verify phase: the
         // queued survivors are checked against their full rules, 64 at a
         // time, with the chunk sets dead.  Then filtering resumes.  A quad
         // of lookups queues at most 256 entries, so every round advances.
-        for (int32_t jr = 0; jr < tn4;) {
+        for (int32_t jr = jb; jr < je;) {
             // an opaque copy of G keeps the 96 load addresses from being
             // hoisted out of the loops (and spilled) as invariants
             int32_t Gr = G;
@@ -593,7 +700,7 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
                 for (int x = 0; x < 16; ++x) F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * Gr + g] : 0u;
             int32_t qn = 0;
             int32_t j0 = jr;
-            for (; j0 < tn4; j0 += 4) {
+            for (; j0 < je; j0 += 4) {
                 uint4 X[kChunks];
 #pragma unroll
                 for (int c = 0; c < kChunks; ++c) X[c] = reinterpret_cast<const uint4 *>(cidx[c])[j0 >> 2];
@@ -692,7 +799,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                                                  const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
                                                  uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
-                                                 int32_t *__restrict__ walk)
+                                                 int32_t *__restrict__ walk, const uint32_t *__restrict__ cpos)
 {
     __shared__ unsigned long long best;
     const int32_t n = *nlive;
@@ -710,11 +817,14 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
             const int32_t G = gcount[s];
             const uint32_t *fs = filt + static_cast<int64_t>(gofs[s]) * kPlaneWords;
             const int64_t rb = rule_off[s];
+            const uint32_t cp = cpos[s];
+            uint32_t x[kChunks];
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) x[c] = key_nibble(h.w[0], h.w[1], h.w[2], h.w[3], chunk_pos(cp, c));
             for (int32_t g = threadIdx.x; g < G; g += blockDim.x) {
                 uint32_t surv = ~0u;
 #pragma unroll
-                for (int c = 0; c < kChunks; ++c)
-                    surv &= fs[static_cast<int64_t>(c * 16 + ((h.w[2] >> (4 * c)) & 15u)) * G + g];
+                for (int c = 0; c < kChunks; ++c) surv &= fs[static_cast<int64_t>(c * 16 + x[c]) * G + g];
                 if (surv) verify_group(surv, rules + rb + static_cast<int64_t>(g) * 32, static_cast<uint32_t>(g) * 32, h,
                                        &best);
             }
@@ -893,6 +1003,21 @@ unsigned grid_for(int64_t n, int threads)
     return b > 0 ? static_cast<unsigned>(b) : 1u;
 }
 
+// Header histogram, then each switch's filter chunks.
+int choose_chunks(pc_ctx *ctx, int32_t S, const int32_t *rule_off, int64_t n_rules, const pc_rule *rules,
+                  const pc_key *hdr, int32_t T, uint32_t *hh, uint32_t *cpos, hipStream_t stream)
+{
+    launch_fill_u32(hh, kKeyNibbles * 16, 0, stream);
+    if (T > 0)
+        PC_TIMED(ctx, "k_tr_hdr_hist", stream,
+                 hipLaunchKernelGGL(k_tr_hdr_hist, dim3(64), dim3(256), 0, stream, hdr, T, hh));
+    PC_TIMED(ctx, "k_tr_choose", stream,
+             hipLaunchKernelGGL(k_tr_choose, dim3(static_cast<unsigned>(S)), dim3(256), 0, stream, S, rule_off,
+                                n_rules, rules, hh, cpos));
+    PC_LAUNCH_CHECK(ctx);
+    return PC_OK;
+}
+
 }  // namespace
 
 int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
@@ -904,9 +1029,11 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     struct Bufs {
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
         int32_t *cur, *hops, *rank, *live0, *live1, *bucket;
-        uint32_t *jm, *filt;
+        uint32_t *jm, *filt, *cpos, *hh;
     } B;
     auto carve = [&](Carver &c) {
+        B.cpos = c.take<uint32_t>(S + 1);
+        B.hh = c.take<uint32_t>(kKeyNibbles * 16);
         B.gcount = c.take<int32_t>(S + 1);
         B.bcount = c.take<int32_t>(S + 1);
         B.gofs = c.take<int32_t>(S + 1);
@@ -936,6 +1063,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         B.filt = const_cast<uint32_t *>(pre->filt);
         B.gcount = const_cast<int32_t *>(pre->gcount);
         B.gofs = const_cast<int32_t *>(pre->gofs);
+        B.cpos = const_cast<uint32_t *>(pre->cpos);
     } else if (S > 0) {
         PC_TIMED(ctx, "k_tr_switch_info", stream, hipLaunchKernelGGL(k_tr_switch_info, dim3(grid_for(S, 256)), dim3(256), 0, stream, S, port_off, n_ports, jur,
                            rule_off, n_rules, B.gcount, B.bcount, ctx->d_err));
@@ -960,10 +1088,12 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                                port_peer, S, ctx->d_err));
             PC_LAUNCH_CHECK(ctx);
         }
+        rc = choose_chunks(ctx, S, rule_off, n_rules, rules, hdr, T, B.hh, B.cpos, stream);
+        if (rc) return rc;
         if (prep_blocks > 0) {
             PC_TIMED(ctx, "k_tr_prep", stream, hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(prep_blocks)), dim3(kPrepWaves * 64), 0, stream, S,
                                port_off, n_ports, rule_off, rules, B.gcount, B.gofs, B.bofs, B.filt, ctx->d_err,
-                               nullptr, nullptr));
+                               nullptr, nullptr, B.cpos));
             PC_LAUNCH_CHECK(ctx);
         }
     }
@@ -1012,7 +1142,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_TIMED(ctx, "k_tr_walk", stream,
                      hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
                                         rule_off, rules, B.gcount, B.gofs, B.filt, hdr, ttl, live_cur, n_cur, B.cur,
-                                        B.jm, B.hops, out, watch, K, visit, vsum, walk));
+                                        B.jm, B.hops, out, watch, K, visit, vsum, walk, B.cpos));
             PC_LAUNCH_CHECK(ctx);
             break;
         }
@@ -1030,7 +1160,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         PC_TIMED(ctx, "k_tr_match", stream,
                  hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(8 * ((max_items + 7) / 8))),
                                     dim3(kMatchThreads), 0, stream, S, rule_off, rules, B.gcount, B.gofs, B.filt, hdr,
-                                    B.boff, B.ioff, B.bucket, lv));
+                                    B.boff, B.ioff, B.bucket, B.cpos, lv));
         PC_LAUNCH_CHECK(ctx);
         // the count leaving this level
         const int slot = (level + 1) & 1;
@@ -1057,7 +1187,7 @@ namespace {
 // Per-switch arrays of the cached prepared tables in ctx->tc_meta.
 struct TcMeta {
     int32_t *gcount, *bcount, *gofs, *bofs;
-    uint32_t *sw_bad;
+    uint32_t *sw_bad, *cpos, *hh;
 };
 
 TcMeta tc_meta(pc_ctx *ctx, int32_t S)
@@ -1069,16 +1199,18 @@ TcMeta tc_meta(pc_ctx *ctx, int32_t S)
     m.gofs = c.take<int32_t>(static_cast<size_t>(S) + 1);
     m.bofs = c.take<int32_t>(static_cast<size_t>(S) + 1);
     m.sw_bad = c.take<uint32_t>(static_cast<size_t>(S) + 1);
+    m.cpos = c.take<uint32_t>(static_cast<size_t>(S) + 1);
+    m.hh = c.take<uint32_t>(kKeyNibbles * 16);
     return m;
 }
 
-size_t tc_meta_bytes(int32_t S) { return 5 * (256 + (static_cast<size_t>(S) + 1) * 4); }
+size_t tc_meta_bytes(int32_t S) { return 7 * (256 + (static_cast<size_t>(S) + 1) * 4) + kKeyNibbles * 16 * 4; }
 
 // Prepare every switch's tables into the context's cache (and sweep them
 // for data errors); the cache then describes these tables.
 int tc_prepare_all(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *port_peer, int64_t n_ports,
                    const uint8_t *jur, const int32_t *rule_off, const pc_rule *rules, int64_t n_rules,
-                   hipStream_t stream)
+                   const pc_key *hdr, int32_t T, hipStream_t stream)
 {
     ctx->tc_S = -1;
     int rc = pc_ensure_tc_meta(ctx, tc_meta_bytes(S));
@@ -1111,11 +1243,14 @@ int tc_prepare_all(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_
             PC_LAUNCH_CHECK(ctx);
         }
         launch_fill_u32(m.sw_bad, static_cast<size_t>(S), 0, stream);
+        rc = choose_chunks(ctx, S, rule_off, n_rules, rules, hdr, T, m.hh, m.cpos, stream);
+        if (rc) return rc;
         if (blocks > 0) {
             PC_TIMED(ctx, "k_tr_prep", stream,
                      hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(blocks)), dim3(kPrepWaves * 64), 0,
                                         stream, S, port_off, n_ports, rule_off, rules, m.gcount, m.gofs, m.bofs,
-                                        reinterpret_cast<uint32_t *>(ctx->tc_filt), ctx->d_err, nullptr, m.sw_bad));
+                                        reinterpret_cast<uint32_t *>(ctx->tc_filt), ctx->d_err, nullptr, m.sw_bad,
+                                        m.cpos));
             PC_LAUNCH_CHECK(ctx);
         }
     }
@@ -1135,11 +1270,11 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
 {
     if (C < 0) {  // every trace, from scratch; the prepared tables are kept for later deltas
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_retraced), 1, static_cast<uint32_t>(T), stream);
-        int rc = tc_prepare_all(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, stream);
+        int rc = tc_prepare_all(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, T, stream);
         if (rc) return rc;
         if (T == 0) return PC_OK;
         const TcMeta m = tc_meta(ctx, S);
-        const TracePrep pre{reinterpret_cast<const uint32_t *>(ctx->tc_filt), m.gcount, m.gofs};
+        const TracePrep pre{reinterpret_cast<const uint32_t *>(ctx->tc_filt), m.gcount, m.gofs, m.cpos};
         return run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, ingress, T, ttl,
                          nullptr, 0, out, nullptr, vsum, walk, stream, &pre);
     }
@@ -1205,17 +1340,19 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
                                         m.sw_bad));
         }
         if (ctx->tc_blocks > 0 && C > 0) {
+            // the changed switches keep their filter chunks (any choice is exact)
             PC_TIMED(ctx, "k_tr_prep", stream,
                      hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(ctx->tc_blocks)), dim3(kPrepWaves * 64),
                                         0, stream, S, port_off, n_ports, rule_off, rules, m.gcount, m.gofs, m.bofs,
-                                        reinterpret_cast<uint32_t *>(ctx->tc_filt), ctx->d_err, bitmap, m.sw_bad));
+                                        reinterpret_cast<uint32_t *>(ctx->tc_filt), ctx->d_err, bitmap, m.sw_bad,
+                                        m.cpos));
         }
         PC_TIMED(ctx, "k_tc_badsum", stream,
                  hipLaunchKernelGGL(k_tc_badsum, dim3(grid_for(S, 256)), dim3(256), 0, stream, m.sw_bad, S,
                                     ctx->d_err));
         PC_LAUNCH_CHECK(ctx);
     } else {
-        rc = tc_prepare_all(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, stream);
+        rc = tc_prepare_all(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr, T, stream);
         if (rc) return rc;
     }
     if (n > 0) {
@@ -1224,7 +1361,7 @@ int run_trace_delta(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32
                                     ingress, hdr_c, ing_c));
         PC_LAUNCH_CHECK(ctx);
         const TcMeta m = tc_meta(ctx, S);
-        const TracePrep pre{reinterpret_cast<const uint32_t *>(ctx->tc_filt), m.gcount, m.gofs};
+        const TracePrep pre{reinterpret_cast<const uint32_t *>(ctx->tc_filt), m.gcount, m.gofs, m.cpos};
         rc = run_trace(ctx, S, port_off, port_peer, n_ports, jur, rule_off, rules, n_rules, hdr_c, ing_c, n, ttl,
                        nullptr, 0, out_c, nullptr, vsum_c, walk ? walk_c : nullptr, stream, &pre);
         if (rc) return rc;

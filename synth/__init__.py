@@ -506,8 +506,17 @@ def random_keys(rng, n):
     return keys
 
 
+def prefix_masks(rng, m, lo=16, hi=32):
+    """Routing-table masks: a destination-address prefix of a uniform length
+    in [lo, hi] bits; source address, ports and protocol wildcarded."""
+    L = rng.integers(lo, hi + 1, size=m).astype(np.uint64)
+    msk = np.zeros((m, 4), np.uint32)
+    msk[:, 1] = ((np.uint64(0xFFFFFFFF) << (np.uint64(32) - L)) & np.uint64(0xFFFFFFFF)).astype(np.uint32)
+    return msk
+
+
 def build_tables(rng, topo, R, p_care, drop_p=0.05, misroute_p=0.02,
-                 prio="distinct", prio_range=8, flows=None, chunk=256):
+                 prio="distinct", prio_range=8, flows=None, chunk=256, masks="iid"):
     """R rules per switch.  Every slot first holds an i.i.d. rule (random
     value, care bits with probability p_care, action = uniform port or DROP
     with probability drop_p); then, when `flows` = (keys, sw, port, nh) is
@@ -517,8 +526,11 @@ def build_tables(rng, topo, R, p_care, drop_p=0.05, misroute_p=0.02,
     misroute_p.  Priorities: 'distinct' (R distinct uint16 per switch in
     random order: a random permutation of R strata of width 65536/R, a
     uniform offset inside each), 'uniform' (i.i.d. uint16, ties possible) or
-    'small' (uniform over [0, prio_range), many ties)."""
+    'small' (uniform over [0, prio_range), many ties).  masks='prefix':
+    every rule matches a destination prefix only (prefix_masks) instead of
+    i.i.d. care bits."""
     S = topo["S"]
+    mk = (lambda m: prefix_masks(rng, m)) if masks == "prefix" else None
     port_off = topo["port_off"]
     nports = np.diff(port_off).astype(np.int64)
     n = S * R
@@ -530,7 +542,7 @@ def build_tables(rng, topo, R, p_care, drop_p=0.05, misroute_p=0.02,
         s1 = min(S, s0 + chunk)
         m = (s1 - s0) * R
         val = random_keys(rng, m)
-        msk = care_bits(rng, (m, 4), p_care)
+        msk = care_bits(rng, (m, 4), p_care) if mk is None else mk(m)
         msk[:, 3] &= np.uint32(0xFF)
         blk = np.empty((m, 10), np.uint32)
         blk[:, 0:4] = val & msk
@@ -580,7 +592,7 @@ def build_tables(rng, topo, R, p_care, drop_p=0.05, misroute_p=0.02,
             slot[sel] = perm[e_sw[sel] - s0, rank[sel]]
         pos = e_sw * R + slot
         m = pos.shape[0]
-        msk = care_bits(rng, (m, 4), p_care)
+        msk = care_bits(rng, (m, 4), p_care) if mk is None else mk(m)
         msk[:, 3] &= np.uint32(0xFF)
         raw[pos, 0:4] = keys[e_flow] & msk
         raw[pos, 4:8] = msk
@@ -663,18 +675,21 @@ def trace_workload(seed, k, J, R, T, ttl, n_flows, p_care=0.7, variant="rpath",
     from the flows and injected at the flow's ingress edge switch.
     'literal': i.i.d. rules only and uniform random headers at random edge
     switches.  'dense': 95% wildcard bits, small priority range, i.i.d.
-    rules, random headers at random switches."""
+    rules, random headers at random switches.  'prefix': as 'rpath', but
+    every rule (path or noise) matches a destination prefix of 16-32 bits
+    with ports, source and protocol wildcarded, as a routing table does."""
     rng = np.random.default_rng(seed)
     topo = fat_tree(k, J)
     wl = Workload(name, seed)
     wl.meta.update(variant=variant, k=k, J=J, R=R)
-    if variant == "rpath":
+    if variant in ("rpath", "prefix"):
         H = topo["H"]
         hs = rng.integers(0, H, size=n_flows)
         hd = (hs + rng.integers(1, H, size=n_flows)) % H
         keys = flow_keys(rng, topo, hs, hd)
         sw, port, nh = flow_paths(rng, topo, hs, hd)
-        rule_off, rules, dropped = build_tables(rng, topo, R, p_care, flows=(keys, sw, port, nh))
+        rule_off, rules, dropped = build_tables(rng, topo, R, p_care, flows=(keys, sw, port, nh),
+                                                masks="iid" if variant == "rpath" else "prefix")
         pick = rng.integers(0, n_flows, size=T)
         hdr = keys[pick]
         ingress = topo["host_switch"][hs[pick]].astype(np.int32)

@@ -210,9 +210,45 @@ def trace_path(request, monkeypatch):
     return request.param
 
 
-@pytest.mark.parametrize("variant", ["rpath", "literal", "dense"])
+@pytest.mark.parametrize("variant", ["rpath", "literal", "dense", "prefix"])
 def test_trace_fat_tree_small(g, orc, variant, trace_path):
     wl = synth.trace_workload(3, 8, 4, 512, 20000, 24, 3000, variant=variant)
+    _check_workload(g, orc, wl)
+
+
+def test_trace_prefix_tables_multi_slice(g, orc, trace_path):
+    """Routing tables (destination prefixes of 16-32 bits, ports, source and
+    protocol wildcarded): each switch filters on the key nibbles its own
+    rules care about, not on the port bits; 2,048 rules per switch (4
+    slices), many rules per destination, so many filter survivors."""
+    wl = synth.trace_workload(8, 16, 8, 2048, 40000, 32, 20000, variant="prefix")
+    _check_workload(g, orc, wl)
+
+
+def test_trace_mixed_tables(g, orc, trace_path):
+    """Switches whose tables mix i.i.d. care bits, destination prefixes and
+    rules that care only about the protocol byte or nothing at all: the
+    per-switch filter chunks differ from switch to switch."""
+    wl = synth.trace_workload(9, 8, 4, 700, 20000, 24, 3000, variant="rpath")
+    rules = wl["rules"].copy()
+    ro = wl["rule_off"]
+    rng = np.random.default_rng(5)
+    for s in range(wl["S"]):
+        seg = slice(ro[s], ro[s + 1])
+        kind = s % 4
+        if kind == 1:       # destination prefixes
+            m = synth.prefix_masks(rng, ro[s + 1] - ro[s])
+        elif kind == 2:     # protocol byte only, half of them
+            m = np.zeros((ro[s + 1] - ro[s], 4), np.uint32)
+            m[::2, 3] = 0xFF
+        elif kind == 3:     # wildcard everything in every third rule
+            m = rules["mask"][seg].copy()
+            m[::3] = 0
+        else:
+            continue
+        rules["mask"][seg] = m
+        rules["value"][seg] &= m
+    wl.arrays["rules"] = rules
     _check_workload(g, orc, wl)
 
 
