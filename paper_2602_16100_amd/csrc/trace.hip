@@ -51,6 +51,7 @@ constexpr int kPrepGroups = 128;             // groups per prep workgroup (16 wa
 constexpr uint64_t kNoMatch = ~0ull;
 static_assert(kChunk % 4 == 0 && kChunk <= kMatchThreads, "one epilogue thread per lookup");
 constexpr int kCountPad = 32;  // live-trace counters are 128 bytes apart: contended atomics on one line serialise
+constexpr int kPortSlots = 64;  // forwarding ports whose moves a match workgroup counts in LDS
 
 // 16 chunk-value sets of one 4-bit chunk, kept in VGPRs; indexed with a
 // wave-uniform value this lowers to register-indexed moves (s_set_gpr_idx).
@@ -456,6 +457,7 @@ __device__ __forceinline__ int apply_rule(int32_t S, const int32_t *__restrict__
     if (peer < -1 || peer >= S) return PC_MISS;
     if (hops == ttl) return PC_TTL;
     *next = peer;
+    *port = static_cast<uint16_t>(a);  // the forwarding port
     return -1;
 }
 
@@ -689,15 +691,26 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         // time, with the chunk sets dead.  Then filtering resumes.  A quad
         // of lookups queues at most 256 entries, so every round advances.
         for (int32_t jr = jb; jr < je;) {
-            // an opaque copy of G keeps the 96 load addresses from being
-            // hoisted out of the loops (and spilled) as invariants
-            int32_t Gr = G;
-            asm volatile("" : "+s"(Gr));
+            // buffer loads: the lane's group as the vector offset (clamped
+            // into the table), the plane as a scalar offset; an opaque copy
+            // of the plane stride keeps the 96 offsets from being hoisted out
+            // of the loops (and spilled) as invariants.  A lane past the last
+            // group gets empty chunk sets, so it never survives the filter.
+            uint32_t pstride = static_cast<uint32_t>(G) * 4u;
+            asm volatile("" : "+s"(pstride));
+            const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
+                const_cast<uint32_t *>(fs), static_cast<short>(0), kPlaneWords * G * 4, 0x00020000);
+            const uint32_t voff = static_cast<uint32_t>(min(g, G - 1)) * 4u;
             v16u F[kChunks];
 #pragma unroll
             for (int c = 0; c < kChunks; ++c)
 #pragma unroll
-                for (int x = 0; x < 16; ++x) F[c][x] = g < G ? fs[static_cast<int64_t>(c * 16 + x) * Gr + g] : 0u;
+                for (int x = 0; x < 16; ++x)
+                    F[c][x] = __builtin_amdgcn_raw_buffer_load_b32(frs, voff, static_cast<uint32_t>(c * 16 + x) * pstride, 0);
+            if (g >= G) {
+#pragma unroll
+                for (int x = 0; x < 16; ++x) F[0][x] = 0u;
+            }
             int32_t qn = 0;
             int32_t j0 = jr;
             for (; j0 < je; j0 += 4) {
@@ -750,18 +763,24 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
             __builtin_amdgcn_wave_barrier();
         }
     }
+    // per forwarding port of this switch (the first kPortSlots): the item's
+    // traces that leave through it, then one count update of its peer
+    __shared__ int32_t pcnt[kPortSlots], pbase[kPortSlots];
     __shared__ int32_t nmove, mbase;
     if (threadIdx.x == 0) nmove = 0;
+    if (threadIdx.x < kPortSlots) pcnt[threadIdx.x] = 0;
     __syncthreads();
     // apply the first match, then count and list the traces that move on
-    // (one global reservation of live-list slots per workgroup)
-    int32_t slot = -1, t = -1;
+    // (one global reservation of live-list slots per workgroup, one count
+    // update per next switch and workgroup; a trace's rank in its next
+    // switch's bucket is its count's base plus its rank in the item)
+    int32_t slot = -1, t = -1, lrank = -1;
+    uint16_t port = PC_NO_PORT;
     if (threadIdx.x < tn) {  // tn <= kChunk <= kMatchThreads
         t = tids[threadIdx.x];
         if (t >= 0) {
             const int32_t h = lv.hops[t];
             int32_t next = -1;
-            uint16_t port = PC_NO_PORT;
             const int state = apply_rule(lv.S, lv.port_off, lv.port_peer, lv.n_ports, rule_off, rules, lv.ttl, s,
                                          best[threadIdx.x], h, &next, &port);
             if (state >= 0) {
@@ -773,14 +792,24 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
                 if (lv.visit) lv.visit[t] |= watch_bits(lv.watch, lv.K, t, next);
                 if (lv.vsum) lv.vsum[t] |= sum_bit(next);
                 if (lv.walk && h + 1 < kWalkSlots) lv.walk[static_cast<int64_t>(t) * kWalkSlots + h + 1] = next;
-                lv.rank[t] = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
+                if (port < kPortSlots) lrank = atomicAdd(&pcnt[port], 1);
+                else lv.rank[t] = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
                 slot = atomicAdd(&nmove, 1);
             }
         }
     }
     __syncthreads();
     if (threadIdx.x == 0) mbase = nmove ? atomicAdd(lv.nlive_next, nmove) : 0;
+    if (threadIdx.x < kPortSlots) {
+        const int32_t c = pcnt[threadIdx.x];
+        // a port some trace forwarded through: its peer is a valid switch
+        if (c > 0) {
+            const int32_t peer = lv.port_peer[lv.port_off[s] + threadIdx.x];
+            pbase[threadIdx.x] = atomicAdd(&lv.counts_next[static_cast<int64_t>(peer) * kCountPad], c);
+        }
+    }
     __syncthreads();
+    if (lrank >= 0) lv.rank[t] = pbase[port] + lrank;
     if (slot >= 0 && mbase + slot < lv.T) lv.live_next[mbase + slot] = t;
 }
 
