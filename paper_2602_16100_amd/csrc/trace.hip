@@ -417,9 +417,12 @@ __device__ __forceinline__ bool rule_matches(const pc_rule *r, uint32_t h0, uint
             ((h2 ^ r->value.w[2]) & r->mask.w[2]) | ((h3 ^ r->value.w[3]) & r->mask.w[3])) == 0;
 }
 
+// First-match key of a rule: (0xFFFF - priority) << 48 | local index << 16 |
+// action.  The smallest key is the highest priority, ties to the lower
+// index; the action rides along, so applying the match reads no rule.
 __device__ __forceinline__ uint64_t rule_key(const pc_rule *r, uint32_t local)
 {
-    return (static_cast<uint64_t>(0xFFFFu - r->priority) << 32) | local;
+    return (static_cast<uint64_t>(0xFFFFu - r->priority) << 48) | (static_cast<uint64_t>(local) << 16) | r->action;
 }
 
 // Verify the surviving rules of one 32-rule group against the full header
@@ -436,16 +439,14 @@ __device__ __forceinline__ void verify_group(uint32_t surv, const pc_rule *grp, 
     }
 }
 
-// Apply the chosen rule at switch s: returns the terminal state, or -1 when
-// the trace moves on to *next.
+// Apply the chosen rule (its key, see rule_key) at switch s: returns the
+// terminal state, or -1 when the trace moves on to *next through port *port.
 __device__ __forceinline__ int apply_rule(int32_t S, const int32_t *__restrict__ port_off,
-                                          const int32_t *__restrict__ port_peer, int64_t n_ports,
-                                          const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules,
-                                          int32_t ttl, int32_t s, uint64_t key, int32_t hops, int32_t *next,
-                                          uint16_t *port)
+                                          const int32_t *__restrict__ port_peer, int64_t n_ports, int32_t ttl,
+                                          int32_t s, uint64_t key, int32_t hops, int32_t *next, uint16_t *port)
 {
     if (key == kNoMatch) return PC_MISS;
-    const uint32_t a = rules[rule_off[s] + static_cast<uint32_t>(key)].action;
+    const uint32_t a = static_cast<uint32_t>(key & 0xFFFFu);
     if (a == PC_ACTION_DROP) return PC_DROP;
     const int64_t pb = port_off[s], pe = port_off[s + 1];
     if (!pc_range_ok(pb, pe, n_ports) || static_cast<int64_t>(a) >= pe - pb) return PC_MISS;
@@ -627,6 +628,8 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     __shared__ __align__(16) uint32_t cidx[kChunks][kChunk];  // each lookup's values of the switch's filter chunks
     __shared__ __align__(16) pc_key keys[kChunk];
     __shared__ int32_t tids[kChunk];
+    __shared__ int32_t thops[kChunk];  // each lookup's trace: hops so far and jurisdiction mask
+    __shared__ uint32_t tjm[kChunk];
     __shared__ uint2 queue[kMatchWaves][kQueue];  // per wavefront: (survivor set, lookup << 6 | lane)
     // the grid was sized from an upper bound on the item count: blocks past
     // the real count's per-XCD share return at once
@@ -672,9 +675,17 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         int32_t t = bucket[bb + min(i, tn - 1)];
         if (static_cast<uint32_t>(t) >= static_cast<uint32_t>(lv.T)) t = -1;  // not a trace id: skipped
         pc_key h = {};
-        if (t >= 0) h = hdr[t];
+        int32_t hp = 0;
+        uint32_t jmv = 0;
+        if (t >= 0) {
+            h = hdr[t];
+            hp = lv.hops[t];
+            jmv = lv.jm[t];
+        }
         tids[i] = t;
         keys[i] = h;
+        thops[i] = hp;
+        tjm[i] = jmv;
         best[i] = kNoMatch;
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) cidx[c][i] = key_nibble(h.w[0], h.w[1], h.w[2], h.w[3], chunk_pos(cp, c));
@@ -779,16 +790,17 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     if (threadIdx.x < tn) {  // tn <= kChunk <= kMatchThreads
         t = tids[threadIdx.x];
         if (t >= 0) {
-            const int32_t h = lv.hops[t];
+            const int32_t h = thops[threadIdx.x];
+            const uint32_t jmv = tjm[threadIdx.x];
             int32_t next = -1;
-            const int state = apply_rule(lv.S, lv.port_off, lv.port_peer, lv.n_ports, rule_off, rules, lv.ttl, s,
-                                         best[threadIdx.x], h, &next, &port);
+            const int state = apply_rule(lv.S, lv.port_off, lv.port_peer, lv.n_ports, lv.ttl, s, best[threadIdx.x],
+                                         h, &next, &port);
             if (state >= 0) {
-                write_out(lv.out, t, lv.jm[t], s, port, h, state);
+                write_out(lv.out, t, jmv, s, port, h, state);
             } else {
                 lv.cur[t] = next;
                 lv.hops[t] = h + 1;
-                lv.jm[t] |= jur_bit(lv.jur, next);
+                lv.jm[t] = jmv | jur_bit(lv.jur, next);
                 if (lv.visit) lv.visit[t] |= watch_bits(lv.watch, lv.K, t, next);
                 if (lv.vsum) lv.vsum[t] |= sum_bit(next);
                 if (lv.walk && h + 1 < kWalkSlots) lv.walk[static_cast<int64_t>(t) * kWalkSlots + h + 1] = next;
@@ -861,8 +873,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
             const uint64_t key = best;
             int32_t next = -1;
             uint16_t port = PC_NO_PORT;
-            const int state = apply_rule(S, port_off, port_peer, n_ports, rule_off, rules, ttl, s, key, hops, &next,
-                                         &port);
+            const int state = apply_rule(S, port_off, port_peer, n_ports, ttl, s, key, hops, &next, &port);
             __syncthreads();  // everyone has read `best` before it is reset
             if (state >= 0) {
                 if (threadIdx.x == 0) {
