@@ -45,11 +45,13 @@ constexpr int kPlaneWords = kChunks * 16;  // words per 32-rule group
 constexpr int kMatchWaves = 8;
 constexpr int kMatchThreads = kMatchWaves * 64;
 constexpr int kSliceGroups = kMatchThreads;  // one group (32 rules) per lane
-constexpr int kChunk = 256;                  // lookups per match work item (a multiple of 4, <= kMatchThreads)
+constexpr int kChunk = 256;                  // lookups per match work item and lookup stream (a multiple of 4)
+constexpr int kMaxChunk = 512;               // lookups per work item at most (<= kMatchThreads)
 constexpr int kQueue = 512;                  // queued filter survivors per wavefront (>= 4 x 64)
 constexpr int kPrepGroups = 128;             // groups per prep workgroup (16 wavefronts x 4 rounds x 2 groups)
 constexpr uint64_t kNoMatch = ~0ull;
-static_assert(kChunk % 4 == 0 && kChunk <= kMatchThreads, "one epilogue thread per lookup");
+static_assert(kChunk % 4 == 0 && kMaxChunk % kChunk == 0 && kMaxChunk <= kMatchThreads,
+              "one epilogue thread per lookup");
 constexpr int kCountPad = 32;  // live-trace counters are 128 bytes apart: contended atomics on one line serialise
 constexpr int kPortSlots = 64;  // forwarding ports whose moves a match workgroup counts in LDS
 
@@ -498,11 +500,20 @@ struct Level {
     int32_t *walk;          // [T][kWalkSlots] walk records or nullptr
 };
 
+// Lookups per match work item of a switch of G groups: kChunk per lookup
+// stream (a table of fewer than kSliceGroups groups leaves wavefronts free
+// for further streams), at most kMaxChunk.
+__device__ __forceinline__ int32_t item_lookups(int32_t G)
+{
+    const int32_t gws = G >= kSliceGroups ? kMatchWaves : max(1, (G + 63) / 64);
+    return min(kMaxChunk, kChunk * (kMatchWaves / gws));
+}
+
 // Per level: bucket offsets boff = exclusive scan of counts (which are
 // cleared for reuse) and work-item offsets ioff = exclusive scan of
-// ceil(counts / kChunk); one workgroup of 1024 threads.
+// ceil(counts / item_lookups(G)); one workgroup of 1024 threads.
 __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, int32_t S, int32_t *__restrict__ boff,
-                                                  int32_t *__restrict__ ioff)
+                                                  int32_t *__restrict__ ioff, const int32_t *__restrict__ gcount)
 {
     __shared__ int32_t wsum[2][16];
     __shared__ int32_t carry_s[2];
@@ -512,7 +523,8 @@ __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, 
     for (int32_t base = 0; base < S; base += 1024) {
         const int32_t i = base + tid;
         const int32_t v0 = i < S ? counts[static_cast<int64_t>(i) * kCountPad] : 0;
-        const int32_t v1 = (v0 + kChunk - 1) / kChunk;
+        const int32_t ch = i < S ? item_lookups(gcount[i]) : kChunk;
+        const int32_t v1 = (v0 + ch - 1) / ch;
         int32_t x0 = v0, x1 = v1;
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
@@ -615,21 +627,21 @@ __device__ __forceinline__ void filter_quad(const uint32_t (&x)[kChunks][4], con
 }
 #undef PC_IDX
 
-// One workgroup per work item = (switch, chunk of at most kChunk lookups of
-// its bucket).  Items are dealt to XCDs in contiguous ranges, so the chunks
-// of one switch share an L2.
+// One workgroup per work item = (switch, chunk of at most item_lookups(G)
+// lookups of its bucket).  Items are dealt to XCDs in contiguous ranges, so
+// the chunks of one switch share an L2.
 __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     int32_t S, const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules,
     const int32_t *__restrict__ gcount, const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
     const pc_key *__restrict__ hdr, const int32_t *__restrict__ boff, const int32_t *__restrict__ ioff,
     const int32_t *__restrict__ bucket, const uint32_t *__restrict__ cpos, Level lv)
 {
-    __shared__ uint64_t best[kChunk];
-    __shared__ __align__(16) uint32_t cidx[kChunks][kChunk];  // each lookup's values of the switch's filter chunks
-    __shared__ __align__(16) pc_key keys[kChunk];
-    __shared__ int32_t tids[kChunk];
-    __shared__ int32_t thops[kChunk];  // each lookup's trace: hops so far and jurisdiction mask
-    __shared__ uint32_t tjm[kChunk];
+    __shared__ uint64_t best[kMaxChunk];
+    __shared__ __align__(16) uint32_t cidx[kChunks][kMaxChunk];  // each lookup's values of the switch's filter chunks
+    __shared__ __align__(16) pc_key keys[kMaxChunk];
+    __shared__ int32_t tids[kMaxChunk];
+    __shared__ int32_t thops[kMaxChunk];  // each lookup's trace: hops so far and jurisdiction mask
+    __shared__ uint32_t tjm[kMaxChunk];
     __shared__ uint2 queue[kMatchWaves][kQueue];  // per wavefront: (survivor set, lookup << 6 | lane)
     // the grid was sized from an upper bound on the item count: blocks past
     // the real count's per-XCD share return at once
@@ -647,8 +659,9 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         else hi = mid;
     }
     const int32_t s = lo;
-    const int32_t bb = boff[s] + (item - ioff[s]) * kChunk;
-    const int32_t tn = min(kChunk, min(boff[s + 1], lv.T) - bb);  // bucket holds at most T entries
+    const int32_t chunk = item_lookups(gcount[s]);
+    const int32_t bb = boff[s] + (item - ioff[s]) * chunk;
+    const int32_t tn = min(chunk, min(boff[s + 1], lv.T) - bb);  // bucket holds at most T entries
     if (tn <= 0) return;
     const int32_t tn4 = (tn + 3) & ~3;
     const int lane = threadIdx.x & 63;
@@ -787,7 +800,7 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     // switch's bucket is its count's base plus its rank in the item)
     int32_t slot = -1, t = -1, lrank = -1;
     uint16_t port = PC_NO_PORT;
-    if (threadIdx.x < tn) {  // tn <= kChunk <= kMatchThreads
+    if (threadIdx.x < tn) {  // tn <= kMaxChunk <= kMatchThreads
         t = tids[threadIdx.x];
         if (t >= 0) {
             const int32_t h = thops[threadIdx.x];
@@ -1188,7 +1201,8 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         }
         const int32_t nlive = static_cast<int32_t>(known);
         PC_TIMED(ctx, "k_tr_plan", stream,
-                 hipLaunchKernelGGL(k_tr_plan, dim3(1), dim3(1024), 0, stream, cnt_cur, S, B.boff, B.ioff));
+                 hipLaunchKernelGGL(k_tr_plan, dim3(1), dim3(1024), 0, stream, cnt_cur, S, B.boff, B.ioff,
+                                    B.gcount));
         PC_TIMED(ctx, "k_tr_scatter", stream,
                  hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, T,
                                     B.cur, B.rank, B.boff, B.bucket));
@@ -1196,7 +1210,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         const Level lv{S,     T,     port_off, port_peer, n_ports, jur,   ttl, B.cur, B.jm,
                        B.hops, B.rank, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit, vsum, walk};
         // at most nlive / kChunk + (switches with a partial chunk) items
-        const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);
+        const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);  // item >= kChunk
         PC_TIMED(ctx, "k_tr_match", stream,
                  hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(8 * ((max_items + 7) / 8))),
                                     dim3(kMatchThreads), 0, stream, S, rule_off, rules, B.gcount, B.gofs, B.filt, hdr,
