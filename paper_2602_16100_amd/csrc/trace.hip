@@ -352,8 +352,8 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
 __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__restrict__ jur,
                                                  const int32_t *__restrict__ ingress, int32_t T,
                                                  int32_t *__restrict__ cur, uint32_t *__restrict__ jm,
-                                                 int32_t *__restrict__ hops, int32_t *__restrict__ rank,
-                                                 int32_t *__restrict__ live, int32_t *__restrict__ nlive,
+                                                 int32_t *__restrict__ hops, int4 *__restrict__ live,
+                                                 int32_t *__restrict__ nlive,
                                                  int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
                                                  uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
@@ -363,10 +363,10 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
     if (threadIdx.x == 0) nloc = 0;
     __syncthreads();
     const int32_t t = blockIdx.x * 256 + threadIdx.x;
-    int32_t slot = -1;
+    int32_t slot = -1, s = -1, rk = 0;
     bool bad = false;
     if (t < T) {
-        const int32_t s = ingress[t];
+        s = ingress[t];
         if (s < 0 || s >= S) {
             bad = true;
             pc_trace_out o;
@@ -388,28 +388,29 @@ __global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__res
             if (walk)
                 for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = j ? -1 : s;
             hops[t] = 0;
-            rank[t] = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
+            rk = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
             slot = atomicAdd(&nloc, 1);
         }
     }
     __syncthreads();
     if (threadIdx.x == 0) base = nloc ? atomicAdd(nlive, nloc) : 0;
     __syncthreads();
-    if (slot >= 0) live[base + slot] = t;
+    if (slot >= 0) live[base + slot] = make_int4(t, s, rk, 0);
     if (__ballot(bad) && (threadIdx.x & 63) == 0) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
-// Bucket the live traces by current switch: trace t goes to slot
-// boff[cur[t]] + rank[t], its rank having been taken when it was counted.
-__global__ void k_tr_scatter(const int32_t *__restrict__ live, const int32_t *__restrict__ nlive, int32_t T,
-                             const int32_t *__restrict__ cur, const int32_t *__restrict__ rank,
-                             const int32_t *__restrict__ boff, int32_t *__restrict__ bucket)
+// Bucket the live traces by current switch: a live entry (t, switch, rank)
+// puts trace t at slot boff[switch] + rank, its rank having been taken when
+// it was counted.
+__global__ void k_tr_scatter(const int4 *__restrict__ live, const int32_t *__restrict__ nlive, int32_t T,
+                             int32_t S, const int32_t *__restrict__ boff, int32_t *__restrict__ bucket)
 {
     const int32_t n = min(*nlive, T);
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-        const int32_t t = live[i];
-        const int32_t pos = boff[cur[t]] + rank[t];
-        if (pos >= 0 && pos < T) bucket[pos] = t;
+        const int4 e = live[i];
+        if (e.y < 0 || e.y >= S) continue;
+        const int32_t pos = boff[e.y] + e.z;
+        if (pos >= 0 && pos < T) bucket[pos] = e.x;
     }
 }
 
@@ -488,8 +489,7 @@ struct Level {
     int32_t *cur;
     uint32_t *jm;
     int32_t *hops;
-    int32_t *rank;          // slot of the trace within its next switch's bucket
-    int32_t *live_next;     // traces still in flight after this level
+    int4 *live_next;        // traces still in flight after this level: (t, next switch, rank in its bucket)
     int32_t *nlive_next;
     int32_t *counts_next;   // live traces per switch after this level
     pc_trace_out *out;
@@ -798,14 +798,13 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     // (one global reservation of live-list slots per workgroup, one count
     // update per next switch and workgroup; a trace's rank in its next
     // switch's bucket is its count's base plus its rank in the item)
-    int32_t slot = -1, t = -1, lrank = -1;
+    int32_t slot = -1, t = -1, lrank = -1, next = -1, rk = 0;
     uint16_t port = PC_NO_PORT;
     if (threadIdx.x < tn) {  // tn <= kMaxChunk <= kMatchThreads
         t = tids[threadIdx.x];
         if (t >= 0) {
             const int32_t h = thops[threadIdx.x];
             const uint32_t jmv = tjm[threadIdx.x];
-            int32_t next = -1;
             const int state = apply_rule(lv.S, lv.port_off, lv.port_peer, lv.n_ports, lv.ttl, s, best[threadIdx.x],
                                          h, &next, &port);
             if (state >= 0) {
@@ -818,7 +817,7 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
                 if (lv.vsum) lv.vsum[t] |= sum_bit(next);
                 if (lv.walk && h + 1 < kWalkSlots) lv.walk[static_cast<int64_t>(t) * kWalkSlots + h + 1] = next;
                 if (port < kPortSlots) lrank = atomicAdd(&pcnt[port], 1);
-                else lv.rank[t] = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
+                else rk = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
                 slot = atomicAdd(&nmove, 1);
             }
         }
@@ -834,8 +833,8 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         }
     }
     __syncthreads();
-    if (lrank >= 0) lv.rank[t] = pbase[port] + lrank;
-    if (slot >= 0 && mbase + slot < lv.T) lv.live_next[mbase + slot] = t;
+    if (lrank >= 0) rk = pbase[port] + lrank;
+    if (slot >= 0 && mbase + slot < lv.T) lv.live_next[mbase + slot] = make_int4(t, next, rk, 0);
 }
 
 // Sparse tail: one workgroup per trace still in flight walks it to its end,
@@ -848,7 +847,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                                                  const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
                                                  const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
                                                  const pc_key *__restrict__ hdr, int32_t ttl,
-                                                 const int32_t *__restrict__ live, const int32_t *__restrict__ nlive,
+                                                 const int4 *__restrict__ live, const int32_t *__restrict__ nlive,
                                                  const int32_t *__restrict__ cur, const uint32_t *__restrict__ jm0,
                                                  const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
@@ -858,7 +857,7 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
     __shared__ unsigned long long best;
     const int32_t n = *nlive;
     for (int32_t i = blockIdx.x; i < n; i += gridDim.x) {
-        const int32_t t = live[i];
+        const int32_t t = live[i].x;
         const pc_key h = hdr[t];
         int32_t s = cur[t];
         uint32_t jm = jm0[t];
@@ -1081,7 +1080,8 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
 {
     struct Bufs {
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
-        int32_t *cur, *hops, *rank, *live0, *live1, *bucket;
+        int32_t *cur, *hops, *bucket;
+        int4 *live0, *live1;
         uint32_t *jm, *filt, *cpos, *hh;
     } B;
     auto carve = [&](Carver &c) {
@@ -1097,9 +1097,8 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         B.ioff = c.take<int32_t>(S + 1);
         B.cur = c.take<int32_t>(T + 1);
         B.hops = c.take<int32_t>(T + 1);
-        B.rank = c.take<int32_t>(T + 1);
-        B.live0 = c.take<int32_t>(T + 1);
-        B.live1 = c.take<int32_t>(T + 1);
+        B.live0 = c.take<int4>(T + 1);
+        B.live1 = c.take<int4>(T + 1);
         B.bucket = c.take<int32_t>(T + 1);
         B.jm = c.take<uint32_t>(T + 1);
     };
@@ -1167,11 +1166,11 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
     }
     PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
-                       B.hops, B.rank, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk, ctx->d_err));
+                       B.hops, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk, ctx->d_err));
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
-    int32_t *live_cur = B.live0, *live_nxt = B.live1;
+    int4 *live_cur = B.live0, *live_nxt = B.live1;
     int32_t *cnt_cur = B.counts0, *cnt_nxt = B.counts1;
     int32_t *n_cur = d_n, *n_nxt = d_n + 1;
     // Levels with few traces in flight are cheaper as independent walks than
@@ -1205,10 +1204,10 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                                     B.gcount));
         PC_TIMED(ctx, "k_tr_scatter", stream,
                  hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, T,
-                                    B.cur, B.rank, B.boff, B.bucket));
+                                    S, B.boff, B.bucket));
         launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
         const Level lv{S,     T,     port_off, port_peer, n_ports, jur,   ttl, B.cur, B.jm,
-                       B.hops, B.rank, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit, vsum, walk};
+                       B.hops, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit, vsum, walk};
         // at most nlive / kChunk + (switches with a partial chunk) items
         const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);  // item >= kChunk
         PC_TIMED(ctx, "k_tr_match", stream,
@@ -1228,8 +1227,8 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
             PC_HIP(ctx, hipEventSynchronize(ctx->lvl_ev[level & 1]));
             known = h_cnt[level & 1];
         }
+        std::swap(live_cur, live_nxt);
         int32_t *tmp;
-        tmp = live_cur; live_cur = live_nxt; live_nxt = tmp;
         tmp = cnt_cur; cnt_cur = cnt_nxt; cnt_nxt = tmp;
         tmp = n_cur; n_cur = n_nxt; n_nxt = tmp;
     }
