@@ -349,53 +349,95 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
     }
 }
 
-__global__ __launch_bounds__(256) void k_tr_init(int32_t S, const uint8_t *__restrict__ jur,
-                                                 const int32_t *__restrict__ ingress, int32_t T,
-                                                 int32_t *__restrict__ cur, uint32_t *__restrict__ jm,
-                                                 int32_t *__restrict__ hops, int4 *__restrict__ live,
-                                                 int32_t *__restrict__ nlive,
-                                                 int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
-                                                 const int32_t *__restrict__ watch, int32_t K,
-                                                 uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
-                                                 int32_t *__restrict__ walk, uint32_t *__restrict__ d_err)
+// Level 0: every trace starts at its ingress switch (an invalid ingress
+// ends it at once as MISS).  A workgroup takes kInitPer traces, kInitPer /
+// 1024 per thread: with kLds (S small enough) it counts them per switch in
+// LDS and reserves each switch's share with one global count update, a
+// trace's rank being that share's base plus its rank in the workgroup;
+// otherwise every trace updates its switch's count itself.  Live-list slots
+// are reserved once per workgroup.
+constexpr int kInitThreads = 1024;
+constexpr int kInitRounds = 4;
+constexpr int kInitPer = kInitThreads * kInitRounds;
+constexpr int kInitLdsS = 8192;  // switches counted in LDS at most (32 KB)
+template <bool kLds>
+__global__ __launch_bounds__(kInitThreads) void k_tr_init(int32_t S, const uint8_t *__restrict__ jur,
+                                                          const int32_t *__restrict__ ingress, int32_t T,
+                                                          int32_t *__restrict__ cur, uint32_t *__restrict__ jm,
+                                                          int32_t *__restrict__ hops, int4 *__restrict__ live,
+                                                          int32_t *__restrict__ nlive,
+                                                          int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
+                                                          const int32_t *__restrict__ watch, int32_t K,
+                                                          uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
+                                                          int32_t *__restrict__ walk, uint32_t *__restrict__ d_err)
 {
+    extern __shared__ int32_t lcnt[];  // [S] with kLds
     __shared__ int32_t nloc, base;
     if (threadIdx.x == 0) nloc = 0;
+    if constexpr (kLds)
+        for (int32_t b = threadIdx.x; b < S; b += kInitThreads) lcnt[b] = 0;
     __syncthreads();
-    const int32_t t = blockIdx.x * 256 + threadIdx.x;
-    int32_t slot = -1, s = -1, rk = 0;
+    const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kInitPer;
+    int32_t sw[kInitRounds], rk[kInitRounds], slot[kInitRounds];
     bool bad = false;
-    if (t < T) {
-        s = ingress[t];
-        if (s < 0 || s >= S) {
-            bad = true;
-            pc_trace_out o;
-            o.jmask = 0;
-            o.last_switch = s;
-            o.last_port = PC_NO_PORT;
-            o.hops = 0;
-            o.state = PC_MISS;
-            out[t] = o;
-            if (visit) visit[t] = 0;
-            if (vsum) vsum[t] = 0;
-            if (walk)
-                for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = -1;
-        } else {
-            cur[t] = s;
-            jm[t] = jur_bit(jur, s);
-            if (visit) visit[t] = watch_bits(watch, K, t, s);
-            if (vsum) vsum[t] = sum_bit(s);
-            if (walk)
-                for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = j ? -1 : s;
-            hops[t] = 0;
-            rk = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
-            slot = atomicAdd(&nloc, 1);
+#pragma unroll
+    for (int k = 0; k < kInitRounds; ++k) {
+        const int64_t t64 = t0 + k * kInitThreads + threadIdx.x;
+        const int32_t t = static_cast<int32_t>(t64);
+        sw[k] = -1;
+        rk[k] = 0;
+        if (t64 < T) {
+            const int32_t s = ingress[t];
+            if (s < 0 || s >= S) {
+                bad = true;
+                pc_trace_out o;
+                o.jmask = 0;
+                o.last_switch = s;
+                o.last_port = PC_NO_PORT;
+                o.hops = 0;
+                o.state = PC_MISS;
+                out[t] = o;
+                if (visit) visit[t] = 0;
+                if (vsum) vsum[t] = 0;
+                if (walk)
+                    for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = -1;
+            } else {
+                cur[t] = s;
+                jm[t] = jur_bit(jur, s);
+                if (visit) visit[t] = watch_bits(watch, K, t, s);
+                if (vsum) vsum[t] = sum_bit(s);
+                if (walk)
+                    for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = j ? -1 : s;
+                hops[t] = 0;
+                sw[k] = s;
+                if constexpr (kLds) rk[k] = atomicAdd(&lcnt[s], 1);
+                else rk[k] = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
+            }
         }
+        // a slot in the workgroup's share of the live list: one LDS update per wavefront
+        const uint64_t m = __ballot(sw[k] >= 0);
+        int32_t wb = 0;
+        if ((threadIdx.x & 63) == 0 && m) wb = atomicAdd(&nloc, static_cast<int32_t>(__popcll(m)));
+        wb = __shfl(wb, 0, 64);
+        slot[k] = sw[k] >= 0 ? wb + static_cast<int32_t>(__builtin_amdgcn_mbcnt_hi(
+                                        static_cast<uint32_t>(m >> 32),
+                                        __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m), 0u)))
+                             : -1;
     }
     __syncthreads();
+    if constexpr (kLds)
+        for (int32_t b = threadIdx.x; b < S; b += kInitThreads) {
+            const int32_t n = lcnt[b];
+            lcnt[b] = n ? atomicAdd(&counts[static_cast<int64_t>(b) * kCountPad], n) : 0;
+        }
     if (threadIdx.x == 0) base = nloc ? atomicAdd(nlive, nloc) : 0;
     __syncthreads();
-    if (slot >= 0) live[base + slot] = make_int4(t, s, rk, 0);
+#pragma unroll
+    for (int k = 0; k < kInitRounds; ++k)
+        if (slot[k] >= 0) {
+            const int32_t t = static_cast<int32_t>(t0 + k * kInitThreads + threadIdx.x);
+            live[base + slot[k]] = make_int4(t, sw[k], kLds ? lcnt[sw[k]] + rk[k] : rk[k], 0);
+        }
     if (__ballot(bad) && (threadIdx.x & 63) == 0) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
@@ -1165,8 +1207,19 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts0), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts1), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
     }
-    PC_TIMED(ctx, "k_tr_init", stream, hipLaunchKernelGGL(k_tr_init, dim3(static_cast<unsigned>((T + 255) / 256)), dim3(256), 0, stream, S, jur, ingress, T, B.cur, B.jm,
-                       B.hops, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk, ctx->d_err));
+    {
+        const dim3 ig(static_cast<unsigned>((static_cast<int64_t>(T) + kInitPer - 1) / kInitPer));
+        if (S <= kInitLdsS)
+            PC_TIMED(ctx, "k_tr_init", stream,
+                     hipLaunchKernelGGL(k_tr_init<true>, ig, dim3(kInitThreads), static_cast<size_t>(S) * 4, stream, S,
+                                        jur, ingress, T, B.cur, B.jm, B.hops, B.live0, d_n, B.counts0, out, watch, K,
+                                        visit, vsum, walk, ctx->d_err));
+        else
+            PC_TIMED(ctx, "k_tr_init", stream,
+                     hipLaunchKernelGGL(k_tr_init<false>, ig, dim3(kInitThreads), 0, stream, S, jur, ingress, T, B.cur,
+                                        B.jm, B.hops, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk,
+                                        ctx->d_err));
+    }
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
