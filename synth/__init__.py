@@ -860,7 +860,9 @@ def combined_workload(seed, N, L, k, J, R, I, ttl=32, p_care=0.7, kmin=1, kmax=8
     Compute and hybrid intents own a selector row (1..kmax predicates).
     Network intents join two distinct uniform hosts; hybrid intents join
     the hosts of two distinct nodes (node n sits on host n mod H) whose
-    selector row is built to hold for both.  Every network and hybrid
+    selector row is built to hold for both, except that 1 in 16 have their
+    destination placed on a uniform node instead (which the row may not
+    admit).  Every network and hybrid
     intent owns one flow (compiled one rule per hop into the tables), one
     trace of the flow's header from its ingress edge switch, and one
     reachability query from the ingress to the egress edge switch.  The
@@ -891,6 +893,14 @@ def combined_workload(seed, N, L, k, J, R, I, ttl=32, p_care=0.7, kmin=1, kmax=8
     # selector rows, in sel_row order
     off_c, preds_c = gen_preds(rng, comp_idx.shape[0], cards, kmin, kmax)
     off_h, preds_h = gen_preds_holding(rng, labels, cards, a, b, kmin, kmax)
+    # a misplaced deployment: 1 in 16 hybrid intents have their destination
+    # pod placed on a uniform node instead (own stream, so nothing else moves);
+    # the row was built for the intended node, so the placed one may fail it
+    rng_m = np.random.default_rng([seed, 9])
+    mis = rng_m.random(hyb_idx.shape[0]) < 1.0 / 16
+    b_m = rng_m.integers(0, N, size=hyb_idx.shape[0])
+    ok_m = (b_m != a) & (b_m % H != a % H)
+    b = np.where(mis & ok_m, b_m, b)
     rows = int(has_sel.sum())
     k_row = np.zeros(rows, np.int64)
     k_row[sel_row[comp_idx]] = np.diff(off_c)

@@ -190,11 +190,15 @@ def test_row_subset_matches_full(orc):
 
 
 def test_hybrid_rows_hold_for_their_endpoints(orc):
-    """The combined generator builds hybrid rows to admit both endpoints."""
-    w = synth.combined_workload(9, 1500, 16, 4, 2, 64, 300)
+    """The combined generator builds hybrid rows to admit both endpoints;
+    only the misplaced destinations (1 in 16) may fall outside them."""
+    w = synth.combined_workload(9, 1500, 16, 4, 2, 64, 3000)
     feas, pc, _ = orc.selectors(w["labels"], w["pred_off"], w["preds"])
     it = w["intents"]
-    for i in np.flatnonzero(it["kind"] == synth.KIND_HYBRID):
+    hyb = np.flatnonzero(it["kind"] == synth.KIND_HYBRID)
+    dst_out = 0
+    for i in hyb:
         r, a, b = int(it["sel_row"][i]), int(it["src_node"][i]), int(it["dst_node"][i])
         assert (int(feas[r, a >> 6]) >> (a & 63)) & 1
-        assert (int(feas[r, b >> 6]) >> (b & 63)) & 1
+        dst_out += not ((int(feas[r, b >> 6]) >> (b & 63)) & 1)
+    assert 0 < dst_out < hyb.shape[0] / 8
