@@ -45,11 +45,13 @@ constexpr int kPlaneWords = kChunks * 16;  // words per 32-rule group
 constexpr int kMatchWaves = 8;
 constexpr int kMatchThreads = kMatchWaves * 64;
 constexpr int kSliceGroups = kMatchThreads;  // one group (32 rules) per lane
-constexpr int kChunk = 256;                  // lookups per match work item and lookup stream (a multiple of 4)
+constexpr int kChunk = 256;                  // lookups per lookup stream of a small table's work item (a multiple of 4)
 constexpr int kMaxChunk = 512;               // lookups per work item at most (<= kMatchThreads)
+constexpr int kItemCap = 192;                // lookups per work item of a table of kSliceGroups groups or more
 constexpr int kQueue = 512;                  // queued filter survivors per wavefront (>= 4 x 64)
 constexpr int kPrepGroups = 128;             // groups per prep workgroup (16 wavefronts x 4 rounds x 2 groups)
 constexpr uint64_t kNoMatch = ~0ull;
+static_assert(kItemCap % 4 == 0 && kItemCap <= kChunk, "an item holds >= kItemCap lookups unless it is its switch's only one");
 static_assert(kChunk % 4 == 0 && kMaxChunk % kChunk == 0 && kMaxChunk <= kMatchThreads,
               "one epilogue thread per lookup");
 constexpr int kCountPad = 32;  // live-trace counters are 128 bytes apart: contended atomics on one line serialise
@@ -356,15 +358,36 @@ __global__ __launch_bounds__(1024) void k_tr_prep(int32_t S, const int32_t *__re
 // trace's rank being that share's base plus its rank in the workgroup;
 // otherwise every trace updates its switch's count itself.  Live-list slots
 // are reserved once per workgroup.
+// A bucketed lookup: the trace, its jurisdiction mask so far and its
+// header, gathered when the trace is bucketed so that the match stages its
+// lookups with contiguous loads.
+struct __align__(16) BRec {
+    int32_t t;
+    uint32_t jm;
+    uint32_t pad[2];
+    pc_key key;
+};
+
+// A live-list entry: a trace in flight, the switch it is at, its rank in
+// that switch's bucket, its jurisdiction mask so far and its header (next
+// = -1: the slot of a trace that has ended).
+struct __align__(16) LRec {
+    int32_t t;
+    int32_t next;
+    int32_t rk;
+    uint32_t jm;
+    pc_key key;
+};
+
 constexpr int kInitThreads = 1024;
 constexpr int kInitRounds = 4;
 constexpr int kInitPer = kInitThreads * kInitRounds;
 constexpr int kInitLdsS = 8192;  // switches counted in LDS at most (32 KB)
 template <bool kLds>
 __global__ __launch_bounds__(kInitThreads) void k_tr_init(int32_t S, const uint8_t *__restrict__ jur,
-                                                          const int32_t *__restrict__ ingress, int32_t T,
-                                                          int32_t *__restrict__ cur, uint32_t *__restrict__ jm,
-                                                          int32_t *__restrict__ hops, int4 *__restrict__ live,
+                                                          const int32_t *__restrict__ ingress,
+                                                          const pc_key *__restrict__ hdr, int32_t T,
+                                                          LRec *__restrict__ live,
                                                           int32_t *__restrict__ nlive,
                                                           int32_t *__restrict__ counts, pc_trace_out *__restrict__ out,
                                                           const int32_t *__restrict__ watch, int32_t K,
@@ -379,6 +402,7 @@ __global__ __launch_bounds__(kInitThreads) void k_tr_init(int32_t S, const uint8
     __syncthreads();
     const int64_t t0 = static_cast<int64_t>(blockIdx.x) * kInitPer;
     int32_t sw[kInitRounds], rk[kInitRounds], slot[kInitRounds];
+    uint32_t jb[kInitRounds];
     bool bad = false;
 #pragma unroll
     for (int k = 0; k < kInitRounds; ++k) {
@@ -386,6 +410,7 @@ __global__ __launch_bounds__(kInitThreads) void k_tr_init(int32_t S, const uint8
         const int32_t t = static_cast<int32_t>(t64);
         sw[k] = -1;
         rk[k] = 0;
+        jb[k] = 0;
         if (t64 < T) {
             const int32_t s = ingress[t];
             if (s < 0 || s >= S) {
@@ -402,13 +427,11 @@ __global__ __launch_bounds__(kInitThreads) void k_tr_init(int32_t S, const uint8
                 if (walk)
                     for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = -1;
             } else {
-                cur[t] = s;
-                jm[t] = jur_bit(jur, s);
+                jb[k] = jur_bit(jur, s);
                 if (visit) visit[t] = watch_bits(watch, K, t, s);
                 if (vsum) vsum[t] = sum_bit(s);
                 if (walk)
                     for (int j = 0; j < kWalkSlots; ++j) walk[static_cast<int64_t>(t) * kWalkSlots + j] = j ? -1 : s;
-                hops[t] = 0;
                 sw[k] = s;
                 if constexpr (kLds) rk[k] = atomicAdd(&lcnt[s], 1);
                 else rk[k] = atomicAdd(&counts[static_cast<int64_t>(s) * kCountPad], 1);
@@ -436,23 +459,37 @@ __global__ __launch_bounds__(kInitThreads) void k_tr_init(int32_t S, const uint8
     for (int k = 0; k < kInitRounds; ++k)
         if (slot[k] >= 0) {
             const int32_t t = static_cast<int32_t>(t0 + k * kInitThreads + threadIdx.x);
-            live[base + slot[k]] = make_int4(t, sw[k], kLds ? lcnt[sw[k]] + rk[k] : rk[k], 0);
+            LRec e;
+            e.t = t;
+            e.next = sw[k];
+            e.rk = kLds ? lcnt[sw[k]] + rk[k] : rk[k];
+            e.jm = jb[k];
+            e.key = hdr[t];
+            live[base + slot[k]] = e;
         }
     if (__ballot(bad) && (threadIdx.x & 63) == 0) atomicOr(d_err, PC_DERR_SWITCH);
 }
 
-// Bucket the live traces by current switch: a live entry (t, switch, rank)
-// puts trace t at slot boff[switch] + rank, its rank having been taken when
-// it was counted.
-__global__ void k_tr_scatter(const int4 *__restrict__ live, const int32_t *__restrict__ nlive, int32_t T,
-                             int32_t S, const int32_t *__restrict__ boff, int32_t *__restrict__ bucket)
+// Bucket the live traces by current switch: a live entry puts its trace at
+// slot boff[switch] + rank, its rank having been taken when it was counted.
+// The list holds *len entries; traces that ended leave entries with switch
+// -1.
+__global__ void k_tr_scatter(const LRec *__restrict__ live, const int32_t *__restrict__ len, int32_t T, int32_t S,
+                             const int32_t *__restrict__ boff, BRec *__restrict__ bucket)
 {
-    const int32_t n = min(*nlive, T);
+    const int32_t n = min(*len, T);
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
-        const int4 e = live[i];
-        if (e.y < 0 || e.y >= S) continue;
+        const int4 e = reinterpret_cast<const int4 *>(live)[2 * i];  // (t, next, rk, jm)
+        if (e.y < 0 || e.y >= S || static_cast<uint32_t>(e.x) >= static_cast<uint32_t>(T)) continue;
         const int32_t pos = boff[e.y] + e.z;
-        if (pos >= 0 && pos < T) bucket[pos] = e.x;
+        if (pos >= 0 && pos < T) {
+            BRec r;
+            r.t = e.x;
+            r.jm = static_cast<uint32_t>(e.w);
+            r.pad[0] = r.pad[1] = 0;
+            r.key = live[i].key;
+            bucket[pos] = r;
+        }
     }
 }
 
@@ -484,18 +521,19 @@ __device__ __forceinline__ void verify_group(uint32_t surv, const pc_rule *grp, 
     }
 }
 
-// Apply the chosen rule (its key, see rule_key) at switch s: returns the
-// terminal state, or -1 when the trace moves on to *next through port *port.
-__device__ __forceinline__ int apply_rule(int32_t S, const int32_t *__restrict__ port_off,
-                                          const int32_t *__restrict__ port_peer, int64_t n_ports, int32_t ttl,
-                                          int32_t s, uint64_t key, int32_t hops, int32_t *next, uint16_t *port)
+// Apply the chosen rule (its key, see rule_key) at a switch of np ports (np
+// < 0: the switch's port range is invalid) whose port a leads to
+// peer_of(a): returns the terminal state, or -1 when the trace moves on to
+// *next through port *port.
+template <class PeerOf>
+__device__ __forceinline__ int apply_key(int32_t S, int32_t ttl, int64_t np, const PeerOf &peer_of, uint64_t key,
+                                         int32_t hops, int32_t *next, uint16_t *port)
 {
     if (key == kNoMatch) return PC_MISS;
     const uint32_t a = static_cast<uint32_t>(key & 0xFFFFu);
     if (a == PC_ACTION_DROP) return PC_DROP;
-    const int64_t pb = port_off[s], pe = port_off[s + 1];
-    if (!pc_range_ok(pb, pe, n_ports) || static_cast<int64_t>(a) >= pe - pb) return PC_MISS;
-    const int32_t peer = port_peer[pb + a];
+    if (np < 0 || static_cast<int64_t>(a) >= np) return PC_MISS;
+    const int32_t peer = peer_of(a);
     if (peer == -1) {
         *port = static_cast<uint16_t>(a);
         return PC_EGRESS;
@@ -505,6 +543,16 @@ __device__ __forceinline__ int apply_rule(int32_t S, const int32_t *__restrict__
     *next = peer;
     *port = static_cast<uint16_t>(a);  // the forwarding port
     return -1;
+}
+
+// The same, with switch s's ports read from port_off / port_peer.
+__device__ __forceinline__ int apply_rule(int32_t S, const int32_t *__restrict__ port_off,
+                                          const int32_t *__restrict__ port_peer, int64_t n_ports, int32_t ttl,
+                                          int32_t s, uint64_t key, int32_t hops, int32_t *next, uint16_t *port)
+{
+    const int64_t pb = port_off[s], pe = port_off[s + 1];
+    const int64_t np = pc_range_ok(pb, pe, n_ports) ? pe - pb : -1;
+    return apply_key(S, ttl, np, [&](uint32_t a) { return port_peer[pb + a]; }, key, hops, next, port);
 }
 
 __device__ __forceinline__ void write_out(pc_trace_out *out, int32_t t, uint32_t jm, int32_t s, uint16_t port,
@@ -528,11 +576,9 @@ struct Level {
     int64_t n_ports;
     const uint8_t *jur;
     int32_t ttl;
-    int32_t *cur;
-    uint32_t *jm;
-    int32_t *hops;
-    int4 *live_next;        // traces still in flight after this level: (t, next switch, rank in its bucket)
-    int32_t *nlive_next;
+    int32_t hops;           // hops every trace of this level has made (the level's index)
+    LRec *live_next;        // one entry per lookup of this level, at its bucket slot (switch -1: the trace ended)
+    int32_t *nlive_next;    // traces in flight after this level
     int32_t *counts_next;   // live traces per switch after this level
     pc_trace_out *out;
     const int32_t *watch;   // [T][K] switches whose visit is recorded
@@ -542,32 +588,54 @@ struct Level {
     int32_t *walk;          // [T][kWalkSlots] walk records or nullptr
 };
 
-// Lookups per match work item of a switch of G groups: kChunk per lookup
-// stream (a table of fewer than kSliceGroups groups leaves wavefronts free
-// for further streams), at most kMaxChunk.
-__device__ __forceinline__ int32_t item_lookups(int32_t G)
+// Lookups per match work item of a switch of G groups with n lookups in
+// this level: the switch's lookups split evenly (in multiples of 4) over as
+// few items as hold at most kItemCap each, where a table of fewer than
+// kSliceGroups groups, which leaves wavefronts free for further lookup
+// streams, takes kChunk per stream (at most kMaxChunk).
+__device__ __forceinline__ int32_t item_lookups(int32_t G, int32_t n)
 {
     const int32_t gws = G >= kSliceGroups ? kMatchWaves : max(1, (G + 63) / 64);
-    return min(kMaxChunk, kChunk * (kMatchWaves / gws));
+    const int32_t cap = gws == kMatchWaves ? kItemCap : min(kMaxChunk, kChunk * (kMatchWaves / gws));
+    const int32_t items = max(1, (n + cap - 1) / cap);
+    return max(4, ((n + items - 1) / items + 3) & ~3);
 }
 
 // Per level: bucket offsets boff = exclusive scan of counts (which are
-// cleared for reuse) and work-item offsets ioff = exclusive scan of
-// ceil(counts / item_lookups(G)); one workgroup of 1024 threads.
+// cleared for reuse), work-item offsets ioff = exclusive scan of
+// ceil(counts / item_lookups(G, counts)), *total = the level's lookups (the
+// length of the live list its match writes), and *nlive_next = 0 for the
+// match to count the traces that move on.  One workgroup of 1024 threads;
+// each thread takes kPlanPer consecutive switches per pass, so a pass
+// covers 4,096 switches with all of its loads in flight together.
+constexpr int kPlanPer = 4;
 __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, int32_t S, int32_t *__restrict__ boff,
-                                                  int32_t *__restrict__ ioff, const int32_t *__restrict__ gcount)
+                                                  int32_t *__restrict__ ioff, const int32_t *__restrict__ gcount,
+                                                  int32_t *__restrict__ total, int32_t *__restrict__ nlive_next)
 {
     __shared__ int32_t wsum[2][16];
     __shared__ int32_t carry_s[2];
     const int tid = threadIdx.x, lane = tid & 63, wid = tid >> 6;
     if (tid < 2) carry_s[tid] = 0;
+    if (tid == 0) *nlive_next = 0;
     __syncthreads();
-    for (int32_t base = 0; base < S; base += 1024) {
-        const int32_t i = base + tid;
-        const int32_t v0 = i < S ? counts[static_cast<int64_t>(i) * kCountPad] : 0;
-        const int32_t ch = i < S ? item_lookups(gcount[i]) : kChunk;
-        const int32_t v1 = (v0 + ch - 1) / ch;
-        int32_t x0 = v0, x1 = v1;
+    for (int32_t base = 0; base < S; base += 1024 * kPlanPer) {
+        const int32_t i0 = base + tid * kPlanPer;
+        int32_t v0[kPlanPer], g[kPlanPer], v1[kPlanPer];
+#pragma unroll
+        for (int k = 0; k < kPlanPer; ++k) {
+            v0[k] = i0 + k < S ? counts[static_cast<int64_t>(i0 + k) * kCountPad] : 0;
+            g[k] = i0 + k < S ? gcount[i0 + k] : 0;
+        }
+        int32_t s0 = 0, s1 = 0;
+#pragma unroll
+        for (int k = 0; k < kPlanPer; ++k) {
+            const int32_t ch = item_lookups(g[k], v0[k]);
+            v1[k] = (v0[k] + ch - 1) / ch;
+            s0 += v0[k];
+            s1 += v1[k];
+        }
+        int32_t x0 = s0, x1 = s1;
 #pragma unroll
         for (int off = 1; off < 64; off <<= 1) {
             const int32_t y0 = __shfl_up(x0, off, 64), y1 = __shfl_up(x1, off, 64);
@@ -592,11 +660,17 @@ __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, 
         }
         __syncthreads();
         const int32_t c0 = carry_s[0], c1 = carry_s[1];
-        if (i < S) {
-            boff[i] = c0 + (wid ? wsum[0][wid - 1] : 0) + x0 - v0;
-            ioff[i] = c1 + (wid ? wsum[1][wid - 1] : 0) + x1 - v1;
-            counts[static_cast<int64_t>(i) * kCountPad] = 0;
-        }
+        int32_t e0 = c0 + (wid ? wsum[0][wid - 1] : 0) + x0 - s0;
+        int32_t e1 = c1 + (wid ? wsum[1][wid - 1] : 0) + x1 - s1;
+#pragma unroll
+        for (int k = 0; k < kPlanPer; ++k)
+            if (i0 + k < S) {
+                boff[i0 + k] = e0;
+                ioff[i0 + k] = e1;
+                counts[static_cast<int64_t>(i0 + k) * kCountPad] = 0;
+                e0 += v0[k];
+                e1 += v1[k];
+            }
         __syncthreads();
         if (tid == 0) {
             carry_s[0] = c0 + wsum[0][15];
@@ -607,6 +681,7 @@ __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, 
     if (tid == 0) {
         boff[S] = carry_s[0];
         ioff[S] = carry_s[1];
+        *total = carry_s[0];
     }
 }
 
@@ -669,22 +744,30 @@ __device__ __forceinline__ void filter_quad(const uint32_t (&x)[kChunks][4], con
 }
 #undef PC_IDX
 
-// One workgroup per work item = (switch, chunk of at most item_lookups(G)
+// One workgroup per work item = (switch, chunk of at most item_lookups(G, n)
 // lookups of its bucket).  Items are dealt to XCDs in contiguous ranges, so
 // the chunks of one switch share an L2.
 __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     int32_t S, const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules,
     const int32_t *__restrict__ gcount, const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
-    const pc_key *__restrict__ hdr, const int32_t *__restrict__ boff, const int32_t *__restrict__ ioff,
-    const int32_t *__restrict__ bucket, const uint32_t *__restrict__ cpos, Level lv)
+    const int32_t *__restrict__ boff, const int32_t *__restrict__ ioff, const BRec *__restrict__ bucket,
+    const uint32_t *__restrict__ cpos, Level lv)
 {
     __shared__ uint64_t best[kMaxChunk];
     __shared__ __align__(16) uint32_t cidx[kChunks][kMaxChunk];  // each lookup's values of the switch's filter chunks
     __shared__ __align__(16) pc_key keys[kMaxChunk];
     __shared__ int32_t tids[kMaxChunk];
-    __shared__ int32_t thops[kMaxChunk];  // each lookup's trace: hops so far and jurisdiction mask
-    __shared__ uint32_t tjm[kMaxChunk];
+    __shared__ uint32_t tjm[kMaxChunk];  // each lookup's trace: jurisdiction mask so far
     __shared__ uint2 queue[kMatchWaves][kQueue];  // per wavefront: (survivor set, lookup << 6 | lane)
+    // the switch's first kPortSlots ports: peer, the peer's jurisdiction
+    // bit, and the item's traces that leave through the port (count, then
+    // the base of their ranks in the peer's bucket)
+    __shared__ int32_t ppeer[kPortSlots], pcnt[kPortSlots], pbase[kPortSlots];
+    __shared__ uint32_t pjb[kPortSlots];
+    // the item's live entries are ordered by forwarding port: port p's run
+    // starts at prun[p], the run of the other ports at prun[kPortSlots]
+    __shared__ int32_t prun[kPortSlots + 1];
+    __shared__ int32_t nother, nmove;  // traces leaving through the other ports; all that move on
     // the grid was sized from an upper bound on the item count: blocks past
     // the real count's per-XCD share return at once
     const int32_t n_items = ioff[S];
@@ -701,7 +784,7 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         else hi = mid;
     }
     const int32_t s = lo;
-    const int32_t chunk = item_lookups(gcount[s]);
+    const int32_t chunk = item_lookups(gcount[s], boff[s + 1] - boff[s]);
     const int32_t bb = boff[s] + (item - ioff[s]) * chunk;
     const int32_t tn = min(chunk, min(boff[s + 1], lv.T) - bb);  // bucket holds at most T entries
     if (tn <= 0) return;
@@ -725,21 +808,34 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     const int32_t per_stream = (nquads + streams - 1) / streams;
     const int32_t jb = st < streams ? min(tn4, 4 * st * per_stream) : tn4;
     const int32_t je = st < streams ? min(tn4, 4 * (st + 1) * per_stream) : tn4;
+    // the switch's ports (np < 0: its port range is invalid)
+    const int64_t pb = lv.port_off[s], pe = lv.port_off[s + 1];
+    const int64_t np = pc_range_ok(pb, pe, lv.n_ports) ? pe - pb : -1;
+    if (threadIdx.x < kPortSlots) {
+        int32_t pp = -2;
+        uint32_t jbit = 0;
+        if (static_cast<int64_t>(threadIdx.x) < np) {
+            pp = lv.port_peer[pb + threadIdx.x];
+            if (pp >= 0 && pp < lv.S) jbit = jur_bit(lv.jur, pp);
+        }
+        ppeer[threadIdx.x] = pp;
+        pjb[threadIdx.x] = jbit;
+        pcnt[threadIdx.x] = 0;
+        if (threadIdx.x == 0) nother = 0;
+    }
     // stage the chunk; pad to a multiple of 4 lookups with copies of the last
     for (int i = threadIdx.x; i < tn4; i += kMatchThreads) {
-        int32_t t = bucket[bb + min(i, tn - 1)];
-        if (static_cast<uint32_t>(t) >= static_cast<uint32_t>(lv.T)) t = -1;  // not a trace id: skipped
-        pc_key h = {};
-        int32_t hp = 0;
-        uint32_t jmv = 0;
-        if (t >= 0) {
-            h = hdr[t];
-            hp = lv.hops[t];
-            jmv = lv.jm[t];
+        const BRec r = bucket[bb + min(i, tn - 1)];
+        int32_t t = r.t;
+        pc_key h = r.key;
+        uint32_t jmv = r.jm;
+        if (static_cast<uint32_t>(t) >= static_cast<uint32_t>(lv.T)) {  // not a trace id: skipped
+            t = -1;
+            h = pc_key{};
+            jmv = 0;
         }
         tids[i] = t;
         keys[i] = h;
-        thops[i] = hp;
         tjm[i] = jmv;
         best[i] = kNoMatch;
 #pragma unroll
@@ -829,54 +925,83 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
             __builtin_amdgcn_wave_barrier();
         }
     }
-    // per forwarding port of this switch (the first kPortSlots): the item's
-    // traces that leave through it, then one count update of its peer
-    __shared__ int32_t pcnt[kPortSlots], pbase[kPortSlots];
-    __shared__ int32_t nmove, mbase;
-    if (threadIdx.x == 0) nmove = 0;
-    if (threadIdx.x < kPortSlots) pcnt[threadIdx.x] = 0;
+    // every wavefront's matches are in best[] (a lookup's matches come from
+    // the wavefronts that hold its groups, its epilogue thread may be another)
     __syncthreads();
-    // apply the first match, then count and list the traces that move on
-    // (one global reservation of live-list slots per workgroup, one count
-    // update per next switch and workgroup; a trace's rank in its next
-    // switch's bucket is its count's base plus its rank in the item)
-    int32_t slot = -1, t = -1, lrank = -1, next = -1, rk = 0;
+    // apply the first match.  A trace that moves on is counted in its next
+    // switch's bucket (one count update per forwarding port and workgroup;
+    // its rank there is the port's base plus its rank in the item) and gets
+    // an entry in the item's share of the live list, grouped by port so that
+    // the bucketing pass writes runs; the slots after the item's moving
+    // traces are marked as ended (switch -1).
+    const int32_t h = lv.hops;
+    int32_t t = -1, lrank = -1, orank = -1, next = -1, rk = 0;
+    uint32_t jm_next = 0;
     uint16_t port = PC_NO_PORT;
     if (threadIdx.x < tn) {  // tn <= kMaxChunk <= kMatchThreads
         t = tids[threadIdx.x];
         if (t >= 0) {
-            const int32_t h = thops[threadIdx.x];
             const uint32_t jmv = tjm[threadIdx.x];
-            const int state = apply_rule(lv.S, lv.port_off, lv.port_peer, lv.n_ports, lv.ttl, s, best[threadIdx.x],
-                                         h, &next, &port);
+            const int state = apply_key(
+                lv.S, lv.ttl, np,
+                [&](uint32_t a) { return a < kPortSlots ? ppeer[a] : lv.port_peer[pb + a]; },
+                best[threadIdx.x], h, &next, &port);
             if (state >= 0) {
                 write_out(lv.out, t, jmv, s, port, h, state);
+                t = -1;
             } else {
-                lv.cur[t] = next;
-                lv.hops[t] = h + 1;
-                lv.jm[t] = jmv | jur_bit(lv.jur, next);
+                jm_next = jmv | (port < kPortSlots ? pjb[port] : jur_bit(lv.jur, next));
                 if (lv.visit) lv.visit[t] |= watch_bits(lv.watch, lv.K, t, next);
                 if (lv.vsum) lv.vsum[t] |= sum_bit(next);
                 if (lv.walk && h + 1 < kWalkSlots) lv.walk[static_cast<int64_t>(t) * kWalkSlots + h + 1] = next;
-                if (port < kPortSlots) lrank = atomicAdd(&pcnt[port], 1);
-                else rk = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
-                slot = atomicAdd(&nmove, 1);
+                if (port < kPortSlots) {
+                    lrank = atomicAdd(&pcnt[port], 1);
+                } else {
+                    rk = atomicAdd(&lv.counts_next[static_cast<int64_t>(next) * kCountPad], 1);
+                    orank = atomicAdd(&nother, 1);
+                }
             }
         }
     }
     __syncthreads();
-    if (threadIdx.x == 0) mbase = nmove ? atomicAdd(lv.nlive_next, nmove) : 0;
+    static_assert(kPortSlots == 64, "one wavefront scans the port counts");
     if (threadIdx.x < kPortSlots) {
         const int32_t c = pcnt[threadIdx.x];
         // a port some trace forwarded through: its peer is a valid switch
-        if (c > 0) {
-            const int32_t peer = lv.port_peer[lv.port_off[s] + threadIdx.x];
-            pbase[threadIdx.x] = atomicAdd(&lv.counts_next[static_cast<int64_t>(peer) * kCountPad], c);
+        if (c > 0) pbase[threadIdx.x] = atomicAdd(&lv.counts_next[static_cast<int64_t>(ppeer[threadIdx.x]) * kCountPad], c);
+        int32_t x = c;
+#pragma unroll
+        for (int off = 1; off < 64; off <<= 1) {
+            const int32_t y = __shfl_up(x, off, 64);
+            if (lane >= off) x += y;
+        }
+        prun[threadIdx.x] = x - c;
+        if (threadIdx.x == kPortSlots - 1) {
+            prun[kPortSlots] = x;
+            const int32_t m = x + nother;
+            nmove = m;
+            if (m) atomicAdd(lv.nlive_next, m);  // the traces in flight after this level
         }
     }
     __syncthreads();
-    if (lrank >= 0) rk = pbase[port] + lrank;
-    if (slot >= 0 && mbase + slot < lv.T) lv.live_next[mbase + slot] = make_int4(t, next, rk, 0);
+    int32_t slot = -1;
+    if (lrank >= 0) {
+        rk = pbase[port] + lrank;
+        slot = prun[port] + lrank;
+    } else if (orank >= 0) {
+        slot = prun[kPortSlots] + orank;
+    }
+    if (slot >= 0) {
+        LRec e;
+        e.t = t;
+        e.next = next;
+        e.rk = rk;
+        e.jm = jm_next;
+        e.key = keys[threadIdx.x];
+        lv.live_next[bb + slot] = e;
+    }
+    if (threadIdx.x >= nmove && threadIdx.x < tn)
+        *reinterpret_cast<int4 *>(lv.live_next + bb + threadIdx.x) = make_int4(-1, -1, 0, 0);
 }
 
 // Sparse tail: one workgroup per trace still in flight walks it to its end,
@@ -888,24 +1013,25 @@ __global__ __launch_bounds__(256) void k_tr_walk(int32_t S, const int32_t *__res
                                                  const uint8_t *__restrict__ jur, const int32_t *__restrict__ rule_off,
                                                  const pc_rule *__restrict__ rules, const int32_t *__restrict__ gcount,
                                                  const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
-                                                 const pc_key *__restrict__ hdr, int32_t ttl,
-                                                 const int4 *__restrict__ live, const int32_t *__restrict__ nlive,
-                                                 const int32_t *__restrict__ cur, const uint32_t *__restrict__ jm0,
-                                                 const int32_t *__restrict__ hops0, pc_trace_out *__restrict__ out,
+                                                 int32_t ttl,
+                                                 const LRec *__restrict__ live, const int32_t *__restrict__ len,
+                                                 int32_t hops0, pc_trace_out *__restrict__ out,
                                                  const int32_t *__restrict__ watch, int32_t K,
                                                  uint32_t *__restrict__ visit, uint64_t *__restrict__ vsum,
                                                  int32_t *__restrict__ walk, const uint32_t *__restrict__ cpos)
 {
     __shared__ unsigned long long best;
-    const int32_t n = *nlive;
+    const int32_t n = *len;
     for (int32_t i = blockIdx.x; i < n; i += gridDim.x) {
-        const int32_t t = live[i].x;
-        const pc_key h = hdr[t];
-        int32_t s = cur[t];
-        uint32_t jm = jm0[t];
+        const LRec e = live[i];
+        if (e.next < 0 || e.next >= S) continue;  // the slot of a trace that has ended
+        const int32_t t = e.t;
+        const pc_key h = e.key;
+        int32_t s = e.next;
+        uint32_t jm = e.jm;
         uint32_t vis = visit ? visit[t] : 0u;
         uint64_t vs = vsum ? vsum[t] : 0ull;
-        int32_t hops = hops0[t];
+        int32_t hops = hops0;
         for (;;) {
             if (threadIdx.x == 0) best = kNoMatch;
             __syncthreads();
@@ -1122,9 +1248,9 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
 {
     struct Bufs {
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
-        int32_t *cur, *hops, *bucket;
-        int4 *live0, *live1;
-        uint32_t *jm, *filt, *cpos, *hh;
+        BRec *bucket;
+        LRec *live0, *live1;
+        uint32_t *filt, *cpos, *hh;
     } B;
     auto carve = [&](Carver &c) {
         B.cpos = c.take<uint32_t>(S + 1);
@@ -1137,12 +1263,9 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         B.counts1 = c.take<int32_t>(static_cast<size_t>(S + 1) * kCountPad);
         B.boff = c.take<int32_t>(S + 1);
         B.ioff = c.take<int32_t>(S + 1);
-        B.cur = c.take<int32_t>(T + 1);
-        B.hops = c.take<int32_t>(T + 1);
-        B.live0 = c.take<int4>(T + 1);
-        B.live1 = c.take<int4>(T + 1);
-        B.bucket = c.take<int32_t>(T + 1);
-        B.jm = c.take<uint32_t>(T + 1);
+        B.live0 = c.take<LRec>(T + 1);
+        B.live1 = c.take<LRec>(T + 1);
+        B.bucket = c.take<BRec>(T + 1);
     };
     Carver dry{nullptr, 0};
     carve(dry);
@@ -1201,7 +1324,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     if (!visit) K = 0;
 
     // ---- level-synchronous walk
-    int32_t *d_n = ctx->d_small;  // [0], [1]: live counts of the two live lists
+    int32_t *d_n = ctx->d_small;  // [0], [1]: live counts of the two live lists ([4], [5]: the reach kernels')
     launch_fill_u32(reinterpret_cast<uint32_t *>(d_n), 2, 0, stream);
     if (S > 0) {
         launch_fill_u32(reinterpret_cast<uint32_t *>(B.counts0), static_cast<size_t>(S + 1) * kCountPad, 0, stream);
@@ -1212,18 +1335,17 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         if (S <= kInitLdsS)
             PC_TIMED(ctx, "k_tr_init", stream,
                      hipLaunchKernelGGL(k_tr_init<true>, ig, dim3(kInitThreads), static_cast<size_t>(S) * 4, stream, S,
-                                        jur, ingress, T, B.cur, B.jm, B.hops, B.live0, d_n, B.counts0, out, watch, K,
-                                        visit, vsum, walk, ctx->d_err));
+                                        jur, ingress, hdr, T, B.live0, d_n, B.counts0, out, watch, K, visit, vsum,
+                                        walk, ctx->d_err));
         else
             PC_TIMED(ctx, "k_tr_init", stream,
-                     hipLaunchKernelGGL(k_tr_init<false>, ig, dim3(kInitThreads), 0, stream, S, jur, ingress, T, B.cur,
-                                        B.jm, B.hops, B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk,
-                                        ctx->d_err));
+                     hipLaunchKernelGGL(k_tr_init<false>, ig, dim3(kInitThreads), 0, stream, S, jur, ingress, hdr, T,
+                                        B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk, ctx->d_err));
     }
     PC_LAUNCH_CHECK(ctx);
     PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
     PC_HIP(ctx, hipStreamSynchronize(stream));
-    int4 *live_cur = B.live0, *live_nxt = B.live1;
+    LRec *live_cur = B.live0, *live_nxt = B.live1;
     int32_t *cnt_cur = B.counts0, *cnt_nxt = B.counts1;
     int32_t *n_cur = d_n, *n_nxt = d_n + 1;
     // Levels with few traces in flight are cheaper as independent walks than
@@ -1237,35 +1359,41 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     // device.  The count entering level L is copied back after level L - 1
     // and waited for (an event one level behind) while level L runs.
     int32_t *h_cnt = ctx->h_small + 8;  // two pinned slots, by level parity
-    int64_t known = ctx->h_small[0];    // an upper bound on the count entering the next level
+    int32_t *d_len = ctx->d_small + 6;  // two slots, by level parity: each level's lookups (its live list's length)
+    // An upper bound on the count entering the next level; from level 1 on,
+    // also the exact length of the live list the previous level wrote (every
+    // lookup of a level leaves an entry, the traces that ended included).
+    int64_t known = ctx->h_small[0];
     for (int level = 0;; ++level) {
         if (level > ttl + 2)
             return pc_set_error(ctx, PC_EDEVICE, "pc_trace_flows: level loop exceeded ttl+2 levels");
         if (known == 0) break;
+        // the live list this level reads: from k_tr_init (as many entries as
+        // traces in flight) or from the previous level's match
+        const int32_t *len_cur = level == 0 ? n_cur : d_len + ((level - 1) & 1);
         if (known <= walk_max) {
             const unsigned wb = static_cast<unsigned>(known < 8192 ? known : 8192);
             PC_TIMED(ctx, "k_tr_walk", stream,
                      hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
-                                        rule_off, rules, B.gcount, B.gofs, B.filt, hdr, ttl, live_cur, n_cur, B.cur,
-                                        B.jm, B.hops, out, watch, K, visit, vsum, walk, B.cpos));
+                                        rule_off, rules, B.gcount, B.gofs, B.filt, ttl, live_cur, len_cur, level,
+                                        out, watch, K, visit, vsum, walk, B.cpos));
             PC_LAUNCH_CHECK(ctx);
             break;
         }
         const int32_t nlive = static_cast<int32_t>(known);
         PC_TIMED(ctx, "k_tr_plan", stream,
                  hipLaunchKernelGGL(k_tr_plan, dim3(1), dim3(1024), 0, stream, cnt_cur, S, B.boff, B.ioff,
-                                    B.gcount));
+                                    B.gcount, d_len + (level & 1), n_nxt));
         PC_TIMED(ctx, "k_tr_scatter", stream,
-                 hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, n_cur, T,
-                                    S, B.boff, B.bucket));
-        launch_fill_u32(reinterpret_cast<uint32_t *>(n_nxt), 1, 0, stream);
-        const Level lv{S,     T,     port_off, port_peer, n_ports, jur,   ttl, B.cur, B.jm,
-                       B.hops, live_nxt, n_nxt,    cnt_nxt, out, watch, K,  visit, vsum, walk};
-        // at most nlive / kChunk + (switches with a partial chunk) items
-        const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kChunk + S, nlive);  // item >= kChunk
+                 hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, len_cur,
+                                    T, S, B.boff, B.bucket));
+        const Level lv{S,     T,     port_off, port_peer, n_ports, jur,  ttl,  level,
+                       live_nxt, n_nxt,  cnt_nxt,  out,       watch,   K,    visit, vsum, walk};
+        // at most nlive / kItemCap + S items: a switch of n lookups takes ceil(n / cap) items with cap >= kItemCap
+        const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kItemCap + S, nlive);
         PC_TIMED(ctx, "k_tr_match", stream,
                  hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(8 * ((max_items + 7) / 8))),
-                                    dim3(kMatchThreads), 0, stream, S, rule_off, rules, B.gcount, B.gofs, B.filt, hdr,
+                                    dim3(kMatchThreads), 0, stream, S, rule_off, rules, B.gcount, B.gofs, B.filt,
                                     B.boff, B.ioff, B.bucket, B.cpos, lv));
         PC_LAUNCH_CHECK(ctx);
         // the count leaving this level
