@@ -11,22 +11,31 @@
 // include/pc.h.
 //
 // Design (gfx950):
-//   prep   : per 32-rule group, for each of kChunks 4-bit chunks of header
-//            word 2 (ports) and each of the 16 chunk values, the 32-bit set
-//            of rules whose mask/value admit that chunk value (per-rule
-//            admit sets from an LDS table, then a bit transpose across the
-//            half-wavefront).  Stored plane-major per switch so a wavefront
-//            loads 64 groups with coalesced reads.  Also validates ports,
-//            jurisdictions, offsets and actions (the data-error sweep).
+//   prep   : per switch, kChunks 4-bit chunks of the 104-bit key chosen from
+//            a sample of its rules and of the headers (the chunks on which
+//            its rules discriminate most among the headers seen); per
+//            32-rule group, for each chunk and each of the 16 chunk values,
+//            the 32-bit set of rules whose mask/value admit that value (per-
+//            rule admit sets from an LDS table, then a bit transpose across
+//            the half-wavefront).  Stored plane-major per switch so a
+//            wavefront loads 64 groups with coalesced reads.  Also validates
+//            ports, jurisdictions, offsets and actions (the data-error sweep).
 //   levels : level-synchronous walk.  Live traces are bucketed by their
-//            current switch (count -> scan -> scatter); one workgroup per
-//            switch keeps the switch's chunk sets in VGPRs (16,384 rules per
-//            8-wave slice) and filters every lookup of its bucket with
+//            current switch: a plan pass scans the per-switch counts, a
+//            scatter pass writes each trace's 32-byte bucket record (trace,
+//            jurisdiction mask, header) at its switch's offset plus its
+//            rank.  One workgroup per work item (a switch and a balanced
+//            share of its bucket) keeps the switch's chunk sets in VGPRs
+//            (8,192 rules per 4-wave slice) and filters every lookup with
 //            kChunks uniform-index register reads and ANDs; the rare
 //            survivors are verified against the full 104-bit rule and the
 //            first match is the minimum of (0xFFFF - priority, index) over
-//            the workgroup (LDS 64-bit atomic min).  An advance pass applies
-//            the action and re-buckets the traces still in flight.
+//            the workgroup (LDS 64-bit atomic min).  The same workgroup then
+//            applies the match with the switch's ports staged in LDS, counts
+//            the moving traces per forwarding port (one count update per
+//            port and workgroup, which also gives each trace its rank in its
+//            next switch's bucket) and writes their live-list entries in its
+//            own share of the list, grouped by port.
 //   tail   : once few traces are left in flight, one workgroup per trace
 //            walks it to its end, reading only the chunk-set words its
 //            header selects.
@@ -42,11 +51,11 @@ constexpr int kChunks = 6;                 // 4-bit chunks of the key used by th
 constexpr int kKeyNibbles = 26;            // the 104-bit key: 8 nibbles in each of w0..w2, 2 in w3's low byte
 constexpr int kChooseSample = 512;         // rules per switch sampled to choose its filter chunks
 constexpr int kPlaneWords = kChunks * 16;  // words per 32-rule group
-constexpr int kMatchWaves = 8;
+constexpr int kMatchWaves = 4;
 constexpr int kMatchThreads = kMatchWaves * 64;
 constexpr int kSliceGroups = kMatchThreads;  // one group (32 rules) per lane
 constexpr int kChunk = 256;                  // lookups per lookup stream of a small table's work item (a multiple of 4)
-constexpr int kMaxChunk = 512;               // lookups per work item at most (<= kMatchThreads)
+constexpr int kMaxChunk = 256;               // lookups per work item at most (<= kMatchThreads)
 constexpr int kItemCap = 192;                // lookups per work item of a table of kSliceGroups groups or more
 constexpr int kQueue = 512;                  // queued filter survivors per wavefront (>= 4 x 64)
 constexpr int kPrepGroups = 128;             // groups per prep workgroup (16 wavefronts x 4 rounds x 2 groups)
@@ -122,6 +131,19 @@ __global__ void k_tr_port_check(int64_t n_ports, const int32_t *__restrict__ por
         bad |= (v < -1 || v >= S);
     }
     if (bad) atomicOr(d_err, PC_DERR_SWITCH);
+}
+
+// Per port: its peer and the peer's jurisdiction bit (0 unless the peer is a
+// switch), read by the match with one load per port.
+__global__ void k_tr_port_info(int64_t n_ports, const int32_t *__restrict__ port_peer, int32_t S,
+                               const uint8_t *__restrict__ jur, int2 *__restrict__ pinfo)
+{
+    for (int64_t p = blockIdx.x * static_cast<int64_t>(blockDim.x) + threadIdx.x; p < n_ports;
+         p += static_cast<int64_t>(gridDim.x) * blockDim.x) {
+        const int32_t v = port_peer[p];
+        const uint32_t j = v >= 0 && v < S ? jur[v] : 32u;
+        pinfo[p] = make_int2(v, j < 32 ? static_cast<int32_t>(1u << j) : 0);
+    }
 }
 
 // Histogram of the headers' nibble values over a strided sample of at most
@@ -573,6 +595,7 @@ struct Level {
     int32_t T;              // capacity of the live list
     const int32_t *port_off;
     const int32_t *port_peer;
+    const int2 *pinfo;      // per port: (peer, the peer's jurisdiction bit)
     int64_t n_ports;
     const uint8_t *jur;
     int32_t ttl;
@@ -811,18 +834,6 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     // the switch's ports (np < 0: its port range is invalid)
     const int64_t pb = lv.port_off[s], pe = lv.port_off[s + 1];
     const int64_t np = pc_range_ok(pb, pe, lv.n_ports) ? pe - pb : -1;
-    if (threadIdx.x < kPortSlots) {
-        int32_t pp = -2;
-        uint32_t jbit = 0;
-        if (static_cast<int64_t>(threadIdx.x) < np) {
-            pp = lv.port_peer[pb + threadIdx.x];
-            if (pp >= 0 && pp < lv.S) jbit = jur_bit(lv.jur, pp);
-        }
-        ppeer[threadIdx.x] = pp;
-        pjb[threadIdx.x] = jbit;
-        pcnt[threadIdx.x] = 0;
-        if (threadIdx.x == 0) nother = 0;
-    }
     // stage the chunk; pad to a multiple of 4 lookups with copies of the last
     for (int i = threadIdx.x; i < tn4; i += kMatchThreads) {
         const BRec r = bucket[bb + min(i, tn - 1)];
@@ -840,6 +851,13 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         best[i] = kNoMatch;
 #pragma unroll
         for (int c = 0; c < kChunks; ++c) cidx[c][i] = key_nibble(h.w[0], h.w[1], h.w[2], h.w[3], chunk_pos(cp, c));
+    }
+    if (threadIdx.x < kPortSlots) {
+        const int2 pi = static_cast<int64_t>(threadIdx.x) < np ? lv.pinfo[pb + threadIdx.x] : make_int2(-2, 0);
+        ppeer[threadIdx.x] = pi.x;
+        pjb[threadIdx.x] = static_cast<uint32_t>(pi.y);
+        pcnt[threadIdx.x] = 0;
+        if (threadIdx.x == 0) nother = 0;
     }
     __syncthreads();
     // one slice of kSliceGroups groups at a time, one group per lane,
@@ -1250,6 +1268,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
         BRec *bucket;
         LRec *live0, *live1;
+        int2 *pinfo;
         uint32_t *filt, *cpos, *hh;
     } B;
     auto carve = [&](Carver &c) {
@@ -1266,6 +1285,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         B.live0 = c.take<LRec>(T + 1);
         B.live1 = c.take<LRec>(T + 1);
         B.bucket = c.take<BRec>(T + 1);
+        B.pinfo = c.take<int2>(static_cast<size_t>(n_ports) + 1);
     };
     Carver dry{nullptr, 0};
     carve(dry);
@@ -1322,6 +1342,12 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         PC_LAUNCH_CHECK(ctx);
     }
     if (!visit) K = 0;
+    if (n_ports > 0) {
+        PC_TIMED(ctx, "k_tr_port_info", stream,
+                 hipLaunchKernelGGL(k_tr_port_info, dim3(static_cast<unsigned>(std::min<int64_t>((n_ports + 255) / 256, 4096))),
+                                    dim3(256), 0, stream, n_ports, port_peer, S, jur, B.pinfo));
+        PC_LAUNCH_CHECK(ctx);
+    }
 
     // ---- level-synchronous walk
     int32_t *d_n = ctx->d_small;  // [0], [1]: live counts of the two live lists ([4], [5]: the reach kernels')
@@ -1387,8 +1413,8 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         PC_TIMED(ctx, "k_tr_scatter", stream,
                  hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, len_cur,
                                     T, S, B.boff, B.bucket));
-        const Level lv{S,     T,     port_off, port_peer, n_ports, jur,  ttl,  level,
-                       live_nxt, n_nxt,  cnt_nxt,  out,       watch,   K,    visit, vsum, walk};
+        const Level lv{S,        T,     port_off, port_peer, B.pinfo, n_ports, jur,   ttl,  level,
+                       live_nxt, n_nxt, cnt_nxt,  out,       watch,   K,       visit, vsum, walk};
         // at most nlive / kItemCap + S items: a switch of n lookups takes ceil(n / cap) items with cap >= kItemCap
         const int64_t max_items = std::min<int64_t>(static_cast<int64_t>(nlive) / kItemCap + S, nlive);
         PC_TIMED(ctx, "k_tr_match", stream,
