@@ -495,10 +495,22 @@ __global__ __launch_bounds__(kInitThreads) void k_tr_init(int32_t S, const uint8
 // Bucket the live traces by current switch: a live entry puts its trace at
 // slot boff[switch] + rank, its rank having been taken when it was counted.
 // The list holds *len entries; traces that ended leave entries with switch
-// -1.
+// -1.  Also maps each match work item to (its switch, its index among the
+// switch's items): the switch is the last s with ioff[s] <= item.
 __global__ void k_tr_scatter(const LRec *__restrict__ live, const int32_t *__restrict__ len, int32_t T, int32_t S,
-                             const int32_t *__restrict__ boff, BRec *__restrict__ bucket)
+                             const int32_t *__restrict__ boff, BRec *__restrict__ bucket,
+                             const int32_t *__restrict__ ioff, int2 *__restrict__ imap, int32_t icap)
 {
+    const int32_t n_items = min(ioff[S], icap);
+    for (int32_t it = blockIdx.x * blockDim.x + threadIdx.x; it < n_items; it += gridDim.x * blockDim.x) {
+        int32_t lo = 0, hi = S;
+        while (hi - lo > 1) {
+            const int32_t mid = (lo + hi) >> 1;
+            if (ioff[mid] <= it) lo = mid;
+            else hi = mid;
+        }
+        imap[it] = make_int2(lo, it - ioff[lo]);
+    }
     const int32_t n = min(*len, T);
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < n; i += gridDim.x * blockDim.x) {
         const int4 e = reinterpret_cast<const int4 *>(live)[2 * i];  // (t, next, rk, jm)
@@ -773,8 +785,8 @@ __device__ __forceinline__ void filter_quad(const uint32_t (&x)[kChunks][4], con
 __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     int32_t S, const int32_t *__restrict__ rule_off, const pc_rule *__restrict__ rules,
     const int32_t *__restrict__ gcount, const int32_t *__restrict__ gofs, const uint32_t *__restrict__ filt,
-    const int32_t *__restrict__ boff, const int32_t *__restrict__ ioff, const BRec *__restrict__ bucket,
-    const uint32_t *__restrict__ cpos, Level lv)
+    const int32_t *__restrict__ boff, const int32_t *__restrict__ ioff, const int2 *__restrict__ imap,
+    const BRec *__restrict__ bucket, const uint32_t *__restrict__ cpos, Level lv)
 {
     __shared__ uint64_t best[kMaxChunk];
     __shared__ __align__(16) uint32_t cidx[kChunks][kMaxChunk];  // each lookup's values of the switch's filter chunks
@@ -799,16 +811,12 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     if (kx >= per) return;
     const int32_t item = static_cast<int32_t>(blockIdx.x & 7) * per + kx;
     if (item >= n_items) return;
-    // switch owning the item: largest s with ioff[s] <= item
-    int32_t lo = 0, hi = S;
-    while (hi - lo > 1) {
-        const int32_t mid = (lo + hi) >> 1;
-        if (ioff[mid] <= item) lo = mid;
-        else hi = mid;
-    }
-    const int32_t s = lo;
+    // the item's switch and its index among the switch's items
+    const int2 im = imap[item];
+    const int32_t s = im.x;
+    if (static_cast<uint32_t>(s) >= static_cast<uint32_t>(S)) return;
     const int32_t chunk = item_lookups(gcount[s], boff[s + 1] - boff[s]);
-    const int32_t bb = boff[s] + (item - ioff[s]) * chunk;
+    const int32_t bb = boff[s] + im.y * chunk;
     const int32_t tn = min(chunk, min(boff[s + 1], lv.T) - bb);  // bucket holds at most T entries
     if (tn <= 0) return;
     const int32_t tn4 = (tn + 3) & ~3;
@@ -1268,9 +1276,11 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         int32_t *gcount, *bcount, *gofs, *bofs, *counts0, *counts1, *boff, *ioff;
         BRec *bucket;
         LRec *live0, *live1;
-        int2 *pinfo;
+        int2 *pinfo, *imap;
         uint32_t *filt, *cpos, *hh;
     } B;
+    // work items of a level: at most T / kItemCap + S (see the match launch)
+    const int32_t icap = static_cast<int32_t>(std::min<int64_t>(static_cast<int64_t>(T) / kItemCap + S + 1, INT32_MAX));
     auto carve = [&](Carver &c) {
         B.cpos = c.take<uint32_t>(S + 1);
         B.hh = c.take<uint32_t>(kKeyNibbles * 16);
@@ -1286,6 +1296,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         B.live1 = c.take<LRec>(T + 1);
         B.bucket = c.take<BRec>(T + 1);
         B.pinfo = c.take<int2>(static_cast<size_t>(n_ports) + 1);
+        B.imap = c.take<int2>(static_cast<size_t>(icap));
     };
     Carver dry{nullptr, 0};
     carve(dry);
@@ -1412,7 +1423,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                                     B.gcount, d_len + (level & 1), n_nxt));
         PC_TIMED(ctx, "k_tr_scatter", stream,
                  hipLaunchKernelGGL(k_tr_scatter, dim3(grid_for(nlive, 256)), dim3(256), 0, stream, live_cur, len_cur,
-                                    T, S, B.boff, B.bucket));
+                                    T, S, B.boff, B.bucket, B.ioff, B.imap, icap));
         const Level lv{S,        T,     port_off, port_peer, B.pinfo, n_ports, jur,   ttl,  level,
                        live_nxt, n_nxt, cnt_nxt,  out,       watch,   K,       visit, vsum, walk};
         // at most nlive / kItemCap + S items: a switch of n lookups takes ceil(n / cap) items with cap >= kItemCap
@@ -1420,7 +1431,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         PC_TIMED(ctx, "k_tr_match", stream,
                  hipLaunchKernelGGL(k_tr_match, dim3(static_cast<unsigned>(8 * ((max_items + 7) / 8))),
                                     dim3(kMatchThreads), 0, stream, S, rule_off, rules, B.gcount, B.gofs, B.filt,
-                                    B.boff, B.ioff, B.bucket, B.cpos, lv));
+                                    B.boff, B.ioff, B.imap, B.bucket, B.cpos, lv));
         PC_LAUNCH_CHECK(ctx);
         // the count leaving this level
         const int slot = (level + 1) & 1;
