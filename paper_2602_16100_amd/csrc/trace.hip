@@ -727,6 +727,7 @@ __global__ __launch_bounds__(1024) void k_tr_plan(int32_t *__restrict__ counts, 
 // sets sit in fixed registers v32..v127 (chunk c at v[32 + 16c .. 47 + 16c]);
 // indices are below 16, so every indexed read stays inside its chunk's
 // sixteen registers.  Two blocks of three chunks keep the operand lists short.
+// Index mode keeps its index in M0, which each block declares clobbered.
 #define PC_IDX(a, b, c, d, base, op)                        \
     "s_set_gpr_idx_idx %" #a "\n\t"                          \
     "v_" op "_b32 %0, v" #base ", %0\n\t"                    \
@@ -755,7 +756,8 @@ __device__ __forceinline__ void filter_quad(const uint32_t (&x)[kChunks][4], con
         : "=&v"(a0), "=&v"(a1), "=&v"(a2), "=&v"(a3)
         : "s"(x[0][0]), "s"(x[0][1]), "s"(x[0][2]), "s"(x[0][3]), "s"(x[1][0]), "s"(x[1][1]), "s"(x[1][2]),
           "s"(x[1][3]), "s"(x[2][0]), "s"(x[2][1]), "s"(x[2][2]), "s"(x[2][3]), "{v[32:47]}"(F[0]),
-          "{v[48:63]}"(F[1]), "{v[64:79]}"(F[2]));
+          "{v[48:63]}"(F[1]), "{v[64:79]}"(F[2])
+        : "m0");
     asm volatile(
         "s_set_gpr_idx_on %4, gpr_idx(SRC0)\n\t"
         "v_and_b32 %0, v80, %0\n\t"
@@ -771,7 +773,8 @@ __device__ __forceinline__ void filter_quad(const uint32_t (&x)[kChunks][4], con
         : "+v"(a0), "+v"(a1), "+v"(a2), "+v"(a3)
         : "s"(x[3][0]), "s"(x[3][1]), "s"(x[3][2]), "s"(x[3][3]), "s"(x[4][0]), "s"(x[4][1]), "s"(x[4][2]),
           "s"(x[4][3]), "s"(x[5][0]), "s"(x[5][1]), "s"(x[5][2]), "s"(x[5][3]), "{v[80:95]}"(F[3]),
-          "{v[96:111]}"(F[4]), "{v[112:127]}"(F[5]));
+          "{v[96:111]}"(F[4]), "{v[112:127]}"(F[5])
+        : "m0");
     sv[0] = a0;
     sv[1] = a1;
     sv[2] = a2;
