@@ -29,6 +29,7 @@
 //                  sums the tiles.
 #include <algorithm>
 #include <mutex>
+#include <type_traits>
 
 #include "pc_internal.h"
 
@@ -696,10 +697,26 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
     uint32_t *prt = part + static_cast<int64_t>(tile) * I;
     const int32_t r0 = chunk * rpc;
     const int32_t r1 = min(I, r0 + rpc);
-    // one row: its record R (uniform, in SGPRs) -> bitset store and count byte
-    auto row = [&](int32_t r, int32_t i, const uint32_t (&R)[kRecWords]) {
+    // One row: its record R (uniform, in SGPRs) -> bitset store and count
+    // byte.  kIn: an interior tile of a line-shifted row (every lane's two
+    // words lie in [0, W - 1), so no masks, and every pair is 16-byte
+    // aligned); its geometry is one subtraction per lane.
+    const uint32_t lane_base = static_cast<uint32_t>(kPad + wt) * 8u;
+    auto row_shift = [&](int32_t r) {
+        const uint32_t rw = (static_cast<uint32_t>(r) & 15u) * (static_cast<uint32_t>(W) & 15u);  // r * W mod 16
+        return shift ? static_cast<int32_t>((base16 + rw) & 15u) : 0;
+    };
+    auto row = [&](auto in_tag, int32_t r, int32_t i, const uint32_t (&R)[kRecWords]) {
+        constexpr bool kIn = decltype(in_tag)::value;
         const int32_t hdr = static_cast<int32_t>(R[0]);
-        geom(r);
+        if constexpr (kIn) {
+            const int32_t sh = row_shift(r);
+            w0 = wt - sh;
+            pl.lane_off = lane_base - static_cast<uint32_t>(sh) * 8u;
+            if constexpr (!kBuf) pl.pcol = planes + kPad + w0;
+        } else {
+            geom(r);
+        }
         Words a{~0ull, ~0ull};
         Words rt{0, 0};  // affinity: OR of the finished terms
         if (hdr == kRowFalse) {
@@ -752,11 +769,13 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
         if constexpr (kTerms) {
             if (hdr > 0 || hdr == kRowIndirect || hdr == kRowLong) a = rt;
         }
-        a.a &= m0;
-        a.b &= m1;
+        if constexpr (!kIn) {
+            a.a &= m0;
+            a.b &= m1;
+        }
         if constexpr (kStore) {
             const int64_t at = static_cast<int64_t>(r) * W + w0;
-            if (pair) {
+            if (kIn || pair) {
                 __builtin_nontemporal_store(u64x2{a.a, a.b}, reinterpret_cast<u64x2 *>(feasible + at));
             } else {
                 if (ok0) __builtin_nontemporal_store(a.a, feasible + at);
@@ -764,6 +783,13 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
             }
         }
         cb[i * kCntStride + lane] = static_cast<uint8_t>(__popcll(a.a) + __popcll(a.b));
+    };
+    // (affinity programs measured slower with the interior path: it is
+    // taken for selector rows only)
+    auto row_any = [&](int32_t r, int32_t i, const uint32_t (&R)[kRecWords]) {
+        const int32_t lo = tile * kTileW - row_shift(r);
+        if (!kTerms && shift && lo >= 0 && lo + kTileW <= W - 1) row(std::true_type{}, r, i, R);
+        else row(std::false_type{}, r, i, R);
     };
     auto load_rec = [&](int32_t r, uint32_t (&R)[kRecWords]) {
         const uint32_t *rp = rec + static_cast<int64_t>(r) * kRecWords;
@@ -778,10 +804,10 @@ __global__ __launch_bounds__(kEvalThreads) void k_sel_eval(
         load_rec(bat, RA);
         for (int32_t i = 0; i < nb; i += 2) {
             load_rec(bat + min(i + 1, nb - 1), RB);
-            row(bat + i, i, RA);
+            row_any(bat + i, i, RA);
             if (i + 1 < nb) {
                 load_rec(bat + min(i + 2, nb - 1), RA);
-                row(bat + i + 1, i + 1, RB);
+                row_any(bat + i + 1, i + 1, RB);
             }
         }
         // the count table was written by every lane of this wavefront
