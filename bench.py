@@ -27,29 +27,35 @@ HBM_PEAK_GBS = 8000.0
 # 256 CUs x 64 lanes x 2.4 GHz: one wave-wide integer VALU instruction per CU per clock
 VALU_PEAK_LANE_OPS = 256 * 64 * 2.4e9
 
-# HBM bytes per launch of k_sel_eval, k_aff_eval and k_tr_prep on the
-# combined workload, from one rocprofv3 FETCH_SIZE pass and one WRITE_SIZE
-# pass each, scaled by what the same counter reads for a plain copy of known
-# size (the command lines and counter values are in
+# HBM bytes per launch of k_sel_eval, k_aff_eval and k_tr_prep (per step of
+# k_tr_match) on the combined workload, from one rocprofv3 FETCH_SIZE pass and
+# one WRITE_SIZE pass each, scaled by what the same counter reads for a plain
+# copy of known size (the command lines and counter values are in
 # profiles/k_sel_eval_k_tr_prep_cfg5_hbm_counters.md).  Valid only for the
 # kernel source they were measured on.
 TRAFFIC = [
     {"source": "paper_2602_16100_amd/csrc/select.hip",
-     "sha256": "32fd272e4456259cbe55b2b205b9511dd1dc619f00d50ec7843a2acc38bb9c0b",
+     "sha256": "8d597cb0302a22b77d1ef2e3e953faef5e1baa4aedaf63a1d1f7325a189c9c34",
      "workload": "cfg5",
-     "bytes_per_launch": {"k_sel_eval": 680_665_526 + 4_407_300_661,
-                          "k_aff_eval": 848_232_795 + 4_408_030_538}},
+     "bytes_per_launch": {"k_sel_eval": 681_065_472 + 4_407_398_400,
+                          "k_aff_eval": 848_318_464 + 4_408_035_328}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
-     "sha256": "a4835d55482cb5524271898947678a16d3070e0962fc1aca6c2a47d57cc47d88",
+     "sha256": "6e66e8603dc83879de6e617ea2d06440549ee8ec4d90728074d5d6c65b0ed1e5",
      "workload": "cfg5",
-     "bytes_per_launch": {"k_tr_prep": 1_888_471_087 + 566_231_040}},
+     # k_tr_match: per step (its 6 launches), like the hop-loop roofline
+     "bytes_per_launch": {"k_tr_prep": 1_888_831_488 + 566_231_040,
+                          "k_tr_match": 2_325_315_584 + 142_243_840}},
 ]
 
 
-# Issue counters of k_tr_match on the combined workload (one rocprofv3 pass;
-# the command and the per-dispatch values are in the profiles folder).
-# Valid only for the kernel source they were measured on.
-MATCH_COUNTERS = {}
+# Issue counters of k_tr_match on the combined workload (one rocprofv3 pass
+# per counter group; the command and the per-step values are in the profiles
+# folder).  Valid only for the kernel source they were measured on.
+MATCH_COUNTERS = {
+    "cfg5": {"source": "paper_2602_16100_amd/csrc/trace.hip",
+             "sha256": "6e66e8603dc83879de6e617ea2d06440549ee8ec4d90728074d5d6c65b0ed1e5",
+             "SQ_INSTS_VALU_per_step": 3.891e8, "SQ_INSTS_SALU_per_step": 3.392e8},
+}
 
 
 def source_unchanged(rec):
@@ -118,7 +124,38 @@ def parse():
                     help="requests of the path-synthesis pass (the first flows of the workload)")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="profiling aid: run a plain device copy of MIB MiB three times (HBM counter calibration)")
+    ap.add_argument("--measure-plain", type=int, default=0, metavar="MIB",
+                    help="profiling aid: time a plain device fill and a plain copy of MIB MiB (the rates an "
+                         "HBM-bound kernel of that size can reach)")
     return ap.parse_args()
+
+
+def measure_plain(mib, reps=10):
+    """Torch's own fill and copy of MIB MiB, timed with events over `reps`
+    launches after 2 untimed ones: the write-only and read+write rates a
+    kernel that streams that many bytes can reach on this GPU."""
+    import torch
+    n = (mib << 20) // 8
+    x = torch.empty(n, dtype=torch.int64, device="cuda:0")
+    y = torch.ones(n, dtype=torch.int64, device="cuda:0")
+    torch.cuda.synchronize()
+
+    def timed(fn):
+        for _ in range(2):
+            fn()
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(reps):
+            fn()
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / reps
+
+    fill_ms = timed(lambda: x.fill_(7))
+    copy_ms = timed(lambda: x.copy_(y))
+    b = n * 8
+    print(json.dumps({"bytes": b, "fill_ms": fill_ms, "fill_gbs": b / fill_ms / 1e6,
+                      "copy_ms": copy_ms, "copy_gbs": 2 * b / copy_ms / 1e6}), flush=True)
 
 
 def calibrate_copy(mib):
@@ -1074,6 +1111,9 @@ def main():
 
     if args.calibrate_copy:
         calibrate_copy(args.calibrate_copy)
+        return
+    if args.measure_plain:
+        measure_plain(args.measure_plain)
         return
 
     import torch
