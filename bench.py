@@ -398,17 +398,7 @@ def time_paths(args, wl, D, pc, ctx, feasible, popcnt):
         pc.pc_report_paths(D["intents"], feasible, popcnt, wl["N"], traces, D["expect"], reach, visit, D["pexp"],
                            pass_=pass_, reason=reason, summary=summary, ctx=ctx)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.profile(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    prof = ctx.profile_read()
-    ctx.profile(False)
+    elapsed, prof = timed_steps(args, ctx, step)
 
     def ktime(prefix):
         return sum(ms for name, (n, ms) in prof.items() if name.startswith(prefix)) / args.steps
@@ -457,18 +447,7 @@ def time_affinity(args, wl, pc, ctx, feasible):
         pc.pc_eval_affinity(D["labels"], D["row_off"], D["term_off"], D["preds"], feasible=feasible, popcnt=popcnt,
                             unknown=unknown, ctx=ctx)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.data_errors(clear=True)
-    ctx.profile(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    prof = ctx.profile_read()
-    ctx.profile(False)
+    elapsed, prof = timed_steps(args, ctx, step)
     flags = ctx.data_errors(clear=True)
     N, L = wl["N"], wl["L"]
     W = (N + 63) // 64
@@ -538,18 +517,7 @@ def time_preferred(args, wl, pc, ctx, feasible):
         pc.pc_score_preferred(D["labels"], D["row_off"], D["term_off"], D["weight"], D["preds"], feasible=feasible,
                               best=best, score=score, count=count, ctx=ctx)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.data_errors(clear=True)
-    ctx.profile(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    prof = ctx.profile_read()
-    ctx.profile(False)
+    elapsed, prof = timed_steps(args, ctx, step)
     flags = ctx.data_errors(clear=True)
     N, L = wl["N"], wl["L"]
     W = (N + 63) // 64
@@ -633,17 +601,7 @@ def time_verdict_only(args, wl, pc, ctx, D, traces, reach):
         pc.pc_report_counts(D["intents"], popcnt, wl["N"], ends, traces, D["expect"], reach, pass_=pass_,
                             reason=reason, summary=summary, ctx=ctx)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.profile(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    prof = ctx.profile_read()
-    ctx.profile(False)
+    elapsed, prof = timed_steps(args, ctx, step)
     return {"ms_per_step": 1e3 * elapsed / args.steps,
             "per_kernel": {name: {"launches_per_step": n / args.steps, "ms_per_step": ms / args.steps}
                            for name, (n, ms) in sorted(prof.items(), key=lambda kv: -kv[1][1])},
@@ -824,18 +782,7 @@ def time_synthesis(args, wl, pc, ctx):
                                D["via"], D["forbid"], D["key"], D["out_port"], prio, ttl, weight=Wd, hops=hops,
                                path=path, rules=rules, ctx=ctx)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.data_errors(clear=True)
-    ctx.profile(True)
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    elapsed = time.perf_counter() - t0
-    prof = ctx.profile_read()
-    ctx.profile(False)
+    elapsed, prof = timed_steps(args, ctx, step)
     flags = ctx.data_errors(clear=True)
     h = hops.cpu().numpy()
     legs = int(Q + (arr["via"] >= 0).sum())
@@ -914,20 +861,27 @@ def oracle_threads():
 
 
 def timed_steps(args, ctx, step):
-    """W warm-up steps, then K steps timed with the per-kernel profiler on;
-    returns (seconds, {kernel: (launches, ms)})."""
+    """W warm-up steps, then K steps timed by the host clock with nothing
+    but the step on the stream, then K more steps with the per-kernel
+    profiler on (its event pair around every launch adds a gap of several
+    microseconds per kernel, so those steps are not the ones timed);
+    returns (seconds of the K plain steps, {kernel: (launches, ms)})."""
     import torch
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
     ctx.data_errors(clear=True)
-    ctx.profile(True)
+    ctx.profile(False)
     torch.cuda.synchronize()
     t0 = time.perf_counter()
     for _ in range(args.steps):
         step()
     torch.cuda.synchronize()
     t1 = time.perf_counter()
+    ctx.profile(True)
+    for _ in range(args.steps):
+        step()
+    torch.cuda.synchronize()
     prof = ctx.profile_read()
     ctx.profile(False)
     return t1 - t0, prof
@@ -1196,21 +1150,8 @@ def main():
             pc.pc_report(D["intents"], feasible, popcnt, N, traces, D["expect"], reach, pass_=pass_, reason=reason,
                          summary=summary, ctx=ctx)
 
-    for _ in range(args.warmup):
-        step()
-    torch.cuda.synchronize()
-    ctx.data_errors(clear=True)
-    ctx.profile(True)
-    torch.cuda.synchronize()
-    t0 = time.perf_counter()
-    for _ in range(args.steps):
-        step()
-    torch.cuda.synchronize()
-    t1 = time.perf_counter()
-    prof = ctx.profile_read()
-    ctx.profile(False)
+    elapsed, prof = timed_steps(args, ctx, step)
     flags = ctx.data_errors(clear=True)
-    elapsed = t1 - t0
     ms_step = 1e3 * elapsed / args.steps
 
     tr = pc.records(traces, pc.TRACE_OUT_DT)

@@ -1323,17 +1323,12 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         launch_scan_i32(B.bcount, S, B.bofs, nullptr, nullptr, stream);
         PC_LAUNCH_CHECK(ctx);
         // exact sizes of the chunk-set buffer and of the prep grid (switch
-        // ranges may overlap, so no host-side bound from n_rules holds)
+        // ranges may overlap, so no host-side bound from n_rules holds); the
+        // host waits for these two counts only, while the port check and
+        // the chunk choice, queued behind them, keep the GPU busy
         PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, B.gofs + S, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
         PC_HIP(ctx, hipMemcpyAsync(ctx->h_small + 1, B.bofs + S, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
-        PC_HIP(ctx, hipStreamSynchronize(stream));
-        const int64_t total_groups = ctx->h_small[0];
-        const int64_t prep_blocks = ctx->h_small[1];
-        if (total_groups < 0 || prep_blocks < 0)
-            return pc_set_error(ctx, PC_EINVAL, "pc_trace_flows: more than 2^31 rule groups");
-        rc = pc_ensure_aux(ctx, static_cast<size_t>(total_groups + 1) * kPlaneWords * sizeof(uint32_t));
-        if (rc) return rc;
-        B.filt = reinterpret_cast<uint32_t *>(ctx->aux);
+        PC_HIP(ctx, hipEventRecord(ctx->lvl_ev[0], stream));
         if (n_ports > 0) {
             PC_TIMED(ctx, "k_tr_port_check", stream, hipLaunchKernelGGL(k_tr_port_check, dim3(grid_for(n_ports, 256)), dim3(256), 0, stream, n_ports,
                                port_peer, S, ctx->d_err));
@@ -1341,6 +1336,14 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         }
         rc = choose_chunks(ctx, S, rule_off, n_rules, rules, hdr, T, B.hh, B.cpos, stream);
         if (rc) return rc;
+        PC_HIP(ctx, hipEventSynchronize(ctx->lvl_ev[0]));
+        const int64_t total_groups = ctx->h_small[0];
+        const int64_t prep_blocks = ctx->h_small[1];
+        if (total_groups < 0 || prep_blocks < 0)
+            return pc_set_error(ctx, PC_EINVAL, "pc_trace_flows: more than 2^31 rule groups");
+        rc = pc_ensure_aux(ctx, static_cast<size_t>(total_groups + 1) * kPlaneWords * sizeof(uint32_t));
+        if (rc) return rc;
+        B.filt = reinterpret_cast<uint32_t *>(ctx->aux);
         if (prep_blocks > 0) {
             PC_TIMED(ctx, "k_tr_prep", stream, hipLaunchKernelGGL(k_tr_prep, dim3(static_cast<unsigned>(prep_blocks)), dim3(kPrepWaves * 64), 0, stream, S,
                                port_off, n_ports, rule_off, rules, B.gcount, B.gofs, B.bofs, B.filt, ctx->d_err,
@@ -1383,8 +1386,6 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
                                         B.live0, d_n, B.counts0, out, watch, K, visit, vsum, walk, ctx->d_err));
     }
     PC_LAUNCH_CHECK(ctx);
-    PC_HIP(ctx, hipMemcpyAsync(ctx->h_small, d_n, sizeof(int32_t), hipMemcpyDeviceToHost, stream));
-    PC_HIP(ctx, hipStreamSynchronize(stream));
     LRec *live_cur = B.live0, *live_nxt = B.live1;
     int32_t *cnt_cur = B.counts0, *cnt_nxt = B.counts1;
     int32_t *n_cur = d_n, *n_nxt = d_n + 1;
@@ -1400,10 +1401,11 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
     // and waited for (an event one level behind) while level L runs.
     int32_t *h_cnt = ctx->h_small + 8;  // two pinned slots, by level parity
     int32_t *d_len = ctx->d_small + 6;  // two slots, by level parity: each level's lookups (its live list's length)
-    // An upper bound on the count entering the next level; from level 1 on,
-    // also the exact length of the live list the previous level wrote (every
+    // An upper bound on the count entering the next level (T for level 0:
+    // the host does not wait for the initial count); from level 2 on, also
+    // the exact length of the live list the previous level wrote (every
     // lookup of a level leaves an entry, the traces that ended included).
-    int64_t known = ctx->h_small[0];
+    int64_t known = T;
     for (int level = 0;; ++level) {
         if (level > ttl + 2)
             return pc_set_error(ctx, PC_EDEVICE, "pc_trace_flows: level loop exceeded ttl+2 levels");
