@@ -258,73 +258,89 @@ __device__ __forceinline__ bool aff_valid(const pc_pred &q, int32_t L)
 // the program, then emit it -- inline in the row record when it has at most
 // 15 entries, else at prog[4 * pred_off[i] ...] (at most 4 entries per
 // predicate; longer programs are decoded at evaluation time).
-__global__ __launch_bounds__(256) void k_sel_compile(const int32_t *__restrict__ pred_off,
-                                                     const pc_pred *__restrict__ preds, int64_t n_preds, int32_t I,
-                                                     int32_t L, const uint64_t *__restrict__ present,
-                                                     const uint32_t *__restrict__ wbase,
-                                                     uint32_t *__restrict__ prog, uint32_t *__restrict__ rec,
-                                                     uint32_t *__restrict__ d_err)
+// One thread per row.  Each row's record is built in LDS and written as
+// four 16-byte stores instead of a store per entry.  (Staging a pass's
+// predicates in LDS as well measured slower: the 50 KB it takes leaves two
+// workgroups per CU.)
+constexpr int kCompThreads = 256;
+__global__ __launch_bounds__(kCompThreads) void k_sel_compile(const int32_t *__restrict__ pred_off,
+                                                              const pc_pred *__restrict__ preds, int64_t n_preds,
+                                                              int32_t I, int32_t L,
+                                                              const uint64_t *__restrict__ present,
+                                                              const uint32_t *__restrict__ wbase,
+                                                              uint32_t *__restrict__ prog, uint32_t *__restrict__ rec,
+                                                              uint32_t *__restrict__ d_err)
 {
+    __shared__ uint32_t srec[kCompThreads][kRecWords + 1];  // each thread's row record (padded row)
+    uint32_t *R = srec[threadIdx.x];
     uint32_t errs = 0;
-    for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
-        uint32_t *rr = rec + static_cast<int64_t>(i) * kRecWords;
+    for (int64_t i0 = static_cast<int64_t>(blockIdx.x) * kCompThreads; i0 < I;
+         i0 += static_cast<int64_t>(gridDim.x) * kCompThreads) {
+        const int64_t i = i0 + threadIdx.x;
+        if (i >= I) continue;
         const int64_t b = pred_off[i], e = pred_off[i + 1];
-        if (!pc_range_ok(b, e, n_preds)) {
-            errs |= PC_DERR_OFFSETS;
-            rr[0] = static_cast<uint32_t>(kRowFalse);
-            continue;
-        }
-        bool empty = false;
-        int64_t n = 0;
-        for (int64_t p = b; p < e; ++p) {
-            const pc_pred q = preds[p];
-            if (!pred_valid(q.label, q.op, q.rsv0, q.rsv1, q.vals[3], L)) {
-                errs |= PC_DERR_PRED;
-                empty = true;
-                continue;
+        // the row's record, in LDS until it is complete
+        [&] {
+            if (!pc_range_ok(b, e, n_preds)) {
+                errs |= PC_DERR_OFFSETS;
+                R[0] = static_cast<uint32_t>(kRowFalse);
+                return;
             }
-            uint64_t sel[4];
-            bool neg;
-            const uint32_t cnt = pred_clause(q, present + static_cast<int64_t>(q.label) * 4, sel, neg);
-            if (cnt == 0 && !neg) empty = true;  // empty OR: no node (a negated empty OR is every node)
-            n += cnt;
-        }
-        if (empty) {
-            rr[0] = static_cast<uint32_t>(kRowFalse);
-            continue;
-        }
-        const bool inl = n <= kInline;
-        if (!inl && n > 4 * (e - b)) {
-            rr[0] = static_cast<uint32_t>(kRowLong);
-            continue;
-        }
-        uint32_t *out = inl ? rr + 1 : prog + 4 * b;
-        int64_t k_out = 0;
-        for (int64_t p = b; p < e; ++p) {
-            const pc_pred q = preds[p];
-            const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
-            const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
-            uint64_t sel[4];
-            bool neg;
-            uint32_t cnt = pred_clause(q, pres, sel, neg);
-            for (int k = 0; k < 4; ++k) {
-                uint64_t m = sel[k];
-                while (m) {
-                    const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
-                    m &= m - 1;
-                    uint32_t ent = plane_id(pres, wb, v);
-                    if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
-                    out[k_out++] = ent;
+            bool empty = false;
+            int64_t n = 0;
+            for (int64_t p = b; p < e; ++p) {
+                const pc_pred q = preds[p];
+                if (!pred_valid(q.label, q.op, q.rsv0, q.rsv1, q.vals[3], L)) {
+                    errs |= PC_DERR_PRED;
+                    empty = true;
+                    continue;
+                }
+                uint64_t sel[4];
+                bool neg;
+                const uint32_t cnt = pred_clause(q, present + static_cast<int64_t>(q.label) * 4, sel, neg);
+                if (cnt == 0 && !neg) empty = true;  // empty OR: no node (a negated empty OR is every node)
+                n += cnt;
+            }
+            if (empty) {
+                R[0] = static_cast<uint32_t>(kRowFalse);
+                return;
+            }
+            const bool inl = n <= kInline;
+            if (!inl && n > 4 * (e - b)) {
+                R[0] = static_cast<uint32_t>(kRowLong);
+                return;
+            }
+            uint32_t *out = inl ? R + 1 : prog + 4 * b;
+            int64_t k_out = 0;
+            for (int64_t p = b; p < e; ++p) {
+                const pc_pred q = preds[p];
+                const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+                const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+                uint64_t sel[4];
+                bool neg;
+                uint32_t cnt = pred_clause(q, pres, sel, neg);
+                for (int k = 0; k < 4; ++k) {
+                    uint64_t m = sel[k];
+                    while (m) {
+                        const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                        m &= m - 1;
+                        uint32_t ent = plane_id(pres, wb, v);
+                        if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
+                        out[k_out++] = ent;
+                    }
                 }
             }
-        }
-        if (inl) {
-            rr[0] = static_cast<uint32_t>(n);  // the evaluator reads entries 1..n only
-        } else {
-            rr[0] = static_cast<uint32_t>(kRowIndirect);
-            rr[1] = static_cast<uint32_t>(b);
-            rr[2] = static_cast<uint32_t>(n);
-        }
+            if (inl) {
+                R[0] = static_cast<uint32_t>(n);  // the evaluator reads entries 1..n only
+            } else {
+                R[0] = static_cast<uint32_t>(kRowIndirect);
+                R[1] = static_cast<uint32_t>(b);
+                R[2] = static_cast<uint32_t>(n);
+            }
+        }();
+        uint4 *dst = reinterpret_cast<uint4 *>(rec + i * kRecWords);
+#pragma unroll
+        for (int k = 0; k < kRecWords / 4; ++k) dst[k] = make_uint4(R[4 * k], R[4 * k + 1], R[4 * k + 2], R[4 * k + 3]);
     }
     if (errs) atomicOr(d_err, errs);
 }
