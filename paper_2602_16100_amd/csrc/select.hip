@@ -423,81 +423,89 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
                                                      unsigned long long *__restrict__ prog_used,
                                                      uint32_t *__restrict__ rec, uint8_t *__restrict__ unknown)
 {
+    // each row's record is built in LDS and written as 16-byte stores
+    __shared__ uint32_t srec[256][kRecWords + 1];
+    uint32_t *rr = srec[threadIdx.x];
     for (int32_t i = blockIdx.x * blockDim.x + threadIdx.x; i < I; i += gridDim.x * blockDim.x) {
-        uint32_t *rr = rec + static_cast<int64_t>(i) * kRecWords;
-        const int64_t tb = row_off[i], te = row_off[i + 1];
-        if (!pc_range_ok(tb, te, n_terms)) {
-            rr[0] = static_cast<uint32_t>(kRowFalse);
-            unknown[i] = 0;
-            continue;
-        }
-        uint32_t unk = 0;
-        for (int64_t t = tb; t < te; ++t) {
-            const int64_t b = term_off[t], e = term_off[t + 1];
-            if (!pc_range_ok(b, e, n_preds)) continue;
-            for (int64_t p = b; p < e; ++p) {
-                const pc_pred q = preds[p];
-                if (aff_valid(q, L)) unk |= aff_unknown(q, present + static_cast<int64_t>(q.label) * 4);
+        [&] {  // the row's record, in LDS until it is complete
+            const int64_t tb = row_off[i], te = row_off[i + 1];
+            if (!pc_range_ok(tb, te, n_terms)) {
+                rr[0] = static_cast<uint32_t>(kRowFalse);
+                unknown[i] = 0;
+                return;
             }
-        }
-        unknown[i] = static_cast<uint8_t>(unk);
-        bool all = tb == te;
-        int64_t n = 0, live = 0;
-        for (int64_t t = tb; t < te && !all; ++t) {
-            int64_t len;
-            if (!aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len)) continue;
-            if (len == 0) all = true;
-            n += len;
-            ++live;
-        }
-        if (all) {
-            rr[0] = 0;
-            continue;
-        }
-        if (live == 0) {
-            rr[0] = static_cast<uint32_t>(kRowFalse);
-            continue;
-        }
-        const bool inl = n <= kInline;
-        uint32_t *out = rr + 1;
-        if (!inl) {
-            // slices are whole multiples of 4 entries: the record stores off / 4
-            const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>((n + 3) & ~int64_t(3)));
-            if (static_cast<int64_t>(off) + n > prog_cap) {
-                rr[0] = static_cast<uint32_t>(kRowLong);
-                continue;
-            }
-            out = prog + off;
-            rr[0] = static_cast<uint32_t>(kRowIndirect);
-            rr[1] = static_cast<uint32_t>(off / 4);
-            rr[2] = static_cast<uint32_t>(n);
-        }
-        int64_t k_out = 0;
-        for (int64_t t = tb; t < te; ++t) {
-            const int64_t b = term_off[t], e = term_off[t + 1];
-            int64_t len;
-            if (!aff_term(preds, b, e, n_preds, L, present, len)) continue;
-            for (int64_t p = b; p < e; ++p) {
-                const pc_pred q = preds[p];
-                const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
-                const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
-                uint64_t sel[4];
-                bool neg;
-                uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
-                for (int k = 0; k < 4; ++k) {
-                    uint64_t m = sel[k];
-                    while (m) {
-                        const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
-                        m &= m - 1;
-                        uint32_t ent = plane_id(pres, wb, v);
-                        if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
-                        out[k_out++] = ent;
-                    }
+            uint32_t unk = 0;
+            for (int64_t t = tb; t < te; ++t) {
+                const int64_t b = term_off[t], e = term_off[t + 1];
+                if (!pc_range_ok(b, e, n_preds)) continue;
+                for (int64_t p = b; p < e; ++p) {
+                    const pc_pred q = preds[p];
+                    if (aff_valid(q, L)) unk |= aff_unknown(q, present + static_cast<int64_t>(q.label) * 4);
                 }
             }
-            out[k_out - 1] |= kTermEnd;
-        }
-        if (inl) rr[0] = static_cast<uint32_t>(n);
+            unknown[i] = static_cast<uint8_t>(unk);
+            bool all = tb == te;
+            int64_t n = 0, live = 0;
+            for (int64_t t = tb; t < te && !all; ++t) {
+                int64_t len;
+                if (!aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len)) continue;
+                if (len == 0) all = true;
+                n += len;
+                ++live;
+            }
+            if (all) {
+                rr[0] = 0;
+                return;
+            }
+            if (live == 0) {
+                rr[0] = static_cast<uint32_t>(kRowFalse);
+                return;
+            }
+            const bool inl = n <= kInline;
+            uint32_t *out = rr + 1;
+            if (!inl) {
+                // slices are whole multiples of 4 entries: the record stores off / 4
+                const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>((n + 3) & ~int64_t(3)));
+                if (static_cast<int64_t>(off) + n > prog_cap) {
+                    rr[0] = static_cast<uint32_t>(kRowLong);
+                    return;
+                }
+                out = prog + off;
+                rr[0] = static_cast<uint32_t>(kRowIndirect);
+                rr[1] = static_cast<uint32_t>(off / 4);
+                rr[2] = static_cast<uint32_t>(n);
+            }
+            int64_t k_out = 0;
+            for (int64_t t = tb; t < te; ++t) {
+                const int64_t b = term_off[t], e = term_off[t + 1];
+                int64_t len;
+                if (!aff_term(preds, b, e, n_preds, L, present, len)) continue;
+                for (int64_t p = b; p < e; ++p) {
+                    const pc_pred q = preds[p];
+                    const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+                    const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
+                    uint64_t sel[4];
+                    bool neg;
+                    uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
+                    for (int k = 0; k < 4; ++k) {
+                        uint64_t m = sel[k];
+                        while (m) {
+                            const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+                            m &= m - 1;
+                            uint32_t ent = plane_id(pres, wb, v);
+                            if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
+                            out[k_out++] = ent;
+                        }
+                    }
+                }
+                out[k_out - 1] |= kTermEnd;
+            }
+            if (inl) rr[0] = static_cast<uint32_t>(n);
+        }();
+        uint4 *dst = reinterpret_cast<uint4 *>(rec + static_cast<int64_t>(i) * kRecWords);
+#pragma unroll
+        for (int k = 0; k < kRecWords / 4; ++k)
+            dst[k] = make_uint4(rr[4 * k], rr[4 * k + 1], rr[4 * k + 2], rr[4 * k + 3]);
     }
 }
 
@@ -924,9 +932,8 @@ __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_
                                      const uint32_t *__restrict__ weight, const pc_pred *__restrict__ preds,
                                      int64_t n_preds, int32_t L, const uint64_t *__restrict__ present,
                                      const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog, int64_t prog_cap,
-                                     unsigned long long *__restrict__ prog_used, uint32_t *__restrict__ rec)
+                                     unsigned long long *__restrict__ prog_used, uint32_t *rr)
 {
-    uint32_t *rr = rec + static_cast<int64_t>(i) * kPrefRec;
     rr[0] = kPrefNone << 24;
     if (!pref_row_ok(row_off, i, n_terms)) return 3;
     const int64_t tb = row_off[i], te = row_off[i + 1];
@@ -1004,13 +1011,22 @@ __global__ __launch_bounds__(256) void k_pref_compile(const int32_t *__restrict_
                                                       uint32_t *__restrict__ rec, int32_t *__restrict__ list,
                                                       uint32_t *__restrict__ list_len)
 {
+    // each row's record is built in LDS and written as 16-byte stores
+    __shared__ uint32_t srec[256][kPrefRec + 1];
+    uint32_t *R = srec[threadIdx.x];
     const int lane = threadIdx.x & 63;
     for (int64_t base = static_cast<int64_t>(blockIdx.x) * blockDim.x; base < I;
          base += static_cast<int64_t>(gridDim.x) * blockDim.x) {
         const int32_t i = static_cast<int32_t>(base + threadIdx.x);
-        const uint32_t cls = i < I ? pref_compile_row(row_off, i, term_off, n_terms, weight, preds, n_preds, L,
-                                                      present, wbase, prog, prog_cap, prog_used, rec)
-                                   : kPrefClasses;
+        uint32_t cls = kPrefClasses;
+        if (i < I) {
+            cls = pref_compile_row(row_off, i, term_off, n_terms, weight, preds, n_preds, L, present, wbase, prog,
+                                   prog_cap, prog_used, R);
+            uint4 *dst = reinterpret_cast<uint4 *>(rec + static_cast<int64_t>(i) * kPrefRec);
+#pragma unroll
+            for (int k = 0; k < kPrefRec / 4; ++k)
+                dst[k] = make_uint4(R[4 * k], R[4 * k + 1], R[4 * k + 2], R[4 * k + 3]);
+        }
         // append i to its class list: one counter update per class and wavefront
         for (uint32_t c = 0; c < kPrefClasses; ++c) {
             const uint64_t mask = __ballot(cls == c);
