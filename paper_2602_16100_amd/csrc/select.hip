@@ -239,6 +239,91 @@ __device__ __forceinline__ uint32_t expr_clause(uint32_t op, const uint64_t vals
     return use_in ? ms : mc;
 }
 
+// The largest present value (0..254, the absent value 255 excluded) at or
+// below x, or -1.
+__device__ __forceinline__ int32_t pres_max_le(const uint64_t *pres, int64_t x)
+{
+    if (x < 0) return -1;
+    if (x > 254) x = 254;
+    const int kx = static_cast<int>(x >> 6);
+    for (int k = kx; k >= 0; --k) {
+        uint64_t m = pres[k];
+        if (k == 3) m &= ~(1ull << 63);
+        if (k == kx && (x & 63) != 63) m &= (1ull << ((x & 63) + 1)) - 1;
+        if (m) return k * 64 + 63 - __builtin_clzll(m);
+    }
+    return -1;
+}
+
+// Gt / Lt over the label's prefix planes (plane pfx0 + plane_id(v) is the
+// OR of the planes of the label's present values <= v, built by
+// k_aff_prefix): Lt t is the prefix of the largest present value below t,
+// one entry; Gt t is NOT (the prefix of the largest present value <= t OR
+// the absent-value plane), at most two entries.  The node sets are those
+// expr_clause selects value by value.  Returns the entry count (ids in e)
+// with neg as in expr_clause: 0 entries without neg is a clause no node
+// satisfies, 0 entries with neg one every node does.
+__device__ __forceinline__ uint32_t cmp_clause(uint32_t op, int64_t t, const uint64_t *pres, const uint32_t *wb,
+                                               uint32_t pfx0, uint32_t (&e)[2], bool &neg)
+{
+    uint32_t n = 0;
+    neg = false;
+    if (op == PC_OP_LT) {
+        const int32_t u = t <= 0 ? -1 : pres_max_le(pres, t - 1);
+        if (u >= 0) e[n++] = pfx0 + plane_id(pres, wb, static_cast<uint32_t>(u));
+        return n;
+    }
+    const int32_t top = pres_max_le(pres, 254);
+    if (top < 0 || t >= top) return 0;  // no present value above t
+    neg = true;
+    const int32_t u = pres_max_le(pres, t);
+    if (u >= 0) e[n++] = pfx0 + plane_id(pres, wb, static_cast<uint32_t>(u));
+    if (pres[3] >> 63) e[n++] = plane_id(pres, wb, 255);
+    return n;
+}
+
+// cmp_clause's entry count and neg, without the plane ids.
+__device__ __forceinline__ uint32_t cmp_count(uint32_t op, int64_t t, const uint64_t *pres, bool &neg)
+{
+    neg = false;
+    if (op == PC_OP_LT) return (t > 0 && pres_max_le(pres, t - 1) >= 0) ? 1u : 0u;
+    const int32_t top = pres_max_le(pres, 254);
+    if (top < 0 || t >= top) return 0;
+    neg = true;
+    return (pres_max_le(pres, t) >= 0 ? 1u : 0u) + static_cast<uint32_t>(pres[3] >> 63);
+}
+
+// The program entries of one affinity expression (label present table
+// pres / plane bases wb): Gt / Lt through the prefix planes, the rest value
+// by value.  emit(entry) receives each entry, the clause's last with kLast
+// and, when the clause is negated, kNeg.  Returns the count and the
+// clause's emptiness as expr_clause does (count 0 without neg: no node).
+template <class Emit>
+__device__ __forceinline__ uint32_t aff_entries(const pc_pred &q, const uint64_t *pres, const uint32_t *wb,
+                                                uint32_t pfx0, bool &neg, const Emit &emit)
+{
+    if (q.op == PC_OP_GT || q.op == PC_OP_LT) {
+        uint32_t e[2];
+        const uint32_t n = cmp_clause(q.op, static_cast<int64_t>(q.vals[0]), pres, wb, pfx0, e, neg);
+        for (uint32_t i = 0; i < n; ++i) emit(e[i] | (i + 1 == n ? kLast | (neg ? kNeg : 0u) : 0u));
+        return n;
+    }
+    uint64_t sel[4];
+    uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
+    const uint32_t n = cnt;
+    for (int k = 0; k < 4; ++k) {
+        uint64_t m = sel[k];
+        while (m) {
+            const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+            m &= m - 1;
+            uint32_t ent = plane_id(pres, wb, v);
+            if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
+            emit(ent);
+        }
+    }
+    return n;
+}
+
 __device__ __forceinline__ uint32_t pred_clause(const pc_pred &q, const uint64_t *pres, uint64_t sel[4], bool &neg)
 {
     return expr_clause(q.op, q.vals, pres, sel, neg);
@@ -388,7 +473,7 @@ __device__ __forceinline__ uint32_t aff_unknown(const pc_pred &q, const uint64_t
 
 // Whether term [b, e) can hold for some node at all (valid offsets, at
 // least one expression, every expression well-formed, no clause that is an
-// empty OR), and its program length.
+// empty OR), and its program length (Gt / Lt in the prefix form).
 __device__ __forceinline__ bool aff_term(const pc_pred *__restrict__ preds, int64_t b, int64_t e, int64_t n_preds,
                                          int32_t L, const uint64_t *__restrict__ present, int64_t &len)
 {
@@ -398,9 +483,15 @@ __device__ __forceinline__ bool aff_term(const pc_pred *__restrict__ preds, int6
     for (int64_t p = b; p < e; ++p) {
         const pc_pred q = preds[p];
         if (!aff_valid(q, L)) return false;
-        uint64_t sel[4];
+        const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
         bool neg;
-        const uint32_t cnt = expr_clause(q.op, q.vals, present + static_cast<int64_t>(q.label) * 4, sel, neg);
+        uint32_t cnt;
+        if (q.op == PC_OP_GT || q.op == PC_OP_LT) {
+            cnt = cmp_count(q.op, static_cast<int64_t>(q.vals[0]), pres, neg);
+        } else {
+            uint64_t sel[4];
+            cnt = expr_clause(q.op, q.vals, pres, sel, neg);
+        }
         if (cnt == 0 && !neg) ok = false;
         len += cnt;
     }
@@ -421,7 +512,8 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
                                                      const uint32_t *__restrict__ wbase,
                                                      uint32_t *__restrict__ prog, int64_t prog_cap,
                                                      unsigned long long *__restrict__ prog_used,
-                                                     uint32_t *__restrict__ rec, uint8_t *__restrict__ unknown)
+                                                     uint32_t *__restrict__ rec, uint8_t *__restrict__ unknown,
+                                                     uint32_t pfx0)
 {
     // each row's record is built in LDS and written as 16-byte stores
     __shared__ uint32_t srec[256][kRecWords + 1];
@@ -482,21 +574,9 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
                 if (!aff_term(preds, b, e, n_preds, L, present, len)) continue;
                 for (int64_t p = b; p < e; ++p) {
                     const pc_pred q = preds[p];
-                    const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
-                    const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
-                    uint64_t sel[4];
                     bool neg;
-                    uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
-                    for (int k = 0; k < 4; ++k) {
-                        uint64_t m = sel[k];
-                        while (m) {
-                            const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
-                            m &= m - 1;
-                            uint32_t ent = plane_id(pres, wb, v);
-                            if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
-                            out[k_out++] = ent;
-                        }
-                    }
+                    aff_entries(q, present + static_cast<int64_t>(q.label) * 4, wbase + static_cast<int64_t>(q.label) * 4,
+                                pfx0, neg, [&](uint32_t ent) { out[k_out++] = ent; });
                 }
                 out[k_out - 1] |= kTermEnd;
             }
@@ -932,7 +1012,7 @@ __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_
                                      const uint32_t *__restrict__ weight, const pc_pred *__restrict__ preds,
                                      int64_t n_preds, int32_t L, const uint64_t *__restrict__ present,
                                      const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog, int64_t prog_cap,
-                                     unsigned long long *__restrict__ prog_used, uint32_t *rr)
+                                     unsigned long long *__restrict__ prog_used, uint32_t *rr, uint32_t pfx0)
 {
     rr[0] = kPrefNone << 24;
     if (!pref_row_ok(row_off, i, n_terms)) return 3;
@@ -972,21 +1052,9 @@ __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_
         out[k_out++] = weight[t] << kPrefLenBits | static_cast<uint32_t>(len);
         for (int64_t p = b; p < e; ++p) {
             const pc_pred q = preds[p];
-            const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
-            const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
-            uint64_t sel[4];
             bool neg;
-            uint32_t cnt = expr_clause(q.op, q.vals, pres, sel, neg);
-            for (int k = 0; k < 4; ++k) {
-                uint64_t m = sel[k];
-                while (m) {
-                    const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
-                    m &= m - 1;
-                    uint32_t ent = plane_id(pres, wb, v);
-                    if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
-                    out[k_out++] = ent;
-                }
-            }
+            aff_entries(q, present + static_cast<int64_t>(q.label) * 4, wbase + static_cast<int64_t>(q.label) * 4, pfx0,
+                        neg, [&](uint32_t ent) { out[k_out++] = ent; });
         }
     }
     rr[0] = head | kind << 24;
@@ -1009,7 +1077,7 @@ __global__ __launch_bounds__(256) void k_pref_compile(const int32_t *__restrict_
                                                       const uint32_t *__restrict__ wbase, uint32_t *__restrict__ prog,
                                                       int64_t prog_cap, unsigned long long *__restrict__ prog_used,
                                                       uint32_t *__restrict__ rec, int32_t *__restrict__ list,
-                                                      uint32_t *__restrict__ list_len)
+                                                      uint32_t *__restrict__ list_len, uint32_t pfx0)
 {
     // each row's record is built in LDS and written as 16-byte stores
     __shared__ uint32_t srec[256][kPrefRec + 1];
@@ -1021,7 +1089,7 @@ __global__ __launch_bounds__(256) void k_pref_compile(const int32_t *__restrict_
         uint32_t cls = kPrefClasses;
         if (i < I) {
             cls = pref_compile_row(row_off, i, term_off, n_terms, weight, preds, n_preds, L, present, wbase, prog,
-                                   prog_cap, prog_used, R);
+                                   prog_cap, prog_used, R, pfx0);
             uint4 *dst = reinterpret_cast<uint4 *>(rec + static_cast<int64_t>(i) * kPrefRec);
 #pragma unroll
             for (int k = 0; k < kPrefRec / 4; ++k)
@@ -1422,6 +1490,34 @@ EvalGeom eval_geom(int32_t N)
     return g;
 }
 
+// Prefix planes of the affinity paths: plane pfx0 + plane_id(v) = OR of the
+// planes of the label's present values <= v (v in 0..254), so that Gt / Lt
+// take at most two entries (cmp_clause).  One thread per (label, plane
+// word), over the label's present values in increasing order.
+__global__ __launch_bounds__(256) void k_aff_prefix(const uint64_t *__restrict__ present,
+                                                    const uint32_t *__restrict__ wbase, int32_t L,
+                                                    uint64_t *__restrict__ planes, int64_t Wp, uint32_t pfx0)
+{
+    const int64_t idx = static_cast<int64_t>(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (idx >= static_cast<int64_t>(L) * Wp) return;
+    const int32_t l = static_cast<int32_t>(idx / Wp);
+    const int64_t w = idx % Wp;
+    const uint64_t *pres = present + static_cast<int64_t>(l) * 4;
+    const uint32_t *wb = wbase + static_cast<int64_t>(l) * 4;
+    uint64_t acc = 0;
+    for (int k = 0; k < 4; ++k) {
+        uint64_t m = pres[k];
+        if (k == 3) m &= ~(1ull << 63);  // the absent value has no prefix plane
+        while (m) {
+            const uint32_t v = static_cast<uint32_t>(k * 64 + __builtin_ctzll(m));
+            m &= m - 1;
+            const uint32_t pid = plane_id(pres, wb, v);
+            acc |= planes[static_cast<int64_t>(pid) * Wp + w];
+            planes[static_cast<int64_t>(pfx0 + pid) * Wp + w] = acc;
+        }
+    }
+}
+
 // Value planes of the node labels: presence, plane numbering (d_P = P),
 // the planes themselves, and the all-zero plane pmax.
 int build_planes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, int64_t W, int64_t Wp, int64_t pmax,
@@ -1454,6 +1550,20 @@ int build_planes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, int64
                  hipLaunchKernelGGL(k_sel_planes, gb, dim3(256), 0, stream, labels, N, L, present, wbase, planes, Wp));
         PC_LAUNCH_CHECK(ctx);
     }
+    return PC_OK;
+}
+
+// The prefix planes pmax + 1 + [0, pmax) of the affinity paths (after
+// build_planes).
+int build_prefix(pc_ctx *ctx, int32_t L, int64_t Wp, int64_t pmax, const uint64_t *present, const uint32_t *wbase,
+                 uint64_t *planes, hipStream_t stream)
+{
+    const int64_t n = static_cast<int64_t>(L) * Wp;
+    if (n == 0) return PC_OK;
+    PC_TIMED(ctx, "k_aff_prefix", stream,
+             hipLaunchKernelGGL(k_aff_prefix, dim3(static_cast<unsigned>((n + 255) / 256)), dim3(256), 0, stream,
+                                present, wbase, L, planes, Wp, static_cast<uint32_t>(pmax + 1)));
+    PC_LAUNCH_CHECK(ctx);
     return PC_OK;
 }
 
@@ -1564,7 +1674,9 @@ int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const
     const EvalGeom geo = eval_geom(N);
     const int64_t W = geo.W, Wp = geo.Wp, ntiles = geo.ntiles;
     const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
-    const size_t plane_bytes = static_cast<size_t>(pmax + 1) * static_cast<size_t>(Wp) * 8;
+    // value planes [0, pmax), the all-zero plane pmax, prefix planes pmax + 1 + [0, pmax)
+    const int64_t ptop = 2 * pmax;
+    const size_t plane_bytes = static_cast<size_t>(ptop + 1) * static_cast<size_t>(Wp) * 8;
     if (plane_bytes > (size_t(64) << 30))
         return pc_set_error(ctx, PC_ENOMEM, "pc_eval_affinity: value planes need %zu bytes (L=%d N=%d)", plane_bytes,
                             L, N);
@@ -1578,7 +1690,7 @@ int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const
     auto carve = [&](Carver &cv) {
         present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
         wbase = cv.take<uint32_t>(static_cast<size_t>(L) * 4 + 1);
-        planes = cv.take<uint64_t>(static_cast<size_t>(pmax + 1) * Wp + 2);
+        planes = cv.take<uint64_t>(static_cast<size_t>(ptop + 1) * Wp + 2);
         prog = cv.take<uint32_t>(static_cast<size_t>(prog_cap));
         rec = cv.take<uint32_t>(static_cast<size_t>(I) * kRecWords + kRecWords);
         part = ntiles > 1 ? cv.take<uint32_t>(static_cast<size_t>(ntiles) * I + 1) : nullptr;
@@ -1605,14 +1717,16 @@ int run_affinity(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, const
     launch_fill_u64(reinterpret_cast<uint64_t *>(prog_used), 1, 0, stream);
     rc = build_planes(ctx, labels, N, L, W, Wp, pmax, present, wbase, planes, d_P, stream);
     if (rc) return rc;
+    rc = build_prefix(ctx, L, Wp, pmax, present, wbase, planes, stream);
+    if (rc) return rc;
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
     PC_TIMED(ctx, "k_aff_compile", stream,
              hipLaunchKernelGGL(k_aff_compile, dim3(rgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
                                 preds, n_preds, L, present, wbase, prog, prog_cap,
-                                prog_used, rec, unknown));
+                                prog_used, rec, unknown, static_cast<uint32_t>(pmax + 1)));
     PC_LAUNCH_CHECK(ctx);
     if (W == 0) return PC_OK;
-    return launch_eval<true>(ctx, rec, prog, row_off, preds, present, wbase, planes, pmax, Wp, I, W, N, feasible,
+    return launch_eval<true>(ctx, rec, prog, row_off, preds, present, wbase, planes, ptop, Wp, I, W, N, feasible,
                              popcnt, part, ntiles, term_off, n_preds, L, geo.shift, stream);
 }
 
@@ -1625,7 +1739,8 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     const int64_t ntiles = (W + kTileW - 1) / kTileW;
     const int64_t Wp = kPad + ntiles * kTileW;  // unshifted tiles: every lane's pair lies inside a plane row
     const int64_t pmax = static_cast<int64_t>(L) * (N < 256 ? N : 256);
-    const size_t plane_bytes = static_cast<size_t>(pmax + 1) * static_cast<size_t>(Wp) * 8;
+    const int64_t ptop = 2 * pmax;  // value planes, the all-zero plane pmax, prefix planes
+    const size_t plane_bytes = static_cast<size_t>(ptop + 1) * static_cast<size_t>(Wp) * 8;
     if (plane_bytes > (size_t(64) << 30))
         return pc_set_error(ctx, PC_ENOMEM, "pc_score_preferred: value planes need %zu bytes (L=%d N=%d)",
                             plane_bytes, L, N);
@@ -1638,7 +1753,7 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     auto carve = [&](Carver &cv) {
         present = cv.take<uint64_t>(static_cast<size_t>(L) * 4 + 1);
         wbase = cv.take<uint32_t>(static_cast<size_t>(L) * 4 + 1);
-        planes = cv.take<uint64_t>(static_cast<size_t>(pmax + 1) * Wp + 2);
+        planes = cv.take<uint64_t>(static_cast<size_t>(ptop + 1) * Wp + 2);
         prog = cv.take<uint32_t>(static_cast<size_t>(prog_cap));
         rec = cv.take<uint32_t>(static_cast<size_t>(I) * kPrefRec + kPrefRec);
         list = cv.take<int32_t>(static_cast<size_t>(I) * kPrefClasses + 1);
@@ -1670,11 +1785,13 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
     if (!feasible && W > 0) launch_fill_u64(ones, static_cast<size_t>(W), ~0ull, stream);
     rc = build_planes(ctx, labels, N, L, W, Wp, pmax, present, wbase, planes, d_P, stream);
     if (rc) return rc;
+    rc = build_prefix(ctx, L, Wp, pmax, present, wbase, planes, stream);
+    if (rc) return rc;
     const unsigned rgrid = static_cast<unsigned>(std::min<int64_t>((I + 255) / 256, 8192));
     PC_TIMED(ctx, "k_pref_compile", stream,
              hipLaunchKernelGGL(k_pref_compile, dim3(rgrid), dim3(256), 0, stream, row_off, I, term_off, n_terms,
                                 weight, preds, n_preds, L, present, wbase, prog, prog_cap, prog_used, rec, list,
-                                list_len));
+                                list_len, static_cast<uint32_t>(pmax + 1)));
     PC_LAUNCH_CHECK(ctx);
     if (W > 0) {
         int64_t nchunks = std::max<int64_t>((32768 + ntiles - 1) / ntiles, 1);
@@ -1683,7 +1800,7 @@ int run_preferred(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, cons
         nchunks = (I + rpc - 1) / rpc;
         const int64_t total = ntiles * nchunks;
         const unsigned blocks = static_cast<unsigned>(8 * ((total + 7) / 8));
-        const int64_t pbytes = static_cast<int64_t>(pmax + 1) * Wp * 8;
+        const int64_t pbytes = static_cast<int64_t>(ptop + 1) * Wp * 8;
         auto eval = [&](auto kern, const char *name) {
             PC_TIMED(ctx, name, stream,
                      hipLaunchKernelGGL(kern, dim3(blocks), dim3(kEvalThreads), 0, stream, rec, prog, row_off, term_off,
