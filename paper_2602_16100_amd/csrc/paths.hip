@@ -30,7 +30,7 @@
 
 namespace {
 
-constexpr int kPsThreads = 256;
+constexpr int kPsThreads = 512;  // 8 wavefronts: four such workgroups fit a CU's LDS at fat-tree sizes
 constexpr int kPsWaves = kPsThreads / 64;
 constexpr int32_t kInf = INT32_MAX;
 
