@@ -10,17 +10,20 @@
 //                 pairs of the links u -> v -- counted, scanned and filled.
 //   3. search   : one workgroup per request.  Its usable-switch bitset,
 //                 distances and frontier queues live in LDS.  Each leg is
-//                 a chaotic relaxation in rounds: a wavefront takes a
-//                 frontier switch and its lanes relax the switch's ports
-//                 with LDS atomic minima; a switch whose distance drops
-//                 joins the next round's frontier once (a flag bit per
-//                 switch).  A frontier switch at or beyond the target's
+//                 a chaotic relaxation in rounds: a wavefront takes 64
+//                 frontier switches at a time (one lane each reads the
+//                 port range), then relaxes them one after another, its
+//                 lanes over a switch's ports with LDS atomic minima,
+//                 loading the next switch's links while the current one's
+//                 are relaxed; a switch whose distance drops joins the next
+//                 round's frontier once (a flag bit per switch).  A frontier switch at or beyond the target's
 //                 current distance is skipped: with weights >= 1 it cannot
 //                 shorten the target's path, so every switch nearer than
 //                 the target ends with its exact distance.  The leg is then
 //                 walked back from its end by one wavefront: the
 //                 predecessor of v is the lowest-numbered u among v's
-//                 in-links with dist(u) + w = dist(v) (a wavefront minimum).
+//                 in-links with dist(u) + w = dist(v) (a wavefront minimum;
+//                 the in-link lists carry each link's weight).
 //                 The legs' switches collect in an LDS walk; the rules are
 //                 written from it, one wavefront per switch finding the port
 //                 of least (weight, index) to the next switch.
@@ -105,7 +108,7 @@ __global__ __launch_bounds__(256) void k_ps_in_count(int32_t V, const int32_t *_
         if (link_weight(port_peer, weight, V, p)) atomicAdd(&cnt[port_peer[p]], 1);
 }
 
-// In-link lists: (u, port) pairs in rin[rin_off[v] ..); cursor starts as a
+// In-link lists: (u, link weight) pairs in rin[rin_off[v] ..); cursor starts as a
 // copy of rin_off.  The order within a list is arbitrary (only minima are
 // taken over it).
 __global__ __launch_bounds__(256) void k_ps_in_fill(int32_t V, const int32_t *__restrict__ port_off,
@@ -117,11 +120,13 @@ __global__ __launch_bounds__(256) void k_ps_in_fill(int32_t V, const int32_t *__
     if (u >= V) return;
     const int64_t b = port_off[u], e = port_off[u + 1];
     if (!pc_range_ok(b, e, n_ports)) return;
-    for (int64_t p = b; p < e; ++p)
-        if (link_weight(port_peer, weight, V, p)) {
+    for (int64_t p = b; p < e; ++p) {
+        const uint32_t w = link_weight(port_peer, weight, V, p);
+        if (w) {
             const int32_t pos = atomicAdd(&cursor[port_peer[p]], 1);
-            rin[pos] = make_int2(u, static_cast<int32_t>(p));
+            rin[pos] = make_int2(u, static_cast<int32_t>(w));  // the weight's bits
         }
+    }
 }
 
 // One workgroup per request (see the file header).  Dynamic LDS: dist,
@@ -158,13 +163,12 @@ __global__ __launch_bounds__(kPsThreads) void k_ps_search(
         fail = !pc_range_ok(tb, te, n_ports) || out_port[q] < 0 || out_port[q] >= te - tb;
     }
     const uint32_t A = allowed[q];
-    for (int32_t w = tid; w < VW; w += kPsThreads) {
-        uint32_t bits = 0;
-        for (int b = 0; b < 32; ++b) {
-            const int32_t v = w * 32 + b;
-            if (v < V && region[v] < 32 && ((A >> region[v]) & 1)) bits |= 1u << b;
-        }
-        usable[w] = bits;
+    // usable bits: each wavefront takes 64 switches (two words) at a time
+    for (int32_t v0 = wave * 64; v0 < V; v0 += kPsWaves * 64) {
+        const int32_t v = v0 + lane;
+        const uint32_t r = v < V ? region[v] : 32u;
+        const uint64_t m = __ballot(r < 32 && ((A >> r) & 1u));
+        if (lane < 2 && (v0 >> 5) + lane < VW) usable[(v0 >> 5) + lane] = static_cast<uint32_t>(m >> (32 * lane));
     }
     __syncthreads();
     if (tid < Kf) {
@@ -196,26 +200,89 @@ __global__ __launch_bounds__(kPsThreads) void k_ps_search(
         __syncthreads();
         int32_t nf = 1;
         int32_t *cur = qa, *nxt = qb;
+        // Port p's peer and weight: unconditional loads (an index past the
+        // switch's last port is clamped to it; the caller drops that lane),
+        // whose results nothing touches before relax, so that a wavefront's
+        // next switch is fetched while the current one is relaxed.
+        const uint32_t *wsrc = weight ? weight : reinterpret_cast<const uint32_t *>(port_peer);
+        auto fetch = [&](int64_t p, int64_t e, int32_t &u, uint32_t &w) {
+            const int64_t pc = p < e ? p : e - 1;
+            u = port_peer[pc];
+            w = wsrc[pc];
+        };
+        // (dto: the target's distance when the switch was taken, an upper
+        // bound of the current one, so the pruning stays safe)
+        auto relax = [&](int32_t u, uint32_t w, int32_t dv, int32_t dto, int32_t *nxt) {
+            if (!weight) w = 1u;
+            const bool link = u >= 0 && u < V && w;
+            const int32_t uc = link ? u : 0;
+            const uint32_t ubits = usable[uc >> 5];  // both LDS reads issued together
+            const int32_t du = dist[uc];
+            const int64_t nd64 = static_cast<int64_t>(dv) + w;
+            if (!link || !((ubits >> (uc & 31)) & 1u) || nd64 >= du || nd64 >= dto) return;
+            const int32_t nd = static_cast<int32_t>(nd64);
+            const int32_t old = atomicMin(&dist[u], nd);
+            if (nd < old) {
+                const uint32_t bit = 1u << (u & 31);
+                if (!(atomicOr(&inflag[u >> 5], bit) & bit)) nxt[atomicAdd(&s_nf, 1)] = u;
+            }
+        };
         while (nf > 0) {
-            for (int32_t i = wave; i < nf; i += kPsWaves) {
-                const int32_t v = cur[i];
-                const int32_t dv = dist[v];
-                if (dv >= dist[to]) continue;  // cannot shorten the target's path
-                const int64_t b = port_off[v], e = port_off[v + 1];
-                if (!pc_range_ok(b, e, n_ports)) continue;
-                for (int64_t p = b + lane; p < e; p += 64) {
-                    const uint32_t w = link_weight(port_peer, weight, V, p);
-                    if (!w) continue;
-                    const int32_t u = port_peer[p];
-                    if (!is_usable(u)) continue;
-                    const int64_t nd64 = static_cast<int64_t>(dv) + w;
-                    if (nd64 >= dist[u] || nd64 >= dist[to]) continue;
-                    const int32_t nd = static_cast<int32_t>(nd64);
-                    const int32_t old = atomicMin(&dist[u], nd);
-                    if (nd < old) {
-                        const uint32_t bit = 1u << (u & 31);
-                        if (!(atomicOr(&inflag[u >> 5], bit) & bit)) nxt[atomicAdd(&s_nf, 1)] = u;
+            // Wavefront `wave` takes frontier entries wave, wave + kPsWaves, ...
+            // in batches of 64: each lane reads one entry's port range (one
+            // round of loads for 64 switches), then the switches are
+            // relaxed one after another, each one's first 64 links loaded
+            // while the previous one's are relaxed (two register sets, A
+            // and B, in turn).
+            for (int32_t base = wave; base < nf; base += kPsWaves * 64) {
+                const int32_t idx = base + lane * kPsWaves;
+                int32_t vl = 0, bl = 0, el = 0;
+                if (idx < nf) {
+                    vl = cur[idx];
+                    if (dist[vl] < dist[to]) {  // else it cannot shorten the target's path
+                        const int32_t b = port_off[vl], e = port_off[vl + 1];
+                        if (pc_range_ok(b, e, n_ports)) {
+                            bl = b;
+                            el = e;
+                        }
                     }
+                }
+                uint64_t live = __ballot(el > bl);
+                if (!live) continue;
+                // the next switch of the batch (none left: `prev` again, with more = false)
+                auto take = [&](int32_t prev, bool &more, int32_t &b, int32_t &e) {
+                    more = live != 0;
+                    const int32_t jj = more ? static_cast<int32_t>(__builtin_ctzll(live)) : prev;
+                    live &= live - 1;
+                    b = __builtin_amdgcn_readlane(bl, jj);
+                    e = __builtin_amdgcn_readlane(el, jj);
+                    return jj;
+                };
+                auto expand = [&](int32_t jj, int32_t b, int32_t e, int32_t u, uint32_t w) {
+                    const int32_t dv = dist[__builtin_amdgcn_readlane(vl, jj)];  // current: it may have dropped
+                    const int32_t dto = dist[to];
+                    if (static_cast<int64_t>(b) + lane < e) relax(u, w, dv, dto, nxt);
+                    for (int64_t p = static_cast<int64_t>(b) + 64 + lane; p < e; p += 64) {
+                        int32_t u2;
+                        uint32_t w2;
+                        fetch(p, e, u2, w2);
+                        relax(u2, w2, dv, dto, nxt);
+                    }
+                };
+                bool more;
+                int32_t bA, eA, bB, eB, uA, uB;
+                uint32_t wA, wB;
+                int32_t jA = take(0, more, bA, eA);
+                fetch(static_cast<int64_t>(bA) + lane, eA, uA, wA);
+                while (true) {
+                    const int32_t jB = take(jA, more, bB, eB);
+                    fetch(static_cast<int64_t>(bB) + lane, eB, uB, wB);
+                    expand(jA, bA, eA, uA, wA);
+                    if (!more) break;
+                    jA = take(jB, more, bA, eA);
+                    fetch(static_cast<int64_t>(bA) + lane, eA, uA, wA);
+                    expand(jB, bB, eB, uB, wB);
+                    if (!more) break;
                 }
             }
             __syncthreads();
@@ -248,7 +315,7 @@ __global__ __launch_bounds__(kPsThreads) void k_ps_search(
                 for (int32_t k = rin_off[c] + lane; k < rin_off[c + 1]; k += 64) {
                     const int2 in = rin[k];
                     const int32_t du = dist[in.x];
-                    if (du != kInf && static_cast<int64_t>(du) + link_weight(port_peer, weight, V, in.y) == dc)
+                    if (du != kInf && static_cast<int64_t>(du) + static_cast<uint32_t>(in.y) == dc)
                         best = min(best, in.x);
                 }
                 best = wave_min_i32(best);
