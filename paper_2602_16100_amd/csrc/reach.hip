@@ -198,10 +198,16 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                                                               const int32_t *__restrict__ perm)
 {
     extern __shared__ uint64_t lds[];
+    // visited / frontier / next words of vertex v sit in slot sl(v) =
+    // v ^ ((v >> 4) & 15), a permutation of each block of 16, so that
+    // vertices a multiple of 16 apart (a core switch's aggregation peers,
+    // one per pod) fall in different LDS banks; Vp slots each
+    const int32_t Vp = (V + 15) & ~15;
+    auto sl = [](int32_t v) { return v ^ ((v >> 4) & 15); };
     uint64_t *vis = lds;
-    uint64_t *fr = vis + V;
-    uint64_t *nx = fr + V;
-    uint64_t *rmask = nx + V;                                               // [32]
+    uint64_t *fr = vis + Vp;
+    uint64_t *nx = fr + Vp;
+    uint64_t *rmask = nx + Vp;                                              // [32]
     uint8_t *reg = reinterpret_cast<uint8_t *>(rmask + 32);                 // [V]
     uint16_t *flist = reinterpret_cast<uint16_t *>(reg + ((V + 3) & ~3));  // [V] frontier vertices
     __shared__ int32_t nfr[2];                                              // list lengths, by level parity
@@ -218,11 +224,11 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     const int32_t q0 = blockIdx.x * 64;
     const int32_t nq = min(64, Q - q0);
     if (tid < 64) qid[lane] = lane < nq ? (perm ? perm[q0 + lane] : q0 + lane) : 0;
-    for (int32_t v = tid; v < V; v += kBitsetThreads) {
+    for (int32_t v = tid; v < Vp; v += kBitsetThreads) {
         vis[v] = 0;
         fr[v] = 0;
         nx[v] = 0;
-        reg[v] = region[v];
+        if (v < V) reg[v] = region[v];
     }
     if (tid < 64) {
         const uint32_t A = lane < nq ? allowed[qid[lane] / qdiv] : 0u;
@@ -239,7 +245,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
             const int32_t *fl = forbid + static_cast<int64_t>(qid[lane] / qdiv) * Kf;
             for (int32_t k = 0; k < Kf; ++k) {
                 const int32_t f = fl[k];
-                if (f >= 0 && f < V) atomicOr(reinterpret_cast<unsigned long long *>(&vis[f]), 1ull << lane);
+                if (f >= 0 && f < V) atomicOr(reinterpret_cast<unsigned long long *>(&vis[sl(f)]), 1ull << lane);
             }
         }
         __syncthreads();
@@ -250,25 +256,25 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
     if (tid < 64 && lane < nq) {
         const int32_t q = qid[lane];
         const int32_t s = src[q];
-        const bool s_ok = s >= 0 && s < V && allowed_v(reg, allowed[q / qdiv], s) && !((vis[s] >> lane) & 1);
+        const bool s_ok = s >= 0 && s < V && allowed_v(reg, allowed[q / qdiv], s) && !((vis[sl(s)] >> lane) & 1);
         if (target) {
             // a target that is not allowed, or forbidden, is never reached:
             // the query is resolved (-1) without a search
             tgt = target[q];
             done = !(s_ok && tgt >= 0 && tgt < V && allowed_v(reg, allowed[q / qdiv], tgt) &&
-                     !((vis[tgt] >> lane) & 1));
+                     !((vis[sl(tgt)] >> lane) & 1));
         }
         if (s_ok) {
-            atomicOr(reinterpret_cast<unsigned long long *>(&fr[s]), 1ull << lane);
-            atomicOr(reinterpret_cast<unsigned long long *>(&vis[s]), 1ull << lane);
+            atomicOr(reinterpret_cast<unsigned long long *>(&fr[sl(s)]), 1ull << lane);
+            atomicOr(reinterpret_cast<unsigned long long *>(&vis[sl(s)]), 1ull << lane);
             if (!target) dist[static_cast<int64_t>(q) * V + s] = 0;
         }
     }
     __syncthreads();
     for (int32_t v = tid; v < V; v += kBitsetThreads)
-        wave_append(fr[v] != 0, static_cast<uint16_t>(v), &nfr[0], flist);
+        wave_append(fr[sl(v)] != 0, static_cast<uint16_t>(v), &nfr[0], flist);
     if (tid < 64) {
-        if (!done && ((vis[tgt] >> lane) & 1)) {
+        if (!done && ((vis[sl(tgt)] >> lane) & 1)) {
             res = 0;
             done = true;
         }
@@ -322,7 +328,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                 if (pc_range_ok(b64, e64, n_adj)) {
                     b = static_cast<int32_t>(b64);
                     e = static_cast<int32_t>(e64);
-                    const uint64_t f = fr[u];
+                    const uint64_t f = fr[sl(u)];
                     flo = static_cast<uint32_t>(f);
                     fhi = static_cast<uint32_t>(f >> 32);
                 }
@@ -334,18 +340,19 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                                     static_cast<uint32_t>(__shfl(flo, k, GS));
                 for (int32_t p = bk + gl; p < ek; p += GS) {
                     const int32_t v = adj[p];
-                    if (v >= 0 && v < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[v]), fk);
+                    if (v >= 0 && v < V) atomicOr(reinterpret_cast<unsigned long long *>(&nx[sl(v)]), fk);
                 }
             }
         }
         __syncthreads();
         for (int32_t v = tid; v < V; v += kBitsetThreads) {
-            uint64_t n = nx[v];
+            const int32_t x = sl(v);
+            uint64_t n = nx[x];
             if (n) {
-                nx[v] = 0;
+                nx[x] = 0;
                 const uint32_t r = reg[v];
-                n &= (r < 32 ? rmask[r] : 0ull) & ~vis[v] & live;
-                vis[v] |= n;
+                n &= (r < 32 ? rmask[r] : 0ull) & ~vis[x] & live;
+                vis[x] |= n;
                 if (!target) {
                     uint64_t m = n;
                     while (m) {
@@ -355,7 +362,7 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                     }
                 }
             }
-            fr[v] = n;
+            fr[x] = n;
             wave_append(n != 0, static_cast<uint16_t>(v), &nfr[cur ^ 1], flist);
         }
         if (tid == 0) found = 0;
@@ -373,13 +380,13 @@ __global__ __launch_bounds__(kBitsetThreads) void k_rc_bitset(int32_t V, const i
                     }
                     if (!((a >> lo) & 1)) continue;
                     const int32_t u = adj[tbeg[lo] + (i - toff[lo])];
-                    if (u >= 0 && u < V && ((fr[u] >> lo) & 1)) atomicOr(&found, 1ull << lo);
+                    if (u >= 0 && u < V && ((fr[sl(u)] >> lo) & 1)) atomicOr(&found, 1ull << lo);
                 }
             }
             __syncthreads();
         }
         if (tid < 64) {
-            if (!done && ((fr[tgt] >> lane) & 1)) {
+            if (!done && ((fr[sl(tgt)] >> lane) & 1)) {
                 res = d;
                 done = true;
             } else if (!done && target && ((found >> lane) & 1)) {
@@ -511,8 +518,8 @@ int bfs(pc_ctx *ctx, int32_t V, const int32_t *adj_off, const int32_t *adj, int6
     int max_lds = 0;
     PC_HIP(ctx, hipDeviceGetAttribute(&max_lds, hipDeviceAttributeMaxSharedMemoryPerBlock, ctx->device));
     // visited / frontier / next (8 B each), region (1 B) and list (2 B) per vertex
-    const size_t lds = static_cast<size_t>(V) * 3 * 8 + 32 * 8 + ((static_cast<size_t>(V) + 3) & ~size_t(3)) +
-                       static_cast<size_t>(V) * 2;
+    const size_t lds = ((static_cast<size_t>(V) + 15) & ~size_t(15)) * 3 * 8 + 32 * 8 +
+                       ((static_cast<size_t>(V) + 3) & ~size_t(3)) + static_cast<size_t>(V) * 2;
     hipFuncAttributes fa{};
     PC_HIP(ctx, hipFuncGetAttributes(&fa, reinterpret_cast<const void *>(k_rc_bitset<16>)));  // static LDS
     if (V <= kMaxBitsetV && lds + fa.sharedSizeBytes <= static_cast<size_t>(max_lds)) {
