@@ -17,7 +17,10 @@
 //            adjacency reads) with 64-bit LDS atomic OR, the per-query
 //            allowed mask applied per vertex as a precomputed 64-bit region
 //            mask; stops when every query's target is resolved or no
-//            frontier bit is left.
+//            frontier bit is left.  The per-vertex words sit in XOR-swizzled
+//            slots: vertices 16 apart map to different LDS banks (unswizzled,
+//            a fat-tree core's pushes to its per-pod peers, 48 apart, all
+//            hit one bank pair).
 //   queue  : larger graphs: one workgroup per query, frontier queue in
 //            scratch, the distance row itself (or a scratch row, with
 //            targets) as the visited set claimed with compare-and-swap.
