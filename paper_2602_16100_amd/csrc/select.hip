@@ -526,25 +526,55 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
                 unknown[i] = 0;
                 return;
             }
+            // One pass over the row's expressions: the inventory flags (every
+            // well-formed expression of every term with valid offsets), and
+            // each term's entries emitted into the record's inline area as
+            // they come (counted past its end) and taken back when the term
+            // turns out to hold nowhere (a malformed expression, an empty
+            // clause).  A live term with no entries holds everywhere, and so
+            // does the row.
             uint32_t unk = 0;
+            bool all = tb == te;
+            int64_t n = 0, live = 0, k_out = 0;
+            uint32_t *in_out = rr + 1;
             for (int64_t t = tb; t < te; ++t) {
                 const int64_t b = term_off[t], e = term_off[t + 1];
                 if (!pc_range_ok(b, e, n_preds)) continue;
+                bool ok = b != e;
+                const int64_t start = k_out;
+                int64_t len = 0;
                 for (int64_t p = b; p < e; ++p) {
                     const pc_pred q = preds[p];
-                    if (aff_valid(q, L)) unk |= aff_unknown(q, present + static_cast<int64_t>(q.label) * 4);
+                    if (!aff_valid(q, L)) {
+                        ok = false;
+                        continue;
+                    }
+                    const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
+                    unk |= aff_unknown(q, pres);
+                    if (!ok || all) continue;
+                    bool neg;
+                    const uint32_t cnt = aff_entries(q, pres, wbase + static_cast<int64_t>(q.label) * 4, pfx0, neg,
+                                                     [&](uint32_t ent) {
+                                                         if (k_out < kInline) in_out[k_out] = ent;
+                                                         ++k_out;
+                                                     });
+                    if (cnt == 0 && !neg) ok = false;
+                    len += cnt;
                 }
-            }
-            unknown[i] = static_cast<uint8_t>(unk);
-            bool all = tb == te;
-            int64_t n = 0, live = 0;
-            for (int64_t t = tb; t < te && !all; ++t) {
-                int64_t len;
-                if (!aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len)) continue;
-                if (len == 0) all = true;
+                if (all) continue;
+                if (!ok) {
+                    k_out = start;
+                    continue;
+                }
+                if (len == 0) {
+                    all = true;
+                    continue;
+                }
+                if (k_out <= kInline) in_out[k_out - 1] |= kTermEnd;
                 n += len;
                 ++live;
             }
+            unknown[i] = static_cast<uint8_t>(unk);
             if (all) {
                 rr[0] = 0;
                 return;
@@ -553,21 +583,23 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
                 rr[0] = static_cast<uint32_t>(kRowFalse);
                 return;
             }
-            const bool inl = n <= kInline;
-            uint32_t *out = rr + 1;
-            if (!inl) {
-                // slices are whole multiples of 4 entries: the record stores off / 4
-                const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>((n + 3) & ~int64_t(3)));
-                if (static_cast<int64_t>(off) + n > prog_cap) {
-                    rr[0] = static_cast<uint32_t>(kRowLong);
-                    return;
-                }
-                out = prog + off;
-                rr[0] = static_cast<uint32_t>(kRowIndirect);
-                rr[1] = static_cast<uint32_t>(off / 4);
-                rr[2] = static_cast<uint32_t>(n);
+            if (n <= kInline) {
+                rr[0] = static_cast<uint32_t>(n);
+                return;
             }
-            int64_t k_out = 0;
+            // longer than the inline area: a slice of prog, written by a
+            // second pass (slices are whole multiples of 4 entries: the
+            // record stores off / 4)
+            const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>((n + 3) & ~int64_t(3)));
+            if (static_cast<int64_t>(off) + n > prog_cap) {
+                rr[0] = static_cast<uint32_t>(kRowLong);
+                return;
+            }
+            uint32_t *out = prog + off;
+            rr[0] = static_cast<uint32_t>(kRowIndirect);
+            rr[1] = static_cast<uint32_t>(off / 4);
+            rr[2] = static_cast<uint32_t>(n);
+            int64_t k2 = 0;
             for (int64_t t = tb; t < te; ++t) {
                 const int64_t b = term_off[t], e = term_off[t + 1];
                 int64_t len;
@@ -576,11 +608,10 @@ __global__ __launch_bounds__(256) void k_aff_compile(const int32_t *__restrict__
                     const pc_pred q = preds[p];
                     bool neg;
                     aff_entries(q, present + static_cast<int64_t>(q.label) * 4, wbase + static_cast<int64_t>(q.label) * 4,
-                                pfx0, neg, [&](uint32_t ent) { out[k_out++] = ent; });
+                                pfx0, neg, [&](uint32_t ent) { out[k2++] = ent; });
                 }
-                out[k_out - 1] |= kTermEnd;
+                out[k2 - 1] |= kTermEnd;
             }
-            if (inl) rr[0] = static_cast<uint32_t>(n);
         }();
         uint4 *dst = reinterpret_cast<uint4 *>(rec + static_cast<int64_t>(i) * kRecWords);
 #pragma unroll
