@@ -1048,45 +1048,78 @@ __device__ uint32_t pref_compile_row(const int32_t *__restrict__ row_off, int32_
     rr[0] = kPrefNone << 24;
     if (!pref_row_ok(row_off, i, n_terms)) return 3;
     const int64_t tb = row_off[i], te = row_off[i + 1];
-    int64_t n = 0;
+    // One pass: each live term's header and entries go into the record's
+    // inline words as they come (counted past their end); a term that turns
+    // out dead (weight out of range, a malformed expression, an empty
+    // clause) is taken back.  Programs past the inline words are written
+    // again, into a slice of prog.
+    int64_t n = 0, k_out = 0;
     uint32_t live = 0, sum = 0;
     bool decode = false;
+    uint32_t *in_out = rr + 2;
+    auto put = [&](uint32_t word) {
+        if (k_out < kPrefInlineWords) in_out[k_out] = word;
+        ++k_out;
+    };
     for (int64_t t = tb; t < te; ++t) {
-        int64_t len;
-        if (!pref_weight_ok(weight[t]) || !aff_term(preds, term_off[t], term_off[t + 1], n_preds, L, present, len))
+        const uint32_t w = weight[t];
+        const int64_t b = term_off[t], e = term_off[t + 1];
+        if (!pref_weight_ok(w) || !pc_range_ok(b, e, n_preds) || b == e) continue;
+        const int64_t start = k_out;
+        put(0u);  // the header, set below
+        bool ok = true;
+        int64_t len = 0;
+        for (int64_t p = b; p < e && ok; ++p) {
+            const pc_pred q = preds[p];
+            if (!aff_valid(q, L)) {
+                ok = false;
+                break;
+            }
+            bool neg;
+            const uint32_t cnt = aff_entries(q, present + static_cast<int64_t>(q.label) * 4,
+                                             wbase + static_cast<int64_t>(q.label) * 4, pfx0, neg, put);
+            if (cnt == 0 && !neg) ok = false;
+            len += cnt;
+        }
+        if (!ok) {
+            k_out = start;
             continue;
+        }
         if (len >= (int64_t(1) << kPrefLenBits)) decode = true;
+        if (start < kPrefInlineWords) in_out[start] = w << kPrefLenBits | static_cast<uint32_t>(len);
         n += 1 + len;
-        sum += weight[t];
+        sum += w;
         ++live;
     }
     if (live == 0) return 3;
     const uint32_t head = live | bit_length(sum) << 16;
-    uint32_t *out = rr + 2;
     uint32_t kind = kPrefInline;
     if (!decode && n > kPrefInlineWords) {
         const unsigned long long off = atomicAdd(prog_used, static_cast<unsigned long long>(n));
         decode = static_cast<int64_t>(off) + n > prog_cap;
-        out = prog + off;
-        rr[1] = static_cast<uint32_t>(off);
-        kind = kPrefIndirect;
+        if (!decode) {
+            uint32_t *out = prog + off;
+            rr[1] = static_cast<uint32_t>(off);
+            kind = kPrefIndirect;
+            int64_t k2 = 0;
+            for (int64_t t = tb; t < te; ++t) {
+                const int64_t b = term_off[t], e = term_off[t + 1];
+                int64_t len;
+                if (!pref_weight_ok(weight[t]) || !aff_term(preds, b, e, n_preds, L, present, len)) continue;
+                out[k2++] = weight[t] << kPrefLenBits | static_cast<uint32_t>(len);
+                for (int64_t p = b; p < e; ++p) {
+                    const pc_pred q = preds[p];
+                    bool neg;
+                    aff_entries(q, present + static_cast<int64_t>(q.label) * 4,
+                                wbase + static_cast<int64_t>(q.label) * 4, pfx0, neg,
+                                [&](uint32_t ent) { out[k2++] = ent; });
+                }
+            }
+        }
     }
     if (decode) {
         rr[0] = head | kPrefDecode << 24;
         return 2;
-    }
-    int64_t k_out = 0;
-    for (int64_t t = tb; t < te; ++t) {
-        const int64_t b = term_off[t], e = term_off[t + 1];
-        int64_t len;
-        if (!pref_weight_ok(weight[t]) || !aff_term(preds, b, e, n_preds, L, present, len)) continue;
-        out[k_out++] = weight[t] << kPrefLenBits | static_cast<uint32_t>(len);
-        for (int64_t p = b; p < e; ++p) {
-            const pc_pred q = preds[p];
-            bool neg;
-            aff_entries(q, present + static_cast<int64_t>(q.label) * 4, wbase + static_cast<int64_t>(q.label) * 4, pfx0,
-                        neg, [&](uint32_t ent) { out[k_out++] = ent; });
-        }
     }
     rr[0] = head | kind << 24;
     if (live <= kPrefFewTerms) return 3;
