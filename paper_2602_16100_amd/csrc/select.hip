@@ -371,39 +371,18 @@ __global__ __launch_bounds__(kCompThreads) void k_sel_compile(const int32_t *__r
                 R[0] = static_cast<uint32_t>(kRowFalse);
                 return;
             }
+            // one pass: validity, sizes and the inline entries together
+            // (counted past the inline area; a longer program is written
+            // again into prog below)
             bool empty = false;
             int64_t n = 0;
-            for (int64_t p = b; p < e; ++p) {
-                const pc_pred q = preds[p];
-                if (!pred_valid(q.label, q.op, q.rsv0, q.rsv1, q.vals[3], L)) {
-                    errs |= PC_DERR_PRED;
-                    empty = true;
-                    continue;
-                }
-                uint64_t sel[4];
-                bool neg;
-                const uint32_t cnt = pred_clause(q, present + static_cast<int64_t>(q.label) * 4, sel, neg);
-                if (cnt == 0 && !neg) empty = true;  // empty OR: no node (a negated empty OR is every node)
-                n += cnt;
-            }
-            if (empty) {
-                R[0] = static_cast<uint32_t>(kRowFalse);
-                return;
-            }
-            const bool inl = n <= kInline;
-            if (!inl && n > 4 * (e - b)) {
-                R[0] = static_cast<uint32_t>(kRowLong);
-                return;
-            }
-            uint32_t *out = inl ? R + 1 : prog + 4 * b;
-            int64_t k_out = 0;
-            for (int64_t p = b; p < e; ++p) {
-                const pc_pred q = preds[p];
+            auto emit = [&](const pc_pred &q, uint32_t *out, int64_t &k_out, bool bounded) {
                 const uint64_t *pres = present + static_cast<int64_t>(q.label) * 4;
                 const uint32_t *wb = wbase + static_cast<int64_t>(q.label) * 4;
                 uint64_t sel[4];
                 bool neg;
-                uint32_t cnt = pred_clause(q, pres, sel, neg);
+                const uint32_t cnt0 = pred_clause(q, pres, sel, neg);
+                uint32_t cnt = cnt0;
                 for (int k = 0; k < 4; ++k) {
                     uint64_t m = sel[k];
                     while (m) {
@@ -411,17 +390,41 @@ __global__ __launch_bounds__(kCompThreads) void k_sel_compile(const int32_t *__r
                         m &= m - 1;
                         uint32_t ent = plane_id(pres, wb, v);
                         if (--cnt == 0) ent |= kLast | (neg ? kNeg : 0u);
-                        out[k_out++] = ent;
+                        if (!bounded || k_out < kInline) out[k_out] = ent;
+                        ++k_out;
                     }
                 }
+                return cnt0 == 0 && !neg;  // an empty OR: no node (a negated empty OR is every node)
+            };
+            int64_t k_in = 0;
+            for (int64_t p = b; p < e; ++p) {
+                const pc_pred q = preds[p];
+                if (!pred_valid(q.label, q.op, q.rsv0, q.rsv1, q.vals[3], L)) {
+                    errs |= PC_DERR_PRED;
+                    empty = true;
+                    continue;
+                }
+                if (empty) continue;
+                if (emit(q, R + 1, k_in, true)) empty = true;
             }
-            if (inl) {
+            n = k_in;
+            if (empty) {
+                R[0] = static_cast<uint32_t>(kRowFalse);
+                return;
+            }
+            if (n <= kInline) {
                 R[0] = static_cast<uint32_t>(n);  // the evaluator reads entries 1..n only
-            } else {
-                R[0] = static_cast<uint32_t>(kRowIndirect);
-                R[1] = static_cast<uint32_t>(b);
-                R[2] = static_cast<uint32_t>(n);
+                return;
             }
+            if (n > 4 * (e - b)) {
+                R[0] = static_cast<uint32_t>(kRowLong);
+                return;
+            }
+            int64_t k_out = 0;
+            for (int64_t p = b; p < e; ++p) emit(preds[p], prog + 4 * b, k_out, false);
+            R[0] = static_cast<uint32_t>(kRowIndirect);
+            R[1] = static_cast<uint32_t>(b);
+            R[2] = static_cast<uint32_t>(n);
         }();
         uint4 *dst = reinterpret_cast<uint4 *>(rec + i * kRecWords);
 #pragma unroll
