@@ -35,16 +35,16 @@ VALU_PEAK_LANE_OPS = 256 * 64 * 2.4e9
 # kernel source they were measured on.
 TRAFFIC = [
     {"source": "paper_2602_16100_amd/csrc/select.hip",
-     "sha256": "8d597cb0302a22b77d1ef2e3e953faef5e1baa4aedaf63a1d1f7325a189c9c34",
+     "sha256": "3ba266f186a97c69f5525e79cbd1aa8e8de7774ba0177ee4f0f28a75ebc43f74",
      "workload": "cfg5",
-     "bytes_per_launch": {"k_sel_eval": 681_065_472 + 4_407_398_400,
-                          "k_aff_eval": 848_318_464 + 4_408_035_328}},
+     "bytes_per_launch": {"k_sel_eval": 680_687_937 + 4_407_406_605,
+                          "k_aff_eval": 1_360_481_846 + 4_407_121_613}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
-     "sha256": "6e66e8603dc83879de6e617ea2d06440549ee8ec4d90728074d5d6c65b0ed1e5",
+     "sha256": "d4efbf17c6afb8856b911150214aae10905ad83a222f500c7f07d31c7b5dc778",
      "workload": "cfg5",
      # k_tr_match: per step (its 6 launches), like the hop-loop roofline
-     "bytes_per_launch": {"k_tr_prep": 1_888_831_488 + 566_231_040,
-                          "k_tr_match": 2_325_315_584 + 142_243_840}},
+     "bytes_per_launch": {"k_tr_prep": 1_888_826_156 + 566_231_040,
+                          "k_tr_match": 2_325_154_675 + 142_247_667}},
 ]
 
 
@@ -53,9 +53,38 @@ TRAFFIC = [
 # folder).  Valid only for the kernel source they were measured on.
 MATCH_COUNTERS = {
     "cfg5": {"source": "paper_2602_16100_amd/csrc/trace.hip",
-             "sha256": "6e66e8603dc83879de6e617ea2d06440549ee8ec4d90728074d5d6c65b0ed1e5",
+             "sha256": "d4efbf17c6afb8856b911150214aae10905ad83a222f500c7f07d31c7b5dc778",
              "SQ_INSTS_VALU_per_step": 3.891e8, "SQ_INSTS_SALU_per_step": 3.392e8},
 }
+
+
+# Issue counters of the instruction-bound kernels of two passes on the
+# combined workload, per launch (one rocprofv3 pass; the command and values
+# are in the profiles folder): the preferred-affinity evaluator of rows of at
+# most three terms, and the path search.  Valid only for the kernel source
+# they were measured on.
+PASS_COUNTERS = {
+    "k_pref_eval3": {"source": "paper_2602_16100_amd/csrc/select.hip",
+                     "sha256": "3ba266f186a97c69f5525e79cbd1aa8e8de7774ba0177ee4f0f28a75ebc43f74",
+                     "SQ_INSTS_VALU_per_launch": 1.1454e9, "SQ_INSTS_SALU_per_launch": 7.263e8},
+    "k_ps_search": {"source": "paper_2602_16100_amd/csrc/paths.hip",
+                    "sha256": "fbbfbf39657f5d66cb19ee3da30e4d50be65b87fade578a516808c14bf610773",
+                    "SQ_INSTS_VALU_per_launch": 4.348e9, "SQ_INSTS_SALU_per_launch": 3.4636e9},
+}
+
+
+def alu_view(kernel, ms):
+    """The issue-rate view of a kernel whose counters are recorded for its
+    current source: wave-wide VALU instructions per second against the
+    chip's one per CU per clock (in lane-ops/s), and the same rate for SALU."""
+    c = PASS_COUNTERS.get(kernel)
+    if c is None or not source_unchanged(c) or not ms or ms <= 0:
+        return None
+    lane_ops = c["SQ_INSTS_VALU_per_launch"] * 64 / (ms * 1e-3)
+    return {"kernel": kernel, "bound": "alu", "achieved": lane_ops, "peak": VALU_PEAK_LANE_OPS, "unit": "lane-ops/s",
+            "frac": lane_ops / VALU_PEAK_LANE_OPS,
+            "salu_frac": c["SQ_INSTS_SALU_per_launch"] * 64 / (ms * 1e-3) / VALU_PEAK_LANE_OPS,
+            "source": "issue counters (profiles folder)"}
 
 
 def source_unchanged(rec):
@@ -542,7 +571,10 @@ def time_preferred(args, wl, pc, ctx, feasible):
         "roofline": {"kernel": "+".join(classes), "bound": "hbm", "achieved": achieved, "peak": HBM_PEAK_GBS,
                      "unit": "GB/s", "frac": achieved / HBM_PEAK_GBS,
                      "traffic": measured_traffic(args.workload, "k_pref_eval"), "alg_bytes_per_launch": alg,
-                     "avg_launch_ms": avg_ms},
+                     "avg_launch_ms": avg_ms,
+                     # the class that takes every row at this size is instruction bound
+                     "alu": alu_view("k_pref_eval3", prof["k_pref_eval3"][1] / max(prof["k_pref_eval3"][0], 1)
+                                     if "k_pref_eval3" in prof else None)},
         "placed_rows": int((b >= 0).sum()),
         "mean_best_score": float(score.cpu().numpy()[b >= 0].mean()) if (b >= 0).any() else 0.0,
         "data_error_flags": flags,
@@ -795,6 +827,10 @@ def time_synthesis(args, wl, pc, ctx):
         "synthesized": int((h >= 0).sum()),
         "mean_hops": float(h[h >= 0].mean()) if (h >= 0).any() else None,
         "data_error_flags": flags,
+        # the search is instruction and latency bound (no HBM stream to
+        # price): its issue rate, when counters are recorded for its source
+        "roofline": alu_view("k_ps_search", prof["k_ps_search"][1] / max(prof["k_ps_search"][0], 1)
+                             if "k_ps_search" in prof else None),
     }
     if not args.no_cpu_baseline:
         import oracle
