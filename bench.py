@@ -362,7 +362,7 @@ def trace_levels(wl, pc, ctx, D, full):
 
 def trace_roofline(wl, pc, ctx, D, full, prof, steps, workload):
     """k_tr_match, the hop loop's dominant kernel, against the HBM roofline
-    with the survey's algorithmic bytes: 30 B per rule of every switch a
+    with its algorithmic bytes: 30 B per rule of every switch a
     bucketed level touches, plus 32 B per trace (header, ingress, record).
     `layout_bytes` is what this library's layout needs for the same levels
     (384 B of chunk sets per 32-rule group).  The issue counters of the

@@ -131,6 +131,34 @@ def test_affinity_gt_lt_thresholds(g, orc):
     _check(g, orc, labels, *_csr(rows))
 
 
+def test_affinity_gt_lt_sparse_labels(g, orc):
+    """Gt / Lt over labels whose present values are few or extreme (every node
+    absent; one value; only 0 and 254 plus absent; no absent value), alone and
+    inside multi-expression terms of multi-term rows, at thresholds around each
+    present value: the cases where the largest present value below or at the
+    threshold, or the absent value's plane, decide the entries."""
+    rng = np.random.default_rng(16)
+    N = 9000  # two tiles and a ragged tail
+    labels = np.zeros((N, 4), np.uint8)
+    labels[:, 0] = synth.ABSENT
+    labels[:, 1] = 5
+    labels[:, 2] = np.where(rng.random(N) < 0.5, 0, 254)
+    labels[rng.random(N) < 0.2, 2] = synth.ABSENT
+    labels[:, 3] = rng.integers(10, 13, N)
+    thr = [-(1 << 63), -1, 0, 1, 4, 5, 6, 9, 10, 11, 12, 13, 253, 254, 255, 256, (1 << 63) - 1]
+    rows = [[[_pred(lab, op, thr=t)]] for lab in range(4) for t in thr for op in (4, 5)]
+    for i in range(400):
+        row = []
+        for t in range(int(rng.integers(1, 4))):
+            term = [_pred(int(rng.integers(0, 4)), int(rng.integers(4, 6)), thr=int(rng.choice(thr[1:-1])))
+                    for _ in range(int(rng.integers(1, 4)))]
+            if rng.random() < 0.5:
+                term.append(_pred(3, int(rng.integers(0, 2)), [int(rng.integers(10, 13))]))
+            row.append(term)
+        rows.append(row)
+    _check(g, orc, labels, *_csr(rows))
+
+
 def test_affinity_malformed(g, orc):
     labels = np.array([[0, 1], [1, 1], [2, synth.ABSENT]], np.uint8)
     good = _pred(0, 0, [1, 2])
