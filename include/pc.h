@@ -598,7 +598,9 @@ int pc_update_nodes(pc_ctx *ctx, const uint8_t *labels, int32_t N, int32_t L, co
  *           only; it is returned as found.
  * A request fails when an endpoint or waypoint is out of range or not
  * usable, a leg has no path, out_port[q] is not a port of the target, or the
- * walk has more than max_hops links.
+ * walk has more than max_hops links.  Distances are sums of link weights
+ * below 2^31 - 1: a switch whose minimum distance from the leg's start is
+ * 2^31 - 1 or more counts as unreachable.
  * Limits: 0 <= V <= PC_SYNTH_MAX_V, 0 <= Q, 0 <= Kv, Kf <= 32,
  * 0 <= max_hops <= 255, 0 <= prio <= 65535.  Malformed data: bad port_off
  * pair -> the switch has no ports (PC_DERR_OFFSETS); peer < -1 or >= V, src

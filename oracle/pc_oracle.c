@@ -748,12 +748,18 @@ void orc_reach_via(int64_t V, const int32_t *adj_off, const int32_t *adj, int64_
  * A request fails (hops -1, path -1, rules zero) when an endpoint or
  * waypoint is out of range, a leg has no path, out_port is not a port of
  * the target, or the walk has more than max_hops links.
+ * Distances are sums of link weights below 2^31 - 1 (the paper gives no
+ * range for them; this is the library's reading): a switch whose minimum
+ * distance from the leg's start is 2^31 - 1 or more is unreachable, so a
+ * leg whose target lies that far has no path.
  * Flags (input properties): OFFSETS bad port_off pair; SWITCH a peer < -1
  * or >= V, src / target outside [0, V), a via / forbid entry < -1 or >= V;
  * JUR region >= 32; GRAPH a zero weight (that port is no link); ACTION
  * out_port not a port of a target whose ports are well-formed.
  */
 typedef struct { int64_t d; int64_t v; } ps_item;
+
+#define PS_DIST_LIMIT ((int64_t)2147483647) /* distances stay below 2^31 - 1 */
 
 static void heap_push(ps_item *h, int64_t *n, ps_item x)
 {
@@ -819,6 +825,7 @@ static int64_t ps_leg(const ps_graph *g, uint32_t A, const int32_t *fb, int64_t 
             if (w <= 0) continue;
             const int64_t u = g->port_peer[p];
             if (!usable(g->region, A, fb, Kf, u)) continue;
+            if (it.d + w >= PS_DIST_LIMIT) continue; /* beyond the distance range: unreachable */
             if (dist[u] < 0 || it.d + w < dist[u]) {
                 dist[u] = it.d + w;
                 heap_push(heap, &hn, (ps_item){dist[u], u});

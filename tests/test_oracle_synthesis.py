@@ -191,6 +191,40 @@ def test_weights_pick_the_light_parallel_port(orc):
     assert p[1, :3].tolist() == [0, 1, 2] and r[1, 0]["action"] == 1 and r[1, 1]["action"] == 2
 
 
+def test_distance_range(orc):
+    """Leg distances are sums below 2^31 - 1 (the library's reading: the
+    paper gives no range): a target at distance 2^31 - 2 is reached, one at
+    2^31 - 1 or beyond is not, and a link of weight 2^31 - 1 or more is never
+    taken, so a light detour wins over it."""
+    big = (1 << 31) - 1
+
+    def leg(po, pp, w, s, t):
+        n = po.shape[0] - 1
+        return orc.synthesize(n, po, pp, np.zeros(n, np.uint8), np.array([s], np.int32), np.array([t], np.int32),
+                              np.array([1], np.uint32), np.full((1, 1), -1, np.int32), np.full((1, 1), -1, np.int32),
+                              np.zeros((1, 4), np.uint32), np.array([0], np.int32), 1, 10,
+                              weight=np.array(w, np.uint32))
+    # a line 0 - 1 - 2: ports 0 -> 1, 1 -> 0, 1 -> 2, 2 -> 1
+    po = np.array([0, 1, 3, 4], np.int32)
+    pp = np.array([1, 0, 2, 1], np.int32)
+    h, p, r, e = leg(po, pp, [big - 2, 1, 1, 1], 0, 2)  # 2^31 - 2
+    assert e == 0 and h[0] == 2 and p[0, :3].tolist() == [0, 1, 2]
+    h, p, r, e = leg(po, pp, [big - 2, 1, 2, 1], 0, 2)  # 2^31 - 1
+    assert e == 0 and h[0] == -1
+    h, p, r, e = leg(po, pp, [big - 2, 1, 2, 1], 0, 1)  # the first link alone, 2^31 - 3
+    assert h[0] == 1
+    for w01 in (big, big + 1, (1 << 32) - 1):
+        h, p, r, e = leg(po, pp, [w01, 1, 1, 1], 0, 1)
+        assert e == 0 and h[0] == -1, w01
+    # 0 -> 3 directly at 2^31, or 0 -> 1 -> 2 -> 3 at 5 per link
+    po = np.array([0, 2, 4, 6, 8], np.int32)
+    pp = np.array([3, 1, 0, 2, 1, 3, 2, 0], np.int32)
+    h, p, r, e = leg(po, pp, [1 << 31, 5, 5, 5, 5, 5, 5, 5], 0, 3)
+    assert e == 0 and h[0] == 3 and p[0, :4].tolist() == [0, 1, 2, 3] and r[0, 0]["action"] == 1
+    h, p, r, e = leg(po, pp, [7, 5, 5, 5, 5, 5, 5, 5], 0, 3)  # a light direct link wins
+    assert h[0] == 1 and r[0, 0]["action"] == 0
+
+
 def test_malformed_inputs(orc):
     topo = synth.fat_tree(4, 2)
     req = synth.synthesis_requests(0, topo, 20, Kv=1, Kf=1)
