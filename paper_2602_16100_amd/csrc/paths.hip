@@ -218,9 +218,14 @@ __global__ __launch_bounds__(kPsThreads) void k_ps_search(
             const int32_t uc = link ? u : 0;
             const uint32_t ubits = usable[uc >> 5];  // both LDS reads issued together
             const int32_t du = dist[uc];
-            const int64_t nd64 = static_cast<int64_t>(dv) + w;
-            if (!link || !((ubits >> (uc & 31)) & 1u) || nd64 >= du || nd64 >= dto) return;
-            const int32_t nd = static_cast<int32_t>(nd64);
+            // 32-bit unsigned: distances are below kInf = 2^31 - 1 and a weight
+            // of 2^31 - 1 or more cannot shorten any path, so clamping it
+            // keeps the sum exact where it matters and below 2^32
+            const uint32_t nd32 = static_cast<uint32_t>(dv) + min(w, static_cast<uint32_t>(kInf));
+            if (!link || !((ubits >> (uc & 31)) & 1u) || nd32 >= static_cast<uint32_t>(du) ||
+                nd32 >= static_cast<uint32_t>(dto))
+                return;
+            const int32_t nd = static_cast<int32_t>(nd32);
             const int32_t old = atomicMin(&dist[u], nd);
             if (nd < old) {
                 const uint32_t bit = 1u << (u & 31);
@@ -315,7 +320,9 @@ __global__ __launch_bounds__(kPsThreads) void k_ps_search(
                 for (int32_t k = rin_off[c] + lane; k < rin_off[c + 1]; k += 64) {
                     const int2 in = rin[k];
                     const int32_t du = dist[in.x];
-                    if (du != kInf && static_cast<int64_t>(du) + static_cast<uint32_t>(in.y) == dc)
+                    if (du != kInf &&
+                        static_cast<uint32_t>(du) + min(static_cast<uint32_t>(in.y), static_cast<uint32_t>(kInf)) ==
+                            static_cast<uint32_t>(dc))
                         best = min(best, in.x);
                 }
                 best = wave_min_i32(best);

@@ -56,6 +56,22 @@ def test_synthesis_parity(g, orc, kind, Kv, Kf, weighted):
     assert (ho >= 0).sum() > 100 and (ho == -1).sum() > 0
 
 
+@pytest.mark.parametrize("kind", ["random", "fat_tree"])
+def test_synthesis_huge_weights(g, orc, kind):
+    """Link weights up to 2^32 - 1, so that legs cross the 2^31 - 1 distance
+    bound (beyond it a switch is unreachable) and 64-bit sums would differ from
+    32-bit ones."""
+    rng = np.random.default_rng(21)
+    topo = synth.random_graph(rng, 300, 700, 2, 6) if kind == "random" else synth.fat_tree(8, 4)
+    n = topo["port_peer"].shape[0]
+    choices = np.array([1, 2, 7, 1 << 28, 1 << 29, (1 << 30) - 1, 1 << 30, (1 << 31) - 3, (1 << 31) - 2,
+                        (1 << 31) - 1, 1 << 31, (1 << 32) - 1], np.uint64)
+    weight = choices[rng.integers(0, choices.shape[0], n)].astype(np.uint32)
+    req = synth.synthesis_requests(7, topo, 600, Kv=1, Kf=1)
+    ho, _, _ = _check(g, orc, topo["S"], topo["port_off"], topo["port_peer"], topo["jur"], req, 99, 40, weight)
+    assert (ho >= 0).sum() > 10 and (ho == -1).sum() > 10
+
+
 def test_synthesis_max_hops_and_tiny_budgets(g, orc):
     topo = synth.fat_tree(8, 4)
     req = synth.synthesis_requests(6, topo, 400, Kv=2, Kf=1)
