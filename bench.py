@@ -68,8 +68,8 @@ PASS_COUNTERS = {
                      "sha256": "3ba266f186a97c69f5525e79cbd1aa8e8de7774ba0177ee4f0f28a75ebc43f74",
                      "SQ_INSTS_VALU_per_launch": 1.1454e9, "SQ_INSTS_SALU_per_launch": 7.263e8},
     "k_ps_search": {"source": "paper_2602_16100_amd/csrc/paths.hip",
-                    "sha256": "fbbfbf39657f5d66cb19ee3da30e4d50be65b87fade578a516808c14bf610773",
-                    "SQ_INSTS_VALU_per_launch": 4.348e9, "SQ_INSTS_SALU_per_launch": 3.4636e9},
+                    "sha256": "2cd6a2ef3bef6e4dbc6d79785967370e9c75b27ef64d4f64f685999d7c9ac81e",
+                    "SQ_INSTS_VALU_per_launch": 4.129e9, "SQ_INSTS_SALU_per_launch": 3.355e9},
 }
 
 
