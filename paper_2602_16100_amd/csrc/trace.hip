@@ -1352,6 +1352,13 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         }
     }
     if (T == 0) return PC_OK;
+    // the tail walk's workgroup: about two rule groups per lane of a mean
+    // table (64-256 threads; 256 when the table sizes are not at hand)
+    int walk_threads = 256;
+    if (pre == nullptr && S > 0) {
+        const int64_t mean_groups = ctx->h_small[0] / S;
+        walk_threads = mean_groups <= 128 ? 64 : mean_groups <= 256 ? 128 : 256;
+    }
     if (visit && K > 0) {
         PC_TIMED(ctx, "k_tr_watch_check", stream,
                  hipLaunchKernelGGL(k_tr_port_check, dim3(grid_for(static_cast<int64_t>(T) * K, 256)), dim3(256), 0,
@@ -1416,7 +1423,7 @@ int run_trace(pc_ctx *ctx, int32_t S, const int32_t *port_off, const int32_t *po
         if (known <= walk_max) {
             const unsigned wb = static_cast<unsigned>(known < 8192 ? known : 8192);
             PC_TIMED(ctx, "k_tr_walk", stream,
-                     hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(256), 0, stream, S, port_off, port_peer, n_ports, jur,
+                     hipLaunchKernelGGL(k_tr_walk, dim3(wb), dim3(walk_threads), 0, stream, S, port_off, port_peer, n_ports, jur,
                                         rule_off, rules, B.gcount, B.gofs, B.filt, ttl, live_cur, len_cur, level,
                                         out, watch, K, visit, vsum, walk, B.cpos));
             PC_LAUNCH_CHECK(ctx);
