@@ -40,11 +40,11 @@ TRAFFIC = [
      "bytes_per_launch": {"k_sel_eval": 680_687_937 + 4_407_406_605,
                           "k_aff_eval": 1_360_481_846 + 4_407_121_613}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
-     "sha256": "d4efbf17c6afb8856b911150214aae10905ad83a222f500c7f07d31c7b5dc778",
+     "sha256": "5d4cefd6203722908a276185029d3f28bcd1e279190863a30e935b72b2595379",
      "workload": "cfg5",
      # k_tr_match: per step (its 6 launches), like the hop-loop roofline
-     "bytes_per_launch": {"k_tr_prep": 1_888_826_156 + 566_231_040,
-                          "k_tr_match": 2_325_154_675 + 142_247_667}},
+     "bytes_per_launch": {"k_tr_prep": 1_888_691_607 + 566_231_040,
+                          "k_tr_match": 2_325_128_640 + 142_244_230}},
 ]
 
 
@@ -53,7 +53,7 @@ TRAFFIC = [
 # folder).  Valid only for the kernel source they were measured on.
 MATCH_COUNTERS = {
     "cfg5": {"source": "paper_2602_16100_amd/csrc/trace.hip",
-             "sha256": "d4efbf17c6afb8856b911150214aae10905ad83a222f500c7f07d31c7b5dc778",
+             "sha256": "5d4cefd6203722908a276185029d3f28bcd1e279190863a30e935b72b2595379",
              "SQ_INSTS_VALU_per_step": 3.891e8, "SQ_INSTS_SALU_per_step": 3.392e8},
 }
 
