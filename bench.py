@@ -24,8 +24,15 @@ ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
 HBM_PEAK_GBS = 8000.0
-# 256 CUs x 64 lanes x 2.4 GHz: one wave-wide integer VALU instruction per CU per clock
-VALU_PEAK_LANE_OPS = 256 * 64 * 2.4e9
+# VALU issue peak: two wave-wide 32-bit instructions per CU per clock (256 CUs x
+# 128 lanes x 2.4 GHz = 78.6 T lane-ops/s, the rate the published 157.3 TFLOP/s
+# fp32 vector peak implies at two flops per lane-op).  pc_measure_valu reaches
+# 0.93-0.96 of it with two-source 32-bit operations on vector registers and
+# constants; an operation with a scalar-register operand, a third source or a
+# 64-bit operand issues at half of it (measured 0.48-0.50).
+VALU_PEAK_LANE_OPS = 256 * 128 * 2.4e9
+# scalar ALU: one instruction per CU per clock (measured 0.96 of it)
+SALU_PEAK_INSTR = 256 * 2.4e9
 
 # HBM bytes per launch of k_sel_eval, k_aff_eval and k_tr_prep (per step of
 # k_tr_match) on the combined workload, from one rocprofv3 FETCH_SIZE pass and
@@ -73,18 +80,24 @@ PASS_COUNTERS = {
 }
 
 
+def issue_view(valu_instr, salu_instr, ms):
+    """VALU issue (in lane-ops/s) against the chip's two wave-wide
+    instructions per CU per clock, and the scalar unit's share of its one per
+    CU per clock, from instruction counts over `ms` milliseconds."""
+    lane_ops = valu_instr * 64 / (ms * 1e-3)
+    return {"bound": "alu", "achieved": lane_ops, "peak": VALU_PEAK_LANE_OPS, "unit": "lane-ops/s",
+            "frac": lane_ops / VALU_PEAK_LANE_OPS, "half_rate_peak": VALU_PEAK_LANE_OPS / 2,
+            "salu_frac": salu_instr / (ms * 1e-3) / SALU_PEAK_INSTR,
+            "source": "issue counters (profiles folder)"}
+
+
 def alu_view(kernel, ms):
     """The issue-rate view of a kernel whose counters are recorded for its
-    current source: wave-wide VALU instructions per second against the
-    chip's one per CU per clock (in lane-ops/s), and the same rate for SALU."""
+    current source."""
     c = PASS_COUNTERS.get(kernel)
     if c is None or not source_unchanged(c) or not ms or ms <= 0:
         return None
-    lane_ops = c["SQ_INSTS_VALU_per_launch"] * 64 / (ms * 1e-3)
-    return {"kernel": kernel, "bound": "alu", "achieved": lane_ops, "peak": VALU_PEAK_LANE_OPS, "unit": "lane-ops/s",
-            "frac": lane_ops / VALU_PEAK_LANE_OPS,
-            "salu_frac": c["SQ_INSTS_SALU_per_launch"] * 64 / (ms * 1e-3) / VALU_PEAK_LANE_OPS,
-            "source": "issue counters (profiles folder)"}
+    return {"kernel": kernel, **issue_view(c["SQ_INSTS_VALU_per_launch"], c["SQ_INSTS_SALU_per_launch"], ms)}
 
 
 def source_unchanged(rec):
@@ -151,6 +164,9 @@ def parse():
                     help="skip the timed pass of path synthesis over the same topology")
     ap.add_argument("--synthesis-requests", type=int, default=65536,
                     help="requests of the path-synthesis pass (the first flows of the workload)")
+    ap.add_argument("--measure-valu", action="store_true",
+                    help="measure the VALU and SALU issue rates, per instruction form, that the "
+                         "instruction-issue rooflines are priced against")
     ap.add_argument("--calibrate-copy", type=int, default=0, metavar="MIB",
                     help="profiling aid: run a plain device copy of MIB MiB three times (HBM counter calibration)")
     ap.add_argument("--measure-plain", type=int, default=0, metavar="MIB",
@@ -185,6 +201,30 @@ def measure_plain(mib, reps=10):
     b = n * 8
     print(json.dumps({"bytes": b, "fill_ms": fill_ms, "fill_gbs": b / fill_ms / 1e6,
                       "copy_ms": copy_ms, "copy_gbs": 2 * b / copy_ms / 1e6}), flush=True)
+
+
+def measure_valu():
+    """The chip's achieved wave-wide VALU (and one SALU) issue rate per
+    instruction form (pc_measure_valu), with the shader clock read under that
+    load, against the two VALU instructions per CU per clock the
+    instruction-issue rooflines use."""
+    import torch
+    import paper_2602_16100_amd as pc
+    torch.cuda.set_device(0)
+    ctx = pc.Context(0)
+    cus = torch.cuda.get_device_properties(0).multi_processor_count
+    peak = VALU_PEAK_LANE_OPS / 64
+    out = {"cus": cus, "peak_wave_instr_per_s": peak, "forms": {}}
+    forms = ("add_sub_u32", "xor_b32", "and_or_b32_vvv", "and_or_b32_vvs", "lshlrev_b64", "add_sub_u32_e64",
+             "s_xor_b32", "mov_b64", "cmp_ne_u32_e64", "cndmask_b32_e64", "bfi_b32", "xor_b32_sgpr", "mov_b32",
+             "xor_b32_inline", "xor_b32_literal")
+    for op, name in enumerate(forms):
+        runs = [ctx.measure_valu(op, 10) for _ in range(3)]
+        best, clock = max(runs)
+        out["forms"][name] = {"wave_instr_per_s": [r for r, _ in runs], "clock_hz": [c for _, c in runs],
+                              "best": best, "frac_of_peak": best / (SALU_PEAK_INSTR if name.startswith("s_") else peak),
+                              "per_cu_per_clock": best / (cus * clock) if clock > 0 else None}
+    print(json.dumps(out), flush=True)
 
 
 def calibrate_copy(mib):
@@ -385,10 +425,7 @@ def trace_roofline(wl, pc, ctx, D, full, prof, steps, workload):
            "hop_loop_frac": (alg / (sum(hop_ms.values()) * 1e-3) / 1e9 / HBM_PEAK_GBS) if hop_ms else None}
     c = MATCH_COUNTERS.get(workload)
     if c is not None and source_unchanged(c) and ms > 0:
-        lane_ops = c["SQ_INSTS_VALU_per_step"] * 64 / (ms * 1e-3)
-        out["alu"] = {"bound": "alu", "achieved": lane_ops, "peak": VALU_PEAK_LANE_OPS, "unit": "lane-ops/s",
-                      "frac": lane_ops / VALU_PEAK_LANE_OPS, "salu_frac": c["SQ_INSTS_SALU_per_step"] * 64 /
-                      (ms * 1e-3) / VALU_PEAK_LANE_OPS, "source": "issue counters (profiles folder)"}
+        out["alu"] = issue_view(c["SQ_INSTS_VALU_per_step"], c["SQ_INSTS_SALU_per_step"], ms)
     return out
 
 
@@ -1104,6 +1141,9 @@ def main():
         return
     if args.measure_plain:
         measure_plain(args.measure_plain)
+        return
+    if args.measure_valu:
+        measure_valu()
         return
 
     import torch

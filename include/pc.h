@@ -212,6 +212,26 @@ int pc_data_errors(pc_ctx *ctx, void *stream, uint32_t *flags, int clear);
 int pc_profile(pc_ctx *ctx, int enable);
 int pc_profile_read(pc_ctx *ctx, int idx, const char **name, int64_t *launches, double *total_ms);
 
+/* Measurement aid for the instruction-issue rooflines: times `reps`
+ * launches (after one untimed) of a kernel that fills every wave slot with
+ * eight independent dependency chains of one 32-bit integer VALU form and
+ * touches no memory, and returns the wave-wide VALU instructions retired per
+ * second in *wave_instr_per_s (the nominal peak is one per CU per clock).
+ * op: 0 = v_add_u32 / v_sub_u32, 1 = v_xor_b32, 2 = v_and_or_b32 with three
+ * vector sources, 3 = v_and_or_b32 with two vector sources and a scalar,
+ * 4 = v_lshlrev_b64 by a scalar amount, 5 = v_add_u32 / v_sub_u32 in their
+ * VOP3 encoding, 6 = s_xor_b32 (scalar ALU; the rate is then scalar
+ * instructions per second), 7 = v_mov_b64, 8 = v_cmp_ne_u32 into scalar
+ * register pairs, 9 = v_cndmask_b32 by a scalar register pair, 10 = v_bfi_b32,
+ * 11 = v_xor_b32 with a scalar source, 12 = v_mov_b32, 13 = v_xor_b32 with an
+ * inline constant, 14 = v_xor_b32 with a 32-bit literal.  When clock_hz is not NULL, the first wavefront of the last
+ * timed launch reads the shader-clock and constant-rate counters around its
+ * loop and *clock_hz receives the shader clock under that load (this path
+ * allocates 16 bytes of device memory for the duration of the call).
+ * Waits for its launches on `stream`.  PC_EINVAL for a NULL ctx or rate
+ * output, reps < 1 or an op outside 0..14. */
+int pc_measure_valu(pc_ctx *ctx, int op, int reps, double *wave_instr_per_s, double *clock_hz, void *stream);
+
 /*
  * A1 -- placement constraints.  For every selector row i in [0, I) and node
  * n in [0, N): bit n of feasible[i] is set iff node n satisfies every

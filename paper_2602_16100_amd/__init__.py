@@ -102,6 +102,7 @@ def lib():
     L.pc_profile.argtypes = [P, C]
     L.pc_profile_read.argtypes = [P, C, ctypes.POINTER(ctypes.c_char_p), ctypes.POINTER(I64),
                                   ctypes.POINTER(ctypes.c_double)]
+    L.pc_measure_valu.argtypes = [P, C, C, ctypes.POINTER(ctypes.c_double), ctypes.POINTER(ctypes.c_double), P]
     _lib = L
     return L
 
@@ -110,7 +111,8 @@ EXPORTED = ("pc_create", "pc_destroy", "pc_last_error", "pc_version", "pc_data_e
             "pc_profile_read", "pc_eval_selectors", "pc_eval_affinity", "pc_trace_flows", "pc_masked_reach",
             "pc_report", "pc_trace_flows_watch", "pc_masked_reach_via", "pc_report_paths", "pc_synthesize_paths",
             "pc_update_nodes", "pc_eval_selectors_count", "pc_probe_selectors", "pc_report_counts",
-            "pc_score_preferred", "pc_trace_flows_delta", "pc_trace_keep_tables", "pc_eval_selectors_noalloc")
+            "pc_score_preferred", "pc_trace_flows_delta", "pc_trace_keep_tables", "pc_eval_selectors_noalloc",
+            "pc_measure_valu")
 
 
 class Context:
@@ -158,6 +160,21 @@ class Context:
     def profile(self, enable: bool):
         """Reset the per-kernel timing tallies and switch timing on or off."""
         self.check(lib().pc_profile(self.handle, int(enable)))
+
+    def measure_valu(self, op: int = 0, reps: int = 10, stream=None) -> tuple:
+        """(wave-wide 32-bit integer VALU instructions retired per second,
+        shader clock in Hz) for a kernel that does nothing else; op 0 = add /
+        sub, 1 = xor, 2 = and-or of three vector sources, 3 = and-or with a
+        scalar source, 4 = 64-bit shift, 5 = add / sub in VOP3 encoding, 6 =
+        scalar xor, 7 = 64-bit move, 8 = compare into a scalar mask, 9 =
+        select by a scalar mask, 10 = bit-field insert, 11 = xor with a scalar
+        source, 12 = 32-bit move, 13 = xor with an inline constant, 14 = xor
+        with a 32-bit literal (pc_measure_valu)."""
+        r = ctypes.c_double()
+        c = ctypes.c_double()
+        self.check(lib().pc_measure_valu(self.handle, int(op), int(reps), ctypes.byref(r), ctypes.byref(c),
+                                         _stream(stream)))
+        return float(r.value), float(c.value)
 
     def profile_read(self) -> dict:
         """{kernel name: (launches, total milliseconds)} since the last reset."""
