@@ -47,11 +47,11 @@ TRAFFIC = [
      "bytes_per_launch": {"k_sel_eval": 680_687_937 + 4_407_406_605,
                           "k_aff_eval": 1_360_481_846 + 4_407_121_613}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
-     "sha256": "5d4cefd6203722908a276185029d3f28bcd1e279190863a30e935b72b2595379",
+     "sha256": "d17e07d49b12a4620a8afb6a8e31b0c5c239e33f66a43248b5ed2a20bad3b4d7",
      "workload": "cfg5",
      # k_tr_match: per step (its 6 launches), like the hop-loop roofline
-     "bytes_per_launch": {"k_tr_prep": 1_888_691_607 + 566_231_040,
-                          "k_tr_match": 2_325_128_640 + 142_244_230}},
+     "bytes_per_launch": {"k_tr_prep": 1_888_803_574 + 566_231_040,
+                          "k_tr_match": 2_325_381_413 + 142_254_643}},
 ]
 
 
@@ -60,8 +60,8 @@ TRAFFIC = [
 # folder).  Valid only for the kernel source they were measured on.
 MATCH_COUNTERS = {
     "cfg5": {"source": "paper_2602_16100_amd/csrc/trace.hip",
-             "sha256": "5d4cefd6203722908a276185029d3f28bcd1e279190863a30e935b72b2595379",
-             "SQ_INSTS_VALU_per_step": 3.891e8, "SQ_INSTS_SALU_per_step": 3.392e8},
+             "sha256": "d17e07d49b12a4620a8afb6a8e31b0c5c239e33f66a43248b5ed2a20bad3b4d7",
+             "SQ_INSTS_VALU_per_step": 3.893e8, "SQ_INSTS_SALU_per_step": 3.235e8},
 }
 
 

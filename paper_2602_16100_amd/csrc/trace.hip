@@ -845,9 +845,38 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     // the switch's ports (np < 0: its port range is invalid)
     const int64_t pb = lv.port_off[s], pe = lv.port_off[s + 1];
     const int64_t np = pc_range_ok(pb, pe, lv.n_ports) ? pe - pb : -1;
-    // stage the chunk; pad to a multiple of 4 lookups with copies of the last
-    for (int i = threadIdx.x; i < tn4; i += kMatchThreads) {
-        const BRec r = bucket[bb + min(i, tn - 1)];
+    // A lane's chunk sets of group g: buffer loads with the lane's group as
+    // the vector offset (clamped into the table) and the plane as a scalar
+    // offset; an opaque copy of the plane stride keeps the 96 offsets from
+    // being hoisted out of the loops (and spilled) as invariants.  A lane past
+    // the last group gets empty chunk sets, so it never survives the filter.
+    auto load_sets = [&](int32_t g, v16u (&F)[kChunks]) {
+        uint32_t pstride = static_cast<uint32_t>(G) * 4u;
+        asm volatile("" : "+s"(pstride));
+        const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
+            const_cast<uint32_t *>(fs), static_cast<short>(0), kPlaneWords * G * 4, 0x00020000);
+        const uint32_t voff = static_cast<uint32_t>(min(g, G - 1)) * 4u;
+#pragma unroll
+        for (int c = 0; c < kChunks; ++c)
+#pragma unroll
+            for (int x = 0; x < 16; ++x)
+                F[c][x] = __builtin_amdgcn_raw_buffer_load_b32(frs, voff, static_cast<uint32_t>(c * 16 + x) * pstride, 0);
+        if (g >= G) {
+#pragma unroll
+            for (int x = 0; x < 16; ++x) F[0][x] = 0u;
+        }
+    };
+    // stage the chunk (at most one lookup per thread: tn4 <= kMaxChunk <=
+    // kMatchThreads); pad to a multiple of 4 lookups with copies of the last
+    const int i = static_cast<int>(threadIdx.x);
+    BRec r{};
+    if (i < tn4) r = bucket[bb + min(i, tn - 1)];
+    // the first slice's chunk sets load while the lookups are staged
+    // (whether or not this wavefront filters: the loads are clamped into the
+    // table, and a branch would leave the sets undefined on one path)
+    v16u F0[kChunks];
+    load_sets(gwi * 64 + lane, F0);
+    if (i < tn4) {
         int32_t t = r.t;
         pc_key h = r.key;
         uint32_t jmv = r.jm;
@@ -871,87 +900,80 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
         if (threadIdx.x == 0) nother = 0;
     }
     __syncthreads();
-    // one slice of kSliceGroups groups at a time, one group per lane,
-    // its chunk sets held in VGPRs while the chunk's lookups stream past
+    // Filter phase: survivors of the chunk filter are queued (per wavefront)
+    // until the queue could overflow.  Verify phase: the queued survivors are
+    // checked against their full rules, 64 at a time, with the chunk sets
+    // dead.  Then filtering resumes with the sets loaded again.  A quad of
+    // lookups queues at most 256 entries, so every round advances.  gw is
+    // the group of lane 0.
+    auto round = [&](int32_t gw, int32_t &jr, const v16u (&F)[kChunks]) {
+        int32_t qn = 0;
+        int32_t j0 = jr;
+        for (; j0 < je; j0 += 4) {
+            uint4 X[kChunks];
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) X[c] = reinterpret_cast<const uint4 *>(cidx[c])[j0 >> 2];
+            uint32_t sv[4];
+            uint32_t xi[kChunks][4];
+#pragma unroll
+            for (int c = 0; c < kChunks; ++c) {
+                xi[c][0] = __builtin_amdgcn_readfirstlane(X[c].x);
+                xi[c][1] = __builtin_amdgcn_readfirstlane(X[c].y);
+                xi[c][2] = __builtin_amdgcn_readfirstlane(X[c].z);
+                xi[c][3] = __builtin_amdgcn_readfirstlane(X[c].w);
+            }
+            filter_quad(xi, F, sv);
+            if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
+                uint64_t m[4];
+                int32_t n = 0;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    m[k] = __ballot(sv[k] != 0);
+                    n += __popcll(m[k]);
+                }
+                if (qn + n > kQueue) break;  // resume at this quad after verifying
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    if (sv[k]) {
+                        const uint32_t below = __builtin_amdgcn_mbcnt_hi(
+                            static_cast<uint32_t>(m[k] >> 32),
+                            __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m[k]), 0u));
+                        q[qn + below] = make_uint2(sv[k], static_cast<uint32_t>(j0 + k) << 6 | lane);
+                    }
+                    qn += __popcll(m[k]);
+                }
+            }
+        }
+        jr = j0;
+        // the queue entries were written by other lanes of this wavefront
+        __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
+        __builtin_amdgcn_wave_barrier();
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
+        for (int32_t e = lane; e < qn; e += 64) {
+            const uint2 en = q[e];
+            const int32_t j = static_cast<int32_t>(en.y >> 6);
+            const int32_t gg = gw + static_cast<int32_t>(en.y & 63u);
+            verify_group(en.x, rules + rb + static_cast<int64_t>(gg) * 32, static_cast<uint32_t>(gg) * 32,
+                         keys[j], reinterpret_cast<unsigned long long *>(&best[j]));
+        }
+        __builtin_amdgcn_wave_barrier();
+    };
+    // one slice of kSliceGroups groups at a time, one group per lane, its
+    // chunk sets held in VGPRs while the chunk's lookups stream past.  The
+    // first round of the first slice uses the sets loaded with the staging;
+    // it runs outside the slice loop, so those sets are dead after it and
+    // never live beside a later round's (inside the loop they would be, and
+    // the 192 registers would spill)
+    int32_t jr0 = jb;
+    if (jb < je) round(gwi * 64, jr0, F0);
     for (int32_t sl = 0; sl < nslices; ++sl) {
         const int32_t g = sl * kSliceGroups + gwi * 64 + lane;
-        const int32_t gw = sl * kSliceGroups + gwi * 64;  // group of lane 0
-        // Filter phase: survivors of the chunk filter are queued (per
-        // wavefront) until the queue could overflow.  Verify phase: the
-        // queued survivors are checked against their full rules, 64 at a
-        // time, with the chunk sets dead.  Then filtering resumes.  A quad
-        // of lookups queues at most 256 entries, so every round advances.
-        for (int32_t jr = jb; jr < je;) {
-            // buffer loads: the lane's group as the vector offset (clamped
-            // into the table), the plane as a scalar offset; an opaque copy
-            // of the plane stride keeps the 96 offsets from being hoisted out
-            // of the loops (and spilled) as invariants.  A lane past the last
-            // group gets empty chunk sets, so it never survives the filter.
-            uint32_t pstride = static_cast<uint32_t>(G) * 4u;
-            asm volatile("" : "+s"(pstride));
-            const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
-                const_cast<uint32_t *>(fs), static_cast<short>(0), kPlaneWords * G * 4, 0x00020000);
-            const uint32_t voff = static_cast<uint32_t>(min(g, G - 1)) * 4u;
+        const int32_t gw = sl * kSliceGroups + gwi * 64;
+        int32_t jr = sl == 0 ? jr0 : jb;
+        while (jr < je) {
             v16u F[kChunks];
-#pragma unroll
-            for (int c = 0; c < kChunks; ++c)
-#pragma unroll
-                for (int x = 0; x < 16; ++x)
-                    F[c][x] = __builtin_amdgcn_raw_buffer_load_b32(frs, voff, static_cast<uint32_t>(c * 16 + x) * pstride, 0);
-            if (g >= G) {
-#pragma unroll
-                for (int x = 0; x < 16; ++x) F[0][x] = 0u;
-            }
-            int32_t qn = 0;
-            int32_t j0 = jr;
-            for (; j0 < je; j0 += 4) {
-                uint4 X[kChunks];
-#pragma unroll
-                for (int c = 0; c < kChunks; ++c) X[c] = reinterpret_cast<const uint4 *>(cidx[c])[j0 >> 2];
-                uint32_t sv[4];
-                uint32_t xi[kChunks][4];
-#pragma unroll
-                for (int c = 0; c < kChunks; ++c) {
-                    xi[c][0] = __builtin_amdgcn_readfirstlane(X[c].x);
-                    xi[c][1] = __builtin_amdgcn_readfirstlane(X[c].y);
-                    xi[c][2] = __builtin_amdgcn_readfirstlane(X[c].z);
-                    xi[c][3] = __builtin_amdgcn_readfirstlane(X[c].w);
-                }
-                filter_quad(xi, F, sv);
-                if (__ballot((sv[0] | sv[1] | sv[2] | sv[3]) != 0)) {
-                    uint64_t m[4];
-                    int32_t n = 0;
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        m[k] = __ballot(sv[k] != 0);
-                        n += __popcll(m[k]);
-                    }
-                    if (qn + n > kQueue) break;  // resume at this quad after verifying
-#pragma unroll
-                    for (int k = 0; k < 4; ++k) {
-                        if (sv[k]) {
-                            const uint32_t below = __builtin_amdgcn_mbcnt_hi(
-                                static_cast<uint32_t>(m[k] >> 32),
-                                __builtin_amdgcn_mbcnt_lo(static_cast<uint32_t>(m[k]), 0u));
-                            q[qn + below] = make_uint2(sv[k], static_cast<uint32_t>(j0 + k) << 6 | lane);
-                        }
-                        qn += __popcll(m[k]);
-                    }
-                }
-            }
-            jr = j0;
-            // the queue entries were written by other lanes of this wavefront
-            __builtin_amdgcn_fence(__ATOMIC_RELEASE, "wavefront");
-            __builtin_amdgcn_wave_barrier();
-            __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "wavefront");
-            for (int32_t e = lane; e < qn; e += 64) {
-                const uint2 en = q[e];
-                const int32_t j = static_cast<int32_t>(en.y >> 6);
-                const int32_t gg = gw + static_cast<int32_t>(en.y & 63u);
-                verify_group(en.x, rules + rb + static_cast<int64_t>(gg) * 32, static_cast<uint32_t>(gg) * 32,
-                             keys[j], reinterpret_cast<unsigned long long *>(&best[j]));
-            }
-            __builtin_amdgcn_wave_barrier();
+            load_sets(g, F);
+            round(gw, jr, F);
         }
     }
     // every wavefront's matches are in best[] (a lookup's matches come from
