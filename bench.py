@@ -47,11 +47,11 @@ TRAFFIC = [
      "bytes_per_launch": {"k_sel_eval": 680_687_937 + 4_407_406_605,
                           "k_aff_eval": 1_360_481_846 + 4_407_121_613}},
     {"source": "paper_2602_16100_amd/csrc/trace.hip",
-     "sha256": "d17e07d49b12a4620a8afb6a8e31b0c5c239e33f66a43248b5ed2a20bad3b4d7",
+     "sha256": "c9b11ae36f815781b39e2ccddb1fca6cd58dc757cfef139cb8fdfc38042cac7d",
      "workload": "cfg5",
      # k_tr_match: per step (its 6 launches), like the hop-loop roofline
-     "bytes_per_launch": {"k_tr_prep": 1_888_803_574 + 566_231_040,
-                          "k_tr_match": 2_325_381_413 + 142_254_643}},
+     "bytes_per_launch": {"k_tr_prep": 1_888_686_134 + 566_231_040,
+                          "k_tr_match": 2_325_285_696 + 142_260_102}},
 ]
 
 
@@ -60,8 +60,8 @@ TRAFFIC = [
 # folder).  Valid only for the kernel source they were measured on.
 MATCH_COUNTERS = {
     "cfg5": {"source": "paper_2602_16100_amd/csrc/trace.hip",
-             "sha256": "d17e07d49b12a4620a8afb6a8e31b0c5c239e33f66a43248b5ed2a20bad3b4d7",
-             "SQ_INSTS_VALU_per_step": 3.893e8, "SQ_INSTS_SALU_per_step": 3.235e8},
+             "sha256": "c9b11ae36f815781b39e2ccddb1fca6cd58dc757cfef139cb8fdfc38042cac7d",
+             "SQ_INSTS_VALU_per_step": 3.895e8, "SQ_INSTS_SALU_per_step": 3.235e8},
 }
 
 

@@ -849,13 +849,15 @@ __global__ __launch_bounds__(kMatchThreads, 4) void k_tr_match(
     // the vector offset (clamped into the table) and the plane as a scalar
     // offset; an opaque copy of the plane stride keeps the 96 offsets from
     // being hoisted out of the loops (and spilled) as invariants.  A lane past
-    // the last group gets empty chunk sets, so it never survives the filter.
+    // the last group gets empty chunk sets, so it never survives the filter;
+    // a switch without rules (G = 0) reads offset 0 of an empty buffer, which
+    // returns zeros.
     auto load_sets = [&](int32_t g, v16u (&F)[kChunks]) {
         uint32_t pstride = static_cast<uint32_t>(G) * 4u;
         asm volatile("" : "+s"(pstride));
         const __amdgpu_buffer_rsrc_t frs = __builtin_amdgcn_make_buffer_rsrc(
             const_cast<uint32_t *>(fs), static_cast<short>(0), kPlaneWords * G * 4, 0x00020000);
-        const uint32_t voff = static_cast<uint32_t>(min(g, G - 1)) * 4u;
+        const uint32_t voff = static_cast<uint32_t>(max(0, min(g, G - 1))) * 4u;
 #pragma unroll
         for (int c = 0; c < kChunks; ++c)
 #pragma unroll

@@ -216,6 +216,29 @@ def test_trace_fat_tree_small(g, orc, variant, trace_path):
     _check_workload(g, orc, wl)
 
 
+def test_trace_switches_without_rules(g, orc, trace_path):
+    """Every fifth switch (pod and core switches alike) has an empty flow
+    table: every lookup there is a table miss, so the traces that reach such
+    a switch, at ingress or in transit, end there in MISS."""
+    wl = synth.trace_workload(3, 8, 4, 512, 20000, 24, 3000, variant="rpath")
+    ro = np.asarray(wl["rule_off"], np.int64)
+    S = wl["S"]
+    empty = np.zeros(S, bool)
+    empty[::5] = True
+    keep = [wl["rules"][ro[s]:ro[s + 1]] for s in range(S) if not empty[s]]
+    off = np.zeros(S + 1, np.int32)
+    off[1:] = np.cumsum([0 if empty[s] else ro[s + 1] - ro[s] for s in range(S)])
+    wl.arrays["rule_off"] = off
+    wl.arrays["rules"] = np.concatenate(keep)
+    _, oo = _check_workload(g, orc, wl)
+    tr = oo["traces"]
+    ended = tr["last_switch"] >= 0
+    at_empty = np.zeros(tr.shape[0], bool)
+    at_empty[ended] = empty[tr["last_switch"][ended]]
+    assert np.all(tr["state"][at_empty] == 2)   # MISS
+    assert at_empty.sum() > 100 and (at_empty & (tr["hops"] > 0)).any()
+
+
 def test_trace_prefix_tables_multi_slice(g, orc, trace_path):
     """Routing tables (destination prefixes of 16-32 bits, ports, source and
     protocol wildcarded): each switch filters on the key nibbles its own
