@@ -295,6 +295,25 @@ def test_trace_ties_and_ttl(g, orc, trace_path):
         _same_traces(tg, to)
 
 
+def test_trace_switches_with_many_ports(g, orc, trace_path):
+    """A dense random graph (100 switches of 74-89 ports: most have link
+    ports past the first 64, and every host port is past them) with mostly
+    wildcard rules: traces wander through high ports, whose peers and
+    jurisdictions the match epilogue takes from the port table rather than
+    from its staged first 64 ports."""
+    rng = np.random.default_rng(11)
+    topo = synth.random_graph(rng, 100, 4000, 2, 8)
+    rule_off, rules, _ = synth.build_tables(rng, topo, 40, 0.03, prio="small", prio_range=3)
+    T = 4000
+    hdr = synth.random_keys(rng, T)
+    ingress = rng.integers(0, 100, size=T).astype(np.int32)
+    tg = g.trace(100, topo["port_off"], topo["port_peer"], topo["jur"], rule_off, rules, hdr, ingress, 16)
+    to, _ = orc.trace(100, topo["port_off"], topo["port_peer"], topo["jur"], rule_off, rules, hdr, ingress, 16)
+    _same_traces(tg, to)
+    egress = to["state"] == 0
+    assert egress.sum() > 100 and np.all(to["last_port"][egress] >= 64)
+
+
 def test_trace_malformed_flags(g, orc):
     import paper_2602_16100_amd as pc
     wl = synth.trace_workload(6, 4, 2, 64, 500, 8, 100)
