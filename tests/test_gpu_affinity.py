@@ -75,6 +75,14 @@ def test_affinity_random(g, orc, seed, N, absent):
     assert (po > 0).any() and (po == 0).any()
 
 
+def test_affinity_plane_tables_past_2gib(g, orc):
+    """8,000 labels over 3,000 nodes: value and prefix planes pass 2 GiB, so
+    the evaluator reads them through 64-bit pointers."""
+    wl = synth.affinity_workload(42, 3000, 8000, 300, card_choices=(2, 3, 16, 64), absent_p=0.05)
+    fo, po, uo = _check(g, orc, wl["labels"], wl["row_off"], wl["term_off"], wl["preds"])
+    assert (po > 0).any() and (po == 0).any()
+
+
 def test_affinity_paper_fixture(g, orc):
     fx = json.load(open(os.path.join(HERE, "golden", "paper_affinity.json")))
     keys, nodes = fx["keys"], fx["nodes"]

@@ -433,6 +433,19 @@ def test_report_malformed_intents(g, orc):
     _same(sg["counts"], so["counts"], "counts")
 
 
+def test_selectors_plane_tables_past_2gib(g, orc):
+    """8,000 labels over 3,000 nodes: the value-plane table (8,000 x 256
+    possible values, 144 words each) passes 2 GiB, so the evaluator reads
+    planes through 64-bit pointers instead of 32-bit buffer offsets."""
+    wl = synth.selector_workload(41, 3000, 8000, 300, card_choices=(2, 3, 16, 64), absent_p=0.05)
+    assert 8000 * 256 * 144 * 8 >= 1 << 31
+    fg, pg = g.selectors(wl["labels"], wl["pred_off"], wl["preds"])
+    fo, po, err = orc.selectors(wl["labels"], wl["pred_off"], wl["preds"])
+    _same(fg, fo, "feasible")
+    _same(pg, po, "popcnt")
+    assert err == 0 and (po > 0).sum() > 100
+
+
 def test_empty_inputs(g, orc):
     """N = 0, I = 0, T = 0, Q = 0 and V = 0 all return cleanly."""
     labels = np.zeros((0, 4), np.uint8)

@@ -67,6 +67,15 @@ def test_preferred_random(g, orc, seed, N, absent, p_feas):
     assert (so > 0).sum() > 100 and (co > 1).sum() > 10
 
 
+def test_preferred_plane_tables_past_2gib(g, orc):
+    """8,000 labels over 3,000 nodes: the plane tables pass 2 GiB, so the
+    evaluator reads them through 64-bit pointers."""
+    wl = synth.affinity_workload(43, 3000, 8000, 1, card_choices=(2, 3, 16, 64), absent_p=0.05)
+    row_off, term_off, preds, weight = synth.preferred_rows(43, wl.meta["cards"], 300, tmin=0, tmax=6, kmin=0, kmax=4)
+    bo, so, co = _check(g, orc, wl["labels"], row_off, term_off, weight, preds)
+    assert (so > 0).sum() > 50
+
+
 @pytest.mark.parametrize("seed,wmax", [(5, 1), (6, 2), (7, 3)])
 def test_preferred_few_terms_ties(g, orc, seed, wmax):
     """Rows of zero to three terms (the term-pattern class) with weights of
