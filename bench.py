@@ -52,6 +52,20 @@ TRAFFIC = [
      # k_tr_match: per step (its 6 launches), like the hop-loop roofline
      "bytes_per_launch": {"k_tr_prep": 1_888_686_134 + 566_231_040,
                           "k_tr_match": 2_325_285_696 + 142_260_102}},
+    # the single-kernel configurations (profiles/cfg2_cfg3_cfg4_hbm_counters.md)
+    {"source": "paper_2602_16100_amd/csrc/select.hip",
+     "sha256": "3ba266f186a97c69f5525e79cbd1aa8e8de7774ba0177ee4f0f28a75ebc43f74",
+     "workload": "cfg2",
+     "bytes_per_launch": {"k_sel_eval": 61_279_026 + 206_234_144}},
+    {"source": "paper_2602_16100_amd/csrc/trace.hip",
+     "sha256": "c9b11ae36f815781b39e2ccddb1fca6cd58dc757cfef139cb8fdfc38042cac7d",
+     "workload": "cfg3-rpath",
+     "bytes_per_launch": {"k_tr_match": 1_056_617_428 + 793_564_755}},  # per call (its 7 launches)
+    {"source": "paper_2602_16100_amd/csrc/reach.hip",
+     "sha256": "c5686db7947fd48ea645f261a5cf397dcff66e0567c993962d5520fdb59c8dee",
+     "workload": "cfg4",
+     # per call: k_rc_validate, the -1 fill and k_rc_queue
+     "bytes_per_launch": {"pc_masked_reach": 47_662_753 + 1_047_437_664}},
 ]
 
 
@@ -115,10 +129,10 @@ def measured_traffic(workload, kernel):
     has changed since they were taken."""
     import hashlib
     for t in TRAFFIC:
-        if kernel not in t["bytes_per_launch"]:
+        if kernel not in t["bytes_per_launch"] or workload != t["workload"]:
             continue
         path = os.path.join(ROOT, t["source"])
-        if workload != t["workload"] or not os.path.exists(path):
+        if not os.path.exists(path):
             return None
         with open(path, "rb") as f:
             if hashlib.sha256(f.read()).hexdigest() != t["sha256"]:
@@ -1000,7 +1014,7 @@ def bench_cfg2(args, pc, ctx):
              "kernel_rate_evals_per_s": pairs / (avg * 1e-3),
              "data_error_flags": ctx.data_errors(clear=True)}
     roof = {"kernel": "k_sel_eval", "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": gbs / HBM_PEAK_GBS, "traffic": None, "alg_bytes_per_launch": alg, "avg_launch_ms": avg,
+            "frac": gbs / HBM_PEAK_GBS, "traffic": measured_traffic(args.workload, "k_sel_eval"), "alg_bytes_per_launch": alg, "avg_launch_ms": avg,
             "floor_us_at_peak": alg / (HBM_PEAK_GBS * 1e9) * 1e6}
     if not args.no_cpu_baseline:
         import oracle
@@ -1101,8 +1115,8 @@ def bench_cfg4(args, pc, ctx):
     alg = store + (V + 1) * 4 + int(wl["adj"].shape[0]) * 4 + V
     gbs = alg / (ms * 1e-3) / 1e9
     roof = {"kernel": "+".join(per_k), "bound": "hbm", "achieved": gbs, "peak": HBM_PEAK_GBS, "unit": "GB/s",
-            "frac": gbs / HBM_PEAK_GBS, "traffic": None, "alg_bytes_per_launch": alg, "avg_launch_ms": ms,
-            "floor_us_at_peak": alg / (HBM_PEAK_GBS * 1e9) * 1e6}
+            "frac": gbs / HBM_PEAK_GBS, "traffic": measured_traffic("cfg4", "pc_masked_reach"),
+            "alg_bytes_per_launch": alg, "avg_launch_ms": ms, "floor_us_at_peak": alg / (HBM_PEAK_GBS * 1e9) * 1e6}
     extra = {"per_kernel": per_k, "fill_ms": fill,
              "fill_gbs": store / (fill * 1e-3) / 1e9 if fill else None,
              "data_error_flags": ctx.data_errors(clear=True)}
@@ -1132,7 +1146,7 @@ def main():
     args = parse()
     world = int(os.environ.get("WORLD_SIZE", "1"))
     if args.gpus != 1 or world != 1:
-        print(f"bench.py measures one GPU only (the check shards by intent with no exchange; see DESIGN.md); "
+        print(f"bench.py measures one GPU only (the check shards by intent, with no exchange between GPUs); "
               f"--gpus {args.gpus} is not supported", file=sys.stderr)
         sys.exit(2)
 
